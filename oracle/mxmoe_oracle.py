@@ -1,0 +1,387 @@
+"""CPU oracle for the MxMoE mixed-precision MoE block forward (arXiv 2505.05799).
+
+TEST INFRASTRUCTURE ONLY.  Nothing on the product path imports, links or runs
+this module: only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` use it.  It shares no code with the HIP path and imports
+nothing but numpy.
+
+What it computes is the plain definition of the MoE block, on the same quantized
+operands the GPU receives (codes, scales, zeros - never the packed layout):
+
+* Sec. 2.2, Eq. (1)-(2): each routed expert e maps its tokens X_e through
+  W_down( SiLU(W_gate X_e) * W_up X_e ); the block output is the sum over the
+  token's experts of that result times the router gate weight w_e.  Shared
+  experts are dense experts over every token with weight 1.
+* Sec. 2.1 min-max quantizer and the weight storage of Sec. 5.2: a wNg128 weight
+  dequantizes to s * (q - z) per group of 128 along K; a per-channel symmetric
+  weight (w8a8 / w4a4, Fig. 4 caption) to s_w[n] * q.
+* Sec. 4.2.2 (end): activations of w8a8 / w4a4 linears are quantized dynamically
+  at run time, per token (a_gsize = -1 in the W5A5 allocation table), with the
+  fp32 recipe of :func:`act_quant`.
+
+Floating point runs in fp64; integer GEMMs are exact (fp64 BLAS on integer
+values, every partial sum < 2^53).  Rounding points mirrored from the GPU
+contract: the gated intermediate h is rounded once to the activation dtype
+before the down projection; a8/a4 down projections quantize that rounded h.
+The block output is returned unrounded in fp64.
+
+Parity pins live in ``tests/test_oracle_*.py``.
+"""
+
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+__all__ = [
+    "bf16_bits_to_f64", "round_to_act", "act_values", "route", "dequant",
+    "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
+    "silu",
+]
+
+# ----------------------------------------------------------------------------
+# dtype handling (own implementation; the GPU path has its own)
+# ----------------------------------------------------------------------------
+
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> exact fp64 values."""
+    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+def act_values(a: np.ndarray, act: str) -> np.ndarray:
+    """Activation-dtype storage (float16 array or bf16 bits) -> exact fp64 values."""
+    if act == "fp16":
+        return np.asarray(a, dtype=np.float16).astype(np.float64)
+    if act == "bf16":
+        return bf16_bits_to_f64(a)
+    raise ValueError(act)
+
+
+def round_to_act(x: np.ndarray, act: str) -> np.ndarray:
+    """Round fp64 values to the nearest activation-dtype value (ties to even).
+
+    Returns fp64 values that are exactly representable in the target dtype.
+    fp16 uses numpy's correctly rounded float64 -> float16 cast.  bf16 keeps 8
+    significant bits: the value is snapped to multiples of 2^(e-8) where
+    x = m * 2^e with 0.5 <= |m| < 1 (subnormal spacing 2^-133).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if act == "fp16":
+        return x.astype(np.float16).astype(np.float64)
+    if act != "bf16":
+        raise ValueError(act)
+    _, e = np.frexp(x)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    r = np.rint(x / spacing) * spacing
+    # values that round past the largest finite bf16 become inf (never hit here)
+    big = np.abs(r) > 3.3895313892515355e38
+    return np.where(big, np.copysign(np.inf, x), r)
+
+
+# ----------------------------------------------------------------------------
+# O1: routing / permutation (Eq. 2: which tokens form X_e)
+# ----------------------------------------------------------------------------
+
+
+def route(topk_ids: np.ndarray, E: int) -> Dict[str, np.ndarray]:
+    """Stable grouping of the T*k (token, slot) pairs by expert.
+
+    Pair id p = t*k + s.  Pairs are ordered by (expert, p); pairs whose expert
+    id is outside [0, E) are dropped (they contribute nothing to the output).
+    Returns counts [E], offsets [E+1], sorted_pair [#valid], inv [T*k]
+    (position of pair p in sorted order, -1 if dropped), bad [#pairs] bool.
+    """
+    e = np.asarray(topk_ids, dtype=np.int64).ravel()
+    P = e.size
+    p = np.arange(P, dtype=np.int64)
+    bad = (e < 0) | (e >= E)
+    good = ~bad
+    order = np.lexsort((p[good], e[good]))           # primary key: expert, then pair
+    sorted_pair = p[good][order]
+    counts = np.bincount(e[good], minlength=E)[:E]
+    offsets = np.zeros(E + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    inv = np.full(P, -1, dtype=np.int64)
+    inv[sorted_pair] = np.arange(sorted_pair.size)
+    return {
+        "counts": counts.astype(np.int32),
+        "offsets": offsets.astype(np.int32),
+        "sorted_pair": sorted_pair.astype(np.int32),
+        "inv": inv.astype(np.int32),
+        "bad": bad,
+    }
+
+
+# ----------------------------------------------------------------------------
+# O2: weight dequantization (Sec. 2.1 quantizer, Sec. 5.2 storage)
+# ----------------------------------------------------------------------------
+
+
+def _is_weight_only(s) -> bool:
+    return s.w_bits < 16 and s.a_bits == 16
+
+
+def dequant(lin, act: str) -> np.ndarray:
+    """Exact fp64 value of every weight of a quantized linear, [n, k]."""
+    s = lin.scheme
+    if s.w_bits == 16:
+        w = bf16_bits_to_f64(lin.codes)
+        if act == "fp16":
+            # the 16-bit weights feed an fp16 MFMA: they are converted to fp16 once
+            w = w.astype(np.float16).astype(np.float64)
+        return w
+    if _is_weight_only(s):
+        g = s.w_group
+        q = lin.codes.astype(np.float64).reshape(lin.n, lin.k // g, g)
+        sc = lin.scales.astype(np.float64)[..., None]
+        z = lin.zeros.astype(np.float64)[..., None]
+        return (sc * (q - z)).reshape(lin.n, lin.k)
+    return lin.codes.astype(np.float64) * lin.scales.astype(np.float64)[:, None]
+
+
+# ----------------------------------------------------------------------------
+# O3: dynamic per-token activation quantization (fp32 recipe)
+# ----------------------------------------------------------------------------
+
+
+def act_quant(a: np.ndarray, qmax: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Symmetric per-row quantization of activations, evaluated in IEEE fp32.
+
+    amax = max |a_r| (exact).  amax == 0 gives scale 0 and all-zero codes.
+    Otherwise inv = fl32(qmax / amax), s = fl32(amax / qmax) (correctly rounded
+    divisions) and q = clamp(rne(fl32(a * inv)), -qmax, qmax).
+    Returns codes int8 [rows, cols] and scales fp32 [rows].
+    """
+    a = np.asarray(a, dtype=np.float32)
+    q32 = np.float32(qmax)
+    amax = np.abs(a).max(axis=1) if a.shape[1] else np.zeros(a.shape[0], np.float32)
+    zero = amax == 0
+    safe = np.where(zero, np.float32(1), amax).astype(np.float32)
+    inv = (q32 / safe).astype(np.float32)
+    s = np.where(zero, np.float32(0), (safe / q32).astype(np.float32)).astype(np.float32)
+    prod = (a * inv[:, None]).astype(np.float32)
+    q = np.clip(np.rint(prod), -qmax, qmax)
+    q = np.where(zero[:, None], 0, q)
+    return q.astype(np.int8), s
+
+
+def _qmax(a_bits: int) -> int:
+    return (1 << (a_bits - 1)) - 1
+
+
+# ----------------------------------------------------------------------------
+# O4: one linear y = A W^T on identical operands
+# ----------------------------------------------------------------------------
+
+
+def linear(a: np.ndarray, lin, act: str, w_deq: Optional[np.ndarray] = None,
+           return_int: bool = False):
+    """A [m, k] holds activation-dtype values as fp64.  Returns fp64 [m, n].
+
+    Weight-only and 16-bit linears: sum_c a[m,c] * w_hat[n,c] in fp64.
+    w8a8 / w4a4: codes of A from :func:`act_quant`, exact integer GEMM
+    acc = sum_c qa * qw, then acc * s_a[m] * s_w[n] in fp64.  With
+    ``return_int`` the exact integer accumulators are returned instead.
+    """
+    s = lin.scheme
+    if s.a_bits < 16:
+        qa, sa = act_quant(a.astype(np.float32), _qmax(s.a_bits))
+        acc = qa.astype(np.float64) @ lin.codes.astype(np.float64).T
+        if return_int:
+            return acc.astype(np.int64)
+        return acc * sa.astype(np.float64)[:, None] * lin.scales.astype(np.float64)[None, :]
+    if w_deq is None:
+        w_deq = dequant(lin, act)
+    return a @ w_deq.T
+
+
+def silu(g: np.ndarray) -> np.ndarray:
+    """SiLU(g) = g * sigmoid(g) = g / (1 + exp(-g)) in fp64."""
+    with np.errstate(over="ignore"):
+        return g / (1.0 + np.exp(-g))
+
+
+def _dsilu(g: np.ndarray) -> np.ndarray:
+    with np.errstate(over="ignore"):
+        sg = 1.0 / (1.0 + np.exp(-g))
+    return sg * (1.0 + g * (1.0 - sg))
+
+
+# ----------------------------------------------------------------------------
+# O5-O7: expert MLP, gate-weighted combine (Eq. 1-2)
+# ----------------------------------------------------------------------------
+
+# Bounds on how far the GPU's fp32 g / u may sit from the fp64 values.  They only
+# decide which a8/a4 codes of the down projection are *fragile* (their rounding
+# decision could go either way given fp32 accumulation), see _down_slack.
+_EPS_FLOAT_ACC = 2.0 ** -20   # relative to sum |a||w|, fp32-accumulated GEMMs
+_EPS_INT_EPI = 2.0 ** -21     # relative to |g|, exact int32 acc + 2 fp32 products
+_EPS_EPI = 2.0 ** -20         # relative to |h|, SiLU + product in fp32
+
+
+def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
+                   w_deq: Optional[np.ndarray]) -> np.ndarray:
+    if lin.scheme.a_bits < 16:
+        return _EPS_INT_EPI * np.abs(out)
+    if w_deq is None:
+        w_deq = dequant(lin, act)
+    return _EPS_FLOAT_ACC * (np.abs(a) @ np.abs(w_deq).T)
+
+
+def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
+    """Per-element output slack of an a8/a4 down projection.
+
+    The GPU rounds its fp32 h to the activation dtype; it can land on another
+    neighbour than the oracle's fp64 h when h64 sits within ``dh`` of a rounding
+    midpoint, and that can move an activation code.  Codes are monotone in h and
+    in 1/amax, so the reachable codes lie between the corner cases computed here.
+    Returns slack [m, n] >= |effect on the down output| of every such move.
+    """
+    qmax = _qmax(lin.scheme.a_bits)
+    lo = round_to_act(h64 - dh, act)
+    hi = round_to_act(h64 + dh, act)
+    q0, s0 = act_quant(hb.astype(np.float32), qmax)
+    alo = np.where(np.sign(lo) == np.sign(hi), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
+    ahi = np.maximum(np.abs(lo), np.abs(hi))
+    amax_lo = alo.max(axis=1)
+    amax_hi = ahi.max(axis=1)
+    rows = np.nonzero((lo != hi).any(axis=1) | (amax_lo != amax_hi))[0]
+    m, n = h64.shape[0], lin.n
+    slack = np.zeros((m, n))
+    if rows.size == 0:
+        return slack
+    q32 = np.float32(qmax)
+    dq = np.zeros((rows.size, h64.shape[1]))
+    ds = np.zeros(rows.size)
+    qabs = np.abs(q0[rows].astype(np.float64))
+    for corner_amax in (amax_lo[rows], amax_hi[rows]):
+        am = corner_amax.astype(np.float32)
+        zero = am == 0
+        safe = np.where(zero, np.float32(1), am)
+        inv = np.where(zero, np.float32(0), (q32 / safe).astype(np.float32))
+        sc = np.where(zero, np.float32(0), (safe / q32).astype(np.float32))
+        ds = np.maximum(ds, np.abs(sc.astype(np.float64) - s0[rows].astype(np.float64)))
+        for hv in (lo[rows], hi[rows]):
+            qc = np.clip(np.rint((hv.astype(np.float32) * inv[:, None]).astype(np.float32)),
+                         -qmax, qmax)
+            qc = np.where(zero[:, None], 0, qc)
+            dq = np.maximum(dq, np.abs(qc - q0[rows]))
+    s_max = np.maximum(s0[rows].astype(np.float64), s0[rows].astype(np.float64) + ds)
+    wabs = np.abs(dequant(lin, act))
+    slack[rows] = (dq * s_max[:, None]) @ wabs.T + ds[:, None] * ((qabs + dq) @ wabs.T)
+    return slack
+
+
+def _expert_mlp(a: np.ndarray, lins: Sequence, act: str, want_slack: bool):
+    """Eq. (1) for one expert on rows a [m, H] (fp64 act values).
+
+    Returns (down output fp64 [m, H], h rounded to act [m, F], slack [m, H] or None).
+    """
+    gate, up, down = lins
+    wg = dequant(gate, act) if gate.scheme.a_bits == 16 else None
+    wu = dequant(up, act) if up.scheme.a_bits == 16 else None
+    g = linear(a, gate, act, wg)
+    u = linear(a, up, act, wu)
+    h64 = silu(g) * u
+    hb = round_to_act(h64, act)                  # rounding point: h stored in act dtype
+    d = linear(hb, down, act)
+    slack = None
+    if want_slack and down.scheme.a_bits < 16:
+        dg = _gate_up_bound(a, gate, act, g, wg)
+        du = _gate_up_bound(a, up, act, u, wu)
+        dh = (np.abs(_dsilu(g) * u) * dg + np.abs(silu(g)) * du
+              + _EPS_EPI * np.abs(h64))
+        slack = _down_slack(h64, dh, hb, down, act)
+    return d, hb, slack
+
+
+def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
+                linears: Sequence[Sequence], E: int, act: str,
+                want_slack: bool = False, return_h: bool = False):
+    """Eq. (2): y[t] = sum_s w[t,s] * Expert_{ids[t,s]}(x[t]) + sum_shared Expert_j(x[t]).
+
+    x: [T, H] activations in act storage; topk_ids int32 [T, k]; topk_w fp32
+    [T, k]; linears[e] = (gate, up, down) for e < E routed, then shared experts.
+    Returns dict with y (fp64, unrounded), slack (fp64 [T,H] or None) and
+    optionally per-expert h.
+    """
+    a_all = act_values(x, act)
+    T, H = a_all.shape
+    k = topk_ids.shape[1]
+    r = route(topk_ids, E)
+    w64 = np.asarray(topk_w, dtype=np.float64).ravel()
+    y = np.zeros((T, H))
+    slack = np.zeros((T, H)) if want_slack else None
+    hs = {}
+    for e in range(E):
+        lo, hi = int(r["offsets"][e]), int(r["offsets"][e + 1])
+        if hi == lo:
+            continue
+        pairs = r["sorted_pair"][lo:hi].astype(np.int64)
+        toks = pairs // k
+        d, hb, sl = _expert_mlp(a_all[toks], linears[e], act, want_slack)
+        # pairs of one expert belong to distinct tokens (top-k ids are distinct per token)
+        np.add.at(y, toks, d * w64[pairs][:, None])
+        if sl is not None:
+            np.add.at(slack, toks, sl * np.abs(w64[pairs])[:, None])
+        if return_h:
+            hs[e] = hb
+    for j in range(len(linears) - E):
+        d, hb, sl = _expert_mlp(a_all, linears[E + j], act, want_slack)
+        y += d
+        if sl is not None:
+            slack += sl
+        if return_h:
+            hs[E + j] = hb
+    out = {"y": y, "slack": slack, "route": r}
+    if return_h:
+        out["h"] = hs
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Tile scheduling (Sec. 4.3 "Tile Schedule"; Sec. 4.2.2 runtime model)
+# ----------------------------------------------------------------------------
+
+
+def lpt_makespan(costs: Sequence[float], P: int, presorted: bool = False) -> float:
+    """Greedy list scheduling: tiles in queue order, each to the machine that frees first.
+
+    With the queue sorted by decreasing cost this is the longest-processing-time
+    rule the paper uses (computationally intensive tiles first).
+    """
+    c = list(costs) if presorted else sorted(costs, reverse=True)
+    loads = [0.0] * P
+    for x in c:
+        i = min(range(P), key=lambda j: (loads[j], j))
+        loads[i] += x
+    return max(loads) if loads else 0.0
+
+
+def optimal_makespan(costs: Sequence[float], P: int) -> float:
+    """Exact minimum makespan by exhaustive assignment (tiny instances only)."""
+    c = sorted(costs, reverse=True)
+    best = [math.inf]
+    loads = [0.0] * P
+
+    def rec(i):
+        if max(loads) >= best[0]:
+            return
+        if i == len(c):
+            best[0] = max(loads)
+            return
+        seen = set()
+        for j in range(P):
+            if loads[j] in seen:
+                continue
+            seen.add(loads[j])
+            loads[j] += c[i]
+            rec(i + 1)
+            loads[j] -= c[i]
+
+    rec(0)
+    return best[0] if c else 0.0

@@ -1,0 +1,435 @@
+"""Seeded synthetic inputs for the MoE-block workloads.
+
+This module only *prepares inputs*: token activations, router top-k ids and
+gate weights, and per-linear quantized weights (codes + scales + zeros).  It
+contains none of the arithmetic of the forward pass itself (no GEMM, no
+runtime activation quantizer, no SiLU-gate, no combine).  Both the CPU oracle
+and the GPU path consume what it returns; neither imports the other.
+
+Shapes follow the paper's evaluated models (Sec. 5.1, table ``tab:exp-model``)
+and the two token counts of its throughput study (Sec. 5.3: 512-token
+memory-bound and 8192-token compute-bound regimes).  The real WikiText-2 inputs,
+trained routers and trained weights are not available, so seeded Gaussian data
+with a Zipf-skewed router stands in for them:
+
+* X ~ N(0, 1), rounded to the activation dtype (RNE).
+* router logits ~ N(0, 1) plus a per-expert bias -s*ln(rank) (an unnormalised
+  Zipf pmf in log space); softmax in fp64, top-k by probability (ties go to the
+  lower expert id); gate weights are the fp32 softmax probabilities, not
+  renormalised.
+* weights ~ N(0, 0.02^2) drawn in fp32, rounded to bf16, then quantized offline
+  with round-to-nearest min-max quantizers (Sec. 2.1).  GPTQ and the Hadamard
+  rotation the paper applies offline need calibration data and trained weights;
+  the packed kernel contract (codes + scale + zero) is identical either way.
+
+Offline quantizers (input preparation, not part of the forward pass):
+
+* ``wNg128`` asymmetric (Sec. 5.2: groups of 128 along K, 16-bit scale and zero):
+  s = fp16((max - min) / (2^N - 1)), z = clamp(rne(-min / s), 0, 2^N - 1)
+  stored as fp16, q = clamp(rne(w / s) + z, 0, 2^N - 1); the dequantized value
+  is s * (q - z), the min-max quantizer with x_min snapped onto the grid.
+* per-channel symmetric (``w8a8``/``w4a4``, Fig. 4 caption): qmax = 2^(b-1) - 1,
+  s = fp32(amax_row / qmax), q = clamp(rne(w / s), -qmax, qmax).
+"""
+
+from __future__ import annotations
+
+import math
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, field
+from typing import Callable, Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Schemes (notation wXaY_gZ_{sym,asym} of the paper's Fig. 1 caption)
+# ----------------------------------------------------------------------------
+
+
+@dataclass(frozen=True)
+class Scheme:
+    w_bits: int      # 16, 8, 4, 3, 2
+    a_bits: int      # 16 = weight-only, 8 or 4 = weight-activation
+    w_group: int     # 128 for weight-only groups, -1 = per output channel
+    a_group: int     # -1 = per token
+    symmetric: int   # 1 for w8a8 / w4a4, 0 for wNg128 asym and 16-bit
+
+    @property
+    def name(self) -> str:
+        if self.w_bits == 16:
+            return "w16"
+        if self.a_bits < 16:
+            return f"w{self.w_bits}a{self.a_bits}"
+        return f"w{self.w_bits}g{self.w_group}"
+
+    @property
+    def weight_only(self) -> bool:
+        return self.w_bits < 16 and self.a_bits == 16
+
+    def bits_per_weight(self, k: int) -> float:
+        """Stored bits per weight including scale/zero overhead."""
+        if self.w_bits == 16:
+            return 16.0
+        if self.weight_only:
+            return self.w_bits + 32.0 / self.w_group   # fp16 scale + fp16 zero
+        return self.w_bits + 32.0 / k                 # one fp32 scale per row
+
+
+W16 = Scheme(16, 16, -1, -1, 0)
+W8A8 = Scheme(8, 8, -1, -1, 1)
+W4A4 = Scheme(4, 4, -1, -1, 1)
+W2G128 = Scheme(2, 16, 128, -1, 0)
+W3G128 = Scheme(3, 16, 128, -1, 0)
+W4G128 = Scheme(4, 16, 128, -1, 0)
+W8G128 = Scheme(8, 16, 128, -1, 0)
+ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128)
+SCHEME_BY_NAME = {s.name: s for s in ALL_SCHEMES}
+
+LINEAR_NAMES = ("gate", "up", "down")
+
+# ----------------------------------------------------------------------------
+# Block configurations
+# ----------------------------------------------------------------------------
+
+Alloc = Callable[[int, int], Tuple[Scheme, Scheme, Scheme]]  # (expert, rank) -> schemes
+
+
+@dataclass
+class BlockConfig:
+    name: str
+    T: int                      # tokens
+    H: int                      # hidden
+    F: int                      # routed-expert FFN
+    E: int                      # routed experts
+    k: int                      # top-k
+    n_shared: int               # shared experts (dense over all tokens)
+    F_shared: int               # shared-expert FFN
+    act: str                    # "fp16" | "bf16"
+    zipf_s: Optional[float]     # router skew; None = no bias
+    alloc: Alloc                # routed-expert schemes
+    shared_alloc: Tuple[Scheme, Scheme, Scheme] = (W16, W16, W16)
+    description: str = ""
+
+    def scaled(self, T: int) -> "BlockConfig":
+        """Same block with another token count (used for bounded CPU samples)."""
+        c = BlockConfig(**{**self.__dict__})
+        c.T = T
+        return c
+
+    def flops(self, counts: Sequence[int]) -> float:
+        """Algorithmic FLOPs of the forward: 2*m*N*K per linear, real rows only."""
+        f = sum(6.0 * int(m) * self.H * self.F for m in counts)
+        f += self.n_shared * 6.0 * self.T * self.H * self.F_shared
+        return f
+
+
+def _tiny_alloc(e: int, rank: int):
+    return [
+        (W4G128, W4G128, W4G128),
+        (W8A8, W8A8, W2G128),
+        (W4A4, W4A4, W4A4),
+        (W16, W16, W16),
+    ][e]
+
+
+def _mixtral_alloc(e: int, rank: int):
+    if rank == 1:
+        return (W8A8, W8A8, W8A8)
+    down = W4G128 if rank == 2 else (W3G128 if rank <= 7 else W2G128)
+    return (W2G128, W2G128, down)
+
+
+def _dsv2_alloc(e: int, rank: int):
+    if rank <= 16:
+        return (W8A8, W8A8, W8A8)
+    if rank <= 48:
+        return (W4G128, W4G128, W4G128)
+    return (W2G128, W2G128, W2G128)
+
+
+def _qwen15_uniform(e: int, rank: int):
+    return (W4A4, W4A4, W4A4)
+
+
+def _qwen15_mixed(e: int, rank: int):
+    if rank <= 2:
+        return (W8A8, W8A8, W8A8)
+    if rank <= 28:
+        return (W4A4, W4A4, W4A4)
+    return (W3G128, W3G128, W3G128)
+
+
+def _qwen2_alloc(e: int, rank: int):
+    return (W8A8, W8A8, W8A8) if rank <= 10 else (W4A4, W4A4, W4A4)
+
+
+CONFIGS: Dict[str, BlockConfig] = {
+    "tiny": BlockConfig(
+        "tiny", T=64, H=256, F=512, E=4, k=2, n_shared=0, F_shared=0, act="fp16",
+        zipf_s=None, alloc=_tiny_alloc,
+        description="tiny MoE block: 64 tokens, hidden 256, FFN 512, 4 experts, top-2, fp16"),
+    "mixtral": BlockConfig(
+        "mixtral", T=4096, H=4096, F=14336, E=8, k=2, n_shared=0, F_shared=0, act="bf16",
+        zipf_s=1.0, alloc=_mixtral_alloc,
+        description="Mixtral-8x7B-shaped prefill: 4096 tokens, hidden 4096, FFN 14336, "
+                    "8 experts, top-2, 3.26 avg weight bits"),
+    "dsv2lite": BlockConfig(
+        "dsv2lite", T=2048, H=2048, F=1408, E=64, k=6, n_shared=2, F_shared=1408, act="bf16",
+        zipf_s=1.2, alloc=_dsv2_alloc, shared_alloc=(W8A8, W8A8, W8A8),
+        description="DeepSeek-V2-Lite-shaped: 2048 tokens, hidden 2048, 64 experts FFN 1408, "
+                    "top-6, 2 shared experts"),
+    "qwen15_uniform": BlockConfig(
+        "qwen15_uniform", T=256, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
+        act="bf16", zipf_s=1.5, alloc=_qwen15_uniform, shared_alloc=(W4A4, W4A4, W4A4),
+        description="Qwen1.5-MoE-shaped decode batch: 256 tokens, 60 experts FFN 1408, top-4, "
+                    "shared FFN 5632, uniform w4a4"),
+    "qwen15_mixed": BlockConfig(
+        "qwen15_mixed", T=256, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
+        act="bf16", zipf_s=1.5, alloc=_qwen15_mixed, shared_alloc=(W8A8, W8A8, W8A8),
+        description="Qwen1.5-MoE-shaped decode batch, mixed w8a8/w4a4/w3g128 at equal avg bits"),
+    "qwen2": BlockConfig(
+        "qwen2", T=16384, H=3584, F=2560, E=64, k=8, n_shared=1, F_shared=20480, act="bf16",
+        zipf_s=1.0, alloc=_qwen2_alloc, shared_alloc=(W8A8, W8A8, W8A8),
+        description="Qwen2-57B-A14B-shaped prefill: 16384 tokens, hidden 3584, 64 experts FFN "
+                    "2560, top-8, shared FFN 20480, w8a8/w4a4"),
+}
+
+# ----------------------------------------------------------------------------
+# dtype helpers (input preparation only)
+# ----------------------------------------------------------------------------
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bit patterns, round-to-nearest-even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
+    return ((u + bias) >> 16).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def f64_to_act(x: np.ndarray, act: str) -> np.ndarray:
+    """Round fp64 data to the activation dtype: float16 array or bf16 bits."""
+    if act == "fp16":
+        return x.astype(np.float16)
+    # direct fp64 -> bf16 RNE: 8 significant bits, spacing 2^(e-8)
+    m, e = np.frexp(x)
+    spacing = np.ldexp(1.0, np.maximum(e - 8, -133))
+    r = np.rint(x / spacing) * spacing
+    return f32_to_bf16_bits(r.astype(np.float32))   # r is bf16-exact, conversion is exact
+
+
+def act_to_f32(a: np.ndarray, act: str) -> np.ndarray:
+    return a.astype(np.float32) if act == "fp16" else bf16_bits_to_f32(a)
+
+# ----------------------------------------------------------------------------
+# offline weight quantizers
+# ----------------------------------------------------------------------------
+
+
+def quantize_g128_asym(w: np.ndarray, bits: int, group: int = 128):
+    """Min-max RTN per group along K; returns (codes uint8, scales fp16, zeros fp16)."""
+    n, k = w.shape
+    assert k % group == 0
+    qmax = (1 << bits) - 1
+    codes = np.empty((n, k), np.uint8)
+    scales = np.empty((n, k // group), np.float16)
+    zeros = np.empty((n, k // group), np.float16)
+    rows = max(1, (1 << 22) // k)
+    for r0 in range(0, n, rows):
+        wg = w[r0:r0 + rows].astype(np.float64).reshape(-1, k // group, group)
+        mx = wg.max(axis=2)
+        mn = wg.min(axis=2)
+        s = ((mx - mn) / qmax).astype(np.float16)
+        degenerate = (mx == mn) | (s == 0)
+        s = np.where(degenerate, np.float16(1.0), s)
+        s64 = s.astype(np.float64)
+        z = np.clip(np.rint(-mn / s64), 0, qmax)
+        z = np.where(degenerate, 0.0, z)
+        q = np.clip(np.rint(wg / s64[..., None]) + z[..., None], 0, qmax)
+        codes[r0:r0 + rows] = q.reshape(-1, k).astype(np.uint8)
+        scales[r0:r0 + rows] = s
+        zeros[r0:r0 + rows] = z.astype(np.float16)
+    return codes, scales, zeros
+
+
+def quantize_sym_per_channel(w: np.ndarray, bits: int):
+    """Symmetric per-output-channel RTN; returns (codes int8, scales fp32)."""
+    qmax = (1 << (bits - 1)) - 1
+    w64 = w.astype(np.float64)
+    amax = np.abs(w64).max(axis=1)
+    s = (amax / qmax).astype(np.float32)
+    s64 = s.astype(np.float64)
+    safe = np.where(s64 == 0, 1.0, s64)
+    q = np.clip(np.rint(w64 / safe[:, None]), -qmax, qmax)
+    q = np.where(s64[:, None] == 0, 0, q)
+    return q.astype(np.int8), s
+
+
+@dataclass
+class QLinear:
+    """One quantized linear, W is [n, k] = [out, in] (nn.Linear layout)."""
+    scheme: Scheme
+    n: int
+    k: int
+    codes: np.ndarray                    # uint8 / int8 [n,k]; bf16 bits uint16 for w16
+    scales: Optional[np.ndarray] = None  # fp16 [n, k/128] | fp32 [n]
+    zeros: Optional[np.ndarray] = None   # fp16 [n, k/128]
+
+    @property
+    def nbytes_packed(self) -> int:
+        s = self.scheme
+        if s.w_bits == 16:
+            return 2 * self.n * self.k
+        if s.weight_only:
+            return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
+        return self.n * self.k * s.w_bits // 8 + 4 * self.n
+
+
+def quantize_linear(w_bf16_f32: np.ndarray, scheme: Scheme) -> QLinear:
+    n, k = w_bf16_f32.shape
+    if scheme.w_bits == 16:
+        return QLinear(scheme, n, k, f32_to_bf16_bits(w_bf16_f32))
+    if scheme.weight_only:
+        c, s, z = quantize_g128_asym(w_bf16_f32, scheme.w_bits, scheme.w_group)
+        return QLinear(scheme, n, k, c, s, z)
+    c, s = quantize_sym_per_channel(w_bf16_f32, scheme.w_bits)
+    return QLinear(scheme, n, k, c, s)
+
+
+def draw_weight(seed: int, expert: int, lin: int, n: int, k: int, std: float = 0.02):
+    """bf16-valued fp32 weight [n,k]; one independent stream per (expert, linear)."""
+    g = np.random.default_rng([seed, 2, expert, lin])
+    w = g.standard_normal((n, k), dtype=np.float32) * np.float32(std)
+    return bf16_bits_to_f32(f32_to_bf16_bits(w))
+
+# ----------------------------------------------------------------------------
+# routing and activations
+# ----------------------------------------------------------------------------
+
+
+def expert_ranks(cfg: BlockConfig, seed: int = 0) -> np.ndarray:
+    """Zipf popularity rank of each routed expert (1 = hottest)."""
+    if cfg.zipf_s is None:
+        return np.arange(1, cfg.E + 1)
+    return np.random.default_rng([seed, 3]).permutation(cfg.E) + 1
+
+
+def make_routing(cfg: BlockConfig, seed: int = 0, T: Optional[int] = None):
+    """Top-k ids int32 [T,k] and gate weights fp32 [T,k]."""
+    T = cfg.T if T is None else T
+    logits = np.random.default_rng([seed, 1]).standard_normal((cfg.T, cfg.E))[:T]
+    if cfg.zipf_s is not None:
+        logits = logits - cfg.zipf_s * np.log(expert_ranks(cfg, seed).astype(np.float64))
+    p = np.exp(logits - logits.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    ids = np.argsort(-p, axis=1, kind="stable")[:, : cfg.k]
+    w = np.take_along_axis(p, ids, axis=1).astype(np.float32)
+    return np.ascontiguousarray(ids.astype(np.int32)), np.ascontiguousarray(w)
+
+
+def make_x(cfg: BlockConfig, seed: int = 0, T: Optional[int] = None) -> np.ndarray:
+    T = cfg.T if T is None else T
+    x = np.random.default_rng([seed, 0]).standard_normal((cfg.T, cfg.H))[:T]
+    return np.ascontiguousarray(f64_to_act(x, cfg.act))
+
+
+def schemes_of(cfg: BlockConfig, seed: int = 0) -> List[Tuple[Scheme, Scheme, Scheme]]:
+    ranks = expert_ranks(cfg, seed)
+    out = [tuple(cfg.alloc(e, int(ranks[e]))) for e in range(cfg.E)]
+    out += [tuple(cfg.shared_alloc)] * cfg.n_shared
+    return out
+
+
+def linear_shapes(cfg: BlockConfig, expert: int) -> List[Tuple[int, int]]:
+    F = cfg.F if expert < cfg.E else cfg.F_shared
+    return [(F, cfg.H), (F, cfg.H), (cfg.H, F)]
+
+
+def avg_weight_bits(cfg: BlockConfig, seed: int = 0) -> float:
+    tot_bits = tot = 0.0
+    for e, sch in enumerate(schemes_of(cfg, seed)):
+        for s, (n, k) in zip(sch, linear_shapes(cfg, e)):
+            tot_bits += s.bits_per_weight(k) * n * k
+            tot += n * k
+    return tot_bits / tot
+
+
+@dataclass
+class Block:
+    cfg: BlockConfig
+    seed: int
+    x: np.ndarray                        # [T,H] float16 or bf16 bits (uint16)
+    topk_ids: np.ndarray                 # int32 [T,k]
+    topk_w: np.ndarray                   # fp32 [T,k]
+    linears: List[List[QLinear]] = field(default_factory=list)  # [E+n_sh][3]
+
+    @property
+    def schemes(self):
+        return [tuple(l.scheme for l in ls) for ls in self.linears]
+
+
+def make_linears(cfg: BlockConfig, seed: int = 0, threads: Optional[int] = None):
+    sch = schemes_of(cfg, seed)
+    jobs = []
+    for e in range(cfg.E + cfg.n_shared):
+        for j, (n, k) in enumerate(linear_shapes(cfg, e)):
+            jobs.append((e, j, n, k, sch[e][j]))
+
+    def run(job):
+        e, j, n, k, s = job
+        return quantize_linear(draw_weight(seed, e, j, n, k), s)
+
+    threads = threads or min(16, os.cpu_count() or 1)
+    with ThreadPoolExecutor(threads) as ex:
+        res = list(ex.map(run, jobs))
+    out = [[None] * 3 for _ in range(cfg.E + cfg.n_shared)]
+    for (e, j, *_), q in zip(jobs, res):
+        out[e][j] = q
+    return out
+
+
+def make_block(cfg: BlockConfig | str, seed: int = 0, T: Optional[int] = None,
+               with_weights: bool = True) -> Block:
+    if isinstance(cfg, str):
+        cfg = CONFIGS[cfg]
+    if T is not None and T != cfg.T:
+        base = cfg
+        cfg = cfg.scaled(T)
+        ids, w = make_routing(base, seed, T)
+        x = make_x(base, seed, T)
+    else:
+        ids, w = make_routing(cfg, seed)
+        x = make_x(cfg, seed)
+    lin = make_linears(cfg, seed) if with_weights else []
+    return Block(cfg, seed, x, ids, w, lin)
+
+
+def random_small_block(seed: int, T: int, H: int, F: int, E: int, k: int,
+                       n_shared: int = 0, F_shared: int = 0, act: str = "bf16",
+                       schemes: Optional[Sequence[Tuple[Scheme, Scheme, Scheme]]] = None,
+                       skew: float = 0.0) -> Block:
+    """Small random block for parity sweeps (shapes must keep K % 128 == 0 and N % 16 == 0
+    for the GPU path; the oracle accepts any shape)."""
+    rng = np.random.default_rng([seed, 7])
+    if schemes is None:
+        pool = list(ALL_SCHEMES)
+        schemes = []
+        for _ in range(E + n_shared):
+            gu = pool[rng.integers(len(pool))]
+            dn = pool[rng.integers(len(pool))]
+            schemes.append((gu, gu, dn))
+    alloc = lambda e, r: schemes[e]
+    cfg = BlockConfig(f"rand{seed}", T, H, F, E, k, n_shared, F_shared, act,
+                      skew if skew > 0 else None, alloc,
+                      shared_alloc=schemes[E] if n_shared else (W16, W16, W16))
+    ids, w = make_routing(cfg, seed)
+    x = make_x(cfg, seed)
+    lins = [[None] * 3 for _ in range(E + n_shared)]
+    for e in range(E + n_shared):
+        for j, (n, kk) in enumerate(linear_shapes(cfg, e)):
+            lins[e][j] = quantize_linear(draw_weight(seed, e, j, n, kk), schemes[e][j])
+    return Block(cfg, seed, x, ids, w, lins)

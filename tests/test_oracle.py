@@ -1,0 +1,379 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+Nothing here compares the oracle with itself: worked examples derived by hand
+(tests/golden/worked_examples.json), brute-force pure-Python evaluation of the
+definitions on tiny inputs (own fp32 / bf16 emulation through ``struct`` and
+``math``), closed forms and invariants, and the LPT scheduling bound.
+"""
+
+import json
+import math
+import os
+import struct
+
+import numpy as np
+import pytest
+
+from oracle import mxmoe_oracle as O
+from paper_2505_05799_amd import workloads as W
+
+GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_examples.json")))
+
+# ---------------------------------------------------------------------------
+# independent scalar helpers (pure Python)
+# ---------------------------------------------------------------------------
+
+
+def f32(x: float) -> float:
+    """Round a Python float to the nearest fp32 value (ties to even)."""
+    return struct.unpack("f", struct.pack("f", x))[0]
+
+
+def bf16_round(x: float) -> float:
+    if x == 0 or math.isinf(x):
+        return x
+    _, e = math.frexp(x)
+    sp = 2.0 ** max(e - 8, -133)
+    return round(x / sp) * sp          # round() is half-to-even
+
+
+def f16_round(x: float) -> float:
+    return struct.unpack("e", struct.pack("e", x))[0]
+
+
+def bits_to_float_bf16(b: int) -> float:
+    return struct.unpack("f", struct.pack("I", (int(b) & 0xFFFF) << 16))[0]
+
+
+def py_act_quant(row, qmax):
+    amax = max(abs(v) for v in row)
+    if amax == 0:
+        return [0] * len(row), 0.0
+    inv = f32(qmax / amax)
+    s = f32(amax / qmax)
+    codes = [max(-qmax, min(qmax, round(f32(v * inv)))) for v in row]
+    return codes, s
+
+
+def py_weight(lin, act, n, c):
+    s = lin.scheme
+    if s.w_bits == 16:
+        w = bits_to_float_bf16(lin.codes[n, c])
+        return f16_round(w) if act == "fp16" else w
+    if s.a_bits == 16:
+        g = c // s.w_group
+        return float(lin.scales[n, g]) * (int(lin.codes[n, c]) - float(lin.zeros[n, g]))
+    return float(lin.scales[n]) * int(lin.codes[n, c])
+
+
+def py_linear(a_row, lin, act):
+    s = lin.scheme
+    if s.a_bits < 16:
+        qa, sa = py_act_quant(a_row, (1 << (s.a_bits - 1)) - 1)
+        out = []
+        for n in range(lin.n):
+            acc = sum(qa[c] * int(lin.codes[n, c]) for c in range(lin.k))
+            out.append(acc * sa * float(lin.scales[n]))
+        return out
+    return [sum(a_row[c] * py_weight(lin, act, n, c) for c in range(lin.k)) for n in range(lin.n)]
+
+
+def py_round_act(x, act):
+    return f16_round(x) if act == "fp16" else bf16_round(x)
+
+
+def py_expert(a_row, lins, act):
+    g = py_linear(a_row, lins[0], act)
+    u = py_linear(a_row, lins[1], act)
+    h = [py_round_act(gi / (1.0 + math.exp(-gi)) * ui, act) for gi, ui in zip(g, u)]
+    return py_linear(h, lins[2], act)
+
+
+def py_moe(block):
+    cfg = block.cfg
+    x = O.act_values(block.x, cfg.act)
+    T, H = x.shape
+    y = np.zeros((T, H))
+    for t in range(T):
+        row = [float(v) for v in x[t]]
+        for s in range(cfg.k):
+            e = int(block.topk_ids[t, s])
+            if not (0 <= e < cfg.E):
+                continue
+            d = py_expert(row, block.linears[e], cfg.act)
+            for h in range(H):
+                y[t, h] += float(block.topk_w[t, s]) * d[h]
+        for j in range(cfg.n_shared):
+            d = py_expert(row, block.linears[cfg.E + j], cfg.act)
+            for h in range(H):
+                y[t, h] += d[h]
+    return y
+
+
+def _lin(scheme, codes, scales=None, zeros=None):
+    codes = np.asarray(codes)
+    return W.QLinear(scheme, codes.shape[0], codes.shape[1], codes, scales, zeros)
+
+# ---------------------------------------------------------------------------
+# worked examples
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("case", GOLDEN["act_quant"]["cases"])
+def test_act_quant_worked(case):
+    codes, s = O.act_quant(np.array([case["row"]], np.float32), case["qmax"])
+    assert codes[0].tolist() == case["codes"]
+    assert float(s[0]) == case["scale"]
+
+
+def test_dequant_g128_worked():
+    g = GOLDEN["dequant_g128"]
+    codes = np.full((1, 128), g["fill_code"], np.uint8)
+    codes[0, :3] = g["codes_first3"]
+    lin = _lin(W.W4G128, codes, np.array([[g["scale"]]], np.float16), np.array([[g["zero"]]], np.float16))
+    w = O.dequant(lin, "bf16")
+    assert w[0, :3].tolist() == g["values_first3"]
+    assert np.all(w[0, 3:] == g["fill_value"])
+
+
+def test_linear_w8a8_worked():
+    g = GOLDEN["linear_w8a8"]
+    lin = _lin(W.W8A8, np.array([g["w_codes"]], np.int8), np.array([g["w_scale"]], np.float32))
+    a = np.array([g["a"]])
+    assert int(O.linear(a, lin, "bf16", return_int=True)[0, 0]) == g["acc"]
+    assert float(O.linear(a, lin, "bf16")[0, 0]) == g["out"]
+
+
+def test_moe_w16_worked():
+    g = GOLDEN["moe_w16"]
+    bf = lambda m: W.f32_to_bf16_bits(np.array(m, np.float32))
+    zero = [_lin(W.W16, bf([[0.0, 0.0]])), _lin(W.W16, bf([[0.0, 0.0]])), _lin(W.W16, bf([[0.0], [0.0]]))]
+    one = [_lin(W.W16, bf(g["w_gate"])), _lin(W.W16, bf(g["w_up"])), _lin(W.W16, bf(g["w_down"]))]
+    x = bf([g["x"]])
+    out = O.moe_forward(x, np.array([[g["topk_id"]]], np.int32), np.array([[g["topk_w"]]], np.float32),
+                        [zero, one], 2, "bf16", return_h=True)
+    assert out["h"][1][0, 0] == g["h"]
+    assert out["y"][0].tolist() == g["y"]
+
+# ---------------------------------------------------------------------------
+# routing: brute force and invariants
+# ---------------------------------------------------------------------------
+
+
+def _py_route(ids, E):
+    flat = [int(v) for v in np.asarray(ids).ravel()]
+    sorted_pair, counts = [], [0] * E
+    for e in range(E):
+        for p, v in enumerate(flat):
+            if v == e:
+                sorted_pair.append(p)
+                counts[e] += 1
+    return counts, sorted_pair
+
+
+@pytest.mark.parametrize("T,k,E,seed", [(1, 1, 1, 0), (7, 3, 5, 1), (33, 2, 4, 2), (64, 4, 4, 3),
+                                         (100, 6, 64, 4), (0, 2, 3, 5), (50, 8, 8, 6)])
+def test_route_brute_force(T, k, E, seed):
+    rng = np.random.default_rng(seed)
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]) if T else np.zeros((0, k), np.int64)
+    r = O.route(ids, E)
+    counts, sp = _py_route(ids, E)
+    assert r["counts"].tolist() == counts
+    assert r["sorted_pair"].tolist() == sp
+    assert int(r["offsets"][-1]) == T * k == sum(counts)
+    assert np.all(r["inv"][r["sorted_pair"]] == np.arange(T * k))
+    assert sorted(r["sorted_pair"].tolist()) == list(range(T * k))
+
+
+def test_route_special_cases():
+    T, k = 9, 3
+    # E = 1 with k = 1: identity order
+    r = O.route(np.zeros((T, 1), np.int32), 1)
+    assert r["sorted_pair"].tolist() == list(range(T))
+    # k = E: every expert gets every token, in token order
+    ids = np.array([np.random.default_rng(t).permutation(k) for t in range(T)])
+    r = O.route(ids, k)
+    assert r["counts"].tolist() == [T] * k
+    for e in range(k):
+        toks = r["sorted_pair"][r["offsets"][e]:r["offsets"][e + 1]] // k
+        assert toks.tolist() == list(range(T))
+
+
+def test_route_bad_ids_dropped():
+    ids = np.array([[0, 5], [-1, 1], [2, 1]], np.int32)
+    r = O.route(ids, 3)
+    assert r["bad"].tolist() == [False, True, True, False, False, False]
+    assert r["sorted_pair"].tolist() == [0, 3, 5, 4]
+    assert r["inv"].tolist() == [0, -1, -1, 1, 3, 2]
+
+# ---------------------------------------------------------------------------
+# quantization: dequant against the original weights, act-quant properties
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W8A8, W.W4A4])
+def test_dequant_recovers_weights(scheme):
+    w = W.draw_weight(11, 0, 0, 48, 384)
+    lin = W.quantize_linear(w, scheme)
+    deq = O.dequant(lin, "bf16")
+    if scheme.a_bits == 16:
+        s = np.repeat(lin.scales.astype(np.float64), 128, axis=1)
+        qmax = (1 << scheme.w_bits) - 1
+        inner = (lin.codes > 0) & (lin.codes < qmax)
+        err = np.abs(deq - w.astype(np.float64))
+        assert np.all(err[inner] <= 0.5 * s[inner] * (1 + 1e-12))
+        # clamped codes sit at the ends of the range: error bounded by one step
+        assert np.all(err <= 1.0 * s + 1e-12)
+        assert inner.mean() > 0.5 if scheme.w_bits > 2 else True
+    else:
+        s = lin.scales.astype(np.float64)[:, None]
+        assert np.all(np.abs(deq - w) <= 0.5 * s * (1 + 1e-12))
+        qmax = (1 << (scheme.w_bits - 1)) - 1
+        assert np.all(np.abs(lin.codes).max(axis=1) == qmax)
+
+
+def test_w16_fp16_conversion():
+    w = np.array([[1.0, -0.0078125, 3.0e-6, 60000.0, 1.0e-7]], np.float32)
+    lin = W.quantize_linear(w, W.W16)
+    assert O.dequant(lin, "bf16")[0].tolist() == [bf16_round(v) for v in w[0].tolist()]
+    assert O.dequant(lin, "fp16")[0].tolist() == [f16_round(bf16_round(v)) for v in w[0].tolist()]
+
+
+@pytest.mark.parametrize("qmax", [7, 127])
+def test_act_quant_properties(qmax):
+    rng = np.random.default_rng(qmax)
+    a = rng.standard_normal((40, 300)).astype(np.float32)
+    a[3] = 0
+    q, s = O.act_quant(a, qmax)
+    assert q.dtype == np.int8 and np.all(np.abs(q) <= qmax)
+    assert s[3] == 0 and np.all(q[3] == 0)
+    rows = [r for r in range(40) if r != 3]
+    # the amax element maps to +-qmax
+    am = np.abs(a).argmax(axis=1)
+    assert np.all(np.abs(q[rows, am[rows]]) == qmax)
+    # dequantization error within half a step (plus fp32 rounding)
+    err = np.abs(q[rows].astype(np.float64) * s[rows, None] - a[rows])
+    assert np.all(err <= 0.5 * s[rows, None] * (1 + 1e-5) + 1e-30)
+    # scaling by a power of two keeps the codes and scales the step exactly
+    q2, s2 = O.act_quant(a * np.float32(4.0), qmax)
+    assert np.array_equal(q, q2) and np.array_equal(s2, s * np.float32(4.0))
+    # brute force on a few rows
+    for r in (0, 5, 17):
+        pq, ps = py_act_quant([float(v) for v in a[r]], qmax)
+        assert q[r].tolist() == pq and float(s[r]) == ps
+
+# ---------------------------------------------------------------------------
+# linear and block: brute force on tiny shapes
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+def test_linear_brute_force(scheme, act):
+    m, n, k = 3, 5, 256
+    lin = W.quantize_linear(W.draw_weight(3, 1, 2, n, k), scheme)
+    x = W.f64_to_act(np.random.default_rng(4).standard_normal((m, k)), act)
+    a = O.act_values(x, act)
+    got = O.linear(a, lin, act)
+    for i in range(m):
+        ref = py_linear([float(v) for v in a[i]], lin, act)
+        np.testing.assert_allclose(got[i], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_int_linear_doubling():
+    lin = W.quantize_linear(W.draw_weight(5, 0, 0, 16, 256), W.W8A8)
+    a = O.act_values(W.f64_to_act(np.random.default_rng(1).standard_normal((4, 256)), "bf16"), "bf16")
+    assert np.array_equal(O.linear(2 * a, lin, "bf16"), 2 * O.linear(a, lin, "bf16"))
+    assert np.array_equal(O.linear(2 * a, lin, "bf16", return_int=True),
+                          O.linear(a, lin, "bf16", return_int=True))
+
+
+MIXED = [(W.W4G128, W.W4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4), (W.W16, W.W16, W.W8A8),
+         (W.W3G128, W.W3G128, W.W16), (W.W4A4, W.W8G128, W.W4G128)]
+
+
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+def test_moe_brute_force(act):
+    blk = W.random_small_block(21, T=5, H=128, F=128, E=4, k=2, n_shared=1, F_shared=128, act=act,
+                               schemes=MIXED)
+    blk.topk_ids[2, 1] = 9          # an invalid expert id is skipped
+    out = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 4, act)
+    np.testing.assert_allclose(out["y"], py_moe(blk), rtol=1e-9, atol=1e-12)
+
+
+def test_moe_zero_input():
+    blk = W.random_small_block(2, T=5, H=128, F=128, E=3, k=2, schemes=MIXED[:3])
+    blk.x[:] = 0
+    out = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 3, "bf16")
+    assert np.all(out["y"] == 0)
+
+
+def test_moe_equivariance_and_relabel():
+    blk = W.random_small_block(3, T=12, H=128, F=128, E=4, k=2, n_shared=1, F_shared=256,
+                               schemes=MIXED)
+    base = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 4, "bf16")["y"]
+    perm = np.random.default_rng(0).permutation(12)
+    out = O.moe_forward(blk.x[perm], blk.topk_ids[perm], blk.topk_w[perm], blk.linears, 4, "bf16")["y"]
+    assert np.array_equal(out, base[perm])
+    relabel = np.array([2, 0, 3, 1])           # expert e becomes relabel[e]
+    lin2 = [None] * 4
+    for e in range(4):
+        lin2[relabel[e]] = blk.linears[e]
+    lin2 += blk.linears[4:]
+    out = O.moe_forward(blk.x, relabel[blk.topk_ids].astype(np.int32), blk.topk_w, lin2, 4, "bf16")["y"]
+    np.testing.assert_allclose(out, base, rtol=1e-12, atol=1e-14)
+
+
+def test_uniform_bf16_is_dense_mlp():
+    """E = 1, k = 1, w = 1 with 16-bit weights is a dense gated-SiLU MLP."""
+    blk = W.random_small_block(4, T=7, H=128, F=24, E=1, k=1, schemes=[(W.W16, W.W16, W.W16)])
+    blk.topk_w[:] = 1.0
+    y = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 1, "bf16")["y"]
+    x = np.array([[bits_to_float_bf16(b) for b in row] for row in blk.x])
+    wg, wu, wd = [np.array([[bits_to_float_bf16(b) for b in r] for r in l.codes]) for l in blk.linears[0]]
+    g, u = x @ wg.T, x @ wu.T
+    h = np.vectorize(bf16_round)(g * u / (1 + np.exp(-g)))
+    np.testing.assert_allclose(y, h @ wd.T, rtol=1e-12, atol=1e-14)
+
+
+def test_slack_properties():
+    blk = W.random_small_block(8, T=16, H=128, F=128, E=2, k=1,
+                               schemes=[(W.W16, W.W16, W.W4A4), (W.W4G128, W.W4G128, W.W16)])
+    out = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 2, "bf16", want_slack=True)
+    sl = out["slack"]
+    assert np.all(sl >= 0)
+    # tokens routed only to the 16-bit-activation down projection carry no slack
+    only1 = blk.topk_ids[:, 0] == 1
+    assert np.all(sl[only1] == 0)
+
+# ---------------------------------------------------------------------------
+# tile scheduling: LPT against the exact optimum (Graham's bound)
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_lpt_graham_bound(seed):
+    rng = np.random.default_rng(seed)
+    P = int(rng.integers(2, 4))
+    costs = rng.integers(1, 20, size=int(rng.integers(P + 1, 9))).astype(float).tolist()
+    opt = O.optimal_makespan(costs, P)
+    lpt = O.lpt_makespan(costs, P)
+    assert opt <= lpt <= (4.0 / 3.0 - 1.0 / (3 * P)) * opt + 1e-9
+    assert opt >= max(max(costs), sum(costs) / P) - 1e-9
+
+
+def test_lpt_tight_instance():
+    # Graham's tight example for P = 2: {3,3,2,2,2} has OPT 6 and LPT 7 = (4/3 - 1/6) * 6
+    assert O.optimal_makespan([3, 3, 2, 2, 2], 2) == 6
+    assert O.lpt_makespan([3, 3, 2, 2, 2], 2) == 7
+
+
+def test_runtime_model_many_tiles():
+    """Sec. 4.2.2: with #tiles >> #processors, makespan ~ sum(c) / P."""
+    rng = np.random.default_rng(0)
+    P = 256
+    errs = []
+    for n in (512, 4096, 32768):
+        c = rng.choice([1.0, 2.5, 7.0], size=n)
+        errs.append(O.lpt_makespan(c, P) / (c.sum() / P) - 1)
+    assert errs[-1] < 0.01 and errs[0] > errs[-1]
