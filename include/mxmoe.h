@@ -1,0 +1,242 @@
+/*
+ * mxmoe.h - C ABI of the MI355X (gfx950) mixed-precision MoE block.
+ *
+ * The library evaluates one MoE block forward (MxMoE, arXiv 2505.05799,
+ * Sec. 2.2 Eq. (1)-(2)):
+ *
+ *     y[t] = sum_{s<k} w[t,s] * Expert_{ids[t,s]}(x[t]) + sum_j Shared_j(x[t])
+ *     Expert(x) = W_down( SiLU(W_gate x) * (W_up x) )
+ *
+ * where every linear block (gate, up, down) of every expert carries its own
+ * quantization scheme (linear-block granularity, Sec. 3.1).  Supported schemes
+ * (notation wXaY_gZ of the Fig. 1 caption):
+ *
+ *   w16      16-bit weights (bf16, or fp16 when activations are fp16)
+ *   wNg128   weight-only, N in {2,3,4,8}, asymmetric, fp16 scale and fp16 zero
+ *            per group of 128 along K (Sec. 5.2): w = s * (q - z)
+ *   w8a8     8-bit per-output-channel symmetric weights (fp32 scale, codes in
+ *            [-127,127]) and 8-bit per-token symmetric activations
+ *   w4a4     same with 4 bits (codes in [-7,7])
+ *
+ * Activations of w8a8 / w4a4 linears are quantized at run time, per token
+ * (Sec. 4.2.2): amax = max|a|, inv = fl32(qmax/amax), s = fl32(amax/qmax),
+ * q = clamp(rne(fl32(a*inv)), -qmax, qmax); an all-zero row gets s = 0.
+ *
+ * Conventions for every entry point:
+ *   - Pointers are DEVICE pointers unless marked (host).
+ *   - The caller owns every buffer.  No call allocates device memory, frees,
+ *     or synchronizes the stream; work is enqueued on `stream` (0 = null
+ *     stream) and completes asynchronously.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     failed validation returns a status and enqueues nothing.
+ *   - MXMOE_ERR_HIP means a launch failed; the stream state is then undefined.
+ *   - Calls on different streams with separate workspaces may run concurrently.
+ *   - Identical inputs give bitwise identical outputs (no floating-point
+ *     atomics; routing order is fixed).
+ */
+#ifndef MXMOE_H
+#define MXMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#if defined(__GNUC__)
+#define MXMOE_API __attribute__((visibility("default")))
+#else
+#define MXMOE_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MXMOE_OK = 0,
+  MXMOE_ERR_INVALID_ARG = 1,  /* null / misaligned pointer, bad size or count   */
+  MXMOE_ERR_UNSUPPORTED = 2,  /* scheme or shape outside the supported set      */
+  MXMOE_ERR_WORKSPACE = 3,    /* workspace or packed buffer too small           */
+  MXMOE_ERR_HIP = 4           /* a HIP launch failed                            */
+} mxmoe_status;
+
+typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
+
+/* Quantization scheme of one linear block: w{w_bits}a{a_bits}_g{w_group}.
+ * Accepted combinations:
+ *   {16,16,-1,-1,0}  {8,8,-1,-1,1}  {4,4,-1,-1,1}  {N,16,128,-1,0} N=2,3,4,8  */
+typedef struct {
+  int32_t w_bits;
+  int32_t a_bits;     /* 16 = weight-only                                       */
+  int32_t w_group;    /* 128, or -1 = per output channel                        */
+  int32_t a_group;    /* -1 = per token (the only activation granularity here)  */
+  int32_t symmetric;  /* 1 for w8a8 / w4a4, 0 otherwise                         */
+} mxmoe_scheme;
+
+/* One linear block y = x W^T with W of shape [n, k] = [out, in].
+ * Requirements: n % 16 == 0, k % 128 == 0, n,k > 0.                          */
+typedef struct {
+  int32_t n;
+  int32_t k;
+  mxmoe_scheme s;
+} mxmoe_linear;
+
+/* ---------------------------------------------------------------- packing */
+
+/* Bytes of the packed form of linear *L (host) for activations `act`:
+ *   wNg128: n*k*N/8 + (n*k/128)*4   (N + 0.25 bits per weight, Sec. 5.2)
+ *   w8a8/w4a4: n*k*b/8 + 4*n
+ *   w16: 2*n*k
+ * Returns 0 if *L is not supported.                                          */
+MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
+
+/* Pack the quantized operands of one linear into the tile-major layout the
+ * Group-GEMM streams (weight fragments in MFMA lane order, group metadata next
+ * to its codes).  Runs once per weight load.
+ *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4 int8 [n,k] in
+ *            [-qmax, qmax]; w16: 16-bit weights [n,k] of dtype `w16_src`.
+ *   scales : wNg128 fp16 [n, k/128]; w8a8/w4a4 fp32 [n]; NULL for w16.
+ *   zeros  : wNg128 fp16 [n, k/128] holding integers in [0, 2^N-1]; else NULL.
+ *   w16_src: dtype of 16-bit source weights; converted (RNE) to `act`.
+ *   packed : output, mxmoe_packed_bytes(L, act) bytes, 256-byte aligned.
+ * All inputs 4-byte aligned.  Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE
+ * (packed_bytes too small), HIP.                                             */
+MXMOE_API mxmoe_status mxmoe_pack_weights(const mxmoe_linear* L, mxmoe_dtype act, mxmoe_dtype w16_src,
+                                const void* codes, const void* scales, const void* zeros,
+                                void* packed, size_t packed_bytes, hipStream_t stream);
+
+/* Inverse of mxmoe_pack_weights (testing and inspection): writes codes,
+ * scales and zeros in the input formats above (w16: `act` dtype values).    */
+MXMOE_API mxmoe_status mxmoe_unpack_weights(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
+                                  void* codes, void* scales, void* zeros, hipStream_t stream);
+
+/* ---------------------------------------------------------------- routing */
+
+/* Scratch bytes mxmoe_route_permute needs for T tokens, top-k, E experts.   */
+MXMOE_API size_t mxmoe_route_workspace_bytes(int32_t T, int32_t k, int32_t E);
+
+/* Group the T*k (token, slot) pairs by expert (the X_e of Eq. (2)).  Pair id
+ * p = t*k + s.  Pairs are ordered by (expert, p): stable, so the result is
+ * unique.  Pairs whose id lies outside [0, E) are dropped.
+ *   topk_ids   : int32 [T,k]
+ *   counts     : int32 [E]       pairs per expert
+ *   offsets    : int32 [E+1]     exclusive prefix of counts
+ *   sorted_pair: int32 [T*k]     pair ids in sorted order (first offsets[E])
+ *   inv        : int32 [T*k]     position of pair p, -1 if dropped
+ *   status     : int32 [1]       0, or 1 + the smallest dropped pair id
+ * Limits: 1 <= k <= E <= 1024, T >= 0, T*k < 2^31.                           */
+MXMOE_API mxmoe_status mxmoe_route_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E,
+                                 int32_t* counts, int32_t* offsets, int32_t* sorted_pair,
+                                 int32_t* inv, int32_t* status, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------ activation quant */
+
+/* Per-row symmetric quantization of a [rows, cols] activation matrix (row
+ * stride `ld` elements) with the fp32 recipe in the header comment.
+ *   codes: int8 [rows, cols] (dense), scales: fp32 [rows].  qmax = 127 or 7. */
+MXMOE_API mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32_t cols,
+                             int64_t ld, int32_t qmax, int8_t* codes, float* scales,
+                             hipStream_t stream);
+
+/* --------------------------------------------------------- one linear */
+
+MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
+
+/* out = a W^T for one packed linear, through the same micro-kernels the block
+ * uses (testing and single-GEMM measurement).
+ *   a  : [m, k] `act` activations (dense)
+ *   out: w8a8 / w4a4 -> int32 [m, n] exact integer accumulators
+ *        sum_c qa[m,c]*qw[n,c] (qa from the per-token quantizer);
+ *        other schemes -> fp32 [m, n] with fp32 accumulation.               */
+MXMOE_API mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
+                                  int32_t m, const void* a, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------- MoE block */
+
+typedef struct {
+  int32_t hidden;        /* H: multiple of 128                                 */
+  int32_t ffn;           /* F of routed experts: multiple of 128               */
+  int32_t n_experts;     /* E routed experts, 1..1024                          */
+  int32_t top_k;         /* k, 1..E                                            */
+  int32_t n_shared;      /* shared experts run densely over all tokens, 0..64  */
+  int32_t ffn_shared;    /* F of shared experts (multiple of 128 if n_shared)  */
+  mxmoe_dtype act;       /* dtype of x, y and the gated intermediate h         */
+  /* host [(n_experts + n_shared) * 3]: gate, up, down of expert 0, 1, ...,
+   * routed experts first.  Gate and up of one expert must share a scheme.    */
+  const mxmoe_scheme* scheme;
+  /* host array of device pointers to the packed linears, same order          */
+  const void* const* packed;
+} mxmoe_block;
+
+/* Size of, and host-side fill for, the device block table: the caller copies
+ * the filled host buffer to device memory once (e.g. hipMemcpy) and passes
+ * it to every forward.  It holds the packed pointers, so it must be refilled
+ * when weights move.                                                        */
+MXMOE_API size_t mxmoe_block_table_bytes(const mxmoe_block* B);
+MXMOE_API mxmoe_status mxmoe_block_table_fill(const mxmoe_block* B, void* host_buf, size_t host_bytes);
+
+/* Workspace bytes mxmoe_moe_forward needs for T tokens (256-byte aligned
+ * buffer).  Holds routing arrays, the tile plan, activation codes, the gated
+ * intermediate h, and fp32 per-slot down-projection rows.                   */
+MXMOE_API size_t mxmoe_workspace_bytes(const mxmoe_block* B, int32_t T);
+
+/* The MoE block forward.
+ *   x       : [T, hidden] act            topk_ids: int32 [T, k]
+ *   topk_w  : fp32 [T, k] gate weights   y       : [T, hidden] act (output)
+ * Out-of-range expert ids contribute nothing; the workspace status word
+ * (see mxmoe_workspace_layout) records 1 + the first such pair id.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.                          */
+MXMOE_API mxmoe_status mxmoe_moe_forward(const mxmoe_block* B, const void* block_table, int32_t T,
+                               const void* x, const int32_t* topk_ids, const float* topk_w,
+                               void* y, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/* Options of mxmoe_moe_forward_ex (measurement and testing).                 */
+typedef struct {
+  /* host [(n_experts + n_shared)] or NULL: experts with mask 0 get no tiles
+   * (their rows keep whatever the workspace held); used to time subsets.   */
+  const uint8_t* expert_mask;
+  /* 1: run gate/up, h-quantization and down as separate launches instead of
+   * one persistent launch.                                                  */
+  int32_t split_phases;
+  /* 1: skip the combine (y untouched) - to time the Group-GEMM alone.       */
+  int32_t skip_combine;
+  int32_t reserved[4];
+} mxmoe_forward_opts;
+
+MXMOE_API mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table, int32_t T,
+                                  const void* x, const int32_t* topk_ids, const float* topk_w,
+                                  void* y, void* workspace, size_t workspace_bytes,
+                                  const mxmoe_forward_opts* opts, hipStream_t stream);
+
+/* Byte offsets of the intermediates inside the forward workspace (testing).
+ * An offset of SIZE_MAX means the buffer is not present for this block.    */
+typedef struct {
+  size_t status;        /* int32 [4]: [0] = 0 or 1 + first dropped pair      */
+  size_t counts;        /* int32 [E]                                         */
+  size_t offsets;       /* int32 [E+1]                                       */
+  size_t sorted_pair;   /* int32 [T*k]                                       */
+  size_t inv;           /* int32 [T*k]                                       */
+  size_t plan;          /* int32 [2][n_experts+n_shared][8] tile plan        */
+  size_t xq8, xs8;      /* int8 [T,H], fp32 [T]: x codes for a8 gate/up      */
+  size_t xq4, xs4;      /* int8 [T,H], fp32 [T]: x codes for a4 gate/up      */
+  size_t h;             /* act [T*k, F]: routed h rows, sorted-pair order    */
+  size_t h_shared;      /* act [n_shared, T, F_shared]                       */
+  size_t hq, hs;        /* int8 [T*k, F], fp32 [T*k]: routed h codes         */
+  size_t hq_shared, hs_shared; /* int8 [n_shared,T,F_shared], fp32 [n_shared,T] */
+  size_t slots;         /* fp32 [T, k + n_shared, H]: weighted down rows     */
+  size_t total;         /* = mxmoe_workspace_bytes                           */
+} mxmoe_ws_layout;
+
+MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);
+
+MXMOE_API const char* mxmoe_status_string(mxmoe_status s);
+
+/* Library version, (major << 16) | minor.                                    */
+MXMOE_API int32_t mxmoe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MXMOE_H */

@@ -1,0 +1,459 @@
+// Host side of the C ABI: argument validation, workspace carving and launch
+// sequencing.  Nothing here allocates device memory or synchronizes.
+#include <string.h>
+
+#include <algorithm>
+
+#include "mxmoe_internal.h"
+
+using namespace mxmoe;
+
+namespace {
+
+constexpr int kMaxE = 1024;
+constexpr int kMaxShared = 64;
+constexpr int kMaxG = 2048;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// scheme -> micro-kernel kind, -1 if unsupported
+int scheme_kind(const mxmoe_scheme& s) {
+  if (s.a_group != -1) return -1;
+  if (s.w_bits == 16 && s.a_bits == 16 && s.w_group == -1 && s.symmetric == 0) return K_W16;
+  if (s.a_bits == 8 && s.w_bits == 8 && s.w_group == -1 && s.symmetric == 1) return K_W8A8;
+  if (s.a_bits == 4 && s.w_bits == 4 && s.w_group == -1 && s.symmetric == 1) return K_W4A4;
+  if (s.a_bits == 16 && s.w_group == 128 && s.symmetric == 0) {
+    switch (s.w_bits) {
+      case 2: return K_W2G;
+      case 3: return K_W3G;
+      case 4: return K_W4G;
+      case 8: return K_W8G;
+    }
+  }
+  return -1;
+}
+
+bool same_scheme(const mxmoe_scheme& a, const mxmoe_scheme& b) {
+  return a.w_bits == b.w_bits && a.a_bits == b.a_bits && a.w_group == b.w_group && a.a_group == b.a_group &&
+         a.symmetric == b.symmetric;
+}
+
+bool valid_dtype(int d) { return d == MXMOE_F16 || d == MXMOE_BF16; }
+
+mxmoe_status check_linear(const mxmoe_linear* L, int* kind) {
+  if (!L) return MXMOE_ERR_INVALID_ARG;
+  if (L->n <= 0 || L->k <= 0) return MXMOE_ERR_INVALID_ARG;
+  const int kd = scheme_kind(L->s);
+  if (kd < 0) return MXMOE_ERR_UNSUPPORTED;
+  if (L->n % 16 || L->k % 128) return MXMOE_ERR_UNSUPPORTED;
+  if ((int64_t)L->n * L->k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
+  *kind = kd;
+  return MXMOE_OK;
+}
+
+size_t packed_bytes_kind(int kd, int n, int k) {
+  size_t b = (size_t)codes_bytes(kd, n, k);
+  if (kind_is_int(kd)) b += 4 * (size_t)n;
+  return b;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+struct BlockInfo {
+  int H, F, E, k, nsh, Fsh, act, G;
+  bool any_x8 = false, any_x4 = false, any_hq = false, any_hq_sh = false;
+  int kinds[kMaxG][3];
+};
+
+mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
+  if (!B || !B->scheme) return MXMOE_ERR_INVALID_ARG;
+  if (!valid_dtype(B->act)) return MXMOE_ERR_INVALID_ARG;
+  if (B->hidden <= 0 || B->ffn <= 0 || B->n_experts <= 0 || B->top_k <= 0) return MXMOE_ERR_INVALID_ARG;
+  if (B->n_experts > kMaxE || B->top_k > B->n_experts) return MXMOE_ERR_INVALID_ARG;
+  if (B->n_shared < 0 || B->n_shared > kMaxShared) return MXMOE_ERR_INVALID_ARG;
+  if (B->n_shared > 0 && B->ffn_shared <= 0) return MXMOE_ERR_INVALID_ARG;
+  if (B->hidden % 128 || B->ffn % 128 || (B->n_shared > 0 && B->ffn_shared % 128)) return MXMOE_ERR_UNSUPPORTED;
+  bi->H = B->hidden;
+  bi->F = B->ffn;
+  bi->E = B->n_experts;
+  bi->k = B->top_k;
+  bi->nsh = B->n_shared;
+  bi->Fsh = B->n_shared > 0 ? B->ffn_shared : 0;
+  bi->act = B->act;
+  bi->G = bi->E + bi->nsh;
+  bi->any_x8 = bi->any_x4 = bi->any_hq = bi->any_hq_sh = false;
+  if (bi->G > kMaxG) return MXMOE_ERR_UNSUPPORTED;
+  for (int g = 0; g < bi->G; ++g) {
+    const mxmoe_scheme* s = B->scheme + 3 * g;
+    for (int j = 0; j < 3; ++j) {
+      const int kd = scheme_kind(s[j]);
+      if (kd < 0) return MXMOE_ERR_UNSUPPORTED;
+      bi->kinds[g][j] = kd;
+    }
+    if (!same_scheme(s[0], s[1])) return MXMOE_ERR_UNSUPPORTED;  // gate|up share one tile
+    const bool sh = g >= bi->E;
+    const int kg = bi->kinds[g][0];
+    if (kg == K_W8A8) bi->any_x8 = true;
+    if (kg == K_W4A4) bi->any_x4 = true;
+    if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
+  }
+  return MXMOE_OK;
+}
+
+WsLayout layout_of(const BlockInfo& bi, int T) {
+  WsLayout L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align256(o + bytes);
+    return at;
+  };
+  const size_t P = (size_t)T * bi.k;
+  const size_t nchunks = (P + kRouteChunk - 1) / kRouteChunk;
+  L.status = take(16 * 4);
+  L.counts = take(4 * (size_t)bi.E);
+  L.offsets = take(4 * ((size_t)bi.E + 1));
+  L.sorted_pair = take(4 * P);
+  L.inv = take(4 * P);
+  L.chunk_counts = take(4 * nchunks * bi.E);
+  L.chunk_bad = take(4 * nchunks);
+  L.plan = take(4 * (size_t)plan_ints(bi.G));
+  L.down_qmax = take(4 * (size_t)bi.G);
+  L.xq8 = L.xs8 = L.xq4 = L.xs4 = kNone;
+  if (bi.any_x8) { L.xq8 = take((size_t)T * bi.H); L.xs8 = take(4 * (size_t)T); }
+  if (bi.any_x4) { L.xq4 = take((size_t)T * bi.H); L.xs4 = take(4 * (size_t)T); }
+  L.h = take(2 * P * bi.F);
+  L.h_shared = bi.nsh ? take(2 * (size_t)bi.nsh * T * bi.Fsh) : kNone;
+  L.hq = L.hs = L.hq_shared = L.hs_shared = kNone;
+  if (bi.any_hq) { L.hq = take(P * bi.F); L.hs = take(4 * P); }
+  if (bi.any_hq_sh) { L.hq_shared = take((size_t)bi.nsh * T * bi.Fsh); L.hs_shared = take(4 * (size_t)bi.nsh * T); }
+  L.slots = take(4 * (size_t)T * (bi.k + bi.nsh) * bi.H);
+  L.total = o;
+  return L;
+}
+
+template <typename TT> TT* at(void* ws, size_t off) {
+  return off == kNone ? nullptr : reinterpret_cast<TT*>(reinterpret_cast<uint8_t*>(ws) + off);
+}
+
+mxmoe_status hip_status(hipError_t e) { return e == hipSuccess ? MXMOE_OK : MXMOE_ERR_HIP; }
+
+int current_device() {
+  int d = 0;
+  if (hipGetDevice(&d) != hipSuccess) d = 0;
+  return d;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t mxmoe_version(void) { return (0 << 16) | 1; }
+
+const char* mxmoe_status_string(mxmoe_status s) {
+  switch (s) {
+    case MXMOE_OK: return "ok";
+    case MXMOE_ERR_INVALID_ARG: return "invalid argument";
+    case MXMOE_ERR_UNSUPPORTED: return "unsupported scheme or shape";
+    case MXMOE_ERR_WORKSPACE: return "workspace or buffer too small";
+    case MXMOE_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act) {
+  int kd;
+  if (!valid_dtype(act) || check_linear(L, &kd) != MXMOE_OK) return 0;
+  return packed_bytes_kind(kd, L->n, L->k);
+}
+
+mxmoe_status mxmoe_pack_weights(const mxmoe_linear* L, mxmoe_dtype act, mxmoe_dtype w16_src, const void* codes,
+                                const void* scales, const void* zeros, void* packed, size_t packed_bytes,
+                                hipStream_t stream) {
+  int kd;
+  mxmoe_status st = check_linear(L, &kd);
+  if (st != MXMOE_OK) return st;
+  if (!valid_dtype(act) || !valid_dtype(w16_src)) return MXMOE_ERR_INVALID_ARG;
+  if (!codes || !packed || !aligned(packed, 256) || !aligned(codes, 4)) return MXMOE_ERR_INVALID_ARG;
+  if (kd != K_W16 && (!scales || !aligned(scales, 4))) return MXMOE_ERR_INVALID_ARG;
+  if (kind_is_wonly(kd) && (!zeros || !aligned(zeros, 4))) return MXMOE_ERR_INVALID_ARG;
+  if (packed_bytes < packed_bytes_kind(kd, L->n, L->k)) return MXMOE_ERR_WORKSPACE;
+  return hip_status(launch_pack(kd, L->n, L->k, act, w16_src, codes, scales, zeros, (uint8_t*)packed, stream));
+}
+
+mxmoe_status mxmoe_unpack_weights(const mxmoe_linear* L, mxmoe_dtype act, const void* packed, void* codes,
+                                  void* scales, void* zeros, hipStream_t stream) {
+  int kd;
+  mxmoe_status st = check_linear(L, &kd);
+  if (st != MXMOE_OK) return st;
+  if (!valid_dtype(act) || !codes || !packed || !aligned(packed, 256)) return MXMOE_ERR_INVALID_ARG;
+  if (kd != K_W16 && !scales) return MXMOE_ERR_INVALID_ARG;
+  if (kind_is_wonly(kd) && !zeros) return MXMOE_ERR_INVALID_ARG;
+  return hip_status(launch_unpack(kd, L->n, L->k, act, (const uint8_t*)packed, codes, scales, zeros, stream));
+}
+
+size_t mxmoe_route_workspace_bytes(int32_t T, int32_t k, int32_t E) {
+  if (T < 0 || k <= 0 || E <= 0) return 0;
+  const size_t P = (size_t)T * k;
+  const size_t nchunks = (P + kRouteChunk - 1) / kRouteChunk;
+  return align256(4 * nchunks * E) + align256(4 * nchunks) + 256;
+}
+
+mxmoe_status mxmoe_route_permute(const int32_t* topk_ids, int32_t T, int32_t k, int32_t E, int32_t* counts,
+                                 int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  if (T < 0 || k <= 0 || E <= 0 || k > E || E > kMaxE) return MXMOE_ERR_INVALID_ARG;
+  if ((int64_t)T * k >= (1LL << 31)) return MXMOE_ERR_INVALID_ARG;
+  if (!counts || !offsets || !status || !workspace) return MXMOE_ERR_INVALID_ARG;
+  if (T > 0 && (!topk_ids || !sorted_pair || !inv)) return MXMOE_ERR_INVALID_ARG;
+  if (!aligned(workspace, 256)) return MXMOE_ERR_INVALID_ARG;
+  if (workspace_bytes < mxmoe_route_workspace_bytes(T, k, E)) return MXMOE_ERR_WORKSPACE;
+  const size_t P = (size_t)T * k;
+  const size_t nchunks = (P + kRouteChunk - 1) / kRouteChunk;
+  int32_t* cc = reinterpret_cast<int32_t*>(workspace);
+  int32_t* cb = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) + align256(4 * nchunks * E));
+  return hip_status(launch_route(topk_ids, T, k, E, counts, offsets, sorted_pair, inv, status, cc, cb, stream));
+}
+
+mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32_t cols, int64_t ld, int32_t qmax,
+                             int8_t* codes, float* scales, hipStream_t stream) {
+  if (!valid_dtype(act) || rows < 0 || cols <= 0 || ld < cols) return MXMOE_ERR_INVALID_ARG;
+  if (qmax != 127 && qmax != 7) return MXMOE_ERR_UNSUPPORTED;
+  if (rows > 0 && (!a || !codes || !scales)) return MXMOE_ERR_INVALID_ARG;
+  return hip_status(launch_act_quant(a, act, rows, cols, ld, qmax, codes, scales, stream));
+}
+
+// -------------------------------------------------------- single linear
+namespace {
+struct LinWs { size_t plan, aq, as, total; };
+LinWs lin_layout(int kd, int m, int k) {
+  LinWs w;
+  size_t o = 0;
+  w.plan = o; o = align256(o + 4 * (size_t)plan_ints(1));
+  w.aq = w.as = kNone;
+  if (kind_is_int(kd)) {
+    w.aq = o; o = align256(o + (size_t)m * k);
+    w.as = o; o = align256(o + 4 * (size_t)m);
+  }
+  w.total = o;
+  return w;
+}
+}  // namespace
+
+size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m) {
+  int kd;
+  if (m < 0 || check_linear(L, &kd) != MXMOE_OK) return 0;
+  return lin_layout(kd, m, L->k).total;
+}
+
+mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed, int32_t m,
+                                  const void* a, void* out, void* workspace, size_t workspace_bytes,
+                                  hipStream_t stream) {
+  int kd;
+  mxmoe_status st = check_linear(L, &kd);
+  if (st != MXMOE_OK) return st;
+  if (!valid_dtype(act) || m < 0) return MXMOE_ERR_INVALID_ARG;
+  if (m == 0) return MXMOE_OK;
+  if (!packed || !a || !out || !workspace) return MXMOE_ERR_INVALID_ARG;
+  if (!aligned(packed, 256) || !aligned(a, 16) || !aligned(out, 16) || !aligned(workspace, 256))
+    return MXMOE_ERR_INVALID_ARG;
+  const LinWs w = lin_layout(kd, m, L->k);
+  if (workspace_bytes < w.total) return MXMOE_ERR_WORKSPACE;
+  DevLinear dl;
+  dl.packed = reinterpret_cast<const uint8_t*>(packed);
+  dl.wscale = kind_is_int(kd) ? reinterpret_cast<const float*>(dl.packed + codes_bytes(kd, L->n, L->k)) : nullptr;
+  dl.n = L->n;
+  dl.k = L->k;
+  dl.kind = kd;
+  dl.pad = 0;
+  GemmArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  ga.plan = at<int32_t>(workspace, w.plan);
+  ga.x = a;
+  ga.T = m;
+  ga.k = 1;
+  ga.act = act;
+  ga.G = 1;
+  ga.E_routed = 1;
+  ga.raw_lin = dl;
+  ga.raw_out = out;
+  if (kind_is_int(kd)) {
+    int8_t* aq = at<int8_t>(workspace, w.aq);
+    float* as = at<float>(workspace, w.as);
+    hipError_t e = launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
+    if (e != hipSuccess) return MXMOE_ERR_HIP;
+    if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
+  }
+  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, m, dl, nullptr, ga.plan, nullptr, stream);
+  if (e != hipSuccess) return MXMOE_ERR_HIP;
+  return hip_status(launch_group_gemm(ga, 2, group_gemm_grid(current_device()), stream));
+}
+
+// -------------------------------------------------------- MoE block
+size_t mxmoe_block_table_bytes(const mxmoe_block* B) {
+  static thread_local BlockInfo bi;
+  if (check_block(B, &bi) != MXMOE_OK) return 0;
+  return sizeof(DevExpert) * (size_t)bi.G;
+}
+
+mxmoe_status mxmoe_block_table_fill(const mxmoe_block* B, void* host_buf, size_t host_bytes) {
+  static thread_local BlockInfo bi;
+  mxmoe_status st = check_block(B, &bi);
+  if (st != MXMOE_OK) return st;
+  if (!host_buf || !B->packed) return MXMOE_ERR_INVALID_ARG;
+  if (host_bytes < sizeof(DevExpert) * (size_t)bi.G) return MXMOE_ERR_WORKSPACE;
+  DevExpert* ex = reinterpret_cast<DevExpert*>(host_buf);
+  for (int g = 0; g < bi.G; ++g) {
+    const bool sh = g >= bi.E;
+    const int F = sh ? bi.Fsh : bi.F;
+    for (int j = 0; j < 3; ++j) {
+      const void* p = B->packed[3 * g + j];
+      if (!p || !aligned(p, 256)) return MXMOE_ERR_INVALID_ARG;
+      DevLinear& d = ex[g].lin[j];
+      d.kind = bi.kinds[g][j];
+      d.n = j < 2 ? F : bi.H;
+      d.k = j < 2 ? bi.H : F;
+      d.packed = reinterpret_cast<const uint8_t*>(p);
+      d.wscale = kind_is_int(d.kind) ? reinterpret_cast<const float*>(d.packed + codes_bytes(d.kind, d.n, d.k))
+                                     : nullptr;
+      d.pad = 0;
+    }
+  }
+  return MXMOE_OK;
+}
+
+size_t mxmoe_workspace_bytes(const mxmoe_block* B, int32_t T) {
+  static thread_local BlockInfo bi;
+  if (T < 0 || check_block(B, &bi) != MXMOE_OK) return 0;
+  return layout_of(bi, T).total;
+}
+
+mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out) {
+  static thread_local BlockInfo bi;
+  if (!out || T < 0) return MXMOE_ERR_INVALID_ARG;
+  mxmoe_status st = check_block(B, &bi);
+  if (st != MXMOE_OK) return st;
+  const WsLayout L = layout_of(bi, T);
+  out->status = L.status;
+  out->counts = L.counts;
+  out->offsets = L.offsets;
+  out->sorted_pair = L.sorted_pair;
+  out->inv = L.inv;
+  out->plan = L.plan;
+  out->xq8 = L.xq8;
+  out->xs8 = L.xs8;
+  out->xq4 = L.xq4;
+  out->xs4 = L.xs4;
+  out->h = L.h;
+  out->h_shared = L.h_shared;
+  out->hq = L.hq;
+  out->hs = L.hs;
+  out->hq_shared = L.hq_shared;
+  out->hs_shared = L.hs_shared;
+  out->slots = L.slots;
+  out->total = L.total;
+  return MXMOE_OK;
+}
+
+mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table, int32_t T, const void* x,
+                                  const int32_t* topk_ids, const float* topk_w, void* y, void* workspace,
+                                  size_t workspace_bytes, const mxmoe_forward_opts* opts, hipStream_t stream) {
+  static thread_local BlockInfo bi;
+  mxmoe_status st = check_block(B, &bi);
+  if (st != MXMOE_OK) return st;
+  if (T < 0) return MXMOE_ERR_INVALID_ARG;
+  if ((int64_t)T * bi.k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
+  if (T == 0) return MXMOE_OK;
+  if (!block_table || !x || !topk_ids || !topk_w || !y || !workspace) return MXMOE_ERR_INVALID_ARG;
+  if (!aligned(block_table, 16) || !aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256) ||
+      !aligned(topk_ids, 4) || !aligned(topk_w, 4))
+    return MXMOE_ERR_INVALID_ARG;
+  const WsLayout L = layout_of(bi, T);
+  if (workspace_bytes < L.total) return MXMOE_ERR_WORKSPACE;
+
+  uint32_t mask_words[64];
+  const uint32_t* mask = nullptr;
+  if (opts && opts->expert_mask) {
+    memset(mask_words, 0, sizeof(mask_words));
+    for (int g = 0; g < bi.G; ++g)
+      if (opts->expert_mask[g]) mask_words[g >> 5] |= 1u << (g & 31);
+    mask = mask_words;
+  }
+  const DevExpert* experts = reinterpret_cast<const DevExpert*>(block_table);
+  hipError_t e;
+#define MX_CHECK(call)                       \
+  do {                                       \
+    e = (call);                              \
+    if (e != hipSuccess) return MXMOE_ERR_HIP; \
+  } while (0)
+
+  int32_t* counts = at<int32_t>(workspace, L.counts);
+  int32_t* offsets = at<int32_t>(workspace, L.offsets);
+  int32_t* sorted_pair = at<int32_t>(workspace, L.sorted_pair);
+  int32_t* plan = at<int32_t>(workspace, L.plan);
+  int32_t* down_qmax = at<int32_t>(workspace, L.down_qmax);
+  MX_CHECK(launch_route(topk_ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
+                        at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
+                        at<int32_t>(workspace, L.chunk_bad), stream));
+  DevLinear none;
+  memset(&none, 0, sizeof(none));
+  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, -1, none, mask, plan, down_qmax, stream));
+  if (bi.any_x8)
+    MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
+                              stream));
+  if (bi.any_x4)
+    MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4), at<float>(workspace, L.xs4),
+                              stream));
+  GemmArgs ga;
+  memset(&ga, 0, sizeof(ga));
+  ga.experts = experts;
+  ga.plan = plan;
+  ga.sorted_pair = sorted_pair;
+  ga.offsets = offsets;
+  ga.topk_w = topk_w;
+  ga.x = x;
+  ga.xq8 = at<int8_t>(workspace, L.xq8);
+  ga.xs8 = at<float>(workspace, L.xs8);
+  ga.xq4 = at<int8_t>(workspace, L.xq4);
+  ga.xs4 = at<float>(workspace, L.xs4);
+  ga.h = at<void>(workspace, L.h);
+  ga.h_shared = at<void>(workspace, L.h_shared);
+  ga.hq = at<int8_t>(workspace, L.hq);
+  ga.hs = at<float>(workspace, L.hs);
+  ga.hq_shared = at<int8_t>(workspace, L.hq_shared);
+  ga.hs_shared = at<float>(workspace, L.hs_shared);
+  ga.slots = at<float>(workspace, L.slots);
+  ga.down_qmax = down_qmax;
+  ga.T = T;
+  ga.k = bi.k;
+  ga.act = bi.act;
+  ga.G = bi.G;
+  ga.E_routed = bi.E;
+  ga.n_shared = bi.nsh;
+  const int grid = group_gemm_grid(current_device());
+  MX_CHECK(launch_group_gemm(ga, 0, grid, stream));
+  if (bi.any_hq)
+    MX_CHECK(launch_hquant_routed(ga.h, bi.act, T * bi.k, bi.F, offsets, bi.E, down_qmax, at<int8_t>(workspace, L.hq),
+                                  at<float>(workspace, L.hs), stream));
+  for (int j = 0; j < bi.nsh; ++j) {
+    const int qm = kind_qmax(bi.kinds[bi.E + j][2]);
+    if (!qm) continue;
+    const size_t rows = (size_t)j * T;
+    MX_CHECK(launch_act_quant(reinterpret_cast<const uint8_t*>(ga.h_shared) + rows * bi.Fsh * 2, bi.act, T, bi.Fsh,
+                              bi.Fsh, qm, at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh,
+                              at<float>(workspace, L.hs_shared) + rows, stream));
+  }
+  MX_CHECK(launch_group_gemm(ga, 1, grid, stream));
+  if (!(opts && opts->skip_combine))
+    MX_CHECK(launch_combine(ga.slots, topk_ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
+#undef MX_CHECK
+  return MXMOE_OK;
+}
+
+mxmoe_status mxmoe_moe_forward(const mxmoe_block* B, const void* block_table, int32_t T, const void* x,
+                               const int32_t* topk_ids, const float* topk_w, void* y, void* workspace,
+                               size_t workspace_bytes, hipStream_t stream) {
+  return mxmoe_moe_forward_ex(B, block_table, T, x, topk_ids, topk_w, y, workspace, workspace_bytes, nullptr, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,169 @@
+// Internal declarations shared by the HIP translation units of libmxmoe.
+// Device layouts of the block table, the tile plan and the packed weights.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <type_traits>
+
+#include "../../include/mxmoe.h"
+
+namespace mxmoe {
+
+// ---------------------------------------------------------------- schemes
+// Kind ids of the micro-kernels (one per supported scheme).
+enum Kind : int32_t {
+  K_W16 = 0,   // 16-bit weights, 16-bit MFMA
+  K_W8A8 = 1,  // int8 x int8 MFMA, per-channel / per-token scales
+  K_W4A4 = 2,  // int4 codes widened to int8 (x16) on the fly, int8 MFMA
+  K_W2G = 3,   // weight-only 2-bit, group 128
+  K_W3G = 4,   // weight-only 3-bit (2+1 bit planes), group 128
+  K_W4G = 5,   // weight-only 4-bit, group 128
+  K_W8G = 6,   // weight-only 8-bit, group 128
+  K_COUNT = 7
+};
+
+__host__ __device__ constexpr inline bool kind_is_int(int kd) { return kd == K_W8A8 || kd == K_W4A4; }
+__host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G; }
+__host__ __device__ constexpr inline int kind_wbits(int kd) {
+  switch (kd) {
+    case K_W16: return 16;
+    case K_W8A8: return 8;
+    case K_W4A4: return 4;
+    case K_W2G: return 2;
+    case K_W3G: return 3;
+    case K_W4G: return 4;
+    default: return 8;
+  }
+}
+// activation qmax of an integer scheme (0 for 16-bit activations)
+__host__ __device__ constexpr inline int kind_qmax(int kd) {
+  return kd == K_W8A8 ? 127 : (kd == K_W4A4 ? 7 : 0);
+}
+
+// Packed layout: the weight matrix [n, k] is cut into fragment blocks of
+// 16 output rows x 128 reduction columns, stored n-block major, k-block minor.
+// A block holds 64 lanes x lane_bytes(kind) bytes in MFMA lane order (lane l
+// owns output row l%16 and reduction quarter l/16); weight-only blocks are
+// followed by 16 (scale, zero) fp16 pairs, one per output row of the block.
+// Per-channel fp32 scales of w8a8/w4a4 follow the last block.
+__host__ __device__ constexpr inline int lane_bytes(int kd) {
+  switch (kd) {
+    case K_W16: return 64;
+    case K_W8A8: return 32;
+    case K_W4A4: return 16;
+    case K_W2G: return 8;
+    case K_W3G: return 12;
+    case K_W4G: return 16;
+    default: return 32;  // K_W8G
+  }
+}
+__host__ __device__ constexpr inline int block_bytes(int kd) {
+  return 64 * lane_bytes(kd) + (kind_is_wonly(kd) ? 64 : 0);
+}
+__host__ __device__ inline int64_t codes_bytes(int kd, int n, int k) {
+  return (int64_t)(n / 16) * (k / 128) * block_bytes(kd);
+}
+
+// ------------------------------------------------------------ block table
+struct DevLinear {
+  const uint8_t* packed;  // fragment blocks
+  const float* wscale;    // per-channel scales (w8a8/w4a4) or nullptr
+  int32_t n, k;
+  int32_t kind;
+  int32_t pad;
+};
+static_assert(sizeof(DevLinear) == 32, "DevLinear layout");
+
+struct DevExpert {
+  DevLinear lin[3];  // gate, up, down
+};
+
+struct DevHeader {
+  int32_t hidden, ffn, E, topk, n_shared, ffn_shared, act, G;  // G = E + n_shared
+};
+
+// ------------------------------------------------------------- tile plan
+// Tile configurations of the persistent Group-GEMM.  All use 256 threads
+// (4 wavefronts); the wavefront grid is WM x WN and a wavefront computes
+// MB x NB fragments of 16 x 16 outputs (per linear).
+enum Cfg : int32_t { CFG_S = 0, CFG_M = 1, CFG_L = 2, CFG_COUNT = 3 };
+
+// Plan record per (phase, expert): int32 fields.
+enum PlanField : int32_t {
+  PF_EXPERT = 0, PF_M = 1, PF_CFG = 2, PF_MTILES = 3, PF_NTILES = 4,
+  PF_START = 5, PF_COST = 6, PF_RANK = 7, PF_N = 8
+};
+
+// Plan region layout (int32): [2][G][PF_N] records, [2][G] queue order
+// (group index per rank), [16] counters.
+__host__ __device__ inline int64_t plan_ints(int G) { return 2LL * G * PF_N + 2LL * G + 16; }
+enum PlanCounter : int32_t { PC_HEAD0 = 0, PC_HEAD1 = 1, PC_TOTAL0 = 2, PC_TOTAL1 = 3 };
+
+// Workspace layout (byte offsets), shared by host code of the forward.
+struct WsLayout {
+  size_t status, counts, offsets, sorted_pair, inv, chunk_counts, chunk_bad, plan, down_qmax;
+  size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
+};
+
+constexpr int kRouteChunk = 2048;  // pairs per routing workgroup
+constexpr size_t kNone = (size_t)-1;
+
+// ----------------------------------------------------------- launchers
+// (defined in the .hip files; all return hipError_t of the launch)
+hipError_t launch_pack(int kind, int n, int k, int act, int w16_src, const void* codes,
+                       const void* scales, const void* zeros, uint8_t* packed, hipStream_t s);
+hipError_t launch_unpack(int kind, int n, int k, int act, const uint8_t* packed, void* codes,
+                         void* scales, void* zeros, hipStream_t s);
+
+hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts,
+                        int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
+                        int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
+
+hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax,
+                            int8_t* codes, float* scales, hipStream_t s);
+
+// Quantize routed h rows whose expert's down projection is a8/a4 (qmax from
+// down_qmax[expert]); rows of other experts are skipped.
+hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets,
+                                int E, const int32_t* down_qmax, int8_t* hq, float* hs,
+                                hipStream_t s);
+
+struct GemmArgs {
+  const DevExpert* experts;  // device [G]
+  int32_t* plan;             // device plan region
+  const int32_t* sorted_pair;
+  const int32_t* offsets;
+  const float* topk_w;
+  const void* x;             // [T,H] act
+  const int8_t* xq8; const float* xs8;
+  const int8_t* xq4; const float* xs4;
+  void* h; void* h_shared;
+  const int8_t* hq; const float* hs;
+  const int8_t* hq_shared; const float* hs_shared;
+  float* slots;
+  const int32_t* down_qmax;
+  int32_t T, k;
+  int32_t act;
+  int32_t G;          // experts incl. shared
+  int32_t E_routed;
+  int32_t n_shared;
+  // single-linear mode (mxmoe_linear_forward): raw int32 / fp32 output
+  DevLinear raw_lin;
+  void* raw_out;
+};
+
+// raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of
+// both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
+hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
+                       int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
+                       int32_t* plan, int32_t* down_qmax, hipStream_t s);
+hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
+int group_gemm_grid(int device);
+
+hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int n_sh,
+                          int H, int act, void* y, hipStream_t s);
+
+}  // namespace mxmoe

@@ -1,0 +1,161 @@
+// Routing / permutation: stable counting sort of the T*k (token, slot) pairs
+// by expert id, which forms the per-expert row groups X_e of Eq. (2).
+//
+// Three launches, no atomics on anything order-dependent:
+//   1. route_count   : one workgroup per chunk of kRouteChunk pairs builds the
+//                      chunk's expert histogram (integer LDS atomics: the
+//                      counts do not depend on their order) and the smallest
+//                      out-of-range pair id of the chunk.
+//   2. route_scan    : one workgroup scans chunk histograms in (expert, chunk)
+//                      order -> counts, offsets and each chunk's base per expert.
+//   3. route_scatter : each chunk walks its pairs in order, 256 at a time; a
+//                      wavefront finds lanes with equal expert ids with one
+//                      ballot per id bit, ranks them by lane, and wavefront
+//                      totals are combined through LDS in wavefront order.
+#include "mxmoe_internal.h"
+
+namespace mxmoe {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxE = 1024;
+
+__global__ void __launch_bounds__(kThreads) route_count(const int32_t* __restrict__ ids, int P, int E,
+                                                         int32_t* __restrict__ chunk_counts,
+                                                         int32_t* __restrict__ chunk_bad) {
+  __shared__ int32_t hist[kMaxE];
+  __shared__ int32_t bad;
+  const int c = blockIdx.x;
+  for (int e = threadIdx.x; e < E; e += kThreads) hist[e] = 0;
+  if (threadIdx.x == 0) bad = 0x7fffffff;
+  __syncthreads();
+  const int p0 = c * kRouteChunk;
+  const int p1 = min(P, p0 + kRouteChunk);
+  for (int p = p0 + threadIdx.x; p < p1; p += kThreads) {
+    int e = ids[p];
+    if (e >= 0 && e < E) atomicAdd(&hist[e], 1);
+    else atomicMin(&bad, p);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += kThreads) chunk_counts[(int64_t)c * E + e] = hist[e];
+  if (threadIdx.x == 0) chunk_bad[c] = bad;
+}
+
+__global__ void __launch_bounds__(1024) route_scan(int nchunks, int E, int32_t* __restrict__ chunk_counts,
+                                                   const int32_t* __restrict__ chunk_bad,
+                                                   int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                                                   int32_t* __restrict__ status) {
+  __shared__ int32_t tot[kMaxE];
+  __shared__ int32_t wsum[16];
+  const int tid = threadIdx.x;  // blockDim = 1024 >= E
+  int mine = 0;
+  if (tid < E)
+    for (int c = 0; c < nchunks; ++c) mine += chunk_counts[(int64_t)c * E + tid];
+  // exclusive scan of per-expert totals across the workgroup
+  const int lane = tid & 63, w = tid >> 6;
+  int incl = mine;
+  for (int d = 1; d < 64; d <<= 1) {
+    int v = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += v;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int base = 0;
+  for (int i = 0; i < w; ++i) base += wsum[i];
+  const int excl = base + incl - mine;
+  if (tid < E) {
+    counts[tid] = mine;
+    offsets[tid] = excl;
+    tot[tid] = excl;
+    // chunk bases, in place: chunk_counts[c][e] <- offset of chunk c's first pair of e
+    int run = excl;
+    for (int c = 0; c < nchunks; ++c) {
+      int64_t i = (int64_t)c * E + tid;
+      int v = chunk_counts[i];
+      chunk_counts[i] = run;
+      run += v;
+    }
+  }
+  if (tid == E - 1) offsets[E] = excl + mine;
+  if (tid == 0) {
+    int b = 0x7fffffff;
+    for (int c = 0; c < nchunks; ++c) b = min(b, chunk_bad[c]);
+    status[0] = b == 0x7fffffff ? 0 : b + 1;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restrict__ ids, int P, int E, int ebits,
+                                                          const int32_t* __restrict__ chunk_base,
+                                                          int32_t* __restrict__ sorted_pair,
+                                                          int32_t* __restrict__ inv) {
+  __shared__ int32_t base[kMaxE];
+  __shared__ int32_t wcnt[kThreads / 64][kMaxE];
+  const int c = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int e = tid; e < E; e += kThreads) base[e] = chunk_base[(int64_t)c * E + e];
+  const int p0 = c * kRouteChunk;
+  const int p1 = min(P, p0 + kRouteChunk);
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  for (int s = p0; s < p1; s += kThreads) {
+    for (int e = tid; e < E; e += kThreads)
+      for (int i = 0; i < kThreads / 64; ++i) wcnt[i][e] = 0;
+    __syncthreads();
+    const int p = s + tid;
+    int e = -1;
+    if (p < p1) {
+      e = ids[p];
+      if (e < 0 || e >= E) e = -1;
+    }
+    // lanes holding the same valid expert id
+    uint64_t same = __ballot(e >= 0);
+    for (int b = 0; b < ebits; ++b) {
+      const bool bit = e >= 0 && ((e >> b) & 1);
+      const uint64_t m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    if (e < 0) same = 0;
+    const int rank = __popcll(same & below);
+    if (e >= 0 && rank == 0) wcnt[w][e] = __popcll(same);
+    __syncthreads();
+    if (e >= 0) {
+      int pos = base[e] + rank;
+      for (int i = 0; i < w; ++i) pos += wcnt[i][e];
+      sorted_pair[pos] = p;
+      inv[p] = pos;
+    } else if (p < p1) {
+      inv[p] = -1;
+    }
+    __syncthreads();
+    for (int ee = tid; ee < E; ee += kThreads) {
+      int add = 0;
+      for (int i = 0; i < kThreads / 64; ++i) add += wcnt[i][ee];
+      base[ee] += add;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts, int32_t* offsets,
+                        int32_t* sorted_pair, int32_t* inv, int32_t* status, int32_t* chunk_counts,
+                        int32_t* chunk_bad, hipStream_t s) {
+  const int P = T * k;
+  const int nchunks = (P + kRouteChunk - 1) / kRouteChunk;
+  int ebits = 0;
+  while ((1 << ebits) < E) ++ebits;
+  if (nchunks > 0) {
+    hipLaunchKernelGGL(route_count, dim3(nchunks), dim3(kThreads), 0, s, ids, P, E, chunk_counts, chunk_bad);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  hipLaunchKernelGGL(route_scan, dim3(1), dim3(1024), 0, s, nchunks, E, chunk_counts, chunk_bad, counts,
+                     offsets, status);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || nchunks == 0) return err;
+  hipLaunchKernelGGL(route_scatter, dim3(nchunks), dim3(kThreads), 0, s, ids, P, E, ebits, chunk_counts,
+                     sorted_pair, inv);
+  return hipGetLastError();
+}
+
+}  // namespace mxmoe

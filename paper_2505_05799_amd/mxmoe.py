@@ -1,0 +1,334 @@
+"""ctypes binding of libmxmoe.so (C ABI in include/mxmoe.h).
+
+Argument marshalling only: every step of the forward runs in the library's HIP
+kernels.  PyTorch provides device memory and the current stream.  There is no
+fallback: if the library is missing or a call fails, an exception is raised.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmxmoe.so")
+
+F16, BF16 = 0, 1
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
+
+
+class Scheme_t(C.Structure):
+    _fields_ = [("w_bits", C.c_int32), ("a_bits", C.c_int32), ("w_group", C.c_int32),
+                ("a_group", C.c_int32), ("symmetric", C.c_int32)]
+
+
+class Linear_t(C.Structure):
+    _fields_ = [("n", C.c_int32), ("k", C.c_int32), ("s", Scheme_t)]
+
+
+class Block_t(C.Structure):
+    _fields_ = [("hidden", C.c_int32), ("ffn", C.c_int32), ("n_experts", C.c_int32),
+                ("top_k", C.c_int32), ("n_shared", C.c_int32), ("ffn_shared", C.c_int32),
+                ("act", C.c_int), ("scheme", C.POINTER(Scheme_t)), ("packed", C.POINTER(C.c_void_p))]
+
+
+class ForwardOpts_t(C.Structure):
+    _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("split_phases", C.c_int32),
+                ("skip_combine", C.c_int32), ("reserved", C.c_int32 * 4)]
+
+
+WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
+             "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total"]
+
+
+class WsLayout_t(C.Structure):
+    _fields_ = [(f, C.c_size_t) for f in WS_FIELDS]
+
+
+EXPORTS = [
+    "mxmoe_packed_bytes", "mxmoe_pack_weights", "mxmoe_unpack_weights", "mxmoe_route_workspace_bytes",
+    "mxmoe_route_permute", "mxmoe_act_quant", "mxmoe_linear_workspace_bytes", "mxmoe_linear_forward",
+    "mxmoe_block_table_bytes", "mxmoe_block_table_fill", "mxmoe_workspace_bytes", "mxmoe_moe_forward",
+    "mxmoe_moe_forward_ex", "mxmoe_workspace_layout", "mxmoe_status_string", "mxmoe_version",
+]
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> C.CDLL:
+    """Load libmxmoe.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2505_05799_amd.build`")
+    lib = C.CDLL(path)
+    vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    PL, PB = C.POINTER(Linear_t), C.POINTER(Block_t)
+    sig = {
+        "mxmoe_packed_bytes": (sz, [PL, C.c_int]),
+        "mxmoe_pack_weights": (C.c_int, [PL, C.c_int, C.c_int, vp, vp, vp, vp, sz, vp]),
+        "mxmoe_unpack_weights": (C.c_int, [PL, C.c_int, vp, vp, vp, vp, vp]),
+        "mxmoe_route_workspace_bytes": (sz, [i32, i32, i32]),
+        "mxmoe_route_permute": (C.c_int, [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "mxmoe_act_quant": (C.c_int, [vp, C.c_int, i32, i32, i64, i32, vp, vp, vp]),
+        "mxmoe_linear_workspace_bytes": (sz, [PL, i32]),
+        "mxmoe_linear_forward": (C.c_int, [PL, C.c_int, vp, i32, vp, vp, vp, sz, vp]),
+        "mxmoe_block_table_bytes": (sz, [PB]),
+        "mxmoe_block_table_fill": (C.c_int, [PB, vp, sz]),
+        "mxmoe_workspace_bytes": (sz, [PB, i32]),
+        "mxmoe_moe_forward": (C.c_int, [PB, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
+        "mxmoe_moe_forward_ex": (C.c_int, [PB, vp, i32, vp, vp, vp, vp, vp, sz,
+                                           C.POINTER(ForwardOpts_t), vp]),
+        "mxmoe_workspace_layout": (C.c_int, [PB, i32, C.POINTER(WsLayout_t)]),
+        "mxmoe_status_string": (C.c_char_p, [C.c_int]),
+        "mxmoe_version": (i32, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+class MxmoeError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        lib = load_library()
+        super().__init__(f"{what}: {lib.mxmoe_status_string(status).decode()} (status {status})")
+        self.status = status
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise MxmoeError(status, what)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t) -> C.c_void_p:
+    return C.c_void_p(0 if t is None else t.data_ptr())
+
+
+def scheme_t(s) -> Scheme_t:
+    return Scheme_t(s.w_bits, s.a_bits, s.w_group, s.a_group, s.symmetric)
+
+
+def act_code(act: str) -> int:
+    return {"fp16": F16, "bf16": BF16}[act]
+
+
+def _dev(arr: np.ndarray, device):
+    """numpy -> device tensor with the same bytes (16-bit data travels as int16)."""
+    torch = _torch()
+    a = np.ascontiguousarray(arr)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    if a.dtype == np.float16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a.copy()).to(device)
+
+
+def act_tensor(x: np.ndarray, act: str, device="cuda"):
+    """numpy activation storage (float16 or bf16 bits) -> torch tensor of the act dtype."""
+    torch = _torch()
+    t = _dev(x, device)
+    return t.view(torch.float16 if act == "fp16" else torch.bfloat16)
+
+
+def act_numpy(t, act: str) -> np.ndarray:
+    """torch act tensor -> numpy storage (float16 array or bf16 bits)."""
+    torch = _torch()
+    a = t.detach().contiguous().view(torch.int16).cpu().numpy()
+    return a.view(np.float16) if act == "fp16" else a.view(np.uint16)
+
+
+def empty_aligned(nbytes: int, device="cuda"):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# --------------------------------------------------------------- packing
+class PackedLinear:
+    """One linear packed on the device (owns the packed buffer)."""
+
+    def __init__(self, q, act: str, device="cuda", stream=None):
+        lib = load_library()
+        self.q = q
+        self.act = act
+        self.L = Linear_t(q.n, q.k, scheme_t(q.scheme))
+        nbytes = lib.mxmoe_packed_bytes(C.byref(self.L), act_code(act))
+        if nbytes == 0:
+            raise MxmoeError(ERR_UNSUPPORTED, f"packed_bytes({q.scheme.name} {q.n}x{q.k})")
+        self.nbytes = nbytes
+        self.buf = empty_aligned(nbytes, device)
+        codes = _dev(q.codes, device)
+        scales = _dev(q.scales, device) if q.scales is not None else None
+        zeros = _dev(q.zeros, device) if q.zeros is not None else None
+        _check(lib.mxmoe_pack_weights(C.byref(self.L), act_code(act), BF16, _ptr(codes), _ptr(scales),
+                                      _ptr(zeros), _ptr(self.buf), nbytes, _stream_ptr(stream)),
+               "mxmoe_pack_weights")
+        self._keep = (codes, scales, zeros)   # alive until the pack kernel has run
+
+    def release_sources(self):
+        self._keep = None
+
+    def unpack(self, stream=None):
+        """Device unpack -> (codes, scales, zeros) as numpy arrays."""
+        torch = _torch()
+        lib = load_library()
+        q = self.q
+        s = q.scheme
+        if s.w_bits == 16:
+            codes = torch.empty((q.n, q.k), dtype=torch.int16, device=self.buf.device)
+        else:
+            codes = torch.empty((q.n, q.k), dtype=torch.uint8, device=self.buf.device)
+        scales = zeros = None
+        if s.w_bits < 16 and s.a_bits == 16:
+            scales = torch.empty((q.n, q.k // 128), dtype=torch.int16, device=self.buf.device)
+            zeros = torch.empty_like(scales)
+        elif s.w_bits < 16:
+            scales = torch.empty(q.n, dtype=torch.float32, device=self.buf.device)
+        _check(lib.mxmoe_unpack_weights(C.byref(self.L), act_code(self.act), _ptr(self.buf), _ptr(codes),
+                                        _ptr(scales), _ptr(zeros), _stream_ptr(stream)),
+               "mxmoe_unpack_weights")
+        torch.cuda.synchronize()
+        c = codes.cpu().numpy()
+        if s.w_bits == 16:
+            c = c.view(np.uint16)
+        elif s.a_bits < 16:
+            c = c.view(np.int8)
+        sc = None if scales is None else scales.cpu().numpy()
+        if sc is not None and s.a_bits == 16:
+            sc = sc.view(np.float16)
+        z = None if zeros is None else zeros.cpu().numpy().view(np.float16)
+        return c, sc, z
+
+
+def linear_forward(pl: PackedLinear, a, stream=None):
+    """out = a W^T through the micro-kernels: int32 for w8a8/w4a4, else fp32."""
+    torch = _torch()
+    lib = load_library()
+    m = a.shape[0]
+    s = pl.q.scheme
+    out = torch.empty((m, pl.q.n), dtype=torch.int32 if s.a_bits < 16 else torch.float32, device=a.device)
+    wsb = lib.mxmoe_linear_workspace_bytes(C.byref(pl.L), m)
+    ws = empty_aligned(wsb, a.device)
+    _check(lib.mxmoe_linear_forward(C.byref(pl.L), act_code(pl.act), _ptr(pl.buf), m, _ptr(a.contiguous()),
+                                    _ptr(out), _ptr(ws), wsb, _stream_ptr(stream)), "mxmoe_linear_forward")
+    return out
+
+
+# --------------------------------------------------------------- routing
+def route_permute(topk_ids, E: int, stream=None):
+    torch = _torch()
+    lib = load_library()
+    T, k = topk_ids.shape
+    dev = topk_ids.device
+    counts = torch.empty(E, dtype=torch.int32, device=dev)
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    sp = torch.full((max(T * k, 1),), -7, dtype=torch.int32, device=dev)
+    inv = torch.empty(max(T * k, 1), dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    wsb = lib.mxmoe_route_workspace_bytes(T, k, E)
+    ws = empty_aligned(wsb, dev)
+    _check(lib.mxmoe_route_permute(_ptr(topk_ids.contiguous()), T, k, E, _ptr(counts), _ptr(offsets), _ptr(sp),
+                                   _ptr(inv), _ptr(status), _ptr(ws), wsb, _stream_ptr(stream)),
+           "mxmoe_route_permute")
+    return {"counts": counts, "offsets": offsets, "sorted_pair": sp[: T * k], "inv": inv[: T * k],
+            "status": status}
+
+
+def act_quant(a, act: str, qmax: int, stream=None):
+    torch = _torch()
+    lib = load_library()
+    rows, cols = a.shape
+    codes = torch.empty((rows, cols), dtype=torch.int8, device=a.device)
+    scales = torch.empty(rows, dtype=torch.float32, device=a.device)
+    _check(lib.mxmoe_act_quant(_ptr(a), act_code(act), rows, cols, a.stride(0), qmax, _ptr(codes), _ptr(scales),
+                               _stream_ptr(stream)), "mxmoe_act_quant")
+    return codes, scales
+
+
+# --------------------------------------------------------------- block
+class MoEBlock:
+    """A packed MoE block on one GPU: weights, block table and workspace."""
+
+    def __init__(self, block, device="cuda", T_max: Optional[int] = None, stream=None):
+        torch = _torch()
+        lib = load_library()
+        cfg = block.cfg
+        self.cfg = cfg
+        self.act = cfg.act
+        self.device = device
+        self.packed: List[List[PackedLinear]] = []
+        for e, lins in enumerate(block.linears):
+            self.packed.append([PackedLinear(q, cfg.act, device, stream) for q in lins])
+        G = cfg.E + cfg.n_shared
+        self._schemes = (Scheme_t * (3 * G))(*[scheme_t(q.scheme) for lins in block.linears for q in lins])
+        self._ptrs = (C.c_void_p * (3 * G))(*[p.buf.data_ptr() for ps in self.packed for p in ps])
+        self.B = Block_t(cfg.H, cfg.F, cfg.E, cfg.k, cfg.n_shared, cfg.F_shared if cfg.n_shared else 0,
+                         act_code(cfg.act), C.cast(self._schemes, C.POINTER(Scheme_t)),
+                         C.cast(self._ptrs, C.POINTER(C.c_void_p)))
+        tb = lib.mxmoe_block_table_bytes(C.byref(self.B))
+        if tb == 0:
+            raise MxmoeError(ERR_UNSUPPORTED, "mxmoe_block_table_bytes")
+        host = (C.c_uint8 * tb)()
+        _check(lib.mxmoe_block_table_fill(C.byref(self.B), host, tb), "mxmoe_block_table_fill")
+        self.table = torch.frombuffer(bytearray(host), dtype=torch.uint8).to(device)
+        self.T_max = T_max or cfg.T
+        self.ws_bytes = lib.mxmoe_workspace_bytes(C.byref(self.B), self.T_max)
+        self.ws = empty_aligned(self.ws_bytes, device)
+        torch.cuda.synchronize()
+        for ps in self.packed:
+            for p in ps:
+                p.release_sources()
+
+    def workspace_layout(self, T: int) -> dict:
+        lay = WsLayout_t()
+        _check(load_library().mxmoe_workspace_layout(C.byref(self.B), T, C.byref(lay)), "mxmoe_workspace_layout")
+        return {f: getattr(lay, f) for f in WS_FIELDS}
+
+    def forward(self, x, topk_ids, topk_w, y=None, expert_mask: Optional[Sequence[int]] = None,
+                skip_combine: bool = False, stream=None):
+        torch = _torch()
+        lib = load_library()
+        T = x.shape[0]
+        if T > self.T_max:
+            raise ValueError(f"T={T} exceeds the workspace sized for {self.T_max} tokens")
+        if y is None:
+            y = torch.empty_like(x)
+        opts = None
+        if expert_mask is not None or skip_combine:
+            o = ForwardOpts_t()
+            if expert_mask is not None:
+                self._mask = (C.c_uint8 * len(expert_mask))(*[1 if v else 0 for v in expert_mask])
+                o.expert_mask = C.cast(self._mask, C.POINTER(C.c_uint8))
+            o.skip_combine = 1 if skip_combine else 0
+            opts = C.byref(o)
+        st = lib.mxmoe_moe_forward_ex(C.byref(self.B), _ptr(self.table), T, _ptr(x), _ptr(topk_ids), _ptr(topk_w),
+                                      _ptr(y), _ptr(self.ws), self.ws_bytes, opts, _stream_ptr(stream))
+        _check(st, "mxmoe_moe_forward")
+        return y
+
+    def ws_view(self, field: str, dtype, count: int, T: int):
+        """Typed view of an intermediate buffer inside the workspace (after a forward)."""
+        off = self.workspace_layout(T)[field]
+        if off == (1 << 64) - 1:
+            return None
+        torch = _torch()
+        nbytes = count * torch.empty((), dtype=dtype).element_size()
+        return self.ws[off: off + nbytes].view(dtype)

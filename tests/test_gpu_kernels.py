@@ -1,0 +1,148 @@
+"""GPU parity of the individual steps against the CPU oracle: weight packing
+(round trip), routing / permutation (bit-exact), per-token activation
+quantization (bit-exact) and every micro-kernel as a single linear (exact
+int32 accumulators for w8a8 / w4a4, fp32 within an accumulation bound else)."""
+
+import numpy as np
+import pytest
+
+from oracle import mxmoe_oracle as O
+from paper_2505_05799_amd import mxmoe as M
+from paper_2505_05799_amd import workloads as W
+from tests.gpuhelp import say, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+# ---------------------------------------------------------------- packing
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+@pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
+def test_pack_roundtrip(scheme, act):
+    torch_mod()
+    w = W.draw_weight(5, 0, 0, 48, 384)
+    w[0, :4] = [3.0e-6, -1.0e-7, 60000.0, -0.0]        # fp16 subnormal / rounding corner cases
+    q = W.quantize_linear(w, scheme)
+    pl = M.PackedLinear(q, act)
+    c, s, z = pl.unpack()
+    if scheme.w_bits == 16:
+        want = q.codes if act == "bf16" else \
+            O.bf16_bits_to_f64(q.codes).astype(np.float16).view(np.uint16)
+        assert np.array_equal(c, want)
+    else:
+        assert np.array_equal(c.astype(np.int64), q.codes.astype(np.int64))
+        assert np.array_equal(s.view(np.uint8), q.scales.view(np.uint8))
+        if z is not None:
+            assert np.array_equal(z.view(np.uint8), q.zeros.view(np.uint8))
+
+
+# ---------------------------------------------------------------- routing
+ROUTE_CASES = [(1, 1, 1, "uniform"), (64, 2, 4, "uniform"), (257, 6, 64, "uniform"),
+               (2049, 8, 64, "uniform"), (1000, 4, 60, "skew"), (300, 2, 8, "one"),
+               (0, 2, 4, "uniform"), (513, 3, 7, "bad"), (5000, 2, 1024, "uniform"),
+               (16384, 8, 64, "zipf")]
+
+
+def _ids(T, k, E, kind, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "one":
+        ids = np.stack([np.r_[3, rng.permutation([e for e in range(E) if e != 3])[: k - 1]] for _ in range(T)])
+    elif kind in ("skew", "zipf"):
+        bias = -1.5 * np.log(np.arange(1, E + 1))
+        logits = rng.standard_normal((T, E)) + bias
+        ids = np.argsort(-logits, axis=1, kind="stable")[:, :k]
+    else:
+        ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]) if T else np.zeros((0, k))
+    ids = ids.astype(np.int32).reshape(T, k)
+    if kind == "bad":
+        ids[5, 1] = E + 3
+        ids[400, 0] = -2
+    return ids
+
+
+@pytest.mark.parametrize("T,k,E,kind", ROUTE_CASES)
+def test_route_permute(T, k, E, kind):
+    torch = torch_mod()
+    ids = _ids(T, k, E, kind, T * 31 + E)
+    r = O.route(ids, E)
+    g = M.route_permute(torch.from_numpy(ids).cuda(), E)
+    torch.cuda.synchronize()
+    assert np.array_equal(g["counts"].cpu().numpy(), r["counts"])
+    assert np.array_equal(g["offsets"].cpu().numpy(), r["offsets"])
+    nv = int(r["offsets"][-1])
+    assert np.array_equal(g["sorted_pair"].cpu().numpy()[:nv], r["sorted_pair"])
+    assert np.array_equal(g["inv"].cpu().numpy(), r["inv"])
+    bad = np.nonzero(r["bad"])[0]
+    assert int(g["status"].cpu().item()) == (int(bad[0]) + 1 if bad.size else 0)
+
+
+# ------------------------------------------------------- activation quant
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+@pytest.mark.parametrize("qmax", [127, 7])
+@pytest.mark.parametrize("rows,cols", [(1, 128), (37, 2048), (300, 3584)])
+def test_act_quant_bit_exact(act, qmax, rows, cols):
+    torch = torch_mod()
+    rng = np.random.default_rng(rows + cols + qmax)
+    x64 = rng.standard_normal((rows, cols)) * np.exp(rng.uniform(-3, 3, size=(rows, 1)))
+    x = W.f64_to_act(x64, act)
+    if rows > 2:
+        x[1] = 0                                       # zero row
+        x[2, 5] = x[2, 0]                             # ties in amax
+    a = M.act_tensor(x, act)
+    codes, scales = M.act_quant(a, act, qmax)
+    torch.cuda.synchronize()
+    rc, rs = O.act_quant(O.act_values(x, act).astype(np.float32), qmax)
+    assert np.array_equal(codes.cpu().numpy(), rc)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+
+
+# ------------------------------------------------------------- one linear
+LIN_SHAPES = [(48, 384), (272, 256)]
+LIN_M = [1, 5, 16, 17, 64, 65, 130, 300]
+
+
+def _linear_case(scheme, act, m, n, k, seed):
+    torch = torch_mod()
+    q = W.quantize_linear(W.draw_weight(seed, 1, 0, n, k), scheme)
+    x = W.f64_to_act(np.random.default_rng(seed).standard_normal((m, k)), act)
+    pl = M.PackedLinear(q, act)
+    out = M.linear_forward(pl, M.act_tensor(x, act))
+    torch.cuda.synchronize()
+    a = O.act_values(x, act)
+    return q, a, out.cpu().numpy()
+
+
+@pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
+@pytest.mark.parametrize("m", LIN_M)
+@pytest.mark.parametrize("n,k", LIN_SHAPES)
+def test_linear_bf16(scheme, m, n, k):
+    q, a, got = _linear_case(scheme, "bf16", m, n, k, m * 7 + n)
+    if scheme.a_bits < 16:
+        want = O.linear(a, q, "bf16", return_int=True)
+        assert np.array_equal(got.astype(np.int64), want)
+    else:
+        want = O.linear(a, q, "bf16")
+        bound = 2.0 ** -16 * (np.abs(a) @ np.abs(O.dequant(q, "bf16")).T) + 1e-30
+        assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
+
+
+@pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
+@pytest.mark.parametrize("m", [3, 33, 129])
+def test_linear_fp16(scheme, m):
+    q, a, got = _linear_case(scheme, "fp16", m, 48, 256, m + 11)
+    if scheme.a_bits < 16:
+        assert np.array_equal(got.astype(np.int64), O.linear(a, q, "fp16", return_int=True))
+    else:
+        want = O.linear(a, q, "fp16")
+        bound = 2.0 ** -16 * (np.abs(a) @ np.abs(O.dequant(q, "fp16")).T) + 1e-30
+        assert np.all(np.abs(got - want) <= bound)
+
+
+def test_linear_deterministic():
+    torch = torch_mod()
+    q = W.quantize_linear(W.draw_weight(9, 0, 0, 256, 512), W.W4G128)
+    x = W.f64_to_act(np.random.default_rng(1).standard_normal((100, 512)), "bf16")
+    pl = M.PackedLinear(q, "bf16")
+    a = M.act_tensor(x, "bf16")
+    o1 = M.linear_forward(pl, a).cpu().numpy()
+    o2 = M.linear_forward(pl, a).cpu().numpy()
+    assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
