@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""MoE-block forward benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mixtral]
+
+One step = one full block forward through libmxmoe (routing, plan, activation
+quantization, gate/up Group-GEMM with fused SiLU-gate, h quantization, down
+Group-GEMM, combine) on synthetic inputs already resident in HBM.  Prints one
+JSON line: effective TFLOP/s (2*m*N*K over real routed rows, summed over all
+linears) and microseconds per layer, the roofline of the dominant kernel (the
+gate/up Group-GEMM launch, timed with HIP events on the library's stream), and
+the CPU oracle timed on a bounded token sample.
+
+The default workload is the Mixtral-8x7B-shaped prefill block: 4096 tokens,
+hidden 4096, expert FFN 14336, 8 experts, top-2, Zipf(1.0) routing skew,
+3.26 average weight bits (hot expert w8a8, cold experts w2/w3/w4 g128).
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np
+
+HBM_PEAK = 8.0e12            # B/s
+MFMA_PEAK = {"i8": 5.0e15, "bf16": 2.5e15, "fp16": 2.5e15}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def group_stats(blk, counts):
+    """Per (phase, expert) algorithmic flops / bytes and the MFMA dtype."""
+    from paper_2505_05799_amd import workloads as W
+    cfg = blk.cfg
+    out = []
+    for e, lins in enumerate(blk.linears):
+        m = int(counts[e]) if e < cfg.E else cfg.T
+        if m == 0:
+            continue
+        for phase, idx in ((0, (0, 1)), (1, (2,))):
+            fl = by = 0.0
+            for j in idx:
+                q = lins[j]
+                fl += 2.0 * m * q.n * q.k
+                a_bytes = 1.0 if q.scheme.a_bits < 16 else 2.0
+                by += q.nbytes_packed + m * q.k * a_bytes
+            n_out = lins[idx[0]].n
+            by += m * n_out * (2.0 if phase == 0 else 4.0)
+            s = lins[idx[0]].scheme
+            dt = "i8" if s.a_bits < 16 else cfg.act
+            out.append({"expert": e, "phase": phase, "m": m, "flops": fl, "bytes": by, "dtype": dt,
+                        "scheme": s.name})
+    return out
+
+
+def roofline(groups, phase, t_s):
+    g = [x for x in groups if x["phase"] == phase]
+    flops = sum(x["flops"] for x in g)
+    nbytes = sum(x["bytes"] for x in g)
+    t_mfma = sum(x["flops"] / MFMA_PEAK[x["dtype"]] for x in g)
+    t_hbm = nbytes / HBM_PEAK
+    if t_mfma >= t_hbm:
+        peak = flops / t_mfma / 1e12          # dtype-weighted MFMA peak
+        ach = flops / t_s / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": None}
+    ach = nbytes / t_s / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+            "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None}
+
+
+def cpu_baseline(blk, tokens):
+    """The CPU oracle as it stands, on the first `tokens` tokens of the workload."""
+    from oracle import mxmoe_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count() or 1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    cfg = blk.cfg
+    # Bounded sample: the first `tokens` tokens whose experts all lie among the
+    # few hottest experts (so only those experts' weights are dequantized).
+    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
+    hot = list(np.argsort(-counts, kind="stable"))
+    for ns in range(cfg.k, cfg.E + 1):
+        ok = np.isin(blk.topk_ids, hot[:ns]).all(axis=1)
+        if ok.sum() >= tokens or ns == cfg.E:
+            break
+    sel = np.nonzero(ok)[0][:tokens]
+    ids = blk.topk_ids[sel]
+    n = len(sel)
+    flops = cfg.scaled(n).flops(np.bincount(ids.ravel(), minlength=cfg.E))
+    t0 = time.perf_counter()
+    O.moe_forward(blk.x[sel], ids, blk.topk_w[sel], blk.linears, cfg.E, cfg.act)
+    dt = time.perf_counter() - t0
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{n} of {cfg.T} tokens (the first routed only to the {ns} hottest experts), "
+                      f"fp64 numpy incl. dequantization of those experts", "seconds": round(dt, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the multi-GPU expert-parallel layout is a design, not a measured path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2505_05799_amd import mxmoe as M
+    from paper_2505_05799_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    M.load_library()
+    cfg = W.CONFIGS[args.workload]
+    t0 = time.perf_counter()
+    log(f"[bench] generating {cfg.name}: {cfg.description}")
+    blk = W.make_block(cfg, seed=args.seed)
+    log(f"[bench] inputs ready in {time.perf_counter() - t0:.1f}s; packing")
+    mb = M.MoEBlock(blk)
+    x = M.act_tensor(blk.x, cfg.act)
+    ids = torch.from_numpy(blk.topk_ids.copy()).cuda()
+    w = torch.from_numpy(blk.topk_w.copy()).cuda()
+    y = torch.empty_like(x)
+    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
+    flops = cfg.flops(counts)
+    log(f"[bench] packed {sum(p.nbytes for ps in mb.packed for p in ps) / 1e6:.1f} MB; "
+        f"{flops / 1e9:.1f} GFLOP per forward; warmup {args.warmup}")
+
+    for _ in range(args.warmup):
+        mb.forward(x, ids, w, y=y)
+    torch.cuda.synchronize()
+    evs = [M.PhaseEvents() for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for i in range(args.steps):
+        mb.forward(x, ids, w, y=y, events=evs[i])
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    ms = (t2 - t1) * 1e3 / args.steps
+    phases = np.array([e.elapsed_ms() for e in evs])          # [steps, 5]
+    ph_mean = phases.mean(axis=0)
+    groups = group_stats(blk, counts)
+    dom = 1  # gate/up Group-GEMM launch
+    roof = roofline(groups, 0, ph_mean[dom] / 1e3)
+    roof["kernel"] = "group_gemm_kernel<bf16, gate|up>" if cfg.act == "bf16" else "group_gemm_kernel<fp16, gate|up>"
+    roof["launch_ms"] = round(float(ph_mean[dom]), 4)
+    down = roofline(groups, 1, ph_mean[3] / 1e3)
+
+    rec = {
+        "metric": "MoE-block us/layer + effective TFLOP/s; % of HBM/MFMA roofline per group",
+        "value": round(flops / (ms / 1e3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "us_per_layer": round(ms * 1e3, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "i8+bf16" if cfg.act == "bf16" else "i8+fp16",
+        "data": "synthetic",
+        "config": {"workload": cfg.description, "tokens": cfg.T, "hidden": cfg.H, "ffn": cfg.F,
+                   "experts": cfg.E, "top_k": cfg.k, "shared_experts": cfg.n_shared,
+                   "avg_weight_bits": round(W.avg_weight_bits(cfg), 3), "gflop": round(flops / 1e9, 2)},
+        "roofline": roof,
+        "roofline_down": down,
+        "phases_ms": {n: round(float(v), 4) for n, v in zip(M.PHASE_NAMES, ph_mean)},
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] CPU oracle on {args.cpu_tokens} tokens")
+        rec["cpu_baseline"] = cpu_baseline(blk, args.cpu_tokens)
+    else:
+        rec["cpu_baseline"] = None
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

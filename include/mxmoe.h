@@ -202,8 +202,15 @@ typedef struct {
   int32_t split_phases;
   /* 1: skip the combine (y untouched) - to time the Group-GEMM alone.       */
   int32_t skip_combine;
-  int32_t reserved[4];
+  /* host array of 2*MXMOE_N_PHASES caller-created events, or NULL: event 2i
+   * is recorded on `stream` before phase i and event 2i+1 after it (phases:
+   * 0 routing + plan + x quantization, 1 gate/up Group-GEMM, 2 h quantization,
+   * 3 down Group-GEMM, 4 combine).                                          */
+  hipEvent_t* events;
+  int32_t reserved[2];
 } mxmoe_forward_opts;
+
+#define MXMOE_N_PHASES 5
 
 MXMOE_API mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table, int32_t T,
                                   const void* x, const int32_t* topk_ids, const float* topk_w,

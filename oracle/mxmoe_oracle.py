@@ -25,7 +25,7 @@ contract: the gated intermediate h is rounded once to the activation dtype
 before the down projection; a8/a4 down projections quantize that rounded h.
 The block output is returned unrounded in fp64.
 
-Parity pins live in ``tests/test_oracle_*.py``.
+Parity pins live in ``tests/test_oracle.py``.
 """
 
 from __future__ import annotations
@@ -38,7 +38,7 @@ import numpy as np
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "dequant",
     "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
-    "silu",
+    "silu", "tile_plan",
 ]
 
 # ----------------------------------------------------------------------------
@@ -385,3 +385,60 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 
     rec(0)
     return best[0] if c else 0.0
+
+
+# ----------------------------------------------------------------------------
+# Tile plan of the Group-GEMM (Sec. 4.3 tile configuration and tile schedule)
+# ----------------------------------------------------------------------------
+#
+# The paper fixes tile configurations offline per linear (the y variables of its
+# allocation problem, Eq. (7)) and orders tiles greedily, longest first.  This
+# library picks the configuration at run time from the group's row count m and
+# orders groups by a static per-tile cost.  The rule, restated here:
+#   configuration S (m <= 16): 16 rows x (gate|up 128, down 256) channels
+#   configuration M (m <= 64): 64 rows x (gate|up 64, down 128) channels
+#   configuration L (m > 64) : 128 rows x (gate|up 64, down 128) channels
+#   cost of a tile (ps) = max(bytes * 32, flops * 1000 / rate), truncated to an
+#   integer, with bytes = linears * BN * K * wbits / 8 + BM * K * abytes,
+#   flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
+#   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s;
+#   queue order: decreasing cost, ties by lower expert index.
+
+_TILE_BM = (16, 64, 128)
+_TILE_BN = ((128, 64, 64), (256, 128, 128))   # [phase][config]
+
+
+def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
+    """Tile configuration, tile counts, cost and queue rank per group of a phase.
+
+    ms[g]: rows of group g; lins[g]: its linear (gate for phase 0, down for 1).
+    Returns a list of dicts (cfg, mtiles, ntiles, cost, rank) and the queue
+    order (group indices with tiles, longest tile first).
+    """
+    out = []
+    for m, lin in zip(ms, lins):
+        s = lin.scheme
+        cfg = 0 if m <= 16 else (1 if m <= 64 else 2)
+        bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
+        mt = -(-m // bm) if m > 0 else 0
+        nt = -(-lin.n // bn)
+        nl = 2 if phase == 0 else 1
+        is_int = s.a_bits < 16
+        wbytes = float(nl * bn * lin.k * s.w_bits) / 8.0
+        abytes = float(bm) * lin.k * (1.0 if is_int else 2.0)
+        flops = 2.0 * nl * bm * bn * lin.k
+        c = max((wbytes + abytes) * 32.0, flops * 1000.0 / (19531.0 if is_int else 9766.0))
+        c = min(c, 2.0e9)
+        tiles = mt * nt
+        out.append({"cfg": cfg, "mtiles": mt, "ntiles": nt, "tiles": tiles,
+                    "cost": int(c) if tiles else 0})
+    live = [g for g, r in enumerate(out) if r["tiles"] > 0]
+    order = sorted(live, key=lambda g: (-out[g]["cost"], g))
+    for r in out:
+        r["rank"] = -1
+    start = 0
+    for rank, g in enumerate(order):
+        out[g]["rank"] = rank
+        out[g]["start"] = start
+        start += out[g]["tiles"]
+    return out, order

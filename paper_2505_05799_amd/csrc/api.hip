@@ -387,11 +387,18 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     if (e != hipSuccess) return MXMOE_ERR_HIP; \
   } while (0)
 
+  hipEvent_t* ev = (opts && opts->events) ? opts->events : nullptr;
+#define MX_EVENT(i)                                          \
+  do {                                                       \
+    if (ev && hipEventRecord(ev[i], stream) != hipSuccess) return MXMOE_ERR_HIP; \
+  } while (0)
+
   int32_t* counts = at<int32_t>(workspace, L.counts);
   int32_t* offsets = at<int32_t>(workspace, L.offsets);
   int32_t* sorted_pair = at<int32_t>(workspace, L.sorted_pair);
   int32_t* plan = at<int32_t>(workspace, L.plan);
   int32_t* down_qmax = at<int32_t>(workspace, L.down_qmax);
+  MX_EVENT(0);
   MX_CHECK(launch_route(topk_ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
                         at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
                         at<int32_t>(workspace, L.chunk_bad), stream));
@@ -431,7 +438,11 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.E_routed = bi.E;
   ga.n_shared = bi.nsh;
   const int grid = group_gemm_grid(current_device());
+  MX_EVENT(1);
+  MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));
+  MX_EVENT(3);
+  MX_EVENT(4);
   if (bi.any_hq)
     MX_CHECK(launch_hquant_routed(ga.h, bi.act, T * bi.k, bi.F, offsets, bi.E, down_qmax, at<int8_t>(workspace, L.hq),
                                   at<float>(workspace, L.hs), stream));
@@ -443,9 +454,15 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
                               bi.Fsh, qm, at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh,
                               at<float>(workspace, L.hs_shared) + rows, stream));
   }
+  MX_EVENT(5);
+  MX_EVENT(6);
   MX_CHECK(launch_group_gemm(ga, 1, grid, stream));
+  MX_EVENT(7);
+  MX_EVENT(8);
   if (!(opts && opts->skip_combine))
     MX_CHECK(launch_combine(ga.slots, topk_ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
+  MX_EVENT(9);
+#undef MX_EVENT
 #undef MX_CHECK
   return MXMOE_OK;
 }

@@ -36,9 +36,14 @@ class Block_t(C.Structure):
                 ("act", C.c_int), ("scheme", C.POINTER(Scheme_t)), ("packed", C.POINTER(C.c_void_p))]
 
 
+N_PHASES = 5
+PHASE_NAMES = ("route_plan_xquant", "gemm_gate_up", "hquant", "gemm_down", "combine")
+
+
 class ForwardOpts_t(C.Structure):
     _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("split_phases", C.c_int32),
-                ("skip_combine", C.c_int32), ("reserved", C.c_int32 * 4)]
+                ("skip_combine", C.c_int32), ("events", C.POINTER(C.c_void_p)),
+                ("reserved", C.c_int32 * 2)]
 
 
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
@@ -303,7 +308,7 @@ class MoEBlock:
         return {f: getattr(lay, f) for f in WS_FIELDS}
 
     def forward(self, x, topk_ids, topk_w, y=None, expert_mask: Optional[Sequence[int]] = None,
-                skip_combine: bool = False, stream=None):
+                skip_combine: bool = False, events=None, stream=None):
         torch = _torch()
         lib = load_library()
         T = x.shape[0]
@@ -312,8 +317,10 @@ class MoEBlock:
         if y is None:
             y = torch.empty_like(x)
         opts = None
-        if expert_mask is not None or skip_combine:
+        if expert_mask is not None or skip_combine or events is not None:
             o = ForwardOpts_t()
+            if events is not None:
+                o.events = events.array
             if expert_mask is not None:
                 self._mask = (C.c_uint8 * len(expert_mask))(*[1 if v else 0 for v in expert_mask])
                 o.expert_mask = C.cast(self._mask, C.POINTER(C.c_uint8))
@@ -332,3 +339,40 @@ class MoEBlock:
         torch = _torch()
         nbytes = count * torch.empty((), dtype=dtype).element_size()
         return self.ws[off: off + nbytes].view(dtype)
+
+
+# --------------------------------------------------------------- HIP events
+class PhaseEvents:
+    """2 * N_PHASES hipEvents for MoEBlock.forward(events=...), via the HIP runtime."""
+
+    def __init__(self):
+        self.hip = C.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [C.POINTER(C.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [C.POINTER(C.c_float), C.c_void_p, C.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [C.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [C.c_void_p]
+        self.array = (C.c_void_p * (2 * N_PHASES))()
+        for i in range(2 * N_PHASES):
+            ev = C.c_void_p()
+            if self.hip.hipEventCreate(C.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.array[i] = ev
+        self.array = C.cast(self.array, C.POINTER(C.c_void_p))
+
+    def elapsed_ms(self):
+        """Per-phase durations (ms) of the last forward recorded with these events."""
+        out = []
+        self.hip.hipEventSynchronize(self.array[2 * N_PHASES - 1])
+        for i in range(N_PHASES):
+            t = C.c_float()
+            if self.hip.hipEventElapsedTime(C.byref(t), self.array[2 * i], self.array[2 * i + 1]) != 0:
+                raise RuntimeError("hipEventElapsedTime failed")
+            out.append(float(t.value))
+        return out
+
+    def __del__(self):
+        try:
+            for i in range(2 * N_PHASES):
+                self.hip.hipEventDestroy(self.array[i])
+        except Exception:
+            pass

@@ -377,3 +377,23 @@ def test_runtime_model_many_tiles():
         c = rng.choice([1.0, 2.5, 7.0], size=n)
         errs.append(O.lpt_makespan(c, P) / (c.sum() / P) - 1)
     assert errs[-1] < 0.01 and errs[0] > errs[-1]
+
+
+@pytest.mark.parametrize("name", ["tiny", "dsv2lite", "qwen15_mixed"])
+def test_tile_plan_covers_every_output(name):
+    blk = W.make_block(name, with_weights=False)
+    cfg = blk.cfg
+    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E).tolist() + [cfg.T] * cfg.n_shared
+    for phase, (n, k) in ((0, (cfg.F, cfg.H)), (1, (cfg.H, cfg.F))):
+        lins = [W.QLinear(s[0 if phase == 0 else 2], n if e < cfg.E else
+                          (cfg.F_shared if phase == 0 else cfg.H),
+                          k if e < cfg.E else (cfg.H if phase == 0 else cfg.F_shared), None)
+                for e, s in enumerate(W.schemes_of(cfg))]
+        plan, order = O.tile_plan(counts, lins, phase)
+        for m, lin, r in zip(counts, lins, plan):
+            bm, bn = (16, 64, 128)[r["cfg"]], ((128, 64, 64), (256, 128, 128))[phase][r["cfg"]]
+            assert r["mtiles"] * bm >= m > (r["mtiles"] - 1) * bm or m == r["mtiles"] == 0
+            assert r["ntiles"] * bn >= lin.n > (r["ntiles"] - 1) * bn
+        costs = [plan[g]["cost"] for g in order]
+        assert costs == sorted(costs, reverse=True)
+        assert sorted(order) == [g for g, m in enumerate(counts) if m > 0]
