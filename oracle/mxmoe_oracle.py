@@ -395,17 +395,18 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 # allocation problem, Eq. (7)) and orders tiles greedily, longest first.  This
 # library picks the configuration at run time from the group's row count m and
 # orders groups by a static per-tile cost.  The rule, restated here:
-#   configuration S (m <= 16): 16 rows x (gate|up 128, down 256) channels
-#   configuration M (m <= 64): 64 rows x (gate|up 64, down 128) channels
-#   configuration L (m > 64) : 128 rows x (gate|up 64, down 128) channels
+#   configuration S (m <= 16): 16 rows x (gate|up 256, down 512) channels
+#   configuration T (m <= 32): 32 rows x (gate|up 256, down 512) channels
+#   configuration M (m <= 64): 64 rows x (gate|up 128, down 256) channels
+#   configuration L (m > 64) : 128 rows x (gate|up 128, down 256) channels
 #   cost of a tile (ps) = max(bytes * 32, flops * 1000 / rate), truncated to an
 #   integer, with bytes = linears * BN * K * wbits / 8 + BM * K * abytes,
 #   flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
 #   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s;
 #   queue order: decreasing cost, ties by lower expert index.
 
-_TILE_BM = (16, 64, 128)
-_TILE_BN = ((128, 64, 64), (256, 128, 128))   # [phase][config]
+_TILE_BM = (16, 32, 64, 128)
+_TILE_BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][config]
 
 
 def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
@@ -418,7 +419,7 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
     out = []
     for m, lin in zip(ms, lins):
         s = lin.scheme
-        cfg = 0 if m <= 16 else (1 if m <= 64 else 2)
+        cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-lin.n // bn)

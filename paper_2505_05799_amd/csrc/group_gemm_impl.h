@@ -1,0 +1,643 @@
+// Mixed-precision Group-GEMM of the MoE block (Sec. 4.3 of the paper:
+// micro-kernel specialization, equal-resource tile configurations, and a
+// greedy longest-tile-first schedule), written for gfx950.
+//
+//   plan_kernel        one workgroup: per (phase, expert) group picks a tile
+//                      configuration from the group's row count, counts its
+//                      tiles, estimates a per-tile cost and orders the groups by
+//                      decreasing tile cost (ties: lower expert first).  The tile
+//                      queue of a phase is the concatenation of the groups'
+//                      tiles in that order: workgroups that free up take the next
+//                      tile, i.e. list scheduling with the longest tiles first.
+//   group_gemm_kernel  persistent: every workgroup pops tile indices from an
+//                      atomic head counter and dispatches, outside the MAC loop,
+//                      to the micro-kernel of the tile's (scheme, configuration).
+//
+// Every configuration uses 4 wavefronts (equal resources for all micro-kernels,
+// as the paper requires for horizontal fusion) stacked along the output
+// channels: a tile is BM rows x BN channels (per linear) and wavefront w owns
+// channels [w*BN/4, (w+1)*BN/4).  Activation rows of the tile are staged per
+// 128-wide k block into LDS with direct global->LDS loads (16-byte chunks,
+// XOR-swizzled so that MFMA fragment reads are bank-conflict free), double
+// buffered; weights stream from HBM straight into registers in the packed
+// fragment order (each weight is read once per tile, by one wavefront).
+//
+// MFMA roles: activations are the A operand (16 rows x 32/64 k), weights the B
+// operand (32/64 k x 16 channels).  A lane's four accumulators are four rows of
+// one output channel, so a lane needs one (scale, zero) pair per fragment.
+//
+// Numerics per scheme (every result is exact up to fp32 accumulation):
+//   w16   : 16-bit MFMA, fp32 accumulation.
+//   w8a8  : int8 MFMA, exact int32 sums, then fp32 (acc * s_a) * s_w.
+//   w4a4  : nibbles widened to int8 as 16*q, int8 MFMA, exact sum / 16.
+//   wNg128: the 16-bit operand is formed exactly.  bf16 activations: a packed
+//           integer add turns the codes of two slots into bf16 values
+//           c + (q - z), c = 128 + 2^N - 1, and the row sums R of the staged
+//           activations (computed by an MFMA against ones) remove c * R.  fp16
+//           activations: the same bit pattern in fp16 minus 1024 + 2^N - 1 gives
+//           q - z exactly.  8-bit codes are converted through fp32.  Each
+//           128-wide group has its own fp16 scale s_g: the running sum Q is kept
+//           in units of the current group's scale, Q_g = Q_{g-1} * s_{g-1}/s_g +
+//           sum_g a*(q - z) (the correction -c*R folded into the same FMA), and
+//           the output is s_last * Q_last.
+//
+// Phase 0 computes gate and up of an expert in the same tile and applies the
+// SiLU gate in registers: h = SiLU(g) * u, rounded once to the activation
+// dtype.  Phase 1 computes the down projection, multiplies each row by its
+// router gate weight and stores fp32 rows in the per-(token, slot) buffer that
+// the combine sums in a fixed order.
+#pragma once
+#include "mxmoe_internal.h"
+
+namespace mxmoe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kThreads = 256;
+constexpr int kPhaseRaw = 2;
+constexpr int KC = 128;        // k per stage = one weight group
+constexpr int BM_MAX = 128;
+constexpr int STAGE_BYTES = BM_MAX * 256;
+
+// ------------------------------------------------------------ tile configs
+// MF: 16-row fragments per tile (BM = 16 MF); NF: 16-channel fragments per
+// wavefront and linear.  Accumulator registers per lane = 4 * MF * NF * NL.
+__host__ __device__ constexpr int cfg_mf(int c) { return c == CFG_S ? 1 : (c == CFG_T ? 2 : (c == CFG_M ? 4 : 8)); }
+__host__ __device__ constexpr int cfg_nf(int c, int phase) {
+  return phase == 0 ? ((c == CFG_S || c == CFG_T) ? 4 : 2) : ((c == CFG_S || c == CFG_T) ? 8 : 4);
+}
+__host__ __device__ constexpr int cfg_bm(int c) { return 16 * cfg_mf(c); }
+__host__ __device__ constexpr int cfg_bn(int c, int phase) { return 64 * cfg_nf(c, phase); }
+__host__ __device__ inline int pick_cfg(int m) {
+  return m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
+}
+
+// ---------------------------------------------------------- MFMA helpers
+template <int ACT> __device__ inline f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  if constexpr (ACT == MXMOE_BF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b),
+                                                  c, 0, 0, 0);
+}
+
+__device__ inline float act_to_f32(uint16_t b, int act) {
+  if (act == MXMOE_BF16) return __uint_as_float(((uint32_t)b) << 16);
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+template <int ACT> __device__ inline uint16_t f32_to_act(float f) {
+  if constexpr (ACT == MXMOE_BF16) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+  } else {
+    return __builtin_bit_cast(uint16_t, (_Float16)f);
+  }
+}
+
+__device__ inline float silu_f32(float g) { return g / (1.0f + expf(-g)); }
+
+// ------------------------------------------------------- weight operands
+// Low-bit kinds prefetch a whole 128-wide group (8-16 bytes per lane); the wide
+// kinds (w16, w8g, w8a8: 32-64 bytes per lane) stream one MFMA step at a time.
+template <int KD> constexpr bool streamed() { return KD == K_W16 || KD == K_W8G || KD == K_W8A8; }
+template <int KD> struct Raw { u32x4 d[1]; };
+template <> struct Raw<K_W2G> { u32x2 d; };
+template <> struct Raw<K_W3G> { uint32_t d[3]; };
+
+template <int KD> __device__ inline void load_raw(Raw<KD>& r, const uint8_t* p) {
+  if constexpr (KD == K_W2G) {
+    r.d = *reinterpret_cast<const u32x2*>(p);
+  } else if constexpr (KD == K_W3G) {
+    const uint32_t* q = reinterpret_cast<const uint32_t*>(p);  // 12-byte lanes: 4-byte aligned
+    r.d[0] = q[0]; r.d[1] = q[1]; r.d[2] = q[2];
+  } else if constexpr (!streamed<KD>()) {
+    r.d[0] = *reinterpret_cast<const u32x4*>(p);
+  }
+}
+
+// streamed kinds: the lane's bytes of MFMA step j
+template <int KD> __device__ inline u32x4 load_step(const uint8_t* p, int j) {
+  if constexpr (KD == K_W8G) {
+    const u32x2 v = *reinterpret_cast<const u32x2*>(p + 8 * j);
+    return u32x4{v[0], v[1], 0u, 0u};
+  } else {
+    return *reinterpret_cast<const u32x4*>(p + 16 * j);
+  }
+}
+
+// bias constant b = 2^N - 1 of the exact magic-number dequantization
+template <int KD> constexpr int wbias() { return KD == K_W2G ? 3 : (KD == K_W3G ? 7 : 15); }
+
+template <int ACT> __device__ inline uint32_t pack_exact(float lo, float hi) {
+  if constexpr (ACT == MXMOE_BF16)  // small integers: truncation to bf16 is exact
+    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+  else
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+}
+
+// 16-bit weight operand of MFMA step j (8 slots) for the lane's channel.
+// bz: per-group constant (bias pair for 2/3/4-bit codes, zero point for 8-bit).
+template <int KD, int ACT>
+__device__ inline u32x4 wfrag16(const Raw<KD>& r, u32x4 step, int j, uint32_t bz, float zf) {
+  u32x4 o;
+  if constexpr (KD == K_W16) {
+    o = step;
+  } else if constexpr (KD == K_W8G) {
+    const uint32_t a = step[0], b = step[1];
+    o[0] = pack_exact<ACT>((float)(a & 0xFFu) - zf, (float)((a >> 8) & 0xFFu) - zf);
+    o[1] = pack_exact<ACT>((float)((a >> 16) & 0xFFu) - zf, (float)(a >> 24) - zf);
+    o[2] = pack_exact<ACT>((float)(b & 0xFFu) - zf, (float)((b >> 8) & 0xFFu) - zf);
+    o[3] = pack_exact<ACT>((float)((b >> 16) & 0xFFu) - zf, (float)(b >> 24) - zf);
+  } else {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t v;
+      if constexpr (KD == K_W4G) {
+        v = (r.d[0][j] >> (4 * p)) & 0x000F000Fu;
+      } else if constexpr (KD == K_W2G) {
+        const int P = 4 * (j & 1) + p;
+        v = (r.d[j >> 1] >> (2 * P)) & 0x00030003u;
+      } else {  // K_W3G
+        const int P = 4 * (j & 1) + p, P3 = 4 * j + p;
+        const uint32_t hi = (P3 >= 2 ? (r.d[2] >> (P3 - 2)) : (r.d[2] << (2 - P3))) & 0x00040004u;
+        v = ((r.d[j >> 1] >> (2 * P)) & 0x00030003u) | hi;
+      }
+      v += bz;
+      if constexpr (ACT == MXMOE_F16) {
+        // fp16 1024 + b + (q - z)  ->  q - z, exact
+        const f16x2 off = {(_Float16)(-(1024 + wbias<KD>())), (_Float16)(-(1024 + wbias<KD>()))};
+        v = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) + off);
+      }
+      o[p] = v;
+    }
+  }
+  return o;
+}
+
+// int8 weight operand of MFMA step j (16 slots)
+template <int KD> __device__ inline i32x4 wfrag8(const Raw<KD>& r, u32x4 step, int j) {
+  if constexpr (KD == K_W8A8) {
+    return __builtin_bit_cast(i32x4, step);
+  } else {
+    const uint32_t d0 = r.d[0][2 * j], d1 = r.d[0][2 * j + 1];
+    i32x4 o;
+    o[0] = (int)((d0 << 4) & 0xF0F0F0F0u);
+    o[1] = (int)(d0 & 0xF0F0F0F0u);
+    o[2] = (int)((d1 << 4) & 0xF0F0F0F0u);
+    o[3] = (int)(d1 & 0xF0F0F0F0u);
+    return o;
+  }
+}
+
+// ------------------------------------------------------------- LDS stage
+struct __align__(16) Smem {
+  uint8_t act[2][STAGE_BYTES];   // activation rows of the tile, one 128-wide k block per stage
+  float rsum[2][BM_MAX];         // per-row sums of a stage (bf16 weight-only kinds)
+  int32_t rowsrc[BM_MAX];        // activation row index of every tile row
+  int32_t tile;
+};
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Stage one k block of BM rows into act[buf] with direct global->LDS loads.
+// 16-bit rows are 256 bytes (16 chunks, chunk c stored at c ^ (r & 15)), int8
+// rows 128 bytes (8 chunks, chunk c stored at c ^ ((r >> 1) & 7)); one
+// wavefront instruction fills 1 KB (4 or 8 rows).
+template <bool INT, int BM>
+__device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, int64_t row_bytes, int kb, int tid) {
+  constexpr int RB = INT ? 128 : 256;
+  constexpr int ROWS_PER_BLK = 1024 / RB;
+  constexpr int NBLK = BM * RB / 1024;
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int blk = wave; blk < NBLK; blk += 4) {
+    const int r = blk * ROWS_PER_BLK + lane / (RB / 16);
+    const int p = lane % (RB / 16);
+    const int cc = INT ? (p ^ ((r >> 1) & 7)) : (p ^ (r & 15));
+    const uint8_t* src = base + (int64_t)sm.rowsrc[r] * row_bytes + (int64_t)kb * RB + cc * 16;
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sm.act[buf] + blk * 1024), 16, 0, 0);
+  }
+}
+
+template <bool INT> __device__ inline u32x4 act_frag(const Smem& sm, int buf, int r, int cc) {
+  const int pos = INT ? (cc ^ ((r >> 1) & 7)) : (cc ^ (r & 15));
+  return *reinterpret_cast<const u32x4*>(sm.act[buf] + r * (INT ? 128 : 256) + pos * 16);
+}
+
+// Row sums of a 16-bit stage: MFMA of each 16-row fragment against ones; the
+// fragments are shared out over the wavefronts.
+template <int ACT, int MF> __device__ inline void stage_rowsum(Smem& sm, int buf, int tid) {
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 15, q = lane >> 4;
+  const u32x4 ones = ACT == MXMOE_BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
+                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
+  for (int mf = wave; mf < MF; mf += 4) {
+    f32x4 s = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s = mfma16<ACT>(act_frag<false>(sm, buf, mf * 16 + li, 4 * j + q), ones, s);
+    if (li == 0) *reinterpret_cast<f32x4*>(&sm.rsum[buf][mf * 16 + 4 * q]) = s;
+  }
+}
+
+// ---------------------------------------------------------- tile body
+template <int KD, int ACT, int CFG, int PHASE>
+__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt) {
+  constexpr int MF = cfg_mf(CFG);
+  constexpr int NF = cfg_nf(CFG, PHASE == 0 ? 0 : 1);
+  constexpr int NL = PHASE == 0 ? 2 : 1;
+  constexpr bool INT = kind_is_int(KD);
+  constexpr bool WONLY = kind_is_wonly(KD);
+  constexpr bool MAGIC = WONLY && KD != K_W8G;          // 2/3/4-bit codes
+  constexpr bool RSUM = MAGIC && ACT == MXMOE_BF16;     // bias removed through row sums
+  constexpr int BM = 16 * MF;
+  constexpr int BN = 64 * NF;
+  constexpr int LB = lane_bytes(KD);
+  constexpr int BB = block_bytes(KD);
+  constexpr float CB = (float)(128 + (MAGIC ? wbias<KD>() : 0));
+
+  // Opaque thread id: keeps lane-derived values inside the tile body instead of
+  // letting the persistent loop hoist them for every micro-kernel at once.
+  int tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int wave = tid >> 6, lane = tid & 63;
+  const int li = lane & 15, q = lane >> 4;
+  const bool shared = g >= a.E_routed;
+  const DevLinear* lins[NL];
+  if constexpr (PHASE == 0) { lins[0] = &ex->lin[0]; lins[1] = &ex->lin[1]; }
+  else if constexpr (PHASE == 1) { lins[0] = &ex->lin[2]; }
+  else { lins[0] = &a.raw_lin; }
+  const int N = lins[0]->n, K = lins[0]->k;
+  const int kblocks = K / 128;
+  const int row0 = mt * BM;
+  const int nb0 = (nt * BN) / 16 + wave * NF;   // first 16-channel block of this wavefront
+  int nvalid = N / 16 - nb0;
+  nvalid = nvalid < 0 ? 0 : (nvalid > NF ? NF : nvalid);
+  const int off_e = (!shared && PHASE != kPhaseRaw) ? a.offsets[g] : 0;
+
+  // ---- activation source rows
+  if (tid < BM) {
+    int m = row0 + tid;
+    if (m >= m_g) m = m_g - 1;
+    int src;
+    if constexpr (PHASE == 0) src = shared ? m : a.sorted_pair[off_e + m] / a.k;
+    else if constexpr (PHASE == 1) src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
+    else src = m;
+    sm.rowsrc[tid] = src;
+  }
+  const uint8_t* abase;
+  const float* ascale = nullptr;
+  if constexpr (INT) {
+    const int8_t* qb;
+    if constexpr (PHASE == 1) { qb = shared ? a.hq_shared : a.hq; ascale = shared ? a.hs_shared : a.hs; }
+    else { qb = KD == K_W8A8 ? a.xq8 : a.xq4; ascale = KD == K_W8A8 ? a.xs8 : a.xs4; }
+    abase = reinterpret_cast<const uint8_t*>(qb);
+  } else {
+    abase = reinterpret_cast<const uint8_t*>(PHASE == 1 ? (shared ? a.h_shared : a.h) : a.x);
+  }
+  const int64_t row_bytes = (int64_t)K * (INT ? 1 : 2);
+  __syncthreads();
+
+  // ---- accumulators and weight streams
+  typedef typename std::conditional<INT, i32x4, f32x4>::type AccT;
+  typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
+  constexpr int J = INT ? 2 : 4;                 // MFMA steps per 128-wide k block
+  constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
+  // 3/4-bit codes in the 128-row tiles: the next group is fetched dword by dword
+  // into registers whose codes have been consumed (no second copy of the group)
+  constexpr bool SPLIT = false;
+  AccT acc[NL][NF][MF];
+#pragma unroll
+  for (int l = 0; l < NL; ++l)
+#pragma unroll
+    for (int nf = 0; nf < NF; ++nf)
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = AccT{0, 0, 0, 0};
+
+  const uint8_t* wp[NL][NF];
+#pragma unroll
+  for (int l = 0; l < NL; ++l)
+#pragma unroll
+    for (int nf = 0; nf < NF; ++nf)
+      wp[l][nf] = lins[l]->packed + (int64_t)(nb0 + (nf < nvalid ? nf : 0)) * kblocks * BB + lane * LB;
+
+  Raw<KD> raw[NL][NF];   // low-bit kinds: next group, prefetched a group ahead
+  u32x4 st[NL][NF];      // streamed kinds: next MFMA step, prefetched a step ahead
+  uint32_t meta[NL][NF];
+  float s_prev[NL][NF];
+  auto load_group = [&](int kb) {
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf)
+        if (nf < nvalid) {
+          const uint8_t* blk = wp[l][nf] + (int64_t)kb * BB;
+          load_raw<KD>(raw[l][nf], blk);
+          if constexpr (WONLY) meta[l][nf] = reinterpret_cast<const uint32_t*>(blk - lane * LB + 64 * LB)[li];
+        }
+  };
+  auto load_meta = [&](int kb) {
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf)
+        if (nf < nvalid) meta[l][nf] = reinterpret_cast<const uint32_t*>(wp[l][nf] + (int64_t)kb * BB - lane * LB + 64 * LB)[li];
+  };
+  // dword `w` of every fragment's next group (SPLIT kinds)
+  auto load_dword = [&](int kb, int w) {
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf)
+        if (nf < nvalid) {
+          const uint32_t v = reinterpret_cast<const uint32_t*>(wp[l][nf] + (int64_t)kb * BB)[w];
+          if constexpr (KD == K_W4G) raw[l][nf].d[0][w] = v;
+          else if constexpr (KD == K_W3G) raw[l][nf].d[w] = v;
+        }
+  };
+  auto load_steps = [&](int kb, int j) {
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf)
+        if (nf < nvalid) st[l][nf] = load_step<KD>(wp[l][nf] + (int64_t)kb * BB, j);
+  };
+
+  stage_load<INT, BM>(sm, 0, abase, row_bytes, 0, tid);
+  load_group(0);
+  if constexpr (streamed<KD>()) load_steps(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if constexpr (RSUM) {
+    stage_rowsum<ACT, MF>(sm, 0, tid);
+    __syncthreads();
+  }
+
+  for (int kb = 0; kb < kblocks; ++kb) {
+    const int cur = kb & 1;
+    const bool more = kb + 1 < kblocks;
+    if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, row_bytes, kb + 1, tid);
+    Raw<KD> rw[NL][NF];
+    uint32_t hi3[NL][NF];  // SPLIT w3g: hi-bit plane of the current group
+    uint32_t bz[NL][NF];
+    float zf[NL][NF];
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf) {
+        if constexpr (!SPLIT) rw[l][nf] = raw[l][nf];
+        if constexpr (SPLIT && KD == K_W3G) hi3[l][nf] = raw[l][nf].d[2];
+        bz[l][nf] = 0;
+        zf[l][nf] = 0.f;
+        if constexpr (WONLY) {
+          const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu));
+          const float z = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] >> 16));
+          zf[l][nf] = z;
+          if constexpr (MAGIC) {
+            const uint32_t base = ACT == MXMOE_BF16 ? 0x43004300u : 0x64006400u;
+            bz[l][nf] = base + (uint32_t)(wbias<KD>() - (int)z) * 0x00010001u;
+          }
+          // move the running sum into units of this group's scale
+          const float r = kb ? s_prev[l][nf] * __builtin_amdgcn_rcpf(s) : 0.f;
+          s_prev[l][nf] = s;
+#pragma unroll
+          for (int mf = 0; mf < MF; ++mf) {
+            f32x4 cr = {0, 0, 0, 0};
+            if constexpr (RSUM) cr = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][mf * 16 + 4 * q]) * (-CB);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[l][nf][mf][i] = __builtin_fmaf(acc[l][nf][mf][i], r, cr[i]);
+          }
+        }
+      }
+    if (more && !streamed<KD>() && !SPLIT) load_group(kb + 1);
+    if (more && (SPLIT || (streamed<KD>() && WONLY))) load_meta(kb + 1);
+
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      u32x4 sj[NL][NF];
+      if constexpr (streamed<KD>()) {
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) sj[l][nf] = st[l][nf];
+        if (j + 1 < J) load_steps(kb, j + 1);
+        else if (more) load_steps(kb + 1, 0);
+      }
+      auto wop = [&](int l, int nf) -> OpT {
+        const u32x4 sv = streamed<KD>() ? sj[l][nf] : u32x4{0u, 0u, 0u, 0u};
+        Raw<KD> rv;
+        if constexpr (SPLIT) {
+          rv = raw[l][nf];
+          if constexpr (KD == K_W3G) rv.d[2] = hi3[l][nf];
+        } else {
+          rv = rw[l][nf];
+        }
+        if constexpr (INT) return wfrag8<KD>(rv, sv, j);
+        else return wfrag16<KD, ACT>(rv, sv, j, bz[l][nf], zf[l][nf]);
+      };
+      auto aop = [&](int mf) -> OpT {
+        return __builtin_bit_cast(OpT, act_frag<INT>(sm, cur, mf * 16 + li, 4 * j + q));
+      };
+      auto mma = [&](const OpT& af, const OpT& wf, AccT c) -> AccT {
+        if constexpr (INT) return __builtin_amdgcn_mfma_i32_16x16x64_i8(af, wf, c, 0, 0, 0);
+        else return mfma16<ACT>(af, wf, c);
+      };
+      if constexpr (HOLD_W) {
+        OpT wf[NL][NF];
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) wf[l][nf] = wop(l, nf);
+        if constexpr (SPLIT) {
+          if (more) {
+            if constexpr (KD == K_W4G) load_dword(kb + 1, j);          // step j's codes are consumed
+            else if (j == 0) load_dword(kb + 1, 2);                     // hi plane was copied
+            else if (j == 1) load_dword(kb + 1, 0);                     // steps 0-1 consumed
+            else if (j == 3) load_dword(kb + 1, 1);                     // steps 2-3 consumed
+          }
+        }
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          const OpT af = aop(mf);
+#pragma unroll
+          for (int l = 0; l < NL; ++l)
+#pragma unroll
+            for (int nf = 0; nf < NF; ++nf)
+              if (nf < nvalid) acc[l][nf][mf] = mma(af, wf[l][nf], acc[l][nf][mf]);
+        }
+      } else {
+        OpT af[MF];
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) af[mf] = aop(mf);
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            if (nf < nvalid) {
+              const OpT wf = wop(l, nf);
+#pragma unroll
+              for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = mma(af[mf], wf, acc[l][nf][mf]);
+            }
+          }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if constexpr (RSUM) {
+      if (more) {
+        stage_rowsum<ACT, MF>(sm, cur ^ 1, tid);
+        __syncthreads();
+      }
+    }
+  }
+
+  // ---- epilogue: lane holds rows 4q + i of fragment mf, channel li of fragment nf
+  float rscale[MF][4];
+  int rows[MF][4];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = mf * 16 + 4 * q + i;
+      rows[mf][i] = row0 + r;
+      rscale[mf][i] = 1.f;
+      if constexpr (INT) rscale[mf][i] = ascale[sm.rowsrc[r]];
+    }
+#pragma unroll
+  for (int nf = 0; nf < NF; ++nf) {
+    if (nf >= nvalid) continue;
+    const int n = 16 * (nb0 + nf) + li;
+    float cs[NL];
+#pragma unroll
+    for (int l = 0; l < NL; ++l) {
+      cs[l] = 1.f;
+      if constexpr (INT) cs[l] = lins[l]->wscale[n];
+      if constexpr (WONLY) cs[l] = s_prev[l][nf];
+    }
+#pragma unroll
+    for (int mf = 0; mf < MF; ++mf) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = rows[mf][i];
+        if (m >= m_g) continue;
+        float v[NL];
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+          if constexpr (INT) {
+            int iv = acc[l][nf][mf][i];
+            if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
+            v[l] = ((float)iv * rscale[mf][i]) * cs[l];
+          } else {
+            v[l] = acc[l][nf][mf][i] * cs[l];
+          }
+        }
+        if constexpr (PHASE == 0) {
+          uint16_t* hb = reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h);
+          const int64_t hrow = shared ? (int64_t)(g - a.E_routed) * a.T + m : (int64_t)off_e + m;
+          hb[hrow * N + n] = f32_to_act<ACT>(silu_f32(v[0]) * v[1]);
+        } else if constexpr (PHASE == 1) {
+          int64_t srow;
+          float gw;
+          if (shared) {
+            srow = (int64_t)m * (a.k + a.n_shared) + a.k + (g - a.E_routed);
+            gw = 1.f;
+          } else {
+            const int p = a.sorted_pair[off_e + m];
+            srow = (int64_t)(p / a.k) * (a.k + a.n_shared) + (p % a.k);
+            gw = a.topk_w[p];
+          }
+          a.slots[srow * N + n] = v[0] * gw;
+        } else {
+          if constexpr (INT) {
+            int iv = acc[0][nf][mf][i];
+            if constexpr (KD == K_W4A4) iv >>= 4;
+            reinterpret_cast<int32_t*>(a.raw_out)[(int64_t)m * N + n] = iv;
+          } else {
+            reinterpret_cast<float*>(a.raw_out)[(int64_t)m * N + n] = v[0];
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();  // the next tile rewrites rowsrc and the stages
+}
+
+template <int ACT, int PHASE, int CFG>
+__device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
+                                     int kd) {
+  switch (kd) {
+    case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    default: break;
+  }
+}
+
+template <int ACT, int PHASE>
+__global__ void __launch_bounds__(kThreads, 2) group_gemm_kernel(GemmArgs a) {
+  __shared__ Smem sm;
+  const int G = a.G;
+  const int pidx = PHASE == kPhaseRaw ? 0 : PHASE;
+  const int32_t* rec = a.plan + (int64_t)pidx * G * PF_N;
+  const int32_t* order = a.plan + 2LL * G * PF_N + (int64_t)pidx * G;
+  int32_t* ctr = a.plan + 2LL * G * PF_N + 2LL * G;
+  const int total = ctr[PC_TOTAL0 + pidx];
+  const int ng = ctr[4 + pidx];
+  for (;;) {
+    if (threadIdx.x == 0) sm.tile = atomicAdd(&ctr[PC_HEAD0 + pidx], 1);
+    __syncthreads();
+    // wave-uniform from here on: tile bookkeeping and weight pointers live in SGPRs
+    const int tile = __builtin_amdgcn_readfirstlane(sm.tile);
+    __syncthreads();
+    if (tile >= total) break;
+    int lo = 0, hi = ng;  // largest rank whose first tile <= tile
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (rec[(int64_t)order[mid] * PF_N + PF_START] <= tile) lo = mid; else hi = mid;
+    }
+    const int g = __builtin_amdgcn_readfirstlane(order[lo]);
+    const int32_t* r = rec + (int64_t)g * PF_N;
+    const int local = tile - __builtin_amdgcn_readfirstlane(r[PF_START]);
+    const int mtiles = __builtin_amdgcn_readfirstlane(r[PF_MTILES]);
+    const int mt = local % mtiles, nt = local / mtiles;
+    const DevExpert* ex = PHASE == kPhaseRaw ? nullptr : a.experts + g;
+    const int kd = __builtin_amdgcn_readfirstlane(PHASE == kPhaseRaw ? a.raw_lin.kind : ex->lin[PHASE == 0 ? 0 : 2].kind);
+    const int m_g = __builtin_amdgcn_readfirstlane(r[PF_M]);
+    switch (__builtin_amdgcn_readfirstlane(r[PF_CFG])) {
+      case CFG_S: dispatch_kind<ACT, PHASE, CFG_S>(sm, a, ex, g, m_g, mt, nt, kd); break;
+      case CFG_T: dispatch_kind<ACT, PHASE, CFG_T>(sm, a, ex, g, m_g, mt, nt, kd); break;
+      case CFG_M: dispatch_kind<ACT, PHASE, CFG_M>(sm, a, ex, g, m_g, mt, nt, kd); break;
+      default: dispatch_kind<ACT, PHASE, CFG_L>(sm, a, ex, g, m_g, mt, nt, kd); break;
+    }
+  }
+}
+
+}  // namespace
+
+// Per-(activation dtype, phase) launchers, one translation unit each.
+#define MXMOE_GG_LAUNCHER(NAME, ACT, PHASE)                                                   \
+  hipError_t NAME(const GemmArgs& a, int grid, hipStream_t s) {                               \
+    hipLaunchKernelGGL((group_gemm_kernel<ACT, PHASE>), dim3(grid), dim3(kThreads), 0, s, a); \
+    return hipGetLastError();                                                                 \
+  }
+
+hipError_t gg_bf16_p0(const GemmArgs& a, int grid, hipStream_t s);
+hipError_t gg_bf16_p1(const GemmArgs& a, int grid, hipStream_t s);
+hipError_t gg_bf16_raw(const GemmArgs& a, int grid, hipStream_t s);
+hipError_t gg_f16_p0(const GemmArgs& a, int grid, hipStream_t s);
+hipError_t gg_f16_p1(const GemmArgs& a, int grid, hipStream_t s);
+hipError_t gg_f16_raw(const GemmArgs& a, int grid, hipStream_t s);
+
+}  // namespace mxmoe

@@ -86,10 +86,9 @@ struct DevHeader {
 };
 
 // ------------------------------------------------------------- tile plan
-// Tile configurations of the persistent Group-GEMM.  All use 256 threads
-// (4 wavefronts); the wavefront grid is WM x WN and a wavefront computes
-// MB x NB fragments of 16 x 16 outputs (per linear).
-enum Cfg : int32_t { CFG_S = 0, CFG_M = 1, CFG_L = 2, CFG_COUNT = 3 };
+// Tile configurations of the persistent Group-GEMM (16, 32, 64, 128 rows).
+// All use 256 threads (4 wavefronts stacked along the output channels).
+enum Cfg : int32_t { CFG_S = 0, CFG_T = 1, CFG_M = 2, CFG_L = 3, CFG_COUNT = 4 };
 
 // Plan record per (phase, expert): int32 fields.
 enum PlanField : int32_t {

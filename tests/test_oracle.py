@@ -391,7 +391,8 @@ def test_tile_plan_covers_every_output(name):
                 for e, s in enumerate(W.schemes_of(cfg))]
         plan, order = O.tile_plan(counts, lins, phase)
         for m, lin, r in zip(counts, lins, plan):
-            bm, bn = (16, 64, 128)[r["cfg"]], ((128, 64, 64), (256, 128, 128))[phase][r["cfg"]]
+            bm = (16, 32, 64, 128)[r["cfg"]]
+            bn = ((256, 256, 128, 128), (512, 512, 256, 256))[phase][r["cfg"]]
             assert r["mtiles"] * bm >= m > (r["mtiles"] - 1) * bm or m == r["mtiles"] == 0
             assert r["ntiles"] * bn >= lin.n > (r["ntiles"] - 1) * bn
         costs = [plan[g]["cost"] for g in order]
