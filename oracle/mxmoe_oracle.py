@@ -38,7 +38,7 @@ import numpy as np
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "dequant",
     "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
-    "silu", "tile_plan",
+    "silu", "tile_plan", "xcd_queues",
 ]
 
 # ----------------------------------------------------------------------------
@@ -443,3 +443,35 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
         out[g]["start"] = start
         start += out[g]["tiles"]
     return out, order
+
+
+# Super-tiles and per-XCD queues.  A group of mt x nt tiles is cut into
+# super-tiles of sm = min(mt, 8) row tiles by sn = min(nt, 64 // sm) channel
+# tiles, numbered with the row index fastest; the super-tiles of all groups, in
+# queue (rank) order, are dealt round-robin to 8 queues.  Each queue lists
+# (group, super-tile, first tile) with first tiles as a running sum of the
+# super-tiles' tile counts.
+
+
+def _super_dims(mt: int, nt: int):
+    sm = min(mt, 8)
+    sn = min(nt, 64 // max(sm, 1))
+    return sm, sn, -(-mt // sm), -(-nt // sn)
+
+
+def xcd_queues(plan, order, n_queues: int = 8):
+    """Expected queue entries [(group, super-tile, first tile)] and tile totals."""
+    queues = [[] for _ in range(n_queues)]
+    totals = [0] * n_queues
+    u = 0
+    for g in order:
+        mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"])
+        sm, sn, nsm, nsn = _super_dims(mt, nt)
+        for s in range(nsm * nsn):
+            smi, sni = s % nsm, s // nsm
+            size = min(sm, mt - smi * sm) * min(sn, nt - sni * sn)
+            x = u % n_queues
+            queues[x].append((g, s, totals[x]))
+            totals[x] += size
+            u += 1
+    return queues, totals

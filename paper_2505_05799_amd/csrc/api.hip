@@ -117,7 +117,8 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.inv = take(4 * P);
   L.chunk_counts = take(4 * nchunks * bi.E);
   L.chunk_bad = take(4 * nchunks);
-  L.plan = take(4 * (size_t)plan_ints(bi.G));
+  L.qcap = plan_queue_cap((int64_t)T * bi.k + (int64_t)bi.nsh * T, bi.G, std::max(std::max(bi.F, bi.Fsh), bi.H));
+  L.plan = take(4 * (size_t)plan_layout(bi.G, L.qcap).total);
   L.down_qmax = take(4 * (size_t)bi.G);
   L.xq8 = L.xs8 = L.xq4 = L.xs4 = kNone;
   if (bi.any_x8) { L.xq8 = take((size_t)T * bi.H); L.xs8 = take(4 * (size_t)T); }
@@ -225,11 +226,12 @@ mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32
 
 // -------------------------------------------------------- single linear
 namespace {
-struct LinWs { size_t plan, aq, as, total; };
-LinWs lin_layout(int kd, int m, int k) {
+struct LinWs { size_t plan, aq, as, total; int qcap; };
+LinWs lin_layout(int kd, int m, int n, int k) {
   LinWs w;
   size_t o = 0;
-  w.plan = o; o = align256(o + 4 * (size_t)plan_ints(1));
+  w.qcap = plan_queue_cap(m, 1, n);
+  w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap).total);
   w.aq = w.as = kNone;
   if (kind_is_int(kd)) {
     w.aq = o; o = align256(o + (size_t)m * k);
@@ -243,7 +245,7 @@ LinWs lin_layout(int kd, int m, int k) {
 size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m) {
   int kd;
   if (m < 0 || check_linear(L, &kd) != MXMOE_OK) return 0;
-  return lin_layout(kd, m, L->k).total;
+  return lin_layout(kd, m, L->n, L->k).total;
 }
 
 mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed, int32_t m,
@@ -257,7 +259,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   if (!packed || !a || !out || !workspace) return MXMOE_ERR_INVALID_ARG;
   if (!aligned(packed, 256) || !aligned(a, 16) || !aligned(out, 16) || !aligned(workspace, 256))
     return MXMOE_ERR_INVALID_ARG;
-  const LinWs w = lin_layout(kd, m, L->k);
+  const LinWs w = lin_layout(kd, m, L->n, L->k);
   if (workspace_bytes < w.total) return MXMOE_ERR_WORKSPACE;
   DevLinear dl;
   dl.packed = reinterpret_cast<const uint8_t*>(packed);
@@ -277,6 +279,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   ga.E_routed = 1;
   ga.raw_lin = dl;
   ga.raw_out = out;
+  ga.qcap = w.qcap;
   if (kind_is_int(kd)) {
     int8_t* aq = at<int8_t>(workspace, w.aq);
     float* as = at<float>(workspace, w.as);
@@ -284,7 +287,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
   }
-  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, m, dl, nullptr, ga.plan, nullptr, stream);
+  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, m, dl, nullptr, ga.plan, w.qcap, nullptr, stream);
   if (e != hipSuccess) return MXMOE_ERR_HIP;
   return hip_status(launch_group_gemm(ga, 2, group_gemm_grid(current_device()), stream));
 }
@@ -352,6 +355,7 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->hs_shared = L.hs_shared;
   out->slots = L.slots;
   out->total = L.total;
+  out->plan_queue_cap = (size_t)L.qcap;
   return MXMOE_OK;
 }
 
@@ -404,7 +408,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
                         at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
   memset(&none, 0, sizeof(none));
-  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, -1, none, mask, plan, down_qmax, stream));
+  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, -1, none, mask, plan, L.qcap, down_qmax, stream));
   if (bi.any_x8)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
                               stream));
@@ -437,6 +441,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.G = bi.G;
   ga.E_routed = bi.E;
   ga.n_shared = bi.nsh;
+  ga.qcap = L.qcap;
   const int grid = group_gemm_grid(current_device());
   MX_EVENT(1);
   MX_EVENT(2);

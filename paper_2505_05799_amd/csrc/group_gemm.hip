@@ -1,22 +1,72 @@
 // Tile plan of the mixed-precision Group-GEMM and the launch dispatch (the
 // micro-kernels themselves are in group_gemm_impl.h, one translation unit per
 // activation dtype and phase).
+//
+// plan_kernel (one workgroup, no host round trip):
+//   1. per (phase, expert) group: rows m (routing counts, T for shared experts),
+//      tile configuration from m, tile counts, a static per-tile cost;
+//   2. rank the groups by decreasing tile cost (ties: lower expert first) - the
+//      greedy longest-tile-first order of the paper's tile schedule;
+//   3. cut every group into super-tiles (up to 64 tiles that share row and
+//      channel blocks) and deal them round-robin, in rank order, to one queue
+//      per XCD; per-queue prefix sums give each entry's first tile.
 #include "group_gemm_impl.h"
 
 namespace mxmoe {
 namespace {
 
-// ---------------------------------------------------------------- plan
 struct MaskBits { uint32_t w[64]; };
+
+// In-place exclusive scan of n ints v[0], v[stride], ... by one workgroup
+// (chunk sums per thread, wavefront prefix sums, then wavefront totals);
+// returns the sum.  red: LDS scratch of blockDim/64 + 1 ints.
+__device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
+  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, w = tid >> 6, nw = nt >> 6;
+  const int per = (n + nt - 1) / nt;
+  const int lo = tid * per, hi = min(n, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += v[(int64_t)i * stride];
+  int incl = s;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int t = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += t;
+  }
+  if (lane == 63) red[w] = incl;
+  __syncthreads();
+  if (tid == 0) {
+    int run = 0;
+    for (int i = 0; i < nw; ++i) {
+      const int t = red[i];
+      red[i] = run;
+      run += t;
+    }
+    red[nw] = run;
+  }
+  __syncthreads();
+  int run = red[w] + incl - s;
+  for (int i = lo; i < hi; ++i) {
+    const int t = v[(int64_t)i * stride];
+    v[(int64_t)i * stride] = run;
+    run += t;
+  }
+  const int total = red[nw];
+  __syncthreads();
+  return total;
+}
 
 __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict__ experts, int E, int G, int T,
                                                     const int32_t* __restrict__ counts, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
-                                                    int32_t* __restrict__ down_qmax) {
+                                                    int qcap, int32_t* __restrict__ down_qmax) {
   __shared__ int32_t s_cost[2][2048];
   __shared__ int32_t s_tiles[2][2048];
+  __shared__ int32_t s_red[1025];
+  __shared__ int32_t s_ns[2048];
   const int tid = threadIdx.x;
   const int nphase = raw_m >= 0 ? 1 : 2;
+  const PlanLayout PL = plan_layout(G, qcap);
+  int32_t* misc = plan + PL.misc;
+  if (tid == 0) misc[4] = 0;
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
@@ -38,20 +88,21 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
       double c = t_mem > t_mma ? t_mem : t_mma;
       if (c > 2.0e9) c = 2.0e9;
-      int32_t* r = plan + ((int64_t)ph * G + g) * PF_N;
+      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
       r[PF_EXPERT] = g;
       r[PF_M] = m;
       r[PF_CFG] = cfg;
       r[PF_MTILES] = mt;
       r[PF_NTILES] = nt;
       r[PF_COST] = tiles ? (int32_t)c : 0;
+      r[PF_START] = 0;
       s_cost[ph][g] = tiles ? (int32_t)c : 0;
       s_tiles[ph][g] = tiles;
       if (ph == 0 && raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
     }
   }
   __syncthreads();
-  int32_t* order = plan + 2LL * G * PF_N;
+  int32_t* order = plan + PL.order;
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       int rank = -1;
@@ -65,47 +116,82 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
         }
         order[(int64_t)ph * G + rank] = g;
       }
-      plan[((int64_t)ph * G + g) * PF_N + PF_RANK] = rank;
+      plan[PL.rec + ((int64_t)ph * G + g) * PF_N + PF_RANK] = rank;
     }
   }
   __syncthreads();
-  if (tid < nphase) {
-    const int ph = tid;
-    int run = 0, ng = 0;
-    for (int g = 0; g < G; ++g) ng += s_tiles[ph][g] > 0;
-    for (int r = 0; r < ng; ++r) {
-      const int g = order[(int64_t)ph * G + r];
-      plan[((int64_t)ph * G + g) * PF_N + PF_START] = run;
-      run += s_tiles[ph][g];
+  for (int ph = 0; ph < nphase; ++ph) {
+    int ng = 0;
+    for (int g = 0; g < G; ++g) ng += s_tiles[ph][g] > 0;  // same value in every thread
+    for (int r = ng + tid; r < G; r += blockDim.x) order[(int64_t)ph * G + r] = -1;
+    for (int r = tid; r < ng; r += blockDim.x) {
+      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + order[(int64_t)ph * G + r]) * PF_N;
+      s_ns[r] = super_tiles(rec[PF_MTILES], rec[PF_NTILES]);
     }
-    for (int r = ng; r < G; ++r) order[(int64_t)ph * G + r] = -1;
-    int32_t* ctr = plan + 2LL * G * PF_N + 2LL * G;
-    ctr[PC_HEAD0 + ph] = 0;
-    ctr[PC_TOTAL0 + ph] = run;
-    ctr[4 + ph] = ng;
+    __syncthreads();
+    const int S = block_scan(s_ns, ng, s_red);  // s_ns[r]: first global super-tile of rank r
+    int32_t* ent = plan + PL.ent + (int64_t)ph * kXcd * qcap * 3;
+    // deal super-tile u to queue u % kXcd, position u / kXcd
+    for (int u = tid; u < S; u += blockDim.x) {
+      int lo = 0, hi = ng;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_ns[mid] <= u) lo = mid; else hi = mid;
+      }
+      const int g = order[(int64_t)ph * G + lo];
+      const int s = u - s_ns[lo];
+      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+      if (u / kXcd >= qcap) {  // cannot happen with the host's capacity bound
+        misc[4] = 1;
+        continue;
+      }
+      int32_t* e = ent + ((int64_t)(u % kXcd) * qcap + u / kXcd) * 3;
+      e[0] = g;
+      e[1] = s;
+      e[2] = super_tile_size(rec[PF_MTILES], rec[PF_NTILES], s);
+    }
+    __syncthreads();
+    int32_t* ctr = plan + PL.ctr + (int64_t)ph * kXcd * 4;
+    for (int x = 0; x < kXcd; ++x) {
+      int n = S / kXcd + (x < S % kXcd ? 1 : 0);
+      n = n < qcap ? n : qcap;
+      const int total = block_scan(ent + (int64_t)x * qcap * 3 + 2, n, s_red, 3);
+      if (tid == 0) {
+        ctr[x * 4 + 0] = 0;
+        ctr[x * 4 + 1] = total;
+        ctr[x * 4 + 2] = n;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) misc[2 + ph] = ng;
+    __syncthreads();
   }
-  if (nphase == 1 && tid == 1) {
-    int32_t* ctr = plan + 2LL * G * PF_N + 2LL * G;
-    ctr[PC_HEAD1] = 0;
-    ctr[PC_TOTAL1] = 0;
-    ctr[5] = 0;
+  if (nphase == 1) {  // single-linear mode: the second phase is empty
+    int32_t* ctr = plan + PL.ctr + (int64_t)kXcd * 4;
+    if (tid < kXcd) {
+      ctr[tid * 4 + 0] = 0;
+      ctr[tid * 4 + 1] = 0;
+      ctr[tid * 4 + 2] = 0;
+    }
+    if (tid == 0) misc[3] = 0;
   }
 }
 
 }  // namespace
 
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts, int raw_m,
-                       const DevLinear& raw_lin, const uint32_t* mask_words, int32_t* plan, int32_t* down_qmax,
-                       hipStream_t s) {
+                       const DevLinear& raw_lin, const uint32_t* mask_words, int32_t* plan, int qcap,
+                       int32_t* down_qmax, hipStream_t s) {
   MaskBits mb;
   for (int i = 0; i < 64; ++i) mb.w[i] = mask_words ? mask_words[i] : 0xffffffffu;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, raw_m, raw_lin, mb, plan,
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, raw_m, raw_lin, mb, plan, qcap,
                      down_qmax);
   return hipGetLastError();
 }
 
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s) {
-  if (a.act == MXMOE_BF16) return phase == 0 ? gg_bf16_p0(a, grid, s) : (phase == 1 ? gg_bf16_p1(a, grid, s) : gg_bf16_raw(a, grid, s));
+  if (a.act == MXMOE_BF16)
+    return phase == 0 ? gg_bf16_p0(a, grid, s) : (phase == 1 ? gg_bf16_p1(a, grid, s) : gg_bf16_raw(a, grid, s));
   return phase == 0 ? gg_f16_p0(a, grid, s) : (phase == 1 ? gg_f16_p1(a, grid, s) : gg_f16_raw(a, grid, s));
 }
 
@@ -115,7 +201,7 @@ int group_gemm_grid(int device) {
   if (!cached[device]) {
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || cus <= 0) cus = 256;
-    cached[device] = cus * 2;
+    cached[device] = cus * 2;  // two resident workgroups per CU
   }
   return cached[device];
 }

@@ -79,6 +79,38 @@ __host__ __device__ inline int pick_cfg(int m) {
   return m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
 }
 
+// Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
+// (sm = min(mt, 8), sn = min(nt, 64 / sm)), nsm x nsn super-tiles, super-tile
+// s at (s % nsm, s / nsm); inside, tile t at (t % em, t / em).
+struct SuperDims { int sm, sn, nsm, nsn; };
+__host__ __device__ inline SuperDims super_dims(int mt, int nt) {
+  SuperDims d;
+  d.sm = mt < 8 ? mt : 8;
+  const int cap = kSuperTiles / (d.sm > 0 ? d.sm : 1);
+  d.sn = nt < cap ? nt : cap;
+  d.nsm = d.sm ? (mt + d.sm - 1) / d.sm : 0;
+  d.nsn = d.sn ? (nt + d.sn - 1) / d.sn : 0;
+  return d;
+}
+__host__ __device__ inline int super_tiles(int mt, int nt) {
+  if (mt <= 0 || nt <= 0) return 0;
+  const SuperDims d = super_dims(mt, nt);
+  return d.nsm * d.nsn;
+}
+__host__ __device__ inline int super_tile_size(int mt, int nt, int s) {
+  const SuperDims d = super_dims(mt, nt);
+  const int smi = s % d.nsm, sni = s / d.nsm;
+  const int em = min(d.sm, mt - smi * d.sm), en = min(d.sn, nt - sni * d.sn);
+  return em * en;
+}
+__host__ __device__ inline void super_tile_pos(int mt, int nt, int s, int t, int* mi, int* ni) {
+  const SuperDims d = super_dims(mt, nt);
+  const int smi = s % d.nsm, sni = s / d.nsm;
+  const int em = min(d.sm, mt - smi * d.sm);
+  *mi = smi * d.sm + t % em;
+  *ni = sni * d.sn + t / em;
+}
+
 // ---------------------------------------------------------- MFMA helpers
 template <int ACT> __device__ inline f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
   if constexpr (ACT == MXMOE_BF16)
@@ -114,24 +146,32 @@ template <int KD> struct Raw { u32x4 d[1]; };
 template <> struct Raw<K_W2G> { u32x2 d; };
 template <> struct Raw<K_W3G> { uint32_t d[3]; };
 
+// loads through the global address space (the pointers come from the block
+// table, so the compiler cannot infer it and would emit flat loads)
+template <typename V> __device__ inline V gload(const void* p) {
+  typedef __attribute__((address_space(1))) const V GV;
+  return *(GV*)p;
+}
+
 template <int KD> __device__ inline void load_raw(Raw<KD>& r, const uint8_t* p) {
   if constexpr (KD == K_W2G) {
-    r.d = *reinterpret_cast<const u32x2*>(p);
-  } else if constexpr (KD == K_W3G) {
-    const uint32_t* q = reinterpret_cast<const uint32_t*>(p);  // 12-byte lanes: 4-byte aligned
-    r.d[0] = q[0]; r.d[1] = q[1]; r.d[2] = q[2];
+    r.d = gload<u32x2>(p);
+  } else if constexpr (KD == K_W3G) {  // 12-byte lanes: 4-byte aligned
+    r.d[0] = gload<uint32_t>(p);
+    r.d[1] = gload<uint32_t>(p + 4);
+    r.d[2] = gload<uint32_t>(p + 8);
   } else if constexpr (!streamed<KD>()) {
-    r.d[0] = *reinterpret_cast<const u32x4*>(p);
+    r.d[0] = gload<u32x4>(p);
   }
 }
 
 // streamed kinds: the lane's bytes of MFMA step j
 template <int KD> __device__ inline u32x4 load_step(const uint8_t* p, int j) {
   if constexpr (KD == K_W8G) {
-    const u32x2 v = *reinterpret_cast<const u32x2*>(p + 8 * j);
+    const u32x2 v = gload<u32x2>(p + 8 * j);
     return u32x4{v[0], v[1], 0u, 0u};
   } else {
-    return *reinterpret_cast<const u32x4*>(p + 16 * j);
+    return gload<u32x4>(p + 16 * j);
   }
 }
 
@@ -204,7 +244,7 @@ struct __align__(16) Smem {
   uint8_t act[2][STAGE_BYTES];   // activation rows of the tile, one 128-wide k block per stage
   float rsum[2][BM_MAX];         // per-row sums of a stage (bf16 weight-only kinds)
   int32_t rowsrc[BM_MAX];        // activation row index of every tile row
-  int32_t tile;
+  int32_t tile, tidx;            // popped queue and tile index
 };
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -212,19 +252,39 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // Stage one k block of BM rows into act[buf] with direct global->LDS loads.
 // 16-bit rows are 256 bytes (16 chunks, chunk c stored at c ^ (r & 15)), int8
 // rows 128 bytes (8 chunks, chunk c stored at c ^ ((r >> 1) & 7)); one
-// wavefront instruction fills 1 KB (4 or 8 rows).
+// wavefront instruction fills 1 KB (4 or 8 rows).  Wavefront w fills blocks
+// w, w + 4, ...; its lanes' source offsets (row start + swizzled chunk, at k
+// block 0) are computed once per tile.
+template <bool INT, int BM> struct StageOffs {
+  static constexpr int RB = INT ? 128 : 256;
+  static constexpr int NBLK = BM * RB / 1024;
+  static constexpr int PER_WAVE = (NBLK + 3) / 4;
+  uint32_t off[PER_WAVE];
+};
+
 template <bool INT, int BM>
-__device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, int64_t row_bytes, int kb, int tid) {
-  constexpr int RB = INT ? 128 : 256;
-  constexpr int ROWS_PER_BLK = 1024 / RB;
-  constexpr int NBLK = BM * RB / 1024;
-  const int wave = tid >> 6, lane = tid & 63;
-  for (int blk = wave; blk < NBLK; blk += 4) {
-    const int r = blk * ROWS_PER_BLK + lane / (RB / 16);
-    const int p = lane % (RB / 16);
+__device__ inline void stage_offsets(StageOffs<INT, BM>& so, const Smem& sm, int64_t row_bytes, int wave, int lane) {
+  using S = StageOffs<INT, BM>;
+#pragma unroll
+  for (int i = 0; i < S::PER_WAVE; ++i) {
+    const int blk = wave + 4 * i;
+    const int r = (blk < S::NBLK ? blk : 0) * (1024 / S::RB) + lane / (S::RB / 16);
+    const int p = lane % (S::RB / 16);
     const int cc = INT ? (p ^ ((r >> 1) & 7)) : (p ^ (r & 15));
-    const uint8_t* src = base + (int64_t)sm.rowsrc[r] * row_bytes + (int64_t)kb * RB + cc * 16;
-    __builtin_amdgcn_global_load_lds((const void*)src, (lds_ptr_t)(sm.act[buf] + blk * 1024), 16, 0, 0);
+    so.off[i] = (uint32_t)((int64_t)sm.rowsrc[r] * row_bytes + cc * 16);
+  }
+}
+
+template <bool INT, int BM>
+__device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<INT, BM>& so, int kb,
+                                  int wave) {
+  using S = StageOffs<INT, BM>;
+  const uint8_t* bk = base + (int64_t)kb * S::RB;  // uniform
+#pragma unroll
+  for (int i = 0; i < S::PER_WAVE; ++i) {
+    const int blk = wave + 4 * i;
+    if (blk < S::NBLK)
+      __builtin_amdgcn_global_load_lds((const void*)(bk + so.off[i]), (lds_ptr_t)(sm.act[buf] + blk * 1024), 16, 0, 0);
   }
 }
 
@@ -236,7 +296,7 @@ template <bool INT> __device__ inline u32x4 act_frag(const Smem& sm, int buf, in
 // Row sums of a 16-bit stage: MFMA of each 16-row fragment against ones; the
 // fragments are shared out over the wavefronts.
 template <int ACT, int MF> __device__ inline void stage_rowsum(Smem& sm, int buf, int tid) {
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int li = lane & 15, q = lane >> 4;
   const u32x4 ones = ACT == MXMOE_BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
                                        : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
@@ -268,7 +328,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // letting the persistent loop hoist them for every micro-kernel at once.
   int tid = threadIdx.x;
   asm volatile("" : "+v"(tid));
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;  // wave index is uniform
   const int li = lane & 15, q = lane >> 4;
   const bool shared = g >= a.E_routed;
   const DevLinear* lins[NL];
@@ -305,6 +365,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
   const int64_t row_bytes = (int64_t)K * (INT ? 1 : 2);
   __syncthreads();
+  StageOffs<INT, BM> soffs;
+  stage_offsets<INT, BM>(soffs, sm, row_bytes, wave, lane);
 
   // ---- accumulators and weight streams
   typedef typename std::conditional<INT, i32x4, f32x4>::type AccT;
@@ -322,12 +384,16 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
       for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = AccT{0, 0, 0, 0};
 
+  // Uniform base of every fragment's block stream (fragments past the last
+  // channel block read block 0 and are never stored) and the lane's offset.
   const uint8_t* wp[NL][NF];
 #pragma unroll
   for (int l = 0; l < NL; ++l)
 #pragma unroll
     for (int nf = 0; nf < NF; ++nf)
-      wp[l][nf] = lins[l]->packed + (int64_t)(nb0 + (nf < nvalid ? nf : 0)) * kblocks * BB + lane * LB;
+      wp[l][nf] = lins[l]->packed + (int64_t)(nf < nvalid ? nb0 + nf : 0) * kblocks * BB;
+  const uint32_t loff = (uint32_t)lane * LB;
+  const uint32_t moff = 64u * LB + 4u * li;  // this lane's channel in the group metadata
 
   Raw<KD> raw[NL][NF];   // low-bit kinds: next group, prefetched a group ahead
   u32x4 st[NL][NF];      // streamed kinds: next MFMA step, prefetched a step ahead
@@ -337,41 +403,37 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
-      for (int nf = 0; nf < NF; ++nf)
-        if (nf < nvalid) {
-          const uint8_t* blk = wp[l][nf] + (int64_t)kb * BB;
-          load_raw<KD>(raw[l][nf], blk);
-          if constexpr (WONLY) meta[l][nf] = reinterpret_cast<const uint32_t*>(blk - lane * LB + 64 * LB)[li];
-        }
+      for (int nf = 0; nf < NF; ++nf) {
+        const uint8_t* blk = wp[l][nf] + (int64_t)kb * BB;  // uniform
+        load_raw<KD>(raw[l][nf], blk + loff);
+        if constexpr (WONLY) meta[l][nf] = gload<uint32_t>(blk + moff);
+      }
   };
   auto load_meta = [&](int kb) {
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
-      for (int nf = 0; nf < NF; ++nf)
-        if (nf < nvalid) meta[l][nf] = reinterpret_cast<const uint32_t*>(wp[l][nf] + (int64_t)kb * BB - lane * LB + 64 * LB)[li];
+      for (int nf = 0; nf < NF; ++nf) meta[l][nf] = gload<uint32_t>(wp[l][nf] + (int64_t)kb * BB + moff);
   };
   // dword `w` of every fragment's next group (SPLIT kinds)
   auto load_dword = [&](int kb, int w) {
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
-      for (int nf = 0; nf < NF; ++nf)
-        if (nf < nvalid) {
-          const uint32_t v = reinterpret_cast<const uint32_t*>(wp[l][nf] + (int64_t)kb * BB)[w];
-          if constexpr (KD == K_W4G) raw[l][nf].d[0][w] = v;
-          else if constexpr (KD == K_W3G) raw[l][nf].d[w] = v;
-        }
+      for (int nf = 0; nf < NF; ++nf) {
+        const uint32_t v = gload<uint32_t>(wp[l][nf] + (int64_t)kb * BB + loff + 4 * w);
+        if constexpr (KD == K_W4G) raw[l][nf].d[0][w] = v;
+        else if constexpr (KD == K_W3G) raw[l][nf].d[w] = v;
+      }
   };
   auto load_steps = [&](int kb, int j) {
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
-      for (int nf = 0; nf < NF; ++nf)
-        if (nf < nvalid) st[l][nf] = load_step<KD>(wp[l][nf] + (int64_t)kb * BB, j);
+      for (int nf = 0; nf < NF; ++nf) st[l][nf] = load_step<KD>(wp[l][nf] + (int64_t)kb * BB + loff, j);
   };
 
-  stage_load<INT, BM>(sm, 0, abase, row_bytes, 0, tid);
+  stage_load<INT, BM>(sm, 0, abase, soffs, 0, wave);
   load_group(0);
   if constexpr (streamed<KD>()) load_steps(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
@@ -384,7 +446,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   for (int kb = 0; kb < kblocks; ++kb) {
     const int cur = kb & 1;
     const bool more = kb + 1 < kblocks;
-    if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, row_bytes, kb + 1, tid);
+    if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
     Raw<KD> rw[NL][NF];
     uint32_t hi3[NL][NF];  // SPLIT w3g: hi-bit plane of the current group
     uint32_t bz[NL][NF];
@@ -470,8 +532,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
           for (int l = 0; l < NL; ++l)
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf)
-              if (nf < nvalid) acc[l][nf][mf] = mma(af, wf[l][nf], acc[l][nf][mf]);
+            for (int nf = 0; nf < NF; ++nf) acc[l][nf][mf] = mma(af, wf[l][nf], acc[l][nf][mf]);
         }
       } else {
         OpT af[MF];
@@ -481,11 +542,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int l = 0; l < NL; ++l)
 #pragma unroll
           for (int nf = 0; nf < NF; ++nf) {
-            if (nf < nvalid) {
-              const OpT wf = wop(l, nf);
+            const OpT wf = wop(l, nf);
 #pragma unroll
-              for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = mma(af[mf], wf, acc[l][nf][mf]);
-            }
+            for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = mma(af[mf], wf, acc[l][nf][mf]);
           }
       }
     }
@@ -590,28 +649,49 @@ __global__ void __launch_bounds__(kThreads, 2) group_gemm_kernel(GemmArgs a) {
   __shared__ Smem sm;
   const int G = a.G;
   const int pidx = PHASE == kPhaseRaw ? 0 : PHASE;
-  const int32_t* rec = a.plan + (int64_t)pidx * G * PF_N;
-  const int32_t* order = a.plan + 2LL * G * PF_N + (int64_t)pidx * G;
-  int32_t* ctr = a.plan + 2LL * G * PF_N + 2LL * G;
-  const int total = ctr[PC_TOTAL0 + pidx];
-  const int ng = ctr[4 + pidx];
+  const PlanLayout PL = plan_layout(G, a.qcap);
+  const int32_t* rec = a.plan + PL.rec + (int64_t)pidx * G * PF_N;
+  const int32_t* ent = a.plan + PL.ent + (int64_t)pidx * kXcd * a.qcap * 3;
+  int32_t* ctr = a.plan + PL.ctr + (int64_t)pidx * kXcd * 4;
+  // workgroups are dealt round-robin over the XCDs: start with the local queue
+  const int x0 = blockIdx.x % kXcd;
+  int qi = 0;
   for (;;) {
-    if (threadIdx.x == 0) sm.tile = atomicAdd(&ctr[PC_HEAD0 + pidx], 1);
+    if (threadIdx.x == 0) {
+      int found = -1, idx = 0;
+      while (qi < kXcd) {
+        const int x = (x0 + qi) % kXcd;
+        const int total = ctr[x * 4 + 1];
+        const int i = total > 0 ? atomicAdd(&ctr[x * 4], 1) : 0;
+        if (i < total) {
+          found = x;
+          idx = i;
+          break;
+        }
+        ++qi;
+      }
+      sm.tile = found;
+      sm.tidx = idx;
+    }
     __syncthreads();
     // wave-uniform from here on: tile bookkeeping and weight pointers live in SGPRs
-    const int tile = __builtin_amdgcn_readfirstlane(sm.tile);
+    const int x = __builtin_amdgcn_readfirstlane(sm.tile);
+    const int tile = __builtin_amdgcn_readfirstlane(sm.tidx);
     __syncthreads();
-    if (tile >= total) break;
-    int lo = 0, hi = ng;  // largest rank whose first tile <= tile
+    if (x < 0) break;
+    const int32_t* q = ent + (int64_t)x * a.qcap * 3;
+    int lo = 0, hi = __builtin_amdgcn_readfirstlane(ctr[x * 4 + 2]);  // entry with start <= tile
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
-      if (rec[(int64_t)order[mid] * PF_N + PF_START] <= tile) lo = mid; else hi = mid;
+      if (q[mid * 3 + 2] <= tile) lo = mid; else hi = mid;
     }
-    const int g = __builtin_amdgcn_readfirstlane(order[lo]);
+    const int g = __builtin_amdgcn_readfirstlane(q[lo * 3 + 0]);
+    const int s = __builtin_amdgcn_readfirstlane(q[lo * 3 + 1]);
+    const int local = tile - __builtin_amdgcn_readfirstlane(q[lo * 3 + 2]);
     const int32_t* r = rec + (int64_t)g * PF_N;
-    const int local = tile - __builtin_amdgcn_readfirstlane(r[PF_START]);
-    const int mtiles = __builtin_amdgcn_readfirstlane(r[PF_MTILES]);
-    const int mt = local % mtiles, nt = local / mtiles;
+    int mt, nt;
+    super_tile_pos(__builtin_amdgcn_readfirstlane(r[PF_MTILES]), __builtin_amdgcn_readfirstlane(r[PF_NTILES]), s,
+                   local, &mt, &nt);
     const DevExpert* ex = PHASE == kPhaseRaw ? nullptr : a.experts + g;
     const int kd = __builtin_amdgcn_readfirstlane(PHASE == kPhaseRaw ? a.raw_lin.kind : ex->lin[PHASE == 0 ? 0 : 2].kind);
     const int m_g = __builtin_amdgcn_readfirstlane(r[PF_M]);

@@ -96,15 +96,46 @@ enum PlanField : int32_t {
   PF_START = 5, PF_COST = 6, PF_RANK = 7, PF_N = 8
 };
 
-// Plan region layout (int32): [2][G][PF_N] records, [2][G] queue order
-// (group index per rank), [16] counters.
-__host__ __device__ inline int64_t plan_ints(int G) { return 2LL * G * PF_N + 2LL * G + 16; }
-enum PlanCounter : int32_t { PC_HEAD0 = 0, PC_HEAD1 = 1, PC_TOTAL0 = 2, PC_TOTAL1 = 3 };
+// Tiles are grouped into super-tiles of up to 64 tiles sharing row and channel
+// blocks (min(mt, 8) x min(nt, 64 / that) tiles) and dealt round-robin to one
+// queue per XCD, in decreasing tile-cost order of their groups; each queue is
+// drained first by the workgroups resident on that XCD (L2 reuse of the shared
+// weights and activation rows), then by any workgroup.
+constexpr int kXcd = 8;
+constexpr int kSuperTiles = 64;
+
+// Plan region layout (int32), phases p = 0 (gate|up, or the single linear)
+// and 1 (down):
+//   rec   [2][G][PF_N]       group records
+//   order [2][G]             group index per rank (-1 past the last group with tiles)
+//   ent   [2][kXcd][cap][3]  queue entries: group, super-tile index, first tile
+//   ctr   [2][kXcd][4]       per queue: head, total tiles, entries, -
+//   misc  [16]               [2 + p]: number of groups with tiles in phase p
+struct PlanLayout { int64_t rec, order, ent, ctr, misc, total; };
+__host__ __device__ inline PlanLayout plan_layout(int G, int cap) {
+  PlanLayout L;
+  L.rec = 0;
+  L.order = L.rec + 2LL * G * PF_N;
+  L.ent = L.order + 2LL * G;
+  L.ent = (L.ent + 3) & ~3LL;
+  L.ctr = L.ent + 2LL * kXcd * cap * 3;
+  L.misc = L.ctr + 2LL * kXcd * 4;
+  L.total = L.misc + 16;
+  return L;
+}
+// Per-queue capacity bound from the rows and channel counts (host side):
+// super-tiles of a group <= (mt/8 + 1)(nt/8 + 1) with mt <= m/1024*8 + 1,
+// nt <= N/64 + 1 (smallest tiles are 16 x 64 per linear).
+__host__ __device__ inline int plan_queue_cap(int64_t rows_total, int groups, int n_max) {
+  const int64_t s = (rows_total / 1024 + 2LL * groups + 1) * ((int64_t)n_max / 512 + 2);
+  return (int)(s / kXcd + 2);
+}
 
 // Workspace layout (byte offsets), shared by host code of the forward.
 struct WsLayout {
   size_t status, counts, offsets, sorted_pair, inv, chunk_counts, chunk_bad, plan, down_qmax;
   size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
+  int qcap;  // XCD queue capacity of the tile plan
 };
 
 constexpr int kRouteChunk = 2048;  // pairs per routing workgroup
@@ -149,6 +180,7 @@ struct GemmArgs {
   int32_t G;          // experts incl. shared
   int32_t E_routed;
   int32_t n_shared;
+  int32_t qcap;        // capacity of each XCD queue in the plan region
   // single-linear mode (mxmoe_linear_forward): raw int32 / fp32 output
   DevLinear raw_lin;
   void* raw_out;
@@ -158,7 +190,7 @@ struct GemmArgs {
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int32_t* down_qmax, hipStream_t s);
+                       int32_t* plan, int qcap, int32_t* down_qmax, hipStream_t s);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

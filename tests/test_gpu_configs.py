@@ -32,6 +32,13 @@ def sample_tokens(blk, n_random=10, seed=0):
     return np.array(sorted(picks))
 
 
+def plan_misc(mb, T, G, cap):
+    torch = torch_mod()
+    o_ctr = ((2 * G * 8 + 2 * G + 3) & ~3) + 2 * 8 * cap * 3
+    p = mb.ws_view("plan", torch.int32, o_ctr + 64 + 16, T).cpu().numpy()
+    return p[o_ctr + 64: o_ctr + 80]
+
+
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", NAMES)
 def test_full_workload(name):
@@ -55,8 +62,13 @@ def test_full_workload(name):
     assert np.array_equal(mb.ws_view("inv", torch.int32, T * k, T).cpu().numpy(), r["inv"])
     assert int(mb.ws_view("status", torch.int32, 1, T).cpu().numpy()[0]) == 0
 
-    # tile plan, bit-exact (configuration, tile counts, cost, queue rank, first tile)
-    plan = mb.ws_view("plan", torch.int32, 2 * G * 8 + 2 * G + 16, T).cpu().numpy()
+    # tile plan, bit-exact: configuration, tile counts, cost, rank, queue order,
+    # and the per-XCD queues of super-tiles
+    cap = mb.workspace_layout(T)["plan_queue_cap"]
+    o_ord = 2 * G * 8
+    o_ent = (o_ord + 2 * G + 3) & ~3
+    o_ctr = o_ent + 2 * 8 * cap * 3
+    plan = mb.ws_view("plan", torch.int32, o_ctr + 2 * 8 * 4, T).cpu().numpy()
     rec = plan[: 2 * G * 8].reshape(2, G, 8)
     ms = list(r["counts"]) + [T] * cfg.n_shared
     for phase in (0, 1):
@@ -67,10 +79,16 @@ def test_full_workload(name):
             assert got[1] == ms[g] and got[2] == want[g]["cfg"], (phase, g)
             assert got[3] == want[g]["mtiles"] and got[4] == want[g]["ntiles"], (phase, g)
             assert got[6] == want[g]["cost"] and got[7] == want[g]["rank"], (phase, g)
-            if want[g]["tiles"]:
-                assert got[5] == want[g]["start"], (phase, g)
-        q = plan[2 * G * 8 + phase * G: 2 * G * 8 + (phase + 1) * G]
+        q = plan[o_ord + phase * G: o_ord + (phase + 1) * G]
         assert q[: len(order)].tolist() == order
+        queues, totals = O.xcd_queues(want, order)
+        ent = plan[o_ent + phase * 8 * cap * 3: o_ent + (phase + 1) * 8 * cap * 3].reshape(8, cap, 3)
+        ctr = plan[o_ctr + phase * 32: o_ctr + (phase + 1) * 32].reshape(8, 4)
+        for x in range(8):
+            assert ctr[x, 1] == totals[x] and ctr[x, 2] == len(queues[x]), (phase, x)
+            assert [tuple(e) for e in ent[x, : len(queues[x])].tolist()] == queues[x], (phase, x)
+        assert sum(totals) == sum(w["tiles"] for w in want)
+    assert plan_misc(mb, T, G, cap)[4] == 0      # no queue overflow
 
     # block output on sampled tokens
     sel = sample_tokens(blk)
