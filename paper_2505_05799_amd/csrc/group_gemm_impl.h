@@ -175,6 +175,19 @@ template <int KD> __device__ inline u32x4 load_step(const uint8_t* p, int j) {
   }
 }
 
+// Wait until at most N vector-memory loads of this wavefront are outstanding
+// (loads complete in issue order), leaving LDS and export counters alone.
+template <int N> __device__ inline void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier for LDS hand-offs inside the k loop: waits for this
+// wavefront's LDS operations only.  __syncthreads() carries a fence that also
+// drains every outstanding global load, which would stall the weight prefetch;
+// the direct-to-LDS stage loads are covered by wait_vmem before this barrier.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // bias constant b = 2^N - 1 of the exact magic-number dequantization
 template <int KD> constexpr int wbias() { return KD == K_W2G ? 3 : (KD == K_W3G ? 7 : 15); }
 
@@ -275,16 +288,30 @@ __device__ inline void stage_offsets(StageOffs<INT, BM>& so, const Smem& sm, int
   }
 }
 
+// One direct global->LDS load of 16 bytes per lane: lane l's bytes at
+// base + voff land at LDS address m0 + 16 l.  Issued through inline assembly
+// so that the compiler's wait-counter pass does not treat every later LDS read
+// as a possible reader of this stage (it would drain all outstanding global
+// loads, weight prefetch included, before the first one); completion is
+// waited for explicitly (wait_vmem) before the barrier that publishes the
+// stage.
+__device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "memory", "m0");
+}
+
 template <bool INT, int BM>
 __device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<INT, BM>& so, int kb,
                                   int wave) {
   using S = StageOffs<INT, BM>;
   const uint8_t* bk = base + (int64_t)kb * S::RB;  // uniform
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)sm.act[buf]);
 #pragma unroll
   for (int i = 0; i < S::PER_WAVE; ++i) {
     const int blk = wave + 4 * i;
-    if (blk < S::NBLK)
-      __builtin_amdgcn_global_load_lds((const void*)(bk + so.off[i]), (lds_ptr_t)(sm.act[buf] + blk * 1024), 16, 0, 0);
+    if (blk < S::NBLK) lds_dma16(bk, so.off[i], __builtin_amdgcn_readfirstlane(lds0 + blk * 1024));
   }
 }
 
@@ -373,9 +400,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
   constexpr int J = INT ? 2 : 4;                 // MFMA steps per 128-wide k block
   constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
-  // 3/4-bit codes in the 128-row tiles: the next group is fetched dword by dword
-  // into registers whose codes have been consumed (no second copy of the group)
-  constexpr bool SPLIT = false;
   AccT acc[NL][NF][MF];
 #pragma unroll
   for (int l = 0; l < NL; ++l)
@@ -396,46 +420,44 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const uint32_t moff = 64u * LB + 4u * li;  // this lane's channel in the group metadata
 
   Raw<KD> raw[NL][NF];   // low-bit kinds: next group, prefetched a group ahead
-  u32x4 st[NL][NF];      // streamed kinds: next MFMA step, prefetched a step ahead
+  u32x4 st[J][NL][NF];   // streamed kinds: step j of the k block, reloaded one block ahead
   uint32_t meta[NL][NF];
   float s_prev[NL][NF];
-  auto load_group = [&](int kb) {
+  // The prefetch of block kn is issued unconditionally: past the last block
+  // (last = true) every lane reads the first 16 bytes of the fragment's block 0
+  // instead (one cache line, result unused), so no register keeps two possible
+  // values across the loop and no copy has to wait for an outstanding load.
+  auto load_group = [&](int kn, bool last) {
+    const uint32_t lo = last ? 0u : loff, mo = last ? 0u : moff;
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
-        const uint8_t* blk = wp[l][nf] + (int64_t)kb * BB;  // uniform
-        load_raw<KD>(raw[l][nf], blk + loff);
-        if constexpr (WONLY) meta[l][nf] = gload<uint32_t>(blk + moff);
+        const uint8_t* blk = wp[l][nf] + (last ? 0 : (int64_t)kn * BB);  // uniform
+        if constexpr (!streamed<KD>()) load_raw<KD>(raw[l][nf], blk + lo);
+        if constexpr (WONLY) meta[l][nf] = gload<uint32_t>(blk + mo);
       }
   };
-  auto load_meta = [&](int kb) {
+  auto load_steps = [&](int kn, bool last, int j) {
+    const uint32_t lo = last ? 0u : loff;
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
-      for (int nf = 0; nf < NF; ++nf) meta[l][nf] = gload<uint32_t>(wp[l][nf] + (int64_t)kb * BB + moff);
+      for (int nf = 0; nf < NF; ++nf)
+        st[j][l][nf] = load_step<KD>(wp[l][nf] + (last ? 0 : (int64_t)kn * BB) + lo, j);
   };
-  // dword `w` of every fragment's next group (SPLIT kinds)
-  auto load_dword = [&](int kb, int w) {
-#pragma unroll
-    for (int l = 0; l < NL; ++l)
-#pragma unroll
-      for (int nf = 0; nf < NF; ++nf) {
-        const uint32_t v = gload<uint32_t>(wp[l][nf] + (int64_t)kb * BB + loff + 4 * w);
-        if constexpr (KD == K_W4G) raw[l][nf].d[0][w] = v;
-        else if constexpr (KD == K_W3G) raw[l][nf].d[w] = v;
-      }
-  };
-  auto load_steps = [&](int kb, int j) {
-#pragma unroll
-    for (int l = 0; l < NL; ++l)
-#pragma unroll
-      for (int nf = 0; nf < NF; ++nf) st[l][nf] = load_step<KD>(wp[l][nf] + (int64_t)kb * BB + loff, j);
-  };
+  // Vector-memory loads issued after the activation stage of the next k block,
+  // at least: one per fragment and step (streamed) or per fragment (group
+  // prefetch), plus one metadata dword per fragment (weight-only).  Waiting for
+  // this many leaves the weight prefetch in flight across the barrier.
+  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : 1) + (WONLY ? NL * NF : 0);
 
   stage_load<INT, BM>(sm, 0, abase, soffs, 0, wave);
-  load_group(0);
-  if constexpr (streamed<KD>()) load_steps(0, 0);
+  load_group(0, false);
+  if constexpr (streamed<KD>()) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) load_steps(0, false, j);
+  }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if constexpr (RSUM) {
@@ -447,16 +469,17 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const int cur = kb & 1;
     const bool more = kb + 1 < kblocks;
     if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
+    // every weight load below is issued after the stage (see wait_vmem)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
     Raw<KD> rw[NL][NF];
-    uint32_t hi3[NL][NF];  // SPLIT w3g: hi-bit plane of the current group
     uint32_t bz[NL][NF];
     float zf[NL][NF];
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
-        if constexpr (!SPLIT) rw[l][nf] = raw[l][nf];
-        if constexpr (SPLIT && KD == K_W3G) hi3[l][nf] = raw[l][nf].d[2];
+        rw[l][nf] = raw[l][nf];
         bz[l][nf] = 0;
         zf[l][nf] = 0.f;
         if constexpr (WONLY) {
@@ -479,31 +502,17 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           }
         }
       }
-    if (more && !streamed<KD>() && !SPLIT) load_group(kb + 1);
-    if (more && (SPLIT || (streamed<KD>() && WONLY))) load_meta(kb + 1);
+    load_group(kb + 1, !more);
+    // keep the prefetch here: the scheduler would otherwise sink it below the
+    // MFMAs, next to its first use
+    __builtin_amdgcn_sched_barrier(0);
 
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      u32x4 sj[NL][NF];
-      if constexpr (streamed<KD>()) {
-#pragma unroll
-        for (int l = 0; l < NL; ++l)
-#pragma unroll
-          for (int nf = 0; nf < NF; ++nf) sj[l][nf] = st[l][nf];
-        if (j + 1 < J) load_steps(kb, j + 1);
-        else if (more) load_steps(kb + 1, 0);
-      }
       auto wop = [&](int l, int nf) -> OpT {
-        const u32x4 sv = streamed<KD>() ? sj[l][nf] : u32x4{0u, 0u, 0u, 0u};
-        Raw<KD> rv;
-        if constexpr (SPLIT) {
-          rv = raw[l][nf];
-          if constexpr (KD == K_W3G) rv.d[2] = hi3[l][nf];
-        } else {
-          rv = rw[l][nf];
-        }
-        if constexpr (INT) return wfrag8<KD>(rv, sv, j);
-        else return wfrag16<KD, ACT>(rv, sv, j, bz[l][nf], zf[l][nf]);
+        const u32x4 sv = streamed<KD>() ? st[j][l][nf] : u32x4{0u, 0u, 0u, 0u};
+        if constexpr (INT) return wfrag8<KD>(rw[l][nf], sv, j);
+        else return wfrag16<KD, ACT>(rw[l][nf], sv, j, bz[l][nf], zf[l][nf]);
       };
       auto aop = [&](int mf) -> OpT {
         return __builtin_bit_cast(OpT, act_frag<INT>(sm, cur, mf * 16 + li, 4 * j + q));
@@ -518,14 +527,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int l = 0; l < NL; ++l)
 #pragma unroll
           for (int nf = 0; nf < NF; ++nf) wf[l][nf] = wop(l, nf);
-        if constexpr (SPLIT) {
-          if (more) {
-            if constexpr (KD == K_W4G) load_dword(kb + 1, j);          // step j's codes are consumed
-            else if (j == 0) load_dword(kb + 1, 2);                     // hi plane was copied
-            else if (j == 1) load_dword(kb + 1, 0);                     // steps 0-1 consumed
-            else if (j == 3) load_dword(kb + 1, 1);                     // steps 2-3 consumed
-          }
-        }
 #pragma unroll
         for (int mf = 0; mf < MF; ++mf) {
           const OpT af = aop(mf);
@@ -547,13 +548,21 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = mma(af[mf], wf, acc[l][nf][mf]);
           }
       }
+      if constexpr (streamed<KD>()) {
+        // step j's registers are free: refill them with step j of the next block
+        load_steps(kb + 1, !more, j);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    // The next stage has landed once no more than the weight prefetch is
+    // outstanding (vector-memory loads complete in issue order).
+    if (more) wait_vmem<kLoadsAfterStage>();
+    else wait_vmem<0>();
+    lds_barrier();
     if constexpr (RSUM) {
       if (more) {
         stage_rowsum<ACT, MF>(sm, cur ^ 1, tid);
-        __syncthreads();
+        lds_barrier();
       }
     }
   }
