@@ -527,13 +527,24 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int l = 0; l < NL; ++l)
 #pragma unroll
           for (int nf = 0; nf < NF; ++nf) wf[l][nf] = wop(l, nf);
+        OpT af[MF];
 #pragma unroll
-        for (int mf = 0; mf < MF; ++mf) {
-          const OpT af = aop(mf);
+        for (int mf = 0; mf < MF; ++mf) af[mf] = aop(mf);
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf)
 #pragma unroll
           for (int l = 0; l < NL; ++l)
 #pragma unroll
-            for (int nf = 0; nf < NF; ++nf) acc[l][nf][mf] = mma(af, wf[l][nf], acc[l][nf][mf]);
+            for (int nf = 0; nf < NF; ++nf) acc[l][nf][mf] = mma(af[mf], wf[l][nf], acc[l][nf][mf]);
+        // Software pipeline of the activation fragments: two LDS reads ahead,
+        // then the MFMAs of one fragment and the read of the fragment two
+        // places further, so an MFMA group never waits for a read issued just
+        // before it.
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
+          if (mf + 2 < MF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
         }
       } else {
         OpT af[MF];
