@@ -125,26 +125,38 @@ __device__ inline float act_to_f32(uint16_t b, int act) {
   if (act == MXMOE_BF16) return __uint_as_float(((uint32_t)b) << 16);
   return (float)__builtin_bit_cast(_Float16, b);
 }
+// fp32 -> activation dtype, round to nearest even (NaN stays NaN)
 template <int ACT> __device__ inline uint16_t f32_to_act(float f) {
-  if constexpr (ACT == MXMOE_BF16) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
-  } else {
+  if constexpr (ACT == MXMOE_BF16)
+    return __builtin_bit_cast(uint16_t, (__bf16)f);
+  else
     return __builtin_bit_cast(uint16_t, (_Float16)f);
-  }
 }
 
-__device__ inline float silu_f32(float g) { return g / (1.0f + expf(-g)); }
+// SiLU(g) = g / (1 + e^-g) with e^-g = 2^t, t = -g log2(e) carried as a rounded
+// product plus its FMA-recovered error (and that of log2(e) itself), so the
+// result is within a few ulp of the exact value; t is capped so that large
+// negative g yields a tiny finite value instead of inf * 0.
+__device__ inline float silu_f32(float g) {
+  const float kL = 1.44269502162933349609375f;      // log2(e) rounded to fp32
+  const float kLlo = 1.925963033500011079e-8f;       // log2(e) - kL
+  float t = -g * kL;
+  const float tl = __builtin_fmaf(-g, kLlo, __builtin_fmaf(-g, kL, -t));
+  t = fminf(t, 126.0f);
+  const float e = __builtin_amdgcn_exp2f(t);
+  const float ex = __builtin_fmaf(e, tl * 0.693147180559945309f, e);
+  return g * __builtin_amdgcn_rcpf(1.0f + ex);
+}
 
 // ------------------------------------------------------- weight operands
-// Low-bit kinds prefetch a whole 128-wide group (8-16 bytes per lane); the wide
-// kinds (w16, w8g, w8a8: 32-64 bytes per lane) stream one MFMA step at a time.
-template <int KD> constexpr bool streamed() { return KD == K_W16 || KD == K_W8G || KD == K_W8A8; }
+// Low-bit kinds and w8a8 prefetch a whole 128-wide k block (8-32 bytes per
+// lane); the 16-bit-operand wide kinds (w16, w8g: 32-64 bytes per lane) stream
+// one MFMA step at a time.
+template <int KD> constexpr bool streamed() { return KD == K_W16 || KD == K_W8G; }
 template <int KD> struct Raw { u32x4 d[1]; };
 template <> struct Raw<K_W2G> { u32x2 d; };
 template <> struct Raw<K_W3G> { uint32_t d[3]; };
+template <> struct Raw<K_W8A8> { u32x4 d[2]; };
 
 // loads through the global address space (the pointers come from the block
 // table, so the compiler cannot infer it and would emit flat loads)
@@ -160,6 +172,9 @@ template <int KD> __device__ inline void load_raw(Raw<KD>& r, const uint8_t* p) 
     r.d[0] = gload<uint32_t>(p);
     r.d[1] = gload<uint32_t>(p + 4);
     r.d[2] = gload<uint32_t>(p + 8);
+  } else if constexpr (KD == K_W8A8) {
+    r.d[0] = gload<u32x4>(p);
+    r.d[1] = gload<u32x4>(p + 16);
   } else if constexpr (!streamed<KD>()) {
     r.d[0] = gload<u32x4>(p);
   }
@@ -240,7 +255,7 @@ __device__ inline u32x4 wfrag16(const Raw<KD>& r, u32x4 step, int j, uint32_t bz
 // int8 weight operand of MFMA step j (16 slots)
 template <int KD> __device__ inline i32x4 wfrag8(const Raw<KD>& r, u32x4 step, int j) {
   if constexpr (KD == K_W8A8) {
-    return __builtin_bit_cast(i32x4, step);
+    return __builtin_bit_cast(i32x4, r.d[j]);
   } else {
     const uint32_t d0 = r.d[0][2 * j], d1 = r.d[0][2 * j + 1];
     i32x4 o;
@@ -257,6 +272,9 @@ struct __align__(16) Smem {
   uint8_t act[2][STAGE_BYTES];   // activation rows of the tile, one 128-wide k block per stage
   float rsum[2][BM_MAX];         // per-row sums of a stage (bf16 weight-only kinds)
   int32_t rowsrc[BM_MAX];        // activation row index of every tile row
+  int32_t rowout[BM_MAX];        // output row index of every tile row, -1 past the group's rows
+  float rowscale[BM_MAX];        // per-token activation scale (a8/a4), else 1
+  float rowgw[BM_MAX];           // router gate weight of the row's (token, slot) (down phase), else 1
   int32_t tile, tidx;            // popped queue and tile index
 };
 
@@ -370,16 +388,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   nvalid = nvalid < 0 ? 0 : (nvalid > NF ? NF : nvalid);
   const int off_e = (!shared && PHASE != kPhaseRaw) ? a.offsets[g] : 0;
 
-  // ---- activation source rows
-  if (tid < BM) {
-    int m = row0 + tid;
-    if (m >= m_g) m = m_g - 1;
-    int src;
-    if constexpr (PHASE == 0) src = shared ? m : a.sorted_pair[off_e + m] / a.k;
-    else if constexpr (PHASE == 1) src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
-    else src = m;
-    sm.rowsrc[tid] = src;
-  }
   const uint8_t* abase;
   const float* ascale = nullptr;
   if constexpr (INT) {
@@ -389,6 +397,35 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     abase = reinterpret_cast<const uint8_t*>(qb);
   } else {
     abase = reinterpret_cast<const uint8_t*>(PHASE == 1 ? (shared ? a.h_shared : a.h) : a.x);
+  }
+
+  // ---- per-row data: activation source row (rows past the group repeat its
+  // last row), output row, activation scale, router gate weight
+  if (tid < BM) {
+    const int m0 = row0 + tid;
+    const int m = m0 < m_g ? m0 : m_g - 1;
+    int src, out;
+    float gw = 1.f;
+    if constexpr (PHASE == 0) {
+      src = shared ? m : a.sorted_pair[off_e + m] / a.k;
+      out = shared ? (g - a.E_routed) * a.T + m : off_e + m;
+    } else if constexpr (PHASE == 1) {
+      src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
+      if (shared) {
+        out = m * (a.k + a.n_shared) + a.k + (g - a.E_routed);
+      } else {
+        const int p = a.sorted_pair[off_e + m];
+        out = (p / a.k) * (a.k + a.n_shared) + (p % a.k);
+        gw = a.topk_w[p];
+      }
+    } else {
+      src = m;
+      out = m;
+    }
+    sm.rowsrc[tid] = src;
+    sm.rowout[tid] = m0 < m_g ? out : -1;
+    sm.rowgw[tid] = gw;
+    sm.rowscale[tid] = INT ? ascale[src] : 1.f;
   }
   const int64_t row_bytes = (int64_t)K * (INT ? 1 : 2);
   __syncthreads();
@@ -447,10 +484,11 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         st[j][l][nf] = load_step<KD>(wp[l][nf] + (last ? 0 : (int64_t)kn * BB) + lo, j);
   };
   // Vector-memory loads issued after the activation stage of the next k block,
-  // at least: one per fragment and step (streamed) or per fragment (group
-  // prefetch), plus one metadata dword per fragment (weight-only).  Waiting for
+  // at least: one per fragment and step (streamed), one per fragment (group
+  // prefetch; two 16-byte loads for w8a8), plus one metadata dword per fragment
+  // (weight-only).  Waiting for
   // this many leaves the weight prefetch in flight across the barrier.
-  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : 1) + (WONLY ? NL * NF : 0);
+  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (WONLY ? NL * NF : 0);
 
   stage_load<INT, BM>(sm, 0, abase, soffs, 0, wave);
   load_group(0, false);
@@ -579,73 +617,65 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
 
   // ---- epilogue: lane holds rows 4q + i of fragment mf, channel li of fragment nf
-  float rscale[MF][4];
-  int rows[MF][4];
+  // (the per-row data is re-read from LDS for every fragment: holding it for
+  // all fragments would cost 64-96 registers next to the accumulators)
+  const bool full = row0 + BM <= m_g;  // uniform: no row of the tile lies past the group
+  auto epilogue = [&](auto guard) {
+    constexpr bool GUARD = decltype(guard)::value;
 #pragma unroll
-  for (int mf = 0; mf < MF; ++mf)
+    for (int nf = 0; nf < NF; ++nf) {
+      if (nf >= nvalid) continue;
+      const int n = 16 * (nb0 + nf) + li;
+      float cs[NL];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = mf * 16 + 4 * q + i;
-      rows[mf][i] = row0 + r;
-      rscale[mf][i] = 1.f;
-      if constexpr (INT) rscale[mf][i] = ascale[sm.rowsrc[r]];
-    }
+      for (int l = 0; l < NL; ++l) {
+        cs[l] = 1.f;
+        if constexpr (INT) cs[l] = lins[l]->wscale[n];
+        if constexpr (WONLY) cs[l] = s_prev[l][nf];
+      }
 #pragma unroll
-  for (int nf = 0; nf < NF; ++nf) {
-    if (nf >= nvalid) continue;
-    const int n = 16 * (nb0 + nf) + li;
-    float cs[NL];
+      for (int mf = 0; mf < MF; ++mf) {
+        const int r = mf * 16 + 4 * q;
+        const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
+        const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
+        const i32x4 ro = *reinterpret_cast<const i32x4*>(&sm.rowout[r]);
+        float v[NL][4];
 #pragma unroll
-    for (int l = 0; l < NL; ++l) {
-      cs[l] = 1.f;
-      if constexpr (INT) cs[l] = lins[l]->wscale[n];
-      if constexpr (WONLY) cs[l] = s_prev[l][nf];
-    }
+        for (int l = 0; l < NL; ++l)
 #pragma unroll
-    for (int mf = 0; mf < MF; ++mf) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = rows[mf][i];
-        if (m >= m_g) continue;
-        float v[NL];
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          if constexpr (INT) {
-            int iv = acc[l][nf][mf][i];
-            if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
-            v[l] = ((float)iv * rscale[mf][i]) * cs[l];
-          } else {
-            v[l] = acc[l][nf][mf][i] * cs[l];
+          for (int i = 0; i < 4; ++i) {
+            if constexpr (INT) {
+              int iv = acc[l][nf][mf][i];
+              if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
+              v[l][i] = ((float)iv * rs[i]) * cs[l];
+            } else {
+              v[l][i] = acc[l][nf][mf][i] * cs[l];
+            }
           }
-        }
-        if constexpr (PHASE == 0) {
-          uint16_t* hb = reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h);
-          const int64_t hrow = shared ? (int64_t)(g - a.E_routed) * a.T + m : (int64_t)off_e + m;
-          hb[hrow * N + n] = f32_to_act<ACT>(silu_f32(v[0]) * v[1]);
-        } else if constexpr (PHASE == 1) {
-          int64_t srow;
-          float gw;
-          if (shared) {
-            srow = (int64_t)m * (a.k + a.n_shared) + a.k + (g - a.E_routed);
-            gw = 1.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (GUARD && ro[i] < 0) continue;
+          const int64_t orow = (int64_t)ro[i] * N + n;
+          if constexpr (PHASE == 0) {
+            uint16_t* hb = reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h);
+            hb[orow] = f32_to_act<ACT>(silu_f32(v[0][i]) * v[1][i]);
+          } else if constexpr (PHASE == 1) {
+            a.slots[orow] = v[0][i] * gwv[i];
           } else {
-            const int p = a.sorted_pair[off_e + m];
-            srow = (int64_t)(p / a.k) * (a.k + a.n_shared) + (p % a.k);
-            gw = a.topk_w[p];
-          }
-          a.slots[srow * N + n] = v[0] * gw;
-        } else {
-          if constexpr (INT) {
-            int iv = acc[0][nf][mf][i];
-            if constexpr (KD == K_W4A4) iv >>= 4;
-            reinterpret_cast<int32_t*>(a.raw_out)[(int64_t)m * N + n] = iv;
-          } else {
-            reinterpret_cast<float*>(a.raw_out)[(int64_t)m * N + n] = v[0];
+            if constexpr (INT) {
+              int iv = acc[0][nf][mf][i];
+              if constexpr (KD == K_W4A4) iv >>= 4;
+              reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
+            } else {
+              reinterpret_cast<float*>(a.raw_out)[orow] = v[0][i];
+            }
           }
         }
       }
     }
-  }
+  };
+  if (full) epilogue(std::false_type{});
+  else epilogue(std::true_type{});
   __syncthreads();  // the next tile rewrites rowsrc and the stages
 }
 
