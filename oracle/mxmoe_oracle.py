@@ -38,7 +38,7 @@ import numpy as np
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "dequant",
     "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
-    "silu", "tile_plan", "xcd_queues",
+    "silu", "tile_plan", "xcd_queues", "xcd_tiles",
 ]
 
 # ----------------------------------------------------------------------------
@@ -475,3 +475,20 @@ def xcd_queues(plan, order, n_queues: int = 8):
             totals[x] += size
             u += 1
     return queues, totals
+
+
+def xcd_tiles(plan, order, n_queues: int = 8):
+    """Per-queue tile lists [(group, row tile, channel tile)]: each queue entry
+    expanded into its super-tile's tiles, row tile fastest."""
+    queues, _ = xcd_queues(plan, order, n_queues)
+    out = []
+    for q in queues:
+        tiles = []
+        for g, s, _first in q:
+            mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"])
+            sm, sn, nsm, _nsn = _super_dims(mt, nt)
+            smi, sni = s % nsm, s // nsm
+            em, en = min(sm, mt - smi * sm), min(sn, nt - sni * sn)
+            tiles += [(g, smi * sm + t % em, sni * sn + t // em) for t in range(em * en)]
+        out.append(tiles)
+    return out

@@ -118,8 +118,14 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.chunk_counts = take(4 * nchunks * bi.E);
   L.chunk_bad = take(4 * nchunks);
   L.qcap = plan_queue_cap((int64_t)T * bi.k + (int64_t)bi.nsh * T, bi.G, std::max(std::max(bi.F, bi.Fsh), bi.H));
-  L.plan = take(4 * (size_t)plan_layout(bi.G, L.qcap).total);
+  L.fcap = plan_flat_cap(L.qcap);
+  L.plan = take(4 * (size_t)plan_layout(bi.G, L.qcap, L.fcap).total);
   L.down_qmax = take(4 * (size_t)bi.G);
+  L.rtok = take(4 * P);
+  L.rslot = take(4 * P);
+  L.rgw = take(4 * P);
+  L.rxs8 = bi.any_x8 ? take(4 * P) : kNone;
+  L.rxs4 = bi.any_x4 ? take(4 * P) : kNone;
   L.xq8 = L.xs8 = L.xq4 = L.xs4 = kNone;
   if (bi.any_x8) { L.xq8 = take((size_t)T * bi.H); L.xs8 = take(4 * (size_t)T); }
   if (bi.any_x4) { L.xq4 = take((size_t)T * bi.H); L.xs4 = take(4 * (size_t)T); }
@@ -226,12 +232,13 @@ mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32
 
 // -------------------------------------------------------- single linear
 namespace {
-struct LinWs { size_t plan, aq, as, total; int qcap; };
+struct LinWs { size_t plan, aq, as, total; int qcap, fcap; };
 LinWs lin_layout(int kd, int m, int n, int k) {
   LinWs w;
   size_t o = 0;
   w.qcap = plan_queue_cap(m, 1, n);
-  w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap).total);
+  w.fcap = plan_flat_cap(w.qcap);
+  w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap, w.fcap).total);
   w.aq = w.as = kNone;
   if (kind_is_int(kd)) {
     w.aq = o; o = align256(o + (size_t)m * k);
@@ -280,6 +287,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   ga.raw_lin = dl;
   ga.raw_out = out;
   ga.qcap = w.qcap;
+  ga.fcap = w.fcap;
   if (kind_is_int(kd)) {
     int8_t* aq = at<int8_t>(workspace, w.aq);
     float* as = at<float>(workspace, w.as);
@@ -287,7 +295,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
   }
-  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, m, dl, nullptr, ga.plan, w.qcap, nullptr, stream);
+  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, nullptr, stream);
   if (e != hipSuccess) return MXMOE_ERR_HIP;
   return hip_status(launch_group_gemm(ga, 2, group_gemm_grid(current_device()), stream));
 }
@@ -356,6 +364,7 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->slots = L.slots;
   out->total = L.total;
   out->plan_queue_cap = (size_t)L.qcap;
+  out->plan_flat_cap = (size_t)L.fcap;
   return MXMOE_OK;
 }
 
@@ -408,13 +417,18 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
                         at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
   memset(&none, 0, sizeof(none));
-  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, -1, none, mask, plan, L.qcap, down_qmax, stream));
+  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, down_qmax,
+                       stream));
   if (bi.any_x8)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
                               stream));
   if (bi.any_x4)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4), at<float>(workspace, L.xs4),
                               stream));
+  MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, topk_w, at<float>(workspace, L.xs8),
+                           at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
+                           at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
+                           stream));
   GemmArgs ga;
   memset(&ga, 0, sizeof(ga));
   ga.experts = experts;
@@ -442,6 +456,12 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.E_routed = bi.E;
   ga.n_shared = bi.nsh;
   ga.qcap = L.qcap;
+  ga.fcap = L.fcap;
+  ga.rtok = at<int32_t>(workspace, L.rtok);
+  ga.rslot = at<int32_t>(workspace, L.rslot);
+  ga.rgw = at<float>(workspace, L.rgw);
+  ga.rxs8 = at<float>(workspace, L.rxs8);
+  ga.rxs4 = at<float>(workspace, L.rxs4);
   const int grid = group_gemm_grid(current_device());
   MX_EVENT(1);
   MX_EVENT(2);

@@ -9,7 +9,10 @@
 //      greedy longest-tile-first order of the paper's tile schedule;
 //   3. cut every group into super-tiles (up to 64 tiles that share row and
 //      channel blocks) and deal them round-robin, in rank order, to one queue
-//      per XCD; per-queue prefix sums give each entry's first tile.
+//      per XCD; per-queue prefix sums give each entry's first tile;
+//   4. expand every queue into one 16-byte entry per tile (group, configuration,
+//      kind, tile coordinates, first sorted row and rows of the group), so that
+//      a workgroup resolves a popped tile with a single load.
 #include "group_gemm_impl.h"
 
 namespace mxmoe {
@@ -55,16 +58,17 @@ __device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
 }
 
 __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict__ experts, int E, int G, int T,
-                                                    const int32_t* __restrict__ counts, int raw_m,
+                                                    const int32_t* __restrict__ counts,
+                                                    const int32_t* __restrict__ offsets, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
-                                                    int qcap, int32_t* __restrict__ down_qmax) {
+                                                    int qcap, int fcap, int32_t* __restrict__ down_qmax) {
   __shared__ int32_t s_cost[2][2048];
   __shared__ int32_t s_tiles[2][2048];
   __shared__ int32_t s_red[1025];
   __shared__ int32_t s_ns[2048];
   const int tid = threadIdx.x;
   const int nphase = raw_m >= 0 ? 1 : 2;
-  const PlanLayout PL = plan_layout(G, qcap);
+  const PlanLayout PL = plan_layout(G, qcap, fcap);
   int32_t* misc = plan + PL.misc;
   if (tid == 0) misc[4] = 0;
   for (int ph = 0; ph < nphase; ++ph) {
@@ -163,6 +167,32 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       }
     }
     __syncthreads();
+    // expand the queues: one thread per queue entry writes its tiles
+    int32_t* flat = plan + PL.flat + (int64_t)ph * kXcd * fcap * 4;
+    for (int u = tid; u < S; u += blockDim.x) {
+      const int x = u % kXcd, pos = u / kXcd;
+      if (pos >= qcap) continue;
+      const int32_t* e = ent + ((int64_t)x * qcap + pos) * 3;
+      const int g = e[0], st = e[1], first = e[2];
+      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+      const int mt = rec[PF_MTILES], nt = rec[PF_NTILES];
+      const int size = super_tile_size(mt, nt, st);
+      if (first + size > fcap) {  // cannot happen with the host's capacity bound
+        misc[4] = 1;
+        continue;
+      }
+      const int kd = raw_m >= 0 ? raw_lin.kind : experts[g].lin[ph == 0 ? 0 : 2].kind;
+      const int w0 = tile_word0(g, rec[PF_CFG], kd);
+      const int off_e = (raw_m < 0 && g < E) ? offsets[g] : 0;
+      const int m_g = rec[PF_M];
+      int32_t* f = flat + ((int64_t)x * fcap + first) * 4;
+      for (int t = 0; t < size; ++t) {
+        int mi, ni;
+        super_tile_pos(mt, nt, st, t, &mi, &ni);
+        *reinterpret_cast<int4*>(f + 4 * t) = make_int4(w0, mi | (ni << 16), off_e, m_g);
+      }
+    }
+    __syncthreads();
     if (tid == 0) misc[2 + ph] = ng;
     __syncthreads();
   }
@@ -179,13 +209,13 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
 
 }  // namespace
 
-hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts, int raw_m,
-                       const DevLinear& raw_lin, const uint32_t* mask_words, int32_t* plan, int qcap,
-                       int32_t* down_qmax, hipStream_t s) {
+hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
+                       const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
+                       int32_t* plan, int qcap, int fcap, int32_t* down_qmax, hipStream_t s) {
   MaskBits mb;
   for (int i = 0; i < 64; ++i) mb.w[i] = mask_words ? mask_words[i] : 0xffffffffu;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, raw_m, raw_lin, mb, plan, qcap,
-                     down_qmax);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin, mb,
+                     plan, qcap, fcap, down_qmax);
   return hipGetLastError();
 }
 

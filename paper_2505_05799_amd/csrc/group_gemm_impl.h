@@ -275,8 +275,36 @@ struct __align__(16) Smem {
   int32_t rowout[BM_MAX];        // output row index of every tile row, -1 past the group's rows
   float rowscale[BM_MAX];        // per-token activation scale (a8/a4), else 1
   float rowgw[BM_MAX];           // router gate weight of the row's (token, slot) (down phase), else 1
-  int32_t tile, tidx;            // popped queue and tile index
+  int4 entry;                    // the next tile (plan tile entry; group -1: none left)
+  int32_t qtotal[kXcd];          // tiles per XCD queue
+  int32_t qi;                    // queues tried so far by this workgroup
 };
+
+// Tile queues of one phase, rebuilt from the kernel arguments where needed so
+// that no queue state stays in registers across a tile.  Thread 0 of a
+// workgroup claims tiles: first from the queue of its own XCD, then from the
+// others in turn once that is empty (sm.qi counts the queues tried).
+struct TileQueue {
+  int32_t* ctr;       // [kXcd][4] head counters (field 0)
+  const int4* flat;   // [kXcd][fcap] tile entries
+  int fcap;
+  int x0;             // queue of this workgroup's XCD
+};
+__device__ inline TileQueue tile_queue(const GemmArgs& a, int pidx) {
+  int32_t* plan = a.plan;
+  asm volatile("" : "+s"(plan));  // recomputed here, not kept live from an earlier use
+  const PlanLayout PL = plan_layout(a.G, a.qcap, a.fcap);
+  TileQueue Q;
+  Q.ctr = plan + PL.ctr + (int64_t)pidx * kXcd * 4;
+  Q.flat = reinterpret_cast<const int4*>(plan + PL.flat) + (int64_t)pidx * kXcd * a.fcap;
+  Q.fcap = a.fcap;
+  Q.x0 = blockIdx.x % kXcd;  // workgroups are dealt round-robin over the XCDs
+  return Q;
+}
+// claim the next index of the current queue (thread 0)
+__device__ inline int pop_start(const TileQueue& Q, int qi) {
+  return qi < kXcd ? atomicAdd(&Q.ctr[((Q.x0 + qi) % kXcd) * 4], 1) : 0;
+}
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
@@ -320,6 +348,32 @@ __device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t ld
                : "memory", "m0");
 }
 
+// Claim the next tile and load its entry straight into sm.entry (thread 0;
+// the caller waits for the load with its vector-memory count), or mark the
+// end with group -1.  The first claim of a workgroup uses a plain load.
+template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& sm) {
+  int qi = sm.qi;
+  int idx = pop_start(Q, qi);
+  while (qi < kXcd) {
+    const int x = (Q.x0 + qi) % kXcd;
+    if (idx < sm.qtotal[x]) {
+      sm.qi = qi;
+      if constexpr (DMA) {
+        const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.entry);
+        lds_dma16(reinterpret_cast<const uint8_t*>(Q.flat), (uint32_t)(((int64_t)x * Q.fcap + idx) * 16),
+                  __builtin_amdgcn_readfirstlane(lds));
+      } else {
+        sm.entry = Q.flat[(int64_t)x * Q.fcap + idx];
+      }
+      return;
+    }
+    ++qi;
+    idx = pop_start(Q, qi);
+  }
+  sm.qi = qi;
+  sm.entry.x = -1;  // only the group field is read when no tile is left
+}
+
 template <bool INT, int BM>
 __device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<INT, BM>& so, int kb,
                                   int wave) {
@@ -355,7 +409,8 @@ template <int ACT, int MF> __device__ inline void stage_rowsum(Smem& sm, int buf
 
 // ---------------------------------------------------------- tile body
 template <int KD, int ACT, int CFG, int PHASE>
-__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt) {
+__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
+                                int off_e) {
   constexpr int MF = cfg_mf(CFG);
   constexpr int NF = cfg_nf(CFG, PHASE == 0 ? 0 : 1);
   constexpr int NL = PHASE == 0 ? 2 : 1;
@@ -386,7 +441,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const int nb0 = (nt * BN) / 16 + wave * NF;   // first 16-channel block of this wavefront
   int nvalid = N / 16 - nb0;
   nvalid = nvalid < 0 ? 0 : (nvalid > NF ? NF : nvalid);
-  const int off_e = (!shared && PHASE != kPhaseRaw) ? a.offsets[g] : 0;
 
   const uint8_t* abase;
   const float* ascale = nullptr;
@@ -406,26 +460,29 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const int m = m0 < m_g ? m0 : m_g - 1;
     int src, out;
     float gw = 1.f;
+    float sc = 1.f;
     if constexpr (PHASE == 0) {
-      src = shared ? m : a.sorted_pair[off_e + m] / a.k;
+      src = shared ? m : a.rtok[off_e + m];
       out = shared ? (g - a.E_routed) * a.T + m : off_e + m;
+      if constexpr (INT) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
     } else if constexpr (PHASE == 1) {
       src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
       if (shared) {
         out = m * (a.k + a.n_shared) + a.k + (g - a.E_routed);
       } else {
-        const int p = a.sorted_pair[off_e + m];
-        out = (p / a.k) * (a.k + a.n_shared) + (p % a.k);
-        gw = a.topk_w[p];
+        out = a.rslot[off_e + m];
+        gw = a.rgw[off_e + m];
       }
+      if constexpr (INT) sc = ascale[src];
     } else {
       src = m;
       out = m;
+      if constexpr (INT) sc = ascale[m];
     }
     sm.rowsrc[tid] = src;
     sm.rowout[tid] = m0 < m_g ? out : -1;
     sm.rowgw[tid] = gw;
-    sm.rowscale[tid] = INT ? ascale[src] : 1.f;
+    sm.rowscale[tid] = sc;
   }
   const int64_t row_bytes = (int64_t)K * (INT ? 1 : 2);
   __syncthreads();
@@ -603,6 +660,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    // Last k block: claim the next tile and bring its entry into LDS (the
+    // entry is read at the top of the tile loop, after the final barrier).
+    if (!more && tid == 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
     // The next stage has landed once no more than the weight prefetch is
     // outstanding (vector-memory loads complete in issue order).
     if (more) wait_vmem<kLoadsAfterStage>();
@@ -681,15 +741,15 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 
 template <int ACT, int PHASE, int CFG>
 __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
-                                     int kd) {
+                                     int off_e, int kd) {
   switch (kd) {
-    case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
-    case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt); break;
+    case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
     default: break;
   }
 }
@@ -697,59 +757,31 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
 template <int ACT, int PHASE>
 __global__ void __launch_bounds__(kThreads, 2) group_gemm_kernel(GemmArgs a) {
   __shared__ Smem sm;
-  const int G = a.G;
-  const int pidx = PHASE == kPhaseRaw ? 0 : PHASE;
-  const PlanLayout PL = plan_layout(G, a.qcap);
-  const int32_t* rec = a.plan + PL.rec + (int64_t)pidx * G * PF_N;
-  const int32_t* ent = a.plan + PL.ent + (int64_t)pidx * kXcd * a.qcap * 3;
-  int32_t* ctr = a.plan + PL.ctr + (int64_t)pidx * kXcd * 4;
-  // workgroups are dealt round-robin over the XCDs: start with the local queue
-  const int x0 = blockIdx.x % kXcd;
-  int qi = 0;
+  {
+    const TileQueue Q = tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE);
+    if (threadIdx.x < kXcd) sm.qtotal[threadIdx.x] = min(Q.ctr[threadIdx.x * 4 + 1], a.fcap);
+    if (threadIdx.x == 0) sm.qi = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) claim_next<false>(Q, sm);
+    __syncthreads();
+  }
   for (;;) {
-    if (threadIdx.x == 0) {
-      int found = -1, idx = 0;
-      while (qi < kXcd) {
-        const int x = (x0 + qi) % kXcd;
-        const int total = ctr[x * 4 + 1];
-        const int i = total > 0 ? atomicAdd(&ctr[x * 4], 1) : 0;
-        if (i < total) {
-          found = x;
-          idx = i;
-          break;
-        }
-        ++qi;
-      }
-      sm.tile = found;
-      sm.tidx = idx;
-    }
-    __syncthreads();
     // wave-uniform from here on: tile bookkeeping and weight pointers live in SGPRs
-    const int x = __builtin_amdgcn_readfirstlane(sm.tile);
-    const int tile = __builtin_amdgcn_readfirstlane(sm.tidx);
-    __syncthreads();
-    if (x < 0) break;
-    const int32_t* q = ent + (int64_t)x * a.qcap * 3;
-    int lo = 0, hi = __builtin_amdgcn_readfirstlane(ctr[x * 4 + 2]);  // entry with start <= tile
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (q[mid * 3 + 2] <= tile) lo = mid; else hi = mid;
-    }
-    const int g = __builtin_amdgcn_readfirstlane(q[lo * 3 + 0]);
-    const int s = __builtin_amdgcn_readfirstlane(q[lo * 3 + 1]);
-    const int local = tile - __builtin_amdgcn_readfirstlane(q[lo * 3 + 2]);
-    const int32_t* r = rec + (int64_t)g * PF_N;
-    int mt, nt;
-    super_tile_pos(__builtin_amdgcn_readfirstlane(r[PF_MTILES]), __builtin_amdgcn_readfirstlane(r[PF_NTILES]), s,
-                   local, &mt, &nt);
+    const int w0 = __builtin_amdgcn_readfirstlane(sm.entry.x);
+    if (w0 < 0) break;
+    const int w1 = __builtin_amdgcn_readfirstlane(sm.entry.y);
+    const int off_e = __builtin_amdgcn_readfirstlane(sm.entry.z);
+    const int m_g = __builtin_amdgcn_readfirstlane(sm.entry.w);
+    const int g = w0 & 0xFFFF, cfg = (w0 >> 16) & 15, kd = w0 >> 20;
+    const int mt = w1 & 0xFFFF, nt = w1 >> 16;
     const DevExpert* ex = PHASE == kPhaseRaw ? nullptr : a.experts + g;
-    const int kd = __builtin_amdgcn_readfirstlane(PHASE == kPhaseRaw ? a.raw_lin.kind : ex->lin[PHASE == 0 ? 0 : 2].kind);
-    const int m_g = __builtin_amdgcn_readfirstlane(r[PF_M]);
-    switch (__builtin_amdgcn_readfirstlane(r[PF_CFG])) {
-      case CFG_S: dispatch_kind<ACT, PHASE, CFG_S>(sm, a, ex, g, m_g, mt, nt, kd); break;
-      case CFG_T: dispatch_kind<ACT, PHASE, CFG_T>(sm, a, ex, g, m_g, mt, nt, kd); break;
-      case CFG_M: dispatch_kind<ACT, PHASE, CFG_M>(sm, a, ex, g, m_g, mt, nt, kd); break;
-      default: dispatch_kind<ACT, PHASE, CFG_L>(sm, a, ex, g, m_g, mt, nt, kd); break;
+    // (every thread has read the entry: run_tile passes a barrier before
+    // thread 0 claims the next tile into it)
+    switch (cfg) {
+      case CFG_S: dispatch_kind<ACT, PHASE, CFG_S>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
+      case CFG_T: dispatch_kind<ACT, PHASE, CFG_T>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
+      case CFG_M: dispatch_kind<ACT, PHASE, CFG_M>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
+      default: dispatch_kind<ACT, PHASE, CFG_L>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
     }
   }
 }

@@ -106,13 +106,15 @@ constexpr int kSuperTiles = 64;
 
 // Plan region layout (int32), phases p = 0 (gate|up, or the single linear)
 // and 1 (down):
-//   rec   [2][G][PF_N]       group records
-//   order [2][G]             group index per rank (-1 past the last group with tiles)
-//   ent   [2][kXcd][cap][3]  queue entries: group, super-tile index, first tile
-//   ctr   [2][kXcd][4]       per queue: head, total tiles, entries, -
-//   misc  [16]               [2 + p]: number of groups with tiles in phase p
-struct PlanLayout { int64_t rec, order, ent, ctr, misc, total; };
-__host__ __device__ inline PlanLayout plan_layout(int G, int cap) {
+//   rec   [2][G][PF_N]        group records
+//   order [2][G]              group index per rank (-1 past the last group with tiles)
+//   ent   [2][kXcd][cap][3]   queue entries: group, super-tile index, first tile
+//   ctr   [2][kXcd][4]        per queue: head, total tiles, entries, -
+//   misc  [16]                [2 + p]: number of groups with tiles in phase p,
+//                             [4]: 1 if a queue overflowed its capacity
+//   flat  [2][kXcd][fcap][4]  the queues expanded to one entry per tile (TileEntry)
+struct PlanLayout { int64_t rec, order, ent, ctr, misc, flat, total; };
+__host__ __device__ inline PlanLayout plan_layout(int G, int cap, int fcap) {
   PlanLayout L;
   L.rec = 0;
   L.order = L.rec + 2LL * G * PF_N;
@@ -120,7 +122,8 @@ __host__ __device__ inline PlanLayout plan_layout(int G, int cap) {
   L.ent = (L.ent + 3) & ~3LL;
   L.ctr = L.ent + 2LL * kXcd * cap * 3;
   L.misc = L.ctr + 2LL * kXcd * 4;
-  L.total = L.misc + 16;
+  L.flat = L.misc + 16;
+  L.total = L.flat + 2LL * kXcd * fcap * 4;
   return L;
 }
 // Per-queue capacity bound from the rows and channel counts (host side):
@@ -130,12 +133,22 @@ __host__ __device__ inline int plan_queue_cap(int64_t rows_total, int groups, in
   const int64_t s = (rows_total / 1024 + 2LL * groups + 1) * ((int64_t)n_max / 512 + 2);
   return (int)(s / kXcd + 2);
 }
+// Per-queue tile capacity: at most 64 tiles per queue entry.
+__host__ __device__ inline int plan_flat_cap(int qcap) { return qcap * kSuperTiles; }
+
+// One tile of a queue, as the Group-GEMM pops it (int32 x 4):
+//   [0] group | cfg << 16 | kind << 20   [1] row tile | channel tile << 16
+//   [2] first sorted row of the group (0 for shared experts and single linears)
+//   [3] rows of the group
+__host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind) { return g | (cfg << 16) | (kind << 20); }
 
 // Workspace layout (byte offsets), shared by host code of the forward.
 struct WsLayout {
   size_t status, counts, offsets, sorted_pair, inv, chunk_counts, chunk_bad, plan, down_qmax;
+  size_t rtok, rslot, rgw, rxs8, rxs4;
   size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
-  int qcap;  // XCD queue capacity of the tile plan
+  int qcap;  // XCD queue capacity of the tile plan (super-tiles)
+  int fcap;  // XCD queue capacity of the tile plan (tiles)
 };
 
 constexpr int kRouteChunk = 2048;  // pairs per routing workgroup
@@ -154,6 +167,13 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
 
 hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax,
                             int8_t* codes, float* scales, hipStream_t s);
+
+// Per sorted row j < offsets[E] (pair p = sorted_pair[j], token t = p / k,
+// slot s = p % k): rtok[j] = t, rslot[j] = t (k + n_sh) + s, rgw[j] = topk_w[p],
+// and rxs8[j] / rxs4[j] = the token's activation scale where those exist.
+hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, int E, int P, int k, int n_sh,
+                           const float* topk_w, const float* xs8, const float* xs4, int32_t* rtok, int32_t* rslot,
+                           float* rgw, float* rxs8, float* rxs4, hipStream_t s);
 
 // Quantize routed h rows whose expert's down projection is a8/a4 (qmax from
 // down_qmax[expert]); rows of other experts are skipped.
@@ -180,7 +200,10 @@ struct GemmArgs {
   int32_t G;          // experts incl. shared
   int32_t E_routed;
   int32_t n_shared;
-  int32_t qcap;        // capacity of each XCD queue in the plan region
+  int32_t qcap;        // capacity of each XCD queue in the plan region (super-tiles)
+  int32_t fcap;        // capacity of each XCD queue in the plan region (tiles)
+  // per sorted row (see launch_row_meta)
+  const int32_t* rtok; const int32_t* rslot; const float* rgw; const float* rxs8; const float* rxs4;
   // single-linear mode (mxmoe_linear_forward): raw int32 / fp32 output
   DevLinear raw_lin;
   void* raw_out;
@@ -189,8 +212,8 @@ struct GemmArgs {
 // raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
-                       int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int qcap, int32_t* down_qmax, hipStream_t s);
+                       const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
+                       int32_t* plan, int qcap, int fcap, int32_t* down_qmax, hipStream_t s);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

@@ -32,6 +32,18 @@ def sample_tokens(blk, n_random=10, seed=0):
     return np.array(sorted(picks))
 
 
+# micro-kernel ids of the schemes in the plan's tile entries
+KIND = {"w16": 0, "w8a8": 1, "w4a4": 2, "w2g128": 3, "w3g128": 4, "w4g128": 5, "w8g128": 6}
+
+
+def plan_flat(mb, T, G, cap, phase):
+    torch = torch_mod()
+    fcap = mb.workspace_layout(T)["plan_flat_cap"]
+    o_flat = ((2 * G * 8 + 2 * G + 3) & ~3) + 2 * 8 * cap * 3 + 64 + 16
+    p = mb.ws_view("plan", torch.int32, o_flat + 2 * 8 * fcap * 4, T).cpu().numpy()
+    return p[o_flat + phase * 8 * fcap * 4: o_flat + (phase + 1) * 8 * fcap * 4].reshape(8, fcap, 4)
+
+
 def plan_misc(mb, T, G, cap):
     torch = torch_mod()
     o_ctr = ((2 * G * 8 + 2 * G + 3) & ~3) + 2 * 8 * cap * 3
@@ -88,6 +100,14 @@ def test_full_workload(name):
             assert ctr[x, 1] == totals[x] and ctr[x, 2] == len(queues[x]), (phase, x)
             assert [tuple(e) for e in ent[x, : len(queues[x])].tolist()] == queues[x], (phase, x)
         assert sum(totals) == sum(w["tiles"] for w in want)
+        # the queues expanded to one entry per tile
+        tiles = O.xcd_tiles(want, order)
+        offs = r["offsets"]
+        fl = plan_flat(mb, T, G, cap, phase)
+        for x in range(8):
+            exp = np.array([[g | (want[g]["cfg"] << 16) | (KIND[lins[g].scheme.name] << 20), mi | (ni << 16),
+                             offs[g] if g < E else 0, ms[g]] for g, mi, ni in tiles[x]], dtype=np.int64)
+            assert np.array_equal(fl[x, : len(tiles[x])].astype(np.int64), exp.reshape(-1, 4)), (phase, x)
     assert plan_misc(mb, T, G, cap)[4] == 0      # no queue overflow
 
     # block output on sampled tokens

@@ -398,3 +398,15 @@ def test_tile_plan_covers_every_output(name):
         costs = [plan[g]["cost"] for g in order]
         assert costs == sorted(costs, reverse=True)
         assert sorted(order) == [g for g, m in enumerate(counts) if m > 0]
+        # the per-XCD queues hold every tile of every group exactly once, the
+        # queue totals match, and groups appear in rank order within a queue
+        queues, totals = O.xcd_queues(plan, order)
+        tiles = O.xcd_tiles(plan, order)
+        assert [len(t) for t in tiles] == totals
+        flat = [t for q in tiles for t in q]
+        want = [(g, mi, ni) for g in order for mi in range(plan[g]["mtiles"]) for ni in range(plan[g]["ntiles"])]
+        assert sorted(flat) == sorted(want) and len(flat) == len(set(flat))
+        rank = {g: i for i, g in enumerate(order)}
+        for q in tiles:
+            ranks = [rank[g] for g, _, _ in q]
+            assert ranks == sorted(ranks)
