@@ -227,8 +227,10 @@ typedef struct {
   size_t inv;           /* int32 [T*k]                                       */
   size_t plan;          /* int32 tile plan: group records [2][G][8], order [2][G],
                            XCD queues [2][8][plan_queue_cap][3] (16-byte aligned),
-                           queue counters [2][8][4], misc [16], and the queues
-                           expanded to tiles [2][8][plan_flat_cap][4]         */
+                           queue counters [2][8][4], misc [16], the queues
+                           expanded to tiles [2][8][plan_flat_cap][4], and
+                           split-K arrival counters [2][16384]; group records
+                           have 12 fields                                    */
   size_t xq8, xs8;      /* int8 [T,H], fp32 [T]: x codes for a8 gate/up      */
   size_t xq4, xs4;      /* int8 [T,H], fp32 [T]: x codes for a4 gate/up      */
   size_t h;             /* act [T*k, F]: routed h rows, sorted-pair order    */
@@ -239,6 +241,8 @@ typedef struct {
   size_t total;         /* = mxmoe_workspace_bytes                           */
   size_t plan_queue_cap;/* entries per XCD queue in the tile plan            */
   size_t plan_flat_cap; /* tiles per XCD queue in the tile plan              */
+  size_t partial;       /* fp32 split-K partial sums                         */
+  size_t partial_floats;/* size of that buffer (floats)                      */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

@@ -404,35 +404,70 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
 #   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s;
 #   queue order: decreasing cost, ties by lower expert index.
+# Slicing of the reduction (split-K, the paper's slice-K tile parameter):
+#   configurations S/T/M: S = clamp(K/128 // 4, 1, 8) slices;
+#   configuration L: S = min(4, (K/128) // 16) if the group has fewer than 128
+#   tiles and K/128 >= 32, else 1;
+#   budgets, granted in group order: the slices' partial sums (tiles * S * BM *
+#   BN * linears floats) fit the partial buffer and the tiles added by slicing
+#   (tiles * (S - 1)) stay within 16384 per phase, else S = 1;
+#   the cost uses the reduction length of one slice, ceil(K/128 / S) * 128, and
+#   a sliced group queues tiles * S tiles.
 
 _TILE_BM = (16, 32, 64, 128)
 _TILE_BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][config]
+_SPLIT_EXTRA = 16384
 
 
-def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
-    """Tile configuration, tile counts, cost and queue rank per group of a phase.
+def _split_rule(cfg: int, tiles: int, kblocks: int) -> int:
+    if tiles <= 0:
+        return 1
+    if cfg != 3:
+        return max(1, min(8, kblocks // 4))
+    if tiles < 128 and kblocks >= 32:
+        return min(4, kblocks // 16)
+    return 1
 
-    ms[g]: rows of group g; lins[g]: its linear (gate for phase 0, down for 1).
-    Returns a list of dicts (cfg, mtiles, ntiles, cost, rank) and the queue
-    order (group indices with tiles, longest tile first).
+
+def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int = 0):
+    """Tile configuration, tile counts, slices, cost and queue rank per group.
+
+    ms[g]: rows of group g; lins[g]: its linear (gate for phase 0, down for 1);
+    partial_floats: size of the split-K partial buffer.  Returns a list of dicts
+    (cfg, mtiles, ntiles, split, tiles, cost, rank) and the queue order (group
+    indices with tiles, longest tile first).
     """
     out = []
+    nl = 2 if phase == 0 else 1
+    pused = eused = 0
     for m, lin in zip(ms, lins):
-        s = lin.scheme
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-lin.n // bn)
-        nl = 2 if phase == 0 else 1
+        sp = _split_rule(cfg, mt * nt, lin.k // 128)
+        if sp > 1:
+            need = mt * nt * sp * bm * bn * nl
+            extra = mt * nt * (sp - 1)
+            if pused + need > partial_floats or eused + extra > _SPLIT_EXTRA:
+                sp = 1
+            else:
+                pused += need
+                eused += extra
+        out.append({"cfg": cfg, "mtiles": mt, "ntiles": nt, "split": sp})
+    for r, lin in zip(out, lins):
+        s = lin.scheme
+        bm, bn = _TILE_BM[r["cfg"]], _TILE_BN[phase][r["cfg"]]
+        kk = -(-(lin.k // 128) // r["split"]) * 128
         is_int = s.a_bits < 16
-        wbytes = float(nl * bn * lin.k * s.w_bits) / 8.0
-        abytes = float(bm) * lin.k * (1.0 if is_int else 2.0)
-        flops = 2.0 * nl * bm * bn * lin.k
+        wbytes = float(nl * bn * kk * s.w_bits) / 8.0
+        abytes = float(bm) * kk * (1.0 if is_int else 2.0)
+        flops = 2.0 * nl * bm * bn * kk
         c = max((wbytes + abytes) * 32.0, flops * 1000.0 / (19531.0 if is_int else 9766.0))
         c = min(c, 2.0e9)
-        tiles = mt * nt
-        out.append({"cfg": cfg, "mtiles": mt, "ntiles": nt, "tiles": tiles,
-                    "cost": int(c) if tiles else 0})
+        tiles = r["mtiles"] * r["ntiles"] * r["split"]
+        r["tiles"] = tiles
+        r["cost"] = int(c) if tiles else 0
     live = [g for g, r in enumerate(out) if r["tiles"] > 0]
     order = sorted(live, key=lambda g: (-out[g]["cost"], g))
     for r in out:
@@ -445,7 +480,8 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int):
     return out, order
 
 
-# Super-tiles and per-XCD queues.  A group of mt x nt tiles is cut into
+# Super-tiles and per-XCD queues.  A group of mt x nt tiles (nt counting the
+# slices of a sliced group as extra channel tiles) is cut into
 # super-tiles of sm = min(mt, 8) row tiles by sn = min(nt, 64 // sm) channel
 # tiles, numbered with the row index fastest; the super-tiles of all groups, in
 # queue (rank) order, are dealt round-robin to 8 queues.  Each queue lists
@@ -465,7 +501,7 @@ def xcd_queues(plan, order, n_queues: int = 8):
     totals = [0] * n_queues
     u = 0
     for g in order:
-        mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"])
+        mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"]) * int(plan[g].get("split", 1))
         sm, sn, nsm, nsn = _super_dims(mt, nt)
         for s in range(nsm * nsn):
             smi, sni = s % nsm, s // nsm
@@ -479,13 +515,14 @@ def xcd_queues(plan, order, n_queues: int = 8):
 
 def xcd_tiles(plan, order, n_queues: int = 8):
     """Per-queue tile lists [(group, row tile, channel tile)]: each queue entry
-    expanded into its super-tile's tiles, row tile fastest."""
+    expanded into its super-tile's tiles, row tile fastest.  Channel tiles of a
+    sliced group count slice * ntiles + channel tile."""
     queues, _ = xcd_queues(plan, order, n_queues)
     out = []
     for q in queues:
         tiles = []
         for g, s, _first in q:
-            mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"])
+            mt, nt = int(plan[g]["mtiles"]), int(plan[g]["ntiles"]) * int(plan[g].get("split", 1))
             sm, sn, nsm, _nsn = _super_dims(mt, nt)
             smi, sni = s % nsm, s // nsm
             em, en = min(sm, mt - smi * sm), min(sn, nt - sni * sn)

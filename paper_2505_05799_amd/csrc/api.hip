@@ -126,6 +126,10 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.rgw = take(4 * P);
   L.rxs8 = bi.any_x8 ? take(4 * P) : kNone;
   L.rxs4 = bi.any_x4 ? take(4 * P) : kNone;
+  // split-K partial sums: a few times the largest layer output, at most 256 MB
+  L.pfloats = std::min<int64_t>((int64_t)1 << 26,
+                                4 * ((int64_t)P + (int64_t)bi.nsh * T) * std::max(std::max(bi.F, bi.Fsh), bi.H));
+  L.partial = take(4 * (size_t)L.pfloats);
   L.xq8 = L.xs8 = L.xq4 = L.xs4 = kNone;
   if (bi.any_x8) { L.xq8 = take((size_t)T * bi.H); L.xs8 = take(4 * (size_t)T); }
   if (bi.any_x4) { L.xq4 = take((size_t)T * bi.H); L.xs4 = take(4 * (size_t)T); }
@@ -232,13 +236,15 @@ mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32
 
 // -------------------------------------------------------- single linear
 namespace {
-struct LinWs { size_t plan, aq, as, total; int qcap, fcap; };
+struct LinWs { size_t plan, partial, aq, as, total; int qcap, fcap; int64_t pfloats; };
 LinWs lin_layout(int kd, int m, int n, int k) {
   LinWs w;
   size_t o = 0;
   w.qcap = plan_queue_cap(m, 1, n);
   w.fcap = plan_flat_cap(w.qcap);
   w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap, w.fcap).total);
+  w.pfloats = std::min<int64_t>((int64_t)1 << 24, 4 * (int64_t)m * n);
+  w.partial = o; o = align256(o + 4 * (size_t)w.pfloats);
   w.aq = w.as = kNone;
   if (kind_is_int(kd)) {
     w.aq = o; o = align256(o + (size_t)m * k);
@@ -288,6 +294,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   ga.raw_out = out;
   ga.qcap = w.qcap;
   ga.fcap = w.fcap;
+  ga.partial = at<float>(workspace, w.partial);
   if (kind_is_int(kd)) {
     int8_t* aq = at<int8_t>(workspace, w.aq);
     float* as = at<float>(workspace, w.as);
@@ -295,7 +302,8 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
   }
-  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, nullptr, stream);
+  hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, w.pfloats,
+                             nullptr, stream);
   if (e != hipSuccess) return MXMOE_ERR_HIP;
   return hip_status(launch_group_gemm(ga, 2, group_gemm_grid(current_device()), stream));
 }
@@ -365,6 +373,8 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->total = L.total;
   out->plan_queue_cap = (size_t)L.qcap;
   out->plan_flat_cap = (size_t)L.fcap;
+  out->partial = L.partial;
+  out->partial_floats = (size_t)L.pfloats;
   return MXMOE_OK;
 }
 
@@ -417,8 +427,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
                         at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
   memset(&none, 0, sizeof(none));
-  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, down_qmax,
-                       stream));
+  MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
+                       down_qmax, stream));
   if (bi.any_x8)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
                               stream));
@@ -462,6 +472,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.rgw = at<float>(workspace, L.rgw);
   ga.rxs8 = at<float>(workspace, L.rxs8);
   ga.rxs4 = at<float>(workspace, L.rxs4);
+  ga.partial = at<float>(workspace, L.partial);
   const int grid = group_gemm_grid(current_device());
   MX_EVENT(1);
   MX_EVENT(2);

@@ -11,8 +11,11 @@
 //      channel blocks) and deal them round-robin, in rank order, to one queue
 //      per XCD; per-queue prefix sums give each entry's first tile;
 //   4. expand every queue into one 16-byte entry per tile (group, configuration,
-//      kind, tile coordinates, first sorted row and rows of the group), so that
-//      a workgroup resolves a popped tile with a single load.
+//      kind, slices, tile coordinates, first sorted row and rows of the group),
+//      so that a workgroup resolves a popped tile with a single load.
+// Groups may be sliced along the reduction (split-K, see split_rule): their
+// slices are queued as extra channel tiles, within fixed budgets of added
+// tiles and of partial-sum storage.
 #include "group_gemm_impl.h"
 
 namespace mxmoe {
@@ -61,16 +64,19 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
                                                     const int32_t* __restrict__ counts,
                                                     const int32_t* __restrict__ offsets, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
-                                                    int qcap, int fcap, int32_t* __restrict__ down_qmax) {
+                                                    int qcap, int fcap, int64_t pfloats,
+                                                    int32_t* __restrict__ down_qmax) {
   __shared__ int32_t s_cost[2][2048];
-  __shared__ int32_t s_tiles[2][2048];
+  __shared__ int32_t s_tiles[2][2048];  // queued tiles (output tiles x slices)
   __shared__ int32_t s_red[1025];
   __shared__ int32_t s_ns[2048];
+  __shared__ int32_t s_used[2];         // output-tile counters used per phase
   const int tid = threadIdx.x;
   const int nphase = raw_m >= 0 ? 1 : 2;
   const PlanLayout PL = plan_layout(G, qcap, fcap);
   int32_t* misc = plan + PL.misc;
   if (tid == 0) misc[4] = 0;
+  // 1. per group: rows, configuration, output tiles, proposed slices
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
@@ -81,31 +87,77 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       const int bm = cfg_bm(cfg), bn = cfg_bn(cfg, phase_eff);
       const int mt = m > 0 ? (m + bm - 1) / bm : 0;
       const int nt = (L.n + bn - 1) / bn;
-      const int tiles = mt * nt;
-      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
-      const int kd = L.kind;
-      const double wbytes = (double)nl * bn * L.k * kind_wbits(kd) / 8.0;
-      const double abytes = (double)bm * L.k * (kind_is_int(kd) ? 1.0 : 2.0);
-      const double flops = 2.0 * nl * bm * bn * L.k;
-      // per-CU shares of MI355X peaks: 8 TB/s HBM, 2.5 PF 16-bit / 5 POPS int8 MFMA
-      const double t_mem = (wbytes + abytes) * 32.0;  // ps
-      const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
-      double c = t_mem > t_mma ? t_mem : t_mma;
-      if (c > 2.0e9) c = 2.0e9;
       int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
       r[PF_EXPERT] = g;
       r[PF_M] = m;
       r[PF_CFG] = cfg;
       r[PF_MTILES] = mt;
       r[PF_NTILES] = nt;
-      r[PF_COST] = tiles ? (int32_t)c : 0;
       r[PF_START] = 0;
-      s_cost[ph][g] = tiles ? (int32_t)c : 0;
-      s_tiles[ph][g] = tiles;
+      r[PF_SPLIT] = split_rule(cfg, mt * nt, L.k / 128);
+      r[PF_PBASE] = 0;
+      r[PF_CBASE] = 0;
       if (ph == 0 && raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
     }
   }
   __syncthreads();
+  // 2. slices within the budgets, in group order (one thread per phase)
+  if (tid < nphase) {
+    const int ph = tid;
+    int64_t pused = 0;
+    int eused = 0, cused = 0;
+    for (int g = 0; g < G; ++g) {
+      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+      const int sp = r[PF_SPLIT];
+      if (sp <= 1) continue;
+      const int cfg = r[PF_CFG], tiles = r[PF_MTILES] * r[PF_NTILES];
+      const int phase_eff = raw_m >= 0 ? 1 : ph;
+      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
+      const int64_t need = (int64_t)tiles * sp * cfg_bm(cfg) * cfg_bn(cfg, phase_eff) * nl;
+      const int extra = tiles * (sp - 1);
+      if (pused + need > pfloats || eused + extra > kSplitExtra) {
+        r[PF_SPLIT] = 1;
+        continue;
+      }
+      r[PF_PBASE] = (int32_t)pused;
+      r[PF_CBASE] = cused;
+      pused += need;
+      eused += extra;
+      cused += tiles;
+    }
+    s_used[ph] = cused;
+    misc[6 + ph] = (int32_t)pused;
+  }
+  __syncthreads();
+  // 3. per-tile cost estimate with the final slices, arrival counters cleared
+  for (int ph = 0; ph < nphase; ++ph) {
+    for (int g = tid; g < G; g += blockDim.x) {
+      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+      const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
+      const int cfg = r[PF_CFG], sp = r[PF_SPLIT];
+      const int tiles = r[PF_MTILES] * r[PF_NTILES] * sp;
+      const int phase_eff = raw_m >= 0 ? 1 : ph;
+      const int bm = cfg_bm(cfg), bn = cfg_bn(cfg, phase_eff);
+      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
+      const int kd = L.kind;
+      const double kk = (double)((L.k / 128 + sp - 1) / sp) * 128.0;  // reduction length of one slice
+      const double wbytes = (double)nl * bn * kk * kind_wbits(kd) / 8.0;
+      const double abytes = (double)bm * kk * (kind_is_int(kd) ? 1.0 : 2.0);
+      const double flops = 2.0 * nl * bm * bn * kk;
+      // per-CU shares of MI355X peaks: 8 TB/s HBM, 2.5 PF 16-bit / 5 POPS int8 MFMA
+      const double t_mem = (wbytes + abytes) * 32.0;  // ps
+      const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
+      double c = t_mem > t_mma ? t_mem : t_mma;
+      if (c > 2.0e9) c = 2.0e9;
+      r[PF_COST] = tiles ? (int32_t)c : 0;
+      s_cost[ph][g] = tiles ? (int32_t)c : 0;
+      s_tiles[ph][g] = tiles;
+    }
+    int32_t* cnt = plan + PL.cnt + (int64_t)ph * kSplitExtra;
+    for (int i = tid; i < s_used[ph]; i += blockDim.x) cnt[i] = 0;
+  }
+  __syncthreads();
+  // 4. rank the groups by decreasing tile cost (ties: lower group first)
   int32_t* order = plan + PL.order;
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
@@ -124,13 +176,14 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     }
   }
   __syncthreads();
+  // 5. super-tiles dealt to the XCD queues, 6. expanded to tile entries
   for (int ph = 0; ph < nphase; ++ph) {
     int ng = 0;
     for (int g = 0; g < G; ++g) ng += s_tiles[ph][g] > 0;  // same value in every thread
     for (int r = ng + tid; r < G; r += blockDim.x) order[(int64_t)ph * G + r] = -1;
     for (int r = tid; r < ng; r += blockDim.x) {
       const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + order[(int64_t)ph * G + r]) * PF_N;
-      s_ns[r] = super_tiles(rec[PF_MTILES], rec[PF_NTILES]);
+      s_ns[r] = super_tiles(rec[PF_MTILES], rec[PF_NTILES] * rec[PF_SPLIT]);
     }
     __syncthreads();
     const int S = block_scan(s_ns, ng, s_red);  // s_ns[r]: first global super-tile of rank r
@@ -152,7 +205,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       int32_t* e = ent + ((int64_t)(u % kXcd) * qcap + u / kXcd) * 3;
       e[0] = g;
       e[1] = s;
-      e[2] = super_tile_size(rec[PF_MTILES], rec[PF_NTILES], s);
+      e[2] = super_tile_size(rec[PF_MTILES], rec[PF_NTILES] * rec[PF_SPLIT], s);
     }
     __syncthreads();
     int32_t* ctr = plan + PL.ctr + (int64_t)ph * kXcd * 4;
@@ -175,20 +228,21 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       const int32_t* e = ent + ((int64_t)x * qcap + pos) * 3;
       const int g = e[0], st = e[1], first = e[2];
       const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      const int mt = rec[PF_MTILES], nt = rec[PF_NTILES];
-      const int size = super_tile_size(mt, nt, st);
+      const int sp = rec[PF_SPLIT];
+      const int mt = rec[PF_MTILES], ntv = rec[PF_NTILES] * sp;
+      const int size = super_tile_size(mt, ntv, st);
       if (first + size > fcap) {  // cannot happen with the host's capacity bound
         misc[4] = 1;
         continue;
       }
       const int kd = raw_m >= 0 ? raw_lin.kind : experts[g].lin[ph == 0 ? 0 : 2].kind;
-      const int w0 = tile_word0(g, rec[PF_CFG], kd);
+      const int w0 = tile_word0(g, rec[PF_CFG], kd, sp);
       const int off_e = (raw_m < 0 && g < E) ? offsets[g] : 0;
       const int m_g = rec[PF_M];
       int32_t* f = flat + ((int64_t)x * fcap + first) * 4;
       for (int t = 0; t < size; ++t) {
         int mi, ni;
-        super_tile_pos(mt, nt, st, t, &mi, &ni);
+        super_tile_pos(mt, ntv, st, t, &mi, &ni);
         *reinterpret_cast<int4*>(f + 4 * t) = make_int4(w0, mi | (ni << 16), off_e, m_g);
       }
     }
@@ -211,11 +265,11 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
 
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int qcap, int fcap, int32_t* down_qmax, hipStream_t s) {
+                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, hipStream_t s) {
   MaskBits mb;
   for (int i = 0; i < 64; ++i) mb.w[i] = mask_words ? mask_words[i] : 0xffffffffu;
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin, mb,
-                     plan, qcap, fcap, down_qmax);
+                     plan, qcap, fcap, pfloats, down_qmax);
   return hipGetLastError();
 }
 

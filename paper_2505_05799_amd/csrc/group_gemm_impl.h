@@ -203,6 +203,34 @@ template <int N> __device__ inline void wait_vmem() {
 // the direct-to-LDS stage loads are covered by wait_vmem before this barrier.
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
+// Device-scope coherent 16-byte store and load (scope bit sc1), used for
+// partial sums that another XCD reads within the same launch.  The store is
+// followed by wait states: the compiler, which does not look into the asm,
+// may overwrite the data registers in the next instruction, and a store wider
+// than 8 bytes still reads them then.  The load is asynchronous: wait_loaded()
+// must run before its result is used.
+__device__ inline void store_coherent(float* p, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1\n\ts_nop 1" ::"v"(p), "v"(v) : "memory");
+}
+__device__ inline u32x4 load_coherent(const float* p) {
+  u32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// Wait for every outstanding vector-memory load; the registers of v are tied
+// to the wait so that no use of them is scheduled before it.
+template <int N> __device__ inline void wait_loaded(u32x4 (&v)[N]) {
+  if constexpr (N == 1) asm volatile("s_waitcnt vmcnt(0)" : "+v"(v[0])::"memory");
+  else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(0)" : "+v"(v[0]), "+v"(v[1])::"memory");
+  else if constexpr (N == 4)
+    asm volatile("s_waitcnt vmcnt(0)" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3])::"memory");
+  else {
+    static_assert(N == 8, "fragment count");
+    asm volatile("s_waitcnt vmcnt(0)"
+                 : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7])::"memory");
+  }
+}
+
 // bias constant b = 2^N - 1 of the exact magic-number dequantization
 template <int KD> constexpr int wbias() { return KD == K_W2G ? 3 : (KD == K_W3G ? 7 : 15); }
 
@@ -278,6 +306,7 @@ struct __align__(16) Smem {
   int4 entry;                    // the next tile (plan tile entry; group -1: none left)
   int32_t qtotal[kXcd];          // tiles per XCD queue
   int32_t qi;                    // queues tried so far by this workgroup
+  int32_t last;                  // split-K: this workgroup finishes the output tile
 };
 
 // Tile queues of one phase, rebuilt from the kernel arguments where needed so
@@ -409,8 +438,8 @@ template <int ACT, int MF> __device__ inline void stage_rowsum(Smem& sm, int buf
 
 // ---------------------------------------------------------- tile body
 template <int KD, int ACT, int CFG, int PHASE>
-__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
-                                int off_e) {
+__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int ntv,
+                                int off_e, int split) {
   constexpr int MF = cfg_mf(CFG);
   constexpr int NF = cfg_nf(CFG, PHASE == 0 ? 0 : 1);
   constexpr int NL = PHASE == 0 ? 2 : 1;
@@ -437,6 +466,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   else { lins[0] = &a.raw_lin; }
   const int N = lins[0]->n, K = lins[0]->k;
   const int kblocks = K / 128;
+  // split-K: queued channel tile ntv = slice * (channel tiles) + channel tile;
+  // the slice reduces k blocks [kb0, kb1), balanced so that every slice is
+  // non-empty (the plan only slices when there are >= 4 k blocks per slice)
+  const int ntr = (N + BN - 1) / BN;
+  const int slice = split > 1 ? ntv / ntr : 0;
+  const int nt = ntv - slice * ntr;
+  const int kb0 = slice * kblocks / split;
+  const int kb1 = (slice + 1) * kblocks / split;
   const int row0 = mt * BM;
   const int nb0 = (nt * BN) / 16 + wave * NF;   // first 16-channel block of this wavefront
   int nvalid = N / 16 - nb0;
@@ -547,11 +584,11 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // this many leaves the weight prefetch in flight across the barrier.
   constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (WONLY ? NL * NF : 0);
 
-  stage_load<INT, BM>(sm, 0, abase, soffs, 0, wave);
-  load_group(0, false);
+  stage_load<INT, BM>(sm, 0, abase, soffs, kb0, wave);
+  load_group(kb0, false);
   if constexpr (streamed<KD>()) {
 #pragma unroll
-    for (int j = 0; j < J; ++j) load_steps(0, false, j);
+    for (int j = 0; j < J; ++j) load_steps(kb0, false, j);
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -560,9 +597,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     __syncthreads();
   }
 
-  for (int kb = 0; kb < kblocks; ++kb) {
-    const int cur = kb & 1;
-    const bool more = kb + 1 < kblocks;
+  for (int kb = kb0; kb < kb1; ++kb) {
+    const int cur = (kb - kb0) & 1;
+    const bool more = kb + 1 < kb1;
     if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
@@ -586,7 +623,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             bz[l][nf] = base + (uint32_t)(wbias<KD>() - (int)z) * 0x00010001u;
           }
           // move the running sum into units of this group's scale
-          const float r = kb ? s_prev[l][nf] * __builtin_amdgcn_rcpf(s) : 0.f;
+          const float r = kb != kb0 ? s_prev[l][nf] * __builtin_amdgcn_rcpf(s) : 0.f;
           s_prev[l][nf] = s;
 #pragma unroll
           for (int mf = 0; mf < MF; ++mf) {
@@ -676,6 +713,66 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     }
   }
 
+  // ---- split-K: partial sums of this slice; the last slice to arrive adds
+  // all slices' partials in slice order and runs the epilogue
+  bool finish = true;
+  if (split > 1) {
+    if constexpr (WONLY) {  // partials carry their last group's scale
+#pragma unroll
+      for (int l = 0; l < NL; ++l)
+#pragma unroll
+        for (int nf = 0; nf < NF; ++nf) {
+#pragma unroll
+          for (int mf = 0; mf < MF; ++mf) acc[l][nf][mf] = acc[l][nf][mf] * s_prev[l][nf];
+          s_prev[l][nf] = 1.f;
+        }
+    }
+    constexpr int AREA = BM * BN * NL;  // floats per slice of one output tile
+    const int pidx = PHASE == kPhaseRaw ? 0 : PHASE;
+    const PlanLayout PL = plan_layout(a.G, a.qcap, a.fcap);
+    const int32_t* rec = a.plan + PL.rec + ((int64_t)pidx * a.G + g) * PF_N;
+    const int otile = mt * ntr + nt;
+    int32_t* cnt = a.plan + PL.cnt + (int64_t)pidx * kSplitExtra + rec[PF_CBASE] + otile;
+    float* part = a.partial + rec[PF_PBASE] + (int64_t)otile * split * AREA;
+    auto at_of = [&](int l, int nf, int mf) {  // this lane's 16 bytes of a fragment
+      return ((((wave * NL + l) * NF + nf) * MF + mf) * 64 + lane) * 4;
+    };
+    // The partials are stored and loaded with device-scope coherent accesses
+    // (write-through past this XCD's L2, and re-fetched on the reading side),
+    // so that slices run on different XCDs see each other's sums without
+    // writing back or invalidating whole L2 caches.
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf)
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf)
+          store_coherent(part + (int64_t)slice * AREA + at_of(l, nf, mf), __builtin_bit_cast(u32x4, acc[l][nf][mf]));
+    wait_vmem<0>();  // this wavefront's partials are written
+    __syncthreads();
+    if (tid == 0) sm.last = atomicAdd(cnt, 1) == split - 1;
+    __syncthreads();
+    finish = sm.last;
+    if (finish) {
+      // every slice (this one included) is read back and summed in slice
+      // order, so the result does not depend on which slice finished last
+#pragma unroll
+      for (int l = 0; l < NL; ++l)
+#pragma unroll
+        for (int nf = 0; nf < NF; ++nf)
+          for (int sl = 0; sl < split; ++sl) {
+            u32x4 v[MF];
+#pragma unroll
+            for (int mf = 0; mf < MF; ++mf) v[mf] = load_coherent(part + (int64_t)sl * AREA + at_of(l, nf, mf));
+            wait_loaded<MF>(v);
+#pragma unroll
+            for (int mf = 0; mf < MF; ++mf)
+              acc[l][nf][mf] = sl == 0 ? __builtin_bit_cast(AccT, v[mf]) : acc[l][nf][mf] + __builtin_bit_cast(AccT, v[mf]);
+          }
+      if (tid == 0) *cnt = 0;  // ready for the next forward
+    }
+  }
+
   // ---- epilogue: lane holds rows 4q + i of fragment mf, channel li of fragment nf
   // (the per-row data is re-read from LDS for every fragment: holding it for
   // all fragments would cost 64-96 registers next to the accumulators)
@@ -734,22 +831,24 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       }
     }
   };
-  if (full) epilogue(std::false_type{});
-  else epilogue(std::true_type{});
+  if (finish) {
+    if (full) epilogue(std::false_type{});
+    else epilogue(std::true_type{});
+  }
   __syncthreads();  // the next tile rewrites rowsrc and the stages
 }
 
 template <int ACT, int PHASE, int CFG>
 __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
-                                     int off_e, int kd) {
+                                     int off_e, int kd, int split) {
   switch (kd) {
-    case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
-    case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e); break;
+    case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     default: break;
   }
 }
@@ -772,16 +871,16 @@ __global__ void __launch_bounds__(kThreads, 2) group_gemm_kernel(GemmArgs a) {
     const int w1 = __builtin_amdgcn_readfirstlane(sm.entry.y);
     const int off_e = __builtin_amdgcn_readfirstlane(sm.entry.z);
     const int m_g = __builtin_amdgcn_readfirstlane(sm.entry.w);
-    const int g = w0 & 0xFFFF, cfg = (w0 >> 16) & 15, kd = w0 >> 20;
+    const int g = w0 & 0xFFFF, cfg = (w0 >> 16) & 15, kd = (w0 >> 20) & 15, split = ((w0 >> 24) & 7) + 1;
     const int mt = w1 & 0xFFFF, nt = w1 >> 16;
     const DevExpert* ex = PHASE == kPhaseRaw ? nullptr : a.experts + g;
     // (every thread has read the entry: run_tile passes a barrier before
     // thread 0 claims the next tile into it)
     switch (cfg) {
-      case CFG_S: dispatch_kind<ACT, PHASE, CFG_S>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
-      case CFG_T: dispatch_kind<ACT, PHASE, CFG_T>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
-      case CFG_M: dispatch_kind<ACT, PHASE, CFG_M>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
-      default: dispatch_kind<ACT, PHASE, CFG_L>(sm, a, ex, g, m_g, mt, nt, off_e, kd); break;
+      case CFG_S: dispatch_kind<ACT, PHASE, CFG_S>(sm, a, ex, g, m_g, mt, nt, off_e, kd, split); break;
+      case CFG_T: dispatch_kind<ACT, PHASE, CFG_T>(sm, a, ex, g, m_g, mt, nt, off_e, kd, split); break;
+      case CFG_M: dispatch_kind<ACT, PHASE, CFG_M>(sm, a, ex, g, m_g, mt, nt, off_e, kd, split); break;
+      default: dispatch_kind<ACT, PHASE, CFG_L>(sm, a, ex, g, m_g, mt, nt, off_e, kd, split); break;
     }
   }
 }

@@ -90,11 +90,21 @@ struct DevHeader {
 // All use 256 threads (4 wavefronts stacked along the output channels).
 enum Cfg : int32_t { CFG_S = 0, CFG_T = 1, CFG_M = 2, CFG_L = 3, CFG_COUNT = 4 };
 
-// Plan record per (phase, expert): int32 fields.
+// Plan record per (phase, expert): int32 fields.  A group of mt x nt output
+// tiles whose reduction is sliced S ways (split-K, the paper's slice-K tile
+// parameter) is queued as mt x (S nt) tiles: channel tile index n' = s nt + n.
+// Every slice writes its partial sums to the partial buffer (floats from
+// PF_PBASE, BM x BN x linears per slice) and bumps the output tile's counter
+// (PF_CBASE + tile); the last slice to arrive adds the partials in slice order
+// and runs the epilogue.
 enum PlanField : int32_t {
   PF_EXPERT = 0, PF_M = 1, PF_CFG = 2, PF_MTILES = 3, PF_NTILES = 4,
-  PF_START = 5, PF_COST = 6, PF_RANK = 7, PF_N = 8
+  PF_START = 5, PF_COST = 6, PF_RANK = 7, PF_SPLIT = 8, PF_PBASE = 9, PF_CBASE = 10, PF_N = 12
 };
+// Split-K budgets per phase: at most kSplitExtra tiles added by slicing (and
+// as many output-tile counters); the partial buffer size comes from the host.
+constexpr int kSplitExtra = 16384;
+constexpr int kSplitMax = 8;
 
 // Tiles are grouped into super-tiles of up to 64 tiles sharing row and channel
 // blocks (min(mt, 8) x min(nt, 64 / that) tiles) and dealt round-robin to one
@@ -111,9 +121,11 @@ constexpr int kSuperTiles = 64;
 //   ent   [2][kXcd][cap][3]   queue entries: group, super-tile index, first tile
 //   ctr   [2][kXcd][4]        per queue: head, total tiles, entries, -
 //   misc  [16]                [2 + p]: number of groups with tiles in phase p,
-//                             [4]: 1 if a queue overflowed its capacity
-//   flat  [2][kXcd][fcap][4]  the queues expanded to one entry per tile (TileEntry)
-struct PlanLayout { int64_t rec, order, ent, ctr, misc, flat, total; };
+//                             [4]: 1 if a queue overflowed its capacity,
+//                             [6 + p]: partial-buffer floats used in phase p
+//   flat  [2][kXcd][fcap][4]  the queues expanded to one entry per tile
+//   cnt   [2][kSplitExtra]    arrival counters of sliced output tiles
+struct PlanLayout { int64_t rec, order, ent, ctr, misc, flat, cnt, total; };
 __host__ __device__ inline PlanLayout plan_layout(int G, int cap, int fcap) {
   PlanLayout L;
   L.rec = 0;
@@ -123,32 +135,55 @@ __host__ __device__ inline PlanLayout plan_layout(int G, int cap, int fcap) {
   L.ctr = L.ent + 2LL * kXcd * cap * 3;
   L.misc = L.ctr + 2LL * kXcd * 4;
   L.flat = L.misc + 16;
-  L.total = L.flat + 2LL * kXcd * fcap * 4;
+  L.cnt = L.flat + 2LL * kXcd * fcap * 4;
+  L.total = L.cnt + 2LL * kSplitExtra;
   return L;
 }
 // Per-queue capacity bound from the rows and channel counts (host side):
 // super-tiles of a group <= (mt/8 + 1)(nt/8 + 1) with mt <= m/1024*8 + 1,
-// nt <= N/64 + 1 (smallest tiles are 16 x 64 per linear).
+// nt <= N/64 + 1 (smallest tiles are 16 x 64 per linear), plus the super-tiles
+// that slicing adds (at most one per added tile, dealt round-robin).
 __host__ __device__ inline int plan_queue_cap(int64_t rows_total, int groups, int n_max) {
   const int64_t s = (rows_total / 1024 + 2LL * groups + 1) * ((int64_t)n_max / 512 + 2);
-  return (int)(s / kXcd + 2);
+  return (int)(s / kXcd + 2 + kSplitExtra / kXcd + 1);
 }
-// Per-queue tile capacity: at most 64 tiles per queue entry.
-__host__ __device__ inline int plan_flat_cap(int qcap) { return qcap * kSuperTiles; }
+// Per-queue tile capacity: at most 64 tiles per unsliced queue entry, plus
+// every tile that slicing adds.
+__host__ __device__ inline int plan_flat_cap(int qcap) {
+  return (qcap - kSplitExtra / kXcd - 1) * kSuperTiles + kSplitExtra;
+}
 
 // One tile of a queue, as the Group-GEMM pops it (int32 x 4):
-//   [0] group | cfg << 16 | kind << 20   [1] row tile | channel tile << 16
+//   [0] group | cfg << 16 | kind << 20 | (slices - 1) << 24
+//   [1] row tile | channel tile n' << 16 (n' = slice * channel tiles + channel tile)
 //   [2] first sorted row of the group (0 for shared experts and single linears)
 //   [3] rows of the group
-__host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind) { return g | (cfg << 16) | (kind << 20); }
+__host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int split) {
+  return g | (cfg << 16) | (kind << 20) | ((split - 1) << 24);
+}
+// Slices of a group (split-K): groups of at most 64 rows (bandwidth-bound
+// tiles) are sliced into runs of at least 4 k blocks, up to kSplitMax; 128-row
+// groups only when they have fewer than 128 tiles and at least 32 k blocks, so
+// that their long tiles do not trail the schedule.
+__host__ __device__ inline int split_rule(int cfg, int tiles, int kblocks) {
+  if (tiles <= 0) return 1;
+  if (cfg != CFG_L) {
+    const int s = kblocks / 4;
+    return s < 1 ? 1 : (s > kSplitMax ? kSplitMax : s);
+  }
+  if (tiles < 128 && kblocks >= 32) return kblocks / 16 < 4 ? kblocks / 16 : 4;
+  return 1;
+}
 
 // Workspace layout (byte offsets), shared by host code of the forward.
 struct WsLayout {
   size_t status, counts, offsets, sorted_pair, inv, chunk_counts, chunk_bad, plan, down_qmax;
   size_t rtok, rslot, rgw, rxs8, rxs4;
   size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
+  size_t partial;  // fp32 split-K partial sums (both phases reuse it)
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
+  int64_t pfloats;  // size of the partial buffer
 };
 
 constexpr int kRouteChunk = 2048;  // pairs per routing workgroup
@@ -202,6 +237,7 @@ struct GemmArgs {
   int32_t n_shared;
   int32_t qcap;        // capacity of each XCD queue in the plan region (super-tiles)
   int32_t fcap;        // capacity of each XCD queue in the plan region (tiles)
+  float* partial;      // split-K partial sums
   // per sorted row (see launch_row_meta)
   const int32_t* rtok; const int32_t* rslot; const float* rgw; const float* rxs8; const float* rxs4;
   // single-linear mode (mxmoe_linear_forward): raw int32 / fp32 output
@@ -213,7 +249,7 @@ struct GemmArgs {
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int qcap, int fcap, int32_t* down_qmax, hipStream_t s);
+                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, hipStream_t s);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

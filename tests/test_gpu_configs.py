@@ -36,17 +36,20 @@ def sample_tokens(blk, n_random=10, seed=0):
 KIND = {"w16": 0, "w8a8": 1, "w4a4": 2, "w2g128": 3, "w3g128": 4, "w4g128": 5, "w8g128": 6}
 
 
+PF_N = 12  # int32 fields per group record of the tile plan
+
+
 def plan_flat(mb, T, G, cap, phase):
     torch = torch_mod()
     fcap = mb.workspace_layout(T)["plan_flat_cap"]
-    o_flat = ((2 * G * 8 + 2 * G + 3) & ~3) + 2 * 8 * cap * 3 + 64 + 16
+    o_flat = ((2 * G * PF_N + 2 * G + 3) & ~3) + 2 * 8 * cap * 3 + 64 + 16
     p = mb.ws_view("plan", torch.int32, o_flat + 2 * 8 * fcap * 4, T).cpu().numpy()
     return p[o_flat + phase * 8 * fcap * 4: o_flat + (phase + 1) * 8 * fcap * 4].reshape(8, fcap, 4)
 
 
 def plan_misc(mb, T, G, cap):
     torch = torch_mod()
-    o_ctr = ((2 * G * 8 + 2 * G + 3) & ~3) + 2 * 8 * cap * 3
+    o_ctr = ((2 * G * PF_N + 2 * G + 3) & ~3) + 2 * 8 * cap * 3
     p = mb.ws_view("plan", torch.int32, o_ctr + 64 + 16, T).cpu().numpy()
     return p[o_ctr + 64: o_ctr + 80]
 
@@ -76,21 +79,23 @@ def test_full_workload(name):
 
     # tile plan, bit-exact: configuration, tile counts, cost, rank, queue order,
     # and the per-XCD queues of super-tiles
-    cap = mb.workspace_layout(T)["plan_queue_cap"]
-    o_ord = 2 * G * 8
+    lay = mb.workspace_layout(T)
+    cap = lay["plan_queue_cap"]
+    o_ord = 2 * G * PF_N
     o_ent = (o_ord + 2 * G + 3) & ~3
     o_ctr = o_ent + 2 * 8 * cap * 3
     plan = mb.ws_view("plan", torch.int32, o_ctr + 2 * 8 * 4, T).cpu().numpy()
-    rec = plan[: 2 * G * 8].reshape(2, G, 8)
+    rec = plan[: 2 * G * PF_N].reshape(2, G, PF_N)
     ms = list(r["counts"]) + [T] * cfg.n_shared
     for phase in (0, 1):
         lins = [blk.linears[g][0 if phase == 0 else 2] for g in range(G)]
-        want, order = O.tile_plan(ms, lins, phase)
+        want, order = O.tile_plan(ms, lins, phase, partial_floats=lay["partial_floats"])
         for g in range(G):
             got = rec[phase, g]
             assert got[1] == ms[g] and got[2] == want[g]["cfg"], (phase, g)
             assert got[3] == want[g]["mtiles"] and got[4] == want[g]["ntiles"], (phase, g)
             assert got[6] == want[g]["cost"] and got[7] == want[g]["rank"], (phase, g)
+            assert got[8] == want[g]["split"], (phase, g)
         q = plan[o_ord + phase * G: o_ord + (phase + 1) * G]
         assert q[: len(order)].tolist() == order
         queues, totals = O.xcd_queues(want, order)
@@ -105,7 +110,8 @@ def test_full_workload(name):
         offs = r["offsets"]
         fl = plan_flat(mb, T, G, cap, phase)
         for x in range(8):
-            exp = np.array([[g | (want[g]["cfg"] << 16) | (KIND[lins[g].scheme.name] << 20), mi | (ni << 16),
+            exp = np.array([[g | (want[g]["cfg"] << 16) | (KIND[lins[g].scheme.name] << 20)
+                             | ((want[g]["split"] - 1) << 24), mi | (ni << 16),
                              offs[g] if g < E else 0, ms[g]] for g, mi, ni in tiles[x]], dtype=np.int64)
             assert np.array_equal(fl[x, : len(tiles[x])].astype(np.int64), exp.reshape(-1, 4)), (phase, x)
     assert plan_misc(mb, T, G, cap)[4] == 0      # no queue overflow

@@ -389,7 +389,7 @@ def test_tile_plan_covers_every_output(name):
                           (cfg.F_shared if phase == 0 else cfg.H),
                           k if e < cfg.E else (cfg.H if phase == 0 else cfg.F_shared), None)
                 for e, s in enumerate(W.schemes_of(cfg))]
-        plan, order = O.tile_plan(counts, lins, phase)
+        plan, order = O.tile_plan(counts, lins, phase, partial_floats=1 << 26)
         for m, lin, r in zip(counts, lins, plan):
             bm = (16, 32, 64, 128)[r["cfg"]]
             bn = ((256, 256, 128, 128), (512, 512, 256, 256))[phase][r["cfg"]]
@@ -404,7 +404,11 @@ def test_tile_plan_covers_every_output(name):
         tiles = O.xcd_tiles(plan, order)
         assert [len(t) for t in tiles] == totals
         flat = [t for q in tiles for t in q]
-        want = [(g, mi, ni) for g in order for mi in range(plan[g]["mtiles"]) for ni in range(plan[g]["ntiles"])]
+        want = [(g, mi, ni) for g in order for mi in range(plan[g]["mtiles"])
+                for ni in range(plan[g]["ntiles"] * plan[g]["split"])]
+        for g, r in enumerate(plan):  # slices: at least 4 k blocks each, at most 8
+            k = lins[g].k // 128
+            assert 1 <= r["split"] <= 8 and (r["split"] == 1 or k // r["split"] >= 4)
         assert sorted(flat) == sorted(want) and len(flat) == len(set(flat))
         rank = {g: i for i, g in enumerate(order)}
         for q in tiles:
