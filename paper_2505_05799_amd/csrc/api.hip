@@ -10,10 +10,6 @@ using namespace mxmoe;
 
 namespace {
 
-constexpr int kMaxE = 1024;
-constexpr int kMaxShared = 64;
-constexpr int kMaxG = 2048;
-
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // scheme -> micro-kernel kind, -1 if unsupported

@@ -68,45 +68,189 @@ __global__ void __launch_bounds__(kThreads) act_quant_kernel(const void* a, int 
   quant_row(a, r * ld, cols, act, qmax, codes + r * cols, scales + r, red);
 }
 
-__global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, int act, int F,
+// ---- one wavefront per row, 16-byte loads (8 elements per lane and chunk)
+constexpr int kRowsPerBlock = kThreads / 64;
+
+__device__ inline void unpack8(uint4 u, int act, float* f) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (act == MXMOE_BF16) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    } else {
+      const uint16_t lo = (uint16_t)w[i], hi = (uint16_t)(w[i] >> 16);
+      f[2 * i] = (float)__builtin_bit_cast(_Float16, lo);
+      f[2 * i + 1] = (float)__builtin_bit_cast(_Float16, hi);
+    }
+  }
+}
+
+// Largest magnitude of 8 elements as 16-bit magnitude bits (sign cleared,
+// NaNs as 0): for non-negative values the bit order is the value order, so the
+// row maximum equals the fmaxf reduction of quant_row, which skips NaNs.
+__device__ inline uint32_t amax8_bits(uint4 u, uint32_t nan_lo) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+  uint32_t m = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = w[i] & 0x7fffu, hi = (w[i] >> 16) & 0x7fffu;
+    m = max(m, lo < nan_lo ? lo : 0u);
+    m = max(m, hi < nan_lo ? hi : 0u);
+  }
+  return m;
+}
+__device__ inline float bits_to_f32(uint32_t b, int act) {
+  if (act == MXMOE_BF16) return __uint_as_float(b << 16);
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)b);
+}
+
+// codes of 8 elements with the same fp32 recipe as quant_row
+__device__ inline uint2 codes8(uint4 u, int act, float inv, float q) {
+  float f[8];
+  unpack8(u, act, f);
+  uint32_t w[2] = {0u, 0u};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float r = __builtin_rintf(__fmul_rn(f[i], inv));
+    r = fminf(fmaxf(r, -q), q);
+    w[i >> 2] |= ((uint32_t)(uint8_t)(int8_t)(int)r) << (8 * (i & 3));
+  }
+  return make_uint2(w[0], w[1]);
+}
+
+// Quantizes one row of cols (a multiple of 8) elements with W wavefronts (1:
+// each wavefront of the workgroup takes its own row, 4: the workgroup takes
+// one row).  NC > 0: the row's 16-byte chunks stay in registers
+// (cols <= 512 * W * NC); NC == 0: any length, the row is read twice.
+template <int NC, int W>
+__device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, int act, int qmax,
+                                     uint2* __restrict__ codes, float* __restrict__ scale, uint32_t* red) {
+  const int idx = W == 1 ? (threadIdx.x & 63) : threadIdx.x, nch = cols >> 3;
+  constexpr int kStride = 64 * W;
+  const uint32_t nan_lo = act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;  // smallest NaN magnitude
+  const float q = (float)qmax;
+  uint32_t mb = 0u;
+  uint4 v[NC > 0 ? NC : 1];
+  if constexpr (NC > 0) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = idx + kStride * i;
+      v[i] = c < nch ? row[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int i = 0; i < NC; ++i) mb = max(mb, amax8_bits(v[i], nan_lo));
+  } else {
+    for (int c = idx; c < nch; c += kStride) mb = max(mb, amax8_bits(row[c], nan_lo));
+  }
+  for (int d = 32; d > 0; d >>= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, d, 64));
+  if constexpr (W > 1) {
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mb;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < W; ++i) mb = max(mb, red[i]);
+  }
+  const float amax = bits_to_f32(mb, act);
+  float inv = 0.f, s = 0.f;
+  if (amax > 0.f) {
+    inv = __fdiv_rn(q, amax);
+    s = __fdiv_rn(amax, q);
+  }
+  if constexpr (NC > 0) {
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+      const int c = idx + kStride * i;
+      if (c < nch) codes[c] = codes8(v[i], act, inv, q);
+    }
+  } else {
+    for (int c = idx; c < nch; c += kStride) codes[c] = codes8(row[c], act, inv, q);
+  }
+  if (idx == 0) *scale = s;
+}
+
+// row handled by this thread: W == 1 one per wavefront, W == 4 one per workgroup
+template <int W> __device__ inline int64_t my_row() {
+  return W == 1 ? (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6) : (int64_t)blockIdx.x;
+}
+
+template <int NC, int W>
+__global__ void __launch_bounds__(kThreads) act_quant_vec_kernel(const void* a, int act, int rows, int cols,
+                                                                 int64_t ld, int qmax, int8_t* codes,
+                                                                 float* scales) {
+  __shared__ uint32_t red[kThreads / 64];
+  const int64_t r = my_row<W>();
+  if (r >= rows) return;
+  quant_row_vec<NC, W>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a) + r * ld), cols, act,
+                       qmax, reinterpret_cast<uint2*>(codes + r * cols), scales + r, red);
+}
+
+// Rows of the sorted (token, slot) pairs whose expert's down projection takes
+// a8/a4 activations; the expert of a row is found in an LDS copy of offsets.
+template <int NC, int W>
+__global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, int act, int P, int F,
                                                                  const int32_t* __restrict__ offsets, int E,
                                                                  const int32_t* __restrict__ down_qmax,
                                                                  int8_t* hq, float* hs) {
-  __shared__ float red[kThreads / 64];
-  const int r = blockIdx.x;
-  if (r >= offsets[E]) return;
+  __shared__ int32_t s_off[kMaxE + 1];
+  __shared__ uint32_t red[kThreads / 64];
+  for (int i = threadIdx.x; i <= E; i += kThreads) s_off[i] = offsets[i];
+  __syncthreads();
+  const int r = (int)my_row<W>();
+  if (r >= P || r >= s_off[E]) return;
   int lo = 0, hi = E;  // largest e with offsets[e] <= r
   while (hi - lo > 1) {
-    int mid = (lo + hi) >> 1;
-    if (offsets[mid] <= r) lo = mid; else hi = mid;
+    const int mid = (lo + hi) >> 1;
+    if (s_off[mid] <= r) lo = mid; else hi = mid;
   }
   const int qmax = down_qmax[lo];
   if (qmax == 0) return;
-  quant_row(h, (int64_t)r * F, F, act, qmax, hq + (int64_t)r * F, hs + r, red);
+  quant_row_vec<NC, W>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F,
+                       act, qmax, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hs + r, red);
 }
 
+// 8 outputs per thread.  SC > 0 slots (compile time): every slot row is
+// loaded before the expert ids are consulted (rows of dropped pairs are in
+// bounds, their values unused); SC == 0: any slot count, one slot at a time.
+template <int SC>
 __global__ void __launch_bounds__(kThreads) combine_kernel(const float* __restrict__ slots,
                                                            const int32_t* __restrict__ ids, int T, int k, int E,
-                                                           int nsh, int H, int act, uint16_t* __restrict__ y) {
-  const int64_t i4 = (int64_t)blockIdx.x * kThreads + threadIdx.x;  // index of 4 outputs
-  const int q4 = H / 4;
-  if (i4 >= (int64_t)T * q4) return;
-  const int t = (int)(i4 / q4), h = (int)(i4 % q4) * 4;
-  const int S = k + nsh;
-  const float* base = slots + (int64_t)t * S * H + h;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int s = 0; s < S; ++s) {
-    if (s < k) {
-      int e = ids[(int64_t)t * k + s];
-      if (e < 0 || e >= E) continue;
+                                                           int S, int H, int act, uint16_t* __restrict__ y) {
+  const int64_t i8 = (int64_t)blockIdx.x * kThreads + threadIdx.x;  // index of 8 outputs
+  const int q8 = H / 8;
+  if (i8 >= (int64_t)T * q8) return;
+  const int t = (int)(i8 / q8), h = (int)(i8 % q8) * 8;
+  if constexpr (SC > 0) S = SC;
+  const float4* base = reinterpret_cast<const float4*>(slots + (int64_t)t * S * H + h);
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  auto add = [&](float4 a, float4 b) {
+    acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+    acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+  };
+  auto valid = [&](int s) {
+    if (s >= k) return true;  // shared-expert slots
+    const int e = ids[(int64_t)t * k + s];
+    return e >= 0 && e < E;
+  };
+  if constexpr (SC > 0) {
+    float4 v[SC][2];
+#pragma unroll
+    for (int s = 0; s < SC; ++s) {
+      v[s][0] = base[(int64_t)s * (H / 4)];
+      v[s][1] = base[(int64_t)s * (H / 4) + 1];
     }
-    float4 v = *reinterpret_cast<const float4*>(base + (int64_t)s * H);
-    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+#pragma unroll
+    for (int s = 0; s < SC; ++s)
+      if (valid(s)) add(v[s][0], v[s][1]);
+  } else {
+    for (int s = 0; s < S; ++s)
+      if (valid(s)) add(base[(int64_t)s * (H / 4)], base[(int64_t)s * (H / 4) + 1]);
   }
-  uint2 o;
-  o.x = (uint32_t)f32_to_act(acc.x, act) | ((uint32_t)f32_to_act(acc.y, act) << 16);
-  o.y = (uint32_t)f32_to_act(acc.z, act) | ((uint32_t)f32_to_act(acc.w, act) << 16);
-  *reinterpret_cast<uint2*>(y + (int64_t)t * H + h) = o;
+  uint4 o;
+  o.x = (uint32_t)f32_to_act(acc[0], act) | ((uint32_t)f32_to_act(acc[1], act) << 16);
+  o.y = (uint32_t)f32_to_act(acc[2], act) | ((uint32_t)f32_to_act(acc[3], act) << 16);
+  o.z = (uint32_t)f32_to_act(acc[4], act) | ((uint32_t)f32_to_act(acc[5], act) << 16);
+  o.w = (uint32_t)f32_to_act(acc[6], act) | ((uint32_t)f32_to_act(acc[7], act) << 16);
+  *reinterpret_cast<uint4*>(y + (int64_t)t * H + h) = o;
 }
 
 // Per-row data of the sorted (token, slot) pairs, read by every Group-GEMM
@@ -137,26 +281,75 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
   return hipGetLastError();
 }
 
+namespace {
+// Register-resident shapes by row length: (chunks per lane, wavefronts per row).
+enum RowShape { RS_1x2, RS_1x4, RS_1x8, RS_4x4, RS_4x8, RS_STREAM };
+RowShape row_shape(int cols) {
+  const int nch = cols / 8, per = (nch + 63) / 64, per4 = (nch + 255) / 256;
+  if (per <= 2) return RS_1x2;
+  if (per <= 4) return RS_1x4;
+  if (per <= 8) return RS_1x8;
+  if (per4 <= 4) return RS_4x4;
+  if (per4 <= 8) return RS_4x8;
+  return RS_STREAM;
+}
+template <template <int, int> class K, typename... Args>
+hipError_t launch_rows(int rows, int cols, hipStream_t s, Args... args) {
+  const RowShape rs = row_shape(cols);
+  const dim3 g1((rows + kRowsPerBlock - 1) / kRowsPerBlock), g4(rows), b(kThreads);
+  switch (rs) {
+    case RS_1x2: hipLaunchKernelGGL((K<2, 1>::fn), g1, b, 0, s, args...); break;
+    case RS_1x4: hipLaunchKernelGGL((K<4, 1>::fn), g1, b, 0, s, args...); break;
+    case RS_1x8: hipLaunchKernelGGL((K<8, 1>::fn), g1, b, 0, s, args...); break;
+    case RS_4x4: hipLaunchKernelGGL((K<4, 4>::fn), g4, b, 0, s, args...); break;
+    case RS_4x8: hipLaunchKernelGGL((K<8, 4>::fn), g4, b, 0, s, args...); break;
+    default: hipLaunchKernelGGL((K<0, 1>::fn), g1, b, 0, s, args...); break;
+  }
+  return hipGetLastError();
+}
+template <int NC, int W> struct ActQuantK { static constexpr auto fn = act_quant_vec_kernel<NC, W>; };
+template <int NC, int W> struct HQuantK { static constexpr auto fn = hquant_routed_kernel<NC, W>; };
+}  // namespace
+
 hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax, int8_t* codes,
                             float* scales, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(act_quant_kernel, dim3(rows), dim3(kThreads), 0, s, a, act, cols, ld, qmax, codes, scales);
-  return hipGetLastError();
+  const bool vec = (reinterpret_cast<uintptr_t>(a) & 15) == 0 && (reinterpret_cast<uintptr_t>(codes) & 7) == 0 &&
+                   cols % 8 == 0 && ld % 8 == 0;
+  if (!vec) {  // unaligned rows: one workgroup per row, element loads
+    hipLaunchKernelGGL(act_quant_kernel, dim3(rows), dim3(kThreads), 0, s, a, act, cols, ld, qmax, codes, scales);
+    return hipGetLastError();
+  }
+  return launch_rows<ActQuantK>(rows, cols, s, a, act, rows, cols, ld, qmax, codes, scales);
 }
 
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets, int E,
                                 const int32_t* down_qmax, int8_t* hq, float* hs, hipStream_t s) {
   if (P <= 0) return hipSuccess;
-  hipLaunchKernelGGL(hquant_routed_kernel, dim3(P), dim3(kThreads), 0, s, h, act, F, offsets, E, down_qmax, hq, hs);
-  return hipGetLastError();
+  if ((reinterpret_cast<uintptr_t>(h) & 15) || (reinterpret_cast<uintptr_t>(hq) & 7) || F % 8 || E > kMaxE)
+    return hipErrorInvalidValue;
+  return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs);
 }
 
 hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int nsh, int H, int act,
                           void* y, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  int64_t n4 = (int64_t)T * (H / 4);
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)((n4 + kThreads - 1) / kThreads)), dim3(kThreads), 0, s, slots,
-                     ids, T, k, E, nsh, H, act, (uint16_t*)y);
+  if (H % 8 || (reinterpret_cast<uintptr_t>(y) & 15) || (reinterpret_cast<uintptr_t>(slots) & 15))
+    return hipErrorInvalidValue;
+  const int64_t n8 = (int64_t)T * (H / 8);
+  const dim3 grid((unsigned)((n8 + kThreads - 1) / kThreads));
+  const int S = k + nsh;
+  switch (S) {
+#define MX_COMBINE(S_) \
+  case S_:             \
+    hipLaunchKernelGGL(combine_kernel<S_>, grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act, (uint16_t*)y); \
+    break;
+    MX_COMBINE(1) MX_COMBINE(2) MX_COMBINE(3) MX_COMBINE(4) MX_COMBINE(5) MX_COMBINE(6) MX_COMBINE(7) MX_COMBINE(8)
+    MX_COMBINE(9) MX_COMBINE(10)
+#undef MX_COMBINE
+    default:
+      hipLaunchKernelGGL(combine_kernel<0>, grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act, (uint16_t*)y);
+  }
   return hipGetLastError();
 }
 

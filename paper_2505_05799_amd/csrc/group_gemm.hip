@@ -70,13 +70,16 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   __shared__ int32_t s_tiles[2][2048];  // queued tiles (output tiles x slices)
   __shared__ int32_t s_red[1025];
   __shared__ int32_t s_ns[2048];
+  __shared__ int8_t s_sp[2][2048];      // proposed slices of each group
   __shared__ int32_t s_used[2];         // output-tile counters used per phase
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nphase = raw_m >= 0 ? 1 : 2;
   const PlanLayout PL = plan_layout(G, qcap, fcap);
   int32_t* misc = plan + PL.misc;
   if (tid == 0) misc[4] = 0;
-  // 1. per group: rows, configuration, output tiles, proposed slices
+  // 1. per group: rows, configuration, output tiles, proposed slices; for the
+  //    budget pass the partial-sum floats (capped at pfloats + 1, which no
+  //    budget admits) and the output tiles of every group that would be sliced
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
@@ -87,6 +90,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       const int bm = cfg_bm(cfg), bn = cfg_bn(cfg, phase_eff);
       const int mt = m > 0 ? (m + bm - 1) / bm : 0;
       const int nt = (L.n + bn - 1) / bn;
+      const int sp = split_rule(cfg, mt * nt, L.k / 128);
       int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
       r[PF_EXPERT] = g;
       r[PF_M] = m;
@@ -94,39 +98,81 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       r[PF_MTILES] = mt;
       r[PF_NTILES] = nt;
       r[PF_START] = 0;
-      r[PF_SPLIT] = split_rule(cfg, mt * nt, L.k / 128);
-      r[PF_PBASE] = 0;
-      r[PF_CBASE] = 0;
       if (ph == 0 && raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
+      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
+      const int64_t need = (int64_t)mt * nt * sp * bm * bn * nl;
+      s_sp[ph][g] = (int8_t)sp;
+      s_tiles[ph][g] = sp > 1 ? mt * nt : 0;
+      s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
     }
   }
   __syncthreads();
-  // 2. slices within the budgets, in group order (one thread per phase)
-  if (tid < nphase) {
-    const int ph = tid;
+  // 2. slices within the budgets, greedily in group order: a group is sliced
+  //    if its partial sums and added tiles still fit, else it runs unsliced.
+  //    One wavefront per phase takes 64 groups at a time; a chunk that fits
+  //    whole is accepted at once (what the greedy pass does with it), any
+  //    other chunk is decided group by group.
+  if (wave < nphase) {
+    const int ph = wave;
     int64_t pused = 0;
     int eused = 0, cused = 0;
-    for (int g = 0; g < G; ++g) {
-      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      const int sp = r[PF_SPLIT];
-      if (sp <= 1) continue;
-      const int cfg = r[PF_CFG], tiles = r[PF_MTILES] * r[PF_NTILES];
-      const int phase_eff = raw_m >= 0 ? 1 : ph;
-      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
-      const int64_t need = (int64_t)tiles * sp * cfg_bm(cfg) * cfg_bn(cfg, phase_eff) * nl;
-      const int extra = tiles * (sp - 1);
-      if (pused + need > pfloats || eused + extra > kSplitExtra) {
-        r[PF_SPLIT] = 1;
-        continue;
+    for (int c0 = 0; c0 < G; c0 += 64) {
+      const int g = c0 + lane;
+      const int sp = g < G ? s_sp[ph][g] : 1;
+      const int tl = g < G ? s_tiles[ph][g] : 0;  // 0 unless sliced
+      const int64_t need = g < G ? s_cost[ph][g] : 0;
+      const int extra = tl * (sp - 1) <= kSplitExtra ? tl * (sp - 1) : kSplitExtra + 1;
+      int64_t pin = need;
+      int ein = extra, cin = tl;
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t tp = __shfl_up(pin, d, 64);
+        const int te = __shfl_up(ein, d, 64), tc = __shfl_up(cin, d, 64);
+        if (lane >= d) {
+          pin += tp;
+          ein += te;
+          cin += tc;
+        }
       }
-      r[PF_PBASE] = (int32_t)pused;
-      r[PF_CBASE] = cused;
-      pused += need;
-      eused += extra;
-      cused += tiles;
+      const int64_t ptot = __shfl(pin, 63, 64);
+      const int etot = __shfl(ein, 63, 64), ctot = __shfl(cin, 63, 64);
+      bool take = tl > 0;
+      int64_t pbase = 0;
+      int cbase = 0;
+      if (pused + ptot <= pfloats && (int64_t)eused + etot <= kSplitExtra) {
+        pbase = pused + pin - need;
+        cbase = cused + cin - tl;
+        pused += ptot;
+        eused += etot;
+        cused += ctot;
+      } else {
+        for (int j = 0; j < 64; ++j) {
+          const int64_t nj = __shfl(need, j, 64);
+          const int ej = __shfl(extra, j, 64), tj = __shfl(tl, j, 64);
+          if (tj <= 0) continue;
+          const bool ok = pused + nj <= pfloats && eused + ej <= kSplitExtra;
+          if (lane == j) {
+            take = ok;
+            pbase = pused;
+            cbase = cused;
+          }
+          if (ok) {
+            pused += nj;
+            eused += ej;
+            cused += tj;
+          }
+        }
+      }
+      if (g < G) {
+        int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+        r[PF_SPLIT] = take ? sp : 1;
+        r[PF_PBASE] = take ? (int32_t)pbase : 0;
+        r[PF_CBASE] = take ? cbase : 0;
+      }
     }
-    s_used[ph] = cused;
-    misc[6 + ph] = (int32_t)pused;
+    if (lane == 0) {
+      s_used[ph] = cused;
+      misc[6 + ph] = (int32_t)pused;
+    }
   }
   __syncthreads();
   // 3. per-tile cost estimate with the final slices, arrival counters cleared
@@ -208,14 +254,28 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       e[2] = super_tile_size(rec[PF_MTILES], rec[PF_NTILES] * rec[PF_SPLIT], s);
     }
     __syncthreads();
+    // per-queue exclusive prefix sums of the entry sizes, one wavefront per queue
     int32_t* ctr = plan + PL.ctr + (int64_t)ph * kXcd * 4;
-    for (int x = 0; x < kXcd; ++x) {
+    if (wave < kXcd) {
+      const int x = wave;
       int n = S / kXcd + (x < S % kXcd ? 1 : 0);
       n = n < qcap ? n : qcap;
-      const int total = block_scan(ent + (int64_t)x * qcap * 3 + 2, n, s_red, 3);
-      if (tid == 0) {
+      int32_t* q = ent + (int64_t)x * qcap * 3 + 2;
+      int run = 0;
+      for (int c0 = 0; c0 < n; c0 += 64) {
+        const int i = c0 + lane;
+        const int v = i < n ? q[(int64_t)i * 3] : 0;
+        int incl = v;
+        for (int d = 1; d < 64; d <<= 1) {
+          const int t = __shfl_up(incl, d, 64);
+          if (lane >= d) incl += t;
+        }
+        if (i < n) q[(int64_t)i * 3] = run + incl - v;
+        run += __shfl(incl, 63, 64);
+      }
+      if (lane == 0) {
         ctr[x * 4 + 0] = 0;
-        ctr[x * 4 + 1] = total;
+        ctr[x * 4 + 1] = run;
         ctr[x * 4 + 2] = n;
       }
     }

@@ -106,6 +106,11 @@ enum PlanField : int32_t {
 constexpr int kSplitExtra = 16384;
 constexpr int kSplitMax = 8;
 
+// Limits of a block: routed experts, shared experts, groups (routed + shared).
+constexpr int kMaxE = 1024;
+constexpr int kMaxShared = 64;
+constexpr int kMaxG = 2048;
+
 // Tiles are grouped into super-tiles of up to 64 tiles sharing row and channel
 // blocks (min(mt, 8) x min(nt, 64 / that) tiles) and dealt round-robin to one
 // queue per XCD, in decreasing tile-cost order of their groups; each queue is

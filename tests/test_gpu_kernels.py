@@ -76,10 +76,14 @@ def test_route_permute(T, k, E, kind):
 
 
 # ------------------------------------------------------- activation quant
+# row lengths that reach every kernel shape: one wavefront per row with 2, 4
+# or 8 chunks per lane, one workgroup per row with 4 or 8, a streamed row
+# read twice; ld_pad 3 misaligns the rows (element loads, one workgroup per row)
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
 @pytest.mark.parametrize("qmax", [127, 7])
-@pytest.mark.parametrize("rows,cols", [(1, 128), (37, 2048), (300, 3584)])
-def test_act_quant_bit_exact(act, qmax, rows, cols):
+@pytest.mark.parametrize("rows,cols,ld_pad", [(1, 128, 0), (37, 2048, 0), (300, 3584, 0), (5, 6144, 8),
+                                              (9, 14336, 0), (3, 20480, 0), (6, 1000, 3), (4, 100, 0)])
+def test_act_quant_bit_exact(act, qmax, rows, cols, ld_pad):
     torch = torch_mod()
     rng = np.random.default_rng(rows + cols + qmax)
     x64 = rng.standard_normal((rows, cols)) * np.exp(rng.uniform(-3, 3, size=(rows, 1)))
@@ -87,7 +91,10 @@ def test_act_quant_bit_exact(act, qmax, rows, cols):
     if rows > 2:
         x[1] = 0                                       # zero row
         x[2, 5] = x[2, 0]                             # ties in amax
-    a = M.act_tensor(x, act)
+    wide = np.zeros((rows, cols + ld_pad), dtype=x.dtype)
+    wide[:, :cols] = x
+    a = M.act_tensor(wide, act)[:, :cols]
+    assert a.stride(0) == cols + ld_pad
     codes, scales = M.act_quant(a, act, qmax)
     torch.cuda.synchronize()
     rc, rs = O.act_quant(O.act_values(x, act).astype(np.float32), qmax)
