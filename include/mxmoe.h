@@ -225,12 +225,12 @@ typedef struct {
   size_t offsets;       /* int32 [E+1]                                       */
   size_t sorted_pair;   /* int32 [T*k]                                       */
   size_t inv;           /* int32 [T*k]                                       */
-  size_t plan;          /* int32 tile plan: group records [2][G][8], order [2][G],
+  size_t plan;          /* int32 tile plan: group records [2][G][12], order [2][G],
                            XCD queues [2][8][plan_queue_cap][3] (16-byte aligned),
                            queue counters [2][8][4], misc [16], the queues
                            expanded to tiles [2][8][plan_flat_cap][4], and
-                           split-K arrival counters [2][16384]; group records
-                           have 12 fields                                    */
+                           split-K arrival counters [2][16384]; misc[8] is
+                           the workgroup count the slicing assumed            */
   size_t xq8, xs8;      /* int8 [T,H], fp32 [T]: x codes for a8 gate/up      */
   size_t xq4, xs4;      /* int8 [T,H], fp32 [T]: x codes for a4 gate/up      */
   size_t h;             /* act [T*k, F]: routed h rows, sorted-pair order    */

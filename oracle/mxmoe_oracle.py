@@ -399,53 +399,85 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   configuration T (m <= 32): 32 rows x (gate|up 256, down 512) channels
 #   configuration M (m <= 64): 64 rows x (gate|up 128, down 256) channels
 #   configuration L (m > 64) : 128 rows x (gate|up 128, down 256) channels
-#   cost of a tile (ps) = max(bytes * 32, flops * 1000 / rate), truncated to an
-#   integer, with bytes = linears * BN * K * wbits / 8 + BM * K * abytes,
-#   flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
-#   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s;
+#   cost of a tile (ps) = min(max(bytes * 32, flops * 1000 / rate) + 2e6, 2e9),
+#   truncated to an integer, with bytes = wbytes / mt + abytes / nt (the group's
+#   mt row tiles share a weight tile, its nt channel tiles an activation tile),
+#   wbytes = linears * BN * K * wbits / 8, abytes = BM * K * (1 or 2), plus
+#   8 * BM * BN * linears for a sliced tile (its partial sums written and read
+#   back); flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
+#   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s - and 2e6 ps
+#   (2 us) of fixed per-tile work;
 #   queue order: decreasing cost, ties by lower expert index.
 # Slicing of the reduction (split-K, the paper's slice-K tile parameter):
-#   configurations S/T/M: S = clamp(K/128 // 4, 1, 8) slices;
-#   configuration L: S = min(4, (K/128) // 16) if the group has fewer than 128
-#   tiles and K/128 >= 32, else 1;
+#   theta = (sum over the phase's tiles of the unsliced tile cost) // nwg // 4,
+#   nwg the workgroups of the launch; a group takes the fewest slices S in
+#   1 .. Smax = clamp(K/128 // 4, 1, 8) whose tile cost (reduction length
+#   ceil(K/128 / S) * 128) is at most theta, else the S of the cheapest tile
+#   (the fewest slices among equals); groups without tiles are not sliced;
 #   budgets, granted in group order: the slices' partial sums (tiles * S * BM *
 #   BN * linears floats) fit the partial buffer and the tiles added by slicing
 #   (tiles * (S - 1)) stay within 16384 per phase, else S = 1;
-#   the cost uses the reduction length of one slice, ceil(K/128 / S) * 128, and
 #   a sliced group queues tiles * S tiles.
 
 _TILE_BM = (16, 32, 64, 128)
 _TILE_BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][config]
 _SPLIT_EXTRA = 16384
+_SPLIT_MAX = 8
+_SPLIT_SHARE = 4
+_TILE_FIXED_PS = 2.0e6
 
 
-def _split_rule(cfg: int, tiles: int, kblocks: int) -> int:
-    if tiles <= 0:
+def _tile_cost(bm: int, bn: int, nl: int, scheme, kk: int, split: int, mt: int, nt: int) -> int:
+    is_int = scheme.a_bits < 16
+    wbytes = float(nl * bn * kk * scheme.w_bits) / 8.0
+    abytes = float(bm) * kk * (1.0 if is_int else 2.0)
+    pbytes = 8.0 * bm * bn * nl if split > 1 else 0.0
+    flops = 2.0 * nl * bm * bn * kk
+    t_mem = (wbytes / max(mt, 1) + abytes / max(nt, 1) + pbytes) * 32.0
+    t_mma = flops * 1000.0 / (19531.0 if is_int else 9766.0)
+    c = max(t_mem, t_mma) + _TILE_FIXED_PS
+    return int(min(c, 2.0e9))
+
+
+def _choose_split(bm: int, bn: int, nl: int, scheme, kblocks: int, mt: int, nt: int, theta: int) -> int:
+    if mt * nt <= 0:
         return 1
-    if cfg != 3:
-        return max(1, min(8, kblocks // 4))
-    if tiles < 128 and kblocks >= 32:
-        return min(4, kblocks // 16)
-    return 1
+    smax = max(1, min(_SPLIT_MAX, kblocks // 4))
+    best, cbest = 1, None
+    for sp in range(1, smax + 1):
+        c = _tile_cost(bm, bn, nl, scheme, -(-kblocks // sp) * 128, sp, mt, nt)
+        if c <= theta:
+            return sp
+        if cbest is None or c < cbest:
+            best, cbest = sp, c
+    return best
 
 
-def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int = 0):
+def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int = 0, nwg: int = 512):
     """Tile configuration, tile counts, slices, cost and queue rank per group.
 
     ms[g]: rows of group g; lins[g]: its linear (gate for phase 0, down for 1);
-    partial_floats: size of the split-K partial buffer.  Returns a list of dicts
-    (cfg, mtiles, ntiles, split, tiles, cost, rank) and the queue order (group
-    indices with tiles, longest tile first).
+    partial_floats: size of the split-K partial buffer; nwg: workgroups of the
+    launch.  Returns a list of dicts (cfg, mtiles, ntiles, split, tiles, cost,
+    rank) and the queue order (group indices with tiles, longest tile first).
     """
     out = []
     nl = 2 if phase == 0 else 1
-    pused = eused = 0
+    geo = []
+    work = 0
     for m, lin in zip(ms, lins):
+        m = int(m)  # Python integers: the sums below exceed 32 bits
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
-        nt = -(-lin.n // bn)
-        sp = _split_rule(cfg, mt * nt, lin.k // 128)
+        nt = -(-int(lin.n) // bn)
+        geo.append((cfg, bm, bn, mt, nt))
+        if mt * nt > 0:
+            work += mt * nt * _tile_cost(bm, bn, nl, lin.scheme, (lin.k // 128) * 128, 1, mt, nt)
+    theta = work // nwg // _SPLIT_SHARE
+    pused = eused = 0
+    for (cfg, bm, bn, mt, nt), lin in zip(geo, lins):
+        sp = _choose_split(bm, bn, nl, lin.scheme, lin.k // 128, mt, nt, theta)
         if sp > 1:
             need = mt * nt * sp * bm * bn * nl
             extra = mt * nt * (sp - 1)
@@ -456,18 +488,11 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int
                 eused += extra
         out.append({"cfg": cfg, "mtiles": mt, "ntiles": nt, "split": sp})
     for r, lin in zip(out, lins):
-        s = lin.scheme
         bm, bn = _TILE_BM[r["cfg"]], _TILE_BN[phase][r["cfg"]]
         kk = -(-(lin.k // 128) // r["split"]) * 128
-        is_int = s.a_bits < 16
-        wbytes = float(nl * bn * kk * s.w_bits) / 8.0
-        abytes = float(bm) * kk * (1.0 if is_int else 2.0)
-        flops = 2.0 * nl * bm * bn * kk
-        c = max((wbytes + abytes) * 32.0, flops * 1000.0 / (19531.0 if is_int else 9766.0))
-        c = min(c, 2.0e9)
         tiles = r["mtiles"] * r["ntiles"] * r["split"]
         r["tiles"] = tiles
-        r["cost"] = int(c) if tiles else 0
+        r["cost"] = _tile_cost(bm, bn, nl, lin.scheme, kk, r["split"], r["mtiles"], r["ntiles"]) if tiles else 0
     live = [g for g, r in enumerate(out) if r["tiles"] > 0]
     order = sorted(live, key=lambda g: (-out[g]["cost"], g))
     for r in out:

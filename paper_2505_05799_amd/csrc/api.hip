@@ -122,8 +122,8 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.rgw = take(4 * P);
   L.rxs8 = bi.any_x8 ? take(4 * P) : kNone;
   L.rxs4 = bi.any_x4 ? take(4 * P) : kNone;
-  // split-K partial sums: a few times the largest layer output, at most 256 MB
-  L.pfloats = std::min<int64_t>((int64_t)1 << 26,
+  // split-K partial sums: a few times the largest layer output, at most 512 MB
+  L.pfloats = std::min<int64_t>((int64_t)1 << 27,
                                 4 * ((int64_t)P + (int64_t)bi.nsh * T) * std::max(std::max(bi.F, bi.Fsh), bi.H));
   L.partial = take(4 * (size_t)L.pfloats);
   L.xq8 = L.xs8 = L.xq4 = L.xs4 = kNone;
@@ -298,10 +298,11 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
   }
+  const int grid = group_gemm_grid(current_device());
   hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, w.pfloats,
-                             nullptr, stream);
+                             nullptr, grid, stream);
   if (e != hipSuccess) return MXMOE_ERR_HIP;
-  return hip_status(launch_group_gemm(ga, 2, group_gemm_grid(current_device()), stream));
+  return hip_status(launch_group_gemm(ga, 2, grid, stream));
 }
 
 // -------------------------------------------------------- MoE block
@@ -423,8 +424,9 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
                         at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
   memset(&none, 0, sizeof(none));
+  const int grid = group_gemm_grid(current_device());
   MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
-                       down_qmax, stream));
+                       down_qmax, grid, stream));
   if (bi.any_x8)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
                               stream));
@@ -469,7 +471,6 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.rxs8 = at<float>(workspace, L.rxs8);
   ga.rxs4 = at<float>(workspace, L.rxs4);
   ga.partial = at<float>(workspace, L.partial);
-  const int grid = group_gemm_grid(current_device());
   MX_EVENT(1);
   MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));

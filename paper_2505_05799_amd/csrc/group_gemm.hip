@@ -65,7 +65,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
                                                     const int32_t* __restrict__ offsets, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
                                                     int qcap, int fcap, int64_t pfloats,
-                                                    int32_t* __restrict__ down_qmax) {
+                                                    int32_t* __restrict__ down_qmax, int nwg) {
   __shared__ int32_t s_cost[2][2048];
   __shared__ int32_t s_tiles[2][2048];  // queued tiles (output tiles x slices)
   __shared__ int32_t s_red[1025];
@@ -77,35 +77,62 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   const PlanLayout PL = plan_layout(G, qcap, fcap);
   int32_t* misc = plan + PL.misc;
   if (tid == 0) misc[4] = 0;
-  // 1. per group: rows, configuration, output tiles, proposed slices; for the
-  //    budget pass the partial-sum floats (capped at pfloats + 1, which no
-  //    budget admits) and the output tiles of every group that would be sliced
+  // 1. per group: rows, configuration, output tiles; the phase's work (tiles
+  //    times unsliced tile cost, summed exactly) sets the slicing threshold;
+  //    then the proposed slices and, for the budget pass, the partial-sum
+  //    floats (capped at pfloats + 1, which no budget admits) and the output
+  //    tiles of every group that would be sliced
+  struct Geom { int m, cfg, bm, bn, mt, nt, kb, kd, nl; };
+  auto geom = [&](int ph, int g) {
+    Geom q;
+    q.m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
+    if (!((mask.w[g >> 5] >> (g & 31)) & 1u)) q.m = 0;
+    const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
+    q.cfg = pick_cfg(q.m);
+    const int phase_eff = raw_m >= 0 ? 1 : ph;  // raw mode: one linear
+    q.bm = cfg_bm(q.cfg);
+    q.bn = cfg_bn(q.cfg, phase_eff);
+    q.mt = q.m > 0 ? (q.m + q.bm - 1) / q.bm : 0;
+    q.nt = (L.n + q.bn - 1) / q.bn;
+    q.kb = L.k / 128;
+    q.kd = L.kind;
+    q.nl = (raw_m < 0 && ph == 0) ? 2 : 1;
+    return q;
+  };
+  __shared__ int64_t s_work[2][1024 / 64];
   for (int ph = 0; ph < nphase; ++ph) {
+    int64_t w = 0;
     for (int g = tid; g < G; g += blockDim.x) {
-      int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
-      if (!((mask.w[g >> 5] >> (g & 31)) & 1u)) m = 0;
-      const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
-      const int cfg = pick_cfg(m);
-      const int phase_eff = raw_m >= 0 ? 1 : ph;  // raw mode: one linear
-      const int bm = cfg_bm(cfg), bn = cfg_bn(cfg, phase_eff);
-      const int mt = m > 0 ? (m + bm - 1) / bm : 0;
-      const int nt = (L.n + bn - 1) / bn;
-      const int sp = split_rule(cfg, mt * nt, L.k / 128);
+      const Geom q = geom(ph, g);
+      const int tiles = q.mt * q.nt;
+      if (tiles > 0) w += (int64_t)tiles * tile_cost(q.bm, q.bn, q.nl, q.kd, q.kb * 128, 1, q.mt, q.nt);
+    }
+    for (int d = 32; d > 0; d >>= 1) w += __shfl_xor(w, d, 64);
+    if (lane == 0) s_work[ph][wave] = w;
+  }
+  __syncthreads();
+  for (int ph = 0; ph < nphase; ++ph) {
+    int64_t work = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) work += s_work[ph][i];
+    const int64_t theta = work / nwg / kSplitShare;
+    for (int g = tid; g < G; g += blockDim.x) {
+      const Geom q = geom(ph, g);
+      const int sp = choose_split(q.bm, q.bn, q.nl, q.kd, q.kb, q.mt, q.nt, theta);
       int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
       r[PF_EXPERT] = g;
-      r[PF_M] = m;
-      r[PF_CFG] = cfg;
-      r[PF_MTILES] = mt;
-      r[PF_NTILES] = nt;
+      r[PF_M] = q.m;
+      r[PF_CFG] = q.cfg;
+      r[PF_MTILES] = q.mt;
+      r[PF_NTILES] = q.nt;
       r[PF_START] = 0;
       if (ph == 0 && raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
-      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
-      const int64_t need = (int64_t)mt * nt * sp * bm * bn * nl;
+      const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
       s_sp[ph][g] = (int8_t)sp;
-      s_tiles[ph][g] = sp > 1 ? mt * nt : 0;
+      s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
       s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
     }
   }
+  if (tid == 0) misc[8] = nwg;
   __syncthreads();
   // 2. slices within the budgets, greedily in group order: a group is sliced
   //    if its partial sums and added tiles still fit, else it runs unsliced.
@@ -179,24 +206,12 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
-      const int cfg = r[PF_CFG], sp = r[PF_SPLIT];
-      const int tiles = r[PF_MTILES] * r[PF_NTILES] * sp;
-      const int phase_eff = raw_m >= 0 ? 1 : ph;
-      const int bm = cfg_bm(cfg), bn = cfg_bn(cfg, phase_eff);
-      const int nl = (raw_m < 0 && ph == 0) ? 2 : 1;
-      const int kd = L.kind;
-      const double kk = (double)((L.k / 128 + sp - 1) / sp) * 128.0;  // reduction length of one slice
-      const double wbytes = (double)nl * bn * kk * kind_wbits(kd) / 8.0;
-      const double abytes = (double)bm * kk * (kind_is_int(kd) ? 1.0 : 2.0);
-      const double flops = 2.0 * nl * bm * bn * kk;
-      // per-CU shares of MI355X peaks: 8 TB/s HBM, 2.5 PF 16-bit / 5 POPS int8 MFMA
-      const double t_mem = (wbytes + abytes) * 32.0;  // ps
-      const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
-      double c = t_mem > t_mma ? t_mem : t_mma;
-      if (c > 2.0e9) c = 2.0e9;
-      r[PF_COST] = tiles ? (int32_t)c : 0;
-      s_cost[ph][g] = tiles ? (int32_t)c : 0;
+      const Geom q = geom(ph, g);
+      const int sp = r[PF_SPLIT];
+      const int tiles = q.mt * q.nt * sp;
+      const int c = tiles ? tile_cost(q.bm, q.bn, q.nl, q.kd, (q.kb + sp - 1) / sp * 128, sp, q.mt, q.nt) : 0;
+      r[PF_COST] = c;
+      s_cost[ph][g] = c;
       s_tiles[ph][g] = tiles;
     }
     int32_t* cnt = plan + PL.cnt + (int64_t)ph * kSplitExtra;
@@ -325,11 +340,12 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
 
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, hipStream_t s) {
+                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
+                       hipStream_t s) {
   MaskBits mb;
   for (int i = 0; i < 64; ++i) mb.w[i] = mask_words ? mask_words[i] : 0xffffffffu;
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin, mb,
-                     plan, qcap, fcap, pfloats, down_qmax);
+                     plan, qcap, fcap, pfloats, down_qmax, nwg < 1 ? 1 : nwg);
   return hipGetLastError();
 }
 

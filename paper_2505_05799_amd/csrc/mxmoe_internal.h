@@ -127,7 +127,8 @@ constexpr int kSuperTiles = 64;
 //   ctr   [2][kXcd][4]        per queue: head, total tiles, entries, -
 //   misc  [16]                [2 + p]: number of groups with tiles in phase p,
 //                             [4]: 1 if a queue overflowed its capacity,
-//                             [6 + p]: partial-buffer floats used in phase p
+//                             [6 + p]: partial-buffer floats used in phase p,
+//                             [8]: workgroups the slicing threshold assumes
 //   flat  [2][kXcd][fcap][4]  the queues expanded to one entry per tile
 //   cnt   [2][kSplitExtra]    arrival counters of sliced output tiles
 struct PlanLayout { int64_t rec, order, ent, ctr, misc, flat, cnt, total; };
@@ -166,18 +167,50 @@ __host__ __device__ inline int plan_flat_cap(int qcap) {
 __host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int split) {
   return g | (cfg << 16) | (kind << 20) | ((split - 1) << 24);
 }
-// Slices of a group (split-K): groups of at most 64 rows (bandwidth-bound
-// tiles) are sliced into runs of at least 4 k blocks, up to kSplitMax; 128-row
-// groups only when they have fewer than 128 tiles and at least 32 k blocks, so
-// that their long tiles do not trail the schedule.
-__host__ __device__ inline int split_rule(int cfg, int tiles, int kblocks) {
-  if (tiles <= 0) return 1;
-  if (cfg != CFG_L) {
-    const int s = kblocks / 4;
-    return s < 1 ? 1 : (s > kSplitMax ? kSplitMax : s);
+// Static cost of one tile in ps: the larger of its memory time and its MFMA
+// time at one CU's share of the MI355X peaks (8 TB/s; 5.0 POPS int8, 2.5
+// PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
+// (prologue, epilogue).  The group's mt row tiles share each weight tile and
+// its nt channel tiles share each activation tile through L2, so a tile is
+// charged those shares of its HBM bytes; a sliced tile also writes its partial
+// sums and reads them back.  Every step is a single rounding of exact
+// operands, so the value does not depend on operation fusion.
+constexpr double kTileFixedPs = 2.0e6;
+__host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int kk, int split, int mt, int nt) {
+  const double wbytes = (double)nl * bn * kk * kind_wbits(kd) / 8.0;
+  const double abytes = (double)bm * kk * (kind_is_int(kd) ? 1.0 : 2.0);
+  const double pbytes = split > 1 ? 8.0 * bm * bn * nl : 0.0;
+  const double flops = 2.0 * nl * bm * bn * kk;
+  const double t_mem = (wbytes / (mt > 0 ? mt : 1) + abytes / (nt > 0 ? nt : 1) + pbytes) * 32.0;
+  const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
+  double c = t_mem > t_mma ? t_mem : t_mma;
+  c += kTileFixedPs;
+  if (c > 2.0e9) c = 2.0e9;
+  return (int32_t)c;
+}
+// Slices of a group (split-K, the paper's slice-K tile parameter): the fewest
+// slices whose tile cost is at most theta, with at least 4 k blocks per slice
+// and at most kSplitMax slices; if none is, the slice count of the cheapest
+// tile (the fewest slices among equals).  theta is a quarter of the phase's mean work
+// per workgroup (unsliced tile costs summed over all tiles, over the grid), so
+// that no tile is long next to the schedule it is part of.
+constexpr int kSplitShare = 4;
+__host__ __device__ inline int choose_split(int bm, int bn, int nl, int kd, int kblocks, int mt, int nt,
+                                            int64_t theta) {
+  if (mt * nt <= 0) return 1;
+  int smax = kblocks / 4;
+  smax = smax < 1 ? 1 : (smax > kSplitMax ? kSplitMax : smax);
+  int best = 1;
+  int32_t cbest = 0;
+  for (int s = 1; s <= smax; ++s) {
+    const int32_t c = tile_cost(bm, bn, nl, kd, (kblocks + s - 1) / s * 128, s, mt, nt);
+    if (c <= theta) return s;
+    if (s == 1 || c < cbest) {
+      best = s;
+      cbest = c;
+    }
   }
-  if (tiles < 128 && kblocks >= 32) return kblocks / 16 < 4 ? kblocks / 16 : 4;
-  return 1;
+  return best;
 }
 
 // Workspace layout (byte offsets), shared by host code of the forward.
@@ -254,7 +287,8 @@ struct GemmArgs {
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
-                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, hipStream_t s);
+                       int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
+                       hipStream_t s);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

@@ -87,9 +87,11 @@ def test_full_workload(name):
     plan = mb.ws_view("plan", torch.int32, o_ctr + 2 * 8 * 4, T).cpu().numpy()
     rec = plan[: 2 * G * PF_N].reshape(2, G, PF_N)
     ms = list(r["counts"]) + [T] * cfg.n_shared
+    nwg = int(plan_misc(mb, T, G, cap)[8])           # workgroups the slicing assumed
+    assert nwg == 2 * torch.cuda.get_device_properties(0).multi_processor_count
     for phase in (0, 1):
         lins = [blk.linears[g][0 if phase == 0 else 2] for g in range(G)]
-        want, order = O.tile_plan(ms, lins, phase, partial_floats=lay["partial_floats"])
+        want, order = O.tile_plan(ms, lins, phase, partial_floats=lay["partial_floats"], nwg=nwg)
         for g in range(G):
             got = rec[phase, g]
             assert got[1] == ms[g] and got[2] == want[g]["cfg"], (phase, g)

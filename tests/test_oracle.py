@@ -379,6 +379,55 @@ def test_runtime_model_many_tiles():
     assert errs[-1] < 0.01 and errs[0] > errs[-1]
 
 
+@pytest.mark.parametrize("nwg", [2, 64, 512])
+def test_tile_plan_slices_minimal(nwg):
+    """Slicing invariants: with an ample partial buffer a group takes the fewest
+    slices whose tile cost is within the threshold, or if there are none the
+    cheapest tile's slice count; a budget of zero floats slices nothing."""
+    blk = W.make_block("dsv2lite", with_weights=False)
+    cfg = blk.cfg
+    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E).tolist() + [cfg.T] * cfg.n_shared
+    for phase, (n, k) in ((0, (cfg.F, cfg.H)), (1, (cfg.H, cfg.F))):
+        lins = [W.QLinear(s[0 if phase == 0 else 2], n if e < cfg.E else
+                          (cfg.F_shared if phase == 0 else cfg.H),
+                          k if e < cfg.E else (cfg.H if phase == 0 else cfg.F_shared), None)
+                for e, s in enumerate(W.schemes_of(cfg))]
+        plan, _ = O.tile_plan(counts, lins, phase, partial_floats=1 << 40, nwg=nwg)
+        nl = 2 if phase == 0 else 1
+        bms, bns = (16, 32, 64, 128), ((256, 256, 128, 128), (512, 512, 256, 256))[phase]
+        work = sum(r["mtiles"] * r["ntiles"] * O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme,
+                                                           lin.k // 128 * 128, 1, r["mtiles"], r["ntiles"])
+                   for r, lin in zip(plan, lins) if r["mtiles"] * r["ntiles"])
+        theta = work // nwg // 4
+        for r, lin in zip(plan, lins):
+            if r["mtiles"] * r["ntiles"] == 0:
+                assert r["split"] == 1
+                continue
+            kb = lin.k // 128
+            smax = max(1, min(8, kb // 4))
+            cost = lambda sp: O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme, -(-kb // sp) * 128, sp,
+                                           r["mtiles"], r["ntiles"])
+            sp = r["split"]
+            assert 1 <= sp <= smax
+            if cost(sp) <= theta:   # the fewest slices within the threshold
+                assert sp == 1 or cost(sp - 1) > theta
+            else:                   # none within it: the cheapest tile
+                assert all(cost(s) > theta for s in range(1, smax + 1))
+                assert cost(sp) == min(cost(s) for s in range(1, smax + 1))
+                assert all(cost(s) > cost(sp) for s in range(1, sp))
+        none, _ = O.tile_plan(counts, lins, phase, partial_floats=0, nwg=nwg)
+        assert all(r["split"] == 1 for r in none)
+    # numpy int32 row counts (as routing returns them) plan like Python ints:
+    # the phase's work sum exceeds 32 bits at full size
+    big = [c * 64 for c in counts]
+    assert O.tile_plan([np.int32(c) for c in big], lins, 1, partial_floats=1 << 40)[0] == \
+        O.tile_plan(big, lins, 1, partial_floats=1 << 40)[0]
+    # fewer workgroups -> a larger threshold -> never more slices
+    a, _ = O.tile_plan(counts, lins, 1, partial_floats=1 << 40, nwg=2)
+    b, _ = O.tile_plan(counts, lins, 1, partial_floats=1 << 40, nwg=512)
+    assert all(x["split"] <= y["split"] for x, y in zip(a, b))
+
+
 @pytest.mark.parametrize("name", ["tiny", "dsv2lite", "qwen15_mixed"])
 def test_tile_plan_covers_every_output(name):
     blk = W.make_block(name, with_weights=False)
