@@ -61,7 +61,10 @@ def group_stats(blk, counts):
     return out
 
 
-def roofline(groups, phase, t_s):
+def roofline(groups, phase, t_s, traffic=None):
+    """Roofline of one Group-GEMM launch: algorithmic flops and bytes of the
+    phase's groups over the launch time; traffic: measured HBM bytes per launch
+    (rocprofv3 counters, copy-calibrated) or None."""
     g = [x for x in groups if x["phase"] == phase]
     flops = sum(x["flops"] for x in g)
     nbytes = sum(x["bytes"] for x in g)
@@ -70,11 +73,37 @@ def roofline(groups, phase, t_s):
     if t_mfma >= t_hbm:
         peak = flops / t_mfma / 1e12          # dtype-weighted MFMA peak
         ach = flops / t_s / 1e12
-        return {"bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": None}
-    ach = nbytes / t_s / 1e9
-    return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-            "frac": round(ach / (HBM_PEAK / 1e9), 4), "traffic": None}
+        out = {"bound": "mfma", "achieved": round(ach, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
+               "frac": round(ach / peak, 4)}
+    else:
+        ach = nbytes / t_s / 1e9
+        out = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+               "frac": round(ach / (HBM_PEAK / 1e9), 4)}
+    out["traffic"] = traffic
+    out["algorithmic_bytes"] = round(nbytes)
+    return out
+
+
+def measured_traffic(workload, phase):
+    """HBM bytes per launch from the committed counter summary of this workload
+    and phase, or None if there is none or the kernel sources changed since."""
+    from paper_2505_05799_amd import profiling as P
+    name = ("group_gemm_gate_up_" if phase == 0 else "group_gemm_down_") + workload + "_traffic.txt"
+    rec = P.read_summary(os.path.join(ROOT, "profiles", name))
+    return None if rec is None or rec.get("workload") != workload else rec["traffic_bytes"]
+
+
+def copy_calibration():
+    """A plain device copy of known size, for scaling the memory counters."""
+    import torch
+    from paper_2505_05799_amd import profiling as P
+    a = torch.empty(P.COPY_BYTES, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"[bench] copied {P.COPY_BYTES >> 20} MiB 3 times")
 
 
 def cpu_baseline(blk, tokens):
@@ -115,6 +144,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-tokens", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 256 MiB device copy (memory-counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -130,6 +161,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     M.load_library()
     cfg = W.CONFIGS[args.workload]
     t0 = time.perf_counter()
@@ -162,10 +196,10 @@ def main():
     ph_mean = phases.mean(axis=0)
     groups = group_stats(blk, counts)
     dom = 1  # gate/up Group-GEMM launch
-    roof = roofline(groups, 0, ph_mean[dom] / 1e3)
+    roof = roofline(groups, 0, ph_mean[dom] / 1e3, measured_traffic(args.workload, 0))
     roof["kernel"] = "group_gemm_kernel<bf16, gate|up>" if cfg.act == "bf16" else "group_gemm_kernel<fp16, gate|up>"
     roof["launch_ms"] = round(float(ph_mean[dom]), 4)
-    down = roofline(groups, 1, ph_mean[3] / 1e3)
+    down = roofline(groups, 1, ph_mean[3] / 1e3, measured_traffic(args.workload, 1))
 
     rec = {
         "metric": "MoE-block us/layer + effective TFLOP/s; % of HBM/MFMA roofline per group",

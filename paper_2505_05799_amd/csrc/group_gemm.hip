@@ -25,7 +25,8 @@ struct MaskBits { uint32_t w[64]; };
 
 // In-place exclusive scan of n ints v[0], v[stride], ... by one workgroup
 // (chunk sums per thread, wavefront prefix sums, then wavefront totals);
-// returns the sum.  red: LDS scratch of blockDim/64 + 1 ints.
+// returns the sum.  v and red: LDS (barriers wait for LDS traffic only), red
+// holding blockDim/64 + 1 ints.
 __device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
   const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, w = tid >> 6, nw = nt >> 6;
   const int per = (n + nt - 1) / nt;
@@ -38,7 +39,7 @@ __device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
     if (lane >= d) incl += t;
   }
   if (lane == 63) red[w] = incl;
-  __syncthreads();
+  lds_barrier();
   if (tid == 0) {
     int run = 0;
     for (int i = 0; i < nw; ++i) {
@@ -48,7 +49,7 @@ __device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
     }
     red[nw] = run;
   }
-  __syncthreads();
+  lds_barrier();
   int run = red[w] + incl - s;
   for (int i = lo; i < hi; ++i) {
     const int t = v[(int64_t)i * stride];
@@ -56,8 +57,29 @@ __device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
     run += t;
   }
   const int total = red[nw];
-  __syncthreads();
+  lds_barrier();
   return total;
+}
+
+// x / d for 0 <= x < 2^22 and 1 <= d < 2^22, exactly: a float reciprocal
+// estimate (within one of the quotient there) and one correction step; a
+// fraction of the cost of a general integer division, which the plan's
+// per-tile loops would otherwise repeat thousands of times.
+__device__ inline int div_small(int x, int d) {
+  int q = (int)((float)x * __builtin_amdgcn_rcpf((float)d));
+  q -= q * d > x;
+  q += (q + 1) * d <= x;
+  return q;
+}
+// super_dims with div_small (same values)
+__device__ inline SuperDims plan_super_dims(int mt, int nt) {
+  SuperDims d;
+  d.sm = mt < 8 ? mt : 8;
+  const int cap = div_small(kSuperTiles, d.sm > 0 ? d.sm : 1);
+  d.sn = nt < cap ? nt : cap;
+  d.nsm = d.sm ? div_small(mt + d.sm - 1, d.sm) : 0;
+  d.nsn = d.sn ? div_small(nt + d.sn - 1, d.sn) : 0;
+  return d;
 }
 
 __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict__ experts, int E, int G, int T,
@@ -66,40 +88,70 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
                                                     int qcap, int fcap, int64_t pfloats,
                                                     int32_t* __restrict__ down_qmax, int nwg) {
-  __shared__ int32_t s_cost[2][2048];
-  __shared__ int32_t s_tiles[2][2048];  // queued tiles (output tiles x slices)
+  // Every per-group input is read from global memory once, into LDS; the steps
+  // below work from LDS and only write the plan out, so their barriers wait
+  // for LDS traffic only and the plan's stores drain in the background.
+  __shared__ int32_t s_m[kMaxG];          // rows of each group (0 if masked)
+  __shared__ int32_t s_off[kMaxG];        // first sorted row (routed groups)
+  __shared__ int32_t s_n[2][kMaxG];       // output channels of the phase's linear
+  __shared__ int32_t s_kb[2][kMaxG];      // its 128-wide k blocks
+  __shared__ int8_t s_kd[2][kMaxG];       // its micro-kernel kind
+  __shared__ int8_t s_sp[2][kMaxG];       // slices: proposed, then final
+  __shared__ int32_t s_cost[2][kMaxG];    // budget need, then tile cost
+  __shared__ int32_t s_tiles[2][kMaxG];   // sliced output tiles, then queued tiles
+  __shared__ int32_t s_order[2][kMaxG];   // group per rank
+  __shared__ int32_t s_ns[kMaxG];         // first super-tile per rank (one phase at a time)
   __shared__ int32_t s_red[1025];
-  __shared__ int32_t s_ns[2048];
-  __shared__ int8_t s_sp[2][2048];      // proposed slices of each group
-  __shared__ int32_t s_used[2];         // output-tile counters used per phase
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ int64_t s_work[2][1024 / 64];
+  __shared__ int64_t s_theta[2];          // slicing threshold per phase
+  __shared__ int32_t s_used[2];           // output-tile counters used per phase
+  __shared__ int32_t s_ng[2];             // groups with tiles per phase
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
   const int nphase = raw_m >= 0 ? 1 : 2;
   const PlanLayout PL = plan_layout(G, qcap, fcap);
   int32_t* misc = plan + PL.misc;
-  if (tid == 0) misc[4] = 0;
-  // 1. per group: rows, configuration, output tiles; the phase's work (tiles
-  //    times unsliced tile cost, summed exactly) sets the slicing threshold;
-  //    then the proposed slices and, for the budget pass, the partial-sum
-  //    floats (capped at pfloats + 1, which no budget admits) and the output
-  //    tiles of every group that would be sliced
+  int32_t* order = plan + PL.order;
+  auto rec_of = [&](int ph, int g) { return plan + PL.rec + ((int64_t)ph * G + g) * PF_N; };
+
+  // 0. inputs
+  for (int g = tid; g < G; g += blockDim.x) {
+    int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
+    if (!((mask.w[g >> 5] >> (g & 31)) & 1u)) m = 0;
+    s_m[g] = m;
+    s_off[g] = (raw_m < 0 && g < E) ? offsets[g] : 0;
+    for (int ph = 0; ph < nphase; ++ph) {
+      const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
+      s_n[ph][g] = L.n;
+      s_kb[ph][g] = L.k / 128;
+      s_kd[ph][g] = (int8_t)L.kind;
+    }
+    if (raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
+  }
+  if (tid < 2) s_ng[tid] = 0;
+  if (tid == 0) {
+    misc[4] = 0;
+    misc[8] = nwg;
+  }
+  lds_barrier();
   struct Geom { int m, cfg, bm, bn, mt, nt, kb, kd, nl; };
   auto geom = [&](int ph, int g) {
     Geom q;
-    q.m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
-    if (!((mask.w[g >> 5] >> (g & 31)) & 1u)) q.m = 0;
-    const DevLinear& L = raw_m >= 0 ? raw_lin : experts[g].lin[ph == 0 ? 0 : 2];
+    q.m = s_m[g];
     q.cfg = pick_cfg(q.m);
-    const int phase_eff = raw_m >= 0 ? 1 : ph;  // raw mode: one linear
     q.bm = cfg_bm(q.cfg);
-    q.bn = cfg_bn(q.cfg, phase_eff);
-    q.mt = q.m > 0 ? (q.m + q.bm - 1) / q.bm : 0;
-    q.nt = (L.n + q.bn - 1) / q.bn;
-    q.kb = L.k / 128;
-    q.kd = L.kind;
+    q.bn = cfg_bn(q.cfg, raw_m >= 0 ? 1 : ph);  // raw mode: one linear
+    q.mt = q.m > 0 ? div_small(q.m + q.bm - 1, q.bm) : 0;
+    q.nt = div_small(s_n[ph][g] + q.bn - 1, q.bn);
+    q.kb = s_kb[ph][g];
+    q.kd = s_kd[ph][g];
     q.nl = (raw_m < 0 && ph == 0) ? 2 : 1;
     return q;
   };
-  __shared__ int64_t s_work[2][1024 / 64];
+
+  // 1. the phase's work (tiles times unsliced tile cost, summed exactly) sets
+  //    the slicing threshold; then per group the proposed slices and, for the
+  //    budget pass, the partial-sum floats (capped at pfloats + 1, which no
+  //    budget admits) and the output tiles of every group that would be sliced
   for (int ph = 0; ph < nphase; ++ph) {
     int64_t w = 0;
     for (int g = tid; g < G; g += blockDim.x) {
@@ -110,30 +162,31 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     for (int d = 32; d > 0; d >>= 1) w += __shfl_xor(w, d, 64);
     if (lane == 0) s_work[ph][wave] = w;
   }
-  __syncthreads();
-  for (int ph = 0; ph < nphase; ++ph) {
+  lds_barrier();
+  if (tid < nphase) {
     int64_t work = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) work += s_work[ph][i];
-    const int64_t theta = work / nwg / kSplitShare;
-    for (int g = tid; g < G; g += blockDim.x) {
-      const Geom q = geom(ph, g);
-      const int sp = choose_split(q.bm, q.bn, q.nl, q.kd, q.kb, q.mt, q.nt, theta);
-      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      r[PF_EXPERT] = g;
-      r[PF_M] = q.m;
-      r[PF_CFG] = q.cfg;
-      r[PF_MTILES] = q.mt;
-      r[PF_NTILES] = q.nt;
-      r[PF_START] = 0;
-      if (ph == 0 && raw_m < 0) down_qmax[g] = kind_qmax(experts[g].lin[2].kind);
-      const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
-      s_sp[ph][g] = (int8_t)sp;
-      s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
-      s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
-    }
+    for (int i = 0; i < nwave; ++i) work += s_work[tid][i];
+    s_theta[tid] = work / nwg / kSplitShare;
   }
-  if (tid == 0) misc[8] = nwg;
-  __syncthreads();
+  lds_barrier();
+  for (int item = tid; item < nphase * G; item += blockDim.x) {
+    const int ph = item >= G, g = item - ph * G;
+    const int64_t theta = s_theta[ph];
+    const Geom q = geom(ph, g);
+    const int sp = choose_split(q.bm, q.bn, q.nl, q.kd, q.kb, q.mt, q.nt, theta);
+    int32_t* r = rec_of(ph, g);
+    r[PF_EXPERT] = g;
+    r[PF_M] = q.m;
+    r[PF_CFG] = q.cfg;
+    r[PF_MTILES] = q.mt;
+    r[PF_NTILES] = q.nt;
+    r[PF_START] = 0;
+    const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
+    s_sp[ph][g] = (int8_t)sp;
+    s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
+    s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
+  }
+  lds_barrier();
   // 2. slices within the budgets, greedily in group order: a group is sliced
   //    if its partial sums and added tiles still fit, else it runs unsliced.
   //    One wavefront per phase takes 64 groups at a time; a chunk that fits
@@ -190,10 +243,11 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
         }
       }
       if (g < G) {
-        int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
+        int32_t* r = rec_of(ph, g);
         r[PF_SPLIT] = take ? sp : 1;
         r[PF_PBASE] = take ? (int32_t)pbase : 0;
         r[PF_CBASE] = take ? cbase : 0;
+        s_sp[ph][g] = (int8_t)(take ? sp : 1);
       }
     }
     if (lane == 0) {
@@ -201,92 +255,142 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       misc[6 + ph] = (int32_t)pused;
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 3. per-tile cost estimate with the final slices, arrival counters cleared
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
-      int32_t* r = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
       const Geom q = geom(ph, g);
-      const int sp = r[PF_SPLIT];
+      const int sp = s_sp[ph][g];
       const int tiles = q.mt * q.nt * sp;
       const int c = tiles ? tile_cost(q.bm, q.bn, q.nl, q.kd, (q.kb + sp - 1) / sp * 128, sp, q.mt, q.nt) : 0;
-      r[PF_COST] = c;
+      rec_of(ph, g)[PF_COST] = c;
       s_cost[ph][g] = c;
       s_tiles[ph][g] = tiles;
+      if (tiles > 0) atomicAdd(&s_ng[ph], 1);
     }
     int32_t* cnt = plan + PL.cnt + (int64_t)ph * kSplitExtra;
     for (int i = tid; i < s_used[ph]; i += blockDim.x) cnt[i] = 0;
   }
-  __syncthreads();
-  // 4. rank the groups by decreasing tile cost (ties: lower group first)
-  int32_t* order = plan + PL.order;
-  for (int ph = 0; ph < nphase; ++ph) {
-    for (int g = tid; g < G; g += blockDim.x) {
-      int rank = -1;
-      if (s_tiles[ph][g] > 0) {
-        rank = 0;
-        const int cg = s_cost[ph][g];
-        for (int h = 0; h < G; ++h) {
-          if (s_tiles[ph][h] <= 0) continue;
-          const int ch = s_cost[ph][h];
-          rank += (ch > cg) || (ch == cg && h < g);
-        }
+  lds_barrier();
+  // 4. rank the groups by decreasing tile cost (ties: lower group first); one
+  //    wavefront counts the groups ahead of one group
+  for (int item = wave; item < nphase * G; item += nwave) {
+    const int ph = item >= G, g = item - ph * G;
+    int rank = -1;
+    if (s_tiles[ph][g] > 0) {
+      const int cg = s_cost[ph][g];
+      int ahead = 0;
+      for (int h = lane; h < G; h += 64) {
+        const int ch = s_cost[ph][h];
+        ahead += s_tiles[ph][h] > 0 && ((ch > cg) || (ch == cg && h < g));
+      }
+      for (int d = 32; d > 0; d >>= 1) ahead += __shfl_xor(ahead, d, 64);
+      rank = ahead;
+      if (lane == 0) {
+        s_order[ph][rank] = g;
         order[(int64_t)ph * G + rank] = g;
       }
-      plan[PL.rec + ((int64_t)ph * G + g) * PF_N + PF_RANK] = rank;
     }
+    if (lane == 0) rec_of(ph, g)[PF_RANK] = rank;
   }
-  __syncthreads();
+  lds_barrier();
   // 5. super-tiles dealt to the XCD queues, 6. expanded to tile entries
   for (int ph = 0; ph < nphase; ++ph) {
-    int ng = 0;
-    for (int g = 0; g < G; ++g) ng += s_tiles[ph][g] > 0;  // same value in every thread
+    const int ng = s_ng[ph];
     for (int r = ng + tid; r < G; r += blockDim.x) order[(int64_t)ph * G + r] = -1;
+    auto dims = [&](int g, int* mt, int* ntv) {  // row tiles, channel tiles x slices
+      const Geom q = geom(ph, g);
+      *mt = q.mt;
+      *ntv = q.nt * s_sp[ph][g];
+    };
     for (int r = tid; r < ng; r += blockDim.x) {
-      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + order[(int64_t)ph * G + r]) * PF_N;
-      s_ns[r] = super_tiles(rec[PF_MTILES], rec[PF_NTILES] * rec[PF_SPLIT]);
+      int mt, ntv;
+      dims(s_order[ph][r], &mt, &ntv);
+      const SuperDims dd = plan_super_dims(mt, ntv);
+      s_ns[r] = (mt > 0 && ntv > 0) ? dd.nsm * dd.nsn : 0;
     }
-    __syncthreads();
+    lds_barrier();
     const int S = block_scan(s_ns, ng, s_red);  // s_ns[r]: first global super-tile of rank r
-    int32_t* ent = plan + PL.ent + (int64_t)ph * kXcd * qcap * 3;
-    // deal super-tile u to queue u % kXcd, position u / kXcd
-    for (int u = tid; u < S; u += blockDim.x) {
+    // super-tile u -> (rank, index within the group)
+    auto locate = [&](int u, int* g, int* st) {
       int lo = 0, hi = ng;
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
         if (s_ns[mid] <= u) lo = mid; else hi = mid;
       }
-      const int g = order[(int64_t)ph * G + lo];
-      const int s = u - s_ns[lo];
-      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      if (u / kXcd >= qcap) {  // cannot happen with the host's capacity bound
-        misc[4] = 1;
-        continue;
-      }
-      int32_t* e = ent + ((int64_t)(u % kXcd) * qcap + u / kXcd) * 3;
-      e[0] = g;
-      e[1] = s;
-      e[2] = super_tile_size(rec[PF_MTILES], rec[PF_NTILES] * rec[PF_SPLIT], s);
-    }
-    __syncthreads();
-    // per-queue exclusive prefix sums of the entry sizes, one wavefront per queue
+      *g = s_order[ph][lo];
+      *st = u - s_ns[lo];
+    };
+    int32_t* ent = plan + PL.ent + (int64_t)ph * kXcd * qcap * 3;
     int32_t* ctr = plan + PL.ctr + (int64_t)ph * kXcd * 4;
+    if (tid == 0 && (S + kXcd - 1) / kXcd > qcap) misc[4] = 1;  // cannot happen with the host's capacity bound
+    // deal super-tile u to queue u % kXcd, position u / kXcd; one wavefront per
+    // queue forms the exclusive prefix sums of the entry sizes (each entry's
+    // first tile) and expands each entry into its tiles
+    int32_t* flat = plan + PL.flat + (int64_t)ph * kXcd * fcap * 4;
     if (wave < kXcd) {
       const int x = wave;
       int n = S / kXcd + (x < S % kXcd ? 1 : 0);
       n = n < qcap ? n : qcap;
-      int32_t* q = ent + (int64_t)x * qcap * 3 + 2;
+      int32_t* q = ent + (int64_t)x * qcap * 3;
       int run = 0;
       for (int c0 = 0; c0 < n; c0 += 64) {
         const int i = c0 + lane;
-        const int v = i < n ? q[(int64_t)i * 3] : 0;
+        int g = 0, st = 0, v = 0, mt = 0, ntv = 0;
+        if (i < n) {
+          locate(i * kXcd + x, &g, &st);
+          dims(g, &mt, &ntv);
+          const SuperDims dd = plan_super_dims(mt, ntv);
+          const int sni = div_small(st, dd.nsm), smi = st - sni * dd.nsm;
+          v = min(dd.sm, mt - smi * dd.sm) * min(dd.sn, ntv - sni * dd.sn);
+        }
         int incl = v;
         for (int d = 1; d < 64; d <<= 1) {
           const int t = __shfl_up(incl, d, 64);
           if (lane >= d) incl += t;
         }
-        if (i < n) q[(int64_t)i * 3] = run + incl - v;
+        const int first = run + incl - v;
         run += __shfl(incl, 63, 64);
+        // this lane's entry: its record, and what expanding it takes
+        int w0 = 0, off_e = 0, m_g = 0, mi0 = 0, ni0 = 0, em = 1, inv = 65536, size = 0;
+        if (i < n) {
+          q[(int64_t)i * 3 + 0] = g;
+          q[(int64_t)i * 3 + 1] = st;
+          q[(int64_t)i * 3 + 2] = first;
+          if (first + v <= fcap) {
+            const SuperDims dd = plan_super_dims(mt, ntv);
+            const int sni = div_small(st, dd.nsm), smi = st - sni * dd.nsm;
+            em = min(dd.sm, mt - smi * dd.sm);
+            inv = div_small(65536 + em - 1, em);  // t / em = (t * inv) >> 16 for t < 64, em <= 8
+            mi0 = smi * dd.sm;
+            ni0 = sni * dd.sn;
+            w0 = tile_word0(g, pick_cfg(s_m[g]), s_kd[ph][g], s_sp[ph][g]);
+            off_e = s_off[g];
+            m_g = s_m[g];
+            size = v;
+          } else {
+            misc[4] = 1;  // cannot happen with the host's capacity bound
+          }
+        }
+        // The chunk's entries are expanded one at a time by the whole
+        // wavefront (lane t writes the entry's tile t, row tile fastest, the
+        // order of super_tile_pos), so that every store is contiguous; the
+        // entry's fields come from its lane's registers.
+        const int cnt = n - c0 < 64 ? n - c0 : 64;
+        for (int j = 0; j < cnt; ++j) {
+          const int sz = __builtin_amdgcn_readlane(size, j);
+          if (sz == 0) continue;
+          const int fj = __builtin_amdgcn_readlane(first, j);
+          const int emj = __builtin_amdgcn_readlane(em, j), invj = __builtin_amdgcn_readlane(inv, j);
+          const int w0j = __builtin_amdgcn_readlane(w0, j), offj = __builtin_amdgcn_readlane(off_e, j);
+          const int mgj = __builtin_amdgcn_readlane(m_g, j);
+          const int mi0j = __builtin_amdgcn_readlane(mi0, j), ni0j = __builtin_amdgcn_readlane(ni0, j);
+          if (lane < sz) {
+            const int b2 = (int)(((uint32_t)lane * (uint32_t)invj) >> 16), a2 = lane - b2 * emj;
+            reinterpret_cast<int4*>(flat + ((int64_t)x * fcap + fj) * 4)[lane] =
+                make_int4(w0j, (mi0j + a2) | ((ni0j + b2) << 16), offj, mgj);
+          }
+        }
       }
       if (lane == 0) {
         ctr[x * 4 + 0] = 0;
@@ -294,36 +398,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
         ctr[x * 4 + 2] = n;
       }
     }
-    __syncthreads();
-    // expand the queues: one thread per queue entry writes its tiles
-    int32_t* flat = plan + PL.flat + (int64_t)ph * kXcd * fcap * 4;
-    for (int u = tid; u < S; u += blockDim.x) {
-      const int x = u % kXcd, pos = u / kXcd;
-      if (pos >= qcap) continue;
-      const int32_t* e = ent + ((int64_t)x * qcap + pos) * 3;
-      const int g = e[0], st = e[1], first = e[2];
-      const int32_t* rec = plan + PL.rec + ((int64_t)ph * G + g) * PF_N;
-      const int sp = rec[PF_SPLIT];
-      const int mt = rec[PF_MTILES], ntv = rec[PF_NTILES] * sp;
-      const int size = super_tile_size(mt, ntv, st);
-      if (first + size > fcap) {  // cannot happen with the host's capacity bound
-        misc[4] = 1;
-        continue;
-      }
-      const int kd = raw_m >= 0 ? raw_lin.kind : experts[g].lin[ph == 0 ? 0 : 2].kind;
-      const int w0 = tile_word0(g, rec[PF_CFG], kd, sp);
-      const int off_e = (raw_m < 0 && g < E) ? offsets[g] : 0;
-      const int m_g = rec[PF_M];
-      int32_t* f = flat + ((int64_t)x * fcap + first) * 4;
-      for (int t = 0; t < size; ++t) {
-        int mi, ni;
-        super_tile_pos(mt, ntv, st, t, &mi, &ni);
-        *reinterpret_cast<int4*>(f + 4 * t) = make_int4(w0, mi | (ni << 16), off_e, m_g);
-      }
-    }
-    __syncthreads();
     if (tid == 0) misc[2 + ph] = ng;
-    __syncthreads();
+    lds_barrier();
   }
   if (nphase == 1) {  // single-linear mode: the second phase is empty
     int32_t* ctr = plan + PL.ctr + (int64_t)kXcd * 4;
