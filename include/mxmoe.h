@@ -243,6 +243,10 @@ typedef struct {
   size_t plan_flat_cap; /* tiles per XCD queue in the tile plan              */
   size_t partial;       /* fp32 split-K partial sums                         */
   size_t partial_floats;/* size of that buffer (floats)                      */
+  size_t rsx;           /* fp32 [T, H/128]: row sums of x per 128-wide block
+                           (bf16 blocks with 2/3/4-bit gate|up), else -1    */
+  size_t rsh;           /* fp32 [T*k, F/128]: same for routed h, else -1     */
+  size_t rsh_shared;    /* fp32 [n_shared*T, F_shared/128], else -1          */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

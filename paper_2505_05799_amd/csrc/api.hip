@@ -58,6 +58,7 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 struct BlockInfo {
   int H, F, E, k, nsh, Fsh, act, G;
   bool any_x8 = false, any_x4 = false, any_hq = false, any_hq_sh = false;
+  bool rs_x = false, rs_h = false, rs_hsh = false;  // row sums of x / h / h_shared needed (bf16)
   int kinds[kMaxG][3];
 };
 
@@ -92,6 +93,8 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
     if (kg == K_W8A8) bi->any_x8 = true;
     if (kg == K_W4A4) bi->any_x4 = true;
     if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
+    if (bi->act == MXMOE_BF16 && kind_is_magic(kg)) bi->rs_x = true;
+    if (bi->act == MXMOE_BF16 && kind_is_magic(bi->kinds[g][2])) (sh ? bi->rs_hsh : bi->rs_h) = true;
   }
   return MXMOE_OK;
 }
@@ -135,6 +138,9 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   if (bi.any_hq) { L.hq = take(P * bi.F); L.hs = take(4 * P); }
   if (bi.any_hq_sh) { L.hq_shared = take((size_t)bi.nsh * T * bi.Fsh); L.hs_shared = take(4 * (size_t)bi.nsh * T); }
   L.slots = take(4 * (size_t)T * (bi.k + bi.nsh) * bi.H);
+  L.rsx = bi.rs_x ? take(4 * (size_t)T * (bi.H / 128)) : kNone;
+  L.rsh = bi.rs_h ? take(4 * P * (bi.F / 128)) : kNone;
+  L.rsh_shared = bi.rs_hsh ? take(4 * (size_t)bi.nsh * T * (bi.Fsh / 128)) : kNone;
   L.total = o;
   return L;
 }
@@ -232,7 +238,7 @@ mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32
 
 // -------------------------------------------------------- single linear
 namespace {
-struct LinWs { size_t plan, partial, aq, as, total; int qcap, fcap; int64_t pfloats; };
+struct LinWs { size_t plan, partial, aq, as, rsa, total; int qcap, fcap; int64_t pfloats; };
 LinWs lin_layout(int kd, int m, int n, int k) {
   LinWs w;
   size_t o = 0;
@@ -241,11 +247,13 @@ LinWs lin_layout(int kd, int m, int n, int k) {
   w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap, w.fcap).total);
   w.pfloats = std::min<int64_t>((int64_t)1 << 24, 4 * (int64_t)m * n);
   w.partial = o; o = align256(o + 4 * (size_t)w.pfloats);
-  w.aq = w.as = kNone;
+  w.aq = w.as = w.rsa = kNone;
   if (kind_is_int(kd)) {
     w.aq = o; o = align256(o + (size_t)m * k);
     w.as = o; o = align256(o + 4 * (size_t)m);
   }
+  // row sums of the input per 128-wide k block (used with bf16 activations)
+  if (kind_is_magic(kd)) { w.rsa = o; o = align256(o + 4 * (size_t)m * (k / 128)); }
   w.total = o;
   return w;
 }
@@ -297,6 +305,11 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     hipError_t e = launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
+  }
+  if (act == MXMOE_BF16 && kind_is_magic(kd)) {
+    float* rs = at<float>(workspace, w.rsa);
+    if (launch_rowsum(a, m, L->k, L->k, rs, stream) != hipSuccess) return MXMOE_ERR_HIP;
+    ga.rsx = rs;
   }
   const int grid = group_gemm_grid(current_device());
   hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, w.pfloats,
@@ -372,6 +385,9 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->plan_flat_cap = (size_t)L.fcap;
   out->partial = L.partial;
   out->partial_floats = (size_t)L.pfloats;
+  out->rsx = L.rsx;
+  out->rsh = L.rsh;
+  out->rsh_shared = L.rsh_shared;
   return MXMOE_OK;
 }
 
@@ -433,6 +449,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if (bi.any_x4)
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4), at<float>(workspace, L.xs4),
                               stream));
+  if (bi.rs_x) MX_CHECK(launch_rowsum(x, T, bi.H, bi.H, at<float>(workspace, L.rsx), stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, topk_w, at<float>(workspace, L.xs8),
                            at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
                            at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
@@ -471,6 +488,9 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.rxs8 = at<float>(workspace, L.rxs8);
   ga.rxs4 = at<float>(workspace, L.rxs4);
   ga.partial = at<float>(workspace, L.partial);
+  ga.rsx = at<float>(workspace, L.rsx);
+  ga.rsh = at<float>(workspace, L.rsh);
+  ga.rsh_shared = at<float>(workspace, L.rsh_shared);
   MX_EVENT(1);
   MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));

@@ -208,6 +208,29 @@ __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, 
                        act, qmax, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hs + r, red);
 }
 
+// Row sums of each 128-wide block of bf16 rows, one wavefront per row: a
+// block is 16 chunks of 8 elements, one per lane of a 16-lane group; each lane
+// adds its 8 values in order, then the group adds its lanes pairwise.
+__global__ void __launch_bounds__(kThreads) rowsum_kernel(const uint16_t* __restrict__ a, int rows, int cols,
+                                                          int64_t ld, float* __restrict__ out) {
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const int lane = threadIdx.x & 63, nch = cols >> 3, nb = cols >> 7;
+  const uint4* row = reinterpret_cast<const uint4*>(a + r * ld);
+  for (int c0 = 0; c0 < nch; c0 += 64) {  // nch is a multiple of 16: groups stay whole
+    const int c = c0 + lane;
+    float sum = 0.f;
+    if (c < nch) {
+      float f[8];
+      unpack8(row[c], MXMOE_BF16, f);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sum += f[i];
+    }
+    for (int d = 1; d < 16; d <<= 1) sum += __shfl_xor(sum, d, 64);
+    if ((lane & 15) == 0 && c < nch) out[r * nb + (c >> 4)] = sum;
+  }
+}
+
 // 8 outputs per thread.  SC > 0 slots (compile time): every slot row is
 // loaded before the expert ids are consulted (rows of dropped pairs are in
 // bounds, their values unused); SC == 0: any slot count, one slot at a time.
@@ -310,6 +333,14 @@ hipError_t launch_rows(int rows, int cols, hipStream_t s, Args... args) {
 template <int NC, int W> struct ActQuantK { static constexpr auto fn = act_quant_vec_kernel<NC, W>; };
 template <int NC, int W> struct HQuantK { static constexpr auto fn = hquant_routed_kernel<NC, W>; };
 }  // namespace
+
+hipError_t launch_rowsum(const void* a, int rows, int cols, int64_t ld, float* out, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15) || cols % 128 || ld % 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rowsum_kernel, dim3((rows + kRowsPerBlock - 1) / kRowsPerBlock), dim3(kThreads), 0, s,
+                     reinterpret_cast<const uint16_t*>(a), rows, cols, ld, out);
+  return hipGetLastError();
+}
 
 hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax, int8_t* codes,
                             float* scales, hipStream_t s) {

@@ -295,6 +295,17 @@ template <int KD> __device__ inline i32x4 wfrag8(const Raw<KD>& r, u32x4 step, i
   }
 }
 
+// Sum over each 16-lane row of the wavefront, left in every lane, through DPP
+// lane moves inside the row (neighbour swap, pair swap, half-row mirror, row
+// mirror).
+__device__ inline float row16_sum(float t) {
+  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0xB1, 0xf, 0xf, false));
+  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x4E, 0xf, 0xf, false));
+  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x141, 0xf, 0xf, false));
+  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x140, 0xf, 0xf, false));
+  return t;
+}
+
 // ------------------------------------------------------------- LDS stage
 struct __align__(16) Smem {
   uint8_t act[2][STAGE_BYTES];   // activation rows of the tile, one 128-wide k block per stage
@@ -307,6 +318,7 @@ struct __align__(16) Smem {
   int32_t qtotal[kXcd];          // tiles per XCD queue
   int32_t qi;                    // queues tried so far by this workgroup
   int32_t last;                  // split-K: this workgroup finishes the output tile
+  float hrs[4 * BM_MAX];         // gate|up epilogue: h row sums of each wavefront's channels
 };
 
 // Tile queues of one phase, rebuilt from the kernel arguments where needed so
@@ -421,18 +433,21 @@ template <bool INT> __device__ inline u32x4 act_frag(const Smem& sm, int buf, in
   return *reinterpret_cast<const u32x4*>(sm.act[buf] + r * (INT ? 128 : 256) + pos * 16);
 }
 
-// Row sums of a 16-bit stage: MFMA of each 16-row fragment against ones; the
-// fragments are shared out over the wavefronts.
-template <int ACT, int MF> __device__ inline void stage_rowsum(Smem& sm, int buf, int tid) {
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
-  const int li = lane & 15, q = lane >> 4;
-  const u32x4 ones = ACT == MXMOE_BF16 ? u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u}
-                                       : u32x4{0x3C003C00u, 0x3C003C00u, 0x3C003C00u, 0x3C003C00u};
-  for (int mf = wave; mf < MF; mf += 4) {
-    f32x4 s = {0, 0, 0, 0};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) s = mfma16<ACT>(act_frag<false>(sm, buf, mf * 16 + li, 4 * j + q), ones, s);
-    if (li == 0) *reinterpret_cast<f32x4*>(&sm.rsum[buf][mf * 16 + 4 * q]) = s;
+// Row sums of a stage (bias-dequantized kinds with bf16 activations): one
+// direct global->LDS load of 4 bytes per lane brings the precomputed sums of
+// rows 64w .. 64w + 63 of k block kb into sm.rsum[buf] (wavefronts
+// w < ceil(BM / 64)); rsoff: the lane's row offset (bytes) at k block 0.
+__device__ inline void lds_dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "memory", "m0");
+}
+template <int BM>
+__device__ inline void rowsum_load(Smem& sm, int buf, const float* rsbase, uint32_t rsoff, int kb, int wave) {
+  if (wave * 64 < BM) {
+    const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.rsum[buf][wave * 64]);
+    lds_dma4(reinterpret_cast<const uint8_t*>(rsbase + kb), rsoff, __builtin_amdgcn_readfirstlane(lds));
   }
 }
 
@@ -525,6 +540,15 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   __syncthreads();
   StageOffs<INT, BM> soffs;
   stage_offsets<INT, BM>(soffs, sm, row_bytes, wave, lane);
+  // row sums of the tile's activation rows per k block (bias-dequantized
+  // kinds, bf16): x rows in the gate|up phase, h rows in the down phase
+  const float* rsbase = nullptr;
+  uint32_t rsoff = 0;
+  if constexpr (RSUM) {
+    rsbase = PHASE == 1 ? (shared ? a.rsh_shared : a.rsh) : a.rsx;
+    const int r = wave * 64 + lane;
+    rsoff = (uint32_t)sm.rowsrc[r < BM ? r : 0] * (uint32_t)kblocks * 4u;
+  }
 
   // ---- accumulators and weight streams
   typedef typename std::conditional<INT, i32x4, f32x4>::type AccT;
@@ -577,7 +601,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       for (int nf = 0; nf < NF; ++nf)
         st[j][l][nf] = load_step<KD>(wp[l][nf] + (last ? 0 : (int64_t)kn * BB) + lo, j);
   };
-  // Vector-memory loads issued after the activation stage of the next k block,
+  // Vector-memory loads issued after the activation stage (and its row sums) of
+  // the next k block,
   // at least: one per fragment and step (streamed), one per fragment (group
   // prefetch; two 16-byte loads for w8a8), plus one metadata dword per fragment
   // (weight-only).  Waiting for
@@ -585,6 +610,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (WONLY ? NL * NF : 0);
 
   stage_load<INT, BM>(sm, 0, abase, soffs, kb0, wave);
+  if constexpr (RSUM) rowsum_load<BM>(sm, 0, rsbase, rsoff, kb0, wave);
   load_group(kb0, false);
   if constexpr (streamed<KD>()) {
 #pragma unroll
@@ -592,15 +618,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if constexpr (RSUM) {
-    stage_rowsum<ACT, MF>(sm, 0, tid);
-    __syncthreads();
-  }
 
   for (int kb = kb0; kb < kb1; ++kb) {
     const int cur = (kb - kb0) & 1;
     const bool more = kb + 1 < kb1;
     if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
+    if constexpr (RSUM) {
+      if (more) rowsum_load<BM>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
+    }
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
@@ -705,12 +730,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     if (more) wait_vmem<kLoadsAfterStage>();
     else wait_vmem<0>();
     lds_barrier();
-    if constexpr (RSUM) {
-      if (more) {
-        stage_rowsum<ACT, MF>(sm, cur ^ 1, tid);
-        lds_barrier();
-      }
-    }
   }
 
   // ---- split-K: partial sums of this slice; the last slice to arrive adds
@@ -774,28 +793,40 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
 
   // ---- epilogue: lane holds rows 4q + i of fragment mf, channel li of fragment nf
-  // (the per-row data is re-read from LDS for every fragment: holding it for
-  // all fragments would cost 64-96 registers next to the accumulators)
+  // (the per-row data is re-read from LDS for every row fragment: holding it
+  // for all fragments would cost 64-96 registers next to the accumulators)
   const bool full = row0 + BM <= m_g;  // uniform: no row of the tile lies past the group
+  // gate|up with a bias-dequantized down projection (bf16): the tile also
+  // writes the row sums of its h values per 128-wide block, which the down
+  // phase subtracts (the tile's channels are whole blocks: BN is 128 or 256)
+  float* rsh_out = nullptr;
+  if constexpr (PHASE == 0 && ACT == MXMOE_BF16) {
+    // (the kind is read as a wave-uniform value: the branch around the barrier
+    // below must not look divergent to the compiler)
+    if (kind_is_magic(__builtin_amdgcn_readfirstlane(ex->lin[2].kind))) rsh_out = shared ? a.rsh_shared : a.rsh;
+  }
   auto epilogue = [&](auto guard) {
     constexpr bool GUARD = decltype(guard)::value;
+    float cs[NL][NF];
 #pragma unroll
-    for (int nf = 0; nf < NF; ++nf) {
-      if (nf >= nvalid) continue;
-      const int n = 16 * (nb0 + nf) + li;
-      float cs[NL];
+    for (int nf = 0; nf < NF; ++nf)
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
-        cs[l] = 1.f;
-        if constexpr (INT) cs[l] = lins[l]->wscale[n];
-        if constexpr (WONLY) cs[l] = s_prev[l][nf];
+        cs[l][nf] = 1.f;
+        if constexpr (INT) cs[l][nf] = nf < nvalid ? lins[l]->wscale[16 * (nb0 + nf) + li] : 0.f;
+        if constexpr (WONLY) cs[l][nf] = s_prev[l][nf];
       }
 #pragma unroll
-      for (int mf = 0; mf < MF; ++mf) {
-        const int r = mf * 16 + 4 * q;
-        const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
-        const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
-        const i32x4 ro = *reinterpret_cast<const i32x4*>(&sm.rowout[r]);
+    for (int mf = 0; mf < MF; ++mf) {
+      const int r = mf * 16 + 4 * q;
+      const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
+      const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
+      const i32x4 ro = *reinterpret_cast<const i32x4*>(&sm.rowout[r]);
+      float hsum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int nf = 0; nf < NF; ++nf) {
+        if (nf >= nvalid) continue;
+        const int n = 16 * (nb0 + nf) + li;
         float v[NL][4];
 #pragma unroll
         for (int l = 0; l < NL; ++l)
@@ -804,21 +835,24 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             if constexpr (INT) {
               int iv = acc[l][nf][mf][i];
               if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
-              v[l][i] = ((float)iv * rs[i]) * cs[l];
+              v[l][i] = ((float)iv * rs[i]) * cs[l][nf];
             } else {
-              v[l][i] = acc[l][nf][mf][i] * cs[l];
+              v[l][i] = acc[l][nf][mf][i] * cs[l][nf];
             }
           }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          if (GUARD && ro[i] < 0) continue;
           const int64_t orow = (int64_t)ro[i] * N + n;
           if constexpr (PHASE == 0) {
-            uint16_t* hb = reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h);
-            hb[orow] = f32_to_act<ACT>(silu_f32(v[0][i]) * v[1][i]);
+            const uint16_t hv = f32_to_act<ACT>(silu_f32(v[0][i]) * v[1][i]);
+            hsum[i] += __uint_as_float((uint32_t)hv << 16);  // bf16 value (used only for bf16)
+            if (GUARD && ro[i] < 0) continue;
+            reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h)[orow] = hv;
           } else if constexpr (PHASE == 1) {
+            if (GUARD && ro[i] < 0) continue;
             a.slots[orow] = v[0][i] * gwv[i];
           } else {
+            if (GUARD && ro[i] < 0) continue;
             if constexpr (INT) {
               int iv = acc[0][nf][mf][i];
               if constexpr (KD == K_W4A4) iv >>= 4;
@@ -827,6 +861,30 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
               reinterpret_cast<float*>(a.raw_out)[orow] = v[0][i];
             }
           }
+        }
+      }
+      if constexpr (PHASE == 0) {
+        if (rsh_out) {  // this wavefront's channels: sum over the 16 lanes of a row group
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float t = row16_sum(hsum[i]);
+            if (li == 0) sm.hrs[wave * BM + r + i] = t;
+          }
+        }
+      }
+    }
+    if constexpr (PHASE == 0) {
+      if (rsh_out) {  // the wavefronts of one 128-wide block add their sums
+        lds_barrier();
+        constexpr int KBT = BN / 128, WPK = 4 / KBT;
+        if (tid < BM * KBT) {
+          const int r = tid % BM, j = tid / BM;
+          const int kbg = nt * KBT + j, nkb = N / 128;
+          float t = 0.f;
+#pragma unroll
+          for (int w = 0; w < WPK; ++w) t += sm.hrs[(j * WPK + w) * BM + r];
+          const int ro = sm.rowout[r];
+          if (ro >= 0 && kbg < nkb) rsh_out[(int64_t)ro * nkb + kbg] = t;
         }
       }
     }

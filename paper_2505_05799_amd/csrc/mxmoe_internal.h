@@ -39,6 +39,9 @@ __host__ __device__ constexpr inline int kind_wbits(int kd) {
   }
 }
 // activation qmax of an integer scheme (0 for 16-bit activations)
+// 2/3/4-bit group-wise kinds: dequantized through a bias whose product with
+// the activations is removed through activation row sums (16-bit bf16 path)
+__host__ __device__ constexpr inline bool kind_is_magic(int kd) { return kd == K_W2G || kd == K_W3G || kd == K_W4G; }
 __host__ __device__ constexpr inline int kind_qmax(int kd) {
   return kd == K_W8A8 ? 127 : (kd == K_W4A4 ? 7 : 0);
 }
@@ -219,6 +222,7 @@ struct WsLayout {
   size_t rtok, rslot, rgw, rxs8, rxs4;
   size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
   size_t partial;  // fp32 split-K partial sums (both phases reuse it)
+  size_t rsx, rsh, rsh_shared;  // fp32 row sums per 128-wide k block of x, h, h_shared
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -238,6 +242,9 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
                         int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
                         int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
 
+// Row sums of each 128-wide block of bf16 rows: out[r][b] = sum of a[r][128b ..
+// 128b + 127] in fp32; cols a multiple of 128, rows 16-byte aligned.
+hipError_t launch_rowsum(const void* a, int rows, int cols, int64_t ld, float* out, hipStream_t s);
 hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax,
                             int8_t* codes, float* scales, hipStream_t s);
 
@@ -278,6 +285,11 @@ struct GemmArgs {
   float* partial;      // split-K partial sums
   // per sorted row (see launch_row_meta)
   const int32_t* rtok; const int32_t* rslot; const float* rgw; const float* rxs8; const float* rxs4;
+  // Row sums of each 128-wide k block of the 16-bit activation rows that the
+  // bias-dequantized weight kinds need (bf16): x [T][H/128] (the input in
+  // single-linear mode), routed h [P][F/128] and shared h [n_shared*T][F_sh/128],
+  // the latter two written by the gate|up epilogue.
+  const float* rsx; float* rsh; float* rsh_shared;
   // single-linear mode (mxmoe_linear_forward): raw int32 / fp32 output
   DevLinear raw_lin;
   void* raw_out;

@@ -48,7 +48,7 @@ class ForwardOpts_t(C.Structure):
 
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
              "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total", "plan_queue_cap",
-             "plan_flat_cap", "partial", "partial_floats"]
+             "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared"]
 
 
 class WsLayout_t(C.Structure):
