@@ -61,15 +61,18 @@ typedef enum {
 
 typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
 
-/* Quantization scheme of one linear block: w{w_bits}a{a_bits}_g{w_group}.
+/* Quantization scheme of one linear block: w{w_bits}a{a_bits}_g{w_group}
+ * (notation of Fig. 1; a_gsize of the W5A5 allocation table).
  * Accepted combinations:
- *   {16,16,-1,-1,0}  {8,8,-1,-1,1}  {4,4,-1,-1,1}  {N,16,128,-1,0} N=2,3,4,8  */
+ *   {16,16,-1,-1,0}  {8,8,-1,-1,1}  {4,4,-1,-1,1}  {N,16,128,-1,0} N=2,3,4,8
+ *   {4,4,128,128,1}  w4a4-g128: symmetric 4-bit weights and activations with
+ *                    one scale per 128 consecutive k of a channel / a token  */
 typedef struct {
   int32_t w_bits;
   int32_t a_bits;     /* 16 = weight-only                                       */
   int32_t w_group;    /* 128, or -1 = per output channel                        */
-  int32_t a_group;    /* -1 = per token (the only activation granularity here)  */
-  int32_t symmetric;  /* 1 for w8a8 / w4a4, 0 otherwise                         */
+  int32_t a_group;    /* 128, or -1 = per token                                 */
+  int32_t symmetric;  /* 1 for w8a8 / w4a4 (per channel or g128), 0 otherwise   */
 } mxmoe_scheme;
 
 /* One linear block y = x W^T with W of shape [n, k] = [out, in].
@@ -85,6 +88,7 @@ typedef struct {
 /* Bytes of the packed form of linear *L (host) for activations `act`:
  *   wNg128: n*k*N/8 + (n*k/128)*4   (N + 0.25 bits per weight, Sec. 5.2)
  *   w8a8/w4a4: n*k*b/8 + 4*n
+ *   w4a4-g128: n*k/2 + (n*k/128)*4   (fp16 group scale, 4-byte slot per group)
  *   w16: 2*n*k
  * Returns 0 if *L is not supported.                                          */
 MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
@@ -92,9 +96,10 @@ MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
 /* Pack the quantized operands of one linear into the tile-major layout the
  * Group-GEMM streams (weight fragments in MFMA lane order, group metadata next
  * to its codes).  Runs once per weight load.
- *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4 int8 [n,k] in
- *            [-qmax, qmax]; w16: 16-bit weights [n,k] of dtype `w16_src`.
- *   scales : wNg128 fp16 [n, k/128]; w8a8/w4a4 fp32 [n]; NULL for w16.
+ *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4/w4a4-g128 int8
+ *            [n,k] in [-qmax, qmax]; w16: 16-bit weights [n,k] of `w16_src`.
+ *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4 fp32 [n];
+ *            NULL for w16.
  *   zeros  : wNg128 fp16 [n, k/128] holding integers in [0, 2^N-1]; else NULL.
  *   w16_src: dtype of 16-bit source weights; converted (RNE) to `act`.
  *   packed : output, mxmoe_packed_bytes(L, act) bytes, 256-byte aligned.
@@ -147,6 +152,8 @@ MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
  *   a  : [m, k] `act` activations (dense)
  *   out: w8a8 / w4a4 -> int32 [m, n] exact integer accumulators
  *        sum_c qa[m,c]*qw[n,c] (qa from the per-token quantizer);
+ *        w4a4-g128 -> fp32 [m, n]: per 128-wide block the exact integer sum
+ *        times s_a[m,b]*s_w[n,b], added over the blocks in fp32;
  *        other schemes -> fp32 [m, n] with fp32 accumulation.               */
 MXMOE_API mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
                                   int32_t m, const void* a, void* out, void* workspace,
@@ -247,6 +254,11 @@ typedef struct {
                            (bf16 blocks with 2/3/4-bit gate|up), else -1    */
   size_t rsh;           /* fp32 [T*k, F/128]: same for routed h, else -1     */
   size_t rsh_shared;    /* fp32 [n_shared*T, F_shared/128], else -1          */
+  size_t xq4g, xs4g;    /* int8 [T,H], fp32 [T, H/128]: x codes for w4a4-g128
+                           gate|up (else -1)                                  */
+  size_t hsg;           /* fp32 [T*k, F/128]: group scales of routed h rows
+                           for w4a4-g128 down (codes in hq), else -1         */
+  size_t hsg_shared;    /* fp32 [n_shared*T, F_shared/128], else -1          */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

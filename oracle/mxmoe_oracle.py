@@ -140,6 +140,10 @@ def dequant(lin, act: str) -> np.ndarray:
         sc = lin.scales.astype(np.float64)[..., None]
         z = lin.zeros.astype(np.float64)[..., None]
         return (sc * (q - z)).reshape(lin.n, lin.k)
+    if s.w_group > 0:  # symmetric groups (w4a4-g128): code times its group's scale
+        g = s.w_group
+        q = lin.codes.astype(np.float64).reshape(lin.n, lin.k // g, g)
+        return (q * lin.scales.astype(np.float64)[..., None]).reshape(lin.n, lin.k)
     return lin.codes.astype(np.float64) * lin.scales.astype(np.float64)[:, None]
 
 
@@ -169,6 +173,17 @@ def act_quant(a: np.ndarray, qmax: int) -> Tuple[np.ndarray, np.ndarray]:
     return q.astype(np.int8), s
 
 
+def act_quant_groups(a: np.ndarray, qmax: int, group: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The recipe of :func:`act_quant` applied to every block of `group`
+    consecutive columns of a row (activation group size of Sec. 4.2.2 and the
+    a_gsize column of the W5A5 allocation table).  Returns codes int8
+    [rows, cols] and scales fp32 [rows, cols / group]."""
+    a = np.asarray(a, dtype=np.float32)
+    m, k = a.shape
+    q, sc = act_quant(a.reshape(m * (k // group), group), qmax)
+    return q.reshape(m, k), sc.reshape(m, k // group)
+
+
 def _qmax(a_bits: int) -> int:
     return (1 << (a_bits - 1)) - 1
 
@@ -188,6 +203,16 @@ def linear(a: np.ndarray, lin, act: str, w_deq: Optional[np.ndarray] = None,
     ``return_int`` the exact integer accumulators are returned instead.
     """
     s = lin.scheme
+    if s.a_bits < 16 and s.a_group > 0:
+        # w4a4-g128: per 128-wide block b, the exact integer dot of the block's
+        # codes times s_a[m, b] * s_w[n, b], summed over the blocks in fp64
+        g = s.a_group
+        qa, sa = act_quant_groups(a.astype(np.float32), _qmax(s.a_bits), g)
+        out = np.zeros((a.shape[0], lin.n))
+        for b in range(lin.k // g):
+            blk = qa[:, b * g:(b + 1) * g].astype(np.float64) @ lin.codes[:, b * g:(b + 1) * g].astype(np.float64).T
+            out += blk * sa[:, b].astype(np.float64)[:, None] * lin.scales[:, b].astype(np.float64)[None, :]
+        return out
     if s.a_bits < 16:
         qa, sa = act_quant(a.astype(np.float32), _qmax(s.a_bits))
         acc = qa.astype(np.float64) @ lin.codes.astype(np.float64).T
@@ -225,6 +250,13 @@ _EPS_EPI = 2.0 ** -20         # relative to |h|, SiLU + product in fp32
 
 def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
                    w_deq: Optional[np.ndarray]) -> np.ndarray:
+    if lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
+        # fp32 running sum of block products: bounded like an fp32-accumulated GEMM
+        # on the dequantized operands
+        qa, sa = act_quant_groups(a.astype(np.float32), _qmax(lin.scheme.a_bits), lin.scheme.a_group)
+        ad = (qa.astype(np.float64).reshape(a.shape[0], -1, lin.scheme.a_group)
+              * sa.astype(np.float64)[..., None]).reshape(a.shape)
+        return _EPS_FLOAT_ACC * (np.abs(ad) @ np.abs(dequant(lin, act)).T)
     if lin.scheme.a_bits < 16:
         return _EPS_INT_EPI * np.abs(out)
     if w_deq is None:
@@ -238,42 +270,47 @@ def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
     The GPU rounds its fp32 h to the activation dtype; it can land on another
     neighbour than the oracle's fp64 h when h64 sits within ``dh`` of a rounding
     midpoint, and that can move an activation code.  Codes are monotone in h and
-    in 1/amax, so the reachable codes lie between the corner cases computed here.
+    in 1/amax, so the reachable codes lie between the corner cases computed here,
+    per quantization block (the whole row per token, or each 128-wide group).
     Returns slack [m, n] >= |effect on the down output| of every such move.
     """
     qmax = _qmax(lin.scheme.a_bits)
-    lo = round_to_act(h64 - dh, act)
-    hi = round_to_act(h64 + dh, act)
-    q0, s0 = act_quant(hb.astype(np.float32), qmax)
+    m, F = h64.shape
+    g = lin.scheme.a_group if lin.scheme.a_group > 0 else F
+    nb = F // g
+    lo = round_to_act(h64 - dh, act).reshape(m * nb, g)
+    hi = round_to_act(h64 + dh, act).reshape(m * nb, g)
+    q0, s0 = act_quant(hb.astype(np.float32).reshape(m * nb, g), qmax)
     alo = np.where(np.sign(lo) == np.sign(hi), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
     ahi = np.maximum(np.abs(lo), np.abs(hi))
     amax_lo = alo.max(axis=1)
     amax_hi = ahi.max(axis=1)
     rows = np.nonzero((lo != hi).any(axis=1) | (amax_lo != amax_hi))[0]
-    m, n = h64.shape[0], lin.n
+    n = lin.n
     slack = np.zeros((m, n))
     if rows.size == 0:
         return slack
     q32 = np.float32(qmax)
-    dq = np.zeros((rows.size, h64.shape[1]))
-    ds = np.zeros(rows.size)
-    qabs = np.abs(q0[rows].astype(np.float64))
+    dq = np.zeros((m * nb, g))
+    ds = np.zeros(m * nb)
     for corner_amax in (amax_lo[rows], amax_hi[rows]):
         am = corner_amax.astype(np.float32)
         zero = am == 0
         safe = np.where(zero, np.float32(1), am)
         inv = np.where(zero, np.float32(0), (q32 / safe).astype(np.float32))
         sc = np.where(zero, np.float32(0), (safe / q32).astype(np.float32))
-        ds = np.maximum(ds, np.abs(sc.astype(np.float64) - s0[rows].astype(np.float64)))
+        ds[rows] = np.maximum(ds[rows], np.abs(sc.astype(np.float64) - s0[rows].astype(np.float64)))
         for hv in (lo[rows], hi[rows]):
             qc = np.clip(np.rint((hv.astype(np.float32) * inv[:, None]).astype(np.float32)),
                          -qmax, qmax)
             qc = np.where(zero[:, None], 0, qc)
-            dq = np.maximum(dq, np.abs(qc - q0[rows]))
-    s_max = np.maximum(s0[rows].astype(np.float64), s0[rows].astype(np.float64) + ds)
+            dq[rows] = np.maximum(dq[rows], np.abs(qc - q0[rows]))
+    s_max = np.maximum(s0.astype(np.float64), s0.astype(np.float64) + ds)
+    qabs = np.abs(q0.astype(np.float64))
+    DQ = (dq * s_max[:, None]).reshape(m, F)
+    QD = ((qabs + dq) * ds[:, None]).reshape(m, F)
     wabs = np.abs(dequant(lin, act))
-    slack[rows] = (dq * s_max[:, None]) @ wabs.T + ds[:, None] * ((qabs + dq) @ wabs.T)
-    return slack
+    return (DQ + QD) @ wabs.T
 
 
 def _expert_mlp(a: np.ndarray, lins: Sequence, act: str, want_slack: bool):
@@ -398,7 +435,8 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   configuration S (m <= 16): 16 rows x (gate|up 256, down 512) channels
 #   configuration T (m <= 32): 32 rows x (gate|up 256, down 512) channels
 #   configuration M (m <= 64): 64 rows x (gate|up 128, down 256) channels
-#   configuration L (m > 64) : 128 rows x (gate|up 128, down 256) channels
+#   configuration L (m > 64) : 128 rows x (gate|up 128, down 256) channels,
+#   except w4a4-g128 groups, which stay at configuration M
 #   cost of a tile (ps) = min(max(bytes * 32, flops * 1000 / rate) + 2e6, 2e9),
 #   truncated to an integer, with bytes = wbytes / mt + abytes / nt (the group's
 #   mt row tiles share a weight tile, its nt channel tiles an activation tile),
@@ -468,6 +506,8 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int
     for m, lin in zip(ms, lins):
         m = int(m)  # Python integers: the sums below exceed 32 bits
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
+        if cfg == 3 and lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
+            cfg = 2   # w4a4-g128 groups stop at 64-row tiles
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-int(lin.n) // bn)

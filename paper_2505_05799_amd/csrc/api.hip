@@ -14,6 +14,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // scheme -> micro-kernel kind, -1 if unsupported
 int scheme_kind(const mxmoe_scheme& s) {
+  if (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 128 && s.a_group == 128 && s.symmetric == 1) return K_W4A4G;
   if (s.a_group != -1) return -1;
   if (s.w_bits == 16 && s.a_bits == 16 && s.w_group == -1 && s.symmetric == 0) return K_W16;
   if (s.a_bits == 8 && s.w_bits == 8 && s.w_group == -1 && s.symmetric == 1) return K_W8A8;
@@ -49,7 +50,7 @@ mxmoe_status check_linear(const mxmoe_linear* L, int* kind) {
 
 size_t packed_bytes_kind(int kd, int n, int k) {
   size_t b = (size_t)codes_bytes(kd, n, k);
-  if (kind_is_int(kd)) b += 4 * (size_t)n;
+  if (kind_is_int(kd) && kd != K_W4A4G) b += 4 * (size_t)n;  // per-channel fp32 scales
   return b;
 }
 
@@ -59,6 +60,7 @@ struct BlockInfo {
   int H, F, E, k, nsh, Fsh, act, G;
   bool any_x8 = false, any_x4 = false, any_hq = false, any_hq_sh = false;
   bool rs_x = false, rs_h = false, rs_hsh = false;  // row sums of x / h / h_shared needed (bf16)
+  bool any_x4g = false, any_hg = false, any_hg_sh = false;  // w4a4-g128 gate|up, routed / shared down
   int kinds[kMaxG][3];
 };
 
@@ -92,6 +94,8 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
     const int kg = bi->kinds[g][0];
     if (kg == K_W8A8) bi->any_x8 = true;
     if (kg == K_W4A4) bi->any_x4 = true;
+    if (kg == K_W4A4G) bi->any_x4g = true;
+    if (bi->kinds[g][2] == K_W4A4G) (sh ? bi->any_hg_sh : bi->any_hg) = true;
     if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(kg)) bi->rs_x = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(bi->kinds[g][2])) (sh ? bi->rs_hsh : bi->rs_h) = true;
@@ -141,6 +145,10 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.rsx = bi.rs_x ? take(4 * (size_t)T * (bi.H / 128)) : kNone;
   L.rsh = bi.rs_h ? take(4 * P * (bi.F / 128)) : kNone;
   L.rsh_shared = bi.rs_hsh ? take(4 * (size_t)bi.nsh * T * (bi.Fsh / 128)) : kNone;
+  L.xq4g = bi.any_x4g ? take((size_t)T * bi.H) : kNone;
+  L.xs4g = bi.any_x4g ? take(4 * (size_t)T * (bi.H / 128)) : kNone;
+  L.hsg = bi.any_hg ? take(4 * P * (bi.F / 128)) : kNone;
+  L.hsg_shared = bi.any_hg_sh ? take(4 * (size_t)bi.nsh * T * (bi.Fsh / 128)) : kNone;
   L.total = o;
   return L;
 }
@@ -250,7 +258,7 @@ LinWs lin_layout(int kd, int m, int n, int k) {
   w.aq = w.as = w.rsa = kNone;
   if (kind_is_int(kd)) {
     w.aq = o; o = align256(o + (size_t)m * k);
-    w.as = o; o = align256(o + 4 * (size_t)m);
+    w.as = o; o = align256(o + 4 * (size_t)m * (kd == K_W4A4G ? k / 128 : 1));
   }
   // row sums of the input per 128-wide k block (used with bf16 activations)
   if (kind_is_magic(kd)) { w.rsa = o; o = align256(o + 4 * (size_t)m * (k / 128)); }
@@ -280,7 +288,8 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   if (workspace_bytes < w.total) return MXMOE_ERR_WORKSPACE;
   DevLinear dl;
   dl.packed = reinterpret_cast<const uint8_t*>(packed);
-  dl.wscale = kind_is_int(kd) ? reinterpret_cast<const float*>(dl.packed + codes_bytes(kd, L->n, L->k)) : nullptr;
+  dl.wscale = (kind_is_int(kd) && kd != K_W4A4G)
+                  ? reinterpret_cast<const float*>(dl.packed + codes_bytes(kd, L->n, L->k)) : nullptr;
   dl.n = L->n;
   dl.k = L->k;
   dl.kind = kd;
@@ -302,9 +311,12 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   if (kind_is_int(kd)) {
     int8_t* aq = at<int8_t>(workspace, w.aq);
     float* as = at<float>(workspace, w.as);
-    hipError_t e = launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
+    hipError_t e = kd == K_W4A4G ? launch_act_quant_g128(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream)
+                                 : launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
     if (e != hipSuccess) return MXMOE_ERR_HIP;
-    if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; } else { ga.xq4 = aq; ga.xs4 = as; }
+    if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; }
+    else if (kd == K_W4A4G) { ga.xq4g = aq; ga.xs4g = as; }
+    else { ga.xq4 = aq; ga.xs4 = as; }
   }
   if (act == MXMOE_BF16 && kind_is_magic(kd)) {
     float* rs = at<float>(workspace, w.rsa);
@@ -343,7 +355,8 @@ mxmoe_status mxmoe_block_table_fill(const mxmoe_block* B, void* host_buf, size_t
       d.n = j < 2 ? F : bi.H;
       d.k = j < 2 ? bi.H : F;
       d.packed = reinterpret_cast<const uint8_t*>(p);
-      d.wscale = kind_is_int(d.kind) ? reinterpret_cast<const float*>(d.packed + codes_bytes(d.kind, d.n, d.k))
+      d.wscale = (kind_is_int(d.kind) && d.kind != K_W4A4G)
+                     ? reinterpret_cast<const float*>(d.packed + codes_bytes(d.kind, d.n, d.k))
                                      : nullptr;
       d.pad = 0;
     }
@@ -388,6 +401,10 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->rsx = L.rsx;
   out->rsh = L.rsh;
   out->rsh_shared = L.rsh_shared;
+  out->xq4g = L.xq4g;
+  out->xs4g = L.xs4g;
+  out->hsg = L.hsg;
+  out->hsg_shared = L.hsg_shared;
   return MXMOE_OK;
 }
 
@@ -450,6 +467,9 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4), at<float>(workspace, L.xs4),
                               stream));
   if (bi.rs_x) MX_CHECK(launch_rowsum(x, T, bi.H, bi.H, at<float>(workspace, L.rsx), stream));
+  if (bi.any_x4g)
+    MX_CHECK(launch_act_quant_g128(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4g),
+                                   at<float>(workspace, L.xs4g), stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, topk_w, at<float>(workspace, L.xs8),
                            at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
                            at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
@@ -489,6 +509,10 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.rxs4 = at<float>(workspace, L.rxs4);
   ga.partial = at<float>(workspace, L.partial);
   ga.rsx = at<float>(workspace, L.rsx);
+  ga.xq4g = at<int8_t>(workspace, L.xq4g);
+  ga.xs4g = at<float>(workspace, L.xs4g);
+  ga.hsg = at<float>(workspace, L.hsg);
+  ga.hsg_shared = at<float>(workspace, L.hsg_shared);
   ga.rsh = at<float>(workspace, L.rsh);
   ga.rsh_shared = at<float>(workspace, L.rsh_shared);
   MX_EVENT(1);
@@ -498,14 +522,19 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   MX_EVENT(4);
   if (bi.any_hq)
     MX_CHECK(launch_hquant_routed(ga.h, bi.act, T * bi.k, bi.F, offsets, bi.E, down_qmax, at<int8_t>(workspace, L.hq),
-                                  at<float>(workspace, L.hs), stream));
+                                  at<float>(workspace, L.hs), at<float>(workspace, L.hsg), stream));
   for (int j = 0; j < bi.nsh; ++j) {
     const int qm = kind_qmax(bi.kinds[bi.E + j][2]);
     if (!qm) continue;
     const size_t rows = (size_t)j * T;
-    MX_CHECK(launch_act_quant(reinterpret_cast<const uint8_t*>(ga.h_shared) + rows * bi.Fsh * 2, bi.act, T, bi.Fsh,
-                              bi.Fsh, qm, at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh,
-                              at<float>(workspace, L.hs_shared) + rows, stream));
+    const void* hsrc = reinterpret_cast<const uint8_t*>(ga.h_shared) + rows * bi.Fsh * 2;
+    int8_t* hq = at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh;
+    if (bi.kinds[bi.E + j][2] == K_W4A4G)
+      MX_CHECK(launch_act_quant_g128(hsrc, bi.act, T, bi.Fsh, bi.Fsh, qm, hq,
+                                     at<float>(workspace, L.hsg_shared) + rows * (bi.Fsh / 128), stream));
+    else
+      MX_CHECK(launch_act_quant(hsrc, bi.act, T, bi.Fsh, bi.Fsh, qm, hq, at<float>(workspace, L.hs_shared) + rows,
+                                stream));
   }
   MX_EVENT(5);
   MX_EVENT(6);

@@ -168,6 +168,40 @@ __device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, in
   if (idx == 0) *scale = s;
 }
 
+// Quantizes one row per block of 128 elements (w4a4-g128 activations), one
+// wavefront: a block is 16 chunks of 8, one per lane of a 16-lane group, whose
+// maximum the group shares; the fp32 recipe of quant_row per block.
+__device__ inline void quant_row_groups(const uint4* __restrict__ row, int cols, int act, int qmax,
+                                        uint2* __restrict__ codes, float* __restrict__ scales) {
+  const int lane = threadIdx.x & 63, nch = cols >> 3;
+  const uint32_t nan_lo = act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;
+  const float q = (float)qmax;
+  for (int c0 = 0; c0 < nch; c0 += 64) {  // nch is a multiple of 16: groups stay whole
+    const int c = c0 + lane;
+    const bool ok = c < nch;
+    const uint4 v = ok ? row[c] : make_uint4(0u, 0u, 0u, 0u);
+    uint32_t mb = amax8_bits(v, nan_lo);
+    for (int d = 1; d < 16; d <<= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, d, 64));
+    const float amax = bits_to_f32(mb, act);
+    float inv = 0.f, sc = 0.f;
+    if (amax > 0.f) {
+      inv = __fdiv_rn(q, amax);
+      sc = __fdiv_rn(amax, q);
+    }
+    if (ok) codes[c] = codes8(v, act, inv, q);
+    if (ok && (lane & 15) == 0) scales[c >> 4] = sc;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) act_quant_g128_kernel(const void* a, int act, int rows, int cols,
+                                                                  int64_t ld, int qmax, int8_t* codes,
+                                                                  float* scales) {
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  quant_row_groups(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a) + r * ld), cols, act, qmax,
+                   reinterpret_cast<uint2*>(codes + r * cols), scales + r * (cols >> 7));
+}
+
 // row handled by this thread: W == 1 one per wavefront, W == 4 one per workgroup
 template <int W> __device__ inline int64_t my_row() {
   return W == 1 ? (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6) : (int64_t)blockIdx.x;
@@ -190,7 +224,7 @@ template <int NC, int W>
 __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, int act, int P, int F,
                                                                  const int32_t* __restrict__ offsets, int E,
                                                                  const int32_t* __restrict__ down_qmax,
-                                                                 int8_t* hq, float* hs) {
+                                                                 int8_t* hq, float* hs, float* hsg) {
   __shared__ int32_t s_off[kMaxE + 1];
   __shared__ uint32_t red[kThreads / 64];
   for (int i = threadIdx.x; i <= E; i += kThreads) s_off[i] = offsets[i];
@@ -202,8 +236,15 @@ __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, 
     const int mid = (lo + hi) >> 1;
     if (s_off[mid] <= r) lo = mid; else hi = mid;
   }
-  const int qmax = down_qmax[lo];
-  if (qmax == 0) return;
+  const int qm = down_qmax[lo];
+  if (qm == 0) return;
+  if (qm & kDownQGroup) {  // per-128-group scales: one wavefront per row
+    if (W == 1 || threadIdx.x < 64)
+      quant_row_groups(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F, act,
+                       qm & 0xFF, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hsg + (int64_t)r * (F >> 7));
+    return;
+  }
+  const int qmax = qm;
   quant_row_vec<NC, W>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F,
                        act, qmax, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hs + r, red);
 }
@@ -354,12 +395,23 @@ hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t 
   return launch_rows<ActQuantK>(rows, cols, s, a, act, rows, cols, ld, qmax, codes, scales);
 }
 
+hipError_t launch_act_quant_g128(const void* a, int act, int rows, int cols, int64_t ld, int qmax, int8_t* codes,
+                                 float* scales, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15) || (reinterpret_cast<uintptr_t>(codes) & 7) || cols % 128 || ld % 8)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(act_quant_g128_kernel, dim3((rows + kRowsPerBlock - 1) / kRowsPerBlock), dim3(kThreads), 0, s, a,
+                     act, rows, cols, ld, qmax, codes, scales);
+  return hipGetLastError();
+}
+
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets, int E,
-                                const int32_t* down_qmax, int8_t* hq, float* hs, hipStream_t s) {
+                                const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg, hipStream_t s) {
   if (P <= 0) return hipSuccess;
   if ((reinterpret_cast<uintptr_t>(h) & 15) || (reinterpret_cast<uintptr_t>(hq) & 7) || F % 8 || E > kMaxE)
     return hipErrorInvalidValue;
-  return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs);
+  if (F % 128) return hipErrorInvalidValue;
+  return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs, hsg);
 }
 
 hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int nsh, int H, int act,

@@ -75,8 +75,11 @@ __host__ __device__ constexpr int cfg_nf(int c, int phase) {
 }
 __host__ __device__ constexpr int cfg_bm(int c) { return 16 * cfg_mf(c); }
 __host__ __device__ constexpr int cfg_bn(int c, int phase) { return 64 * cfg_nf(c, phase); }
-__host__ __device__ inline int pick_cfg(int m) {
-  return m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
+// Tile configuration of a group from its rows; w4a4-g128 groups stop at 64-row
+// tiles (their per-group rescale keeps a partial sum next to every accumulator).
+__host__ __device__ inline int pick_cfg(int m, int kind) {
+  const int c = m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
+  return (kind == K_W4A4G && c == CFG_L) ? CFG_M : c;
 }
 
 // Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
@@ -295,17 +298,6 @@ template <int KD> __device__ inline i32x4 wfrag8(const Raw<KD>& r, u32x4 step, i
   }
 }
 
-// Sum over each 16-lane row of the wavefront, left in every lane, through DPP
-// lane moves inside the row (neighbour swap, pair swap, half-row mirror, row
-// mirror).
-__device__ inline float row16_sum(float t) {
-  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0xB1, 0xf, 0xf, false));
-  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x4E, 0xf, 0xf, false));
-  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x141, 0xf, 0xf, false));
-  t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x140, 0xf, 0xf, false));
-  return t;
-}
-
 // ------------------------------------------------------------- LDS stage
 struct __align__(16) Smem {
   uint8_t act[2][STAGE_BYTES];   // activation rows of the tile, one 128-wide k block per stage
@@ -318,7 +310,6 @@ struct __align__(16) Smem {
   int32_t qtotal[kXcd];          // tiles per XCD queue
   int32_t qi;                    // queues tried so far by this workgroup
   int32_t last;                  // split-K: this workgroup finishes the output tile
-  float hrs[4 * BM_MAX];         // gate|up epilogue: h row sums of each wavefront's channels
 };
 
 // Tile queues of one phase, rebuilt from the kernel arguments where needed so
@@ -462,6 +453,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr bool WONLY = kind_is_wonly(KD);
   constexpr bool MAGIC = WONLY && KD != K_W8G;          // 2/3/4-bit codes
   constexpr bool RSUM = MAGIC && ACT == MXMOE_BF16;     // bias removed through row sums
+  constexpr bool GSC = KD == K_W4A4G;                   // per-128-group activation and weight scales
+  constexpr bool GMETA = kind_has_gmeta(KD);            // group metadata after each fragment block
+  constexpr bool RSLOAD = RSUM || GSC;                  // a per-row value per k block rides with the stage
   constexpr int BM = 16 * MF;
   constexpr int BN = 64 * NF;
   constexpr int LB = lane_bytes(KD);
@@ -499,7 +493,10 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   if constexpr (INT) {
     const int8_t* qb;
     if constexpr (PHASE == 1) { qb = shared ? a.hq_shared : a.hq; ascale = shared ? a.hs_shared : a.hs; }
-    else { qb = KD == K_W8A8 ? a.xq8 : a.xq4; ascale = KD == K_W8A8 ? a.xs8 : a.xs4; }
+    else {
+      qb = KD == K_W8A8 ? a.xq8 : (GSC ? a.xq4g : a.xq4);
+      ascale = KD == K_W8A8 ? a.xs8 : a.xs4;
+    }
     abase = reinterpret_cast<const uint8_t*>(qb);
   } else {
     abase = reinterpret_cast<const uint8_t*>(PHASE == 1 ? (shared ? a.h_shared : a.h) : a.x);
@@ -516,7 +513,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     if constexpr (PHASE == 0) {
       src = shared ? m : a.rtok[off_e + m];
       out = shared ? (g - a.E_routed) * a.T + m : off_e + m;
-      if constexpr (INT) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
+      if constexpr (INT && !GSC) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
     } else if constexpr (PHASE == 1) {
       src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
       if (shared) {
@@ -525,11 +522,11 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         out = a.rslot[off_e + m];
         gw = a.rgw[off_e + m];
       }
-      if constexpr (INT) sc = ascale[src];
+      if constexpr (INT && !GSC) sc = ascale[src];
     } else {
       src = m;
       out = m;
-      if constexpr (INT) sc = ascale[m];
+      if constexpr (INT && !GSC) sc = ascale[m];
     }
     sm.rowsrc[tid] = src;
     sm.rowout[tid] = m0 < m_g ? out : -1;
@@ -544,14 +541,16 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // kinds, bf16): x rows in the gate|up phase, h rows in the down phase
   const float* rsbase = nullptr;
   uint32_t rsoff = 0;
-  if constexpr (RSUM) {
-    rsbase = PHASE == 1 ? (shared ? a.rsh_shared : a.rsh) : a.rsx;
+  if constexpr (RSLOAD) {
+    // row sums (bias-dequantized kinds) or activation group scales (w4a4-g128)
+    if constexpr (GSC) rsbase = PHASE == 1 ? (shared ? a.hsg_shared : a.hsg) : a.xs4g;
+    else rsbase = PHASE == 1 ? (shared ? a.rsh_shared : a.rsh) : a.rsx;
     const int r = wave * 64 + lane;
     rsoff = (uint32_t)sm.rowsrc[r < BM ? r : 0] * (uint32_t)kblocks * 4u;
   }
 
   // ---- accumulators and weight streams
-  typedef typename std::conditional<INT, i32x4, f32x4>::type AccT;
+  typedef typename std::conditional<INT && !GSC, i32x4, f32x4>::type AccT;
   typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
   constexpr int J = INT ? 2 : 4;                 // MFMA steps per 128-wide k block
   constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
@@ -590,7 +589,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       for (int nf = 0; nf < NF; ++nf) {
         const uint8_t* blk = wp[l][nf] + (last ? 0 : (int64_t)kn * BB);  // uniform
         if constexpr (!streamed<KD>()) load_raw<KD>(raw[l][nf], blk + lo);
-        if constexpr (WONLY) meta[l][nf] = gload<uint32_t>(blk + mo);
+        if constexpr (GMETA) meta[l][nf] = gload<uint32_t>(blk + mo);
       }
   };
   auto load_steps = [&](int kn, bool last, int j) {
@@ -607,10 +606,10 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // prefetch; two 16-byte loads for w8a8), plus one metadata dword per fragment
   // (weight-only).  Waiting for
   // this many leaves the weight prefetch in flight across the barrier.
-  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (WONLY ? NL * NF : 0);
+  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (GMETA ? NL * NF : 0);
 
   stage_load<INT, BM>(sm, 0, abase, soffs, kb0, wave);
-  if constexpr (RSUM) rowsum_load<BM>(sm, 0, rsbase, rsoff, kb0, wave);
+  if constexpr (RSLOAD) rowsum_load<BM>(sm, 0, rsbase, rsoff, kb0, wave);
   load_group(kb0, false);
   if constexpr (streamed<KD>()) {
 #pragma unroll
@@ -623,7 +622,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const int cur = (kb - kb0) & 1;
     const bool more = kb + 1 < kb1;
     if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
-    if constexpr (RSUM) {
+    if constexpr (RSLOAD) {
       if (more) rowsum_load<BM>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
     }
     // every weight load below is issued after the stage (see wait_vmem)
@@ -632,13 +631,17 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     Raw<KD> rw[NL][NF];
     uint32_t bz[NL][NF];
     float zf[NL][NF];
+    float wsc[NL][NF];  // w4a4-g128: the channel's weight scale of this group / 16
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
-        rw[l][nf] = raw[l][nf];
+        if constexpr (!GSC) rw[l][nf] = raw[l][nf];
         bz[l][nf] = 0;
         zf[l][nf] = 0.f;
+        wsc[l][nf] = 0.f;
+        if constexpr (GSC)  // (the 1/16 undoes the x16 of the widened nibbles, exactly)
+          wsc[l][nf] = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu)) * 0.0625f;
         if constexpr (WONLY) {
           const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu));
           const float z = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] >> 16));
@@ -659,11 +662,47 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           }
         }
       }
+    // w4a4-g128 decodes the whole k block's weight fragments here, before the
+    // prefetch reuses their registers
+    OpT gwf[GSC ? J : 1][NL][NF];
+    if constexpr (GSC) {
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) gwf[j][l][nf] = wfrag8<KD>(raw[l][nf], u32x4{0u, 0u, 0u, 0u}, j);
+    }
     load_group(kb + 1, !more);
     // keep the prefetch here: the scheduler would otherwise sink it below the
     // MFMAs, next to its first use
     __builtin_amdgcn_sched_barrier(0);
 
+    if constexpr (GSC) {
+      // w4a4-g128: per row fragment, the two MFMA steps of this k block give an
+      // exact int32 block sum, which enters the fp32 accumulator scaled by the
+      // row's activation scale and the channel's weight scale of the block
+      auto& wf = gwf;
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        OpT af[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j)
+          af[j] = __builtin_bit_cast(OpT, act_frag<true>(sm, cur, mf * 16 + li, 4 * j + q));
+        const f32x4 sa = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][mf * 16 + 4 * q]);
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            i32x4 p = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[0], wf[0][l][nf], i32x4{0, 0, 0, 0}, 0, 0, 0);
+#pragma unroll
+            for (int j = 1; j < J; ++j) p = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[j], wf[j][l][nf], p, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              acc[l][nf][mf][i] = __builtin_fmaf((float)p[i], sa[i] * wsc[l][nf], acc[l][nf][mf][i]);
+          }
+      }
+    } else {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       auto wop = [&](int l, int nf) -> OpT {
@@ -721,6 +760,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         load_steps(kb + 1, !more, j);
         __builtin_amdgcn_sched_barrier(0);
       }
+    }
     }
     // Last k block: claim the next tile and bring its entry into LDS (the
     // entry is read at the top of the tile loop, after the final barrier).
@@ -813,7 +853,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
         cs[l][nf] = 1.f;
-        if constexpr (INT) cs[l][nf] = nf < nvalid ? lins[l]->wscale[16 * (nb0 + nf) + li] : 0.f;
+        if constexpr (INT && !GSC) cs[l][nf] = nf < nvalid ? lins[l]->wscale[16 * (nb0 + nf) + li] : 0.f;
         if constexpr (WONLY) cs[l][nf] = s_prev[l][nf];
       }
 #pragma unroll
@@ -832,7 +872,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int l = 0; l < NL; ++l)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            if constexpr (INT) {
+            if constexpr (INT && !GSC) {
               int iv = acc[l][nf][mf][i];
               if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
               v[l][i] = ((float)iv * rs[i]) * cs[l][nf];
@@ -853,7 +893,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             a.slots[orow] = v[0][i] * gwv[i];
           } else {
             if (GUARD && ro[i] < 0) continue;
-            if constexpr (INT) {
+            if constexpr (INT && !GSC) {
               int iv = acc[0][nf][mf][i];
               if constexpr (KD == K_W4A4) iv >>= 4;
               reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
@@ -864,25 +904,26 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         }
       }
       if constexpr (PHASE == 0) {
-        if (rsh_out) {  // this wavefront's channels: sum over the 16 lanes of a row group
+        if (rsh_out) {  // each lane's partial row sums go to LDS (the stages are idle here)
+          float* part = reinterpret_cast<float*>(sm.act[0]);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float t = row16_sum(hsum[i]);
-            if (li == 0) sm.hrs[wave * BM + r + i] = t;
-          }
+          for (int i = 0; i < 4; ++i) part[(wave * BM + r + i) * 16 + li] = hsum[i];
         }
       }
     }
     if constexpr (PHASE == 0) {
-      if (rsh_out) {  // the wavefronts of one 128-wide block add their sums
+      if (rsh_out) {  // the lanes and wavefronts of one 128-wide block add their sums
         lds_barrier();
         constexpr int KBT = BN / 128, WPK = 4 / KBT;
         if (tid < BM * KBT) {
           const int r = tid % BM, j = tid / BM;
           const int kbg = nt * KBT + j, nkb = N / 128;
+          const float* part = reinterpret_cast<const float*>(sm.act[0]);
           float t = 0.f;
 #pragma unroll
-          for (int w = 0; w < WPK; ++w) t += sm.hrs[(j * WPK + w) * BM + r];
+          for (int w = 0; w < WPK; ++w)
+#pragma unroll
+            for (int c = 0; c < 16; ++c) t += part[((j * WPK + w) * BM + r) * 16 + c];
           const int ro = sm.rowout[r];
           if (ro >= 0 && kbg < nkb) rsh_out[(int64_t)ro * nkb + kbg] = t;
         }
@@ -907,6 +948,9 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
     case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W4A4G:  // never planned in 128-row tiles
+      if constexpr (CFG != CFG_L) run_tile<K_W4A4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
+      break;
     default: break;
   }
 }

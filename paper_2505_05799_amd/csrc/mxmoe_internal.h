@@ -22,16 +22,23 @@ enum Kind : int32_t {
   K_W3G = 4,   // weight-only 3-bit (2+1 bit planes), group 128
   K_W4G = 5,   // weight-only 4-bit, group 128
   K_W8G = 6,   // weight-only 8-bit, group 128
-  K_COUNT = 7
+  K_W4A4G = 7, // int4 weights and activations with per-128-group scales (w4a4-g128)
+  K_COUNT = 8
 };
 
-__host__ __device__ constexpr inline bool kind_is_int(int kd) { return kd == K_W8A8 || kd == K_W4A4; }
-__host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G; }
+__host__ __device__ constexpr inline bool kind_is_int(int kd) {
+  return kd == K_W8A8 || kd == K_W4A4 || kd == K_W4A4G;
+}
+__host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G && kd <= K_W8G; }
+// kinds whose scales come per 128-wide group along K (a 64-byte metadata tail
+// per fragment block): the weight-only kinds and w4a4-g128
+__host__ __device__ constexpr inline bool kind_has_gmeta(int kd) { return kind_is_wonly(kd) || kd == K_W4A4G; }
 __host__ __device__ constexpr inline int kind_wbits(int kd) {
   switch (kd) {
     case K_W16: return 16;
     case K_W8A8: return 8;
     case K_W4A4: return 4;
+    case K_W4A4G: return 4;
     case K_W2G: return 2;
     case K_W3G: return 3;
     case K_W4G: return 4;
@@ -43,20 +50,22 @@ __host__ __device__ constexpr inline int kind_wbits(int kd) {
 // the activations is removed through activation row sums (16-bit bf16 path)
 __host__ __device__ constexpr inline bool kind_is_magic(int kd) { return kd == K_W2G || kd == K_W3G || kd == K_W4G; }
 __host__ __device__ constexpr inline int kind_qmax(int kd) {
-  return kd == K_W8A8 ? 127 : (kd == K_W4A4 ? 7 : 0);
+  return kd == K_W8A8 ? 127 : ((kd == K_W4A4 || kd == K_W4A4G) ? 7 : 0);
 }
 
 // Packed layout: the weight matrix [n, k] is cut into fragment blocks of
 // 16 output rows x 128 reduction columns, stored n-block major, k-block minor.
 // A block holds 64 lanes x lane_bytes(kind) bytes in MFMA lane order (lane l
-// owns output row l%16 and reduction quarter l/16); weight-only blocks are
-// followed by 16 (scale, zero) fp16 pairs, one per output row of the block.
-// Per-channel fp32 scales of w8a8/w4a4 follow the last block.
+// owns output row l%16 and reduction quarter l/16); blocks of the group-scaled
+// kinds are followed by 16 (scale, zero) fp16 pairs, one per output row of the
+// block (zero 0 for w4a4-g128).  Per-channel fp32 scales of w8a8/w4a4 follow
+// the last block.
 __host__ __device__ constexpr inline int lane_bytes(int kd) {
   switch (kd) {
     case K_W16: return 64;
     case K_W8A8: return 32;
     case K_W4A4: return 16;
+    case K_W4A4G: return 16;
     case K_W2G: return 8;
     case K_W3G: return 12;
     case K_W4G: return 16;
@@ -64,7 +73,7 @@ __host__ __device__ constexpr inline int lane_bytes(int kd) {
   }
 }
 __host__ __device__ constexpr inline int block_bytes(int kd) {
-  return 64 * lane_bytes(kd) + (kind_is_wonly(kd) ? 64 : 0);
+  return 64 * lane_bytes(kd) + (kind_has_gmeta(kd) ? 64 : 0);
 }
 __host__ __device__ inline int64_t codes_bytes(int kd, int n, int k) {
   return (int64_t)(n / 16) * (k / 128) * block_bytes(kd);
@@ -223,6 +232,7 @@ struct WsLayout {
   size_t xq8, xs8, xq4, xs4, h, h_shared, hq, hs, hq_shared, hs_shared, slots, total;
   size_t partial;  // fp32 split-K partial sums (both phases reuse it)
   size_t rsx, rsh, rsh_shared;  // fp32 row sums per 128-wide k block of x, h, h_shared
+  size_t xq4g, xs4g, hsg, hsg_shared;  // w4a4-g128 codes and group scales
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -245,6 +255,10 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
 // Row sums of each 128-wide block of bf16 rows: out[r][b] = sum of a[r][128b ..
 // 128b + 127] in fp32; cols a multiple of 128, rows 16-byte aligned.
 hipError_t launch_rowsum(const void* a, int rows, int cols, int64_t ld, float* out, hipStream_t s);
+// Per-(row, 128-wide block) quantization (w4a4-g128 activations): codes int8
+// [rows, cols], scales fp32 [rows][cols/128]; cols a multiple of 128.
+hipError_t launch_act_quant_g128(const void* a, int act, int rows, int cols, int64_t ld, int qmax, int8_t* codes,
+                                 float* scales, hipStream_t s);
 hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t ld, int qmax,
                             int8_t* codes, float* scales, hipStream_t s);
 
@@ -257,8 +271,12 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
 
 // Quantize routed h rows whose expert's down projection is a8/a4 (qmax from
 // down_qmax[expert]); rows of other experts are skipped.
+// Routed h rows of the experts whose down linear quantizes its activations:
+// down_qmax[e] = qmax | kDownQGroup for per-128-group scales (into hsg
+// [P][F/128]), else per-row scales (into hs); 0 = not quantized.
+constexpr int kDownQGroup = 0x100;
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets,
-                                int E, const int32_t* down_qmax, int8_t* hq, float* hs,
+                                int E, const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg,
                                 hipStream_t s);
 
 struct GemmArgs {
@@ -270,6 +288,10 @@ struct GemmArgs {
   const void* x;             // [T,H] act
   const int8_t* xq8; const float* xs8;
   const int8_t* xq4; const float* xs4;
+  // w4a4-g128: x codes [T,H] with scales [T][H/128]; group scales of h rows
+  // (routed [P][F/128], shared [n_shared*T][F_sh/128]; codes in hq / hq_shared)
+  const int8_t* xq4g; const float* xs4g;
+  const float* hsg; const float* hsg_shared;
   void* h; void* h_shared;
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;

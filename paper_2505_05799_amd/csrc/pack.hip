@@ -6,7 +6,7 @@
 // and the reduction quarter qd = l/16.  Its 32 values, in slot order
 // v = 0..31, are
 //   16-bit MFMA kinds (w16, wNg128): k = 128*kb + 32*(v/8) + 8*qd + v%8
-//   int8 MFMA kinds  (w8a8, w4a4):   k = 128*kb + 64*(v/16) + 16*qd + v%16
+//   int8 MFMA kinds  (w8a8, w4a4, w4a4-g128): k = 128*kb + 64*(v/16) + 16*qd + v%16
 // so that one 16x16x32 bf16/fp16 MFMA (or one 16x16x64 int8 MFMA) consumes
 // slots 8j..8j+7 (16j..16j+15) of every lane.  Slot encodings (j = v/8 is the
 // MFMA step, p = (v%8)/2 the 16-bit pair, h = v%2 the half of the pair):
@@ -17,13 +17,14 @@
 //   w3g  : low two bits as w2g; bit 2 of the slot in dword 2 at bit 16h + P'
 //          with P' = 4j + p
 //   w8a8 : 32 x int8 codes in slot order
-//   w4a4 : dword 2j+d holds slots 16j+8d..+7 as 4-bit two's complement
+//   w4a4 (and w4a4-g128): dword 2j+d holds slots 16j+8d..+7 as 4-bit two's complement
 //          nibbles; nibble 2i is slot i, nibble 2i+1 is slot 4+i (i < 4) so
 //          that (D << 4) & 0xF0F0F0F0 and D & 0xF0F0F0F0 are the int8 slots
 //          (times 16) in order.
 // Weight-only blocks end with 16 (scale, zero) fp16 pairs, one per channel.
 // A group whose scale is zero dequantizes to zero whatever its codes: it is
 // stored with scale 1 and every code equal to its zero point (same values).
+// w4a4-g128 blocks end with 16 (scale, 0) pairs; a zero scale stays zero.
 #include "mxmoe_internal.h"
 
 namespace mxmoe {
@@ -92,6 +93,8 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
     z16 = reinterpret_cast<const uint16_t*>(zeros)[g];
     zero_group = (s16 & 0x7FFFu) == 0;
     if (zero_group) s16 = 0x3C00u;  // 1.0
+  } else if (kd == K_W4A4G) {
+    s16 = reinterpret_cast<const uint16_t*>(scales)[(int64_t)row * kblocks + kb];
   }
   const uint32_t zcode = zero_group ? (uint32_t)(float)__builtin_bit_cast(_Float16, z16) : 0u;
   uint32_t w[16];
@@ -109,11 +112,11 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
   }
   uint32_t* o32 = reinterpret_cast<uint32_t*>(out);
   for (int i = 0; i < lane_bytes(kd) / 4; ++i) o32[i] = w[i];
-  if (kind_is_wonly(kd) && qd == 0) {
+  if (kind_has_gmeta(kd) && qd == 0) {
     const uint32_t sz = (uint32_t)s16 | ((uint32_t)z16 << 16);
     reinterpret_cast<uint32_t*>(packed + blk * block_bytes(kd) + 64 * lane_bytes(kd))[lane & 15] = sz;
   }
-  if (kind_is_int(kd) && kb == 0 && qd == 0) {
+  if (kind_is_int(kd) && kd != K_W4A4G && kb == 0 && qd == 0) {
     float* ws = reinterpret_cast<float*>(packed + codes_bytes(kd, n, k));
     ws[row] = reinterpret_cast<const float*>(scales)[row];
   }
@@ -140,16 +143,16 @@ __global__ void unpack_kernel(int kd, int n, int k, int act, const uint8_t* __re
     uint32_t c = (w[dw] >> bit) & mask;
     if (kd == K_W3G) c |= ((w[2] >> w3_hibit(v)) & 1u) << 2;
     if (kd == K_W16) reinterpret_cast<uint16_t*>(codes)[idx] = (uint16_t)c;
-    else if (kd == K_W4A4) codes[idx] = (uint8_t)(int8_t)((int32_t)(c << 28) >> 28);  // sign-extend
+    else if (kd == K_W4A4 || kd == K_W4A4G) codes[idx] = (uint8_t)(int8_t)((int32_t)(c << 28) >> 28);  // sign-extend
     else codes[idx] = (uint8_t)c;
   }
-  if (kind_is_wonly(kd) && qd == 0) {
+  if (kind_has_gmeta(kd) && qd == 0) {
     uint32_t sz = reinterpret_cast<const uint32_t*>(packed + blk * block_bytes(kd) + 64 * lane_bytes(kd))[lane & 15];
     int64_t g = (int64_t)row * kblocks + kb;
     reinterpret_cast<uint16_t*>(scales)[g] = (uint16_t)(sz & 0xFFFF);
-    reinterpret_cast<uint16_t*>(zeros)[g] = (uint16_t)(sz >> 16);
+    if (kind_is_wonly(kd)) reinterpret_cast<uint16_t*>(zeros)[g] = (uint16_t)(sz >> 16);
   }
-  if (kind_is_int(kd) && kb == 0 && qd == 0) {
+  if (kind_is_int(kd) && kd != K_W4A4G && kb == 0 && qd == 0) {
     const float* ws = reinterpret_cast<const float*>(packed + codes_bytes(kd, n, k));
     reinterpret_cast<float*>(scales)[row] = ws[row];
   }

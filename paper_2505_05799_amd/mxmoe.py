@@ -48,7 +48,8 @@ class ForwardOpts_t(C.Structure):
 
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
              "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total", "plan_queue_cap",
-             "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared"]
+             "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared", "xq4g", "xs4g", "hsg",
+             "hsg_shared"]
 
 
 class WsLayout_t(C.Structure):
@@ -206,6 +207,8 @@ class PackedLinear:
         if s.w_bits < 16 and s.a_bits == 16:
             scales = torch.empty((q.n, q.k // 128), dtype=torch.int16, device=self.buf.device)
             zeros = torch.empty_like(scales)
+        elif s.w_bits < 16 and s.w_group > 0:     # w4a4-g128: fp16 group scales
+            scales = torch.empty((q.n, q.k // 128), dtype=torch.int16, device=self.buf.device)
         elif s.w_bits < 16:
             scales = torch.empty(q.n, dtype=torch.float32, device=self.buf.device)
         _check(lib.mxmoe_unpack_weights(C.byref(self.L), act_code(self.act), _ptr(self.buf), _ptr(codes),
@@ -218,19 +221,21 @@ class PackedLinear:
         elif s.a_bits < 16:
             c = c.view(np.int8)
         sc = None if scales is None else scales.cpu().numpy()
-        if sc is not None and s.a_bits == 16:
+        if sc is not None and (s.a_bits == 16 or s.w_group > 0):
             sc = sc.view(np.float16)
         z = None if zeros is None else zeros.cpu().numpy().view(np.float16)
         return c, sc, z
 
 
 def linear_forward(pl: PackedLinear, a, stream=None):
-    """out = a W^T through the micro-kernels: int32 for w8a8/w4a4, else fp32."""
+    """out = a W^T through the micro-kernels: int32 for w8a8/w4a4 (per channel),
+    else fp32."""
     torch = _torch()
     lib = load_library()
     m = a.shape[0]
     s = pl.q.scheme
-    out = torch.empty((m, pl.q.n), dtype=torch.int32 if s.a_bits < 16 else torch.float32, device=a.device)
+    raw_int = s.a_bits < 16 and s.a_group < 0
+    out = torch.empty((m, pl.q.n), dtype=torch.int32 if raw_int else torch.float32, device=a.device)
     wsb = lib.mxmoe_linear_workspace_bytes(C.byref(pl.L), m)
     ws = empty_aligned(wsb, a.device)
     _check(lib.mxmoe_linear_forward(C.byref(pl.L), act_code(pl.act), _ptr(pl.buf), m, _ptr(a.contiguous()),

@@ -51,16 +51,17 @@ import numpy as np
 class Scheme:
     w_bits: int      # 16, 8, 4, 3, 2
     a_bits: int      # 16 = weight-only, 8 or 4 = weight-activation
-    w_group: int     # 128 for weight-only groups, -1 = per output channel
-    a_group: int     # -1 = per token
-    symmetric: int   # 1 for w8a8 / w4a4, 0 for wNg128 asym and 16-bit
+    w_group: int     # 128 for groups along K, -1 = per output channel
+    a_group: int     # 128 for groups along K, -1 = per token
+    symmetric: int   # 1 for w8a8 / w4a4 (per channel or g128), 0 for wNg128 asym and 16-bit
 
     @property
     def name(self) -> str:
         if self.w_bits == 16:
             return "w16"
         if self.a_bits < 16:
-            return f"w{self.w_bits}a{self.a_bits}"
+            g = f"g{self.w_group}" if self.w_group > 0 else ""
+            return f"w{self.w_bits}a{self.a_bits}{g}"
         return f"w{self.w_bits}g{self.w_group}"
 
     @property
@@ -73,6 +74,8 @@ class Scheme:
             return 16.0
         if self.weight_only:
             return self.w_bits + 32.0 / self.w_group   # fp16 scale + fp16 zero
+        if self.w_group > 0:
+            return self.w_bits + 16.0 / self.w_group   # fp16 scale per group
         return self.w_bits + 32.0 / k                 # one fp32 scale per row
 
 
@@ -83,7 +86,8 @@ W2G128 = Scheme(2, 16, 128, -1, 0)
 W3G128 = Scheme(3, 16, 128, -1, 0)
 W4G128 = Scheme(4, 16, 128, -1, 0)
 W8G128 = Scheme(8, 16, 128, -1, 0)
-ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128)
+W4A4G128 = Scheme(4, 4, 128, 128, 1)   # 4-bit weights and activations, per-128 group scales
+ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128)
 SCHEME_BY_NAME = {s.name: s for s in ALL_SCHEMES}
 
 LINEAR_NAMES = ("gate", "up", "down")
@@ -160,6 +164,21 @@ def _qwen15_mixed(e: int, rank: int):
     return (W3G128, W3G128, W3G128)
 
 
+# The W5A5 allocation the paper prints for layer 5 of Qwen1.5-MoE (appendix
+# table of per-linear schemes): one character per expert, experts 0..59 then
+# the shared expert.  g = w4a4 with 128-groups on both operands, c = w4a4 per
+# channel / per token, 8 = w8a8 per channel / per token.  Gate and up carry the
+# same scheme in every row of that table, so one string serves both.
+_W5A5_GATE_UP = "ggggcggcggggggcggggggg8gggggggggggggggggggggcgggggggggcccgcgc"
+_W5A5_DOWN = "g888gg8g88888gg88888g88g8g8g8gg8gg88888gg888g88g88gg8gggggg88"
+_W5A5_CODE = {"g": W4A4G128, "c": W4A4, "8": W8A8}
+
+
+def _qwen15_w5a5(e: int, rank: int):
+    gu = _W5A5_CODE[_W5A5_GATE_UP[e]]
+    return (gu, gu, _W5A5_CODE[_W5A5_DOWN[e]])
+
+
 def _qwen2_alloc(e: int, rank: int):
     return (W8A8, W8A8, W8A8) if rank <= 10 else (W4A4, W4A4, W4A4)
 
@@ -188,6 +207,11 @@ CONFIGS: Dict[str, BlockConfig] = {
         "qwen15_mixed", T=256, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
         act="bf16", zipf_s=1.5, alloc=_qwen15_mixed, shared_alloc=(W8A8, W8A8, W8A8),
         description="Qwen1.5-MoE-shaped decode batch, mixed w8a8/w4a4/w3g128 at equal avg bits"),
+    "qwen15_w5a5": BlockConfig(
+        "qwen15_w5a5", T=8192, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
+        act="bf16", zipf_s=1.5, alloc=_qwen15_w5a5, shared_alloc=_qwen15_w5a5(60, 0),
+        description="Qwen1.5-MoE-shaped compute-bound batch (8192 tokens) with the paper's "
+                    "printed W5A5 allocation for layer 5 (w4a4-g128 / w4a4 / w8a8 per linear)"),
     "qwen2": BlockConfig(
         "qwen2", T=16384, H=3584, F=2560, E=64, k=8, n_shared=1, F_shared=20480, act="bf16",
         zipf_s=1.0, alloc=_qwen2_alloc, shared_alloc=(W8A8, W8A8, W8A8),
@@ -269,6 +293,23 @@ def quantize_sym_per_channel(w: np.ndarray, bits: int):
     return q.astype(np.int8), s
 
 
+def quantize_sym_g128(w: np.ndarray, bits: int, group: int = 128):
+    """Symmetric RTN per (output channel, group of `group` along K) with an fp16
+    scale: s = fp16(amax / qmax), q = clamp(rne(w / s), -qmax, qmax); an all-zero
+    group (or one whose scale rounds to 0) gets s = 0 and zero codes.
+    Returns (codes int8 [n, k], scales fp16 [n, k/group])."""
+    n, k = w.shape
+    assert k % group == 0
+    qmax = (1 << (bits - 1)) - 1
+    wg = w.astype(np.float64).reshape(n, k // group, group)
+    s = (np.abs(wg).max(axis=2) / qmax).astype(np.float16)
+    s64 = s.astype(np.float64)
+    safe = np.where(s64 == 0, 1.0, s64)
+    q = np.clip(np.rint(wg / safe[..., None]), -qmax, qmax)
+    q = np.where(s64[..., None] == 0, 0, q)
+    return q.reshape(n, k).astype(np.int8), s
+
+
 @dataclass
 class QLinear:
     """One quantized linear, W is [n, k] = [out, in] (nn.Linear layout)."""
@@ -276,7 +317,7 @@ class QLinear:
     n: int
     k: int
     codes: np.ndarray                    # uint8 / int8 [n,k]; bf16 bits uint16 for w16
-    scales: Optional[np.ndarray] = None  # fp16 [n, k/128] | fp32 [n]
+    scales: Optional[np.ndarray] = None  # fp16 [n, k/128] (groups) | fp32 [n] (per channel)
     zeros: Optional[np.ndarray] = None   # fp16 [n, k/128]
 
     @property
@@ -285,6 +326,8 @@ class QLinear:
         if s.w_bits == 16:
             return 2 * self.n * self.k
         if s.weight_only:
+            return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
+        if s.w_group > 0:   # packed with the same 4-byte metadata slot per group
             return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
         return self.n * self.k * s.w_bits // 8 + 4 * self.n
 
@@ -296,6 +339,9 @@ def quantize_linear(w_bf16_f32: np.ndarray, scheme: Scheme) -> QLinear:
     if scheme.weight_only:
         c, s, z = quantize_g128_asym(w_bf16_f32, scheme.w_bits, scheme.w_group)
         return QLinear(scheme, n, k, c, s, z)
+    if scheme.w_group > 0:
+        c, s = quantize_sym_g128(w_bf16_f32, scheme.w_bits, scheme.w_group)
+        return QLinear(scheme, n, k, c, s)
     c, s = quantize_sym_per_channel(w_bf16_f32, scheme.w_bits)
     return QLinear(scheme, n, k, c, s)
 

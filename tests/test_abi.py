@@ -55,6 +55,8 @@ def test_packed_bytes_closed_form(lib, s):
         want = 2 * n * k
     elif s.a_bits == 16:
         want = n * k * s.w_bits // 8 + (n * k // 128) * 4      # N + 0.25 bits per weight
+    elif s.w_group > 0:
+        want = n * k * s.w_bits // 8 + (n * k // 128) * 4      # fp16 group scale in a 4-byte slot
     else:
         want = n * k * s.w_bits // 8 + 4 * n
     assert got == want == W.QLinear(s, n, k, None).nbytes_packed
@@ -69,7 +71,9 @@ def test_packed_bits_per_weight_paper_accounting(lib):
 
 @pytest.mark.parametrize("n,k,scheme", [(250, 512, W.W4G128), (256, 500, W.W8A8), (0, 128, W.W16),
                                         (16, 128, W.Scheme(5, 16, 128, -1, 0)),
-                                        (16, 128, W.Scheme(4, 4, 128, 128, 1)),
+                                        (16, 128, W.Scheme(4, 4, 128, -1, 1)),
+                                        (16, 128, W.Scheme(8, 8, 128, 128, 1)),
+                                        (16, 64, W.W4A4G128),
                                         (16, 128, W.Scheme(8, 8, -1, -1, 0))])
 def test_packed_bytes_rejects(lib, n, k, scheme):
     assert lib.mxmoe_packed_bytes(C.byref(_L(scheme, n, k)), M.BF16) == 0

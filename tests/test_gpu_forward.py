@@ -58,6 +58,11 @@ MIXES = [
     [(W.W8A8,) * 3] * 7,
     [(W.W4A4, W.W4A4, W.W16), (W.W16, W.W16, W.W4A4), (W.W3G128, W.W3G128, W.W8G128), (W.W4G128,) * 3,
      (W.W2G128,) * 3, (W.W8A8,) * 3, (W.W4A4,) * 3],
+    # w4a4-g128 beside every neighbour: row sums of h for a magic-dequant down
+    # behind a w4a4-g128 gate/up, group-quantized h for a w4a4-g128 down
+    [(W.W4A4G128,) * 3, (W.W4A4G128, W.W4A4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4G128),
+     (W.W4A4G128, W.W4A4G128, W.W8A8), (W.W16, W.W16, W.W4A4G128), (W.W3G128, W.W3G128, W.W4A4G128),
+     (W.W4A4G128, W.W4A4G128, W.W4A4)],
 ]
 
 

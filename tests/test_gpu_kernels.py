@@ -118,12 +118,28 @@ def _linear_case(scheme, act, m, n, k, seed):
     return q, a, out.cpu().numpy()
 
 
+def _check_group_linear(q, a, got, act):
+    """w4a4-g128: an fp32 running sum over the 128-blocks of exact block dots
+    times fp32 scale products; each block adds at most two fp32 roundings, so
+    with at most 2^4 blocks the error stays below 2^-20 of sum |a_hat| |w_hat|
+    on the dequantized operands."""
+    s = q.scheme
+    assert q.k // s.a_group <= 16
+    want = O.linear(a, q, act)
+    qa, sa = O.act_quant_groups(a.astype(np.float32), 2 ** (s.a_bits - 1) - 1, s.a_group)
+    ad = (qa.astype(np.float64).reshape(a.shape[0], -1, s.a_group) * sa.astype(np.float64)[..., None]).reshape(a.shape)
+    bound = 2.0 ** -20 * (np.abs(ad) @ np.abs(O.dequant(q, act)).T) + 1e-30
+    assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
+
+
 @pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
 @pytest.mark.parametrize("m", LIN_M)
 @pytest.mark.parametrize("n,k", LIN_SHAPES)
 def test_linear_bf16(scheme, m, n, k):
     q, a, got = _linear_case(scheme, "bf16", m, n, k, m * 7 + n)
-    if scheme.a_bits < 16:
+    if scheme.a_group > 0:
+        _check_group_linear(q, a, got, "bf16")
+    elif scheme.a_bits < 16:
         want = O.linear(a, q, "bf16", return_int=True)
         assert np.array_equal(got.astype(np.int64), want)
     else:
@@ -136,7 +152,9 @@ def test_linear_bf16(scheme, m, n, k):
 @pytest.mark.parametrize("m", [3, 33, 129])
 def test_linear_fp16(scheme, m):
     q, a, got = _linear_case(scheme, "fp16", m, 48, 256, m + 11)
-    if scheme.a_bits < 16:
+    if scheme.a_group > 0:
+        _check_group_linear(q, a, got, "fp16")
+    elif scheme.a_bits < 16:
         assert np.array_equal(got.astype(np.int64), O.linear(a, q, "fp16", return_int=True))
     else:
         want = O.linear(a, q, "fp16")

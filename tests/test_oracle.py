@@ -63,11 +63,23 @@ def py_weight(lin, act, n, c):
     if s.a_bits == 16:
         g = c // s.w_group
         return float(lin.scales[n, g]) * (int(lin.codes[n, c]) - float(lin.zeros[n, g]))
+    if s.w_group > 0:
+        return float(lin.scales[n, c // s.w_group]) * int(lin.codes[n, c])
     return float(lin.scales[n]) * int(lin.codes[n, c])
 
 
 def py_linear(a_row, lin, act):
     s = lin.scheme
+    if s.a_bits < 16 and s.a_group > 0:
+        # per 128-wide block: integer dot of the block's codes, times both block scales
+        g, qmax = s.a_group, (1 << (s.a_bits - 1)) - 1
+        out = [0.0] * lin.n
+        for b in range(lin.k // g):
+            qa, sa = py_act_quant(a_row[b * g:(b + 1) * g], qmax)
+            for n in range(lin.n):
+                acc = sum(qa[c] * int(lin.codes[n, b * g + c]) for c in range(g))
+                out[n] += acc * sa * float(lin.scales[n, b])
+        return out
     if s.a_bits < 16:
         qa, sa = py_act_quant(a_row, (1 << (s.a_bits - 1)) - 1)
         out = []
@@ -211,7 +223,7 @@ def test_route_bad_ids_dropped():
 # ---------------------------------------------------------------------------
 
 
-@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W8A8, W.W4A4])
+@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W8A8, W.W4A4, W.W4A4G128])
 def test_dequant_recovers_weights(scheme):
     w = W.draw_weight(11, 0, 0, 48, 384)
     lin = W.quantize_linear(w, scheme)
@@ -225,6 +237,15 @@ def test_dequant_recovers_weights(scheme):
         # clamped codes sit at the ends of the range: error bounded by one step
         assert np.all(err <= 1.0 * s + 1e-12)
         assert inner.mean() > 0.5 if scheme.w_bits > 2 else True
+    elif scheme.w_group > 0:
+        # symmetric groups with an fp16 scale: the scale rounding can push the
+        # group maximum just past qmax * s, where the clamp adds at most
+        # qmax * |s - amax/qmax| <= qmax * 2^-11 * s
+        qmax = (1 << (scheme.w_bits - 1)) - 1
+        s = np.repeat(lin.scales.astype(np.float64), scheme.w_group, axis=1)
+        assert np.all(np.abs(deq - w) <= (0.5 + qmax * 2.0 ** -11) * s * (1 + 1e-12))
+        groups = np.abs(lin.codes.astype(np.int64)).reshape(lin.n, -1, scheme.w_group).max(axis=2)
+        assert np.all(groups == qmax)
     else:
         s = lin.scales.astype(np.float64)[:, None]
         assert np.all(np.abs(deq - w) <= 0.5 * s * (1 + 1e-12))
@@ -288,14 +309,37 @@ def test_int_linear_doubling():
                           O.linear(a, lin, "bf16", return_int=True))
 
 
+def test_group_linear_blocks_add_up():
+    """w4a4-g128: the linear over K = 384 is the sum of three independent
+    w4a4-g128 linears over its 128-wide column blocks, each with its own slice
+    of codes and scales (a misplaced block index or scale column fails this)."""
+    lin = W.quantize_linear(W.draw_weight(8, 0, 1, 24, 384), W.W4A4G128)
+    a = O.act_values(W.f64_to_act(np.random.default_rng(6).standard_normal((7, 384)), "bf16"), "bf16")
+    whole = O.linear(a, lin, "bf16")
+    parts = sum(O.linear(a[:, b * 128:(b + 1) * 128],
+                         _lin(W.W4A4G128, lin.codes[:, b * 128:(b + 1) * 128], lin.scales[:, b:b + 1]), "bf16")
+                for b in range(3))
+    np.testing.assert_allclose(whole, parts, rtol=1e-13, atol=1e-15)
+    # one block: w4a4-g128 is w4a4 per token / per channel with the fp16 scale
+    one = _lin(W.W4A4G128, lin.codes[:, :128], lin.scales[:, :1])
+    pc = _lin(W.W4A4, lin.codes[:, :128], lin.scales[:, 0].astype(np.float32))
+    np.testing.assert_allclose(O.linear(a[:, :128], one, "bf16"), O.linear(a[:, :128], pc, "bf16"),
+                               rtol=1e-13, atol=1e-15)
+    # doubling the activations keeps every code and doubles every block scale
+    assert np.array_equal(O.linear(2 * a, lin, "bf16"), 2 * whole)
+
+
 MIXED = [(W.W4G128, W.W4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4), (W.W16, W.W16, W.W8A8),
          (W.W3G128, W.W3G128, W.W16), (W.W4A4, W.W8G128, W.W4G128)]
+MIXED_G = [(W.W4A4G128, W.W4A4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4G128), (W.W4A4G128,) * 3,
+           (W.W16, W.W16, W.W4A4G128), (W.W4A4G128, W.W4A4G128, W.W8A8)]
 
 
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
-def test_moe_brute_force(act):
-    blk = W.random_small_block(21, T=5, H=128, F=128, E=4, k=2, n_shared=1, F_shared=128, act=act,
-                               schemes=MIXED)
+@pytest.mark.parametrize("mix,H,F", [(MIXED, 128, 128), (MIXED_G, 256, 256)])
+def test_moe_brute_force(act, mix, H, F):
+    blk = W.random_small_block(21, T=5, H=H, F=F, E=4, k=2, n_shared=1, F_shared=128, act=act,
+                               schemes=mix)
     blk.topk_ids[2, 1] = 9          # an invalid expert id is skipped
     out = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 4, act)
     np.testing.assert_allclose(out["y"], py_moe(blk), rtol=1e-9, atol=1e-12)
@@ -428,7 +472,7 @@ def test_tile_plan_slices_minimal(nwg):
     assert all(x["split"] <= y["split"] for x, y in zip(a, b))
 
 
-@pytest.mark.parametrize("name", ["tiny", "dsv2lite", "qwen15_mixed"])
+@pytest.mark.parametrize("name", ["tiny", "dsv2lite", "qwen15_mixed", "qwen15_w5a5"])
 def test_tile_plan_covers_every_output(name):
     blk = W.make_block(name, with_weights=False)
     cfg = blk.cfg

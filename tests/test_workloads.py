@@ -27,9 +27,24 @@ def test_prefix_sample_matches_full():
 
 @pytest.mark.parametrize("name,bits", [("tiny", 7.63), ("mixtral", 3.26), ("dsv2lite", 4.79),
                                        ("qwen15_uniform", 4.02), ("qwen15_mixed", 4.01),
-                                       ("qwen2", 5.01)])
+                                       ("qwen15_w5a5", 4.92), ("qwen2", 5.01)])
 def test_avg_weight_bits(name, bits):
     assert abs(W.avg_weight_bits(W.CONFIGS[name]) - bits) < 0.006
+
+
+def test_w5a5_allocation_counts():
+    """The printed W5A5 allocation (Qwen1.5-MoE layer 5): gate/up mostly
+    w4a4-g128 with a few per-channel w4a4 rows and one w8a8 row; down split
+    between w8a8 and w4a4-g128; the shared expert is row 60."""
+    from collections import Counter
+    cfg = W.CONFIGS["qwen15_w5a5"]
+    rows = [cfg.alloc(e, 0) for e in range(cfg.E)] + [cfg.shared_alloc]
+    assert all(r[0] == r[1] for r in rows)
+    gu = Counter(r[0].name for r in rows)
+    dn = Counter(r[2].name for r in rows)
+    assert gu == {"w4a4g128": 51, "w4a4": 9, "w8a8": 1}
+    assert dn == {"w8a8": 35, "w4a4g128": 26}
+    assert cfg.shared_alloc == (W.W4A4, W.W4A4, W.W8A8)
 
 
 def test_packed_size_closed_form():
