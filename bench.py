@@ -135,6 +135,64 @@ def cpu_baseline(blk, tokens):
                       f"fp64 numpy incl. dequantization of those experts", "seconds": round(dt, 2)}
 
 
+def compare_per_expert(args):
+    """One Group-GEMM launch per phase against the same micro-kernels launched
+    once per expert (the per-expert invocation the paper's motivation study
+    measures, Sec. 2.3 and its throughput figure): 60 experts, gate+up of shape
+    [N, K] = [2816, 2048] per expert, top-4, 512 tokens, uniform schemes.  The
+    per-expert figure sums the HIP-event durations of the single-expert
+    launches (each runs after its own plan, which is not counted), so it
+    leaves out launch gaps: a lower bound on sequential execution."""
+    import torch
+    from paper_2505_05799_amd import mxmoe as M
+    from paper_2505_05799_amd import workloads as W
+    out = []
+    for sch in (W.W16, W.W4G128, W.W8A8):
+        cfg = W.BlockConfig(f"per_expert_{sch.name}", T=512, H=2048, F=1408, E=60, k=4, n_shared=0, F_shared=0,
+                            act="bf16", zipf_s=args.zipf, alloc=lambda e, r, s=sch: (s, s, s),
+                            description="60 experts [2816, 2048] gate+up, top-4, 512 tokens")
+        blk = W.make_block(cfg, seed=args.seed)
+        mb = M.MoEBlock(blk)
+        x = M.act_tensor(blk.x, cfg.act)
+        ids = torch.from_numpy(blk.topk_ids.copy()).cuda()
+        w = torch.from_numpy(blk.topk_w.copy()).cuda()
+        counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
+        live = [e for e in range(cfg.E) if counts[e] > 0]
+        fl_gu = sum(2.0 * 2 * int(counts[e]) * cfg.F * cfg.H for e in live)
+        for _ in range(args.warmup):
+            mb.forward(x, ids, w, skip_combine=True)
+        reps = max(args.steps, 3)
+        ev = M.PhaseEvents()
+        fused = []
+        for _ in range(reps):
+            mb.forward(x, ids, w, skip_combine=True, events=ev)
+            torch.cuda.synchronize()
+            fused.append(ev.elapsed_ms())
+        seq = []
+        for _ in range(reps):
+            tot = np.zeros(M.N_PHASES)
+            for e in live:
+                mask = [0] * cfg.E
+                mask[e] = 1
+                mb.forward(x, ids, w, skip_combine=True, events=ev, expert_mask=mask)
+                torch.cuda.synchronize()
+                tot += np.array(ev.elapsed_ms())
+            seq.append(tot)
+        f = np.mean(fused, axis=0)
+        q = np.mean(seq, axis=0)
+        rec = {"scheme": sch.name, "tokens": 512, "experts_live": len(live),
+               "gate_up_ms_fused": round(float(f[1]), 4), "gate_up_ms_per_expert_sum": round(float(q[1]), 4),
+               "gate_up_tflops_fused": round(fl_gu / (f[1] / 1e3) / 1e12, 1),
+               "gate_up_tflops_per_expert": round(fl_gu / (q[1] / 1e3) / 1e12, 1),
+               "down_ms_fused": round(float(f[3]), 4), "down_ms_per_expert_sum": round(float(q[3]), 4),
+               "speedup_gate_up": round(float(q[1] / f[1]), 2)}
+        print(json.dumps(rec), flush=True)
+        out.append(rec)
+        del mb
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -146,6 +204,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (memory-counter calibration)")
+    ap.add_argument("--compare-per-expert", action="store_true",
+                    help="one Group-GEMM launch vs per-expert launches of the same micro-kernels "
+                         "(60 experts [2816, 2048], top-4, 512 tokens); one JSON line per scheme")
+    ap.add_argument("--zipf", type=float, default=1.5, help="router skew of --compare-per-expert")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -163,6 +225,10 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.compare_per_expert:
+        M.load_library()
+        compare_per_expert(args)
         return
     M.load_library()
     cfg = W.CONFIGS[args.workload]

@@ -134,6 +134,27 @@ MXMOE_API mxmoe_status mxmoe_route_permute(const int32_t* topk_ids, int32_t T, i
                                  int32_t* inv, int32_t* status, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream);
 
+/* Router front-end (Eq. (2): the gate weights w_e come from a softmax over
+ * the router's logits).  Per token t, one wavefront:
+ *   p_e = exp(l_e - max l) / sum_e' exp(l_e' - max l)      (fp32)
+ *   topk_ids[t, 0..k-1]: the k largest logits in decreasing order, ties to
+ *            the lower expert id (the same order as the probabilities);
+ *   topk_w[t, s] = p of that expert, or, with renormalize = 1,
+ *            exp(l - max l) / (sum of it over the k chosen experts);
+ *   shared_w[t, j] = 1 / (1 + exp(-shared_logits[t, j])): the sigmoid gate a
+ *            shared expert's output is multiplied by (Qwen-MoE style), only
+ *            if shared_logits is not NULL.
+ *   logits       : fp32 [T, E], finite values (a NaN is never chosen; a token
+ *                  left with only NaN candidates gets id -1 in its last slots)
+ *   shared_logits: fp32 [T, n_shared] or NULL
+ *   topk_ids: int32 [T, k], topk_w: fp32 [T, k], shared_w: fp32 [T, n_shared]
+ * Limits: 1 <= k <= min(E, 64), E <= 1024, 0 <= n_shared <= 64.  All device
+ * pointers, 4-byte aligned.  Errors: INVALID_ARG, HIP.                      */
+MXMOE_API mxmoe_status mxmoe_router_topk(const float* logits, int32_t T, int32_t E, int32_t k,
+                               int32_t renormalize, const float* shared_logits, int32_t n_shared,
+                               int32_t* topk_ids, float* topk_w, float* shared_w,
+                               hipStream_t stream);
+
 /* ------------------------------------------------------ activation quant */
 
 /* Per-row symmetric quantization of a [rows, cols] activation matrix (row
@@ -214,6 +235,18 @@ typedef struct {
    * 0 routing + plan + x quantization, 1 gate/up Group-GEMM, 2 h quantization,
    * 3 down Group-GEMM, 4 combine).                                          */
   hipEvent_t* events;
+  /* fp32 [T, E] router logits, or NULL.  When set, the forward starts with
+   * the router front-end of mxmoe_router_topk: topk_ids / topk_w may then be
+   * NULL and are not read; the chosen ids and weights land in the workspace
+   * (router_ids / router_w of mxmoe_ws_layout).                              */
+  const float* router_logits;
+  int32_t renormalize;           /* with router_logits: as in mxmoe_router_topk */
+  /* With router_logits: fp32 [T, n_shared] shared-expert gate logits or NULL;
+   * their sigmoid multiplies each shared expert's output.                    */
+  const float* shared_logits;
+  /* Without router_logits: fp32 [T, n_shared] weights of the shared experts'
+   * outputs, or NULL for weight 1.                                           */
+  const float* shared_w;
   int32_t reserved[2];
 } mxmoe_forward_opts;
 
@@ -259,6 +292,10 @@ typedef struct {
   size_t hsg;           /* fp32 [T*k, F/128]: group scales of routed h rows
                            for w4a4-g128 down (codes in hq), else -1         */
   size_t hsg_shared;    /* fp32 [n_shared*T, F_shared/128], else -1          */
+  size_t router_ids;    /* int32 [T, k]: ids chosen by the router front-end  */
+  size_t router_w;      /* fp32 [T, k]: their gate weights                   */
+  size_t shared_w;      /* fp32 [T, n_shared]: sigmoid shared gates (-1 if no
+                           shared experts)                                   */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

@@ -15,6 +15,10 @@ operands the GPU receives (codes, scales, zeros - never the packed layout):
 * Sec. 2.1 min-max quantizer and the weight storage of Sec. 5.2: a wNg128 weight
   dequantizes to s * (q - z) per group of 128 along K; a per-channel symmetric
   weight (w8a8 / w4a4, Fig. 4 caption) to s_w[n] * q.
+* Sec. 2.2, Eq. (2), router front-end: the gate weights are the router's
+  softmax probabilities of the token's k largest logits (optionally
+  renormalised over those k); a shared expert's output may be scaled by a
+  per-token sigmoid gate (Qwen-MoE style shared experts).
 * Sec. 4.2.2 (end): activations of w8a8 / w4a4 linears are quantized dynamically
   at run time, per token (a_gsize = -1 in the W5A5 allocation table), with the
   fp32 recipe of :func:`act_quant`.
@@ -36,7 +40,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 __all__ = [
-    "bf16_bits_to_f64", "round_to_act", "act_values", "route", "dequant",
+    "bf16_bits_to_f64", "round_to_act", "act_values", "route", "router_topk", "shared_gate", "dequant",
     "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
     "silu", "tile_plan", "xcd_queues", "xcd_tiles",
 ]
@@ -114,6 +118,31 @@ def route(topk_ids: np.ndarray, E: int) -> Dict[str, np.ndarray]:
         "inv": inv.astype(np.int32),
         "bad": bad,
     }
+
+
+def router_topk(logits: np.ndarray, k: int, renormalize: bool = False) -> Tuple[np.ndarray, np.ndarray]:
+    """Router front-end of Eq. (2) on fp32 logits [T, E].
+
+    The chosen experts are the k largest logits, in decreasing order, ties to
+    the lower expert id (softmax is increasing, so this is the top-k of the
+    probabilities).  Weights: p_e = exp(l_e - max l) / sum exp(l - max l) in
+    fp64, or with ``renormalize`` the chosen exp(l - max l) over their own sum.
+    Returns ids int32 [T, k] and weights fp64 [T, k].
+    """
+    l = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    T, E = l.shape
+    order = np.argsort(-l, axis=1, kind="stable")[:, :k]     # stable: equal logits keep id order
+    ex = np.exp(l - l.max(axis=1, keepdims=True))
+    sel = np.take_along_axis(ex, order, axis=1)
+    den = sel.sum(axis=1, keepdims=True) if renormalize else ex.sum(axis=1, keepdims=True)
+    return order.astype(np.int32), sel / den
+
+
+def shared_gate(logits: np.ndarray) -> np.ndarray:
+    """Sigmoid gate of the shared experts, 1 / (1 + exp(-l)), fp64."""
+    l = np.asarray(logits, dtype=np.float32).astype(np.float64)
+    with np.errstate(over="ignore"):
+        return 1.0 / (1.0 + np.exp(-l))
 
 
 # ----------------------------------------------------------------------------
@@ -338,8 +367,10 @@ def _expert_mlp(a: np.ndarray, lins: Sequence, act: str, want_slack: bool):
 
 def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
                 linears: Sequence[Sequence], E: int, act: str,
-                want_slack: bool = False, return_h: bool = False):
-    """Eq. (2): y[t] = sum_s w[t,s] * Expert_{ids[t,s]}(x[t]) + sum_shared Expert_j(x[t]).
+                want_slack: bool = False, return_h: bool = False,
+                shared_w: Optional[np.ndarray] = None):
+    """Eq. (2): y[t] = sum_s w[t,s] * Expert_{ids[t,s]}(x[t]) + sum_j g[t,j] * Shared_j(x[t]),
+    with g = ``shared_w`` [T, n_shared] (fp32 values) or 1.
 
     x: [T, H] activations in act storage; topk_ids int32 [T, k]; topk_w fp32
     [T, k]; linears[e] = (gate, up, down) for e < E routed, then shared experts.
@@ -369,9 +400,10 @@ def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
             hs[e] = hb
     for j in range(len(linears) - E):
         d, hb, sl = _expert_mlp(a_all, linears[E + j], act, want_slack)
-        y += d
+        gj = np.ones((T, 1)) if shared_w is None else np.asarray(shared_w, dtype=np.float64)[:, j:j + 1]
+        y += d * gj
         if sl is not None:
-            slack += sl
+            slack += sl * np.abs(gj)
         if return_h:
             hs[E + j] = hb
     out = {"y": y, "slack": slack, "route": r}

@@ -149,6 +149,9 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.xs4g = bi.any_x4g ? take(4 * (size_t)T * (bi.H / 128)) : kNone;
   L.hsg = bi.any_hg ? take(4 * P * (bi.F / 128)) : kNone;
   L.hsg_shared = bi.any_hg_sh ? take(4 * (size_t)bi.nsh * T * (bi.Fsh / 128)) : kNone;
+  L.rids = take(4 * P);
+  L.rw = take(4 * P);
+  L.shw = bi.nsh ? take(4 * (size_t)T * bi.nsh) : kNone;
   L.total = o;
   return L;
 }
@@ -234,6 +237,22 @@ mxmoe_status mxmoe_route_permute(const int32_t* topk_ids, int32_t T, int32_t k, 
   int32_t* cc = reinterpret_cast<int32_t*>(workspace);
   int32_t* cb = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) + align256(4 * nchunks * E));
   return hip_status(launch_route(topk_ids, T, k, E, counts, offsets, sorted_pair, inv, status, cc, cb, stream));
+}
+
+mxmoe_status mxmoe_router_topk(const float* logits, int32_t T, int32_t E, int32_t k, int32_t renormalize,
+                               const float* shared_logits, int32_t n_shared, int32_t* topk_ids, float* topk_w,
+                               float* shared_w, hipStream_t stream) {
+  if (T < 0 || E <= 0 || E > kMaxE || k <= 0 || k > E || k > kRouterMaxK) return MXMOE_ERR_INVALID_ARG;
+  if (n_shared < 0 || n_shared > kMaxShared || (renormalize != 0 && renormalize != 1)) return MXMOE_ERR_INVALID_ARG;
+  if ((int64_t)T * E >= (1LL << 31)) return MXMOE_ERR_INVALID_ARG;
+  if (T == 0) return MXMOE_OK;
+  if (!logits || !topk_ids || !topk_w) return MXMOE_ERR_INVALID_ARG;
+  if (shared_logits && n_shared > 0 && !shared_w) return MXMOE_ERR_INVALID_ARG;
+  if (!aligned(logits, 4) || !aligned(topk_ids, 4) || !aligned(topk_w, 4) || !aligned(shared_logits, 4) ||
+      !aligned(shared_w, 4))
+    return MXMOE_ERR_INVALID_ARG;
+  return hip_status(launch_router_topk(logits, T, E, k, renormalize, n_shared > 0 ? shared_logits : nullptr, n_shared,
+                                       topk_ids, topk_w, shared_w, stream));
 }
 
 mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32_t cols, int64_t ld, int32_t qmax,
@@ -405,6 +424,9 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->xs4g = L.xs4g;
   out->hsg = L.hsg;
   out->hsg_shared = L.hsg_shared;
+  out->router_ids = L.rids;
+  out->router_w = L.rw;
+  out->shared_w = L.shw;
   return MXMOE_OK;
 }
 
@@ -416,8 +438,19 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if (st != MXMOE_OK) return st;
   if (T < 0) return MXMOE_ERR_INVALID_ARG;
   if ((int64_t)T * bi.k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
+  const bool router = opts && opts->router_logits;
+  if (router) {
+    if (opts->renormalize != 0 && opts->renormalize != 1) return MXMOE_ERR_INVALID_ARG;
+    if (opts->shared_w || !aligned(opts->router_logits, 4) || !aligned(opts->shared_logits, 4))
+      return MXMOE_ERR_INVALID_ARG;
+    if (bi.k > kRouterMaxK) return MXMOE_ERR_UNSUPPORTED;
+  } else {
+    if (opts && opts->shared_logits) return MXMOE_ERR_INVALID_ARG;
+    if (opts && !aligned(opts->shared_w, 4)) return MXMOE_ERR_INVALID_ARG;
+  }
   if (T == 0) return MXMOE_OK;
-  if (!block_table || !x || !topk_ids || !topk_w || !y || !workspace) return MXMOE_ERR_INVALID_ARG;
+  if (!block_table || !x || !y || !workspace) return MXMOE_ERR_INVALID_ARG;
+  if (!router && (!topk_ids || !topk_w)) return MXMOE_ERR_INVALID_ARG;
   if (!aligned(block_table, 16) || !aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 256) ||
       !aligned(topk_ids, 4) || !aligned(topk_w, 4))
     return MXMOE_ERR_INVALID_ARG;
@@ -452,7 +485,21 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   int32_t* plan = at<int32_t>(workspace, L.plan);
   int32_t* down_qmax = at<int32_t>(workspace, L.down_qmax);
   MX_EVENT(0);
-  MX_CHECK(launch_route(topk_ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
+  // router front-end: ids and gate weights come from the logits, into the workspace
+  const int32_t* ids = topk_ids;
+  const float* tw = topk_w;
+  const float* shw = opts ? opts->shared_w : nullptr;
+  if (router) {
+    int32_t* rids = at<int32_t>(workspace, L.rids);
+    float* rw = at<float>(workspace, L.rw);
+    float* rshw = (bi.nsh && opts->shared_logits) ? at<float>(workspace, L.shw) : nullptr;
+    MX_CHECK(launch_router_topk(opts->router_logits, T, bi.E, bi.k, opts->renormalize, rshw ? opts->shared_logits : nullptr,
+                                bi.nsh, rids, rw, rshw, stream));
+    ids = rids;
+    tw = rw;
+    shw = rshw;
+  }
+  MX_CHECK(launch_route(ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
                         at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
                         at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
@@ -470,7 +517,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if (bi.any_x4g)
     MX_CHECK(launch_act_quant_g128(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4g),
                                    at<float>(workspace, L.xs4g), stream));
-  MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, topk_w, at<float>(workspace, L.xs8),
+  MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
                            at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
                            at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
                            stream));
@@ -480,7 +527,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.plan = plan;
   ga.sorted_pair = sorted_pair;
   ga.offsets = offsets;
-  ga.topk_w = topk_w;
+  ga.topk_w = tw;
+  ga.shared_w = shw;
   ga.x = x;
   ga.xq8 = at<int8_t>(workspace, L.xq8);
   ga.xs8 = at<float>(workspace, L.xs8);
@@ -542,7 +590,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   MX_EVENT(7);
   MX_EVENT(8);
   if (!(opts && opts->skip_combine))
-    MX_CHECK(launch_combine(ga.slots, topk_ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
+    MX_CHECK(launch_combine(ga.slots, ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
   MX_EVENT(9);
 #undef MX_EVENT
 #undef MX_CHECK

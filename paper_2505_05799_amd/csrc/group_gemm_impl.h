@@ -518,6 +518,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
       if (shared) {
         out = m * (a.k + a.n_shared) + a.k + (g - a.E_routed);
+        if (a.shared_w) gw = a.shared_w[(int64_t)m * a.n_shared + (g - a.E_routed)];
       } else {
         out = a.rslot[off_e + m];
         gw = a.rgw[off_e + m];

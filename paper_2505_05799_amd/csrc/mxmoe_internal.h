@@ -233,6 +233,7 @@ struct WsLayout {
   size_t partial;  // fp32 split-K partial sums (both phases reuse it)
   size_t rsx, rsh, rsh_shared;  // fp32 row sums per 128-wide k block of x, h, h_shared
   size_t xq4g, xs4g, hsg, hsg_shared;  // w4a4-g128 codes and group scales
+  size_t rids, rw, shw;  // router front-end outputs: ids, gate weights, shared-expert gates
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -251,6 +252,11 @@ hipError_t launch_unpack(int kind, int n, int k, int act, const uint8_t* packed,
 hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
                         int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
+// Router front-end, one wavefront per token: softmax top-k of fp32 logits
+// [T,E] (E <= 1024, k <= 64) and, if shared_logits, sigmoid gates [T,n_sh].
+constexpr int kRouterMaxK = 64;
+hipError_t launch_router_topk(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
+                              int n_sh, int32_t* ids, float* w, float* shared_w, hipStream_t s);
 
 // Row sums of each 128-wide block of bf16 rows: out[r][b] = sum of a[r][128b ..
 // 128b + 127] in fp32; cols a multiple of 128, rows 16-byte aligned.
@@ -296,6 +302,7 @@ struct GemmArgs {
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;
   float* slots;
+  const float* shared_w;     // [T][n_shared] weights of the shared experts' rows, or null (weight 1)
   const int32_t* down_qmax;
   int32_t T, k;
   int32_t act;

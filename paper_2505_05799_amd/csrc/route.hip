@@ -1,3 +1,5 @@
+// Router front-end and routing.
+//
 // Routing / permutation: stable counting sort of the T*k (token, slot) pairs
 // by expert id, which forms the per-expert row groups X_e of Eq. (2).
 //
@@ -135,7 +137,99 @@ __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restr
   }
 }
 
+// ---------------------------------------------------------- router front-end
+// Eq. (2) weights its experts by the router's softmax.  One wavefront per
+// token; lane l holds the logits of experts l, l + 64, ... in registers.  The
+// k largest are found in k rounds of a wavefront arg-max under the strict
+// order (larger logit, then lower id), which all lanes agree on, so the
+// result is unique and every lane of the butterfly ends with the same value.
+constexpr int kRouterJ = kMaxE / 64;
+
+__device__ inline bool router_better(float va, int ea, float vb, int eb) {
+  return va > vb || (va == vb && ea < eb);
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int d = 32; d; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+__global__ void __launch_bounds__(kThreads) router_topk_kernel(const float* __restrict__ logits, int T, int E,
+                                                                int k, int renorm,
+                                                                const float* __restrict__ shared_logits, int n_sh,
+                                                                int32_t* __restrict__ ids, float* __restrict__ w,
+                                                                float* __restrict__ shared_w) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (t >= T) return;  // a whole wavefront leaves together
+  const float* row = logits + (int64_t)t * E;
+  const int J = (E + 63) >> 6;
+  float v[kRouterJ];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kRouterJ; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = (j < J && e < E) ? row[e] : -INFINITY;
+    m = fmaxf(m, v[j]);
+  }
+#pragma unroll
+  for (int d = 32; d; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+  float se = 0.f;
+#pragma unroll
+  for (int j = 0; j < kRouterJ; ++j)
+    if (j < J && lane + 64 * j < E) se += expf(v[j] - m);
+  se = wave_sum(se);
+
+  uint32_t taken = 0;  // bit j: this lane's v[j] is chosen
+  int my_e = -1;
+  float my_v = -INFINITY;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int be = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < kRouterJ; ++j) {
+      const int e = lane + 64 * j;
+      if (j < J && e < E && !((taken >> j) & 1u) && router_better(v[j], e, bv, be)) {
+        bv = v[j];
+        be = e;
+      }
+    }
+#pragma unroll
+    for (int d = 32; d; d >>= 1) {
+      const float ov = __shfl_xor(bv, d, 64);
+      const int oe = __shfl_xor(be, d, 64);
+      if (router_better(ov, oe, bv, be)) {
+        bv = ov;
+        be = oe;
+      }
+    }
+    if (be != 0x7fffffff && (be & 63) == lane) taken |= 1u << (be >> 6);
+    if (lane == r) {
+      my_e = be == 0x7fffffff ? -1 : be;
+      my_v = bv;
+    }
+  }
+  const float q = (lane < k && my_e >= 0) ? expf(my_v - m) : 0.f;
+  const float den = renorm ? wave_sum(q) : se;
+  if (lane < k) {
+    ids[(int64_t)t * k + lane] = my_e;
+    w[(int64_t)t * k + lane] = q / den;
+  }
+  if (shared_logits && lane < n_sh)
+    shared_w[(int64_t)t * n_sh + lane] = 1.f / (1.f + expf(-shared_logits[(int64_t)t * n_sh + lane]));
+}
+
 }  // namespace
+
+hipError_t launch_router_topk(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
+                              int n_sh, int32_t* ids, float* w, float* shared_w, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  const int per = kThreads / 64;
+  hipLaunchKernelGGL(router_topk_kernel, dim3((T + per - 1) / per), dim3(kThreads), 0, s, logits, T, E, k, renorm,
+                     shared_logits, n_sh, ids, w, shared_w);
+  return hipGetLastError();
+}
 
 hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts, int32_t* offsets,
                         int32_t* sorted_pair, int32_t* inv, int32_t* status, int32_t* chunk_counts,

@@ -43,13 +43,14 @@ PHASE_NAMES = ("route_plan_xquant", "gemm_gate_up", "hquant", "gemm_down", "comb
 class ForwardOpts_t(C.Structure):
     _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("split_phases", C.c_int32),
                 ("skip_combine", C.c_int32), ("events", C.POINTER(C.c_void_p)),
-                ("reserved", C.c_int32 * 2)]
+                ("router_logits", C.c_void_p), ("renormalize", C.c_int32), ("shared_logits", C.c_void_p),
+                ("shared_w", C.c_void_p), ("reserved", C.c_int32 * 2)]
 
 
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
              "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total", "plan_queue_cap",
              "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared", "xq4g", "xs4g", "hsg",
-             "hsg_shared"]
+             "hsg_shared", "router_ids", "router_w", "shared_w"]
 
 
 class WsLayout_t(C.Structure):
@@ -58,7 +59,7 @@ class WsLayout_t(C.Structure):
 
 EXPORTS = [
     "mxmoe_packed_bytes", "mxmoe_pack_weights", "mxmoe_unpack_weights", "mxmoe_route_workspace_bytes",
-    "mxmoe_route_permute", "mxmoe_act_quant", "mxmoe_linear_workspace_bytes", "mxmoe_linear_forward",
+    "mxmoe_route_permute", "mxmoe_router_topk", "mxmoe_act_quant", "mxmoe_linear_workspace_bytes", "mxmoe_linear_forward",
     "mxmoe_block_table_bytes", "mxmoe_block_table_fill", "mxmoe_workspace_bytes", "mxmoe_moe_forward",
     "mxmoe_moe_forward_ex", "mxmoe_workspace_layout", "mxmoe_status_string", "mxmoe_version",
 ]
@@ -82,6 +83,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "mxmoe_unpack_weights": (C.c_int, [PL, C.c_int, vp, vp, vp, vp, vp]),
         "mxmoe_route_workspace_bytes": (sz, [i32, i32, i32]),
         "mxmoe_route_permute": (C.c_int, [vp, i32, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "mxmoe_router_topk": (C.c_int, [vp, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp]),
         "mxmoe_act_quant": (C.c_int, [vp, C.c_int, i32, i32, i64, i32, vp, vp, vp]),
         "mxmoe_linear_workspace_bytes": (sz, [PL, i32]),
         "mxmoe_linear_forward": (C.c_int, [PL, C.c_int, vp, i32, vp, vp, vp, sz, vp]),
@@ -263,6 +265,21 @@ def route_permute(topk_ids, E: int, stream=None):
             "status": status}
 
 
+def router_topk(logits, k: int, renormalize: bool = False, shared_logits=None, stream=None):
+    """Router front-end: (ids int32 [T,k], weights fp32 [T,k], shared gates fp32
+    [T,n_shared] or None) from fp32 logits [T,E] (and shared-gate logits)."""
+    torch = _torch()
+    lib = load_library()
+    T, E = logits.shape
+    ids = torch.empty((T, k), dtype=torch.int32, device=logits.device)
+    w = torch.empty((T, k), dtype=torch.float32, device=logits.device)
+    n_sh = 0 if shared_logits is None else shared_logits.shape[1]
+    shw = None if shared_logits is None else torch.empty((T, n_sh), dtype=torch.float32, device=logits.device)
+    _check(lib.mxmoe_router_topk(_ptr(logits), T, E, k, 1 if renormalize else 0, _ptr(shared_logits), n_sh, _ptr(ids),
+                                 _ptr(w), _ptr(shw), _stream_ptr(stream)), "mxmoe_router_topk")
+    return ids, w, shw
+
+
 def act_quant(a, act: str, qmax: int, stream=None):
     torch = _torch()
     lib = load_library()
@@ -314,7 +331,10 @@ class MoEBlock:
         return {f: getattr(lay, f) for f in WS_FIELDS}
 
     def forward(self, x, topk_ids, topk_w, y=None, expert_mask: Optional[Sequence[int]] = None,
-                skip_combine: bool = False, events=None, stream=None):
+                skip_combine: bool = False, events=None, stream=None, router_logits=None,
+                renormalize: bool = False, shared_logits=None, shared_w=None):
+        """topk_ids / topk_w may be None when router_logits (fp32 [T,E]) is
+        given; the router's choice is then left in the workspace."""
         torch = _torch()
         lib = load_library()
         T = x.shape[0]
@@ -323,8 +343,13 @@ class MoEBlock:
         if y is None:
             y = torch.empty_like(x)
         opts = None
-        if expert_mask is not None or skip_combine or events is not None:
+        if (expert_mask is not None or skip_combine or events is not None or router_logits is not None
+                or shared_w is not None):
             o = ForwardOpts_t()
+            o.router_logits = _ptr(router_logits)
+            o.renormalize = 1 if renormalize else 0
+            o.shared_logits = _ptr(shared_logits)
+            o.shared_w = _ptr(shared_w)
             if events is not None:
                 o.events = events.array
             if expert_mask is not None:

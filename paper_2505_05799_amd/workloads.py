@@ -377,6 +377,20 @@ def make_routing(cfg: BlockConfig, seed: int = 0, T: Optional[int] = None):
     return np.ascontiguousarray(ids.astype(np.int32)), np.ascontiguousarray(w)
 
 
+def router_logits(T: int, E: int, seed: int = 0, zipf_s: Optional[float] = None,
+                  n_shared: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """fp32 router logits [T, E] (N(0,1) plus the Zipf bias of make_routing,
+    expert ranks a seeded permutation) and fp32 shared-gate logits [T, n_shared]
+    (N(0,1)), for the router front-end."""
+    rng = np.random.default_rng([seed, 4])
+    l = rng.standard_normal((T, E))
+    if zipf_s is not None:
+        ranks = np.random.default_rng([seed, 5]).permutation(E) + 1
+        l = l - zipf_s * np.log(ranks.astype(np.float64))
+    sh = np.random.default_rng([seed, 6]).standard_normal((T, n_shared))
+    return np.ascontiguousarray(l.astype(np.float32)), np.ascontiguousarray(sh.astype(np.float32))
+
+
 def make_x(cfg: BlockConfig, seed: int = 0, T: Optional[int] = None) -> np.ndarray:
     T = cfg.T if T is None else T
     x = np.random.default_rng([seed, 0]).standard_normal((cfg.T, cfg.H))[:T]

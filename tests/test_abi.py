@@ -168,3 +168,39 @@ def test_block_validation(lib):
 def test_status_strings(lib):
     for s in range(5):
         assert lib.mxmoe_status_string(s)
+
+
+def test_router_validation(lib):
+    p = C.c_void_p(1 << 20)
+    f = lib.mxmoe_router_topk
+    assert f(p, 4, 8, 0, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG     # k = 0
+    assert f(p, 4, 8, 9, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG     # k > E
+    assert f(p, 4, 100, 65, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG  # k > 64
+    assert f(p, 4, 1025, 2, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG  # E > 1024
+    assert f(p, 4, 8, 2, 2, None, 0, p, p, None, None) == M.ERR_INVALID_ARG     # renormalize not 0/1
+    assert f(p, 4, 8, 2, 0, p, 65, p, p, p, None) == M.ERR_INVALID_ARG          # n_shared > 64
+    assert f(p, 4, 8, 2, 0, p, 1, p, p, None, None) == M.ERR_INVALID_ARG        # shared gates without output
+    assert f(None, 4, 8, 2, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG
+    assert f(C.c_void_p((1 << 20) + 2), 4, 8, 2, 0, None, 0, p, p, None, None) == M.ERR_INVALID_ARG
+    assert f(None, 0, 8, 2, 0, None, 0, None, None, None, None) == M.OK          # T = 0
+
+
+def test_forward_router_mode_validation(lib):
+    B, keep = _block("tiny")
+    p = C.c_void_p(1 << 20)
+    o = M.ForwardOpts_t()
+    o.router_logits = p
+    o.renormalize = 3
+    assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, None, None, p, p, 10 ** 9, C.byref(o), None) == \
+        M.ERR_INVALID_ARG
+    o.renormalize = 0
+    o.shared_w = p                          # direct shared weights belong to the ids mode
+    assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, None, None, p, p, 10 ** 9, C.byref(o), None) == \
+        M.ERR_INVALID_ARG
+    o2 = M.ForwardOpts_t()
+    o2.shared_logits = p                    # gate logits need router mode
+    assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, p, p, p, p, 10 ** 9, C.byref(o2), None) == \
+        M.ERR_INVALID_ARG
+    o3 = M.ForwardOpts_t()                  # ids mode without ids
+    assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, None, None, p, p, 10 ** 9, C.byref(o3), None) == \
+        M.ERR_INVALID_ARG

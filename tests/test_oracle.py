@@ -507,3 +507,79 @@ def test_tile_plan_covers_every_output(name):
         for q in tiles:
             ranks = [rank[g] for g, _, _ in q]
             assert ranks == sorted(ranks)
+
+
+# ---------------------------------------------------------------------------
+# router front-end (Eq. 2 gate weights from the router softmax)
+# ---------------------------------------------------------------------------
+
+
+def py_router(row, k, renorm):
+    """Brute force: sort expert ids by (-logit, id), softmax with math.exp."""
+    E = len(row)
+    order = sorted(range(E), key=lambda e: (-row[e], e))[:k]
+    m = max(row)
+    ex = [math.exp(v - m) for v in row]
+    den = sum(ex[e] for e in order) if renorm else sum(ex)
+    return order, [ex[e] / den for e in order]
+
+
+@pytest.mark.parametrize("renorm", [False, True])
+@pytest.mark.parametrize("T,E,k", [(5, 8, 2), (7, 60, 4), (3, 65, 8), (4, 64, 64)])
+def test_router_brute_force(T, E, k, renorm):
+    l, _ = W.router_logits(T, E, seed=E + k, zipf_s=1.0)
+    l[0, :4] = l[0, 4]                       # ties go to the lower id
+    ids, w = O.router_topk(l, k, renorm)
+    for t in range(T):
+        pi, pw = py_router([float(v) for v in l[t]], k, renorm)
+        assert ids[t].tolist() == pi
+        np.testing.assert_allclose(w[t], pw, rtol=1e-13)
+
+
+def test_router_closed_forms():
+    # equal logits: ids in order, weights 1/E, renormalised 1/k
+    ids, w = O.router_topk(np.zeros((2, 8), np.float32), 3)
+    assert ids.tolist() == [[0, 1, 2]] * 2 and np.all(w == 1 / 8)
+    ids, w = O.router_topk(np.zeros((1, 8), np.float32), 3, renormalize=True)
+    assert np.allclose(w, 1 / 3, rtol=1e-15)
+    # [1, 3, 3, 2], k = 2: the tied 3s in id order, each e^3 / (e + 2 e^3 + e^2)
+    ids, w = O.router_topk(np.array([[1, 3, 3, 2]], np.float32), 2)
+    assert ids.tolist() == [[1, 2]]
+    assert np.allclose(w, math.exp(3) / (math.exp(1) + 2 * math.exp(3) + math.exp(2)), rtol=1e-15)
+    # k = E: a permutation sorted by logit, probabilities summing to 1
+    l, _ = W.router_logits(9, 16, seed=3)
+    ids, w = O.router_topk(l, 16)
+    assert all(sorted(r) == list(range(16)) for r in ids.tolist())
+    assert np.all(np.diff(np.take_along_axis(l, ids, axis=1), axis=1) <= 0)
+    assert np.allclose(w.sum(axis=1), 1.0, rtol=1e-14)
+    # a constant shift of the logits changes nothing (logits on a 2^-10 grid,
+    # so the shift is exact in fp32)
+    l = (np.rint(l * 1024) / 1024).astype(np.float32)
+    ids, w = O.router_topk(l, 16)
+    ids2, w2 = O.router_topk(l + np.float32(4.0), 16)
+    assert np.array_equal(ids, ids2) and np.allclose(w, w2, rtol=1e-12)
+
+
+def test_shared_gate_closed_forms():
+    assert O.shared_gate(np.array([0.0], np.float32))[0] == 0.5
+    x = np.linspace(-8, 8, 33).astype(np.float32)
+    g = O.shared_gate(x)
+    assert np.allclose(g + O.shared_gate(-x), 1.0, rtol=1e-15)
+    assert np.allclose(g, [1 / (1 + math.exp(-float(v))) for v in x], rtol=1e-15)
+
+
+def test_moe_shared_gate_is_linear_in_the_gate():
+    blk = W.random_small_block(4, T=6, H=128, F=128, E=3, k=2, n_shared=2, F_shared=128,
+                               schemes=MIXED[:3] + [MIXED[3], MIXED[4]])
+    args = (blk.x, blk.topk_ids, blk.topk_w, blk.linears, 3, "bf16")
+    base = O.moe_forward(*args)["y"]
+    ones = O.moe_forward(*args, shared_w=np.ones((6, 2), np.float32))["y"]
+    assert np.array_equal(base, ones)
+    routed = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears[:3], 3, "bf16")["y"]
+    zero = O.moe_forward(*args, shared_w=np.zeros((6, 2), np.float32))["y"]
+    assert np.array_equal(zero, routed)
+    g = np.random.default_rng(1).random((6, 2)).astype(np.float32)
+    y = O.moe_forward(*args, shared_w=g)["y"]
+    s0 = O.moe_forward(*args, shared_w=np.array([[1, 0]] * 6, np.float32))["y"] - routed
+    s1 = O.moe_forward(*args, shared_w=np.array([[0, 1]] * 6, np.float32))["y"] - routed
+    np.testing.assert_allclose(y, routed + g[:, :1] * s0 + g[:, 1:] * s1, rtol=1e-12, atol=1e-14)
