@@ -333,9 +333,17 @@ __device__ inline TileQueue tile_queue(const GemmArgs& a, int pidx) {
   Q.x0 = blockIdx.x % kXcd;  // workgroups are dealt round-robin over the XCDs
   return Q;
 }
-// claim the next index of the current queue (thread 0)
-__device__ inline int pop_start(const TileQueue& Q, int qi) {
-  return qi < kXcd ? atomicAdd(&Q.ctr[((Q.x0 + qi) % kXcd) * 4], 1) : 0;
+// claim the next index of the current queue (thread 0).  A queue whose head
+// has already passed its tile count is skipped after a plain load: once the
+// tiles run out, every workgroup would otherwise add to every head counter,
+// and those same-address atomics serialize in L2 (hundreds per counter).
+// Heads only grow, so a stale read can only cost one extra atomic.
+__device__ inline int pop_start(const TileQueue& Q, const Smem& sm, int qi) {
+  if (qi >= kXcd) return 0;
+  const int x = (Q.x0 + qi) % kXcd;
+  int32_t* c = &Q.ctr[x * 4];
+  if (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= sm.qtotal[x]) return 0x7fffffff;
+  return atomicAdd(c, 1);
 }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -385,7 +393,7 @@ __device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t ld
 // end with group -1.  The first claim of a workgroup uses a plain load.
 template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& sm) {
   int qi = sm.qi;
-  int idx = pop_start(Q, qi);
+  int idx = pop_start(Q, sm, qi);
   while (qi < kXcd) {
     const int x = (Q.x0 + qi) % kXcd;
     if (idx < sm.qtotal[x]) {
@@ -400,7 +408,7 @@ template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& 
       return;
     }
     ++qi;
-    idx = pop_start(Q, qi);
+    idx = pop_start(Q, sm, qi);
   }
   sm.qi = qi;
   sm.entry.x = -1;  // only the group field is read when no tile is left

@@ -239,7 +239,7 @@ struct WsLayout {
   int64_t pfloats;  // size of the partial buffer
 };
 
-constexpr int kRouteChunk = 2048;  // pairs per routing workgroup
+constexpr int kRouteChunk = 512;  // pairs per routing workgroup
 constexpr size_t kNone = (size_t)-1;
 
 // ----------------------------------------------------------- launchers
