@@ -141,8 +141,11 @@ def act_code(act: str) -> int:
 
 
 def _dev(arr: np.ndarray, device):
-    """numpy -> device tensor with the same bytes (16-bit data travels as int16)."""
+    """numpy -> device tensor with the same bytes (16-bit data travels as int16);
+    a torch tensor is moved as it is."""
     torch = _torch()
+    if isinstance(arr, torch.Tensor):
+        return arr.contiguous().to(device)
     a = np.ascontiguousarray(arr)
     if a.dtype == np.uint16:
         a = a.view(np.int16)
@@ -295,18 +298,24 @@ def act_quant(a, act: str, qmax: int, stream=None):
 class MoEBlock:
     """A packed MoE block on one GPU: weights, block table and workspace."""
 
-    def __init__(self, block, device="cuda", T_max: Optional[int] = None, stream=None):
+    def __init__(self, block, device="cuda", T_max: Optional[int] = None, stream=None,
+                 packed: Optional[List[List[PackedLinear]]] = None):
+        """`packed`: already packed linears per expert (may repeat objects) instead
+        of packing block.linears."""
         torch = _torch()
         lib = load_library()
         cfg = block.cfg
         self.cfg = cfg
         self.act = cfg.act
         self.device = device
-        self.packed: List[List[PackedLinear]] = []
-        for e, lins in enumerate(block.linears):
-            self.packed.append([PackedLinear(q, cfg.act, device, stream) for q in lins])
+        self.packed: List[List[PackedLinear]] = [list(ps) for ps in packed] if packed is not None else []
+        if packed is None:
+            for lins in block.linears:
+                self.packed.append([PackedLinear(q, cfg.act, device, stream) for q in lins])
         G = cfg.E + cfg.n_shared
-        self._schemes = (Scheme_t * (3 * G))(*[scheme_t(q.scheme) for lins in block.linears for q in lins])
+        if len(self.packed) != G:
+            raise ValueError(f"{len(self.packed)} packed experts for a block of {G}")
+        self._schemes = (Scheme_t * (3 * G))(*[scheme_t(p.q.scheme) for ps in self.packed for p in ps])
         self._ptrs = (C.c_void_p * (3 * G))(*[p.buf.data_ptr() for ps in self.packed for p in ps])
         self.B = Block_t(cfg.H, cfg.F, cfg.E, cfg.k, cfg.n_shared, cfg.F_shared if cfg.n_shared else 0,
                          act_code(cfg.act), C.cast(self._schemes, C.POINTER(Scheme_t)),

@@ -1,0 +1,270 @@
+"""Tile costs and the runtime model of the allocator (Sec. 3.2, runtime cost
+modelling).
+
+The paper decomposes each linear block into tiles, profiles the cost c_t of a
+tile of every candidate configuration ahead of time, and estimates a block's
+execution time as the serial time of all its tiles over the number of
+parallel workers P (valid when tiles far outnumber workers):
+
+    T = (1 / P) * sum over linear blocks of n_tiles * c_t
+
+Here a worker is one slot of the persistent Group-GEMM grid (two workgroups
+per CU, P = 2 * 256), and a tile is one unsliced output tile of the kernel:
+BM rows x BN channels over the whole K (phase 0 covers gate and up together).
+`profile()` measures c_t on the GPU for every (phase, scheme, configuration)
+as D * P / n_tiles, where D is the duration of a Group-GEMM launch over
+n_tiles >= 4 P equal tiles, at two reduction depths, and fits
+c_t(K) = a + b * K / 128.  The table is stored as JSON beside this module.
+
+    python -m paper_2505_05799_amd.tile_cost --out paper_2505_05799_amd/tile_costs_mi355x.json
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+DEFAULT_TABLE = os.path.join(HERE, "tile_costs_mi355x.json")
+
+N_CFG = 4
+BM = (16, 32, 64, 128)
+BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][configuration]
+P_SLOTS = 512                                        # persistent grid: 2 workgroups x 256 CUs
+
+
+def pick_cfg(m: int, scheme) -> int:
+    """The kernel's run-time choice from the group's rows (w4a4-g128 stops at 64)."""
+    c = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
+    if scheme.a_bits < 16 and scheme.a_group > 0 and c == 3:
+        c = 2
+    return c
+
+
+def n_tiles(m: int, n: int, phase: int, cfg: int) -> int:
+    """Unsliced output tiles of a group with m rows and n output channels."""
+    if m <= 0:
+        return 0
+    return -(-m // BM[cfg]) * -(-n // BN[phase][cfg])
+
+
+class CostTable:
+    """c_t(K) = a + b * K / 128 in ns per tile, per (phase, scheme name, configuration)."""
+
+    def __init__(self, data: dict):
+        self.data = data
+        self.P = int(data.get("P", P_SLOTS))
+
+    @classmethod
+    def load(cls, path: str = DEFAULT_TABLE) -> "CostTable":
+        with open(path) as fh:
+            return cls(json.load(fh))
+
+    def tile_ns(self, phase: int, scheme, cfg: int, k: int) -> float:
+        a, b = self.data["cost"][str(phase)][scheme.name][cfg]
+        return a + b * (k / 128.0)
+
+    def linear_ns(self, m: int, n: int, k: int, phase: int, scheme) -> float:
+        """Serial tile time of one linear block (phase 0: gate and up together)."""
+        if m <= 0:
+            return 0.0
+        c = pick_cfg(m, scheme)
+        return n_tiles(m, n, phase, c) * self.tile_ns(phase, scheme, c, k)
+
+    def block_ns(self, cfg, counts: Sequence[int], schemes) -> List[float]:
+        """Modelled Group-GEMM time per phase, T = sum c_t / P, for a block
+        configuration, routed counts per expert and (gate, up, down) schemes."""
+        out = [0.0, 0.0]
+        for e, sch in enumerate(schemes):
+            m = int(counts[e]) if e < cfg.E else cfg.T
+            F = cfg.F if e < cfg.E else cfg.F_shared
+            out[0] += self.linear_ns(m, F, cfg.H, 0, sch[0])
+            out[1] += self.linear_ns(m, cfg.H, F, 1, sch[2])
+        return [v / self.P for v in out]
+
+
+# ----------------------------------------------------------------------------
+# profiling (GPU)
+# ----------------------------------------------------------------------------
+
+
+def _device_linear(scheme, n: int, k: int, gen):
+    """A QLinear whose codes / scales / zeros are random device tensors of the
+    scheme's formats (timing does not depend on the values)."""
+    import torch
+    from . import workloads as W
+    dev = "cuda"
+    s = scheme
+    if s.w_bits == 16:
+        w = (torch.randn((n, k), generator=gen, device=dev) * 0.02).to(torch.bfloat16).view(torch.int16)
+        return W.QLinear(s, n, k, w)
+    if s.weight_only:
+        qm = (1 << s.w_bits) - 1
+        codes = torch.randint(0, qm + 1, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.uint8)
+        scales = (torch.rand((n, k // 128), generator=gen, device=dev) * 0.01 + 0.001).to(torch.float16)
+        zeros = torch.randint(0, qm + 1, (n, k // 128), generator=gen, device=dev).to(torch.float16)
+        return W.QLinear(s, n, k, codes, scales.view(torch.int16), zeros.view(torch.int16))
+    qm = (1 << (s.w_bits - 1)) - 1
+    codes = torch.randint(-qm, qm + 1, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.int8)
+    if s.w_group > 0:
+        scales = (torch.rand((n, k // 128), generator=gen, device=dev) * 0.01 + 0.001).to(torch.float16)
+        return W.QLinear(s, n, k, codes, scales.view(torch.int16))
+    scales = torch.rand(n, generator=gen, device=dev) * 0.01 + 0.001
+    return W.QLinear(s, n, k, codes, scales)
+
+
+def _probe(scheme, phase: int, k: int, cfgs: Sequence[int], reps: int, n_sets: int = 8, log=print):
+    """Launch durations (ms) of the profiled phase for each configuration."""
+    import torch
+    from . import mxmoe as M
+    from . import workloads as W
+    # the profiled phase has N = 8192 output channels and reduction depth k
+    H, F = (k, 8192) if phase == 0 else (8192, k)
+    E = 64 if phase == 0 else 128
+    T_max = E * 128
+    cfg = W.BlockConfig(f"probe_{scheme.name}_p{phase}_k{k}", T=T_max, H=H, F=F, E=E, k=1, n_shared=0,
+                        F_shared=0, act="bf16", zipf_s=None, alloc=lambda e, r: (scheme,) * 3)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1234 + phase * 7 + k)
+    # n_sets distinct weight sets, dealt to the experts in turn: the working set
+    # (several hundred MB at least) stays well above what the caches hold
+    sets = []
+    for _ in range(n_sets):
+        lins = [_device_linear(scheme, F, H, gen), _device_linear(scheme, F, H, gen), _device_linear(scheme, H, F, gen)]
+        sets.append([M.PackedLinear(q, "bf16") for q in lins])
+    torch.cuda.synchronize()
+    for ps in sets:
+        for p in ps:
+            p.release_sources()
+    blk = W.Block(cfg, 0, np.zeros((0, H), np.uint16), np.zeros((0, 1), np.int32), np.zeros((0, 1), np.float32))
+    mb = M.MoEBlock(blk, T_max=T_max, packed=[sets[e % n_sets] for e in range(E)])
+    x = (torch.randn((T_max, H), generator=gen, device="cuda")).to(torch.bfloat16)
+    out = {}
+    ev = M.PhaseEvents()
+    for c in cfgs:
+        m = BM[c]
+        T = E * m
+        ids = (torch.arange(T, device="cuda", dtype=torch.int32) // m).reshape(T, 1).contiguous()
+        w = torch.ones((T, 1), dtype=torch.float32, device="cuda")
+        xs = x[:T].contiguous()
+        for _ in range(2):
+            mb.forward(xs, ids, w, skip_combine=True)
+        torch.cuda.synchronize()
+        d = []
+        for _ in range(reps):
+            mb.forward(xs, ids, w, skip_combine=True, events=ev)
+            torch.cuda.synchronize()
+            d.append(ev.elapsed_ms()[1 if phase == 0 else 3])
+        nt = E * n_tiles(m, F if phase == 0 else H, phase, c)
+        out[c] = (float(np.median(d)), nt)
+        log(f"[tile_cost] {scheme.name} phase {phase} K {k} cfg {c}: {out[c][0]:.4f} ms over {nt} tiles")
+    del mb, sets
+    torch.cuda.empty_cache()
+    return out
+
+
+def profile(schemes=None, k_lo: int = 1024, k_hi: int = 4096, reps: int = 5, log=print) -> dict:
+    from . import workloads as W
+    schemes = list(schemes or W.ALL_SCHEMES)
+    table = {"P": P_SLOTS, "k_points": [k_lo, k_hi], "unit": "ns per tile; c_t(K) = a + b * K / 128",
+             "cost": {"0": {}, "1": {}}, "raw": {"0": {}, "1": {}}}
+    for s in schemes:
+        cfgs = [0, 1, 2] if (s.a_bits < 16 and s.a_group > 0) else [0, 1, 2, 3]
+        for phase in (0, 1):
+            lo = _probe(s, phase, k_lo, cfgs, reps, log=log)
+            hi = _probe(s, phase, k_hi, cfgs, reps, log=log)
+            ab = []
+            raw = []
+            for c in range(N_CFG):
+                cc = c if c in cfgs else 2
+                c1 = lo[cc][0] * 1e6 * P_SLOTS / lo[cc][1]
+                c2 = hi[cc][0] * 1e6 * P_SLOTS / hi[cc][1]
+                b = (c2 - c1) / ((k_hi - k_lo) / 128.0)
+                a = c1 - b * (k_lo / 128.0)
+                ab.append([round(a, 1), round(b, 2)])
+                raw.append([round(c1, 1), round(c2, 1)])
+            table["cost"][str(phase)][s.name] = ab
+            table["raw"][str(phase)][s.name] = raw
+    return table
+
+
+def measure_block(cfg, schemes=None, reps: int = 10, seed: int = 0):
+    """Measured Group-GEMM launch durations (ms, mean of `reps` forwards) of a
+    block configuration, with its own or the given per-expert schemes; also the
+    whole forward (ms) and the routed counts."""
+    import torch
+    from . import mxmoe as M
+    from . import workloads as W
+    if schemes is not None:
+        sch = list(schemes)
+        cfg = W.BlockConfig(**{**cfg.__dict__, "alloc": lambda e, r: sch[e], "shared_alloc": sch[-1]})
+    blk = W.make_block(cfg, seed=seed)
+    mb = M.MoEBlock(blk)
+    x = M.act_tensor(blk.x, cfg.act)
+    ids = torch.from_numpy(blk.topk_ids.copy()).cuda()
+    w = torch.from_numpy(blk.topk_w.copy()).cuda()
+    for _ in range(3):
+        mb.forward(x, ids, w)
+    torch.cuda.synchronize()
+    ev = [M.PhaseEvents() for _ in range(reps)]
+    for i in range(reps):
+        mb.forward(x, ids, w, events=ev[i])
+    torch.cuda.synchronize()
+    ph = np.array([e.elapsed_ms() for e in ev]).mean(axis=0)
+    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
+    del mb
+    torch.cuda.empty_cache()
+    return {"gate_up_ms": float(ph[1]), "down_ms": float(ph[3]), "forward_ms": float(ph.sum()),
+            "counts": counts.tolist(), "schemes": [tuple(s) for s in W.schemes_of(cfg, seed)]}
+
+
+def validate(table: CostTable, names: Sequence[str], log=print) -> List[dict]:
+    """Modelled against measured Group-GEMM launch time on block configurations."""
+    from . import workloads as W
+    out = []
+    for n in names:
+        cfg = W.CONFIGS[n]
+        meas = measure_block(cfg)
+        model = table.block_ns(cfg, meas["counts"], meas["schemes"])
+        rec = {"workload": n, "gate_up_ms": round(meas["gate_up_ms"], 4), "gate_up_model_ms": round(model[0] / 1e6, 4),
+               "down_ms": round(meas["down_ms"], 4), "down_model_ms": round(model[1] / 1e6, 4)}
+        log(f"[tile_cost] validate {json.dumps(rec)}")
+        out.append(rec)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--out", default=DEFAULT_TABLE)
+    ap.add_argument("--schemes", default="", help="comma-separated scheme names (default: all)")
+    ap.add_argument("--reps", type=int, default=5)
+    ap.add_argument("--validate", default="mixtral,dsv2lite,qwen15_uniform,qwen15_mixed,qwen15_w5a5",
+                    help="workloads whose measured launch times are compared with the model ('' = none)")
+    ap.add_argument("--validate-only", action="store_true", help="keep the stored costs, redo the validation")
+    a = ap.parse_args()
+    from . import workloads as W
+    log = lambda *x: print(*x, file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    if a.validate_only:
+        table = CostTable.load(a.out).data
+    else:
+        schemes = [W.SCHEME_BY_NAME[n] for n in a.schemes.split(",") if n] or None
+        table = profile(schemes, reps=a.reps, log=log)
+        table["command"] = "python -m paper_2505_05799_amd.tile_cost" + (f" --schemes {a.schemes}" if a.schemes else "")
+    names = [n for n in a.validate.split(",") if n]
+    if names:
+        table["validation"] = validate(CostTable(table), names, log=log)
+    with open(a.out, "w") as fh:
+        json.dump(table, fh, indent=1)
+    print(f"[tile_cost] wrote {a.out} in {time.perf_counter() - t0:.0f}s", file=sys.stderr)
+
+
+if __name__ == "__main__":
+    main()
