@@ -66,13 +66,22 @@ typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
  * Accepted combinations:
  *   {16,16,-1,-1,0}  {8,8,-1,-1,1}  {4,4,-1,-1,1}  {N,16,128,-1,0} N=2,3,4,8
  *   {4,4,128,128,1}  w4a4-g128: symmetric 4-bit weights and activations with
- *                    one scale per 128 consecutive k of a channel / a token  */
+ *                    one scale per 128 consecutive k of a channel / a token
+ *   {4,4,32,32,1} with fmt = 1: mxfp4, the OCP Microscaling FP4 format the
+ *                    MI355X matrix cores take natively (the paper's scheme set
+ *                    is whatever the hardware supports, Sec. 3.1): FP4 e2m1
+ *                    elements on both operands with one E8M0 power-of-two
+ *                    scale per 32 consecutive k; activations are encoded at
+ *                    run time (e = floor(log2 amax) - 2, elements rounded to
+ *                    nearest, ties to even, clamped to 6)
+ * All other combinations have fmt = 0.                                       */
 typedef struct {
   int32_t w_bits;
   int32_t a_bits;     /* 16 = weight-only                                       */
-  int32_t w_group;    /* 128, or -1 = per output channel                        */
-  int32_t a_group;    /* 128, or -1 = per token                                 */
-  int32_t symmetric;  /* 1 for w8a8 / w4a4 (per channel or g128), 0 otherwise   */
+  int32_t w_group;    /* 128 or 32 (mxfp4), or -1 = per output channel          */
+  int32_t a_group;    /* 128 or 32 (mxfp4), or -1 = per token                   */
+  int32_t symmetric;  /* 1 for w8a8 / w4a4 (per channel or g128) and mxfp4      */
+  int32_t fmt;        /* 0: integer codes; 1: OCP MX floating point (mxfp4)     */
 } mxmoe_scheme;
 
 /* One linear block y = x W^T with W of shape [n, k] = [out, in].
@@ -89,6 +98,7 @@ typedef struct {
  *   wNg128: n*k*N/8 + (n*k/128)*4   (N + 0.25 bits per weight, Sec. 5.2)
  *   w8a8/w4a4: n*k*b/8 + 4*n
  *   w4a4-g128: n*k/2 + (n*k/128)*4   (fp16 group scale, 4-byte slot per group)
+ *   mxfp4: n*k/2 + n*k/32            (4.25 bits per weight)
  *   w16: 2*n*k
  * Returns 0 if *L is not supported.                                          */
 MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
@@ -97,9 +107,10 @@ MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
  * Group-GEMM streams (weight fragments in MFMA lane order, group metadata next
  * to its codes).  Runs once per weight load.
  *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4/w4a4-g128 int8
- *            [n,k] in [-qmax, qmax]; w16: 16-bit weights [n,k] of `w16_src`.
+ *            [n,k] in [-qmax, qmax]; mxfp4 uint8 [n,k] e2m1 codes 0..15
+ *            (sign in bit 3); w16: 16-bit weights [n,k] of `w16_src`.
  *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4 fp32 [n];
- *            NULL for w16.
+ *            mxfp4 uint8 E8M0 [n, k/32]; NULL for w16.
  *   zeros  : wNg128 fp16 [n, k/128] holding integers in [0, 2^N-1]; else NULL.
  *   w16_src: dtype of 16-bit source weights; converted (RNE) to `act`.
  *   packed : output, mxmoe_packed_bytes(L, act) bytes, 256-byte aligned.
@@ -175,6 +186,8 @@ MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
  *        sum_c qa[m,c]*qw[n,c] (qa from the per-token quantizer);
  *        w4a4-g128 -> fp32 [m, n]: per 128-wide block the exact integer sum
  *        times s_a[m,b]*s_w[n,b], added over the blocks in fp32;
+ *        mxfp4 -> fp32 [m, n]: a encoded as mxfp4 at run time, products of
+ *        the decoded operands accumulated in fp32 by the scaled FP4 MFMA;
  *        other schemes -> fp32 [m, n] with fp32 accumulation.               */
 MXMOE_API mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
                                   int32_t m, const void* a, void* out, void* workspace,
@@ -292,6 +305,11 @@ typedef struct {
   size_t hsg;           /* fp32 [T*k, F/128]: group scales of routed h rows
                            for w4a4-g128 down (codes in hq), else -1         */
   size_t hsg_shared;    /* fp32 [n_shared*T, F_shared/128], else -1          */
+  size_t xqmx, xsmx;    /* uint8 [T, H/2] e2m1 codes, uint8 [T, H/32] E8M0: x
+                           for mxfp4 gate|up (else -1)                      */
+  size_t hqmx, hsmx;    /* uint8 [T*k, F/2], [T*k, F/32]: routed h for mxfp4
+                           down (else -1)                                   */
+  size_t hqmx_shared, hsmx_shared; /* the same for shared h (else -1)        */
   size_t router_ids;    /* int32 [T, k]: ids chosen by the router front-end  */
   size_t router_w;      /* fp32 [T, k]: their gate weights                   */
   size_t shared_w;      /* fp32 [T, n_shared]: sigmoid shared gates (-1 if no

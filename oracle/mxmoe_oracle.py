@@ -19,6 +19,10 @@ operands the GPU receives (codes, scales, zeros - never the packed layout):
   softmax probabilities of the token's k largest logits (optionally
   renormalised over those k); a shared expert's output may be scaled by a
   per-token sigmoid gate (Qwen-MoE style shared experts).
+* MXFP4 (the OCP Microscaling format the MI355X matrix cores take natively; the
+  paper's scheme set S is whatever the hardware supports, Sec. 3.1): a value is
+  an FP4 e2m1 element times a power-of-two scale shared by 32 consecutive
+  values along K; activations get the same encoding at run time.
 * Sec. 4.2.2 (end): activations of w8a8 / w4a4 linears are quantized dynamically
   at run time, per token (a_gsize = -1 in the W5A5 allocation table), with the
   fp32 recipe of :func:`act_quant`.
@@ -169,11 +173,59 @@ def dequant(lin, act: str) -> np.ndarray:
         sc = lin.scales.astype(np.float64)[..., None]
         z = lin.zeros.astype(np.float64)[..., None]
         return (sc * (q - z)).reshape(lin.n, lin.k)
+    if getattr(s, "fmt", 0) == 1:  # MXFP4: e2m1 element times 2^(E8M0 - 127) of its 32-block
+        return _mx_values(lin.codes, lin.scales, s.w_group)
     if s.w_group > 0:  # symmetric groups (w4a4-g128): code times its group's scale
         g = s.w_group
         q = lin.codes.astype(np.float64).reshape(lin.n, lin.k // g, g)
         return (q * lin.scales.astype(np.float64)[..., None]).reshape(lin.n, lin.k)
     return lin.codes.astype(np.float64) * lin.scales.astype(np.float64)[:, None]
+
+
+# FP4 e2m1: sign bit 3, two exponent bits (bias 1), one mantissa bit
+_E2M1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def _mx_values(codes: np.ndarray, exps: np.ndarray, block: int) -> np.ndarray:
+    c = np.asarray(codes, dtype=np.int64)
+    v = _E2M1[c & 7] * np.where(c & 8, -1.0, 1.0)
+    r, k = v.shape
+    sc = np.exp2(np.asarray(exps, dtype=np.float64) - 127.0)
+    return (v.reshape(r, k // block, block) * sc[..., None]).reshape(r, k)
+
+
+def _mx_exponent(amax: np.ndarray) -> np.ndarray:
+    """Shared exponent floor(log2(amax)) - 2 in [-127, 127]; -127 for amax = 0."""
+    e = np.full(np.shape(amax), -127, dtype=np.int64)
+    nz = amax > 0
+    e[nz] = np.floor(np.log2(amax[nz])).astype(np.int64) - 2
+    return np.clip(e, -127, 127)
+
+
+def _e2m1_code(x: np.ndarray) -> np.ndarray:
+    """Magnitude code (0..7) of the e2m1 value nearest to x >= 0; an exact tie
+    takes the even code; beyond 6 the code of 6."""
+    d = np.abs(np.asarray(x)[..., None] - _E2M1)
+    cand = d == d.min(axis=-1, keepdims=True)
+    even = cand & (np.arange(8) % 2 == 0)
+    code = np.where(even.any(axis=-1), even.argmax(axis=-1), cand.argmax(axis=-1))
+    return np.where(np.asarray(x) > 6.0, 7, code)
+
+
+def mx_quant(a: np.ndarray, block: int = 32) -> Tuple[np.ndarray, np.ndarray]:
+    """MXFP4 encoding of rows of fp32 values, per `block` along the row (OCP MX):
+    shared exponent e = floor(log2(amax)) - 2 (2 = the largest e2m1 exponent),
+    clamped to [-127, 127], -127 for an all-zero block; element = the e2m1
+    value nearest to a / 2^e (ties to the even code; beyond 6 it is 6), sign
+    kept unless the magnitude is 0.  Division by 2^e is exact.
+    Returns codes uint8 [rows, cols] and E8M0 bytes uint8 [rows, cols/block]."""
+    a = np.asarray(a, dtype=np.float32).astype(np.float64)
+    r, k = a.shape
+    v = a.reshape(r, k // block, block)
+    e = _mx_exponent(np.abs(v).max(axis=2))
+    code = _e2m1_code(np.abs(v) / np.exp2(e.astype(np.float64))[..., None])
+    code = np.where((v < 0) & (code > 0), code | 8, code)
+    return code.reshape(r, k).astype(np.uint8), (e + 127).astype(np.uint8)
 
 
 # ----------------------------------------------------------------------------
@@ -232,6 +284,10 @@ def linear(a: np.ndarray, lin, act: str, w_deq: Optional[np.ndarray] = None,
     ``return_int`` the exact integer accumulators are returned instead.
     """
     s = lin.scheme
+    if getattr(s, "fmt", 0) == 1:
+        # MXFP4: both operands decoded exactly, the product summed in fp64
+        qa, ea = mx_quant(a.astype(np.float32), s.a_group)
+        return _mx_values(qa, ea, s.a_group) @ dequant(lin, act).T
     if s.a_bits < 16 and s.a_group > 0:
         # w4a4-g128: per 128-wide block b, the exact integer dot of the block's
         # codes times s_a[m, b] * s_w[n, b], summed over the blocks in fp64
@@ -279,6 +335,9 @@ _EPS_EPI = 2.0 ** -20         # relative to |h|, SiLU + product in fp32
 
 def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
                    w_deq: Optional[np.ndarray]) -> np.ndarray:
+    if getattr(lin.scheme, "fmt", 0) == 1:
+        qa, ea = mx_quant(a.astype(np.float32), lin.scheme.a_group)
+        return _EPS_FLOAT_ACC * (np.abs(_mx_values(qa, ea, lin.scheme.a_group)) @ np.abs(dequant(lin, act)).T)
     if lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
         # fp32 running sum of block products: bounded like an fp32-accumulated GEMM
         # on the dequantized operands
@@ -303,6 +362,8 @@ def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
     per quantization block (the whole row per token, or each 128-wide group).
     Returns slack [m, n] >= |effect on the down output| of every such move.
     """
+    if getattr(lin.scheme, "fmt", 0) == 1:
+        return _down_slack_mx(h64, dh, hb, lin, act)
     qmax = _qmax(lin.scheme.a_bits)
     m, F = h64.shape
     g = lin.scheme.a_group if lin.scheme.a_group > 0 else F
@@ -340,6 +401,36 @@ def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
     QD = ((qabs + dq) * ds[:, None]).reshape(m, F)
     wabs = np.abs(dequant(lin, act))
     return (DQ + QD) @ wabs.T
+
+
+def _down_slack_mx(h64, dh, hb, lin, act):
+    """The slack of an MXFP4 down projection.  Where the GPU's rounded h can
+    differ from the oracle's (h64 within dh of a rounding midpoint), the
+    GPU's value v of an element lies between the rounded corners lo and hi,
+    and its block's shared exponent between those of the smallest and largest
+    possible block maxima.  For a fixed exponent the decoded value is monotone
+    in v, so it lies between the decoded corners under one of those exponents."""
+    m, F = h64.shape
+    g = lin.scheme.a_group
+    nb = F // g
+    lo = round_to_act(h64 - dh, act).reshape(m, nb, g)
+    hi = round_to_act(h64 + dh, act).reshape(m, nb, g)
+    moved = (lo != hi).any(axis=2)
+    if not moved.any():
+        return np.zeros((m, lin.n))
+    q0, e0 = mx_quant(hb.astype(np.float32), g)
+    d0 = _mx_values(q0, e0, g).reshape(m, nb, g)
+    same = np.sign(lo) == np.sign(hi)
+    e_lo = _mx_exponent(np.where(same, np.minimum(np.abs(lo), np.abs(hi)), 0.0).max(axis=2))
+    e_hi = _mx_exponent(np.maximum(np.abs(lo), np.abs(hi)).max(axis=2))
+    dev = np.zeros((m, nb, g))
+    for step in range(int((e_hi - e_lo).max()) + 1):
+        e = np.minimum(e_lo + step, e_hi).astype(np.float64)[..., None]
+        for corner in (lo, hi):
+            mag = _E2M1[_e2m1_code(np.abs(corner) / np.exp2(e))]
+            dev = np.maximum(dev, np.abs(np.sign(corner) * mag * np.exp2(e) - d0))
+    dev *= moved[..., None]
+    return dev.reshape(m, F) @ np.abs(dequant(lin, act)).T
 
 
 def _expert_mlp(a: np.ndarray, lins: Sequence, act: str, want_slack: bool):
@@ -499,12 +590,13 @@ _TILE_FIXED_PS = 2.0e6
 
 def _tile_cost(bm: int, bn: int, nl: int, scheme, kk: int, split: int, mt: int, nt: int) -> int:
     is_int = scheme.a_bits < 16
+    mx = getattr(scheme, "fmt", 0) == 1
     wbytes = float(nl * bn * kk * scheme.w_bits) / 8.0
-    abytes = float(bm) * kk * (1.0 if is_int else 2.0)
+    abytes = float(bm) * kk * (0.5 if mx else (1.0 if is_int else 2.0))
     pbytes = 8.0 * bm * bn * nl if split > 1 else 0.0
     flops = 2.0 * nl * bm * bn * kk
     t_mem = (wbytes / max(mt, 1) + abytes / max(nt, 1) + pbytes) * 32.0
-    t_mma = flops * 1000.0 / (19531.0 if is_int else 9766.0)
+    t_mma = flops * 1000.0 / (39062.0 if mx else (19531.0 if is_int else 9766.0))
     c = max(t_mem, t_mma) + _TILE_FIXED_PS
     return int(min(c, 2.0e9))
 

@@ -14,6 +14,9 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // scheme -> micro-kernel kind, -1 if unsupported
 int scheme_kind(const mxmoe_scheme& s) {
+  if (s.fmt == 1)  // OCP MX: FP4 e2m1 on both operands, E8M0 scale per 32
+    return (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 32 && s.a_group == 32 && s.symmetric == 1) ? K_MXFP4 : -1;
+  if (s.fmt != 0) return -1;
   if (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 128 && s.a_group == 128 && s.symmetric == 1) return K_W4A4G;
   if (s.a_group != -1) return -1;
   if (s.w_bits == 16 && s.a_bits == 16 && s.w_group == -1 && s.symmetric == 0) return K_W16;
@@ -32,7 +35,7 @@ int scheme_kind(const mxmoe_scheme& s) {
 
 bool same_scheme(const mxmoe_scheme& a, const mxmoe_scheme& b) {
   return a.w_bits == b.w_bits && a.a_bits == b.a_bits && a.w_group == b.w_group && a.a_group == b.a_group &&
-         a.symmetric == b.symmetric;
+         a.symmetric == b.symmetric && a.fmt == b.fmt;
 }
 
 bool valid_dtype(int d) { return d == MXMOE_F16 || d == MXMOE_BF16; }
@@ -61,6 +64,7 @@ struct BlockInfo {
   bool any_x8 = false, any_x4 = false, any_hq = false, any_hq_sh = false;
   bool rs_x = false, rs_h = false, rs_hsh = false;  // row sums of x / h / h_shared needed (bf16)
   bool any_x4g = false, any_hg = false, any_hg_sh = false;  // w4a4-g128 gate|up, routed / shared down
+  bool any_xmx = false, any_hmx = false, any_hmx_sh = false;  // mxfp4 gate|up, routed / shared down
   int kinds[kMaxG][3];
 };
 
@@ -81,6 +85,9 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
   bi->act = B->act;
   bi->G = bi->E + bi->nsh;
   bi->any_x8 = bi->any_x4 = bi->any_hq = bi->any_hq_sh = false;
+  bi->rs_x = bi->rs_h = bi->rs_hsh = false;
+  bi->any_x4g = bi->any_hg = bi->any_hg_sh = false;
+  bi->any_xmx = bi->any_hmx = bi->any_hmx_sh = false;
   if (bi->G > kMaxG) return MXMOE_ERR_UNSUPPORTED;
   for (int g = 0; g < bi->G; ++g) {
     const mxmoe_scheme* s = B->scheme + 3 * g;
@@ -96,6 +103,8 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
     if (kg == K_W4A4) bi->any_x4 = true;
     if (kg == K_W4A4G) bi->any_x4g = true;
     if (bi->kinds[g][2] == K_W4A4G) (sh ? bi->any_hg_sh : bi->any_hg) = true;
+    if (kg == K_MXFP4) bi->any_xmx = true;
+    if (bi->kinds[g][2] == K_MXFP4) (sh ? bi->any_hmx_sh : bi->any_hmx) = true;
     if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(kg)) bi->rs_x = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(bi->kinds[g][2])) (sh ? bi->rs_hsh : bi->rs_h) = true;
@@ -149,6 +158,12 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.xs4g = bi.any_x4g ? take(4 * (size_t)T * (bi.H / 128)) : kNone;
   L.hsg = bi.any_hg ? take(4 * P * (bi.F / 128)) : kNone;
   L.hsg_shared = bi.any_hg_sh ? take(4 * (size_t)bi.nsh * T * (bi.Fsh / 128)) : kNone;
+  L.xqmx = bi.any_xmx ? take((size_t)T * bi.H / 2) : kNone;
+  L.xsmx = bi.any_xmx ? take((size_t)T * bi.H / 32) : kNone;
+  L.hqmx = bi.any_hmx ? take(P * bi.F / 2) : kNone;
+  L.hsmx = bi.any_hmx ? take(P * bi.F / 32) : kNone;
+  L.hqmx_shared = bi.any_hmx_sh ? take((size_t)bi.nsh * T * bi.Fsh / 2) : kNone;
+  L.hsmx_shared = bi.any_hmx_sh ? take((size_t)bi.nsh * T * bi.Fsh / 32) : kNone;
   L.rids = take(4 * P);
   L.rw = take(4 * P);
   L.shw = bi.nsh ? take(4 * (size_t)T * bi.nsh) : kNone;
@@ -279,6 +294,10 @@ LinWs lin_layout(int kd, int m, int n, int k) {
     w.aq = o; o = align256(o + (size_t)m * k);
     w.as = o; o = align256(o + 4 * (size_t)m * (kd == K_W4A4G ? k / 128 : 1));
   }
+  if (kind_is_mx(kd)) {  // e2m1 codes and E8M0 bytes of the input
+    w.aq = o; o = align256(o + (size_t)m * k / 2);
+    w.as = o; o = align256(o + (size_t)m * k / 32);
+  }
   // row sums of the input per 128-wide k block (used with bf16 activations)
   if (kind_is_magic(kd)) { w.rsa = o; o = align256(o + 4 * (size_t)m * (k / 128)); }
   w.total = o;
@@ -336,6 +355,13 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; }
     else if (kd == K_W4A4G) { ga.xq4g = aq; ga.xs4g = as; }
     else { ga.xq4 = aq; ga.xs4 = as; }
+  }
+  if (kind_is_mx(kd)) {
+    uint8_t* aq = at<uint8_t>(workspace, w.aq);
+    uint8_t* ae = at<uint8_t>(workspace, w.as);
+    if (launch_act_quant_mx(a, act, m, L->k, L->k, aq, ae, stream) != hipSuccess) return MXMOE_ERR_HIP;
+    ga.xqmx = aq;
+    ga.xsmx = ae;
   }
   if (act == MXMOE_BF16 && kind_is_magic(kd)) {
     float* rs = at<float>(workspace, w.rsa);
@@ -424,6 +450,12 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->xs4g = L.xs4g;
   out->hsg = L.hsg;
   out->hsg_shared = L.hsg_shared;
+  out->xqmx = L.xqmx;
+  out->xsmx = L.xsmx;
+  out->hqmx = L.hqmx;
+  out->hsmx = L.hsmx;
+  out->hqmx_shared = L.hqmx_shared;
+  out->hsmx_shared = L.hsmx_shared;
   out->router_ids = L.rids;
   out->router_w = L.rw;
   out->shared_w = L.shw;
@@ -517,6 +549,9 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if (bi.any_x4g)
     MX_CHECK(launch_act_quant_g128(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4g),
                                    at<float>(workspace, L.xs4g), stream));
+  if (bi.any_xmx)
+    MX_CHECK(launch_act_quant_mx(x, bi.act, T, bi.H, bi.H, at<uint8_t>(workspace, L.xqmx), at<uint8_t>(workspace, L.xsmx),
+                                 stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
                            at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
                            at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
@@ -563,19 +598,31 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.hsg_shared = at<float>(workspace, L.hsg_shared);
   ga.rsh = at<float>(workspace, L.rsh);
   ga.rsh_shared = at<float>(workspace, L.rsh_shared);
+  ga.xqmx = at<uint8_t>(workspace, L.xqmx);
+  ga.xsmx = at<uint8_t>(workspace, L.xsmx);
+  ga.hqmx = at<uint8_t>(workspace, L.hqmx);
+  ga.hsmx = at<uint8_t>(workspace, L.hsmx);
+  ga.hqmx_shared = at<uint8_t>(workspace, L.hqmx_shared);
+  ga.hsmx_shared = at<uint8_t>(workspace, L.hsmx_shared);
   MX_EVENT(1);
   MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));
   MX_EVENT(3);
   MX_EVENT(4);
-  if (bi.any_hq)
+  if (bi.any_hq || bi.any_hmx)
     MX_CHECK(launch_hquant_routed(ga.h, bi.act, T * bi.k, bi.F, offsets, bi.E, down_qmax, at<int8_t>(workspace, L.hq),
-                                  at<float>(workspace, L.hs), at<float>(workspace, L.hsg), stream));
+                                  at<float>(workspace, L.hs), at<float>(workspace, L.hsg), at<uint8_t>(workspace, L.hqmx),
+                                  at<uint8_t>(workspace, L.hsmx), stream));
   for (int j = 0; j < bi.nsh; ++j) {
-    const int qm = kind_qmax(bi.kinds[bi.E + j][2]);
-    if (!qm) continue;
     const size_t rows = (size_t)j * T;
     const void* hsrc = reinterpret_cast<const uint8_t*>(ga.h_shared) + rows * bi.Fsh * 2;
+    if (bi.kinds[bi.E + j][2] == K_MXFP4) {
+      MX_CHECK(launch_act_quant_mx(hsrc, bi.act, T, bi.Fsh, bi.Fsh, at<uint8_t>(workspace, L.hqmx_shared) + rows * bi.Fsh / 2,
+                                   at<uint8_t>(workspace, L.hsmx_shared) + rows * bi.Fsh / 32, stream));
+      continue;
+    }
+    const int qm = kind_qmax(bi.kinds[bi.E + j][2]);
+    if (!qm) continue;
     int8_t* hq = at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh;
     if (bi.kinds[bi.E + j][2] == K_W4A4G)
       MX_CHECK(launch_act_quant_g128(hsrc, bi.act, T, bi.Fsh, bi.Fsh, qm, hq,

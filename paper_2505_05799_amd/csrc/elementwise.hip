@@ -193,6 +193,59 @@ __device__ inline void quant_row_groups(const uint4* __restrict__ row, int cols,
   }
 }
 
+// MXFP4 encoding of one row (OCP MX: FP4 e2m1 elements, one E8M0 scale per 32
+// consecutive values), one wavefront: a lane takes a whole 32-wide block (64
+// bytes) per step.  Shared exponent e = floor(log2(amax)) - 2, clamped to
+// [-127, 127] (-127 for an all-zero block); element = nearest e2m1 value to
+// |a| 2^-e (an exact power-of-two scaling of a 16-bit value), ties to the even
+// code, clamped to 6; the sign is kept unless the magnitude code is 0.
+// Element i of the block is nibble i of its 16 output bytes.
+__device__ inline uint32_t e2m1_mag(float x) {
+  return (uint32_t)(x > 0.25f) + (uint32_t)(x >= 0.75f) + (uint32_t)(x > 1.25f) + (uint32_t)(x >= 1.75f) +
+         (uint32_t)(x > 2.5f) + (uint32_t)(x >= 3.5f) + (uint32_t)(x > 5.0f);
+}
+__device__ inline void quant_row_mx(const uint4* __restrict__ row, int cols, int act, uint4* __restrict__ codes,
+                                    uint8_t* __restrict__ exps) {
+  const int lane = threadIdx.x & 63, nb = cols >> 5;
+  for (int b = lane; b < nb; b += 64) {
+    float v[32];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint4 u = row[4 * b + c];
+      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint16_t lo = (uint16_t)(w[i] & 0xFFFFu), hi = (uint16_t)(w[i] >> 16);
+        v[8 * c + 2 * i] = act == MXMOE_BF16 ? __uint_as_float((uint32_t)lo << 16) : (float)__builtin_bit_cast(_Float16, lo);
+        v[8 * c + 2 * i + 1] = act == MXMOE_BF16 ? __uint_as_float((uint32_t)hi << 16) : (float)__builtin_bit_cast(_Float16, hi);
+      }
+    }
+    float amax = 0.f;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) amax = fmaxf(amax, fabsf(v[i]));
+    int e = amax > 0.f ? (int)((__float_as_uint(amax) >> 23) & 0xFFu) - 127 - 2 : -127;
+    e = e < -127 ? -127 : (e > 127 ? 127 : e);
+    const float inv = __builtin_amdgcn_ldexpf(1.0f, -e);
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      uint32_t c = e2m1_mag(fabsf(v[i]) * inv);
+      if (v[i] < 0.f && c) c |= 8u;
+      o[i >> 3] |= c << (4 * (i & 7));
+    }
+    codes[b] = make_uint4(o[0], o[1], o[2], o[3]);
+    exps[b] = (uint8_t)(e + 127);
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) act_quant_mx_kernel(const void* a, int act, int rows, int cols,
+                                                                int64_t ld, uint8_t* codes, uint8_t* exps) {
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  quant_row_mx(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a) + r * ld), cols, act,
+               reinterpret_cast<uint4*>(codes + r * (cols >> 1)), exps + r * (cols >> 5));
+}
+
 __global__ void __launch_bounds__(kThreads) act_quant_g128_kernel(const void* a, int act, int rows, int cols,
                                                                   int64_t ld, int qmax, int8_t* codes,
                                                                   float* scales) {
@@ -224,7 +277,8 @@ template <int NC, int W>
 __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, int act, int P, int F,
                                                                  const int32_t* __restrict__ offsets, int E,
                                                                  const int32_t* __restrict__ down_qmax,
-                                                                 int8_t* hq, float* hs, float* hsg) {
+                                                                 int8_t* hq, float* hs, float* hsg, uint8_t* hqmx,
+                                                                 uint8_t* hsmx) {
   __shared__ int32_t s_off[kMaxE + 1];
   __shared__ uint32_t red[kThreads / 64];
   for (int i = threadIdx.x; i <= E; i += kThreads) s_off[i] = offsets[i];
@@ -238,6 +292,12 @@ __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, 
   }
   const int qm = down_qmax[lo];
   if (qm == 0) return;
+  if (qm & kDownQMX) {  // MXFP4 down projection: one wavefront per row
+    if (W == 1 || threadIdx.x < 64)
+      quant_row_mx(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F, act,
+                   reinterpret_cast<uint4*>(hqmx + (int64_t)r * (F >> 1)), hsmx + (int64_t)r * (F >> 5));
+    return;
+  }
   if (qm & kDownQGroup) {  // per-128-group scales: one wavefront per row
     if (W == 1 || threadIdx.x < 64)
       quant_row_groups(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F, act,
@@ -405,13 +465,24 @@ hipError_t launch_act_quant_g128(const void* a, int act, int rows, int cols, int
   return hipGetLastError();
 }
 
+hipError_t launch_act_quant_mx(const void* a, int act, int rows, int cols, int64_t ld, uint8_t* codes, uint8_t* exps,
+                               hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15) || (reinterpret_cast<uintptr_t>(codes) & 15) || cols % 128 || ld % 8)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(act_quant_mx_kernel, dim3((rows + kRowsPerBlock - 1) / kRowsPerBlock), dim3(kThreads), 0, s, a,
+                     act, rows, cols, ld, codes, exps);
+  return hipGetLastError();
+}
+
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets, int E,
-                                const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg, hipStream_t s) {
+                                const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg, uint8_t* hqmx,
+                                uint8_t* hsmx, hipStream_t s) {
   if (P <= 0) return hipSuccess;
   if ((reinterpret_cast<uintptr_t>(h) & 15) || (reinterpret_cast<uintptr_t>(hq) & 7) || F % 8 || E > kMaxE)
     return hipErrorInvalidValue;
   if (F % 128) return hipErrorInvalidValue;
-  return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs, hsg);
+  return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs, hsg, hqmx, hsmx);
 }
 
 hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int nsh, int H, int act,

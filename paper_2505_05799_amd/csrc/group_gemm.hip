@@ -127,7 +127,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     }
     if (raw_m < 0) {
       const int dk = experts[g].lin[2].kind;
-      down_qmax[g] = kind_qmax(dk) | (dk == K_W4A4G ? kDownQGroup : 0);
+      down_qmax[g] = dk == K_MXFP4 ? kDownQMX : (kind_qmax(dk) | (dk == K_W4A4G ? kDownQGroup : 0));
     }
   }
   if (tid < 2) s_ng[tid] = 0;

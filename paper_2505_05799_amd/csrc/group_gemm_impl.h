@@ -28,6 +28,8 @@
 //
 // Numerics per scheme (every result is exact up to fp32 accumulation):
 //   w16   : 16-bit MFMA, fp32 accumulation.
+//   mxfp4 : scaled FP4 MFMA (e2m1 x e2m1 with an E8M0 scale per 32 on both
+//           operands), fp32 accumulation.
 //   w8a8  : int8 MFMA, exact int32 sums, then fp32 (acc * s_a) * s_w.
 //   w4a4  : nibbles widened to int8 as 16*q, int8 MFMA, exact sum / 16.
 //   wNg128: the 16-bit operand is formed exactly.  bf16 activations: a packed
@@ -59,6 +61,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kThreads = 256;
 constexpr int kPhaseRaw = 2;
@@ -75,11 +78,13 @@ __host__ __device__ constexpr int cfg_nf(int c, int phase) {
 }
 __host__ __device__ constexpr int cfg_bm(int c) { return 16 * cfg_mf(c); }
 __host__ __device__ constexpr int cfg_bn(int c, int phase) { return 64 * cfg_nf(c, phase); }
-// Tile configuration of a group from its rows; w4a4-g128 groups stop at 64-row
-// tiles (their per-group rescale keeps a partial sum next to every accumulator).
+// Tile configuration of a group from its rows; w4a4-g128 and mxfp4 groups stop
+// at 64-row tiles (the per-group rescale keeps a partial sum next to every
+// accumulator; the scaled FP4 operands add their scale registers), which keeps
+// the whole kernel within its register budget.
 __host__ __device__ inline int pick_cfg(int m, int kind) {
   const int c = m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
-  return (kind == K_W4A4G && c == CFG_L) ? CFG_M : c;
+  return ((kind == K_W4A4G || kind == K_MXFP4) && c == CFG_L) ? CFG_M : c;
 }
 
 // Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
@@ -349,27 +354,33 @@ __device__ inline int pop_start(const TileQueue& Q, const Smem& sm, int qi) {
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // Stage one k block of BM rows into act[buf] with direct global->LDS loads.
-// 16-bit rows are 256 bytes (16 chunks, chunk c stored at c ^ (r & 15)), int8
-// rows 128 bytes (8 chunks, chunk c stored at c ^ ((r >> 1) & 7)); one
-// wavefront instruction fills 1 KB (4 or 8 rows).  Wavefront w fills blocks
-// w, w + 4, ...; its lanes' source offsets (row start + swizzled chunk, at k
-// block 0) are computed once per tile.
-template <bool INT, int BM> struct StageOffs {
-  static constexpr int RB = INT ? 128 : 256;
+// A row's k block is RB bytes: 256 for 16-bit rows (16 chunks, chunk c stored
+// at c ^ (r & 15)), 128 for int8 codes (8 chunks, at c ^ ((r >> 1) & 7)), 64
+// for FP4 codes (4 chunks, at c ^ ((r >> 2) & 3)), so that the 16 rows one
+// fragment read touches hit distinct banks.  One wavefront instruction fills
+// 1 KB (4, 8 or 16 rows).  Wavefront w fills blocks w, w + 4, ...; its lanes'
+// source offsets (row start + swizzled chunk, at k block 0) are computed once
+// per tile.
+template <int KD> constexpr int stage_rb() { return kind_is_mx(KD) ? 64 : (kind_is_int(KD) ? 128 : 256); }
+template <int RB> __device__ constexpr int stage_swz(int c, int r) {
+  return RB == 256 ? (c ^ (r & 15)) : (RB == 128 ? (c ^ ((r >> 1) & 7)) : (c ^ ((r >> 2) & 3)));
+}
+template <int RB_, int BM> struct StageOffs {
+  static constexpr int RB = RB_;
   static constexpr int NBLK = BM * RB / 1024;
   static constexpr int PER_WAVE = (NBLK + 3) / 4;
   uint32_t off[PER_WAVE];
 };
 
-template <bool INT, int BM>
-__device__ inline void stage_offsets(StageOffs<INT, BM>& so, const Smem& sm, int64_t row_bytes, int wave, int lane) {
-  using S = StageOffs<INT, BM>;
+template <int RB, int BM>
+__device__ inline void stage_offsets(StageOffs<RB, BM>& so, const Smem& sm, int64_t row_bytes, int wave, int lane) {
+  using S = StageOffs<RB, BM>;
 #pragma unroll
   for (int i = 0; i < S::PER_WAVE; ++i) {
     const int blk = wave + 4 * i;
-    const int r = (blk < S::NBLK ? blk : 0) * (1024 / S::RB) + lane / (S::RB / 16);
-    const int p = lane % (S::RB / 16);
-    const int cc = INT ? (p ^ ((r >> 1) & 7)) : (p ^ (r & 15));
+    const int r = (blk < S::NBLK ? blk : 0) * (1024 / RB) + lane / (RB / 16);
+    const int p = lane % (RB / 16);
+    const int cc = stage_swz<RB>(p, r);
     so.off[i] = (uint32_t)((int64_t)sm.rowsrc[r] * row_bytes + cc * 16);
   }
 }
@@ -381,10 +392,19 @@ __device__ inline void stage_offsets(StageOffs<INT, BM>& so, const Smem& sm, int
 // loads, weight prefetch included, before the first one); completion is
 // waited for explicitly (wait_vmem) before the barrier that publishes the
 // stage.
+// The base address is uniform by construction; it passes through
+// readfirstlane so that the scalar operand never depends on the compiler
+// proving that (in large instantiations it may keep the value in a VGPR).
+__device__ inline const uint8_t* uniform_ptr(const uint8_t* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
 __device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "v"(voff), "s"(uniform_ptr(base)), "s"(lds_addr)
                : "memory", "m0");
 }
 
@@ -414,10 +434,10 @@ template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& 
   sm.entry.x = -1;  // only the group field is read when no tile is left
 }
 
-template <bool INT, int BM>
-__device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<INT, BM>& so, int kb,
+template <int RB, int BM>
+__device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<RB, BM>& so, int kb,
                                   int wave) {
-  using S = StageOffs<INT, BM>;
+  using S = StageOffs<RB, BM>;
   const uint8_t* bk = base + (int64_t)kb * S::RB;  // uniform
   const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)sm.act[buf]);
 #pragma unroll
@@ -427,9 +447,8 @@ __device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const 
   }
 }
 
-template <bool INT> __device__ inline u32x4 act_frag(const Smem& sm, int buf, int r, int cc) {
-  const int pos = INT ? (cc ^ ((r >> 1) & 7)) : (cc ^ (r & 15));
-  return *reinterpret_cast<const u32x4*>(sm.act[buf] + r * (INT ? 128 : 256) + pos * 16);
+template <int RB> __device__ inline u32x4 act_frag(const Smem& sm, int buf, int r, int cc) {
+  return *reinterpret_cast<const u32x4*>(sm.act[buf] + r * RB + stage_swz<RB>(cc, r) * 16);
 }
 
 // Row sums of a stage (bias-dequantized kinds with bf16 activations): one
@@ -439,7 +458,7 @@ template <bool INT> __device__ inline u32x4 act_frag(const Smem& sm, int buf, in
 __device__ inline void lds_dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
                :
-               : "v"(voff), "s"(base), "s"(lds_addr)
+               : "v"(voff), "s"(uniform_ptr(base)), "s"(lds_addr)
                : "memory", "m0");
 }
 template <int BM>
@@ -462,8 +481,10 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr bool MAGIC = WONLY && KD != K_W8G;          // 2/3/4-bit codes
   constexpr bool RSUM = MAGIC && ACT == MXMOE_BF16;     // bias removed through row sums
   constexpr bool GSC = KD == K_W4A4G;                   // per-128-group activation and weight scales
+  constexpr bool MX = kind_is_mx(KD);                   // FP4 e2m1 operands with E8M0 scales per 32
   constexpr bool GMETA = kind_has_gmeta(KD);            // group metadata after each fragment block
-  constexpr bool RSLOAD = RSUM || GSC;                  // a per-row value per k block rides with the stage
+  constexpr bool RSLOAD = RSUM || GSC || MX;            // a per-row value per k block rides with the stage
+  constexpr int RB = stage_rb<KD>();                    // activation bytes per row and k block
   constexpr int BM = 16 * MF;
   constexpr int BN = 64 * NF;
   constexpr int LB = lane_bytes(KD);
@@ -498,7 +519,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 
   const uint8_t* abase;
   const float* ascale = nullptr;
-  if constexpr (INT) {
+  if constexpr (MX) {
+    abase = PHASE == 1 ? (shared ? a.hqmx_shared : a.hqmx) : a.xqmx;
+  } else if constexpr (INT) {
     const int8_t* qb;
     if constexpr (PHASE == 1) { qb = shared ? a.hq_shared : a.hq; ascale = shared ? a.hs_shared : a.hs; }
     else {
@@ -542,17 +565,20 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     sm.rowgw[tid] = gw;
     sm.rowscale[tid] = sc;
   }
-  const int64_t row_bytes = (int64_t)K * (INT ? 1 : 2);
+  const int64_t row_bytes = MX ? (int64_t)K / 2 : (int64_t)K * (INT ? 1 : 2);
   __syncthreads();
-  StageOffs<INT, BM> soffs;
-  stage_offsets<INT, BM>(soffs, sm, row_bytes, wave, lane);
+  StageOffs<RB, BM> soffs;
+  stage_offsets<RB, BM>(soffs, sm, row_bytes, wave, lane);
   // row sums of the tile's activation rows per k block (bias-dequantized
   // kinds, bf16): x rows in the gate|up phase, h rows in the down phase
   const float* rsbase = nullptr;
   uint32_t rsoff = 0;
   if constexpr (RSLOAD) {
-    // row sums (bias-dequantized kinds) or activation group scales (w4a4-g128)
-    if constexpr (GSC) rsbase = PHASE == 1 ? (shared ? a.hsg_shared : a.hsg) : a.xs4g;
+    // row sums (bias-dequantized kinds), activation group scales (w4a4-g128)
+    // or the four E8M0 bytes of a row's k block (mxfp4)
+    if constexpr (MX)
+      rsbase = reinterpret_cast<const float*>(PHASE == 1 ? (shared ? a.hsmx_shared : a.hsmx) : a.xsmx);
+    else if constexpr (GSC) rsbase = PHASE == 1 ? (shared ? a.hsg_shared : a.hsg) : a.xs4g;
     else rsbase = PHASE == 1 ? (shared ? a.rsh_shared : a.rsh) : a.rsx;
     const int r = wave * 64 + lane;
     rsoff = (uint32_t)sm.rowsrc[r < BM ? r : 0] * (uint32_t)kblocks * 4u;
@@ -561,7 +587,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // ---- accumulators and weight streams
   typedef typename std::conditional<INT && !GSC, i32x4, f32x4>::type AccT;
   typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
-  constexpr int J = INT ? 2 : 4;                 // MFMA steps per 128-wide k block
+  constexpr int J = MX ? 1 : (INT ? 2 : 4);      // MFMA steps per 128-wide k block
   constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
   AccT acc[NL][NF][MF];
 #pragma unroll
@@ -617,7 +643,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // this many leaves the weight prefetch in flight across the barrier.
   constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (GMETA ? NL * NF : 0);
 
-  stage_load<INT, BM>(sm, 0, abase, soffs, kb0, wave);
+  stage_load<RB, BM>(sm, 0, abase, soffs, kb0, wave);
   if constexpr (RSLOAD) rowsum_load<BM>(sm, 0, rsbase, rsoff, kb0, wave);
   load_group(kb0, false);
   if constexpr (streamed<KD>()) {
@@ -630,7 +656,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   for (int kb = kb0; kb < kb1; ++kb) {
     const int cur = (kb - kb0) & 1;
     const bool more = kb + 1 < kb1;
-    if (more) stage_load<INT, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
+    if (more) stage_load<RB, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
     if constexpr (RSLOAD) {
       if (more) rowsum_load<BM>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
     }
@@ -641,6 +667,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     uint32_t bz[NL][NF];
     float zf[NL][NF];
     float wsc[NL][NF];  // w4a4-g128: the channel's weight scale of this group / 16
+    uint32_t wsx[NL][NF];  // mxfp4: the E8M0 byte of this lane's 32-wide block
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
@@ -649,6 +676,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         bz[l][nf] = 0;
         zf[l][nf] = 0.f;
         wsc[l][nf] = 0.f;
+        wsx[l][nf] = 0u;
+        if constexpr (MX) wsx[l][nf] = (meta[l][nf] >> (8 * q)) & 0xFFu;
         if constexpr (GSC)  // (the 1/16 undoes the x16 of the widened nibbles, exactly)
           wsc[l][nf] = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu)) * 0.0625f;
         if constexpr (WONLY) {
@@ -687,7 +716,26 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     // MFMAs, next to its first use
     __builtin_amdgcn_sched_barrier(0);
 
-    if constexpr (GSC) {
+    if constexpr (MX) {
+      // mxfp4: one scaled FP4 MFMA per (row fragment, channel fragment) covers
+      // the whole k block; lane l's operands are 32 consecutive elements of its
+      // row (channel) with the E8M0 scale of that 32-wide block
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const u32x4 af = act_frag<RB>(sm, cur, mf * 16 + li, q);
+        const int sa = (int)((__float_as_uint(sm.rsum[cur][mf * 16 + li]) >> (8 * q)) & 0xFFu);
+        const i32x8 A = {(int)af[0], (int)af[1], (int)af[2], (int)af[3], 0, 0, 0, 0};
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            const u32x4 w = rw[l][nf].d[0];
+            const i32x8 B = {(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
+            acc[l][nf][mf] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(A, B, acc[l][nf][mf], 4, 4, 0, sa, 0,
+                                                                             (int)wsx[l][nf]);
+          }
+      }
+    } else if constexpr (GSC) {
       // w4a4-g128: per row fragment, the two MFMA steps of this k block give an
       // exact int32 block sum, which enters the fp32 accumulator scaled by the
       // row's activation scale and the channel's weight scale of the block
@@ -697,7 +745,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         OpT af[J];
 #pragma unroll
         for (int j = 0; j < J; ++j)
-          af[j] = __builtin_bit_cast(OpT, act_frag<true>(sm, cur, mf * 16 + li, 4 * j + q));
+          af[j] = __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, mf * 16 + li, 4 * j + q));
         const f32x4 sa = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][mf * 16 + 4 * q]);
 #pragma unroll
         for (int l = 0; l < NL; ++l)
@@ -720,7 +768,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         else return wfrag16<KD, ACT>(rw[l][nf], sv, j, bz[l][nf], zf[l][nf]);
       };
       auto aop = [&](int mf) -> OpT {
-        return __builtin_bit_cast(OpT, act_frag<INT>(sm, cur, mf * 16 + li, 4 * j + q));
+        return __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, mf * 16 + li, 4 * j + q));
       };
       auto mma = [&](const OpT& af, const OpT& wf, AccT c) -> AccT {
         if constexpr (INT) return __builtin_amdgcn_mfma_i32_16x16x64_i8(af, wf, c, 0, 0, 0);
@@ -959,6 +1007,9 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
     case K_W8G: run_tile<K_W8G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W4A4G:  // never planned in 128-row tiles
       if constexpr (CFG != CFG_L) run_tile<K_W4A4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
+      break;
+    case K_MXFP4:  // never planned in 128-row tiles
+      if constexpr (CFG != CFG_L) run_tile<K_MXFP4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
       break;
     default: break;
   }

@@ -23,7 +23,8 @@ enum Kind : int32_t {
   K_W4G = 5,   // weight-only 4-bit, group 128
   K_W8G = 6,   // weight-only 8-bit, group 128
   K_W4A4G = 7, // int4 weights and activations with per-128-group scales (w4a4-g128)
-  K_COUNT = 8
+  K_MXFP4 = 8, // FP4 e2m1 weights and activations with E8M0 scales per 32 (scaled FP4 MFMA)
+  K_COUNT = 9
 };
 
 __host__ __device__ constexpr inline bool kind_is_int(int kd) {
@@ -32,13 +33,19 @@ __host__ __device__ constexpr inline bool kind_is_int(int kd) {
 __host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G && kd <= K_W8G; }
 // kinds whose scales come per 128-wide group along K (a 64-byte metadata tail
 // per fragment block): the weight-only kinds and w4a4-g128
-__host__ __device__ constexpr inline bool kind_has_gmeta(int kd) { return kind_is_wonly(kd) || kd == K_W4A4G; }
+__host__ __device__ constexpr inline bool kind_has_gmeta(int kd) {
+  return kind_is_wonly(kd) || kd == K_W4A4G || kd == K_MXFP4;
+}
+__host__ __device__ constexpr inline bool kind_is_mx(int kd) { return kd == K_MXFP4; }
+// activations of the kind arrive quantized (integer codes or MX elements)
+__host__ __device__ constexpr inline bool kind_quant_act(int kd) { return kind_is_int(kd) || kind_is_mx(kd); }
 __host__ __device__ constexpr inline int kind_wbits(int kd) {
   switch (kd) {
     case K_W16: return 16;
     case K_W8A8: return 8;
     case K_W4A4: return 4;
     case K_W4A4G: return 4;
+    case K_MXFP4: return 4;
     case K_W2G: return 2;
     case K_W3G: return 3;
     case K_W4G: return 4;
@@ -66,6 +73,7 @@ __host__ __device__ constexpr inline int lane_bytes(int kd) {
     case K_W8A8: return 32;
     case K_W4A4: return 16;
     case K_W4A4G: return 16;
+    case K_MXFP4: return 16;
     case K_W2G: return 8;
     case K_W3G: return 12;
     case K_W4G: return 16;
@@ -180,8 +188,8 @@ __host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int spli
   return g | (cfg << 16) | (kind << 20) | ((split - 1) << 24);
 }
 // Static cost of one tile in ps: the larger of its memory time and its MFMA
-// time at one CU's share of the MI355X peaks (8 TB/s; 5.0 POPS int8, 2.5
-// PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
+// time at one CU's share of the MI355X peaks (8 TB/s; 10 PFLOP/s FP4, 5.0
+// POPS int8, 2.5 PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
 // (prologue, epilogue).  The group's mt row tiles share each weight tile and
 // its nt channel tiles share each activation tile through L2, so a tile is
 // charged those shares of its HBM bytes; a sliced tile also writes its partial
@@ -190,11 +198,11 @@ __host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int spli
 constexpr double kTileFixedPs = 2.0e6;
 __host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int kk, int split, int mt, int nt) {
   const double wbytes = (double)nl * bn * kk * kind_wbits(kd) / 8.0;
-  const double abytes = (double)bm * kk * (kind_is_int(kd) ? 1.0 : 2.0);
+  const double abytes = (double)bm * kk * (kind_is_mx(kd) ? 0.5 : (kind_is_int(kd) ? 1.0 : 2.0));
   const double pbytes = split > 1 ? 8.0 * bm * bn * nl : 0.0;
   const double flops = 2.0 * nl * bm * bn * kk;
   const double t_mem = (wbytes / (mt > 0 ? mt : 1) + abytes / (nt > 0 ? nt : 1) + pbytes) * 32.0;
-  const double t_mma = flops * 1000.0 / (kind_is_int(kd) ? 19531.0 : 9766.0);
+  const double t_mma = flops * 1000.0 / (kind_is_mx(kd) ? 39062.0 : (kind_is_int(kd) ? 19531.0 : 9766.0));
   double c = t_mem > t_mma ? t_mem : t_mma;
   c += kTileFixedPs;
   if (c > 2.0e9) c = 2.0e9;
@@ -234,6 +242,7 @@ struct WsLayout {
   size_t rsx, rsh, rsh_shared;  // fp32 row sums per 128-wide k block of x, h, h_shared
   size_t xq4g, xs4g, hsg, hsg_shared;  // w4a4-g128 codes and group scales
   size_t rids, rw, shw;  // router front-end outputs: ids, gate weights, shared-expert gates
+  size_t xqmx, xsmx, hqmx, hsmx, hqmx_shared, hsmx_shared;  // mxfp4 activation codes and E8M0 bytes
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -281,9 +290,14 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
 // down_qmax[e] = qmax | kDownQGroup for per-128-group scales (into hsg
 // [P][F/128]), else per-row scales (into hs); 0 = not quantized.
 constexpr int kDownQGroup = 0x100;
+constexpr int kDownQMX = 0x200;  // MXFP4 codes into hqmx [P][F/2], E8M0 bytes into hsmx [P][F/32]
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets,
                                 int E, const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg,
-                                hipStream_t s);
+                                uint8_t* hqmx, uint8_t* hsmx, hipStream_t s);
+// MXFP4 encoding of rows (cols a multiple of 128): codes [rows][cols/2] (two
+// e2m1 nibbles a byte, element order), E8M0 bytes [rows][cols/32].
+hipError_t launch_act_quant_mx(const void* a, int act, int rows, int cols, int64_t ld, uint8_t* codes, uint8_t* exps,
+                               hipStream_t s);
 
 struct GemmArgs {
   const DevExpert* experts;  // device [G]
@@ -298,6 +312,10 @@ struct GemmArgs {
   // (routed [P][F/128], shared [n_shared*T][F_sh/128]; codes in hq / hq_shared)
   const int8_t* xq4g; const float* xs4g;
   const float* hsg; const float* hsg_shared;
+  // mxfp4: e2m1 codes [rows][K/2] and E8M0 bytes [rows][K/32] of x, routed h and shared h
+  const uint8_t* xqmx; const uint8_t* xsmx;
+  const uint8_t* hqmx; const uint8_t* hsmx;
+  const uint8_t* hqmx_shared; const uint8_t* hsmx_shared;
   void* h; void* h_shared;
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;

@@ -25,12 +25,17 @@
 // A group whose scale is zero dequantizes to zero whatever its codes: it is
 // stored with scale 1 and every code equal to its zero point (same values).
 // w4a4-g128 blocks end with 16 (scale, 0) pairs; a zero scale stays zero.
+//   mxfp4: lane l holds k = 128*kb + 32*qd + v for v = 0..31, slot v in nibble
+//          v (dword v/8, bits 4(v%8)): the operand layout of one 16x16x128 FP4
+//          MFMA.  The block ends with 16 dwords, one per channel, whose byte b
+//          is the E8M0 scale of the channel's 32-wide block b of this k block.
 #include "mxmoe_internal.h"
 
 namespace mxmoe {
 namespace {
 
 __device__ inline int slot_k(int kd, int v, int qd) {
+  if (kd == K_MXFP4) return 32 * qd + v;
   if (kind_is_int(kd)) return 64 * (v >> 4) + 16 * qd + (v & 15);
   return 32 * (v >> 3) + 8 * qd + (v & 7);
 }
@@ -45,6 +50,7 @@ __device__ inline void slot_field(int kd, int v, int* dw, int* bit, uint32_t* ma
     case K_W4G: *dw = j; *bit = 16 * h + 4 * p; *mask = 0xFu; break;
     case K_W2G:
     case K_W3G: *dw = j >> 1; *bit = 16 * h + 2 * (4 * (j & 1) + p); *mask = 0x3u; break;
+    case K_MXFP4: *dw = v >> 3; *bit = 4 * (v & 7); *mask = 0xFu; break;
     default: {  // K_W4A4
       const int jj = v >> 4, ii = v & 15, d = ii >> 3, i8 = ii & 7;
       *dw = 2 * jj + d;
@@ -96,6 +102,11 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
   } else if (kd == K_W4A4G) {
     s16 = reinterpret_cast<const uint16_t*>(scales)[(int64_t)row * kblocks + kb];
   }
+  uint32_t mxs = 0;  // mxfp4: the four E8M0 bytes of the channel's 32-wide blocks of this k block
+  if (kd == K_MXFP4) {
+    const uint8_t* e = scales + (int64_t)row * (k / 32) + 4 * kb;
+    mxs = (uint32_t)e[0] | ((uint32_t)e[1] << 8) | ((uint32_t)e[2] << 16) | ((uint32_t)e[3] << 24);
+  }
   const uint32_t zcode = zero_group ? (uint32_t)(float)__builtin_bit_cast(_Float16, z16) : 0u;
   uint32_t w[16];
   for (int i = 0; i < 16; ++i) w[i] = 0;
@@ -113,7 +124,7 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
   uint32_t* o32 = reinterpret_cast<uint32_t*>(out);
   for (int i = 0; i < lane_bytes(kd) / 4; ++i) o32[i] = w[i];
   if (kind_has_gmeta(kd) && qd == 0) {
-    const uint32_t sz = (uint32_t)s16 | ((uint32_t)z16 << 16);
+    const uint32_t sz = kd == K_MXFP4 ? mxs : ((uint32_t)s16 | ((uint32_t)z16 << 16));
     reinterpret_cast<uint32_t*>(packed + blk * block_bytes(kd) + 64 * lane_bytes(kd))[lane & 15] = sz;
   }
   if (kind_is_int(kd) && kd != K_W4A4G && kb == 0 && qd == 0) {
@@ -148,6 +159,11 @@ __global__ void unpack_kernel(int kd, int n, int k, int act, const uint8_t* __re
   }
   if (kind_has_gmeta(kd) && qd == 0) {
     uint32_t sz = reinterpret_cast<const uint32_t*>(packed + blk * block_bytes(kd) + 64 * lane_bytes(kd))[lane & 15];
+    if (kd == K_MXFP4) {
+      uint8_t* e = scales + (int64_t)row * (k / 32) + 4 * kb;
+      for (int b = 0; b < 4; ++b) e[b] = (uint8_t)(sz >> (8 * b));
+      return;
+    }
     int64_t g = (int64_t)row * kblocks + kb;
     reinterpret_cast<uint16_t*>(scales)[g] = (uint16_t)(sz & 0xFFFF);
     if (kind_is_wonly(kd)) reinterpret_cast<uint16_t*>(zeros)[g] = (uint16_t)(sz >> 16);

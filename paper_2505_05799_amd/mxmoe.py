@@ -23,7 +23,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 
 class Scheme_t(C.Structure):
     _fields_ = [("w_bits", C.c_int32), ("a_bits", C.c_int32), ("w_group", C.c_int32),
-                ("a_group", C.c_int32), ("symmetric", C.c_int32)]
+                ("a_group", C.c_int32), ("symmetric", C.c_int32), ("fmt", C.c_int32)]
 
 
 class Linear_t(C.Structure):
@@ -50,7 +50,8 @@ class ForwardOpts_t(C.Structure):
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
              "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total", "plan_queue_cap",
              "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared", "xq4g", "xs4g", "hsg",
-             "hsg_shared", "router_ids", "router_w", "shared_w"]
+             "hsg_shared", "xqmx", "xsmx", "hqmx", "hsmx", "hqmx_shared", "hsmx_shared", "router_ids", "router_w",
+             "shared_w"]
 
 
 class WsLayout_t(C.Structure):
@@ -133,7 +134,7 @@ def _ptr(t) -> C.c_void_p:
 
 
 def scheme_t(s) -> Scheme_t:
-    return Scheme_t(s.w_bits, s.a_bits, s.w_group, s.a_group, s.symmetric)
+    return Scheme_t(s.w_bits, s.a_bits, s.w_group, s.a_group, s.symmetric, getattr(s, "fmt", 0))
 
 
 def act_code(act: str) -> int:
@@ -212,6 +213,8 @@ class PackedLinear:
         if s.w_bits < 16 and s.a_bits == 16:
             scales = torch.empty((q.n, q.k // 128), dtype=torch.int16, device=self.buf.device)
             zeros = torch.empty_like(scales)
+        elif s.fmt == 1:                          # mxfp4: E8M0 bytes per 32
+            scales = torch.empty((q.n, q.k // 32), dtype=torch.uint8, device=self.buf.device)
         elif s.w_bits < 16 and s.w_group > 0:     # w4a4-g128: fp16 group scales
             scales = torch.empty((q.n, q.k // 128), dtype=torch.int16, device=self.buf.device)
         elif s.w_bits < 16:
@@ -223,10 +226,10 @@ class PackedLinear:
         c = codes.cpu().numpy()
         if s.w_bits == 16:
             c = c.view(np.uint16)
-        elif s.a_bits < 16:
+        elif s.a_bits < 16 and s.fmt == 0:
             c = c.view(np.int8)
         sc = None if scales is None else scales.cpu().numpy()
-        if sc is not None and (s.a_bits == 16 or s.w_group > 0):
+        if sc is not None and s.fmt == 0 and (s.a_bits == 16 or s.w_group > 0):
             sc = sc.view(np.float16)
         z = None if zeros is None else zeros.cpu().numpy().view(np.float16)
         return c, sc, z

@@ -30,6 +30,11 @@ Offline quantizers (input preparation, not part of the forward pass):
   is s * (q - z), the min-max quantizer with x_min snapped onto the grid.
 * per-channel symmetric (``w8a8``/``w4a4``, Fig. 4 caption): qmax = 2^(b-1) - 1,
   s = fp32(amax_row / qmax), q = clamp(rne(w / s), -qmax, qmax).
+* ``mxfp4`` (the OCP Microscaling MXFP4 format, one of the 4-bit schemes the
+  MI355X matrix cores run natively): per 32 consecutive weights along K a
+  shared power-of-two scale 2^e (E8M0 byte e + 127), e = floor(log2(amax)) - 2,
+  and FP4 e2m1 elements rne(w / 2^e) on the grid {0, 0.5, 1, 1.5, 2, 3, 4, 6}
+  (ties to the even code, magnitudes above 6 clamp to 6).
 """
 
 from __future__ import annotations
@@ -54,9 +59,12 @@ class Scheme:
     w_group: int     # 128 for groups along K, -1 = per output channel
     a_group: int     # 128 for groups along K, -1 = per token
     symmetric: int   # 1 for w8a8 / w4a4 (per channel or g128), 0 for wNg128 asym and 16-bit
+    fmt: int = 0     # 0 integer codes; 1 OCP MX floating point (e2m1 elements, E8M0 scale per 32)
 
     @property
     def name(self) -> str:
+        if self.fmt == 1:
+            return "mxfp4"
         if self.w_bits == 16:
             return "w16"
         if self.a_bits < 16:
@@ -72,6 +80,8 @@ class Scheme:
         """Stored bits per weight including scale/zero overhead."""
         if self.w_bits == 16:
             return 16.0
+        if self.fmt == 1:
+            return self.w_bits + 8.0 / self.w_group    # one E8M0 byte per 32
         if self.weight_only:
             return self.w_bits + 32.0 / self.w_group   # fp16 scale + fp16 zero
         if self.w_group > 0:
@@ -87,7 +97,8 @@ W3G128 = Scheme(3, 16, 128, -1, 0)
 W4G128 = Scheme(4, 16, 128, -1, 0)
 W8G128 = Scheme(8, 16, 128, -1, 0)
 W4A4G128 = Scheme(4, 4, 128, 128, 1)   # 4-bit weights and activations, per-128 group scales
-ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128)
+MXFP4 = Scheme(4, 4, 32, 32, 1, 1)     # FP4 e2m1 weights and activations, E8M0 scale per 32
+ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128, MXFP4)
 SCHEME_BY_NAME = {s.name: s for s in ALL_SCHEMES}
 
 LINEAR_NAMES = ("gate", "up", "down")
@@ -310,6 +321,29 @@ def quantize_sym_g128(w: np.ndarray, bits: int, group: int = 128):
     return q.reshape(n, k).astype(np.int8), s
 
 
+E2M1_VALUES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def quantize_mxfp4(w: np.ndarray, block: int = 32):
+    """MXFP4 (OCP MX) quantizer of the weights: codes uint8 [n, k] (e2m1, sign
+    in bit 3), E8M0 scales uint8 [n, k/32].  An all-zero block gets e = -127."""
+    n, k = w.shape
+    assert k % block == 0
+    v = w.astype(np.float64).reshape(n, k // block, block)
+    amax = np.abs(v).max(axis=2)
+    _, ex = np.frexp(amax)                      # amax = f 2^ex, f in [0.5, 1): floor(log2) = ex - 1
+    e = np.where(amax > 0, ex - 1 - 2, -127).clip(-127, 127)
+    r = np.abs(v) / np.exp2(e)[..., None]
+    # round to the e2m1 grid, ties to the even code: at the midpoint above an
+    # even code stay, above an odd code go up
+    mids = (0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0)
+    code = np.zeros(r.shape, np.int64)
+    for c, mp in enumerate(mids):
+        code += (r > mp) if c % 2 == 0 else (r >= mp)
+    code = np.where((v < 0) & (code > 0), code | 8, code)
+    return code.reshape(n, k).astype(np.uint8), (e + 127).astype(np.uint8)
+
+
 @dataclass
 class QLinear:
     """One quantized linear, W is [n, k] = [out, in] (nn.Linear layout)."""
@@ -327,6 +361,8 @@ class QLinear:
             return 2 * self.n * self.k
         if s.weight_only:
             return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
+        if s.fmt == 1:      # e2m1 nibbles + one E8M0 byte per 32
+            return self.n * self.k // 2 + self.n * self.k // 32
         if s.w_group > 0:   # packed with the same 4-byte metadata slot per group
             return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
         return self.n * self.k * s.w_bits // 8 + 4 * self.n
@@ -339,6 +375,9 @@ def quantize_linear(w_bf16_f32: np.ndarray, scheme: Scheme) -> QLinear:
     if scheme.weight_only:
         c, s, z = quantize_g128_asym(w_bf16_f32, scheme.w_bits, scheme.w_group)
         return QLinear(scheme, n, k, c, s, z)
+    if scheme.fmt == 1:
+        c, s = quantize_mxfp4(w_bf16_f32, scheme.w_group)
+        return QLinear(scheme, n, k, c, s)
     if scheme.w_group > 0:
         c, s = quantize_sym_g128(w_bf16_f32, scheme.w_bits, scheme.w_group)
         return QLinear(scheme, n, k, c, s)

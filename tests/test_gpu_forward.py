@@ -63,7 +63,37 @@ MIXES = [
     [(W.W4A4G128,) * 3, (W.W4A4G128, W.W4A4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4G128),
      (W.W4A4G128, W.W4A4G128, W.W8A8), (W.W16, W.W16, W.W4A4G128), (W.W3G128, W.W3G128, W.W4A4G128),
      (W.W4A4G128, W.W4A4G128, W.W4A4)],
+    # mxfp4 (FP4 e2m1 with E8M0 scales, on the scaled FP4 MFMA) beside the others
+    [(W.MXFP4,) * 3, (W.MXFP4, W.MXFP4, W.W2G128), (W.W8A8, W.W8A8, W.MXFP4), (W.W16, W.W16, W.MXFP4),
+     (W.MXFP4, W.MXFP4, W.W4A4G128), (W.W3G128, W.W3G128, W.MXFP4), (W.MXFP4, W.MXFP4, W.W8A8)],
 ]
+
+
+def test_mx_activation_codes_bit_exact():
+    """The forward's MXFP4 encoding of x and of the routed and shared h rows
+    equals the oracle's encoder, byte for byte."""
+    torch = torch_mod()
+    for act in ("bf16", "fp16"):
+        blk = W.random_small_block(91, T=77, H=256, F=384, E=4, k=2, n_shared=1, F_shared=256, act=act,
+                                   schemes=[(W.MXFP4,) * 3] * 5, skew=0.5)
+        mb, _ = run_block(blk)
+        T, H, F, k = 77, 256, 384, 2
+        xq = mb.ws_view("xqmx", torch.uint8, T * H // 2, T).cpu().numpy().reshape(T, H // 2)
+        xe = mb.ws_view("xsmx", torch.uint8, T * H // 32, T).cpu().numpy().reshape(T, H // 32)
+        qx, ex = O.mx_quant(O.act_values(blk.x, act).astype(np.float32))
+        assert np.array_equal(xq, (qx[:, 0::2] | (qx[:, 1::2] << 4)).astype(np.uint8))
+        assert np.array_equal(xe, ex)
+        # routed h rows, in sorted-pair order, against the encoder of the GPU's own h
+        P = int(mb.ws_view("offsets", torch.int32, 5, T).cpu().numpy()[4])
+        hdt = torch.int16
+        h = mb.ws_view("h", hdt, T * k * F, T).cpu().numpy()[: P * F].reshape(P, F)
+        hv = O.act_values(h.view(np.float16) if act == "fp16" else h.view(np.uint16), act)
+        hq = mb.ws_view("hqmx", torch.uint8, T * k * F // 2, T).cpu().numpy()[: P * F // 2].reshape(P, F // 2)
+        he = mb.ws_view("hsmx", torch.uint8, T * k * F // 32, T).cpu().numpy()[: P * F // 32].reshape(P, F // 32)
+        qh, eh = O.mx_quant(hv.astype(np.float32))
+        assert np.array_equal(hq, (qh[:, 0::2] | (qh[:, 1::2] << 4)).astype(np.uint8))
+        assert np.array_equal(he, eh)
+        say(f"mx codes {act}: x and {P} routed h rows bit-exact")
 
 
 @pytest.mark.parametrize("act", ["bf16", "fp16"])

@@ -132,12 +132,26 @@ def _check_group_linear(q, a, got, act):
     assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
 
 
+def _check_mx_linear(q, a, got, act):
+    """mxfp4: the scaled FP4 MFMA sums exact products of the decoded operands
+    in fp32; at most two roundings per 128-wide k block and at most 2^4 blocks
+    keep the error below 2^-20 of sum |a_hat| |w_hat|."""
+    assert q.k // 128 <= 16
+    want = O.linear(a, q, act)
+    qa, ea = O.mx_quant(a.astype(np.float32), 32)
+    ad = O._mx_values(qa, ea, 32)
+    bound = 2.0 ** -20 * (np.abs(ad) @ np.abs(O.dequant(q, act)).T) + 1e-30
+    assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
+
+
 @pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
 @pytest.mark.parametrize("m", LIN_M)
 @pytest.mark.parametrize("n,k", LIN_SHAPES)
 def test_linear_bf16(scheme, m, n, k):
     q, a, got = _linear_case(scheme, "bf16", m, n, k, m * 7 + n)
-    if scheme.a_group > 0:
+    if scheme.fmt == 1:
+        _check_mx_linear(q, a, got, "bf16")
+    elif scheme.a_group > 0:
         _check_group_linear(q, a, got, "bf16")
     elif scheme.a_bits < 16:
         want = O.linear(a, q, "bf16", return_int=True)
@@ -152,7 +166,9 @@ def test_linear_bf16(scheme, m, n, k):
 @pytest.mark.parametrize("m", [3, 33, 129])
 def test_linear_fp16(scheme, m):
     q, a, got = _linear_case(scheme, "fp16", m, 48, 256, m + 11)
-    if scheme.a_group > 0:
+    if scheme.fmt == 1:
+        _check_mx_linear(q, a, got, "fp16")
+    elif scheme.a_group > 0:
         _check_group_linear(q, a, got, "fp16")
     elif scheme.a_bits < 16:
         assert np.array_equal(got.astype(np.int64), O.linear(a, q, "fp16", return_int=True))

@@ -55,8 +55,37 @@ def py_act_quant(row, qmax):
     return codes, s
 
 
+E2M1 = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+
+
+def py_e2m1(code):
+    v = E2M1[code & 7]
+    return -v if code & 8 else v
+
+
+def py_mx_quant(vals):
+    """Brute-force MXFP4 encoding of one 32-block of Python floats: the
+    exponent from frexp, then the grid value nearest to each scaled element
+    (ties: the one with an even code), clamped to 6."""
+    amax = max(abs(v) for v in vals)
+    e = -127 if amax == 0 else max(-127, min(127, math.frexp(amax)[1] - 1 - 2))
+    codes = []
+    for v in vals:
+        x = abs(v) / 2.0 ** e
+        best = None
+        for c, g in enumerate(E2M1):
+            key = (abs(x - g), c % 2)          # nearer first, then the even code
+            if best is None or key < best[0]:
+                best = (key, c)
+        c = 7 if x > 6 else best[1]
+        codes.append(c | 8 if (v < 0 and c) else c)
+    return codes, e
+
+
 def py_weight(lin, act, n, c):
     s = lin.scheme
+    if getattr(s, "fmt", 0) == 1:
+        return py_e2m1(int(lin.codes[n, c])) * 2.0 ** (int(lin.scales[n, c // 32]) - 127)
     if s.w_bits == 16:
         w = bits_to_float_bf16(lin.codes[n, c])
         return f16_round(w) if act == "fp16" else w
@@ -70,6 +99,12 @@ def py_weight(lin, act, n, c):
 
 def py_linear(a_row, lin, act):
     s = lin.scheme
+    if getattr(s, "fmt", 0) == 1:
+        a_hat = []
+        for b in range(lin.k // 32):
+            codes, e = py_mx_quant([float(f32(v)) for v in a_row[32 * b: 32 * b + 32]])
+            a_hat += [py_e2m1(cd) * 2.0 ** e for cd in codes]
+        return [sum(a_hat[c] * py_weight(lin, act, n, c) for c in range(lin.k)) for n in range(lin.n)]
     if s.a_bits < 16 and s.a_group > 0:
         # per 128-wide block: integer dot of the block's codes, times both block scales
         g, qmax = s.a_group, (1 << (s.a_bits - 1)) - 1
@@ -253,6 +288,41 @@ def test_dequant_recovers_weights(scheme):
         assert np.all(np.abs(lin.codes).max(axis=1) == qmax)
 
 
+def test_mxfp4_quantizer_pins():
+    """OCP MX FP4: values on the e2m1 grid times a power of two; the error of
+    an element is at most a quarter of max(|x|, 1) in units of its block scale
+    (half the grid spacing in every binade, 2 at most above 6); a block of
+    equal values encodes exactly; doubling the input adds one to every scale
+    and keeps every code; brute force on a few blocks."""
+    w = W.draw_weight(12, 0, 0, 48, 384)
+    lin = W.quantize_linear(w, W.MXFP4)
+    deq = O.dequant(lin, "bf16")
+    sc = np.exp2(np.repeat(lin.scales.astype(np.float64) - 127, 32, axis=1))
+    x = np.abs(w.astype(np.float64)) / sc
+    assert np.all(np.abs(deq - w) <= 0.25 * np.maximum(x, 1.0) * sc * (1 + 1e-12))
+    assert np.all(np.isin(np.abs(deq) / sc, O._E2M1))
+    # every block reaches a code of 4 or 6 (its maximum lies in [4, 8) scaled)
+    mags = (lin.codes & 7).reshape(48, -1, 32).max(axis=2)
+    assert np.all(mags >= 6)
+    # activations: the oracle's encoder on equal, doubled and brute-forced rows
+    a = np.full((1, 64), 1.0, np.float32)
+    q, e = O.mx_quant(a)
+    assert np.all(O._mx_values(q, e, 32) == 1.0)
+    rng = np.random.default_rng(3)
+    r = rng.standard_normal((5, 128)).astype(np.float32)
+    q1, e1 = O.mx_quant(r)
+    q2, e2 = O.mx_quant(r * np.float32(2))
+    assert np.array_equal(q1, q2) and np.array_equal(e2.astype(int), e1.astype(int) + 1)
+    for i in range(5):
+        for b in range(4):
+            pc, pe = py_mx_quant([float(v) for v in r[i, 32 * b: 32 * b + 32]])
+            assert q1[i, 32 * b: 32 * b + 32].tolist() == pc and int(e1[i, b]) - 127 == pe
+    # the weight quantizer of the input generator agrees with the oracle's encoder
+    cw, ew = W.quantize_mxfp4(w)
+    co, eo = O.mx_quant(w)
+    assert np.array_equal(cw, co) and np.array_equal(ew, eo)
+
+
 def test_w16_fp16_conversion():
     w = np.array([[1.0, -0.0078125, 3.0e-6, 60000.0, 1.0e-7]], np.float32)
     lin = W.quantize_linear(w, W.W16)
@@ -333,10 +403,12 @@ MIXED = [(W.W4G128, W.W4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4), (W.W16, W.W16
          (W.W3G128, W.W3G128, W.W16), (W.W4A4, W.W8G128, W.W4G128)]
 MIXED_G = [(W.W4A4G128, W.W4A4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4G128), (W.W4A4G128,) * 3,
            (W.W16, W.W16, W.W4A4G128), (W.W4A4G128, W.W4A4G128, W.W8A8)]
+MIXED_MX = [(W.MXFP4,) * 3, (W.MXFP4, W.MXFP4, W.W3G128), (W.W8A8, W.W8A8, W.MXFP4), (W.W16, W.W16, W.MXFP4),
+            (W.MXFP4, W.MXFP4, W.W4A4G128)]
 
 
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
-@pytest.mark.parametrize("mix,H,F", [(MIXED, 128, 128), (MIXED_G, 256, 256)])
+@pytest.mark.parametrize("mix,H,F", [(MIXED, 128, 128), (MIXED_G, 256, 256), (MIXED_MX, 128, 256)])
 def test_moe_brute_force(act, mix, H, F):
     blk = W.random_small_block(21, T=5, H=H, F=F, E=4, k=2, n_shared=1, F_shared=128, act=act,
                                schemes=mix)
