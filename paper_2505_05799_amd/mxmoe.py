@@ -175,11 +175,44 @@ def empty_aligned(nbytes: int, device="cuda"):
 
 
 # --------------------------------------------------------------- packing
+def operand_bytes(scheme, n: int, k: int):
+    """Bytes the packer reads from (codes, scales, zeros) for a scheme (None: not read)."""
+    s = scheme
+    if s.w_bits == 16:
+        return 2 * n * k, None, None
+    if getattr(s, "fmt", 0) == 1:
+        return n * k, n * (k // 32), None
+    if s.a_bits == 16:
+        return n * k, 2 * n * (k // 128), 2 * n * (k // 128)
+    if s.w_group > 0:
+        return n * k, 2 * n * (k // 128), None
+    return n * k, 4 * n, None
+
+
+def _nbytes(arr) -> int:
+    if arr is None:
+        return 0
+    if hasattr(arr, "element_size"):
+        return arr.numel() * arr.element_size()
+    return np.asarray(arr).nbytes
+
+
+def check_operands(q):
+    """Raise ValueError unless the codes / scales / zeros of a QLinear hold at
+    least the bytes the packer reads for its scheme (the packer takes raw
+    pointers and cannot check their extent)."""
+    want = operand_bytes(q.scheme, q.n, q.k)
+    for name, arr, need in zip(("codes", "scales", "zeros"), (q.codes, q.scales, q.zeros), want):
+        if need is not None and (arr is None or _nbytes(arr) < need):
+            raise ValueError(f"{q.scheme.name} {q.n}x{q.k}: {name} hold {_nbytes(arr)} bytes, the packer reads {need}")
+
+
 class PackedLinear:
     """One linear packed on the device (owns the packed buffer)."""
 
     def __init__(self, q, act: str, device="cuda", stream=None):
         lib = load_library()
+        check_operands(q)
         self.q = q
         self.act = act
         self.L = Linear_t(q.n, q.k, scheme_t(q.scheme))

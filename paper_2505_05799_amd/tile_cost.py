@@ -95,12 +95,11 @@ class CostTable:
 # ----------------------------------------------------------------------------
 
 
-def _device_linear(scheme, n: int, k: int, gen):
-    """A QLinear whose codes / scales / zeros are random device tensors of the
-    scheme's formats (timing does not depend on the values)."""
+def _device_linear(scheme, n: int, k: int, gen, dev: str = "cuda"):
+    """A QLinear whose codes / scales / zeros are random tensors (on `dev`) of
+    the scheme's formats (timing does not depend on the values)."""
     import torch
     from . import workloads as W
-    dev = "cuda"
     s = scheme
     if s.w_bits == 16:
         w = (torch.randn((n, k), generator=gen, device=dev) * 0.02).to(torch.bfloat16).view(torch.int16)
@@ -111,6 +110,10 @@ def _device_linear(scheme, n: int, k: int, gen):
         scales = (torch.rand((n, k // 128), generator=gen, device=dev) * 0.01 + 0.001).to(torch.float16)
         zeros = torch.randint(0, qm + 1, (n, k // 128), generator=gen, device=dev).to(torch.float16)
         return W.QLinear(s, n, k, codes, scales.view(torch.int16), zeros.view(torch.int16))
+    if s.fmt == 1:   # mxfp4: e2m1 codes 0..15, E8M0 bytes per 32 near 2^-7
+        codes = torch.randint(0, 16, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.uint8)
+        scales = torch.randint(118, 124, (n, k // 32), generator=gen, device=dev, dtype=torch.int32).to(torch.uint8)
+        return W.QLinear(s, n, k, codes, scales)
     qm = (1 << (s.w_bits - 1)) - 1
     codes = torch.randint(-qm, qm + 1, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.int8)
     if s.w_group > 0:

@@ -204,3 +204,21 @@ def test_forward_router_mode_validation(lib):
     o3 = M.ForwardOpts_t()                  # ids mode without ids
     assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, None, None, p, p, 10 ** 9, C.byref(o3), None) == \
         M.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("s", W.ALL_SCHEMES)
+def test_pack_operand_extent_is_checked(s):
+    """The binding refuses operands smaller than what the packer reads."""
+    q = W.quantize_linear(W.draw_weight(2, 0, 0, 32, 256), s)
+    M.check_operands(q)                                   # the generator's own operands fit
+    if q.scales is not None:
+        short = W.QLinear(s, q.n, q.k, q.codes, q.scales.reshape(-1)[: q.scales.size // 2], q.zeros)
+        with pytest.raises(ValueError):
+            M.check_operands(short)
+    with pytest.raises(ValueError):
+        M.check_operands(W.QLinear(s, q.n, q.k, q.codes.reshape(-1)[:10], q.scales, q.zeros))
+    # the wrong format's scales (w4a4-g128's fp16 [n, k/128] for mxfp4) are refused
+    if s == W.MXFP4:
+        g = W.quantize_linear(W.draw_weight(2, 0, 0, 32, 256), W.W4A4G128)
+        with pytest.raises(ValueError):
+            M.check_operands(W.QLinear(s, q.n, q.k, q.codes, g.scales))

@@ -112,3 +112,16 @@ def test_block_problem_memory_and_mapping():
                  + W.QLinear(t[2], cfg.H, cfg.F if g < cfg.E else cfg.F_shared, None).nbytes_packed
                  for g, t in enumerate(sch))
     assert packed == pytest.approx(info["W_bytes"]) and packed <= p.M
+
+
+@pytest.mark.parametrize("s", W.ALL_SCHEMES)
+def test_profiler_operands_fit_the_packer(s):
+    """The profiler's random operands have the extent the packer reads for
+    every scheme (regression: mxfp4 once got another format's scales)."""
+    torch = pytest.importorskip("torch")
+    from paper_2505_05799_amd import mxmoe as M
+    g = torch.Generator(device="cpu")
+    g.manual_seed(0)
+    q = TC._device_linear(s, 256, 512, g, dev="cpu")
+    M.check_operands(q)
+    assert (q.n, q.k) == (256, 512)
