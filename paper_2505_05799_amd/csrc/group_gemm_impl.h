@@ -392,19 +392,21 @@ __device__ inline void stage_offsets(StageOffs<RB, BM>& so, const Smem& sm, int6
 // loads, weight prefetch included, before the first one); completion is
 // waited for explicitly (wait_vmem) before the barrier that publishes the
 // stage.
-// The base address is uniform by construction; it passes through
-// readfirstlane so that the scalar operand never depends on the compiler
-// proving that (in large instantiations it may keep the value in a VGPR).
+// The base address is uniform by construction.  With UP it passes through
+// readfirstlane, so that the scalar operand does not depend on the compiler
+// proving that; the mxfp4 tiles need it (without it the compiler keeps the
+// base in a VGPR there), the others do without (the extra copies would cost
+// registers across the whole kernel).
 __device__ inline const uint8_t* uniform_ptr(const uint8_t* p) {
   const uint64_t v = reinterpret_cast<uint64_t>(p);
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
 }
-__device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+template <bool UP = false> __device__ inline void lds_dma16(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(voff), "s"(uniform_ptr(base)), "s"(lds_addr)
+               : "v"(voff), "s"(UP ? uniform_ptr(base) : base), "s"(lds_addr)
                : "memory", "m0");
 }
 
@@ -443,7 +445,7 @@ __device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const 
 #pragma unroll
   for (int i = 0; i < S::PER_WAVE; ++i) {
     const int blk = wave + 4 * i;
-    if (blk < S::NBLK) lds_dma16(bk, so.off[i], __builtin_amdgcn_readfirstlane(lds0 + blk * 1024));
+    if (blk < S::NBLK) lds_dma16<RB == 64>(bk, so.off[i], __builtin_amdgcn_readfirstlane(lds0 + blk * 1024));
   }
 }
 
@@ -455,17 +457,17 @@ template <int RB> __device__ inline u32x4 act_frag(const Smem& sm, int buf, int 
 // direct global->LDS load of 4 bytes per lane brings the precomputed sums of
 // rows 64w .. 64w + 63 of k block kb into sm.rsum[buf] (wavefronts
 // w < ceil(BM / 64)); rsoff: the lane's row offset (bytes) at k block 0.
-__device__ inline void lds_dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
+template <bool UP = false> __device__ inline void lds_dma4(const uint8_t* base, uint32_t voff, uint32_t lds_addr) {
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
                :
-               : "v"(voff), "s"(uniform_ptr(base)), "s"(lds_addr)
+               : "v"(voff), "s"(UP ? uniform_ptr(base) : base), "s"(lds_addr)
                : "memory", "m0");
 }
-template <int BM>
+template <int BM, bool UP = false>
 __device__ inline void rowsum_load(Smem& sm, int buf, const float* rsbase, uint32_t rsoff, int kb, int wave) {
   if (wave * 64 < BM) {
     const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.rsum[buf][wave * 64]);
-    lds_dma4(reinterpret_cast<const uint8_t*>(rsbase + kb), rsoff, __builtin_amdgcn_readfirstlane(lds));
+    lds_dma4<UP>(reinterpret_cast<const uint8_t*>(rsbase + kb), rsoff, __builtin_amdgcn_readfirstlane(lds));
   }
 }
 
@@ -644,7 +646,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (GMETA ? NL * NF : 0);
 
   stage_load<RB, BM>(sm, 0, abase, soffs, kb0, wave);
-  if constexpr (RSLOAD) rowsum_load<BM>(sm, 0, rsbase, rsoff, kb0, wave);
+  if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, 0, rsbase, rsoff, kb0, wave);
   load_group(kb0, false);
   if constexpr (streamed<KD>()) {
 #pragma unroll
@@ -658,7 +660,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const bool more = kb + 1 < kb1;
     if (more) stage_load<RB, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
     if constexpr (RSLOAD) {
-      if (more) rowsum_load<BM>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
+      if (more) rowsum_load<BM, MX>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
     }
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
