@@ -436,12 +436,14 @@ template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& 
   sm.entry.x = -1;  // only the group field is read when no tile is left
 }
 
+// sub: sub-stage of the buffer (tiles that stage two k blocks per step put
+// the second one's BM rows after the first one's)
 template <int RB, int BM>
 __device__ inline void stage_load(Smem& sm, int buf, const uint8_t* base, const StageOffs<RB, BM>& so, int kb,
-                                  int wave) {
+                                  int wave, int sub = 0) {
   using S = StageOffs<RB, BM>;
   const uint8_t* bk = base + (int64_t)kb * S::RB;  // uniform
-  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)sm.act[buf]);
+  const uint32_t lds0 = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)sm.act[buf]) + sub * BM * RB;
 #pragma unroll
   for (int i = 0; i < S::PER_WAVE; ++i) {
     const int blk = wave + 4 * i;
@@ -463,10 +465,12 @@ template <bool UP = false> __device__ inline void lds_dma4(const uint8_t* base, 
                : "v"(voff), "s"(UP ? uniform_ptr(base) : base), "s"(lds_addr)
                : "memory", "m0");
 }
+// (sub-stage s of a tile of at most 64 rows takes rsum[buf][64 s ..])
 template <int BM, bool UP = false>
-__device__ inline void rowsum_load(Smem& sm, int buf, const float* rsbase, uint32_t rsoff, int kb, int wave) {
+__device__ inline void rowsum_load(Smem& sm, int buf, const float* rsbase, uint32_t rsoff, int kb, int wave,
+                                   int sub = 0) {
   if (wave * 64 < BM) {
-    const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.rsum[buf][wave * 64]);
+    const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.rsum[buf][sub * 64 + wave * 64]);
     lds_dma4<UP>(reinterpret_cast<const uint8_t*>(rsbase + kb), rsoff, __builtin_amdgcn_readfirstlane(lds));
   }
 }
@@ -610,23 +614,30 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const uint32_t loff = (uint32_t)lane * LB;
   const uint32_t moff = 64u * LB + 4u * li;  // this lane's channel in the group metadata
 
-  Raw<KD> raw[NL][NF];   // low-bit kinds: next group, prefetched a group ahead
+  // Tiles of at most 32 rows of the kinds with at most 16 bytes per lane and
+  // k block take two k blocks per step: both blocks' stages and weights are in
+  // flight together, which halves the memory round trips a short tile waits
+  // for (its MFMA work per block is too small to hide one).  Slot s of the
+  // weight registers serves k block kb + s and is refilled right after use.
+  constexpr int KBI = (BM <= 32 && !streamed<KD>() && LB <= 16) ? 2 : 1;
+  Raw<KD> raw[KBI][NL][NF];   // low-bit kinds: next group(s), prefetched a step ahead
   u32x4 st[J][NL][NF];   // streamed kinds: step j of the k block, reloaded one block ahead
-  uint32_t meta[NL][NF];
+  uint32_t meta[KBI][NL][NF];
   float s_prev[NL][NF];
   // The prefetch of block kn is issued unconditionally: past the last block
   // (last = true) every lane reads the first 16 bytes of the fragment's block 0
   // instead (one cache line, result unused), so no register keeps two possible
   // values across the loop and no copy has to wait for an outstanding load.
-  auto load_group = [&](int kn, bool last) {
+  auto load_group = [&](auto S, int kn, bool last) {
+    constexpr int SL = decltype(S)::value;
     const uint32_t lo = last ? 0u : loff, mo = last ? 0u : moff;
 #pragma unroll
     for (int l = 0; l < NL; ++l)
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
         const uint8_t* blk = wp[l][nf] + (last ? 0 : (int64_t)kn * BB);  // uniform
-        if constexpr (!streamed<KD>()) load_raw<KD>(raw[l][nf], blk + lo);
-        if constexpr (GMETA) meta[l][nf] = gload<uint32_t>(blk + mo);
+        if constexpr (!streamed<KD>()) load_raw<KD>(raw[SL][l][nf], blk + lo);
+        if constexpr (GMETA) meta[SL][l][nf] = gload<uint32_t>(blk + mo);
       }
   };
   auto load_steps = [&](int kn, bool last, int j) {
@@ -647,7 +658,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 
   stage_load<RB, BM>(sm, 0, abase, soffs, kb0, wave);
   if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, 0, rsbase, rsoff, kb0, wave);
-  load_group(kb0, false);
+  if constexpr (KBI == 2) {
+    if (kb0 + 1 < kb1) {
+      stage_load<RB, BM>(sm, 0, abase, soffs, kb0 + 1, wave, 1);
+      if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, 0, rsbase, rsoff, kb0 + 1, wave, 1);
+    }
+  }
+  load_group(std::integral_constant<int, 0>{}, kb0, false);
+  if constexpr (KBI == 2) load_group(std::integral_constant<int, 1>{}, kb0 + 1, kb0 + 1 >= kb1);
   if constexpr (streamed<KD>()) {
 #pragma unroll
     for (int j = 0; j < J; ++j) load_steps(kb0, false, j);
@@ -655,16 +673,25 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  for (int kb = kb0; kb < kb1; ++kb) {
-    const int cur = (kb - kb0) & 1;
-    const bool more = kb + 1 < kb1;
-    if (more) stage_load<RB, BM>(sm, cur ^ 1, abase, soffs, kb + 1, wave);
-    if constexpr (RSLOAD) {
-      if (more) rowsum_load<BM, MX>(sm, cur ^ 1, rsbase, rsoff, kb + 1, wave);
+  for (int kb = kb0, it = 0; kb < kb1; kb += KBI, ++it) {
+    const int cur = it & 1;
+    const bool more = kb + KBI < kb1;
+#pragma unroll
+    for (int sb = 0; sb < KBI; ++sb) {
+      if (kb + KBI + sb < kb1) {
+        stage_load<RB, BM>(sm, cur ^ 1, abase, soffs, kb + KBI + sb, wave, sb);
+        if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, cur ^ 1, rsbase, rsoff, kb + KBI + sb, wave, sb);
+      }
     }
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
+    // one k block (kbs = kb + SL) of the step
+    auto kstep = [&](auto S) {
+    constexpr int SL = decltype(S)::value;
+    const int kbs = kb + SL;
+    const int ra = SL * BM;   // first staged row of this k block
+    const int rs0 = SL * 64;  // its per-row values
     Raw<KD> rw[NL][NF];
     uint32_t bz[NL][NF];
     float zf[NL][NF];
@@ -674,29 +701,29 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     for (int l = 0; l < NL; ++l)
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
-        if constexpr (!GSC) rw[l][nf] = raw[l][nf];
+        if constexpr (!GSC && KBI == 1) rw[l][nf] = raw[0][l][nf];
         bz[l][nf] = 0;
         zf[l][nf] = 0.f;
         wsc[l][nf] = 0.f;
         wsx[l][nf] = 0u;
-        if constexpr (MX) wsx[l][nf] = (meta[l][nf] >> (8 * q)) & 0xFFu;
+        if constexpr (MX) wsx[l][nf] = (meta[SL][l][nf] >> (8 * q)) & 0xFFu;
         if constexpr (GSC)  // (the 1/16 undoes the x16 of the widened nibbles, exactly)
-          wsc[l][nf] = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu)) * 0.0625f;
+          wsc[l][nf] = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[SL][l][nf] & 0xFFFFu)) * 0.0625f;
         if constexpr (WONLY) {
-          const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] & 0xFFFFu));
-          const float z = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[l][nf] >> 16));
+          const float s = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[SL][l][nf] & 0xFFFFu));
+          const float z = (float)__builtin_bit_cast(_Float16, (uint16_t)(meta[SL][l][nf] >> 16));
           zf[l][nf] = z;
           if constexpr (MAGIC) {
             const uint32_t base = ACT == MXMOE_BF16 ? 0x43004300u : 0x64006400u;
             bz[l][nf] = base + (uint32_t)(wbias<KD>() - (int)z) * 0x00010001u;
           }
           // move the running sum into units of this group's scale
-          const float r = kb != kb0 ? s_prev[l][nf] * __builtin_amdgcn_rcpf(s) : 0.f;
+          const float r = kbs != kb0 ? s_prev[l][nf] * __builtin_amdgcn_rcpf(s) : 0.f;
           s_prev[l][nf] = s;
 #pragma unroll
           for (int mf = 0; mf < MF; ++mf) {
             f32x4 cr = {0, 0, 0, 0};
-            if constexpr (RSUM) cr = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][mf * 16 + 4 * q]) * (-CB);
+            if constexpr (RSUM) cr = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][rs0 + mf * 16 + 4 * q]) * (-CB);
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[l][nf][mf][i] = __builtin_fmaf(acc[l][nf][mf][i], r, cr[i]);
           }
@@ -711,12 +738,20 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
         for (int l = 0; l < NL; ++l)
 #pragma unroll
-          for (int nf = 0; nf < NF; ++nf) gwf[j][l][nf] = wfrag8<KD>(raw[l][nf], u32x4{0u, 0u, 0u, 0u}, j);
+          for (int nf = 0; nf < NF; ++nf) gwf[j][l][nf] = wfrag8<KD>(raw[SL][l][nf], u32x4{0u, 0u, 0u, 0u}, j);
     }
-    load_group(kb + 1, !more);
-    // keep the prefetch here: the scheduler would otherwise sink it below the
-    // MFMAs, next to its first use
-    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (KBI == 1) {
+      load_group(S, kb + 1, !more);
+      // keep the prefetch here: the scheduler would otherwise sink it below the
+      // MFMAs, next to its first use
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // the weight operands of this k block: the copy (one step per block), or
+    // the slot itself, refilled only after the MFMAs below
+    auto& wr = [&]() -> Raw<KD>(&)[NL][NF] {
+      if constexpr (KBI == 1) return rw;
+      else return raw[SL];
+    }();
 
     if constexpr (MX) {
       // mxfp4: one scaled FP4 MFMA per (row fragment, channel fragment) covers
@@ -724,14 +759,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       // row (channel) with the E8M0 scale of that 32-wide block
 #pragma unroll
       for (int mf = 0; mf < MF; ++mf) {
-        const u32x4 af = act_frag<RB>(sm, cur, mf * 16 + li, q);
-        const int sa = (int)((__float_as_uint(sm.rsum[cur][mf * 16 + li]) >> (8 * q)) & 0xFFu);
+        const u32x4 af = act_frag<RB>(sm, cur, ra + mf * 16 + li, q);
+        const int sa = (int)((__float_as_uint(sm.rsum[cur][rs0 + mf * 16 + li]) >> (8 * q)) & 0xFFu);
         const i32x8 A = {(int)af[0], (int)af[1], (int)af[2], (int)af[3], 0, 0, 0, 0};
 #pragma unroll
         for (int l = 0; l < NL; ++l)
 #pragma unroll
           for (int nf = 0; nf < NF; ++nf) {
-            const u32x4 w = rw[l][nf].d[0];
+            const u32x4 w = wr[l][nf].d[0];
             const i32x8 B = {(int)w[0], (int)w[1], (int)w[2], (int)w[3], 0, 0, 0, 0};
             acc[l][nf][mf] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(A, B, acc[l][nf][mf], 4, 4, 0, sa, 0,
                                                                              (int)wsx[l][nf]);
@@ -747,8 +782,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         OpT af[J];
 #pragma unroll
         for (int j = 0; j < J; ++j)
-          af[j] = __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, mf * 16 + li, 4 * j + q));
-        const f32x4 sa = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][mf * 16 + 4 * q]);
+          af[j] = __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, ra + mf * 16 + li, 4 * j + q));
+        const f32x4 sa = *reinterpret_cast<const f32x4*>(&sm.rsum[cur][rs0 + mf * 16 + 4 * q]);
 #pragma unroll
         for (int l = 0; l < NL; ++l)
 #pragma unroll
@@ -766,11 +801,11 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     for (int j = 0; j < J; ++j) {
       auto wop = [&](int l, int nf) -> OpT {
         const u32x4 sv = streamed<KD>() ? st[j][l][nf] : u32x4{0u, 0u, 0u, 0u};
-        if constexpr (INT) return wfrag8<KD>(rw[l][nf], sv, j);
-        else return wfrag16<KD, ACT>(rw[l][nf], sv, j, bz[l][nf], zf[l][nf]);
+        if constexpr (INT) return wfrag8<KD>(wr[l][nf], sv, j);
+        else return wfrag16<KD, ACT>(wr[l][nf], sv, j, bz[l][nf], zf[l][nf]);
       };
       auto aop = [&](int mf) -> OpT {
-        return __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, mf * 16 + li, 4 * j + q));
+        return __builtin_bit_cast(OpT, act_frag<RB>(sm, cur, ra + mf * 16 + li, 4 * j + q));
       };
       auto mma = [&](const OpT& af, const OpT& wf, AccT c) -> AccT {
         if constexpr (INT) return __builtin_amdgcn_mfma_i32_16x16x64_i8(af, wf, c, 0, 0, 0);
@@ -821,12 +856,23 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       }
     }
     }
+    if constexpr (KBI == 2) {
+      // this slot's registers are free: prefetch the k block one step ahead
+      load_group(S, kbs + KBI, kbs + KBI >= kb1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    };  // kstep
+    kstep(std::integral_constant<int, 0>{});
+    if constexpr (KBI == 2) {
+      if (kb + 1 < kb1) kstep(std::integral_constant<int, 1>{});
+    }
     // Last k block: claim the next tile and bring its entry into LDS (the
     // entry is read at the top of the tile loop, after the final barrier).
     if (!more && tid == 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
-    // The next stage has landed once no more than the weight prefetch is
-    // outstanding (vector-memory loads complete in issue order).
-    if (more) wait_vmem<kLoadsAfterStage>();
+    // The next stages have landed once no more than the weight prefetch is
+    // outstanding (vector-memory loads complete in issue order; when more
+    // steps follow, every k block of this one issued its prefetch).
+    if (more) wait_vmem<kLoadsAfterStage * KBI>();
     else wait_vmem<0>();
     lds_barrier();
   }
