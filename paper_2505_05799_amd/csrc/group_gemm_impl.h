@@ -961,78 +961,96 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         if constexpr (INT && !GSC) cs[l][nf] = nf < nvalid ? lins[l]->wscale[16 * (nb0 + nf) + li] : 0.f;
         if constexpr (WONLY) cs[l][nf] = s_prev[l][nf];
       }
+    // value of accumulator (l, nf, mf, i) after the scheme's scales
+    auto outv = [&](int l, int nf, int mf, int i, const f32x4& rs) -> float {
+      if constexpr (INT && !GSC) {
+        int iv = acc[l][nf][mf][i];
+        if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
+        return ((float)iv * rs[i]) * cs[l][nf];
+      } else {
+        return acc[l][nf][mf][i] * cs[l][nf];
+      }
+    };
+    if constexpr (PHASE == 0) {
+      // h = SiLU(g) u of the tile goes to LDS first (rows of BN values, the
+      // idle stage buffers), then out in 16-byte row pieces; the h row sums of
+      // a bias-dequantized down projection are added from the same LDS rows
+      constexpr int HP = BN + 8;  // row pitch in elements (16-byte pad: reads of 16 rows hit distinct banks)
+      static_assert(BM * HP * 2 <= 2 * STAGE_BYTES, "h tile fits the stage buffers");
+      uint16_t* hl = reinterpret_cast<uint16_t*>(&sm.act[0][0]);
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const int r = mf * 16 + 4 * q;
+        const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
+#pragma unroll
+        for (int nf = 0; nf < NF; ++nf) {
+          if (nf >= nvalid) continue;
+          const int c = (wave * NF + nf) * 16 + li;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            hl[(r + i) * HP + c] = f32_to_act<ACT>(silu_f32(outv(0, nf, mf, i, rs)) * outv(1, nf, mf, i, rs));
+        }
+      }
+      lds_barrier();
+      constexpr int CH = BN / 8;  // 16-byte pieces of a tile row
+      int nch = (N - nt * BN) / 8;
+      nch = nch > CH ? CH : nch;
+      uint16_t* hout = reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h);
+      for (int idx = tid; idx < BM * CH; idx += kThreads) {
+        const int r = idx / CH, c = idx % CH;
+        const int ro = sm.rowout[r];
+        if (ro >= 0 && c < nch)
+          *reinterpret_cast<u32x4*>(hout + (int64_t)ro * N + nt * BN + 8 * c) =
+              *reinterpret_cast<const u32x4*>(hl + r * HP + 8 * c);
+      }
+      if (rsh_out) {  // one thread per (row, 128-wide block): its 128 bf16 values in order
+        constexpr int KBT = BN / 128;
+        const int nkb = N / 128;
+        for (int idx = tid; idx < BM * KBT; idx += kThreads) {
+          const int r = idx % BM, j = idx / BM;
+          const int kbg = nt * KBT + j;
+          const int ro = sm.rowout[r];
+          if (ro < 0 || kbg >= nkb) continue;
+          float t = 0.f;
+#pragma unroll
+          for (int c8 = 0; c8 < 16; ++c8) {
+            const u32x4 p = *reinterpret_cast<const u32x4*>(hl + r * HP + 128 * j + 8 * c8);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              t += __uint_as_float(p[e] << 16);
+              t += __uint_as_float(p[e] & 0xFFFF0000u);
+            }
+          }
+          rsh_out[(int64_t)ro * nkb + kbg] = t;
+        }
+      }
+    } else {
 #pragma unroll
     for (int mf = 0; mf < MF; ++mf) {
       const int r = mf * 16 + 4 * q;
       const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
       const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
       const i32x4 ro = *reinterpret_cast<const i32x4*>(&sm.rowout[r]);
-      float hsum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
         if (nf >= nvalid) continue;
         const int n = 16 * (nb0 + nf) + li;
-        float v[NL][4];
-#pragma unroll
-        for (int l = 0; l < NL; ++l)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            if constexpr (INT && !GSC) {
-              int iv = acc[l][nf][mf][i];
-              if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
-              v[l][i] = ((float)iv * rs[i]) * cs[l][nf];
-            } else {
-              v[l][i] = acc[l][nf][mf][i] * cs[l][nf];
-            }
-          }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int64_t orow = (int64_t)ro[i] * N + n;
-          if constexpr (PHASE == 0) {
-            const uint16_t hv = f32_to_act<ACT>(silu_f32(v[0][i]) * v[1][i]);
-            hsum[i] += __uint_as_float((uint32_t)hv << 16);  // bf16 value (used only for bf16)
-            if (GUARD && ro[i] < 0) continue;
-            reinterpret_cast<uint16_t*>(shared ? a.h_shared : a.h)[orow] = hv;
-          } else if constexpr (PHASE == 1) {
-            if (GUARD && ro[i] < 0) continue;
-            a.slots[orow] = v[0][i] * gwv[i];
+          if (GUARD && ro[i] < 0) continue;
+          if constexpr (PHASE == 1) {
+            a.slots[orow] = outv(0, nf, mf, i, rs) * gwv[i];
+          } else if constexpr (INT && !GSC) {
+            int iv = acc[0][nf][mf][i];
+            if constexpr (KD == K_W4A4) iv >>= 4;
+            reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
           } else {
-            if (GUARD && ro[i] < 0) continue;
-            if constexpr (INT && !GSC) {
-              int iv = acc[0][nf][mf][i];
-              if constexpr (KD == K_W4A4) iv >>= 4;
-              reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
-            } else {
-              reinterpret_cast<float*>(a.raw_out)[orow] = v[0][i];
-            }
+            reinterpret_cast<float*>(a.raw_out)[orow] = outv(0, nf, mf, i, rs);
           }
         }
       }
-      if constexpr (PHASE == 0) {
-        if (rsh_out) {  // each lane's partial row sums go to LDS (the stages are idle here)
-          float* part = reinterpret_cast<float*>(sm.act[0]);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) part[(wave * BM + r + i) * 16 + li] = hsum[i];
-        }
-      }
     }
-    if constexpr (PHASE == 0) {
-      if (rsh_out) {  // the lanes and wavefronts of one 128-wide block add their sums
-        lds_barrier();
-        constexpr int KBT = BN / 128, WPK = 4 / KBT;
-        if (tid < BM * KBT) {
-          const int r = tid % BM, j = tid / BM;
-          const int kbg = nt * KBT + j, nkb = N / 128;
-          const float* part = reinterpret_cast<const float*>(sm.act[0]);
-          float t = 0.f;
-#pragma unroll
-          for (int w = 0; w < WPK; ++w)
-#pragma unroll
-            for (int c = 0; c < 16; ++c) t += part[((j * WPK + w) * BM + r) * 16 + c];
-          const int ro = sm.rowout[r];
-          if (ro >= 0 && kbg < nkb) rsh_out[(int64_t)ro * nkb + kbg] = t;
-        }
-      }
     }
   };
   if (finish) {
