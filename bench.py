@@ -84,6 +84,46 @@ def roofline(groups, phase, t_s, traffic=None):
     return out
 
 
+def per_group(mb, blk, x, ids, w, groups, reps=5):
+    """Groups of one phase with the same scheme and the same bound (HBM when
+    moving the group's bytes at 8 TB/s takes longer than its MFMA work at the
+    dtype's peak, else MFMA), each timed alone with an expert mask (the launch
+    then holds only their tiles), against the roof of its bound."""
+    import torch
+    from paper_2505_05799_amd import mxmoe as M
+    cfg = blk.cfg
+    G = cfg.E + cfg.n_shared
+    classes = {}
+    for g in groups:
+        t_mem = g["bytes"] / HBM_PEAK
+        t_mma = g["flops"] / MFMA_PEAK[g["dtype"]]
+        key = (g["phase"], g["scheme"], "hbm" if t_mem > t_mma else "mfma")
+        classes.setdefault(key, []).append(g)
+    out = []
+    ev = M.PhaseEvents()
+    for (phase, scheme, bound), gs in sorted(classes.items()):
+        mask = [0] * G
+        for g in gs:
+            mask[g["expert"]] = 1
+        for _ in range(2):
+            mb.forward(x, ids, w, expert_mask=mask, skip_combine=True)
+        ts = []
+        for _ in range(reps):
+            mb.forward(x, ids, w, expert_mask=mask, skip_combine=True, events=ev)
+            torch.cuda.synchronize()
+            ts.append(ev.elapsed_ms()[1 if phase == 0 else 3])
+        t = float(np.median(ts)) / 1e3
+        if bound == "hbm":
+            frac = sum(g["bytes"] for g in gs) / t / HBM_PEAK
+        else:
+            frac = sum(g["flops"] / MFMA_PEAK[g["dtype"]] for g in gs) / t
+        rows = [g["m"] for g in gs]
+        out.append({"phase": "gate_up" if phase == 0 else "down", "scheme": scheme, "bound": bound,
+                    "experts": len(gs), "rows": [min(rows), max(rows)], "ms_alone": round(t * 1e3, 4),
+                    "frac": round(frac, 3)})
+    return out
+
+
 def measured_traffic(workload, phase):
     """HBM bytes per launch from the committed counter summary of this workload
     and phase, or None if there is none or the kernel sources changed since."""
@@ -208,6 +248,7 @@ def main():
                     help="one Group-GEMM launch vs per-expert launches of the same micro-kernels "
                          "(60 experts [2816, 2048], top-4, 512 tokens); one JSON line per scheme")
     ap.add_argument("--zipf", type=float, default=1.5, help="router skew of --compare-per-expert")
+    ap.add_argument("--no-groups", action="store_true", help="skip the per-group roofline breakdown")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -288,6 +329,9 @@ def main():
         "roofline_down": down,
         "phases_ms": {n: round(float(v), 4) for n, v in zip(M.PHASE_NAMES, ph_mean)},
     }
+    if not args.no_groups:
+        log("[bench] per-group rooflines (each class of groups timed alone)")
+        rec["groups"] = per_group(mb, blk, x, ids, w, groups)
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle on {args.cpu_tokens} tokens")
         rec["cpu_baseline"] = cpu_baseline(blk, args.cpu_tokens)
