@@ -5,7 +5,10 @@
 
 One step = one full block forward through libmxmoe (routing, plan, activation
 quantization, gate/up Group-GEMM with fused SiLU-gate, h quantization, down
-Group-GEMM, combine) on synthetic inputs already resident in HBM.  Prints one
+Group-GEMM, combine) on synthetic inputs already resident in HBM.  The timed
+steps carry no per-phase events (those run in separate eager forwards after
+the timed region); --graph times replays of the forward captured once in a
+HIP graph instead.  Prints one
 JSON line: effective TFLOP/s (2*m*N*K over real routed rows, summed over all
 linears) and microseconds per layer, the roofline of the dominant kernel (the
 gate/up Group-GEMM launch, timed with HIP events on the library's stream), and
@@ -249,6 +252,8 @@ def main():
                          "(60 experts [2816, 2048], top-4, 512 tokens); one JSON line per scheme")
     ap.add_argument("--zipf", type=float, default=1.5, help="router skew of --compare-per-expert")
     ap.add_argument("--no-groups", action="store_true", help="skip the per-group roofline breakdown")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the forward captured in a HIP graph instead of eager forwards")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -290,15 +295,39 @@ def main():
     for _ in range(args.warmup):
         mb.forward(x, ids, w, y=y)
     torch.cuda.synchronize()
-    evs = [M.PhaseEvents() for _ in range(args.steps)]
-    log(f"[bench] timing {args.steps} steps")
+    graph = None
+    if args.graph:
+        # the whole forward captured once; a replay issues the same kernels
+        # without host launch overhead between them
+        cs = torch.cuda.Stream()
+        cs.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cs):
+            mb.forward(x, ids, w, y=y)
+        torch.cuda.current_stream().wait_stream(cs)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            mb.forward(x, ids, w, y=y)
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps ({'eager' if graph is None else 'graph replays'})")
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(args.steps):
-        mb.forward(x, ids, w, y=y, events=evs[i])
+        if graph is None:
+            mb.forward(x, ids, w, y=y)
+        else:
+            graph.replay()
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     ms = (t2 - t1) * 1e3 / args.steps
+    # per-phase launch durations: eager forwards with HIP events on the
+    # library's stream (not part of the timed region)
+    evs = [M.PhaseEvents() for _ in range(args.steps)]
+    for i in range(args.steps):
+        mb.forward(x, ids, w, y=y, events=evs[i])
+    torch.cuda.synchronize()
     phases = np.array([e.elapsed_ms() for e in evs])          # [steps, 5]
     ph_mean = phases.mean(axis=0)
     groups = group_stats(blk, counts)
@@ -328,6 +357,7 @@ def main():
         "roofline": roof,
         "roofline_down": down,
         "phases_ms": {n: round(float(v), 4) for n, v in zip(M.PHASE_NAMES, ph_mean)},
+        "timing": "eager forwards" if graph is None else "replays of the forward captured in a HIP graph",
     }
     if not args.no_groups:
         log("[bench] per-group rooflines (each class of groups timed alone)")
