@@ -614,12 +614,19 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const uint32_t loff = (uint32_t)lane * LB;
   const uint32_t moff = 64u * LB + 4u * li;  // this lane's channel in the group metadata
 
-  // Tiles of at most 32 rows of the kinds with at most 16 bytes per lane and
-  // k block take two k blocks per step: both blocks' stages and weights are in
-  // flight together, which halves the memory round trips a short tile waits
-  // for (its MFMA work per block is too small to hide one).  Slot s of the
-  // weight registers serves k block kb + s and is refilled right after use.
-  constexpr int KBI = (BM <= 32 && !streamed<KD>() && LB <= 16) ? 2 : 1;
+  // Some tiles take two k blocks per step: both blocks' stages and weights
+  // are in flight together, which doubles the prefetch distance and halves
+  // the barriers per block.  Tiles of at most 32 rows with at most 16 weight
+  // bytes per lane and block gain most (their MFMA work per block is too
+  // small to hide one memory round trip); down tiles gain a little at any
+  // size whose two-block stage fits one stage buffer, gate/up tiles of more
+  // rows lose a little (their two weight sets already fill the registers).
+  // Slot s of the weight registers serves k block kb + s and is refilled
+  // right after its MFMAs (no register copy).  The per-row values of the
+  // second block sit at rsum[buf][64..], so tiles with them stop at 64 rows.
+  constexpr bool KBI_FITS = !streamed<KD>() && BM * RB * 2 <= STAGE_BYTES && (!RSLOAD || BM <= 64);
+  constexpr int KBI = (KBI_FITS && (PHASE == 1 || (BM <= 32 && LB <= 16))) ? 2 : 1;
+  static_assert(KBI == 1 || KBI_FITS, "two-block stage layout");
   Raw<KD> raw[KBI][NL][NF];   // low-bit kinds: next group(s), prefetched a step ahead
   u32x4 st[J][NL][NF];   // streamed kinds: step j of the k block, reloaded one block ahead
   uint32_t meta[KBI][NL][NF];
