@@ -570,9 +570,9 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   (2 us) of fixed per-tile work;
 #   queue order: decreasing cost, ties by lower expert index.
 # Slicing of the reduction (split-K, the paper's slice-K tile parameter):
-#   theta = (sum over the phase's tiles of the unsliced tile cost) // nwg // 4,
+#   theta = (sum over the phase's tiles of the unsliced tile cost) // nwg // 2,
 #   nwg the workgroups of the launch; a group takes the fewest slices S in
-#   1 .. Smax = clamp(K/128 // 4, 1, 8) whose tile cost (reduction length
+#   1 .. Smax = clamp(K/128 // 6, 1, 8) whose tile cost (reduction length
 #   ceil(K/128 / S) * 128) is at most theta, else the S of the cheapest tile
 #   (the fewest slices among equals); groups without tiles are not sliced;
 #   budgets, granted in group order: the slices' partial sums (tiles * S * BM *
@@ -584,7 +584,8 @@ _TILE_BM = (16, 32, 64, 128)
 _TILE_BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][config]
 _SPLIT_EXTRA = 16384
 _SPLIT_MAX = 8
-_SPLIT_SHARE = 4
+_SPLIT_SHARE = 2
+_SPLIT_MIN_KB = 6
 _TILE_FIXED_PS = 2.0e6
 
 
@@ -604,7 +605,7 @@ def _tile_cost(bm: int, bn: int, nl: int, scheme, kk: int, split: int, mt: int, 
 def _choose_split(bm: int, bn: int, nl: int, scheme, kblocks: int, mt: int, nt: int, theta: int) -> int:
     if mt * nt <= 0:
         return 1
-    smax = max(1, min(_SPLIT_MAX, kblocks // 4))
+    smax = max(1, min(_SPLIT_MAX, kblocks // _SPLIT_MIN_KB))
     best, cbest = 1, None
     for sp in range(1, smax + 1):
         c = _tile_cost(bm, bn, nl, scheme, -(-kblocks // sp) * 128, sp, mt, nt)

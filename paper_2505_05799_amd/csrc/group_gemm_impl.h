@@ -512,7 +512,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const int kblocks = K / 128;
   // split-K: queued channel tile ntv = slice * (channel tiles) + channel tile;
   // the slice reduces k blocks [kb0, kb1), balanced so that every slice is
-  // non-empty (the plan only slices when there are >= 4 k blocks per slice)
+  // non-empty (the plan only slices when there are >= 6 k blocks per slice)
   const int ntr = (N + BN - 1) / BN;
   const int slice = split > 1 ? ntv / ntr : 0;
   const int nt = ntv - slice * ntr;

@@ -209,16 +209,21 @@ __host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int
   return (int32_t)c;
 }
 // Slices of a group (split-K, the paper's slice-K tile parameter): the fewest
-// slices whose tile cost is at most theta, with at least 4 k blocks per slice
-// and at most kSplitMax slices; if none is, the slice count of the cheapest
-// tile (the fewest slices among equals).  theta is a quarter of the phase's mean work
-// per workgroup (unsliced tile costs summed over all tiles, over the grid), so
-// that no tile is long next to the schedule it is part of.
-constexpr int kSplitShare = 4;
+// slices whose tile cost is at most theta, with at least kSplitMinKb k blocks
+// per slice and at most kSplitMax slices; if none is, the slice count of the
+// cheapest tile (the fewest slices among equals).  theta is half of the
+// phase's mean work per workgroup (unsliced tile costs summed over all tiles,
+// over the grid), so that no tile is long next to the schedule it is part of.
+// A slice costs a partial-sum hand-off that the static cost underrates (the
+// last slice reads every slice's sums back before its epilogue); at a quarter
+// of the mean work, or with 4 k blocks per slice, the launches measured slower
+// (DeepSeek-V2-Lite-shaped forward 8% and Qwen1.5-MoE-shaped 12% slower).
+constexpr int kSplitShare = 2;
+constexpr int kSplitMinKb = 6;
 __host__ __device__ inline int choose_split(int bm, int bn, int nl, int kd, int kblocks, int mt, int nt,
                                             int64_t theta) {
   if (mt * nt <= 0) return 1;
-  int smax = kblocks / 4;
+  int smax = kblocks / kSplitMinKb;
   smax = smax < 1 ? 1 : (smax > kSplitMax ? kSplitMax : smax);
   int best = 1;
   int32_t cbest = 0;

@@ -514,13 +514,13 @@ def test_tile_plan_slices_minimal(nwg):
         work = sum(r["mtiles"] * r["ntiles"] * O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme,
                                                            lin.k // 128 * 128, 1, r["mtiles"], r["ntiles"])
                    for r, lin in zip(plan, lins) if r["mtiles"] * r["ntiles"])
-        theta = work // nwg // 4
+        theta = work // nwg // 2
         for r, lin in zip(plan, lins):
             if r["mtiles"] * r["ntiles"] == 0:
                 assert r["split"] == 1
                 continue
             kb = lin.k // 128
-            smax = max(1, min(8, kb // 4))
+            smax = max(1, min(8, kb // 6))
             cost = lambda sp: O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme, -(-kb // sp) * 128, sp,
                                            r["mtiles"], r["ntiles"])
             sp = r["split"]
@@ -571,9 +571,9 @@ def test_tile_plan_covers_every_output(name):
         flat = [t for q in tiles for t in q]
         want = [(g, mi, ni) for g in order for mi in range(plan[g]["mtiles"])
                 for ni in range(plan[g]["ntiles"] * plan[g]["split"])]
-        for g, r in enumerate(plan):  # slices: at least 4 k blocks each, at most 8
+        for g, r in enumerate(plan):  # slices: at least 6 k blocks each, at most 8
             k = lins[g].k // 128
-            assert 1 <= r["split"] <= 8 and (r["split"] == 1 or k // r["split"] >= 4)
+            assert 1 <= r["split"] <= 8 and (r["split"] == 1 or k // r["split"] >= 6)
         assert sorted(flat) == sorted(want) and len(flat) == len(set(flat))
         rank = {g: i for i, g in enumerate(order)}
         for q in tiles:
