@@ -369,8 +369,10 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     ga.rsx = rs;
   }
   const int grid = group_gemm_grid(current_device());
+  XPrep nox;
+  memset(&nox, 0, sizeof(nox));
   hipError_t e = launch_plan(nullptr, 1, 1, m, nullptr, nullptr, m, dl, nullptr, ga.plan, w.qcap, w.fcap, w.pfloats,
-                             nullptr, grid, stream);
+                             nullptr, grid, nox, stream);
   if (e != hipSuccess) return MXMOE_ERR_HIP;
   return hip_status(launch_group_gemm(ga, 2, grid, stream));
 }
@@ -537,21 +539,33 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   DevLinear none;
   memset(&none, 0, sizeof(none));
   const int grid = group_gemm_grid(current_device());
+  // the encodings of x ride on the plan launch (its spare workgroups; x is
+  // 16-byte aligned, checked above)
+  XPrep xp;
+  memset(&xp, 0, sizeof(xp));
+  xp.x = x;
+  xp.act = bi.act;
+  xp.rows = T;
+  xp.cols = bi.H;
+  if (bi.any_x8) {
+    xp.q8 = at<int8_t>(workspace, L.xq8);
+    xp.s8 = at<float>(workspace, L.xs8);
+  }
+  if (bi.any_x4) {
+    xp.q4 = at<int8_t>(workspace, L.xq4);
+    xp.s4 = at<float>(workspace, L.xs4);
+  }
+  if (bi.rs_x) xp.rs = at<float>(workspace, L.rsx);
+  if (bi.any_x4g) {
+    xp.q4g = at<int8_t>(workspace, L.xq4g);
+    xp.s4g = at<float>(workspace, L.xs4g);
+  }
+  if (bi.any_xmx) {
+    xp.qmx = at<uint8_t>(workspace, L.xqmx);
+    xp.smx = at<uint8_t>(workspace, L.xsmx);
+  }
   MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
-                       down_qmax, grid, stream));
-  if (bi.any_x8)
-    MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 127, at<int8_t>(workspace, L.xq8), at<float>(workspace, L.xs8),
-                              stream));
-  if (bi.any_x4)
-    MX_CHECK(launch_act_quant(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4), at<float>(workspace, L.xs4),
-                              stream));
-  if (bi.rs_x) MX_CHECK(launch_rowsum(x, T, bi.H, bi.H, at<float>(workspace, L.rsx), stream));
-  if (bi.any_x4g)
-    MX_CHECK(launch_act_quant_g128(x, bi.act, T, bi.H, bi.H, 7, at<int8_t>(workspace, L.xq4g),
-                                   at<float>(workspace, L.xs4g), stream));
-  if (bi.any_xmx)
-    MX_CHECK(launch_act_quant_mx(x, bi.act, T, bi.H, bi.H, at<uint8_t>(workspace, L.xqmx), at<uint8_t>(workspace, L.xsmx),
-                                 stream));
+                       down_qmax, grid, xp, stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
                            at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
                            at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),

@@ -1,11 +1,14 @@
 // HBM-bound row kernels of the block forward:
 //   * dynamic per-token activation quantization (Sec. 4.2.2; per-token
-//     granularity a_gsize = -1 of the W5A5 allocation table) for x and for the
-//     gated intermediate h of a8/a4 down projections;
+//     granularity a_gsize = -1 of the W5A5 allocation table) of the gated
+//     intermediate h of a8/a4 down projections, and of the input of a single
+//     linear (the block forward encodes x inside the plan launch, with the
+//     same row encoders);
 //   * the weighted combine of Eq. (2): the per-slot down rows, already scaled
 //     by their gate weight, are summed in a fixed order in fp32 and rounded
 //     once to the activation dtype.
 #include "mxmoe_internal.h"
+#include "rowquant.h"
 
 namespace mxmoe {
 namespace {
@@ -70,173 +73,6 @@ __global__ void __launch_bounds__(kThreads) act_quant_kernel(const void* a, int 
 
 // ---- one wavefront per row, 16-byte loads (8 elements per lane and chunk)
 constexpr int kRowsPerBlock = kThreads / 64;
-
-__device__ inline void unpack8(uint4 u, int act, float* f) {
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (act == MXMOE_BF16) {
-      f[2 * i] = __uint_as_float(w[i] << 16);
-      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-    } else {
-      const uint16_t lo = (uint16_t)w[i], hi = (uint16_t)(w[i] >> 16);
-      f[2 * i] = (float)__builtin_bit_cast(_Float16, lo);
-      f[2 * i + 1] = (float)__builtin_bit_cast(_Float16, hi);
-    }
-  }
-}
-
-// Largest magnitude of 8 elements as 16-bit magnitude bits (sign cleared,
-// NaNs as 0): for non-negative values the bit order is the value order, so the
-// row maximum equals the fmaxf reduction of quant_row, which skips NaNs.
-__device__ inline uint32_t amax8_bits(uint4 u, uint32_t nan_lo) {
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-  uint32_t m = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t lo = w[i] & 0x7fffu, hi = (w[i] >> 16) & 0x7fffu;
-    m = max(m, lo < nan_lo ? lo : 0u);
-    m = max(m, hi < nan_lo ? hi : 0u);
-  }
-  return m;
-}
-__device__ inline float bits_to_f32(uint32_t b, int act) {
-  if (act == MXMOE_BF16) return __uint_as_float(b << 16);
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)b);
-}
-
-// codes of 8 elements with the same fp32 recipe as quant_row
-__device__ inline uint2 codes8(uint4 u, int act, float inv, float q) {
-  float f[8];
-  unpack8(u, act, f);
-  uint32_t w[2] = {0u, 0u};
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    float r = __builtin_rintf(__fmul_rn(f[i], inv));
-    r = fminf(fmaxf(r, -q), q);
-    w[i >> 2] |= ((uint32_t)(uint8_t)(int8_t)(int)r) << (8 * (i & 3));
-  }
-  return make_uint2(w[0], w[1]);
-}
-
-// Quantizes one row of cols (a multiple of 8) elements with W wavefronts (1:
-// each wavefront of the workgroup takes its own row, 4: the workgroup takes
-// one row).  NC > 0: the row's 16-byte chunks stay in registers
-// (cols <= 512 * W * NC); NC == 0: any length, the row is read twice.
-template <int NC, int W>
-__device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, int act, int qmax,
-                                     uint2* __restrict__ codes, float* __restrict__ scale, uint32_t* red) {
-  const int idx = W == 1 ? (threadIdx.x & 63) : threadIdx.x, nch = cols >> 3;
-  constexpr int kStride = 64 * W;
-  const uint32_t nan_lo = act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;  // smallest NaN magnitude
-  const float q = (float)qmax;
-  uint32_t mb = 0u;
-  uint4 v[NC > 0 ? NC : 1];
-  if constexpr (NC > 0) {
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = idx + kStride * i;
-      v[i] = c < nch ? row[c] : make_uint4(0u, 0u, 0u, 0u);
-    }
-#pragma unroll
-    for (int i = 0; i < NC; ++i) mb = max(mb, amax8_bits(v[i], nan_lo));
-  } else {
-    for (int c = idx; c < nch; c += kStride) mb = max(mb, amax8_bits(row[c], nan_lo));
-  }
-  for (int d = 32; d > 0; d >>= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, d, 64));
-  if constexpr (W > 1) {
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mb;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < W; ++i) mb = max(mb, red[i]);
-  }
-  const float amax = bits_to_f32(mb, act);
-  float inv = 0.f, s = 0.f;
-  if (amax > 0.f) {
-    inv = __fdiv_rn(q, amax);
-    s = __fdiv_rn(amax, q);
-  }
-  if constexpr (NC > 0) {
-#pragma unroll
-    for (int i = 0; i < NC; ++i) {
-      const int c = idx + kStride * i;
-      if (c < nch) codes[c] = codes8(v[i], act, inv, q);
-    }
-  } else {
-    for (int c = idx; c < nch; c += kStride) codes[c] = codes8(row[c], act, inv, q);
-  }
-  if (idx == 0) *scale = s;
-}
-
-// Quantizes one row per block of 128 elements (w4a4-g128 activations), one
-// wavefront: a block is 16 chunks of 8, one per lane of a 16-lane group, whose
-// maximum the group shares; the fp32 recipe of quant_row per block.
-__device__ inline void quant_row_groups(const uint4* __restrict__ row, int cols, int act, int qmax,
-                                        uint2* __restrict__ codes, float* __restrict__ scales) {
-  const int lane = threadIdx.x & 63, nch = cols >> 3;
-  const uint32_t nan_lo = act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;
-  const float q = (float)qmax;
-  for (int c0 = 0; c0 < nch; c0 += 64) {  // nch is a multiple of 16: groups stay whole
-    const int c = c0 + lane;
-    const bool ok = c < nch;
-    const uint4 v = ok ? row[c] : make_uint4(0u, 0u, 0u, 0u);
-    uint32_t mb = amax8_bits(v, nan_lo);
-    for (int d = 1; d < 16; d <<= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, d, 64));
-    const float amax = bits_to_f32(mb, act);
-    float inv = 0.f, sc = 0.f;
-    if (amax > 0.f) {
-      inv = __fdiv_rn(q, amax);
-      sc = __fdiv_rn(amax, q);
-    }
-    if (ok) codes[c] = codes8(v, act, inv, q);
-    if (ok && (lane & 15) == 0) scales[c >> 4] = sc;
-  }
-}
-
-// MXFP4 encoding of one row (OCP MX: FP4 e2m1 elements, one E8M0 scale per 32
-// consecutive values), one wavefront: a lane takes a whole 32-wide block (64
-// bytes) per step.  Shared exponent e = floor(log2(amax)) - 2, clamped to
-// [-127, 127] (-127 for an all-zero block); element = nearest e2m1 value to
-// |a| 2^-e (an exact power-of-two scaling of a 16-bit value), ties to the even
-// code, clamped to 6; the sign is kept unless the magnitude code is 0.
-// Element i of the block is nibble i of its 16 output bytes.
-__device__ inline uint32_t e2m1_mag(float x) {
-  return (uint32_t)(x > 0.25f) + (uint32_t)(x >= 0.75f) + (uint32_t)(x > 1.25f) + (uint32_t)(x >= 1.75f) +
-         (uint32_t)(x > 2.5f) + (uint32_t)(x >= 3.5f) + (uint32_t)(x > 5.0f);
-}
-__device__ inline void quant_row_mx(const uint4* __restrict__ row, int cols, int act, uint4* __restrict__ codes,
-                                    uint8_t* __restrict__ exps) {
-  const int lane = threadIdx.x & 63, nb = cols >> 5;
-  for (int b = lane; b < nb; b += 64) {
-    float v[32];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint4 u = row[4 * b + c];
-      const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint16_t lo = (uint16_t)(w[i] & 0xFFFFu), hi = (uint16_t)(w[i] >> 16);
-        v[8 * c + 2 * i] = act == MXMOE_BF16 ? __uint_as_float((uint32_t)lo << 16) : (float)__builtin_bit_cast(_Float16, lo);
-        v[8 * c + 2 * i + 1] = act == MXMOE_BF16 ? __uint_as_float((uint32_t)hi << 16) : (float)__builtin_bit_cast(_Float16, hi);
-      }
-    }
-    float amax = 0.f;
-#pragma unroll
-    for (int i = 0; i < 32; ++i) amax = fmaxf(amax, fabsf(v[i]));
-    int e = amax > 0.f ? (int)((__float_as_uint(amax) >> 23) & 0xFFu) - 127 - 2 : -127;
-    e = e < -127 ? -127 : (e > 127 ? 127 : e);
-    const float inv = __builtin_amdgcn_ldexpf(1.0f, -e);
-    uint32_t o[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      uint32_t c = e2m1_mag(fabsf(v[i]) * inv);
-      if (v[i] < 0.f && c) c |= 8u;
-      o[i >> 3] |= c << (4 * (i & 7));
-    }
-    codes[b] = make_uint4(o[0], o[1], o[2], o[3]);
-    exps[b] = (uint8_t)(e + 127);
-  }
-}
 
 __global__ void __launch_bounds__(kThreads) act_quant_mx_kernel(const void* a, int act, int rows, int cols,
                                                                 int64_t ld, uint8_t* codes, uint8_t* exps) {
@@ -316,20 +152,7 @@ __global__ void __launch_bounds__(kThreads) rowsum_kernel(const uint16_t* __rest
                                                           int64_t ld, float* __restrict__ out) {
   const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
   if (r >= rows) return;
-  const int lane = threadIdx.x & 63, nch = cols >> 3, nb = cols >> 7;
-  const uint4* row = reinterpret_cast<const uint4*>(a + r * ld);
-  for (int c0 = 0; c0 < nch; c0 += 64) {  // nch is a multiple of 16: groups stay whole
-    const int c = c0 + lane;
-    float sum = 0.f;
-    if (c < nch) {
-      float f[8];
-      unpack8(row[c], MXMOE_BF16, f);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) sum += f[i];
-    }
-    for (int d = 1; d < 16; d <<= 1) sum += __shfl_xor(sum, d, 64);
-    if ((lane & 15) == 0 && c < nch) out[r * nb + (c >> 4)] = sum;
-  }
+  rowsum_row(reinterpret_cast<const uint4*>(a + r * ld), cols, out + r * (cols >> 7));
 }
 
 // 8 outputs per thread.  SC > 0 slots (compile time): every slot row is

@@ -17,6 +17,7 @@
 // slices are queued as extra channel tiles, within fixed budgets of added
 // tiles and of partial-sum storage.
 #include "group_gemm_impl.h"
+#include "rowquant.h"
 
 namespace mxmoe {
 namespace {
@@ -87,7 +88,15 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
                                                     const int32_t* __restrict__ offsets, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
                                                     int qcap, int fcap, int64_t pfloats,
-                                                    int32_t* __restrict__ down_qmax, int nwg) {
+                                                    int32_t* __restrict__ down_qmax, int nwg, XPrep xp) {
+  // workgroups 1.. encode x, one row per wavefront (grid-stride); the plan
+  // below runs on workgroup 0 alone
+  if (blockIdx.x > 0) {
+    const int64_t nw = (int64_t)(gridDim.x - 1) * (blockDim.x >> 6);
+    for (int64_t r = (int64_t)(blockIdx.x - 1) * (blockDim.x >> 6) + (threadIdx.x >> 6); r < xp.rows; r += nw)
+      x_prep_row(xp, r);
+    return;
+  }
   // Every per-group input is read from global memory once, into LDS; the steps
   // below work from LDS and only write the plan out, so their barriers wait
   // for LDS traffic only and the plan's stores drain in the background.
@@ -420,11 +429,15 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
                        int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
-                       hipStream_t s) {
+                       const XPrep& xp, hipStream_t s) {
   MaskBits mb;
   for (int i = 0; i < 64; ++i) mb.w[i] = mask_words ? mask_words[i] : 0xffffffffu;
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin, mb,
-                     plan, qcap, fcap, pfloats, down_qmax, nwg < 1 ? 1 : nwg);
+  if (xp.rows > 0 && ((reinterpret_cast<uintptr_t>(xp.x) & 15) || xp.cols % 128)) return hipErrorInvalidValue;
+  // 16 rows per encoding workgroup, at most 1024 of them (grid-stride beyond)
+  int nxb = xp.rows > 0 ? (xp.rows + 15) / 16 : 0;
+  nxb = nxb < 1024 ? nxb : 1024;
+  hipLaunchKernelGGL(plan_kernel, dim3(1 + nxb), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin,
+                     mb, plan, qcap, fcap, pfloats, down_qmax, nwg < 1 ? 1 : nwg, xp);
   return hipGetLastError();
 }
 

@@ -347,12 +347,31 @@ struct GemmArgs {
   void* raw_out;
 };
 
+// Encodings of the block input x [rows, cols] (16-bit, rows 16-byte aligned,
+// ld = cols, cols a multiple of 128) that the gate/up linears read; a null
+// output pointer skips that encoding.  rows = 0: none.
+struct XPrep {
+  const void* x;
+  int act, rows, cols;
+  int8_t* q8;     // int8 codes [rows, cols], scales s8 [rows]
+  float* s8;
+  int8_t* q4;     // int4 codes (one per byte), scales s4 [rows]
+  float* s4;
+  float* rs;      // bf16 row sums per 128-wide block [rows, cols / 128]
+  int8_t* q4g;    // int4 codes with per-128-group scales s4g [rows, cols / 128]
+  float* s4g;
+  uint8_t* qmx;   // MXFP4 codes [rows, cols / 2], E8M0 bytes smx [rows, cols / 32]
+  uint8_t* smx;
+};
+
 // raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
+// The same launch encodes xp on its other workgroups (they do not wait for
+// the plan, nor it for them).
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
                        int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
-                       hipStream_t s);
+                       const XPrep& xp, hipStream_t s);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

@@ -96,6 +96,42 @@ def test_mx_activation_codes_bit_exact():
         say(f"mx codes {act}: x and {P} routed h rows bit-exact")
 
 
+@pytest.mark.parametrize("H", [256, 4224])
+def test_x_encodings_bit_exact(H):
+    """Every encoding of x that the plan launch writes on its spare workgroups
+    equals the oracle's encoders byte for byte: int8 and int4 codes per token,
+    int4 codes per 128-group, MXFP4 codes and E8M0 bytes; the bf16 row sums
+    per 128-block lie within the rounding of a 128-term fp32 sum.  H = 4224
+    takes rows longer than the register-resident encoder holds."""
+    torch = torch_mod()
+    T = 300 if H == 256 else 37
+    sch = [(W.W8A8, W.W8A8, W.W16), (W.W4A4,) * 3, (W.W2G128,) * 3, (W.W4A4G128,) * 3, (W.MXFP4,) * 3]
+    blk = W.random_small_block(313 + H, T=T, H=H, F=128, E=5, k=2, act="bf16", schemes=sch, skew=0.3)
+    mb, _ = run_block(blk)
+    xv = O.act_values(blk.x, "bf16").astype(np.float32)
+
+    def ws(name, dt, n, shape):
+        return mb.ws_view(name, dt, n, T).cpu().numpy().reshape(shape)
+
+    q8, s8 = O.act_quant(xv, 127)
+    assert np.array_equal(ws("xq8", torch.int8, T * H, (T, H)), q8)
+    assert np.array_equal(ws("xs8", torch.float32, T, (T,)), s8)
+    q4, s4 = O.act_quant(xv, 7)
+    assert np.array_equal(ws("xq4", torch.int8, T * H, (T, H)), q4)
+    assert np.array_equal(ws("xs4", torch.float32, T, (T,)), s4)
+    qg, sg = O.act_quant_groups(xv, 7, 128)
+    assert np.array_equal(ws("xq4g", torch.int8, T * H, (T, H)), qg)
+    assert np.array_equal(ws("xs4g", torch.float32, T * H // 128, (T, H // 128)), sg)
+    qx, ex = O.mx_quant(xv)
+    assert np.array_equal(ws("xqmx", torch.uint8, T * H // 2, (T, H // 2)),
+                          (qx[:, 0::2] | (qx[:, 1::2] << 4)).astype(np.uint8))
+    assert np.array_equal(ws("xsmx", torch.uint8, T * H // 32, (T, H // 32)), ex)
+    rs = ws("rsx", torch.float32, T * H // 128, (T, H // 128)).astype(np.float64)
+    blocks = xv.astype(np.float64).reshape(T, H // 128, 128)
+    assert np.all(np.abs(rs - blocks.sum(-1)) <= 128 * 2.0 ** -24 * np.abs(blocks).sum(-1))
+    say(f"x encodings H={H}: int8, int4, int4-g128, mxfp4 bit-exact; row sums within bound")
+
+
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
 @pytest.mark.parametrize("mix", range(len(MIXES)))
 @pytest.mark.parametrize("T", [1, 37, 300])
