@@ -3,7 +3,8 @@
 // Routing / permutation: stable counting sort of the T*k (token, slot) pairs
 // by expert id, which forms the per-expert row groups X_e of Eq. (2).
 //
-// Three launches, no atomics on anything order-dependent:
+// Three launches (one workgroup for batches of at most kRouteSmall pairs), no
+// atomics on anything order-dependent:
 //   1. route_count   : one workgroup per chunk of kRouteChunk pairs builds the
 //                      chunk's expert histogram (integer LDS atomics: the
 //                      counts do not depend on their order) and the smallest
@@ -50,9 +51,22 @@ __global__ void __launch_bounds__(1024) route_scan(int nchunks, int E, int32_t* 
   __shared__ int32_t tot[kMaxE];
   __shared__ int32_t wsum[16];
   const int tid = threadIdx.x;  // blockDim = 1024 >= E
+  // the chunk histograms are read kBatch chunks at a time (independent loads
+  // in flight together; one at a time, the loop is a chain of memory round
+  // trips: 26 us for 64 chunks)
+  constexpr int kBatch = 16;
   int mine = 0;
-  if (tid < E)
-    for (int c = 0; c < nchunks; ++c) mine += chunk_counts[(int64_t)c * E + tid];
+  if (tid < E) {
+    int c = 0;
+    for (; c + kBatch <= nchunks; c += kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) v[j] = chunk_counts[(int64_t)(c + j) * E + tid];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) mine += v[j];
+    }
+    for (; c < nchunks; ++c) mine += chunk_counts[(int64_t)c * E + tid];
+  }
   // exclusive scan of per-expert totals across the workgroup
   const int lane = tid & 63, w = tid >> 6;
   int incl = mine;
@@ -71,18 +85,30 @@ __global__ void __launch_bounds__(1024) route_scan(int nchunks, int E, int32_t* 
     tot[tid] = excl;
     // chunk bases, in place: chunk_counts[c][e] <- offset of chunk c's first pair of e
     int run = excl;
-    for (int c = 0; c < nchunks; ++c) {
-      int64_t i = (int64_t)c * E + tid;
-      int v = chunk_counts[i];
+    int c = 0;
+    for (; c + kBatch <= nchunks; c += kBatch) {
+      int v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) v[j] = chunk_counts[(int64_t)(c + j) * E + tid];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        chunk_counts[(int64_t)(c + j) * E + tid] = run;
+        run += v[j];
+      }
+    }
+    for (; c < nchunks; ++c) {
+      const int64_t i = (int64_t)c * E + tid;
+      const int v = chunk_counts[i];
       chunk_counts[i] = run;
       run += v;
     }
   }
   if (tid == E - 1) offsets[E] = excl + mine;
-  if (tid == 0) {
+  if (w == 0) {  // smallest out-of-range pair id over the chunks, one wavefront
     int b = 0x7fffffff;
-    for (int c = 0; c < nchunks; ++c) b = min(b, chunk_bad[c]);
-    status[0] = b == 0x7fffffff ? 0 : b + 1;
+    for (int c = lane; c < nchunks; c += 64) b = min(b, chunk_bad[c]);
+    for (int d = 32; d > 0; d >>= 1) b = min(b, __shfl_xor(b, d, 64));
+    if (lane == 0) status[0] = b == 0x7fffffff ? 0 : b + 1;
   }
 }
 
@@ -134,6 +160,96 @@ __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restr
       base[ee] += add;
     }
     __syncthreads();
+  }
+}
+
+// Batches of at most kRouteSmall pairs: the three steps in one workgroup of
+// 1024 threads, with barriers where the launches were.  The pairs are ranked
+// 1024 at a time by the same ballots; positions follow from the expert's base,
+// the counts of earlier wavefronts of the step and the rank in the wavefront,
+// so the order (expert, then pair id) is the one the chunked launches give.
+constexpr int kRouteSmall = 4096;  // one step costs ~1 us: past 4096 pairs the chunked launches win
+constexpr int kSmallThreads = 1024;
+__global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* __restrict__ ids, int P, int E, int ebits,
+                                                             int32_t* __restrict__ counts,
+                                                             int32_t* __restrict__ offsets,
+                                                             int32_t* __restrict__ sorted_pair,
+                                                             int32_t* __restrict__ inv, int32_t* __restrict__ status) {
+  constexpr int NW = kSmallThreads / 64;
+  __shared__ int32_t base[kMaxE];
+  __shared__ int32_t wcnt[NW][kMaxE];
+  __shared__ int32_t wsum[NW];
+  __shared__ int32_t bad;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int e = tid; e < E; e += kSmallThreads) base[e] = 0;
+  if (tid == 0) bad = 0x7fffffff;
+  __syncthreads();
+  // 1. histogram (LDS atomics: the counts do not depend on their order)
+  for (int p = tid; p < P; p += kSmallThreads) {
+    const int e = ids[p];
+    if (e >= 0 && e < E) atomicAdd(&base[e], 1);
+    else atomicMin(&bad, p);
+  }
+  __syncthreads();
+  // 2. exclusive scan of the counts (E <= 1024: one expert per thread)
+  const int mine = tid < E ? base[tid] : 0;
+  int incl = mine;
+  for (int d = 1; d < 64; d <<= 1) {
+    const int v = __shfl_up(incl, d, 64);
+    if (lane >= d) incl += v;
+  }
+  if (lane == 63) wsum[w] = incl;
+  __syncthreads();
+  int excl = incl - mine;
+  for (int i = 0; i < w; ++i) excl += wsum[i];
+  if (tid < E) {
+    counts[tid] = mine;
+    offsets[tid] = excl;
+    base[tid] = excl;  // only this thread read base[tid]
+  }
+  if (tid == E - 1) offsets[E] = excl + mine;
+  if (tid == 0) status[0] = bad == 0x7fffffff ? 0 : bad + 1;
+  // 3. scatter, 1024 pairs per step
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  for (int s = 0; s < P; s += kSmallThreads) {
+    for (int e = tid; e < E; e += kSmallThreads)
+#pragma unroll
+      for (int i = 0; i < NW; ++i) wcnt[i][e] = 0;
+    __syncthreads();
+    const int p = s + tid;
+    int e = -1;
+    if (p < P) {
+      e = ids[p];
+      if (e < 0 || e >= E) e = -1;
+    }
+    uint64_t same = __ballot(e >= 0);
+    for (int b = 0; b < ebits; ++b) {
+      const bool bit = e >= 0 && ((e >> b) & 1);
+      const uint64_t m = __ballot(bit);
+      same &= bit ? m : ~m;
+    }
+    if (e < 0) same = 0;
+    const int rank = __popcll(same & below);
+    if (e >= 0 && rank == 0) wcnt[w][e] = __popcll(same);
+    __syncthreads();
+    if (e >= 0) {
+      int pos = base[e] + rank;
+      for (int i = 0; i < w; ++i) pos += wcnt[i][e];
+      sorted_pair[pos] = p;
+      inv[p] = pos;
+    } else if (p < P) {
+      inv[p] = -1;
+    }
+    __syncthreads();
+    for (int ee = tid; ee < E; ee += kSmallThreads) {
+      int add = 0;
+#pragma unroll
+      for (int i = 0; i < NW; ++i) add += wcnt[i][ee];
+      base[ee] += add;
+    }
+    // (no barrier here: thread t alone updates base[t], t + 1024, ... and
+    // clears the same columns of wcnt at the next step, whose first barrier
+    // orders both before any other thread reads them)
   }
 }
 
@@ -238,6 +354,11 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
   const int nchunks = (P + kRouteChunk - 1) / kRouteChunk;
   int ebits = 0;
   while ((1 << ebits) < E) ++ebits;
+  if (P <= kRouteSmall) {
+    hipLaunchKernelGGL(route_small, dim3(1), dim3(kSmallThreads), 0, s, ids, P, E, ebits, counts, offsets,
+                       sorted_pair, inv, status);
+    return hipGetLastError();
+  }
   if (nchunks > 0) {
     hipLaunchKernelGGL(route_count, dim3(nchunks), dim3(kThreads), 0, s, ids, P, E, chunk_counts, chunk_bad);
     hipError_t err = hipGetLastError();

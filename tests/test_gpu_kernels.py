@@ -36,10 +36,13 @@ def test_pack_roundtrip(scheme, act):
 
 
 # ---------------------------------------------------------------- routing
+# batches of up to 4096 pairs take the one-workgroup kernel, larger ones the
+# chunked launches (1024 x 4 sits at the limit, 4097 x 1 just past it)
 ROUTE_CASES = [(1, 1, 1, "uniform"), (64, 2, 4, "uniform"), (257, 6, 64, "uniform"),
                (2049, 8, 64, "uniform"), (1000, 4, 60, "skew"), (300, 2, 8, "one"),
                (0, 2, 4, "uniform"), (513, 3, 7, "bad"), (5000, 2, 1024, "uniform"),
-               (16384, 8, 64, "zipf")]
+               (16384, 8, 64, "zipf"), (1024, 4, 64, "zipf"), (4097, 1, 16, "uniform"),
+               (6000, 3, 7, "bad")]
 
 
 def _ids(T, k, E, kind, seed):
