@@ -17,6 +17,9 @@
  *   w8a8     8-bit per-output-channel symmetric weights (fp32 scale, codes in
  *            [-127,127]) and 8-bit per-token symmetric activations
  *   w4a4     same with 4 bits (codes in [-7,7])
+ *   fp8      OCP FP8 e4m3 weights with an fp32 scale per output channel and
+ *            e4m3 activations with an fp32 scale per token (the 8-bit
+ *            floating-point operand of the MI355X matrix cores)
  *
  * Activations of w8a8 / w4a4 linears are quantized at run time, per token
  * (Sec. 4.2.2): amax = max|a|, inv = fl32(qmax/amax), s = fl32(amax/qmax),
@@ -74,6 +77,13 @@ typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
  *                    scale per 32 consecutive k; activations are encoded at
  *                    run time (e = floor(log2 amax) - 2, elements rounded to
  *                    nearest, ties to even, clamped to 6)
+ *   {8,8,-1,-1,1} with fmt = 2: fp8, OCP FP8 e4m3 elements (sign bit 7,
+ *                    exponent bias 7, no infinities, 448 the largest finite
+ *                    value) on both operands; fp32 scale per output channel
+ *                    (weights) and per token (activations, encoded at run
+ *                    time with the recipe above and 448 in place of qmax:
+ *                    element = nearest e4m3 value of fl32(a*inv), ties to the
+ *                    even code, magnitudes past 448 give 448)
  * All other combinations have fmt = 0.                                       */
 typedef struct {
   int32_t w_bits;
@@ -81,7 +91,8 @@ typedef struct {
   int32_t w_group;    /* 128 or 32 (mxfp4), or -1 = per output channel          */
   int32_t a_group;    /* 128 or 32 (mxfp4), or -1 = per token                   */
   int32_t symmetric;  /* 1 for w8a8 / w4a4 (per channel or g128) and mxfp4      */
-  int32_t fmt;        /* 0: integer codes; 1: OCP MX floating point (mxfp4)     */
+  int32_t fmt;        /* 0: integer codes; 1: OCP MX floating point (mxfp4);
+                         2: FP8 e4m3 with per-channel / per-token scales       */
 } mxmoe_scheme;
 
 /* One linear block y = x W^T with W of shape [n, k] = [out, in].
@@ -96,7 +107,7 @@ typedef struct {
 
 /* Bytes of the packed form of linear *L (host) for activations `act`:
  *   wNg128: n*k*N/8 + (n*k/128)*4   (N + 0.25 bits per weight, Sec. 5.2)
- *   w8a8/w4a4: n*k*b/8 + 4*n
+ *   w8a8/w4a4/fp8: n*k*b/8 + 4*n
  *   w4a4-g128: n*k/2 + (n*k/128)*4   (fp16 group scale, 4-byte slot per group)
  *   mxfp4: n*k/2 + n*k/32            (4.25 bits per weight)
  *   w16: 2*n*k
@@ -108,8 +119,9 @@ MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
  * to its codes).  Runs once per weight load.
  *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4/w4a4-g128 int8
  *            [n,k] in [-qmax, qmax]; mxfp4 uint8 [n,k] e2m1 codes 0..15
- *            (sign in bit 3); w16: 16-bit weights [n,k] of `w16_src`.
- *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4 fp32 [n];
+ *            (sign in bit 3); fp8 uint8 [n,k] e4m3 bytes (no NaN code);
+ *            w16: 16-bit weights [n,k] of `w16_src`.
+ *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4/fp8 fp32 [n];
  *            mxfp4 uint8 E8M0 [n, k/32]; NULL for w16.
  *   zeros  : wNg128 fp16 [n, k/128] holding integers in [0, 2^N-1]; else NULL.
  *   w16_src: dtype of 16-bit source weights; converted (RNE) to `act`.
@@ -170,7 +182,8 @@ MXMOE_API mxmoe_status mxmoe_router_topk(const float* logits, int32_t T, int32_t
 
 /* Per-row symmetric quantization of a [rows, cols] activation matrix (row
  * stride `ld` elements) with the fp32 recipe in the header comment.
- *   codes: int8 [rows, cols] (dense), scales: fp32 [rows].  qmax = 127 or 7. */
+ *   codes: int8 [rows, cols] (dense), scales: fp32 [rows].  qmax = 127 or 7;
+ *   qmax = 448 writes FP8 e4m3 bytes (the fp8 scheme's activation encoding). */
 MXMOE_API mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32_t cols,
                              int64_t ld, int32_t qmax, int8_t* codes, float* scales,
                              hipStream_t stream);
@@ -188,6 +201,9 @@ MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
  *        times s_a[m,b]*s_w[n,b], added over the blocks in fp32;
  *        mxfp4 -> fp32 [m, n]: a encoded as mxfp4 at run time, products of
  *        the decoded operands accumulated in fp32 by the scaled FP4 MFMA;
+ *        fp8 -> fp32 [m, n]: a encoded as e4m3 per token at run time, the
+ *        e4m3 products accumulated in fp32 by the FP8 MFMA, times
+ *        s_a[m]*s_w[n];
  *        other schemes -> fp32 [m, n] with fp32 accumulation.               */
 MXMOE_API mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
                                   int32_t m, const void* a, void* out, void* workspace,
@@ -314,6 +330,9 @@ typedef struct {
   size_t router_w;      /* fp32 [T, k]: their gate weights                   */
   size_t shared_w;      /* fp32 [T, n_shared]: sigmoid shared gates (-1 if no
                            shared experts)                                   */
+  size_t xqf8, xsf8;    /* uint8 [T, H] e4m3 codes, fp32 [T] scales: x for fp8
+                           gate|up (else -1); h rows of an fp8 down projection
+                           use hq / hs and hq_shared / hs_shared             */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

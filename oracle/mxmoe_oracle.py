@@ -23,6 +23,10 @@ operands the GPU receives (codes, scales, zeros - never the packed layout):
   paper's scheme set S is whatever the hardware supports, Sec. 3.1): a value is
   an FP4 e2m1 element times a power-of-two scale shared by 32 consecutive
   values along K; activations get the same encoding at run time.
+* FP8 (OCP e4m3, the 8-bit floating-point operand of the MI355X matrix cores;
+  again a member of the hardware's scheme set, Sec. 3.1): a weight is an e4m3
+  value times a per-channel fp32 scale, an activation an e4m3 value times a
+  per-token fp32 scale that maps the row's largest magnitude onto 448.
 * Sec. 4.2.2 (end): activations of w8a8 / w4a4 linears are quantized dynamically
   at run time, per token (a_gsize = -1 in the W5A5 allocation table), with the
   fp32 recipe of :func:`act_quant`.
@@ -45,7 +49,7 @@ import numpy as np
 
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "router_topk", "shared_gate", "dequant",
-    "act_quant", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
+    "act_quant", "fp8_quant", "e4m3_values", "e4m3_code", "fp8_block_bound", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
     "silu", "tile_plan", "xcd_queues", "xcd_tiles",
 ]
 
@@ -175,6 +179,8 @@ def dequant(lin, act: str) -> np.ndarray:
         return (sc * (q - z)).reshape(lin.n, lin.k)
     if getattr(s, "fmt", 0) == 1:  # MXFP4: e2m1 element times 2^(E8M0 - 127) of its 32-block
         return _mx_values(lin.codes, lin.scales, s.w_group)
+    if getattr(s, "fmt", 0) == 2:  # FP8: e4m3 element times the channel's fp32 scale
+        return e4m3_values(lin.codes) * lin.scales.astype(np.float64)[:, None]
     if s.w_group > 0:  # symmetric groups (w4a4-g128): code times its group's scale
         g = s.w_group
         q = lin.codes.astype(np.float64).reshape(lin.n, lin.k // g, g)
@@ -210,6 +216,56 @@ def _e2m1_code(x: np.ndarray) -> np.ndarray:
     even = cand & (np.arange(8) % 2 == 0)
     code = np.where(even.any(axis=-1), even.argmax(axis=-1), cand.argmax(axis=-1))
     return np.where(np.asarray(x) > 6.0, 7, code)
+
+
+# FP8 e4m3 (OCP): sign bit 7, four exponent bits (bias 7), three mantissa bits.
+# Exponent field 0 holds the subnormals m/8 * 2^-6; there are no infinities and
+# the magnitude code 0x7F is NaN, so 0x7E = 448 is the largest finite value.
+# Entry c of the table is the value of magnitude code c (0..126), increasing.
+_E4M3 = np.array([(m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7)
+                  for e in range(16) for m in range(8)][:127])
+E4M3_MAX = 448.0
+
+
+def e4m3_values(codes: np.ndarray) -> np.ndarray:
+    """Exact value of e4m3 codes (uint8; NaN codes are not accepted)."""
+    c = np.asarray(codes).astype(np.int64) & 0xFF
+    mag = c & 0x7F
+    if (mag == 0x7F).any():
+        raise ValueError("e4m3 NaN code")
+    return np.where(c & 0x80, -1.0, 1.0) * _E4M3[mag]
+
+
+def e4m3_code(x: np.ndarray) -> np.ndarray:
+    """Magnitude code (0..126) of the e4m3 value nearest to x >= 0; an exact
+    tie takes the even code; at and beyond 448 the code of 448."""
+    x = np.asarray(x, dtype=np.float64)
+    hi = np.clip(np.searchsorted(_E4M3, x, side="left"), 1, 126)   # _E4M3[hi-1] < x <= _E4M3[hi]
+    lo = hi - 1
+    dl = x - _E4M3[lo]
+    dh = _E4M3[hi] - x
+    code = np.where(dl < dh, lo, np.where(dh < dl, hi, np.where(lo % 2 == 0, lo, hi)))
+    return np.where(x >= E4M3_MAX, 126, code)
+
+
+def fp8_quant(a: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
+    """Per-row FP8 e4m3 encoding of activations, evaluated in IEEE fp32 like
+    :func:`act_quant` with 448 in place of qmax: amax = max |a_r|;
+    inv = fl32(448 / amax), s = fl32(amax / 448); element = the e4m3 value
+    nearest to fl32(a * inv) (ties to the even code, magnitudes past 448 give
+    448), the sign kept unless the magnitude code is 0.  An all-zero row gets
+    s = 0 and zero codes.  Returns codes uint8 [rows, cols], scales fp32 [rows]."""
+    a = np.asarray(a, dtype=np.float32)
+    m32 = np.float32(E4M3_MAX)
+    amax = np.abs(a).max(axis=1) if a.shape[1] else np.zeros(a.shape[0], np.float32)
+    zero = amax == 0
+    safe = np.where(zero, np.float32(1), amax).astype(np.float32)
+    inv = (m32 / safe).astype(np.float32)
+    s = np.where(zero, np.float32(0), (safe / m32).astype(np.float32)).astype(np.float32)
+    prod = (a * inv[:, None]).astype(np.float32)
+    mag = np.where(zero[:, None], 0, e4m3_code(np.abs(prod)))
+    code = np.where((prod < 0) & (mag > 0), mag | 0x80, mag)
+    return code.astype(np.uint8), s
 
 
 def mx_quant(a: np.ndarray, block: int = 32) -> Tuple[np.ndarray, np.ndarray]:
@@ -288,6 +344,11 @@ def linear(a: np.ndarray, lin, act: str, w_deq: Optional[np.ndarray] = None,
         # MXFP4: both operands decoded exactly, the product summed in fp64
         qa, ea = mx_quant(a.astype(np.float32), s.a_group)
         return _mx_values(qa, ea, s.a_group) @ dequant(lin, act).T
+    if getattr(s, "fmt", 0) == 2:
+        # FP8: exact sum of the e4m3 products, times s_a[m] * s_w[n]
+        qa, sa = fp8_quant(a.astype(np.float32))
+        acc = e4m3_values(qa) @ e4m3_values(lin.codes).T
+        return acc * sa.astype(np.float64)[:, None] * lin.scales.astype(np.float64)[None, :]
     if s.a_bits < 16 and s.a_group > 0:
         # w4a4-g128: per 128-wide block b, the exact integer dot of the block's
         # codes times s_a[m, b] * s_w[n, b], summed over the blocks in fp64
@@ -338,6 +399,9 @@ def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
     if getattr(lin.scheme, "fmt", 0) == 1:
         qa, ea = mx_quant(a.astype(np.float32), lin.scheme.a_group)
         return _EPS_FLOAT_ACC * (np.abs(_mx_values(qa, ea, lin.scheme.a_group)) @ np.abs(dequant(lin, act)).T)
+    if getattr(lin.scheme, "fmt", 0) == 2:
+        qa, sa = fp8_quant(a.astype(np.float32))
+        return fp8_block_bound(e4m3_values(qa) * sa.astype(np.float64)[:, None], dequant(lin, act))
     if lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
         # fp32 running sum of block products: bounded like an fp32-accumulated GEMM
         # on the dequantized operands
@@ -352,6 +416,23 @@ def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
     return _EPS_FLOAT_ACC * (np.abs(a) @ np.abs(w_deq).T)
 
 
+# The FP8 MFMA does not add the 128 products of a k block in full fp32: on
+# MI355X its result lies within 2^-11.2 of the block's largest product (random
+# and adversarial operands), consistent with products aligned to the largest
+# one and rounded about 16 bits below it.  Bounds charge 2^-9 of
+# max|a| max|w| per block, then fp32 accumulation across blocks.
+_EPS_F8_BLOCK = 2.0 ** -9
+
+
+def fp8_block_bound(ad: np.ndarray, wd: np.ndarray, block: int = 128) -> np.ndarray:
+    """Bound [m, n] on |FP8 GEMM - exact| for decoded (scaled) operands ad [m, k]
+    and wd [n, k]: per k block 2^-9 max|ad| max|wd|, plus 2^-20 sum |ad||wd|."""
+    m, k = ad.shape
+    am = np.abs(ad).reshape(m, k // block, block).max(axis=2)
+    wm = np.abs(wd).reshape(wd.shape[0], k // block, block).max(axis=2)
+    return _EPS_F8_BLOCK * (am @ wm.T) + _EPS_FLOAT_ACC * (np.abs(ad) @ np.abs(wd).T)
+
+
 def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
     """Per-element output slack of an a8/a4 down projection.
 
@@ -364,13 +445,29 @@ def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
     """
     if getattr(lin.scheme, "fmt", 0) == 1:
         return _down_slack_mx(h64, dh, hb, lin, act)
-    qmax = _qmax(lin.scheme.a_bits)
+    fp8 = getattr(lin.scheme, "fmt", 0) == 2
+    # grid value of a scaled element: the clamped integer code, or the signed
+    # e4m3 value (both monotone in the element and in the inverse scale)
+    if fp8:
+        qmax = E4M3_MAX
+
+        def grid(p):
+            return np.sign(p) * _E4M3[e4m3_code(np.abs(p))]
+    else:
+        qmax = _qmax(lin.scheme.a_bits)
+
+        def grid(p):
+            return np.clip(np.rint(p), -qmax, qmax)
     m, F = h64.shape
     g = lin.scheme.a_group if lin.scheme.a_group > 0 else F
     nb = F // g
     lo = round_to_act(h64 - dh, act).reshape(m * nb, g)
     hi = round_to_act(h64 + dh, act).reshape(m * nb, g)
-    q0, s0 = act_quant(hb.astype(np.float32).reshape(m * nb, g), qmax)
+    if fp8:
+        c0, s0 = fp8_quant(hb.astype(np.float32).reshape(m * nb, g))
+        q0 = e4m3_values(c0)
+    else:
+        q0, s0 = act_quant(hb.astype(np.float32).reshape(m * nb, g), qmax)
     alo = np.where(np.sign(lo) == np.sign(hi), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
     ahi = np.maximum(np.abs(lo), np.abs(hi))
     amax_lo = alo.max(axis=1)
@@ -391,8 +488,7 @@ def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
         sc = np.where(zero, np.float32(0), (safe / q32).astype(np.float32))
         ds[rows] = np.maximum(ds[rows], np.abs(sc.astype(np.float64) - s0[rows].astype(np.float64)))
         for hv in (lo[rows], hi[rows]):
-            qc = np.clip(np.rint((hv.astype(np.float32) * inv[:, None]).astype(np.float32)),
-                         -qmax, qmax)
+            qc = grid((hv.astype(np.float32) * inv[:, None]).astype(np.float32))
             qc = np.where(zero[:, None], 0, qc)
             dq[rows] = np.maximum(dq[rows], np.abs(qc - q0[rows]))
     s_max = np.maximum(s0.astype(np.float64), s0.astype(np.float64) + ds)
@@ -631,8 +727,8 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int
     for m, lin in zip(ms, lins):
         m = int(m)  # Python integers: the sums below exceed 32 bits
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
-        if cfg == 3 and lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
-            cfg = 2   # w4a4-g128 groups stop at 64-row tiles
+        if cfg == 3 and lin.scheme.a_bits < 16 and (lin.scheme.a_group > 0 or getattr(lin.scheme, "fmt", 0) == 2):
+            cfg = 2   # w4a4-g128, mxfp4 and fp8 groups stop at 64-row tiles
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-int(lin.n) // bn)

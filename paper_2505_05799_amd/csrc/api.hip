@@ -16,6 +16,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int scheme_kind(const mxmoe_scheme& s) {
   if (s.fmt == 1)  // OCP MX: FP4 e2m1 on both operands, E8M0 scale per 32
     return (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 32 && s.a_group == 32 && s.symmetric == 1) ? K_MXFP4 : -1;
+  if (s.fmt == 2)  // FP8 e4m3: per-channel weight scales, per-token activation scales
+    return (s.w_bits == 8 && s.a_bits == 8 && s.w_group == -1 && s.a_group == -1 && s.symmetric == 1) ? K_F8A8 : -1;
   if (s.fmt != 0) return -1;
   if (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 128 && s.a_group == 128 && s.symmetric == 1) return K_W4A4G;
   if (s.a_group != -1) return -1;
@@ -65,6 +67,7 @@ struct BlockInfo {
   bool rs_x = false, rs_h = false, rs_hsh = false;  // row sums of x / h / h_shared needed (bf16)
   bool any_x4g = false, any_hg = false, any_hg_sh = false;  // w4a4-g128 gate|up, routed / shared down
   bool any_xmx = false, any_hmx = false, any_hmx_sh = false;  // mxfp4 gate|up, routed / shared down
+  bool any_xf8 = false;  // FP8 gate|up
   int kinds[kMaxG][3];
 };
 
@@ -88,6 +91,7 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
   bi->rs_x = bi->rs_h = bi->rs_hsh = false;
   bi->any_x4g = bi->any_hg = bi->any_hg_sh = false;
   bi->any_xmx = bi->any_hmx = bi->any_hmx_sh = false;
+  bi->any_xf8 = false;
   if (bi->G > kMaxG) return MXMOE_ERR_UNSUPPORTED;
   for (int g = 0; g < bi->G; ++g) {
     const mxmoe_scheme* s = B->scheme + 3 * g;
@@ -104,6 +108,7 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
     if (kg == K_W4A4G) bi->any_x4g = true;
     if (bi->kinds[g][2] == K_W4A4G) (sh ? bi->any_hg_sh : bi->any_hg) = true;
     if (kg == K_MXFP4) bi->any_xmx = true;
+    if (kg == K_F8A8) bi->any_xf8 = true;
     if (bi->kinds[g][2] == K_MXFP4) (sh ? bi->any_hmx_sh : bi->any_hmx) = true;
     if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(kg)) bi->rs_x = true;
@@ -164,6 +169,8 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.hsmx = bi.any_hmx ? take(P * bi.F / 32) : kNone;
   L.hqmx_shared = bi.any_hmx_sh ? take((size_t)bi.nsh * T * bi.Fsh / 2) : kNone;
   L.hsmx_shared = bi.any_hmx_sh ? take((size_t)bi.nsh * T * bi.Fsh / 32) : kNone;
+  L.xqf8 = bi.any_xf8 ? take((size_t)T * bi.H) : kNone;
+  L.xsf8 = bi.any_xf8 ? take(4 * (size_t)T) : kNone;
   L.rids = take(4 * P);
   L.rw = take(4 * P);
   L.shw = bi.nsh ? take(4 * (size_t)T * bi.nsh) : kNone;
@@ -273,7 +280,7 @@ mxmoe_status mxmoe_router_topk(const float* logits, int32_t T, int32_t E, int32_
 mxmoe_status mxmoe_act_quant(const void* a, mxmoe_dtype act, int32_t rows, int32_t cols, int64_t ld, int32_t qmax,
                              int8_t* codes, float* scales, hipStream_t stream) {
   if (!valid_dtype(act) || rows < 0 || cols <= 0 || ld < cols) return MXMOE_ERR_INVALID_ARG;
-  if (qmax != 127 && qmax != 7) return MXMOE_ERR_UNSUPPORTED;
+  if (qmax != 127 && qmax != 7 && qmax != kQmaxF8) return MXMOE_ERR_UNSUPPORTED;
   if (rows > 0 && (!a || !codes || !scales)) return MXMOE_ERR_INVALID_ARG;
   return hip_status(launch_act_quant(a, act, rows, cols, ld, qmax, codes, scales, stream));
 }
@@ -353,6 +360,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
                                  : launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; }
+    else if (kd == K_F8A8) { ga.xqf8 = reinterpret_cast<const uint8_t*>(aq); ga.xsf8 = as; }
     else if (kd == K_W4A4G) { ga.xq4g = aq; ga.xs4g = as; }
     else { ga.xq4 = aq; ga.xs4 = as; }
   }
@@ -458,6 +466,8 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->hsmx = L.hsmx;
   out->hqmx_shared = L.hqmx_shared;
   out->hsmx_shared = L.hsmx_shared;
+  out->xqf8 = L.xqf8;
+  out->xsf8 = L.xsf8;
   out->router_ids = L.rids;
   out->router_w = L.rw;
   out->shared_w = L.shw;
@@ -564,6 +574,10 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     xp.qmx = at<uint8_t>(workspace, L.xqmx);
     xp.smx = at<uint8_t>(workspace, L.xsmx);
   }
+  if (bi.any_xf8) {
+    xp.qf8 = at<uint8_t>(workspace, L.xqf8);
+    xp.sf8 = at<float>(workspace, L.xsf8);
+  }
   MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
                        down_qmax, grid, xp, stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
@@ -618,6 +632,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.hsmx = at<uint8_t>(workspace, L.hsmx);
   ga.hqmx_shared = at<uint8_t>(workspace, L.hqmx_shared);
   ga.hsmx_shared = at<uint8_t>(workspace, L.hsmx_shared);
+  ga.xqf8 = at<uint8_t>(workspace, L.xqf8);
+  ga.xsf8 = at<float>(workspace, L.xsf8);
   MX_EVENT(1);
   MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));

@@ -57,6 +57,10 @@ __device__ inline void quant_row(const void* a, int64_t row_off, int cols, int a
   }
   for (int c = threadIdx.x; c < cols; c += kThreads) {
     float v = load_act(a, row_off + c, act);
+    if (qmax == kQmaxF8) {
+      codes[c] = (int8_t)e4m3_byte(__fmul_rn(v, inv));
+      continue;
+    }
     float r = __builtin_rintf(__fmul_rn(v, inv));
     r = fminf(fmaxf(r, -q), q);
     codes[c] = (int8_t)(int)r;
@@ -140,7 +144,7 @@ __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, 
                        qm & 0xFF, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hsg + (int64_t)r * (F >> 7));
     return;
   }
-  const int qmax = qm;
+  const int qmax = (qm & kDownQF8) ? kQmaxF8 : qm;
   quant_row_vec<NC, W>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F,
                        act, qmax, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hs + r, red);
 }

@@ -78,13 +78,13 @@ __host__ __device__ constexpr int cfg_nf(int c, int phase) {
 }
 __host__ __device__ constexpr int cfg_bm(int c) { return 16 * cfg_mf(c); }
 __host__ __device__ constexpr int cfg_bn(int c, int phase) { return 64 * cfg_nf(c, phase); }
-// Tile configuration of a group from its rows; w4a4-g128 and mxfp4 groups stop
-// at 64-row tiles (the per-group rescale keeps a partial sum next to every
-// accumulator; the scaled FP4 operands add their scale registers), which keeps
-// the whole kernel within its register budget.
+// Tile configuration of a group from its rows; w4a4-g128, mxfp4 and fp8 groups
+// stop at 64-row tiles (the per-group rescale keeps a partial sum next to every
+// accumulator; the scaled FP4 / FP8 MFMAs take 32-byte operands and their
+// scale registers), which keeps the whole kernel within its register budget.
 __host__ __device__ inline int pick_cfg(int m, int kind) {
   const int c = m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
-  return ((kind == K_W4A4G || kind == K_MXFP4) && c == CFG_L) ? CFG_M : c;
+  return ((kind == K_W4A4G || kind == K_MXFP4 || kind == K_F8A8) && c == CFG_L) ? CFG_M : c;
 }
 
 // Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
@@ -165,6 +165,7 @@ template <int KD> struct Raw { u32x4 d[1]; };
 template <> struct Raw<K_W2G> { u32x2 d; };
 template <> struct Raw<K_W3G> { uint32_t d[3]; };
 template <> struct Raw<K_W8A8> { u32x4 d[2]; };
+template <> struct Raw<K_F8A8> { u32x4 d[2]; };
 
 // loads through the global address space (the pointers come from the block
 // table, so the compiler cannot infer it and would emit flat loads)
@@ -180,7 +181,7 @@ template <int KD> __device__ inline void load_raw(Raw<KD>& r, const uint8_t* p) 
     r.d[0] = gload<uint32_t>(p);
     r.d[1] = gload<uint32_t>(p + 4);
     r.d[2] = gload<uint32_t>(p + 8);
-  } else if constexpr (KD == K_W8A8) {
+  } else if constexpr (KD == K_W8A8 || KD == K_F8A8) {
     r.d[0] = gload<u32x4>(p);
     r.d[1] = gload<u32x4>(p + 16);
   } else if constexpr (!streamed<KD>()) {
@@ -488,6 +489,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr bool RSUM = MAGIC && ACT == MXMOE_BF16;     // bias removed through row sums
   constexpr bool GSC = KD == K_W4A4G;                   // per-128-group activation and weight scales
   constexpr bool MX = kind_is_mx(KD);                   // FP4 e2m1 operands with E8M0 scales per 32
+  constexpr bool F8 = kind_is_f8(KD);                   // FP8 e4m3 operands, fp32 accumulation
   constexpr bool GMETA = kind_has_gmeta(KD);            // group metadata after each fragment block
   constexpr bool RSLOAD = RSUM || GSC || MX;            // a per-row value per k block rides with the stage
   constexpr int RB = stage_rb<KD>();                    // activation bytes per row and k block
@@ -531,8 +533,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const int8_t* qb;
     if constexpr (PHASE == 1) { qb = shared ? a.hq_shared : a.hq; ascale = shared ? a.hs_shared : a.hs; }
     else {
-      qb = KD == K_W8A8 ? a.xq8 : (GSC ? a.xq4g : a.xq4);
-      ascale = KD == K_W8A8 ? a.xs8 : a.xs4;
+      qb = F8 ? reinterpret_cast<const int8_t*>(a.xqf8) : (KD == K_W8A8 ? a.xq8 : (GSC ? a.xq4g : a.xq4));
+      ascale = F8 ? a.xsf8 : (KD == K_W8A8 ? a.xs8 : a.xs4);
     }
     abase = reinterpret_cast<const uint8_t*>(qb);
   } else {
@@ -550,7 +552,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     if constexpr (PHASE == 0) {
       src = shared ? m : a.rtok[off_e + m];
       out = shared ? (g - a.E_routed) * a.T + m : off_e + m;
-      if constexpr (INT && !GSC) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
+      if constexpr (F8) sc = ascale[src];
+      else if constexpr (INT && !GSC) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
     } else if constexpr (PHASE == 1) {
       src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
       if (shared) {
@@ -591,7 +594,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
 
   // ---- accumulators and weight streams
-  typedef typename std::conditional<INT && !GSC, i32x4, f32x4>::type AccT;
+  typedef typename std::conditional<INT && !GSC && !F8, i32x4, f32x4>::type AccT;
   typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
   constexpr int J = MX ? 1 : (INT ? 2 : 4);      // MFMA steps per 128-wide k block
   constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
@@ -661,7 +664,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // prefetch; two 16-byte loads for w8a8), plus one metadata dword per fragment
   // (weight-only).  Waiting for
   // this many leaves the weight prefetch in flight across the barrier.
-  constexpr int kLoadsAfterStage = NL * NF * (streamed<KD>() ? J : (KD == K_W8A8 ? 2 : 1)) + (GMETA ? NL * NF : 0);
+  constexpr int kLoadsAfterStage =
+      NL * NF * (streamed<KD>() ? J : ((KD == K_W8A8 || KD == K_F8A8) ? 2 : 1)) + (GMETA ? NL * NF : 0);
 
   stage_load<RB, BM>(sm, 0, abase, soffs, kb0, wave);
   if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, 0, rsbase, rsoff, kb0, wave);
@@ -778,6 +782,37 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             acc[l][nf][mf] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(A, B, acc[l][nf][mf], 4, 4, 0, sa, 0,
                                                                              (int)wsx[l][nf]);
           }
+      }
+    } else if constexpr (F8) {
+      // FP8: one 16x16x128 FP8 MFMA per (row fragment, channel fragment)
+      // covers the k block.  A lane's 32 bytes are the two 16-byte pieces of
+      // the int8 lane layout (k = 16q.. and 64 + 16q..) on both operands, so
+      // both name the same k for every byte position and the dot product is
+      // that of the k block.  Unit scales (E8M0 127) on both operands.
+      i32x8 A[MF];
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const u32x4 a0 = act_frag<RB>(sm, cur, ra + mf * 16 + li, q);
+        const u32x4 a1 = act_frag<RB>(sm, cur, ra + mf * 16 + li, 4 + q);
+        A[mf] = i32x8{(int)a0[0], (int)a0[1], (int)a0[2], (int)a0[3], (int)a1[0], (int)a1[1], (int)a1[2], (int)a1[3]};
+      }
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            const u32x4 w0 = wr[l][nf].d[0], w1 = wr[l][nf].d[1];
+            const i32x8 B = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3], (int)w1[0], (int)w1[1], (int)w1[2], (int)w1[3]};
+            acc[l][nf][mf] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(A[mf], B, acc[l][nf][mf], 0, 0, 0, 127, 0, 127);
+          }
+      // the activation fragments two row fragments ahead of the MFMAs (two
+      // LDS reads each), so that few of them are live at once
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
+        if (mf + 2 < MF) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       }
     } else if constexpr (GSC) {
       // w4a4-g128: per row fragment, the two MFMA steps of this k block give an
@@ -970,7 +1005,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       }
     // value of accumulator (l, nf, mf, i) after the scheme's scales
     auto outv = [&](int l, int nf, int mf, int i, const f32x4& rs) -> float {
-      if constexpr (INT && !GSC) {
+      if constexpr (F8) {
+        return (acc[l][nf][mf][i] * rs[i]) * cs[l][nf];
+      } else if constexpr (INT && !GSC) {
         int iv = acc[l][nf][mf][i];
         if constexpr (KD == K_W4A4) iv >>= 4;  // exact: every product is a multiple of 16
         return ((float)iv * rs[i]) * cs[l][nf];
@@ -1048,7 +1085,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           if (GUARD && ro[i] < 0) continue;
           if constexpr (PHASE == 1) {
             a.slots[orow] = outv(0, nf, mf, i, rs) * gwv[i];
-          } else if constexpr (INT && !GSC) {
+          } else if constexpr (INT && !GSC && !F8) {
             int iv = acc[0][nf][mf][i];
             if constexpr (KD == K_W4A4) iv >>= 4;
             reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
@@ -1073,6 +1110,9 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
   switch (kd) {
     case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_F8A8:  // never planned in 128-row tiles
+      if constexpr (CFG != CFG_L) run_tile<K_F8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
+      break;
     case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;

@@ -24,12 +24,17 @@ enum Kind : int32_t {
   K_W8G = 6,   // weight-only 8-bit, group 128
   K_W4A4G = 7, // int4 weights and activations with per-128-group scales (w4a4-g128)
   K_MXFP4 = 8, // FP4 e2m1 weights and activations with E8M0 scales per 32 (scaled FP4 MFMA)
-  K_COUNT = 9
+  K_F8A8 = 9,  // FP8 e4m3 weights (per-channel fp32 scale) and activations (per-token), FP8 MFMA
+  K_COUNT = 10
 };
 
+// kinds whose activations arrive as one byte per element with a per-token
+// (or per-group) fp32 scale and whose weights carry fp32 channel scales: the
+// integer kinds and FP8, which shares their layouts
 __host__ __device__ constexpr inline bool kind_is_int(int kd) {
-  return kd == K_W8A8 || kd == K_W4A4 || kd == K_W4A4G;
+  return kd == K_W8A8 || kd == K_W4A4 || kd == K_W4A4G || kd == K_F8A8;
 }
+__host__ __device__ constexpr inline bool kind_is_f8(int kd) { return kd == K_F8A8; }
 __host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G && kd <= K_W8G; }
 // kinds whose scales come per 128-wide group along K (a 64-byte metadata tail
 // per fragment block): the weight-only kinds and w4a4-g128
@@ -43,6 +48,7 @@ __host__ __device__ constexpr inline int kind_wbits(int kd) {
   switch (kd) {
     case K_W16: return 16;
     case K_W8A8: return 8;
+    case K_F8A8: return 8;
     case K_W4A4: return 4;
     case K_W4A4G: return 4;
     case K_MXFP4: return 4;
@@ -56,8 +62,11 @@ __host__ __device__ constexpr inline int kind_wbits(int kd) {
 // 2/3/4-bit group-wise kinds: dequantized through a bias whose product with
 // the activations is removed through activation row sums (16-bit bf16 path)
 __host__ __device__ constexpr inline bool kind_is_magic(int kd) { return kd == K_W2G || kd == K_W3G || kd == K_W4G; }
+// FP8 activations are scaled so that the row maximum lands on 448, the
+// largest finite e4m3 value, which takes the place of qmax in the recipe
+constexpr int kQmaxF8 = 448;
 __host__ __device__ constexpr inline int kind_qmax(int kd) {
-  return kd == K_W8A8 ? 127 : ((kd == K_W4A4 || kd == K_W4A4G) ? 7 : 0);
+  return kd == K_W8A8 ? 127 : ((kd == K_W4A4 || kd == K_W4A4G) ? 7 : (kd == K_F8A8 ? kQmaxF8 : 0));
 }
 
 // Packed layout: the weight matrix [n, k] is cut into fragment blocks of
@@ -71,6 +80,7 @@ __host__ __device__ constexpr inline int lane_bytes(int kd) {
   switch (kd) {
     case K_W16: return 64;
     case K_W8A8: return 32;
+    case K_F8A8: return 32;
     case K_W4A4: return 16;
     case K_W4A4G: return 16;
     case K_MXFP4: return 16;
@@ -248,6 +258,7 @@ struct WsLayout {
   size_t xq4g, xs4g, hsg, hsg_shared;  // w4a4-g128 codes and group scales
   size_t rids, rw, shw;  // router front-end outputs: ids, gate weights, shared-expert gates
   size_t xqmx, xsmx, hqmx, hsmx, hqmx_shared, hsmx_shared;  // mxfp4 activation codes and E8M0 bytes
+  size_t xqf8, xsf8;  // FP8 e4m3 codes and per-token scales of x
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -295,7 +306,8 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
 // down_qmax[e] = qmax | kDownQGroup for per-128-group scales (into hsg
 // [P][F/128]), else per-row scales (into hs); 0 = not quantized.
 constexpr int kDownQGroup = 0x100;
-constexpr int kDownQMX = 0x200;  // MXFP4 codes into hqmx [P][F/2], E8M0 bytes into hsmx [P][F/32]
+constexpr int kDownQMX = 0x200;
+constexpr int kDownQF8 = 0x400;  // FP8 e4m3 codes into hq, per-row scales into hs  // MXFP4 codes into hqmx [P][F/2], E8M0 bytes into hsmx [P][F/32]
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets,
                                 int E, const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg,
                                 uint8_t* hqmx, uint8_t* hsmx, hipStream_t s);
@@ -321,6 +333,9 @@ struct GemmArgs {
   const uint8_t* xqmx; const uint8_t* xsmx;
   const uint8_t* hqmx; const uint8_t* hsmx;
   const uint8_t* hqmx_shared; const uint8_t* hsmx_shared;
+  // FP8: e4m3 codes [T,H] and per-token scales [T] of x (h rows of an FP8 down
+  // projection use hq / hs and hq_shared / hs_shared)
+  const uint8_t* xqf8; const float* xsf8;
   void* h; void* h_shared;
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;
@@ -362,6 +377,8 @@ struct XPrep {
   float* s4g;
   uint8_t* qmx;   // MXFP4 codes [rows, cols / 2], E8M0 bytes smx [rows, cols / 32]
   uint8_t* smx;
+  uint8_t* qf8;   // FP8 e4m3 codes [rows, cols], scales sf8 [rows]
+  float* sf8;
 };
 
 // raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of

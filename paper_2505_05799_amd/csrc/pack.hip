@@ -46,7 +46,8 @@ __device__ inline void slot_field(int kd, int v, int* dw, int* bit, uint32_t* ma
   switch (kd) {
     case K_W16: *dw = v >> 1; *bit = 16 * (v & 1); *mask = 0xFFFFu; break;
     case K_W8G:
-    case K_W8A8: *dw = v >> 2; *bit = 8 * (v & 3); *mask = 0xFFu; break;
+    case K_W8A8:
+    case K_F8A8: *dw = v >> 2; *bit = 8 * (v & 3); *mask = 0xFFu; break;
     case K_W4G: *dw = j; *bit = 16 * h + 4 * p; *mask = 0xFu; break;
     case K_W2G:
     case K_W3G: *dw = j >> 1; *bit = 16 * h + 2 * (4 * (j & 1) + p); *mask = 0x3u; break;

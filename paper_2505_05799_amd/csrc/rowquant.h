@@ -3,6 +3,7 @@
 // wavefront (W = 1) or a workgroup of 4 wavefronts (W = 4) takes one row of
 // 16-bit values and writes, with fixed fp32 recipes,
 //   * per-token int8 / int4 codes and scales (Sec. 4.2.2, a_gsize = -1),
+//   * per-token FP8 e4m3 codes and scales (the same recipe with 448 for qmax),
 //   * per-128-group int4 codes and scales (w4a4-g128),
 //   * MXFP4 codes and E8M0 scales (OCP MX, blocks of 32),
 //   * bf16 row sums per 128-wide block (bias-dequantized weight-only tiles).
@@ -49,11 +50,36 @@ __device__ inline float bits_to_f32(uint32_t b, int act) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)b);
 }
 
-// codes of 8 elements with the same fp32 recipe as quant_row
+// FP8 e4m3 byte (OCP: sign bit 7, exponent bias 7, 3 mantissa bits) of the
+// e4m3 value nearest to v, ties to the even code, magnitudes past 448 to 448
+// (the largest finite value; there are no infinities), sign kept unless the
+// magnitude code is 0.  Below 2^-6 the grid is the multiples of 2^-9 (code =
+// count, 8 being the smallest normal); above, the fp32 mantissa is rounded to
+// 3 bits in integer arithmetic and the exponent rebiased (127 -> 7).
+__device__ inline uint32_t e4m3_byte(float v) {
+  const uint32_t sgn = (__float_as_uint(v) >> 24) & 0x80u;
+  const float a = fminf(fabsf(v), 448.0f);
+  uint32_t mag;
+  if (a < 0.015625f) {
+    mag = (uint32_t)__builtin_rintf(a * 512.0f);
+  } else {
+    const uint32_t b = __float_as_uint(a);
+    mag = ((b + 0x7FFFFu + ((b >> 20) & 1u)) >> 20) - (120u << 3);
+  }
+  return mag ? (sgn | mag) : 0u;
+}
+
+// codes of 8 elements with the same fp32 recipe as quant_row; q = 448 gives
+// FP8 e4m3 codes (the row maximum scaled onto 448), else int8 codes
 __device__ inline uint2 codes8(uint4 u, int act, float inv, float q) {
   float f[8];
   unpack8(u, act, f);
   uint32_t w[2] = {0u, 0u};
+  if (q == (float)kQmaxF8) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i >> 2] |= e4m3_byte(__fmul_rn(f[i], inv)) << (8 * (i & 3));
+    return make_uint2(w[0], w[1]);
+  }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     float r = __builtin_rintf(__fmul_rn(f[i], inv));
@@ -219,6 +245,10 @@ __device__ inline void x_prep_row(const XPrep& p, int64_t r) {
     quant_row_groups(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4g + r * cols), p.s4g + r * (cols >> 7));
   if (p.qmx)
     quant_row_mx(row, cols, p.act, reinterpret_cast<uint4*>(p.qmx + r * (cols >> 1)), p.smx + r * (cols >> 5));
+  if (p.qf8) {
+    if (cols <= 4096) quant_row_vec<8, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
+    else quant_row_vec<0, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
+  }
 }
 
 }  // namespace

@@ -41,9 +41,10 @@ P_SLOTS = 512                                        # persistent grid: 2 workgr
 
 
 def pick_cfg(m: int, scheme) -> int:
-    """The kernel's run-time choice from the group's rows (w4a4-g128 stops at 64)."""
+    """The kernel's run-time choice from the group's rows (w4a4-g128, mxfp4 and
+    fp8 stop at 64)."""
     c = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
-    if scheme.a_bits < 16 and scheme.a_group > 0 and c == 3:
+    if scheme.a_bits < 16 and (scheme.a_group > 0 or getattr(scheme, "fmt", 0) == 2) and c == 3:
         c = 2
     return c
 
@@ -114,6 +115,11 @@ def _device_linear(scheme, n: int, k: int, gen, dev: str = "cuda"):
         codes = torch.randint(0, 16, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.uint8)
         scales = torch.randint(118, 124, (n, k // 32), generator=gen, device=dev, dtype=torch.int32).to(torch.uint8)
         return W.QLinear(s, n, k, codes, scales)
+    if s.fmt == 2:   # fp8: finite e4m3 bytes (magnitude codes 0..0x7E, either sign)
+        mag = torch.randint(0, 0x7F, (n, k), generator=gen, device=dev, dtype=torch.int32)
+        sgn = torch.randint(0, 2, (n, k), generator=gen, device=dev, dtype=torch.int32) * 0x80
+        scales = torch.rand(n, generator=gen, device=dev) * 0.01 + 0.001
+        return W.QLinear(s, n, k, (mag | sgn).to(torch.uint8), scales)
     qm = (1 << (s.w_bits - 1)) - 1
     codes = torch.randint(-qm, qm + 1, (n, k), generator=gen, device=dev, dtype=torch.int32).to(torch.int8)
     if s.w_group > 0:

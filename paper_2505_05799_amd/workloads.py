@@ -35,6 +35,10 @@ Offline quantizers (input preparation, not part of the forward pass):
   shared power-of-two scale 2^e (E8M0 byte e + 127), e = floor(log2(amax)) - 2,
   and FP4 e2m1 elements rne(w / 2^e) on the grid {0, 0.5, 1, 1.5, 2, 3, 4, 6}
   (ties to the even code, magnitudes above 6 clamp to 6).
+* ``fp8`` (OCP FP8 e4m3, the 8-bit floating-point operand of the MI355X matrix
+  cores): per output channel s = fp32(amax_row / 448) and elements = the e4m3
+  value nearest to w / s (ties to the even code), taken here from the binary
+  exponent and a rounded 3-bit mantissa (below 2^-6: multiples of 2^-9).
 """
 
 from __future__ import annotations
@@ -59,12 +63,15 @@ class Scheme:
     w_group: int     # 128 for groups along K, -1 = per output channel
     a_group: int     # 128 for groups along K, -1 = per token
     symmetric: int   # 1 for w8a8 / w4a4 (per channel or g128), 0 for wNg128 asym and 16-bit
-    fmt: int = 0     # 0 integer codes; 1 OCP MX floating point (e2m1 elements, E8M0 scale per 32)
+    fmt: int = 0     # 0 integer codes; 1 OCP MX floating point (e2m1 elements, E8M0 scale per 32);
+                     # 2 FP8 e4m3 elements with per-channel / per-token fp32 scales
 
     @property
     def name(self) -> str:
         if self.fmt == 1:
             return "mxfp4"
+        if self.fmt == 2:
+            return "fp8"
         if self.w_bits == 16:
             return "w16"
         if self.a_bits < 16:
@@ -98,7 +105,8 @@ W4G128 = Scheme(4, 16, 128, -1, 0)
 W8G128 = Scheme(8, 16, 128, -1, 0)
 W4A4G128 = Scheme(4, 4, 128, 128, 1)   # 4-bit weights and activations, per-128 group scales
 MXFP4 = Scheme(4, 4, 32, 32, 1, 1)     # FP4 e2m1 weights and activations, E8M0 scale per 32
-ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128, MXFP4)
+FP8 = Scheme(8, 8, -1, -1, 1, 2)       # FP8 e4m3 weights (per channel) and activations (per token)
+ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128, MXFP4, FP8)
 SCHEME_BY_NAME = {s.name: s for s in ALL_SCHEMES}
 
 LINEAR_NAMES = ("gate", "up", "down")
@@ -344,6 +352,26 @@ def quantize_mxfp4(w: np.ndarray, block: int = 32):
     return code.reshape(n, k).astype(np.uint8), (e + 127).astype(np.uint8)
 
 
+def quantize_fp8(w: np.ndarray):
+    """FP8 e4m3 per-channel quantizer: codes uint8 [n, k] (sign bit 7, four
+    exponent bits of bias 7, three mantissa bits), scales fp32 [n] =
+    fp32(amax / 448).  A row of zeros gets scale 0 and zero codes."""
+    w64 = w.astype(np.float64)
+    s = (np.abs(w64).max(axis=1) / 448.0).astype(np.float32)
+    s64 = s.astype(np.float64)
+    r = np.abs(w64) / np.where(s64 == 0, 1.0, s64)[:, None]
+    r = np.where(s64[:, None] == 0, 0.0, np.minimum(r, 448.0))
+    _, ex = np.frexp(r)                         # r = f 2^ex, f in [0.5, 1): exponent ex - 1
+    e = np.maximum(ex - 1, -6)
+    normal = r >= 2.0 ** -6
+    # normal: mantissa steps of 2^(e-3); below 2^-6: steps of 2^-9 (code = count)
+    m = np.rint(np.where(normal, (r / np.exp2(e) - 1.0) * 8.0, r * 512.0)).astype(np.int64)
+    code = np.where(normal, ((e + 7) << 3) + m, m)   # a mantissa carry moves into the exponent
+    code = np.minimum(code, 126)
+    code = np.where((w64 < 0) & (code > 0), code | 0x80, code)
+    return code.astype(np.uint8), s
+
+
 @dataclass
 class QLinear:
     """One quantized linear, W is [n, k] = [out, in] (nn.Linear layout)."""
@@ -377,6 +405,9 @@ def quantize_linear(w_bf16_f32: np.ndarray, scheme: Scheme) -> QLinear:
         return QLinear(scheme, n, k, c, s, z)
     if scheme.fmt == 1:
         c, s = quantize_mxfp4(w_bf16_f32, scheme.w_group)
+        return QLinear(scheme, n, k, c, s)
+    if scheme.fmt == 2:
+        c, s = quantize_fp8(w_bf16_f32)
         return QLinear(scheme, n, k, c, s)
     if scheme.w_group > 0:
         c, s = quantize_sym_g128(w_bf16_f32, scheme.w_bits, scheme.w_group)

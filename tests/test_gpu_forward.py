@@ -66,7 +66,38 @@ MIXES = [
     # mxfp4 (FP4 e2m1 with E8M0 scales, on the scaled FP4 MFMA) beside the others
     [(W.MXFP4,) * 3, (W.MXFP4, W.MXFP4, W.W2G128), (W.W8A8, W.W8A8, W.MXFP4), (W.W16, W.W16, W.MXFP4),
      (W.MXFP4, W.MXFP4, W.W4A4G128), (W.W3G128, W.W3G128, W.MXFP4), (W.MXFP4, W.MXFP4, W.W8A8)],
+    # fp8 (e4m3 with per-channel / per-token scales, on the FP8 MFMA) beside the others
+    [(W.FP8,) * 3, (W.FP8, W.FP8, W.W2G128), (W.W8A8, W.W8A8, W.FP8), (W.W16, W.W16, W.FP8),
+     (W.FP8, W.FP8, W.W4A4G128), (W.MXFP4, W.MXFP4, W.FP8), (W.FP8, W.FP8, W.W8A8)],
 ]
+
+
+def test_f8_activation_codes_bit_exact():
+    """The forward's FP8 encoding of x and of the routed and shared h rows
+    equals the oracle's encoder, byte for byte (h: the encoder applied to the
+    GPU's own rounded h)."""
+    torch = torch_mod()
+    for act in ("bf16", "fp16"):
+        T, H, F, Fs, k = 77, 256, 384, 256, 2
+        blk = W.random_small_block(97, T=T, H=H, F=F, E=4, k=k, n_shared=1, F_shared=Fs, act=act,
+                                   schemes=[(W.FP8,) * 3] * 5, skew=0.5)
+        mb, _ = run_block(blk)
+        qx, sx = O.fp8_quant(O.act_values(blk.x, act).astype(np.float32))
+        assert np.array_equal(mb.ws_view("xqf8", torch.uint8, T * H, T).cpu().numpy().reshape(T, H), qx)
+        assert np.array_equal(mb.ws_view("xsf8", torch.float32, T, T).cpu().numpy(), sx)
+        P = int(mb.ws_view("offsets", torch.int32, 5, T).cpu().numpy()[4])
+
+        def hvals(name, rows, cols):
+            h = mb.ws_view(name, torch.int16, rows * cols, T).cpu().numpy().reshape(rows, cols)
+            return O.act_values(h.view(np.float16) if act == "fp16" else h.view(np.uint16), act).astype(np.float32)
+
+        qh, sh = O.fp8_quant(hvals("h", T * k, F)[:P])
+        assert np.array_equal(mb.ws_view("hq", torch.uint8, T * k * F, T).cpu().numpy()[: P * F].reshape(P, F), qh)
+        assert np.array_equal(mb.ws_view("hs", torch.float32, T * k, T).cpu().numpy()[:P], sh)
+        qs, ss = O.fp8_quant(hvals("h_shared", T, Fs))
+        assert np.array_equal(mb.ws_view("hq_shared", torch.uint8, T * Fs, T).cpu().numpy().reshape(T, Fs), qs)
+        assert np.array_equal(mb.ws_view("hs_shared", torch.float32, T, T).cpu().numpy(), ss)
+        say(f"fp8 codes {act}: x, {P} routed and {T} shared h rows bit-exact")
 
 
 def test_mx_activation_codes_bit_exact():
@@ -100,13 +131,15 @@ def test_mx_activation_codes_bit_exact():
 def test_x_encodings_bit_exact(H):
     """Every encoding of x that the plan launch writes on its spare workgroups
     equals the oracle's encoders byte for byte: int8 and int4 codes per token,
-    int4 codes per 128-group, MXFP4 codes and E8M0 bytes; the bf16 row sums
+    int4 codes per 128-group, MXFP4 codes and E8M0 bytes, FP8 codes and
+    scales per token; the bf16 row sums
     per 128-block lie within the rounding of a 128-term fp32 sum.  H = 4224
     takes rows longer than the register-resident encoder holds."""
     torch = torch_mod()
     T = 300 if H == 256 else 37
-    sch = [(W.W8A8, W.W8A8, W.W16), (W.W4A4,) * 3, (W.W2G128,) * 3, (W.W4A4G128,) * 3, (W.MXFP4,) * 3]
-    blk = W.random_small_block(313 + H, T=T, H=H, F=128, E=5, k=2, act="bf16", schemes=sch, skew=0.3)
+    sch = [(W.W8A8, W.W8A8, W.W16), (W.W4A4,) * 3, (W.W2G128,) * 3, (W.W4A4G128,) * 3, (W.MXFP4,) * 3,
+           (W.FP8,) * 3]
+    blk = W.random_small_block(313 + H, T=T, H=H, F=128, E=6, k=2, act="bf16", schemes=sch, skew=0.3)
     mb, _ = run_block(blk)
     xv = O.act_values(blk.x, "bf16").astype(np.float32)
 
@@ -126,10 +159,13 @@ def test_x_encodings_bit_exact(H):
     assert np.array_equal(ws("xqmx", torch.uint8, T * H // 2, (T, H // 2)),
                           (qx[:, 0::2] | (qx[:, 1::2] << 4)).astype(np.uint8))
     assert np.array_equal(ws("xsmx", torch.uint8, T * H // 32, (T, H // 32)), ex)
+    qf, sf = O.fp8_quant(xv)
+    assert np.array_equal(ws("xqf8", torch.uint8, T * H, (T, H)), qf)
+    assert np.array_equal(ws("xsf8", torch.float32, T, (T,)), sf)
     rs = ws("rsx", torch.float32, T * H // 128, (T, H // 128)).astype(np.float64)
     blocks = xv.astype(np.float64).reshape(T, H // 128, 128)
     assert np.all(np.abs(rs - blocks.sum(-1)) <= 128 * 2.0 ** -24 * np.abs(blocks).sum(-1))
-    say(f"x encodings H={H}: int8, int4, int4-g128, mxfp4 bit-exact; row sums within bound")
+    say(f"x encodings H={H}: int8, int4, int4-g128, mxfp4, fp8 bit-exact; row sums within bound")
 
 
 @pytest.mark.parametrize("act", ["bf16", "fp16"])

@@ -83,7 +83,7 @@ def test_route_permute(T, k, E, kind):
 # or 8 chunks per lane, one workgroup per row with 4 or 8, a streamed row
 # read twice; ld_pad 3 misaligns the rows (element loads, one workgroup per row)
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
-@pytest.mark.parametrize("qmax", [127, 7])
+@pytest.mark.parametrize("qmax", [127, 7, 448])
 @pytest.mark.parametrize("rows,cols,ld_pad", [(1, 128, 0), (37, 2048, 0), (300, 3584, 0), (5, 6144, 8),
                                               (9, 14336, 0), (3, 20480, 0), (6, 1000, 3), (4, 100, 0)])
 def test_act_quant_bit_exact(act, qmax, rows, cols, ld_pad):
@@ -100,6 +100,11 @@ def test_act_quant_bit_exact(act, qmax, rows, cols, ld_pad):
     assert a.stride(0) == cols + ld_pad
     codes, scales = M.act_quant(a, act, qmax)
     torch.cuda.synchronize()
+    if qmax == 448:     # FP8 e4m3 bytes
+        rc, rs = O.fp8_quant(O.act_values(x, act).astype(np.float32))
+        assert np.array_equal(codes.cpu().numpy().view(np.uint8), rc)
+        assert np.array_equal(scales.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+        return
     rc, rs = O.act_quant(O.act_values(x, act).astype(np.float32), qmax)
     assert np.array_equal(codes.cpu().numpy(), rc)
     assert np.array_equal(scales.cpu().numpy().view(np.uint32), rs.view(np.uint32))
@@ -147,6 +152,20 @@ def _check_mx_linear(q, a, got, act):
     assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
 
 
+def _check_f8_linear(q, a, got, act):
+    """fp8: one FP8 MFMA per 128-wide k block adds the block's exact e4m3
+    products in reduced precision (within 2^-9 of max|a| max|w| of the block),
+    blocks and split-K slices are added in fp32, then two fp32 products apply
+    s_a[m] and s_w[n]; with at most 2^4 blocks those add less than 2^-20 of
+    sum |a_hat| |w_hat|."""
+    assert q.k // 128 <= 16
+    want = O.linear(a, q, act)
+    qa, sa = O.fp8_quant(a.astype(np.float32))
+    ad = O.e4m3_values(qa) * sa.astype(np.float64)[:, None]
+    bound = O.fp8_block_bound(ad, O.dequant(q, act)) + 1e-30
+    assert np.all(np.abs(got - want) <= bound), float((np.abs(got - want) / bound).max())
+
+
 @pytest.mark.parametrize("scheme", W.ALL_SCHEMES)
 @pytest.mark.parametrize("m", LIN_M)
 @pytest.mark.parametrize("n,k", LIN_SHAPES)
@@ -154,6 +173,8 @@ def test_linear_bf16(scheme, m, n, k):
     q, a, got = _linear_case(scheme, "bf16", m, n, k, m * 7 + n)
     if scheme.fmt == 1:
         _check_mx_linear(q, a, got, "bf16")
+    elif scheme.fmt == 2:
+        _check_f8_linear(q, a, got, "bf16")
     elif scheme.a_group > 0:
         _check_group_linear(q, a, got, "bf16")
     elif scheme.a_bits < 16:
@@ -171,6 +192,8 @@ def test_linear_fp16(scheme, m):
     q, a, got = _linear_case(scheme, "fp16", m, 48, 256, m + 11)
     if scheme.fmt == 1:
         _check_mx_linear(q, a, got, "fp16")
+    elif scheme.fmt == 2:
+        _check_f8_linear(q, a, got, "fp16")
     elif scheme.a_group > 0:
         _check_group_linear(q, a, got, "fp16")
     elif scheme.a_bits < 16:

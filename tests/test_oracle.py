@@ -82,10 +82,45 @@ def py_mx_quant(vals):
     return codes, e
 
 
+def py_e4m3(code):
+    """Value of an OCP FP8 e4m3 byte from its bit fields (sign, 4-bit exponent
+    of bias 7, 3-bit mantissa; exponent field 0 is subnormal)."""
+    sgn = -1.0 if code & 0x80 else 1.0
+    e, m = (code >> 3) & 15, code & 7
+    assert not (e == 15 and m == 7), "NaN code"
+    return sgn * (m / 8.0 * 2.0 ** -6 if e == 0 else (1 + m / 8.0) * 2.0 ** (e - 7))
+
+
+E4M3_GRID = sorted({py_e4m3(c) for c in range(127)})
+
+
+def py_e4m3_encode(x):
+    """Nearest e4m3 byte to the Python float x by scanning all 127 magnitudes
+    (ties: the even code; beyond 448: 448); sign kept unless the magnitude is 0."""
+    best = None
+    for c in range(127):
+        key = (abs(abs(x) - py_e4m3(c)), c % 2)
+        if best is None or key < best[0]:
+            best = (key, c)
+    c = 126 if abs(x) >= 448 else best[1]
+    return c | 0x80 if (x < 0 and c) else c
+
+
+def py_fp8_quant(row):
+    amax = max(abs(v) for v in row)
+    if amax == 0:
+        return [0] * len(row), 0.0
+    inv = f32(448.0 / amax)
+    s = f32(amax / 448.0)
+    return [py_e4m3_encode(f32(v * inv)) for v in row], s
+
+
 def py_weight(lin, act, n, c):
     s = lin.scheme
     if getattr(s, "fmt", 0) == 1:
         return py_e2m1(int(lin.codes[n, c])) * 2.0 ** (int(lin.scales[n, c // 32]) - 127)
+    if getattr(s, "fmt", 0) == 2:
+        return py_e4m3(int(lin.codes[n, c])) * float(lin.scales[n])
     if s.w_bits == 16:
         w = bits_to_float_bf16(lin.codes[n, c])
         return f16_round(w) if act == "fp16" else w
@@ -105,6 +140,11 @@ def py_linear(a_row, lin, act):
             codes, e = py_mx_quant([float(f32(v)) for v in a_row[32 * b: 32 * b + 32]])
             a_hat += [py_e2m1(cd) * 2.0 ** e for cd in codes]
         return [sum(a_hat[c] * py_weight(lin, act, n, c) for c in range(lin.k)) for n in range(lin.n)]
+    if getattr(s, "fmt", 0) == 2:
+        qa, sa = py_fp8_quant([float(f32(v)) for v in a_row])
+        av = [py_e4m3(cd) for cd in qa]
+        return [sum(av[c] * py_e4m3(int(lin.codes[n, c])) for c in range(lin.k)) * sa * float(lin.scales[n])
+                for n in range(lin.n)]
     if s.a_bits < 16 and s.a_group > 0:
         # per 128-wide block: integer dot of the block's codes, times both block scales
         g, qmax = s.a_group, (1 << (s.a_bits - 1)) - 1
@@ -323,6 +363,64 @@ def test_mxfp4_quantizer_pins():
     assert np.array_equal(cw, co) and np.array_equal(ew, eo)
 
 
+def test_fp8_e4m3_pins():
+    """OCP FP8 e4m3: the oracle's table against the bit-field definition for
+    every byte, anchors (1.0 = 0x38, 448 = 0x7E the largest, 2^-6 the smallest
+    normal, 2^-9 the smallest subnormal), nearest-value encoding with ties to
+    the even code against a scan of all magnitudes, saturation at 448, the
+    round-trip of every grid value, and a relative error of at most 2^-4 in
+    the normal range."""
+    codes = np.array([c for c in range(256) if (c & 0x7F) != 0x7F], np.uint8)
+    assert O.e4m3_values(codes).tolist() == [py_e4m3(int(c)) for c in codes]
+    anchors = {0x38: 1.0, 0x7E: 448.0, 0x08: 2.0 ** -6, 0x01: 2.0 ** -9, 0x40: 2.0, 0xB8: -1.0, 0x07: 7 * 2.0 ** -9}
+    for c, v in anchors.items():
+        assert O.e4m3_values(np.array([c], np.uint8))[0] == v
+    with pytest.raises(ValueError):
+        O.e4m3_values(np.array([0x7F], np.uint8))
+    grid = np.array(E4M3_GRID)
+    assert np.array_equal(O.e4m3_code(grid), np.arange(127))                 # grid values round-trip
+    mids = (grid[:-1] + grid[1:]) / 2
+    assert O.e4m3_code(mids).tolist() == [i if i % 2 == 0 else i + 1 for i in range(126)]  # ties to even
+    rng = np.random.default_rng(5)
+    x = np.concatenate([np.exp2(rng.uniform(-12, 10, 400)), [0.0, 448.0, 460.0, 1e6, 2.0 ** -10, 2.0 ** -10 * 1.0001]])
+    assert O.e4m3_code(x).tolist() == [py_e4m3_encode(float(v)) for v in x]
+    nrm = (x >= 2.0 ** -6) & (x <= 448)
+    assert np.all(np.abs(O._E4M3[O.e4m3_code(x[nrm])] - x[nrm]) <= 2.0 ** -4 * x[nrm])
+
+
+def test_fp8_quantizer_pins():
+    """Per-token FP8 activations: brute force of the fp32 recipe on random rows
+    (the row maximum lands on 448), an all-zero row, sign symmetry, and a
+    linear whose operands are exact scaled e4m3 values reproduces the plain
+    product; the input generator's weight quantizer agrees with a scan of the
+    grid."""
+    rng = np.random.default_rng(6)
+    a = (rng.standard_normal((6, 128)) * np.exp2(rng.uniform(-8, 8, (6, 1)))).astype(np.float32)
+    a[3] = 0
+    q, s = O.fp8_quant(a)
+    for i in range(6):
+        pc, ps = py_fp8_quant([float(v) for v in a[i]])
+        assert q[i].tolist() == pc and float(s[i]) == ps
+    nz = [i for i in range(6) if i != 3]
+    assert np.all(O.e4m3_values(q[nz]).__abs__().max(axis=1) == 448.0)
+    assert np.all(q[3] == 0) and s[3] == 0
+    qn, sn = O.fp8_quant(-a)
+    assert np.array_equal(O.e4m3_values(qn), -O.e4m3_values(q)) and np.array_equal(sn, s)
+    # exact operands: activations 448 * grid / 448 and weights grid * 2^-3 per channel
+    av = np.array([[1.0, -0.5, 448.0, 3.0] * 32], np.float64)
+    wc = np.array([[0x38, 0xC0, 0x01, 0x7E] * 32, [0x30, 0x30, 0x30, 0x30] * 32], np.uint8)
+    lin = W.QLinear(W.FP8, 2, 128, wc, np.array([0.125, 1.0], np.float32))
+    exact = av @ (O.e4m3_values(wc) * np.array([[0.125], [1.0]])).T
+    assert np.array_equal(O.linear(av, lin, "bf16"), exact)
+    # weights: the input generator's e4m3 codes are the nearest grid values
+    w = W.draw_weight(13, 0, 0, 16, 256)
+    lq = W.quantize_linear(w, W.FP8)
+    for n in range(0, 16, 5):
+        sc = float(lq.scales[n])
+        assert sc == f32(float(np.abs(w[n].astype(np.float64)).max()) / 448.0)
+        assert lq.codes[n].tolist() == [py_e4m3_encode(float(v) / sc) for v in w[n].astype(np.float64)]
+
+
 def test_w16_fp16_conversion():
     w = np.array([[1.0, -0.0078125, 3.0e-6, 60000.0, 1.0e-7]], np.float32)
     lin = W.quantize_linear(w, W.W16)
@@ -405,10 +503,13 @@ MIXED_G = [(W.W4A4G128, W.W4A4G128, W.W2G128), (W.W8A8, W.W8A8, W.W4A4G128), (W.
            (W.W16, W.W16, W.W4A4G128), (W.W4A4G128, W.W4A4G128, W.W8A8)]
 MIXED_MX = [(W.MXFP4,) * 3, (W.MXFP4, W.MXFP4, W.W3G128), (W.W8A8, W.W8A8, W.MXFP4), (W.W16, W.W16, W.MXFP4),
             (W.MXFP4, W.MXFP4, W.W4A4G128)]
+MIXED_F8 = [(W.FP8,) * 3, (W.FP8, W.FP8, W.W2G128), (W.W8A8, W.W8A8, W.FP8), (W.W16, W.W16, W.FP8),
+            (W.MXFP4, W.MXFP4, W.FP8)]
 
 
 @pytest.mark.parametrize("act", ["bf16", "fp16"])
-@pytest.mark.parametrize("mix,H,F", [(MIXED, 128, 128), (MIXED_G, 256, 256), (MIXED_MX, 128, 256)])
+@pytest.mark.parametrize("mix,H,F", [(MIXED, 128, 128), (MIXED_G, 256, 256), (MIXED_MX, 128, 256),
+                                     (MIXED_F8, 128, 128)])
 def test_moe_brute_force(act, mix, H, F):
     blk = W.random_small_block(21, T=5, H=H, F=F, E=4, k=2, n_shared=1, F_shared=128, act=act,
                                schemes=mix)
