@@ -190,7 +190,7 @@ def compare_per_expert(args):
     from paper_2505_05799_amd import mxmoe as M
     from paper_2505_05799_amd import workloads as W
     out = []
-    for sch in (W.W16, W.W4G128, W.W8A8, W.MXFP4):
+    for sch in (W.W16, W.W4G128, W.W8A8, W.MXFP4, W.FP8):
         cfg = W.BlockConfig(f"per_expert_{sch.name}", T=512, H=2048, F=1408, E=60, k=4, n_shared=0, F_shared=0,
                             act="bf16", zipf_s=args.zipf, alloc=lambda e, r, s=sch: (s, s, s),
                             description="60 experts [2816, 2048] gate+up, top-4, 512 tokens")

@@ -185,7 +185,7 @@ def profile(schemes=None, k_lo: int = 1024, k_hi: int = 4096, reps: int = 5, log
     table = {"P": P_SLOTS, "k_points": [k_lo, k_hi], "unit": "ns per tile; c_t(K) = a + b * K / 128",
              "cost": {"0": {}, "1": {}}, "raw": {"0": {}, "1": {}}}
     for s in schemes:
-        cfgs = [0, 1, 2] if (s.a_bits < 16 and s.a_group > 0) else [0, 1, 2, 3]
+        cfgs = [0, 1, 2] if pick_cfg(1 << 20, s) == 2 else [0, 1, 2, 3]   # kinds capped at 64-row tiles
         for phase in (0, 1):
             lo = _probe(s, phase, k_lo, cfgs, reps, log=log)
             hi = _probe(s, phase, k_hi, cfgs, reps, log=log)
@@ -257,6 +257,8 @@ def main():
     ap.add_argument("--validate", default="mixtral,dsv2lite,qwen15_uniform,qwen15_mixed,qwen15_w5a5",
                     help="workloads whose measured launch times are compared with the model ('' = none)")
     ap.add_argument("--validate-only", action="store_true", help="keep the stored costs, redo the validation")
+    ap.add_argument("--merge", action="store_true",
+                    help="profile only --schemes and keep the stored costs of every other scheme")
     a = ap.parse_args()
     from . import workloads as W
     log = lambda *x: print(*x, file=sys.stderr, flush=True)
@@ -265,8 +267,18 @@ def main():
         table = CostTable.load(a.out).data
     else:
         schemes = [W.SCHEME_BY_NAME[n] for n in a.schemes.split(",") if n] or None
-        table = profile(schemes, reps=a.reps, log=log)
-        table["command"] = "python -m paper_2505_05799_amd.tile_cost" + (f" --schemes {a.schemes}" if a.schemes else "")
+        new = profile(schemes, reps=a.reps, log=log)
+        cmd = "python -m paper_2505_05799_amd.tile_cost" + (f" --schemes {a.schemes}" if a.schemes else "")
+        if a.merge and schemes:
+            table = CostTable.load(a.out).data
+            for key in ("cost", "raw"):
+                for ph in ("0", "1"):
+                    table[key][ph].update(new[key][ph])
+            prev = table.get("command", "")
+            table["command"] = (prev + "; then " if prev else "") + cmd + " --merge"
+        else:
+            table = new
+            table["command"] = cmd
     names = [n for n in a.validate.split(",") if n]
     if names:
         table["validation"] = validate(CostTable(table), names, log=log)
