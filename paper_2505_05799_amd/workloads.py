@@ -183,6 +183,10 @@ def _qwen15_mixed(e: int, rank: int):
     return (W3G128, W3G128, W3G128)
 
 
+def _qwen15_float(e: int, rank: int):
+    return (FP8, FP8, FP8) if rank <= 6 else (MXFP4, MXFP4, MXFP4)
+
+
 # The W5A5 allocation the paper prints for layer 5 of Qwen1.5-MoE (appendix
 # table of per-linear schemes): one character per expert, experts 0..59 then
 # the shared expert.  g = w4a4 with 128-groups on both operands, c = w4a4 per
@@ -226,6 +230,11 @@ CONFIGS: Dict[str, BlockConfig] = {
         "qwen15_mixed", T=256, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
         act="bf16", zipf_s=1.5, alloc=_qwen15_mixed, shared_alloc=(W8A8, W8A8, W8A8),
         description="Qwen1.5-MoE-shaped decode batch, mixed w8a8/w4a4/w3g128 at equal avg bits"),
+    "qwen15_float": BlockConfig(
+        "qwen15_float", T=8192, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
+        act="bf16", zipf_s=1.5, alloc=_qwen15_float, shared_alloc=(FP8, FP8, FP8),
+        description="Qwen1.5-MoE-shaped compute-bound batch (8192 tokens) on the MI355X floating-point "
+                    "schemes: fp8 for the 6 hottest experts and the shared expert, mxfp4 for the rest"),
     "qwen15_w5a5": BlockConfig(
         "qwen15_w5a5", T=8192, H=2048, F=1408, E=60, k=4, n_shared=1, F_shared=5632,
         act="bf16", zipf_s=1.5, alloc=_qwen15_w5a5, shared_alloc=_qwen15_w5a5(60, 0),

@@ -16,7 +16,7 @@ from tests.gpuhelp import compare_block, say, torch_mod, upload_inputs
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["tiny", "mixtral", "dsv2lite", "qwen15_uniform", "qwen15_mixed", "qwen15_w5a5", "qwen2"]
+NAMES = ["tiny", "mixtral", "dsv2lite", "qwen15_uniform", "qwen15_mixed", "qwen15_w5a5", "qwen15_float", "qwen2"]
 
 
 def sample_tokens(blk, n_random=10, seed=0):
@@ -33,7 +33,8 @@ def sample_tokens(blk, n_random=10, seed=0):
 
 
 # micro-kernel ids of the schemes in the plan's tile entries
-KIND = {"w16": 0, "w8a8": 1, "w4a4": 2, "w2g128": 3, "w3g128": 4, "w4g128": 5, "w8g128": 6, "w4a4g128": 7}
+KIND = {"w16": 0, "w8a8": 1, "w4a4": 2, "w2g128": 3, "w3g128": 4, "w4g128": 5, "w8g128": 6, "w4a4g128": 7,
+        "mxfp4": 8, "fp8": 9}
 
 
 PF_N = 12  # int32 fields per group record of the tile plan

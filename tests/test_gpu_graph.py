@@ -21,7 +21,7 @@ def test_graph_replay_matches_eager(name):
         blk = W.make_block("tiny")
     else:
         sch = [(W.W4G128,) * 3, (W.W8A8, W.W8A8, W.W2G128), (W.W4A4,) * 3, (W.MXFP4,) * 3,
-               (W.W4A4G128, W.W4A4G128, W.W3G128), (W.W16,) * 3, (W.W8A8,) * 3]
+               (W.W4A4G128, W.W4A4G128, W.W3G128), (W.W16,) * 3, (W.FP8, W.FP8, W.W8A8)]
         blk = W.random_small_block(5, T=300, H=256, F=384, E=6, k=2, n_shared=1, F_shared=256, act="bf16",
                                    schemes=sch, skew=1.0)
     mb = M.MoEBlock(blk)
