@@ -727,8 +727,9 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int
     for m, lin in zip(ms, lins):
         m = int(m)  # Python integers: the sums below exceed 32 bits
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
-        if cfg == 3 and lin.scheme.a_bits < 16 and (lin.scheme.a_group > 0 or getattr(lin.scheme, "fmt", 0) == 2):
-            cfg = 2   # w4a4-g128, mxfp4 and fp8 groups stop at 64-row tiles
+        if cfg == 3 and lin.scheme.a_bits < 16 and (lin.scheme.a_group > 0
+                                                     or (getattr(lin.scheme, "fmt", 0) == 2 and phase != 1)):
+            cfg = 2   # w4a4-g128 and mxfp4 groups stop at 64-row tiles, fp8 outside the down phase
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-int(lin.n) // bn)

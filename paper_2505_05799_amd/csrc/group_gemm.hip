@@ -150,7 +150,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   auto geom = [&](int ph, int g) {
     Geom q;
     q.m = s_m[g];
-    q.cfg = pick_cfg(q.m, s_kd[ph][g]);
+    q.cfg = pick_cfg(q.m, s_kd[ph][g], raw_m >= 0 ? 0 : ph);
     q.bm = cfg_bm(q.cfg);
     q.bn = cfg_bn(q.cfg, raw_m >= 0 ? 1 : ph);  // raw mode: one linear
     q.mt = q.m > 0 ? div_small(q.m + q.bm - 1, q.bm) : 0;
@@ -377,7 +377,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
             inv = div_small(65536 + em - 1, em);  // t / em = (t * inv) >> 16 for t < 64, em <= 8
             mi0 = smi * dd.sm;
             ni0 = sni * dd.sn;
-            w0 = tile_word0(g, pick_cfg(s_m[g], s_kd[ph][g]), s_kd[ph][g], s_sp[ph][g]);
+            w0 = tile_word0(g, pick_cfg(s_m[g], s_kd[ph][g], raw_m >= 0 ? 0 : ph), s_kd[ph][g], s_sp[ph][g]);
             off_e = s_off[g];
             m_g = s_m[g];
             size = v;

@@ -78,13 +78,16 @@ __host__ __device__ constexpr int cfg_nf(int c, int phase) {
 }
 __host__ __device__ constexpr int cfg_bm(int c) { return 16 * cfg_mf(c); }
 __host__ __device__ constexpr int cfg_bn(int c, int phase) { return 64 * cfg_nf(c, phase); }
-// Tile configuration of a group from its rows; w4a4-g128, mxfp4 and fp8 groups
-// stop at 64-row tiles (the per-group rescale keeps a partial sum next to every
-// accumulator; the scaled FP4 / FP8 MFMAs take 32-byte operands and their
-// scale registers), which keeps the whole kernel within its register budget.
-__host__ __device__ inline int pick_cfg(int m, int kind) {
+// Tile configuration of a group from its rows; w4a4-g128 and mxfp4 groups stop
+// at 64-row tiles (the per-group rescale keeps a partial sum next to every
+// accumulator; the scaled FP4 MFMA adds its scale registers), and so do fp8
+// groups outside the down phase (its two linears' 32-byte operands do not fit
+// next to 128-row accumulators), which keeps every kernel within its register
+// budget.  phase: 0 gate|up (and single linears), 1 down.
+__host__ __device__ inline int pick_cfg(int m, int kind, int phase) {
   const int c = m <= 16 ? CFG_S : (m <= 32 ? CFG_T : (m <= 64 ? CFG_M : CFG_L));
-  return ((kind == K_W4A4G || kind == K_MXFP4 || kind == K_F8A8) && c == CFG_L) ? CFG_M : c;
+  const bool cap = kind == K_W4A4G || kind == K_MXFP4 || (kind == K_F8A8 && phase != 1);
+  return (cap && c == CFG_L) ? CFG_M : c;
 }
 
 // Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
@@ -1110,8 +1113,8 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
   switch (kd) {
     case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W8A8: run_tile<K_W8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
-    case K_F8A8:  // never planned in 128-row tiles
-      if constexpr (CFG != CFG_L) run_tile<K_F8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
+    case K_F8A8:  // planned in 128-row tiles in the down phase only
+      if constexpr (CFG != CFG_L || PHASE == 1) run_tile<K_F8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
       break;
     case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;

@@ -40,11 +40,12 @@ BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][configuration]
 P_SLOTS = 512                                        # persistent grid: 2 workgroups x 256 CUs
 
 
-def pick_cfg(m: int, scheme) -> int:
-    """The kernel's run-time choice from the group's rows (w4a4-g128, mxfp4 and
-    fp8 stop at 64)."""
+def pick_cfg(m: int, scheme, phase: int = 0) -> int:
+    """The kernel's run-time choice from the group's rows (w4a4-g128 and mxfp4
+    stop at 64, fp8 outside the down phase)."""
     c = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
-    if scheme.a_bits < 16 and (scheme.a_group > 0 or getattr(scheme, "fmt", 0) == 2) and c == 3:
+    capped = scheme.a_group > 0 or (getattr(scheme, "fmt", 0) == 2 and phase != 1)
+    if scheme.a_bits < 16 and capped and c == 3:
         c = 2
     return c
 
@@ -76,7 +77,7 @@ class CostTable:
         """Serial tile time of one linear block (phase 0: gate and up together)."""
         if m <= 0:
             return 0.0
-        c = pick_cfg(m, scheme)
+        c = pick_cfg(m, scheme, phase)
         return n_tiles(m, n, phase, c) * self.tile_ns(phase, scheme, c, k)
 
     def block_ns(self, cfg, counts: Sequence[int], schemes) -> List[float]:
@@ -185,8 +186,8 @@ def profile(schemes=None, k_lo: int = 1024, k_hi: int = 4096, reps: int = 5, log
     table = {"P": P_SLOTS, "k_points": [k_lo, k_hi], "unit": "ns per tile; c_t(K) = a + b * K / 128",
              "cost": {"0": {}, "1": {}}, "raw": {"0": {}, "1": {}}}
     for s in schemes:
-        cfgs = [0, 1, 2] if pick_cfg(1 << 20, s) == 2 else [0, 1, 2, 3]   # kinds capped at 64-row tiles
         for phase in (0, 1):
+            cfgs = [0, 1, 2] if pick_cfg(1 << 20, s, phase) == 2 else [0, 1, 2, 3]   # kinds capped at 64-row tiles
             lo = _probe(s, phase, k_lo, cfgs, reps, log=log)
             hi = _probe(s, phase, k_hi, cfgs, reps, log=log)
             ab = []
@@ -275,7 +276,9 @@ def main():
                 for ph in ("0", "1"):
                     table[key][ph].update(new[key][ph])
             prev = table.get("command", "")
-            table["command"] = (prev + "; then " if prev else "") + cmd + " --merge"
+            step = cmd + " --merge"
+            if step not in prev.split("; then "):
+                table["command"] = (prev + "; then " if prev else "") + step
         else:
             table = new
             table["command"] = cmd

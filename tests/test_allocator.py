@@ -68,7 +68,7 @@ def test_tile_counts_and_configuration_match_the_plan():
             for m, r in zip(counts, plan):
                 if m == 0:
                     continue
-                c = TC.pick_cfg(m, s)
+                c = TC.pick_cfg(m, s, phase)
                 assert c == r["cfg"], (s.name, m)
                 assert TC.n_tiles(m, 1408, phase, c) == r["mtiles"] * r["ntiles"]
 
@@ -87,7 +87,7 @@ def test_block_model_closed_form():
             continue
         F = cfg.F if e < cfg.E else cfg.F_shared
         for ph, (n, k) in enumerate(((F, cfg.H), (cfg.H, F))):
-            c = TC.pick_cfg(m, sch[e][0 if ph == 0 else 2])
+            c = TC.pick_cfg(m, sch[e][0 if ph == 0 else 2], ph)
             a, b = tab["cost"][str(ph)][sch[e][0 if ph == 0 else 2].name][c]
             want[ph] += -(-m // TC.BM[c]) * -(-n // TC.BN[ph][c]) * (a + b * k / 128)
     got = t.block_ns(cfg, counts, sch)
