@@ -14,9 +14,14 @@ linears) and microseconds per layer, the roofline of the dominant kernel (the
 gate/up Group-GEMM launch, timed with HIP events on the library's stream), and
 the CPU oracle timed on a bounded token sample.
 
-The default workload is the Mixtral-8x7B-shaped prefill block: 4096 tokens,
-hidden 4096, expert FFN 14336, 8 experts, top-2, Zipf(1.0) routing skew,
-3.26 average weight bits (hot expert w8a8, cold experts w2/w3/w4 g128).
+The default workload is the Qwen2-57B-A14B-shaped prefill block, the largest
+single-GPU configuration: 16384 tokens, hidden 3584, 64 routed experts of FFN
+2560, top-8, one shared expert of FFN 20480, Zipf(1.0) routing skew; hot
+experts (ranks 1-10) and the shared expert w8a8, the others w4a4.
+
+The 256 MiB Infinity Cache is defeated by rotation: the timed steps cycle
+through ceil(512 MiB / touched bytes) + 1 independent copies of the packed
+weights and of x, so no step finds the previous step's operands in the cache.
 """
 
 import argparse
@@ -32,16 +37,35 @@ if ROOT not in sys.path:
 import numpy as np
 
 HBM_PEAK = 8.0e12            # B/s
-MFMA_PEAK = {"i8": 5.0e15, "bf16": 2.5e15, "fp16": 2.5e15}
+# dense MFMA peaks of MI355X by operand type (int8 in OP/s)
+MFMA_PEAK = {"i8": 5.0e15, "fp8": 5.0e15, "fp4": 10.1e15, "bf16": 2.5e15, "fp16": 2.5e15}
+ROTATE_BYTES = 512 << 20     # Infinity Cache (256 MiB) defeat: rotate copies covering twice its size
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def act_bytes(s):
+    """Bytes per activation element a linear of scheme s reads: 0.5 for MXFP4
+    codes, 1 for int8 / FP8 codes, 2 for 16-bit rows."""
+    if getattr(s, "fmt", 0) == 1:
+        return 0.5
+    return 1.0 if s.a_bits < 16 else 2.0
+
+
+def mfma_dtype(s, act):
+    """Operand type of the MFMA a scheme runs on (the key of MFMA_PEAK)."""
+    fmt = getattr(s, "fmt", 0)
+    if fmt == 1:
+        return "fp4"
+    if fmt == 2:
+        return "fp8"
+    return "i8" if s.a_bits < 16 else act
+
+
 def group_stats(blk, counts):
     """Per (phase, expert) algorithmic flops / bytes and the MFMA dtype."""
-    from paper_2505_05799_amd import workloads as W
     cfg = blk.cfg
     out = []
     for e, lins in enumerate(blk.linears):
@@ -53,14 +77,12 @@ def group_stats(blk, counts):
             for j in idx:
                 q = lins[j]
                 fl += 2.0 * m * q.n * q.k
-                a_bytes = 1.0 if q.scheme.a_bits < 16 else 2.0
-                by += q.nbytes_packed + m * q.k * a_bytes
+                by += q.nbytes_packed + m * q.k * act_bytes(q.scheme)
             n_out = lins[idx[0]].n
             by += m * n_out * (2.0 if phase == 0 else 4.0)
             s = lins[idx[0]].scheme
-            dt = "i8" if s.a_bits < 16 else cfg.act
-            out.append({"expert": e, "phase": phase, "m": m, "flops": fl, "bytes": by, "dtype": dt,
-                        "scheme": s.name})
+            out.append({"expert": e, "phase": phase, "m": m, "flops": fl, "bytes": by,
+                        "dtype": mfma_dtype(s, cfg.act), "scheme": s.name})
     return out
 
 
@@ -87,11 +109,12 @@ def roofline(groups, phase, t_s, traffic=None):
     return out
 
 
-def per_group(mb, blk, x, ids, w, groups, reps=5):
+def per_group(blocks, xs, blk, ids, w, groups, reps=6):
     """Groups of one phase with the same scheme and the same bound (HBM when
     moving the group's bytes at 8 TB/s takes longer than its MFMA work at the
     dtype's peak, else MFMA), each timed alone with an expert mask (the launch
-    then holds only their tiles), against the roof of its bound."""
+    then holds only their tiles), against the roof of its bound.  The
+    repetitions rotate over the cache-defeating copies."""
     import torch
     from paper_2505_05799_amd import mxmoe as M
     cfg = blk.cfg
@@ -108,11 +131,11 @@ def per_group(mb, blk, x, ids, w, groups, reps=5):
         mask = [0] * G
         for g in gs:
             mask[g["expert"]] = 1
-        for _ in range(2):
-            mb.forward(x, ids, w, expert_mask=mask, skip_combine=True)
+        for i in range(2):
+            blocks[i % len(blocks)].forward(xs[i % len(xs)], ids, w, expert_mask=mask, skip_combine=True)
         ts = []
-        for _ in range(reps):
-            mb.forward(x, ids, w, expert_mask=mask, skip_combine=True, events=ev)
+        for i in range(reps):
+            blocks[i % len(blocks)].forward(xs[i % len(xs)], ids, w, expert_mask=mask, skip_combine=True, events=ev)
             torch.cuda.synchronize()
             ts.append(ev.elapsed_ms()[1 if phase == 0 else 3])
         t = float(np.median(ts)) / 1e3
@@ -149,8 +172,20 @@ def copy_calibration():
     log(f"[bench] copied {P.COPY_BYTES >> 20} MiB 3 times")
 
 
-def cpu_baseline(blk, tokens):
-    """The CPU oracle as it stands, on the first `tokens` tokens of the workload."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(blk, tokens, seed=0):
+    """The CPU oracle as it stands, on a uniform random sample of `tokens`
+    tokens of the workload (all their routed experts and the shared experts)."""
     from oracle import mxmoe_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -158,30 +193,56 @@ def cpu_baseline(blk, tokens):
     except Exception:
         cores = os.cpu_count() or 1
     cfg = blk.cfg
-    # Bounded sample: the first `tokens` tokens whose experts all lie among the
-    # few hottest experts (so only those experts' weights are dequantized).
-    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
-    hot = list(np.argsort(-counts, kind="stable"))
-    for ns in range(cfg.k, cfg.E + 1):
-        ok = np.isin(blk.topk_ids, hot[:ns]).all(axis=1)
-        if ok.sum() >= tokens or ns == cfg.E:
-            break
-    sel = np.nonzero(ok)[0][:tokens]
+    n = min(tokens, cfg.T)
+    sel = np.sort(np.random.default_rng([seed, 11]).choice(cfg.T, size=n, replace=False))
     ids = blk.topk_ids[sel]
-    n = len(sel)
-    flops = cfg.scaled(n).flops(np.bincount(ids.ravel(), minlength=cfg.E))
+    counts = np.bincount(ids.ravel(), minlength=cfg.E)
+    flops = cfg.scaled(n).flops(counts)
     t0 = time.perf_counter()
     O.moe_forward(blk.x[sel], ids, blk.topk_w[sel], blk.linears, cfg.E, cfg.act)
     dt = time.perf_counter() - t0
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"{n} of {cfg.T} tokens (the first routed only to the {ns} hottest experts), "
-                      f"fp64 numpy incl. dequantization of those experts", "seconds": round(dt, 2)}
+            "sample": f"{n} of {cfg.T} tokens drawn uniformly at random (seed {seed}): their "
+                      f"{int((counts > 0).sum())} routed experts and {cfg.n_shared} shared expert(s), fp64 "
+                      f"numpy incl. dequantization of every linear touched",
+            "seconds": round(dt, 2), "cpu_model": cpu_model()}
+
+
+def touched_bytes(blk, counts):
+    """Packed weight bytes of the experts that receive tokens, plus x."""
+    cfg = blk.cfg
+    b = 0
+    for e, lins in enumerate(blk.linears):
+        if e < cfg.E and counts[e] == 0:
+            continue
+        b += sum(q.nbytes_packed for q in lins)
+    return b + blk.x.nbytes
+
+
+def rotation_copies(mb, blk, x, n):
+    """n - 1 further MoEBlocks over device copies of the packed weights, and
+    copies of x, for cache-defeating rotation."""
+    import copy
+    from paper_2505_05799_amd import mxmoe as M
+    blocks, xs = [mb], [x]
+    for _ in range(n - 1):
+        packed = []
+        for ps in mb.packed:
+            row = []
+            for p in ps:
+                c = copy.copy(p)
+                c.buf = p.buf.clone()
+                row.append(c)
+            packed.append(row)
+        blocks.append(M.MoEBlock(blk, packed=packed))
+        xs.append(x.clone())
+    return blocks, xs
 
 
 def compare_per_expert(args):
     """One Group-GEMM launch per phase against the same micro-kernels launched
     once per expert (the per-expert invocation the paper's motivation study
-    measures, Sec. 2.3 and its throughput figure): 60 experts, gate+up of shape
+    measures, Sec. 3.2 and its throughput figure): 60 experts, gate+up of shape
     [N, K] = [2816, 2048] per expert, top-4, 512 tokens, uniform schemes.  The
     per-expert figure sums the HIP-event durations of the single-expert
     launches (each runs after its own plan, which is not counted), so it
@@ -236,15 +297,20 @@ def compare_per_expert(args):
     return out
 
 
+def pct(v, q):
+    return round(float(np.percentile(v, q)), 4)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="mixtral")
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen2")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-tokens", type=int, default=1024)
+    ap.add_argument("--cpu-tokens", type=int, default=2048)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rotate", action="store_true", help="time one copy of the operands (no cache defeat)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 256 MiB device copy (memory-counter calibration)")
     ap.add_argument("--compare-per-expert", action="store_true",
@@ -289,53 +355,85 @@ def main():
     y = torch.empty_like(x)
     counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
     flops = cfg.flops(counts)
-    log(f"[bench] packed {sum(p.nbytes for ps in mb.packed for p in ps) / 1e6:.1f} MB; "
+    touched = touched_bytes(blk, counts)
+    ncopy = 1 if args.no_rotate else -(-ROTATE_BYTES // touched) + 1
+    blocks, xs = rotation_copies(mb, blk, x, ncopy)
+    torch.cuda.synchronize()
+    log(f"[bench] packed {sum(p.nbytes for ps in mb.packed for p in ps) / 1e6:.1f} MB "
+        f"({touched / 1e6:.1f} MB touched per forward, {ncopy} rotating copies); "
         f"{flops / 1e9:.1f} GFLOP per forward; warmup {args.warmup}")
 
-    for _ in range(args.warmup):
-        mb.forward(x, ids, w, y=y)
+    def step(i, ev=None):
+        c = i % ncopy
+        blocks[c].forward(xs[c], ids, w, y=y, events=ev)
+
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
-    graph = None
+    graphs = None
     if args.graph:
-        # the whole forward captured once; a replay issues the same kernels
+        # every copy's forward captured once; a replay issues the same kernels
         # without host launch overhead between them
         cs = torch.cuda.Stream()
         cs.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(cs):
-            mb.forward(x, ids, w, y=y)
+            for c in range(ncopy):
+                step(c)
         torch.cuda.current_stream().wait_stream(cs)
         torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            mb.forward(x, ids, w, y=y)
-        for _ in range(args.warmup):
-            graph.replay()
+        graphs = []
+        for c in range(ncopy):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(c)
+            graphs.append(g)
+        for i in range(args.warmup):
+            graphs[i % ncopy].replay()
         torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps ({'eager' if graph is None else 'graph replays'})")
+    # Timed region: exactly `steps` forwards.  Eager steps carry the library's
+    # per-phase HIP events (recorded on the stream the kernels run on), which
+    # give the per-step durations and the dominant launch's duration.
+    evs = [M.PhaseEvents() for _ in range(args.steps)] if graphs is None else None
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)] if graphs is not None else None
+    log(f"[bench] timing {args.steps} steps ({'eager' if graphs is None else 'graph replays'})")
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     for i in range(args.steps):
-        if graph is None:
-            mb.forward(x, ids, w, y=y)
+        if graphs is None:
+            step(i, evs[i])
         else:
-            graph.replay()
+            starts[i].record()
+            graphs[i % ncopy].replay()
+    if starts is not None:
+        starts[args.steps].record()
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     ms = (t2 - t1) * 1e3 / args.steps
-    # per-phase launch durations: eager forwards with HIP events on the
-    # library's stream (not part of the timed region)
-    evs = [M.PhaseEvents() for _ in range(args.steps)]
-    for i in range(args.steps):
-        mb.forward(x, ids, w, y=y, events=evs[i])
-    torch.cuda.synchronize()
-    phases = np.array([e.elapsed_ms() for e in evs])          # [steps, 5]
+    if graphs is None:
+        phases = np.array([e.elapsed_ms() for e in evs])          # [steps, 5]
+        per_step = np.array([e.span_ms() for e in evs])
+    else:
+        # phase durations of graph replays: eager forwards with events after the timed region
+        evs = [M.PhaseEvents() for _ in range(args.steps)]
+        for i in range(args.steps):
+            step(i, evs[i])
+        torch.cuda.synchronize()
+        phases = np.array([e.elapsed_ms() for e in evs])
+        per_step = np.array([starts[i].elapsed_time(starts[i + 1]) for i in range(args.steps)])
     ph_mean = phases.mean(axis=0)
     groups = group_stats(blk, counts)
-    dom = 1  # gate/up Group-GEMM launch
-    roof = roofline(groups, 0, ph_mean[dom] / 1e3, measured_traffic(args.workload, 0))
-    roof["kernel"] = "group_gemm_kernel<bf16, gate|up>" if cfg.act == "bf16" else "group_gemm_kernel<fp16, gate|up>"
+    phase_gu, phase_dn = 1, 3
+    dom = phase_gu if ph_mean[phase_gu] >= ph_mean[phase_dn] else phase_dn
+    dname = "gate|up" if dom == phase_gu else "down"
+    roof = roofline(groups, 0 if dom == phase_gu else 1, ph_mean[dom] / 1e3,
+                    measured_traffic(args.workload, 0 if dom == phase_gu else 1))
+    kact = "bf16" if cfg.act == "bf16" else "fp16"
+    roof["kernel"] = f"group_gemm_kernel<{kact}, {dname}>"
     roof["launch_ms"] = round(float(ph_mean[dom]), 4)
-    down = roofline(groups, 1, ph_mean[3] / 1e3, measured_traffic(args.workload, 1))
+    other = roofline(groups, 1 if dom == phase_gu else 0, ph_mean[phase_dn if dom == phase_gu else phase_gu] / 1e3,
+                     measured_traffic(args.workload, 1 if dom == phase_gu else 0))
+    other["kernel"] = f"group_gemm_kernel<{kact}, {'down' if dom == phase_gu else 'gate|up'}>"
+    dtypes = sorted({g["dtype"] for g in groups})
 
     rec = {
         "metric": "MoE-block us/layer + effective TFLOP/s; % of HBM/MFMA roofline per group",
@@ -346,25 +444,30 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "us_per_layer": round(ms * 1e3, 1),
+        "step_ms": {"median": pct(per_step, 50), "p10": pct(per_step, 10), "p90": pct(per_step, 90)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "i8+bf16" if cfg.act == "bf16" else "i8+fp16",
+        "dtype": "+".join(dtypes),
         "data": "synthetic",
-        "config": {"workload": cfg.description, "tokens": cfg.T, "hidden": cfg.H, "ffn": cfg.F,
+        "config": {"workload": cfg.description, "name": cfg.name, "tokens": cfg.T, "hidden": cfg.H, "ffn": cfg.F,
                    "experts": cfg.E, "top_k": cfg.k, "shared_experts": cfg.n_shared,
-                   "avg_weight_bits": round(W.avg_weight_bits(cfg), 3), "gflop": round(flops / 1e9, 2)},
+                   "ffn_shared": cfg.F_shared, "avg_weight_bits": round(W.avg_weight_bits(cfg), 3),
+                   "gflop": round(flops / 1e9, 2)},
         "roofline": roof,
-        "roofline_down": down,
+        "roofline_other": other,
         "phases_ms": {n: round(float(v), 4) for n, v in zip(M.PHASE_NAMES, ph_mean)},
-        "timing": "eager forwards" if graph is None else "replays of the forward captured in a HIP graph",
+        "timing": ("eager forwards with per-phase HIP events" if graphs is None
+                   else "replays of the forward captured in a HIP graph"),
+        "cache_defeat": (f"rotating {ncopy} copies of the packed weights and x "
+                         f"({touched / 1e6:.1f} MB touched per forward)" if ncopy > 1 else "none"),
     }
     if not args.no_groups:
         log("[bench] per-group rooflines (each class of groups timed alone)")
-        rec["groups"] = per_group(mb, blk, x, ids, w, groups)
+        rec["groups"] = per_group(blocks, xs, blk, ids, w, groups)
     if not args.no_cpu_baseline:
-        log(f"[bench] CPU oracle on {args.cpu_tokens} tokens")
-        rec["cpu_baseline"] = cpu_baseline(blk, args.cpu_tokens)
+        log(f"[bench] CPU oracle on {args.cpu_tokens} random tokens")
+        rec["cpu_baseline"] = cpu_baseline(blk, args.cpu_tokens, args.seed)
     else:
         rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)

@@ -446,6 +446,14 @@ class PhaseEvents:
             out.append(float(t.value))
         return out
 
+    def span_ms(self):
+        """Duration (ms) of the whole last forward recorded with these events."""
+        self.hip.hipEventSynchronize(self.array[2 * N_PHASES - 1])
+        t = C.c_float()
+        if self.hip.hipEventElapsedTime(C.byref(t), self.array[0], self.array[2 * N_PHASES - 1]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(t.value)
+
     def __del__(self):
         try:
             for i in range(2 * N_PHASES):
