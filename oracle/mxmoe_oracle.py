@@ -20,11 +20,11 @@ operands the GPU receives (codes, scales, zeros - never the packed layout):
   renormalised over those k); a shared expert's output may be scaled by a
   per-token sigmoid gate (Qwen-MoE style shared experts).
 * MXFP4 (the OCP Microscaling format the MI355X matrix cores take natively; the
-  paper's scheme set S is whatever the hardware supports, Sec. 3.1): a value is
+  paper's scheme set S is whatever the hardware supports, Sec. 4.2.1): a value is
   an FP4 e2m1 element times a power-of-two scale shared by 32 consecutive
   values along K; activations get the same encoding at run time.
 * FP8 (OCP e4m3, the 8-bit floating-point operand of the MI355X matrix cores;
-  again a member of the hardware's scheme set, Sec. 3.1): a weight is an e4m3
+  again a member of the hardware's scheme set, Sec. 4.2.1): a weight is an e4m3
   value times a per-channel fp32 scale, an activation an e4m3 value times a
   per-token fp32 scale that maps the row's largest magnitude onto 448.
 * Sec. 4.2.2 (end): activations of w8a8 / w4a4 linears are quantized dynamically
@@ -49,7 +49,7 @@ import numpy as np
 
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "router_topk", "shared_gate", "dequant",
-    "act_quant", "fp8_quant", "e4m3_values", "e4m3_code", "fp8_block_bound", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
+    "act_quant", "fp8_quant", "e4m3_values", "e4m3_code", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
     "silu", "tile_plan", "xcd_queues", "xcd_tiles",
 ]
 
@@ -376,193 +376,34 @@ def silu(g: np.ndarray) -> np.ndarray:
         return g / (1.0 + np.exp(-g))
 
 
-def _dsilu(g: np.ndarray) -> np.ndarray:
-    with np.errstate(over="ignore"):
-        sg = 1.0 / (1.0 + np.exp(-g))
-    return sg * (1.0 + g * (1.0 - sg))
-
-
 # ----------------------------------------------------------------------------
 # O5-O7: expert MLP, gate-weighted combine (Eq. 1-2)
 # ----------------------------------------------------------------------------
 
-# Bounds on how far the GPU's fp32 g / u may sit from the fp64 values.  They only
-# decide which a8/a4 codes of the down projection are *fragile* (their rounding
-# decision could go either way given fp32 accumulation), see _down_slack.
-_EPS_FLOAT_ACC = 2.0 ** -20   # relative to sum |a||w|, fp32-accumulated GEMMs
-_EPS_INT_EPI = 2.0 ** -21     # relative to |g|, exact int32 acc + 2 fp32 products
-_EPS_EPI = 2.0 ** -20         # relative to |h|, SiLU + product in fp32
-
-
-def _gate_up_bound(a: np.ndarray, lin, act: str, out: np.ndarray,
-                   w_deq: Optional[np.ndarray]) -> np.ndarray:
-    if getattr(lin.scheme, "fmt", 0) == 1:
-        qa, ea = mx_quant(a.astype(np.float32), lin.scheme.a_group)
-        return _EPS_FLOAT_ACC * (np.abs(_mx_values(qa, ea, lin.scheme.a_group)) @ np.abs(dequant(lin, act)).T)
-    if getattr(lin.scheme, "fmt", 0) == 2:
-        qa, sa = fp8_quant(a.astype(np.float32))
-        return fp8_block_bound(e4m3_values(qa) * sa.astype(np.float64)[:, None], dequant(lin, act))
-    if lin.scheme.a_bits < 16 and lin.scheme.a_group > 0:
-        # fp32 running sum of block products: bounded like an fp32-accumulated GEMM
-        # on the dequantized operands
-        qa, sa = act_quant_groups(a.astype(np.float32), _qmax(lin.scheme.a_bits), lin.scheme.a_group)
-        ad = (qa.astype(np.float64).reshape(a.shape[0], -1, lin.scheme.a_group)
-              * sa.astype(np.float64)[..., None]).reshape(a.shape)
-        return _EPS_FLOAT_ACC * (np.abs(ad) @ np.abs(dequant(lin, act)).T)
-    if lin.scheme.a_bits < 16:
-        return _EPS_INT_EPI * np.abs(out)
-    if w_deq is None:
-        w_deq = dequant(lin, act)
-    return _EPS_FLOAT_ACC * (np.abs(a) @ np.abs(w_deq).T)
-
-
-# The FP8 MFMA does not add the 128 products of a k block in full fp32: on
-# MI355X its result lies within 2^-11.2 of the block's largest product (random
-# and adversarial operands), consistent with products aligned to the largest
-# one and rounded about 16 bits below it.  Bounds charge 2^-9 of
-# max|a| max|w| per block, then fp32 accumulation across blocks.
-_EPS_F8_BLOCK = 2.0 ** -9
-
-
-def fp8_block_bound(ad: np.ndarray, wd: np.ndarray, block: int = 128) -> np.ndarray:
-    """Bound [m, n] on |FP8 GEMM - exact| for decoded (scaled) operands ad [m, k]
-    and wd [n, k]: per k block 2^-9 max|ad| max|wd|, plus 2^-20 sum |ad||wd|."""
-    m, k = ad.shape
-    am = np.abs(ad).reshape(m, k // block, block).max(axis=2)
-    wm = np.abs(wd).reshape(wd.shape[0], k // block, block).max(axis=2)
-    return _EPS_F8_BLOCK * (am @ wm.T) + _EPS_FLOAT_ACC * (np.abs(ad) @ np.abs(wd).T)
-
-
-def _down_slack(h64: np.ndarray, dh: np.ndarray, hb: np.ndarray, lin, act: str):
-    """Per-element output slack of an a8/a4 down projection.
-
-    The GPU rounds its fp32 h to the activation dtype; it can land on another
-    neighbour than the oracle's fp64 h when h64 sits within ``dh`` of a rounding
-    midpoint, and that can move an activation code.  Codes are monotone in h and
-    in 1/amax, so the reachable codes lie between the corner cases computed here,
-    per quantization block (the whole row per token, or each 128-wide group).
-    Returns slack [m, n] >= |effect on the down output| of every such move.
-    """
-    if getattr(lin.scheme, "fmt", 0) == 1:
-        return _down_slack_mx(h64, dh, hb, lin, act)
-    fp8 = getattr(lin.scheme, "fmt", 0) == 2
-    # grid value of a scaled element: the clamped integer code, or the signed
-    # e4m3 value (both monotone in the element and in the inverse scale)
-    if fp8:
-        qmax = E4M3_MAX
-
-        def grid(p):
-            return np.sign(p) * _E4M3[e4m3_code(np.abs(p))]
-    else:
-        qmax = _qmax(lin.scheme.a_bits)
-
-        def grid(p):
-            return np.clip(np.rint(p), -qmax, qmax)
-    m, F = h64.shape
-    g = lin.scheme.a_group if lin.scheme.a_group > 0 else F
-    nb = F // g
-    lo = round_to_act(h64 - dh, act).reshape(m * nb, g)
-    hi = round_to_act(h64 + dh, act).reshape(m * nb, g)
-    if fp8:
-        c0, s0 = fp8_quant(hb.astype(np.float32).reshape(m * nb, g))
-        q0 = e4m3_values(c0)
-    else:
-        q0, s0 = act_quant(hb.astype(np.float32).reshape(m * nb, g), qmax)
-    alo = np.where(np.sign(lo) == np.sign(hi), np.minimum(np.abs(lo), np.abs(hi)), 0.0)
-    ahi = np.maximum(np.abs(lo), np.abs(hi))
-    amax_lo = alo.max(axis=1)
-    amax_hi = ahi.max(axis=1)
-    rows = np.nonzero((lo != hi).any(axis=1) | (amax_lo != amax_hi))[0]
-    n = lin.n
-    slack = np.zeros((m, n))
-    if rows.size == 0:
-        return slack
-    q32 = np.float32(qmax)
-    dq = np.zeros((m * nb, g))
-    ds = np.zeros(m * nb)
-    for corner_amax in (amax_lo[rows], amax_hi[rows]):
-        am = corner_amax.astype(np.float32)
-        zero = am == 0
-        safe = np.where(zero, np.float32(1), am)
-        inv = np.where(zero, np.float32(0), (q32 / safe).astype(np.float32))
-        sc = np.where(zero, np.float32(0), (safe / q32).astype(np.float32))
-        ds[rows] = np.maximum(ds[rows], np.abs(sc.astype(np.float64) - s0[rows].astype(np.float64)))
-        for hv in (lo[rows], hi[rows]):
-            qc = grid((hv.astype(np.float32) * inv[:, None]).astype(np.float32))
-            qc = np.where(zero[:, None], 0, qc)
-            dq[rows] = np.maximum(dq[rows], np.abs(qc - q0[rows]))
-    s_max = np.maximum(s0.astype(np.float64), s0.astype(np.float64) + ds)
-    qabs = np.abs(q0.astype(np.float64))
-    DQ = (dq * s_max[:, None]).reshape(m, F)
-    QD = ((qabs + dq) * ds[:, None]).reshape(m, F)
-    wabs = np.abs(dequant(lin, act))
-    return (DQ + QD) @ wabs.T
-
-
-def _down_slack_mx(h64, dh, hb, lin, act):
-    """The slack of an MXFP4 down projection.  Where the GPU's rounded h can
-    differ from the oracle's (h64 within dh of a rounding midpoint), the
-    GPU's value v of an element lies between the rounded corners lo and hi,
-    and its block's shared exponent between those of the smallest and largest
-    possible block maxima.  For a fixed exponent the decoded value is monotone
-    in v, so it lies between the decoded corners under one of those exponents."""
-    m, F = h64.shape
-    g = lin.scheme.a_group
-    nb = F // g
-    lo = round_to_act(h64 - dh, act).reshape(m, nb, g)
-    hi = round_to_act(h64 + dh, act).reshape(m, nb, g)
-    moved = (lo != hi).any(axis=2)
-    if not moved.any():
-        return np.zeros((m, lin.n))
-    q0, e0 = mx_quant(hb.astype(np.float32), g)
-    d0 = _mx_values(q0, e0, g).reshape(m, nb, g)
-    same = np.sign(lo) == np.sign(hi)
-    e_lo = _mx_exponent(np.where(same, np.minimum(np.abs(lo), np.abs(hi)), 0.0).max(axis=2))
-    e_hi = _mx_exponent(np.maximum(np.abs(lo), np.abs(hi)).max(axis=2))
-    dev = np.zeros((m, nb, g))
-    for step in range(int((e_hi - e_lo).max()) + 1):
-        e = np.minimum(e_lo + step, e_hi).astype(np.float64)[..., None]
-        for corner in (lo, hi):
-            mag = _E2M1[_e2m1_code(np.abs(corner) / np.exp2(e))]
-            dev = np.maximum(dev, np.abs(np.sign(corner) * mag * np.exp2(e) - d0))
-    dev *= moved[..., None]
-    return dev.reshape(m, F) @ np.abs(dequant(lin, act)).T
-
-
-def _expert_mlp(a: np.ndarray, lins: Sequence, act: str, want_slack: bool):
+def _expert_mlp(a: np.ndarray, lins: Sequence, act: str):
     """Eq. (1) for one expert on rows a [m, H] (fp64 act values).
 
-    Returns (down output fp64 [m, H], h rounded to act [m, F], slack [m, H] or None).
+    Returns (down output fp64 [m, H], h rounded to act [m, F]).
     """
     gate, up, down = lins
     wg = dequant(gate, act) if gate.scheme.a_bits == 16 else None
     wu = dequant(up, act) if up.scheme.a_bits == 16 else None
     g = linear(a, gate, act, wg)
     u = linear(a, up, act, wu)
-    h64 = silu(g) * u
-    hb = round_to_act(h64, act)                  # rounding point: h stored in act dtype
-    d = linear(hb, down, act)
-    slack = None
-    if want_slack and down.scheme.a_bits < 16:
-        dg = _gate_up_bound(a, gate, act, g, wg)
-        du = _gate_up_bound(a, up, act, u, wu)
-        dh = (np.abs(_dsilu(g) * u) * dg + np.abs(silu(g)) * du
-              + _EPS_EPI * np.abs(h64))
-        slack = _down_slack(h64, dh, hb, down, act)
-    return d, hb, slack
+    hb = round_to_act(silu(g) * u, act)          # rounding point: h stored in act dtype
+    return linear(hb, down, act), hb
 
 
 def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
                 linears: Sequence[Sequence], E: int, act: str,
-                want_slack: bool = False, return_h: bool = False,
-                shared_w: Optional[np.ndarray] = None):
+                return_h: bool = False, shared_w: Optional[np.ndarray] = None):
     """Eq. (2): y[t] = sum_s w[t,s] * Expert_{ids[t,s]}(x[t]) + sum_j g[t,j] * Shared_j(x[t]),
     with g = ``shared_w`` [T, n_shared] (fp32 values) or 1.
 
     x: [T, H] activations in act storage; topk_ids int32 [T, k]; topk_w fp32
     [T, k]; linears[e] = (gate, up, down) for e < E routed, then shared experts.
-    Returns dict with y (fp64, unrounded), slack (fp64 [T,H] or None) and
-    optionally per-expert h.
+    Returns dict with y (fp64, unrounded), the routing and optionally
+    per-expert h.
     """
     a_all = act_values(x, act)
     T, H = a_all.shape
@@ -570,7 +411,6 @@ def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
     r = route(topk_ids, E)
     w64 = np.asarray(topk_w, dtype=np.float64).ravel()
     y = np.zeros((T, H))
-    slack = np.zeros((T, H)) if want_slack else None
     hs = {}
     for e in range(E):
         lo, hi = int(r["offsets"][e]), int(r["offsets"][e + 1])
@@ -578,22 +418,18 @@ def moe_forward(x: np.ndarray, topk_ids: np.ndarray, topk_w: np.ndarray,
             continue
         pairs = r["sorted_pair"][lo:hi].astype(np.int64)
         toks = pairs // k
-        d, hb, sl = _expert_mlp(a_all[toks], linears[e], act, want_slack)
+        d, hb = _expert_mlp(a_all[toks], linears[e], act)
         # pairs of one expert belong to distinct tokens (top-k ids are distinct per token)
         np.add.at(y, toks, d * w64[pairs][:, None])
-        if sl is not None:
-            np.add.at(slack, toks, sl * np.abs(w64[pairs])[:, None])
         if return_h:
             hs[e] = hb
     for j in range(len(linears) - E):
-        d, hb, sl = _expert_mlp(a_all, linears[E + j], act, want_slack)
+        d, hb = _expert_mlp(a_all, linears[E + j], act)
         gj = np.ones((T, 1)) if shared_w is None else np.asarray(shared_w, dtype=np.float64)[:, j:j + 1]
         y += d * gj
-        if sl is not None:
-            slack += sl * np.abs(gj)
         if return_h:
             hs[E + j] = hb
-    out = {"y": y, "slack": slack, "route": r}
+    out = {"y": y, "route": r}
     if return_h:
         out["h"] = hs
     return out

@@ -294,7 +294,9 @@ LinWs lin_layout(int kd, int m, int n, int k) {
   w.qcap = plan_queue_cap(m, 1, n);
   w.fcap = plan_flat_cap(w.qcap);
   w.plan = o; o = align256(o + 4 * (size_t)plan_layout(1, w.qcap, w.fcap).total);
-  w.pfloats = std::min<int64_t>((int64_t)1 << 24, 4 * (int64_t)m * n);
+  // split-K partial sums: room for every tile of the linear in up to 8 slices
+  // (at most m + 128 rows by n + 512 channels of tiles), at most 64 MB
+  w.pfloats = std::min<int64_t>((int64_t)1 << 24, 8 * ((int64_t)m + 128) * ((int64_t)n + 512));
   w.partial = o; o = align256(o + 4 * (size_t)w.pfloats);
   w.aq = w.as = w.rsa = kNone;
   if (kind_is_int(kd)) {

@@ -268,9 +268,10 @@ class PackedLinear:
         return c, sc, z
 
 
-def linear_forward(pl: PackedLinear, a, stream=None):
+def linear_forward(pl: PackedLinear, a, stream=None, return_ws: bool = False):
     """out = a W^T through the micro-kernels: int32 for w8a8/w4a4 (per channel),
-    else fp32 (fp8: scaled by s_a[m] s_w[n])."""
+    else fp32 (fp8: scaled by s_a[m] s_w[n]).  return_ws: also return the
+    workspace (its tile plan starts at offset 0)."""
     torch = _torch()
     lib = load_library()
     m = a.shape[0]
@@ -281,7 +282,7 @@ def linear_forward(pl: PackedLinear, a, stream=None):
     ws = empty_aligned(wsb, a.device)
     _check(lib.mxmoe_linear_forward(C.byref(pl.L), act_code(pl.act), _ptr(pl.buf), m, _ptr(a.contiguous()),
                                     _ptr(out), _ptr(ws), wsb, _stream_ptr(stream)), "mxmoe_linear_forward")
-    return out
+    return (out, ws) if return_ws else out
 
 
 # --------------------------------------------------------------- routing

@@ -1,8 +1,8 @@
 """GPU parity on the full-size workloads (the launch configuration the
-benchmark times), against the CPU oracle on sampled tokens: routing arrays and
-the tile plan bit-exact over the whole block, block outputs of the sampled
-tokens within tolerance.  The oracle evaluates each sampled token exactly as
-it would inside the full block (every step of the forward is per token)."""
+benchmark times), against the CPU oracle on every token: routing arrays and
+the tile plan bit-exact over the whole block, then the stage-wise check of
+tests/stagewise.py over all rows of every group (h, down-projection codes,
+slot rows, combine, end-to-end output)."""
 
 import time
 
@@ -12,24 +12,12 @@ import pytest
 from oracle import mxmoe_oracle as O
 from paper_2505_05799_amd import mxmoe as M
 from paper_2505_05799_amd import workloads as W
-from tests.gpuhelp import compare_block, say, torch_mod, upload_inputs
+from tests.gpuhelp import say, torch_mod, upload_inputs
+from tests.stagewise import check_forward
 
 pytestmark = pytest.mark.gpu
 
 NAMES = ["tiny", "mixtral", "dsv2lite", "qwen15_uniform", "qwen15_mixed", "qwen15_w5a5", "qwen15_float", "qwen2"]
-
-
-def sample_tokens(blk, n_random=10, seed=0):
-    """Random tokens plus, for the hottest, a middle and the coldest non-empty
-    expert, the first token routed to it."""
-    cfg = blk.cfg
-    rng = np.random.default_rng(seed)
-    picks = set(rng.choice(cfg.T, size=min(n_random, cfg.T), replace=False).tolist())
-    counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E)
-    live = [e for e in np.argsort(-counts, kind="stable") if counts[e] > 0]
-    for e in (live[0], live[len(live) // 2], live[-1]):
-        picks.add(int(np.nonzero((blk.topk_ids == e).any(axis=1))[0][0]))
-    return np.array(sorted(picks))
 
 
 # micro-kernel ids of the schemes in the plan's tile entries
@@ -119,12 +107,8 @@ def test_full_workload(name):
             assert np.array_equal(fl[x, : len(tiles[x])].astype(np.int64), exp.reshape(-1, 4)), (phase, x)
     assert plan_misc(mb, T, G, cap)[4] == 0      # no queue overflow
 
-    # block output on sampled tokens
-    sel = sample_tokens(blk)
-    ref = O.moe_forward(blk.x[sel], blk.topk_ids[sel], blk.topk_w[sel], blk.linears, E, cfg.act, want_slack=True)
-    ynp = M.act_numpy(y, cfg.act)[sel]
-    ratio, nslack = compare_block(ynp, ref, cfg.act, name)
-    say(f"[{name}] {len(sel)} sampled tokens: worst err / (1e-2 rowmax) = {ratio:.4f}, "
-        f"rows with slack {nslack}; {time.perf_counter() - t0:.1f}s")
+    # every token, stage by stage
+    rep = check_forward(mb, blk, y, log=say if G <= 16 else None)
+    say(f"[{name}] all {T} tokens: {rep.line()}; {time.perf_counter() - t0:.1f}s")
     del mb
     torch.cuda.empty_cache()

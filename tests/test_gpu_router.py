@@ -5,13 +5,16 @@ within the fp32 error bound of an exp-sum-divide: each exp within 2 ulp, the
 sum of n positive terms within (n - 1) units of 2^-24, one division, so
 |w - ref| <= (n + 8) 2^-24 ref with n = E (k when renormalised)."""
 
+import dataclasses
+
 import numpy as np
 import pytest
 
 from oracle import mxmoe_oracle as O
 from paper_2505_05799_amd import mxmoe as M
 from paper_2505_05799_amd import workloads as W
-from tests.gpuhelp import compare_block, say, torch_mod, upload_inputs
+from tests.gpuhelp import say, torch_mod, upload_inputs
+from tests.stagewise import check_forward
 
 pytestmark = pytest.mark.gpu
 
@@ -98,9 +101,9 @@ def test_forward_from_logits(renorm):
     assert np.array_equal(M.act_numpy(y2, "bf16"), y_np)
     rids, rw = O.router_topk(l, k, renorm)
     assert np.array_equal(fids, rids)
-    ref = O.moe_forward(blk.x, fids, fw, blk.linears, E, "bf16", want_slack=True, shared_w=fg)
-    ratio, nslack = compare_block(y_np, ref, "bf16", f"router forward renorm={renorm}")
-    say(f"forward from logits renorm={renorm}: ratio {ratio:.4f} slack rows {nslack}")
+    blk2 = dataclasses.replace(blk, topk_ids=fids, topk_w=fw)
+    rep = check_forward(mb, blk2, y, shared_w=fg)
+    say(f"forward from logits renorm={renorm}: {rep.line()}")
 
 
 def test_forward_shared_weights():
@@ -114,5 +117,5 @@ def test_forward_shared_weights():
     x, ids, w = upload_inputs(blk)
     y = mb.forward(x, ids, w, shared_w=torch.from_numpy(g).cuda())
     torch.cuda.synchronize()
-    ref = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 4, "fp16", want_slack=True, shared_w=g)
-    compare_block(M.act_numpy(y, "fp16"), ref, "fp16", "shared weights")
+    rep = check_forward(mb, blk, y, shared_w=g)
+    say(f"shared weights: {rep.line()}")

@@ -553,16 +553,6 @@ def test_uniform_bf16_is_dense_mlp():
     np.testing.assert_allclose(y, h @ wd.T, rtol=1e-12, atol=1e-14)
 
 
-def test_slack_properties():
-    blk = W.random_small_block(8, T=16, H=128, F=128, E=2, k=1,
-                               schemes=[(W.W16, W.W16, W.W4A4), (W.W4G128, W.W4G128, W.W16)])
-    out = O.moe_forward(blk.x, blk.topk_ids, blk.topk_w, blk.linears, 2, "bf16", want_slack=True)
-    sl = out["slack"]
-    assert np.all(sl >= 0)
-    # tokens routed only to the 16-bit-activation down projection carry no slack
-    only1 = blk.topk_ids[:, 0] == 1
-    assert np.all(sl[only1] == 0)
-
 # ---------------------------------------------------------------------------
 # tile scheduling: LPT against the exact optimum (Graham's bound)
 # ---------------------------------------------------------------------------

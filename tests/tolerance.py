@@ -1,0 +1,79 @@
+"""Error models of the GPU arithmetic, used as test tolerances (tests only).
+
+Each bound states the model it rests on; ``tests/test_tolerance.py`` pins the
+models on the CPU by emulating the documented arithmetic in IEEE float32 (in
+the kernels' order of operations) on worst-case-leaning operands, and checks
+that every emulated error stays at least a factor 4 inside the bound.
+
+* ACC16_EPS - GEMMs whose products are exact in fp32 and are added into fp32
+  accumulators (16-bit MFMA for w16 and the dequantized weight-only kinds,
+  the scaled FP4 MFMA for mxfp4): |computed - exact| <= ACC16_EPS * sum |a||w|
+  (a, w the operands as the kernel multiplies them, scales folded in).  The
+  weight-only kinds with bf16 activations add a(c + q - z) with
+  c = 128 + 2^N - 1 and remove c * rowsum(a) per 128-wide group, rescaling the
+  running sum by s_{g-1}/s_g between groups; their emulation includes those
+  steps and the bound is still stated against sum |a| |s (q - z)|.
+* FP8_BLOCK_EPS - the FP8 MFMA adds a 128-wide k block's exact e4m3 products
+  after aligning them to the largest one and dropping bits more than 18
+  places below its leading bit (model reading); a block then errs by less
+  than 127 * 2^(e_max - 18) <= 2^-11 max|p|, and the bound charges
+  FP8_BLOCK_EPS * max|a| * max|w| per block plus ACC16_EPS * sum |a||w| for the
+  fp32 sums across blocks and slices.
+* Gated intermediate h (stage A of the stage-wise check): the GPU forms h in
+  fp32 from fp32 g and u, and rounds it once to the activation dtype.  Under
+  the models above the fp32 value sits within 2^-14 of the row's largest
+  |h| of the exact one, so the stored h lies within one unit in the last
+  place of the activation dtype (at |h|) plus H_ABS_REL * max_row |h| of the
+  exact h.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+U32 = 2.0 ** -24
+ACC16_EPS = 2.0 ** -16
+FP8_BLOCK_EPS = 2.0 ** -9
+H_ABS_REL = 2.0 ** -12
+# fp32 epilogue of the integer kinds: int32 -> fp32 (rounds above 2^24), times
+# the activation scale, times the weight scale, times the gate weight
+INT_EPI_EPS = 4 * U32
+
+
+def acc_bound(a_abs: np.ndarray, w_abs: np.ndarray) -> np.ndarray:
+    """ACC16_EPS * sum_c |a[m,c]| |w[n,c]| for operands given as magnitudes."""
+    return ACC16_EPS * (a_abs @ w_abs.T)
+
+
+def fp8_block_bound(ad: np.ndarray, wd: np.ndarray, block: int = 128) -> np.ndarray:
+    """Bound [m, n] on |FP8 GEMM - exact| for decoded (scaled) operands ad [m, k]
+    and wd [n, k]: per k block FP8_BLOCK_EPS * max|ad| * max|wd|, plus
+    ACC16_EPS * sum |ad| |wd| for the fp32 additions across blocks."""
+    m, k = ad.shape
+    am = np.abs(ad).reshape(m, k // block, block).max(axis=2)
+    wm = np.abs(wd).reshape(wd.shape[0], k // block, block).max(axis=2)
+    return FP8_BLOCK_EPS * (am @ wm.T) + acc_bound(np.abs(ad), np.abs(wd))
+
+
+def ulp_act(x: np.ndarray, act: str) -> np.ndarray:
+    """Spacing of the activation dtype's values at |x| (the distance from |x|
+    rounded down to the dtype to the next larger value)."""
+    ax = np.abs(np.asarray(x, dtype=np.float64))
+    _, e = np.frexp(ax)                 # ax = f 2^e, f in [0.5, 1); 0 -> e = 0
+    if act == "bf16":                   # 8 significant bits, subnormal spacing 2^-133
+        return np.where(ax == 0, 2.0 ** -133, np.ldexp(1.0, np.maximum(e - 8, -133)))
+    if act == "fp16":                   # 11 significant bits, subnormal spacing 2^-24
+        return np.where(ax == 0, 2.0 ** -24, np.ldexp(1.0, np.maximum(e - 11, -24)))
+    raise ValueError(act)
+
+
+def h_tolerance(h64: np.ndarray, act: str) -> np.ndarray:
+    """Per-element tolerance of the GPU's stored h against the exact h64 [m, F]."""
+    rowmax = np.abs(h64).max(axis=1, keepdims=True) if h64.shape[1] else np.zeros((h64.shape[0], 1))
+    return ulp_act(h64, act) + H_ABS_REL * rowmax
+
+
+def f32_bits_equal(a: np.ndarray, b: np.ndarray) -> bool:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    return a.shape == b.shape and np.array_equal(a.view(np.uint32), b.view(np.uint32))
