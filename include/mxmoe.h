@@ -249,6 +249,28 @@ MXMOE_API mxmoe_status mxmoe_moe_forward(const mxmoe_block* B, const void* block
                                void* y, void* workspace, size_t workspace_bytes,
                                hipStream_t stream);
 
+/* Largest workspace mxmoe_moe_forward_noalloc can use (bytes).             */
+#define MXMOE_NOALLOC_SCRATCH_BYTES (128u << 20)
+
+/* mxmoe_moe_forward for callers that cannot allocate device memory or pass a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments and result as mxmoe_moe_forward,
+ * minus the workspace: the library's own device array of
+ * MXMOE_NOALLOC_SCRATCH_BYTES bytes serves as the workspace.  Each GPU holds
+ * its own copy from the first call on it (made with that device current)
+ * until the process ends; nothing is allocated, freed or synchronized.
+ * Blocks whose workspace (mxmoe_workspace_bytes(B, T)) exceeds the array
+ * return MXMOE_ERR_WORKSPACE and enqueue nothing (about 200 tokens of a
+ * Mixtral- or Qwen1.5-MoE-shaped block, 32 of a Qwen2-57B-shaped one).
+ * All calls on one GPU share the array: calls that may overlap on a GPU (on
+ * different streams, or from several threads) race and give undefined
+ * results; serialize them.  Intermediates of the last call stay readable
+ * at the offsets of mxmoe_workspace_layout until the next call.
+ * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.                          */
+MXMOE_API mxmoe_status mxmoe_moe_forward_noalloc(const mxmoe_block* B, const void* block_table, int32_t T,
+                                       const void* x, const int32_t* topk_ids, const float* topk_w,
+                                       void* y, hipStream_t stream);
+
 /* Options of mxmoe_moe_forward_ex (measurement and testing).                 */
 typedef struct {
   /* host [(n_experts + n_shared)] or NULL: experts with mask 0 get no tiles

@@ -3,10 +3,18 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "mxmoe_internal.h"
 
 using namespace mxmoe;
+
+// Workspace of mxmoe_moe_forward_noalloc: one file-scope device array, of
+// which every GPU the library runs on holds its own copy until the process
+// ends.  Host code never uses the array's name as an address: the copy of a
+// device is found once with hipGetSymbolAddress (with that device current)
+// and its address kept per device.
+static __device__ __align__(256) uint8_t scratch[MXMOE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -674,6 +682,47 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
 #undef MX_EVENT
 #undef MX_CHECK
   return MXMOE_OK;
+}
+
+}  // extern "C"
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's copy of `scratch` (looked up on the first
+// call on that device, then cached).
+mxmoe_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return MXMOE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MXMOE_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MXMOE_OK;
+}
+}  // namespace
+
+extern "C" {
+
+mxmoe_status mxmoe_moe_forward_noalloc(const mxmoe_block* B, const void* block_table, int32_t T, const void* x,
+                                       const int32_t* topk_ids, const float* topk_w, void* y, hipStream_t stream) {
+  static thread_local BlockInfo bi;
+  mxmoe_status st = check_block(B, &bi);
+  if (st != MXMOE_OK) return st;
+  if (T < 0) return MXMOE_ERR_INVALID_ARG;
+  if ((int64_t)T * bi.k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
+  if (layout_of(bi, T).total > (size_t)MXMOE_NOALLOC_SCRATCH_BYTES) return MXMOE_ERR_WORKSPACE;
+  if (T == 0) return MXMOE_OK;
+  void* ws = nullptr;
+  st = scratch_of_current_device(&ws);
+  if (st != MXMOE_OK) return st;
+  return mxmoe_moe_forward_ex(B, block_table, T, x, topk_ids, topk_w, y, ws, (size_t)MXMOE_NOALLOC_SCRATCH_BYTES,
+                              nullptr, stream);
 }
 
 mxmoe_status mxmoe_moe_forward(const mxmoe_block* B, const void* block_table, int32_t T, const void* x,

@@ -63,7 +63,9 @@ EXPORTS = [
     "mxmoe_route_permute", "mxmoe_router_topk", "mxmoe_act_quant", "mxmoe_linear_workspace_bytes", "mxmoe_linear_forward",
     "mxmoe_block_table_bytes", "mxmoe_block_table_fill", "mxmoe_workspace_bytes", "mxmoe_moe_forward",
     "mxmoe_moe_forward_ex", "mxmoe_workspace_layout", "mxmoe_status_string", "mxmoe_version",
+    "mxmoe_moe_forward_noalloc",
 ]
+NOALLOC_SCRATCH_BYTES = 128 << 20   # MXMOE_NOALLOC_SCRATCH_BYTES
 
 _lib = None
 
@@ -95,6 +97,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "mxmoe_moe_forward_ex": (C.c_int, [PB, vp, i32, vp, vp, vp, vp, vp, sz,
                                            C.POINTER(ForwardOpts_t), vp]),
         "mxmoe_workspace_layout": (C.c_int, [PB, i32, C.POINTER(WsLayout_t)]),
+        "mxmoe_moe_forward_noalloc": (C.c_int, [PB, vp, i32, vp, vp, vp, vp, vp]),
         "mxmoe_status_string": (C.c_char_p, [C.c_int]),
         "mxmoe_version": (i32, []),
     }
@@ -406,6 +409,18 @@ class MoEBlock:
         st = lib.mxmoe_moe_forward_ex(C.byref(self.B), _ptr(self.table), T, _ptr(x), _ptr(topk_ids), _ptr(topk_w),
                                       _ptr(y), _ptr(self.ws), self.ws_bytes, opts, _stream_ptr(stream))
         _check(st, "mxmoe_moe_forward")
+        return y
+
+    def forward_noalloc(self, x, topk_ids, topk_w, y=None, stream=None):
+        """The forward through mxmoe_moe_forward_noalloc (the library's own
+        scratch array instead of this block's workspace)."""
+        torch = _torch()
+        lib = load_library()
+        if y is None:
+            y = torch.empty_like(x)
+        st = lib.mxmoe_moe_forward_noalloc(C.byref(self.B), _ptr(self.table), x.shape[0], _ptr(x), _ptr(topk_ids),
+                                           _ptr(topk_w), _ptr(y), _stream_ptr(stream))
+        _check(st, "mxmoe_moe_forward_noalloc")
         return y
 
     def ws_view(self, field: str, dtype, count: int, T: int):
