@@ -72,7 +72,7 @@ typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
  *                    one scale per 128 consecutive k of a channel / a token
  *   {4,4,32,32,1} with fmt = 1: mxfp4, the OCP Microscaling FP4 format the
  *                    MI355X matrix cores take natively (the paper's scheme set
- *                    is whatever the hardware supports, Sec. 3.1): FP4 e2m1
+ *                    is whatever the hardware supports, Sec. 4.2.1): FP4 e2m1
  *                    elements on both operands with one E8M0 power-of-two
  *                    scale per 32 consecutive k; activations are encoded at
  *                    run time (e = floor(log2 amax) - 2, elements rounded to
@@ -124,6 +124,11 @@ MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
  *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4/fp8 fp32 [n];
  *            mxfp4 uint8 E8M0 [n, k/32]; NULL for w16.
  *   zeros  : wNg128 fp16 [n, k/128] holding integers in [0, 2^N-1]; else NULL.
+ * Codes and zero points outside these ranges (a zero point that is not an
+ * integer in [0, 2^N-1], a wNg128 code above 2^N-1, a w4a4 / w4a4-g128 code
+ * outside [-7, 7]) are not representable in the packed form: the group's
+ * scale (per-channel w4a4: the channel's scale) is stored as NaN instead, so
+ * every output that uses it is NaN.
  *   w16_src: dtype of 16-bit source weights; converted (RNE) to `act`.
  *   packed : output, mxmoe_packed_bytes(L, act) bytes, 256-byte aligned.
  * All inputs 4-byte aligned.  Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE
@@ -204,7 +209,8 @@ MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
  *        fp8 -> fp32 [m, n]: a encoded as e4m3 per token at run time, the
  *        e4m3 products accumulated in fp32 by the FP8 MFMA, times
  *        s_a[m]*s_w[n];
- *        other schemes -> fp32 [m, n] with fp32 accumulation.               */
+ *        other schemes -> fp32 [m, n] with fp32 accumulation.
+ * Limits: m*k*2 bytes below 4 GiB (UNSUPPORTED beyond).                      */
 MXMOE_API mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const void* packed,
                                   int32_t m, const void* a, void* out, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
@@ -243,6 +249,9 @@ MXMOE_API size_t mxmoe_workspace_bytes(const mxmoe_block* B, int32_t T);
  *   topk_w  : fp32 [T, k] gate weights   y       : [T, hidden] act (output)
  * Out-of-range expert ids contribute nothing; the workspace status word
  * (see mxmoe_workspace_layout) records 1 + the first such pair id.
+ * Limits (UNSUPPORTED beyond them): T*k < 2^31, and x (T*hidden*2 bytes), the
+ * routed h rows (T*k*ffn*2) and the shared h rows (n_shared*T*ffn_shared*2)
+ * each below 4 GiB.
  * Errors: INVALID_ARG, UNSUPPORTED, WORKSPACE, HIP.                          */
 MXMOE_API mxmoe_status mxmoe_moe_forward(const mxmoe_block* B, const void* block_table, int32_t T,
                                const void* x, const int32_t* topk_ids, const float* topk_w,
@@ -276,9 +285,11 @@ typedef struct {
   /* host [(n_experts + n_shared)] or NULL: experts with mask 0 get no tiles
    * (their rows keep whatever the workspace held); used to time subsets.   */
   const uint8_t* expert_mask;
-  /* 1: run gate/up, h-quantization and down as separate launches instead of
-   * one persistent launch.                                                  */
-  int32_t split_phases;
+  /* Must be 0.  (The forward always runs its phases as separate launches:
+   * routing + plan + x encodings, the gate/up Group-GEMM, h quantization,
+   * the down Group-GEMM and the combine; each Group-GEMM launch is one
+   * persistent grid over all experts and schemes of its phase.)             */
+  int32_t reserved0;
   /* 1: skip the combine (y untouched) - to time the Group-GEMM alone.       */
   int32_t skip_combine;
   /* host array of 2*MXMOE_N_PHASES caller-created events, or NULL: event 2i

@@ -125,6 +125,14 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
   return MXMOE_OK;
 }
 
+// The Group-GEMM addresses activation rows with 32-bit byte offsets from the
+// start of their buffer: x, the routed h rows and the shared h rows (and their
+// one-byte and half-byte encodings, which are smaller) stay below 4 GiB.
+bool activations_fit(const BlockInfo& bi, int64_t T) {
+  const int64_t lim = (int64_t)1 << 32;
+  return T * bi.H * 2 < lim && T * bi.k * bi.F * 2 < lim && (int64_t)bi.nsh * T * bi.Fsh * 2 < lim;
+}
+
 WsLayout layout_of(const BlockInfo& bi, int T) {
   WsLayout L;
   size_t o = 0;
@@ -335,6 +343,7 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
   mxmoe_status st = check_linear(L, &kd);
   if (st != MXMOE_OK) return st;
   if (!valid_dtype(act) || m < 0) return MXMOE_ERR_INVALID_ARG;
+  if ((int64_t)m * L->k * 2 >= ((int64_t)1 << 32)) return MXMOE_ERR_UNSUPPORTED;  // 32-bit row offsets
   if (m == 0) return MXMOE_OK;
   if (!packed || !a || !out || !workspace) return MXMOE_ERR_INVALID_ARG;
   if (!aligned(packed, 256) || !aligned(a, 16) || !aligned(out, 16) || !aligned(workspace, 256))
@@ -492,7 +501,9 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if (st != MXMOE_OK) return st;
   if (T < 0) return MXMOE_ERR_INVALID_ARG;
   if ((int64_t)T * bi.k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
+  if (!activations_fit(bi, T)) return MXMOE_ERR_UNSUPPORTED;
   const bool router = opts && opts->router_logits;
+  if (opts && (opts->reserved0 != 0 || opts->reserved[0] != 0 || opts->reserved[1] != 0)) return MXMOE_ERR_INVALID_ARG;
   if (router) {
     if (opts->renormalize != 0 && opts->renormalize != 1) return MXMOE_ERR_INVALID_ARG;
     if (opts->shared_w || !aligned(opts->router_logits, 4) || !aligned(opts->shared_logits, 4))

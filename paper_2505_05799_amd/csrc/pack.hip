@@ -109,6 +109,17 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
     mxs = (uint32_t)e[0] | ((uint32_t)e[1] << 8) | ((uint32_t)e[2] << 16) | ((uint32_t)e[3] << 24);
   }
   const uint32_t zcode = zero_group ? (uint32_t)(float)__builtin_bit_cast(_Float16, z16) : 0u;
+  // Inputs outside the documented domain - a zero point that is not an
+  // integer in [0, 2^N - 1], a weight-only code above 2^N - 1, a w4a4 code
+  // outside [-7, 7] - cannot be represented exactly by the packed form; they
+  // make the group's scale NaN, so every output that uses the group is NaN
+  // rather than silently wrong (per-channel w4a4: poison_channels_kernel).
+  const float qtop = (float)((1 << kind_wbits(kd)) - 1);
+  bool bad = false;
+  if (kind_is_wonly(kd)) {
+    const float zf = (float)__builtin_bit_cast(_Float16, z16);
+    bad = !(zf >= 0.f && zf <= qtop && zf == __builtin_rintf(zf));
+  }
   uint32_t w[16];
   for (int i = 0; i < 16; ++i) w[i] = 0;
   for (int v = 0; v < 32; ++v) {
@@ -116,6 +127,11 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
     uint32_t c;
     if (kd == K_W16) c = cvt16(reinterpret_cast<const uint16_t*>(codes)[idx], w16_src, act);
     else c = zero_group ? zcode : (uint32_t)codes[idx];
+    if (kind_is_wonly(kd) && !zero_group && (float)c > qtop) bad = true;
+    if (kd == K_W4A4G) {
+      const int sc = (int)(int8_t)codes[idx];
+      bad |= sc < -7 || sc > 7;
+    }
     int dw, bit;
     uint32_t mask;
     slot_field(kd, v, &dw, &bit, &mask);
@@ -124,6 +140,12 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
   }
   uint32_t* o32 = reinterpret_cast<uint32_t*>(out);
   for (int i = 0; i < lane_bytes(kd) / 4; ++i) o32[i] = w[i];
+  // the four lanes of a channel (lane % 16 + 16 qd, qd = 0..3) share its
+  // group: an OR over lane ^ 16, then over lane ^ 32, by every lane
+  int b = bad ? 1 : 0;
+  b |= __shfl_xor(b, 16, 64);
+  b |= __shfl_xor(b, 32, 64);
+  if (b) s16 = 0x7E00u;  // fp16 NaN
   if (kind_has_gmeta(kd) && qd == 0) {
     const uint32_t sz = kd == K_MXFP4 ? mxs : ((uint32_t)s16 | ((uint32_t)z16 << 16));
     reinterpret_cast<uint32_t*>(packed + blk * block_bytes(kd) + 64 * lane_bytes(kd))[lane & 15] = sz;
@@ -132,6 +154,24 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
     float* ws = reinterpret_cast<float*>(packed + codes_bytes(kd, n, k));
     ws[row] = reinterpret_cast<const float*>(scales)[row];
   }
+}
+
+// Per-channel w4a4: a channel with a code outside [-7, 7] gets a NaN scale
+// (after pack_kernel wrote the scales, same stream), one workgroup per channel.
+__global__ void __launch_bounds__(256) poison_channels_kernel(int n, int k, const int8_t* __restrict__ codes,
+                                                              float* __restrict__ wscale) {
+  __shared__ int any;
+  if (threadIdx.x == 0) any = 0;
+  __syncthreads();
+  const int64_t row = blockIdx.x;
+  int bad = 0;
+  for (int c = threadIdx.x; c < k; c += blockDim.x) {
+    const int v = codes[row * k + c];
+    bad |= v < -7 || v > 7;
+  }
+  if (bad) atomicOr(&any, 1);
+  __syncthreads();
+  if (threadIdx.x == 0 && any) wscale[row] = __builtin_nanf("");
 }
 
 __global__ void unpack_kernel(int kd, int n, int k, int act, const uint8_t* __restrict__ packed,
@@ -183,6 +223,12 @@ hipError_t launch_pack(int kind, int n, int k, int act, int w16_src, const void*
   int64_t blocks = (threads + 255) / 256;
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, kind, n, k, act, w16_src,
                      (const uint8_t*)codes, (const uint8_t*)scales, (const uint8_t*)zeros, packed);
+  if (kind == K_W4A4) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(poison_channels_kernel, dim3((unsigned)n), dim3(256), 0, s, n, k, (const int8_t*)codes,
+                       reinterpret_cast<float*>(packed + codes_bytes(kind, n, k)));
+  }
   return hipGetLastError();
 }
 

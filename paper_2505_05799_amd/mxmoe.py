@@ -41,7 +41,7 @@ PHASE_NAMES = ("route_plan_xquant", "gemm_gate_up", "hquant", "gemm_down", "comb
 
 
 class ForwardOpts_t(C.Structure):
-    _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("split_phases", C.c_int32),
+    _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("reserved0", C.c_int32),
                 ("skip_combine", C.c_int32), ("events", C.POINTER(C.c_void_p)),
                 ("router_logits", C.c_void_p), ("renormalize", C.c_int32), ("shared_logits", C.c_void_p),
                 ("shared_w", C.c_void_p), ("reserved", C.c_int32 * 2)]

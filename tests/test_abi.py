@@ -222,3 +222,44 @@ def test_pack_operand_extent_is_checked(s):
         g = W.quantize_linear(W.draw_weight(2, 0, 0, 32, 256), W.W4A4G128)
         with pytest.raises(ValueError):
             M.check_operands(W.QLinear(s, q.n, q.k, q.codes, g.scales))
+
+
+def test_activation_buffers_beyond_4gib_are_rejected(lib):
+    """The Group-GEMM addresses activation rows with 32-bit byte offsets: a
+    forward whose x, routed h or shared h would reach 4 GiB, and a single
+    linear whose input would, return UNSUPPORTED before anything is enqueued
+    (the pointers are never dereferenced)."""
+    p = C.c_void_p(1 << 20)
+    B, keep = _block("mixtral")
+    T_ok, T_big = 65536, 81920                  # routed h: T * 2 * 14336 * 2 bytes
+    assert 2 * T_ok * 2 * 14336 < 1 << 32 <= 2 * T_big * 2 * 14336
+    assert lib.mxmoe_moe_forward(C.byref(B), p, T_big, p, p, p, p, p, 1 << 62, None) == M.ERR_UNSUPPORTED
+    assert lib.mxmoe_moe_forward(C.byref(B), p, T_ok, p, p, p, p, p, 16, None) == M.ERR_WORKSPACE
+    B2, keep2 = _block("qwen2")                 # shared h: T * 20480 * 2 bytes
+    assert lib.mxmoe_moe_forward(C.byref(B2), p, 1 << 17, p, p, p, p, p, 1 << 62, None) == M.ERR_UNSUPPORTED
+    L = _L(W.W8A8, 256, 16384)                  # linear input m * k * 2 bytes
+    assert lib.mxmoe_linear_forward(C.byref(L), M.BF16, p, 1 << 17, p, p, p, 1 << 62, None) == M.ERR_UNSUPPORTED
+
+
+def test_forward_reserved_options_must_be_zero(lib):
+    B, keep = _block("tiny")
+    p = C.c_void_p(1 << 20)
+    for field in ("reserved0", "reserved"):
+        o = M.ForwardOpts_t()
+        if field == "reserved0":
+            o.reserved0 = 1
+        else:
+            o.reserved[1] = 1
+        assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, p, p, p, p, 10 ** 9, C.byref(o), None) == \
+            M.ERR_INVALID_ARG
+
+
+def test_noalloc_validation(lib):
+    """mxmoe_moe_forward_noalloc validates on the host: a block whose
+    workspace exceeds the scratch array gets WORKSPACE, T = 0 is a no-op."""
+    B, keep = _block("qwen2")
+    p = C.c_void_p(1 << 20)
+    assert lib.mxmoe_workspace_bytes(C.byref(B), 4096) > M.NOALLOC_SCRATCH_BYTES
+    assert lib.mxmoe_moe_forward_noalloc(C.byref(B), p, 4096, p, p, p, p, None) == M.ERR_WORKSPACE
+    assert lib.mxmoe_moe_forward_noalloc(C.byref(B), p, 0, p, p, p, p, None) == M.OK
+    assert lib.mxmoe_moe_forward_noalloc(C.byref(B), p, -1, p, p, p, p, None) == M.ERR_INVALID_ARG

@@ -231,3 +231,54 @@ def test_linear_deterministic():
     o1 = M.linear_forward(pl, a).cpu().numpy()
     o2 = M.linear_forward(pl, a).cpu().numpy()
     assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
+
+
+@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W4A4G128, W.W4A4])
+def test_pack_domain_of_codes_and_zeros(scheme):
+    """Boundary zero points (0 and 2^N - 1, with the extreme codes) pack
+    exactly and the linear matches the oracle in those channels; a zero
+    point that is not an integer in [0, 2^N - 1], a weight-only code above
+    2^N - 1 or a w4a4 code outside [-7, 7] stores that group's scale (the
+    channel's for per-channel w4a4) as NaN, so its outputs are NaN instead of
+    silently wrong, while the other channels stay exact."""
+    torch = torch_mod()
+    n, k, m = 48, 512, 5
+    q = W.quantize_linear(W.draw_weight(77, 0, 0, n, k), scheme)
+    codes, scales = q.codes.copy(), q.scales.copy()
+    zeros = None if q.zeros is None else q.zeros.copy()
+    poisoned = []
+    if scheme.a_bits == 16:                        # weight-only: boundary zeros, then bad zeros / codes
+        top = (1 << scheme.w_bits) - 1
+        zeros[0, 0], codes[0, :128] = 0, np.arange(128) % (top + 1)
+        zeros[1, 0], codes[1, :128] = top, np.arange(128) % (top + 1)
+        zeros[2, 1] = 1.5                          # not an integer
+        zeros[3, 2] = top + 1                      # above 2^N - 1
+        poisoned += [(2, 1), (3, 2)]
+        if scheme.w_bits < 8:
+            codes[4, 300] = top + 1                # a code beyond N bits
+            poisoned.append((4, 2))
+    else:
+        codes[2, 7] = 8
+        codes[3, 130] = -8
+        poisoned += [(2, 0), (3, 1)]
+    bad = W.QLinear(scheme, n, k, codes, scales, zeros)
+    pl = M.PackedLinear(bad, "bf16")
+    _, sc, _ = pl.unpack()
+    scf = sc.astype(np.float32)
+    for ch, grp in poisoned:
+        assert np.isnan(scf[ch] if scf.ndim == 1 else scf[ch, grp]), (ch, grp)
+    rows = [c for c, _ in poisoned]
+    good = [c for c in range(n) if c not in rows]
+    assert not np.isnan(scf[good]).any()
+    x = W.f64_to_act(np.random.default_rng(5).standard_normal((m, k)), "bf16")
+    out = M.linear_forward(pl, M.act_tensor(x, "bf16")).cpu().numpy()
+    torch.cuda.synchronize()
+    a = O.act_values(x, "bf16")
+    if scheme.a_bits < 16 and scheme.a_group < 0:      # per-channel w4a4: exact int32 in every channel
+        want = O.linear(a, W.QLinear(scheme, n, k, np.clip(codes, -7, 7), scales), "bf16", return_int=True)
+        assert np.array_equal(out[:, good].astype(np.int64), want[:, good])
+    else:
+        assert np.isnan(out[:, rows]).all()
+        okq = W.QLinear(scheme, len(good), k, codes[good], scales[good], None if zeros is None else zeros[good])
+        _check_linear(okq, a, out[:, good], "bf16")
+    say(f"pack domain {scheme.name}: boundary zeros exact, {len(poisoned)} out-of-domain groups poisoned")
