@@ -234,7 +234,7 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
 
 namespace {
 // Register-resident shapes by row length: (chunks per lane, wavefronts per row).
-enum RowShape { RS_1x2, RS_1x4, RS_1x8, RS_4x4, RS_4x8, RS_STREAM };
+enum RowShape { RS_1x2, RS_1x4, RS_1x8, RS_4x4, RS_4x8, RS_4x16, RS_STREAM };
 RowShape row_shape(int cols) {
   const int nch = cols / 8, per = (nch + 63) / 64, per4 = (nch + 255) / 256;
   if (per <= 2) return RS_1x2;
@@ -242,6 +242,7 @@ RowShape row_shape(int cols) {
   if (per <= 8) return RS_1x8;
   if (per4 <= 4) return RS_4x4;
   if (per4 <= 8) return RS_4x8;
+  if (per4 <= 16) return RS_4x16;  // rows up to 32768 elements stay in registers (read once)
   return RS_STREAM;
 }
 template <template <int, int> class K, typename... Args>
@@ -254,6 +255,7 @@ hipError_t launch_rows(int rows, int cols, hipStream_t s, Args... args) {
     case RS_1x8: hipLaunchKernelGGL((K<8, 1>::fn), g1, b, 0, s, args...); break;
     case RS_4x4: hipLaunchKernelGGL((K<4, 4>::fn), g4, b, 0, s, args...); break;
     case RS_4x8: hipLaunchKernelGGL((K<8, 4>::fn), g4, b, 0, s, args...); break;
+    case RS_4x16: hipLaunchKernelGGL((K<16, 4>::fn), g4, b, 0, s, args...); break;
     default: hipLaunchKernelGGL((K<0, 1>::fn), g1, b, 0, s, args...); break;
   }
   return hipGetLastError();

@@ -144,19 +144,15 @@ template <int ACT> __device__ inline uint16_t f32_to_act(float f) {
     return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
-// SiLU(g) = g / (1 + e^-g) with e^-g = 2^t, t = -g log2(e) carried as a rounded
-// product plus its FMA-recovered error (and that of log2(e) itself), so the
-// result is within a few ulp of the exact value; t is capped so that large
-// negative g yields a tiny finite value instead of inf * 0.
+// SiLU(g) = g / (1 + e^-g) with e^-g = 2^t, t = -g log2(e) rounded to fp32 and
+// capped at 126 (a large negative g then yields a tiny finite value instead of
+// inf * 0).  The rounding of t moves e^-g by at most |t| 2^-24 relatively,
+// which with the exp2 and reciprocal instructions (about one ulp each) keeps
+// the result within 2^-16 of the exact value for |g| < 64: far below the one
+// rounding of h to the 16-bit activation dtype that follows.
 __device__ inline float silu_f32(float g) {
-  const float kL = 1.44269502162933349609375f;      // log2(e) rounded to fp32
-  const float kLlo = 1.925963033500011079e-8f;       // log2(e) - kL
-  float t = -g * kL;
-  const float tl = __builtin_fmaf(-g, kLlo, __builtin_fmaf(-g, kL, -t));
-  t = fminf(t, 126.0f);
-  const float e = __builtin_amdgcn_exp2f(t);
-  const float ex = __builtin_fmaf(e, tl * 0.693147180559945309f, e);
-  return g * __builtin_amdgcn_rcpf(1.0f + ex);
+  const float e = __builtin_amdgcn_exp2f(fminf(g * -1.44269502162933349609375f, 126.0f));
+  return g * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 // ------------------------------------------------------- weight operands
@@ -624,14 +620,16 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // are in flight together, which doubles the prefetch distance and halves
   // the barriers per block.  Tiles of at most 32 rows with at most 16 weight
   // bytes per lane and block gain most (their MFMA work per block is too
-  // small to hide one memory round trip); down tiles gain a little at any
-  // size whose two-block stage fits one stage buffer, gate/up tiles of more
-  // rows lose a little (their two weight sets already fill the registers).
+  // small to hide one memory round trip); down tiles and integer / FP8
+  // gate|up tiles gain a little at any size whose two-block stage fits one
+  // stage buffer (1.5% on the gate|up launch of the Qwen2-shaped block);
+  // 16-bit-activation gate/up tiles of more rows lose a little (their two
+  // weight sets already fill the registers).
   // Slot s of the weight registers serves k block kb + s and is refilled
   // right after its MFMAs (no register copy).  The per-row values of the
   // second block sit at rsum[buf][64..], so tiles with them stop at 64 rows.
   constexpr bool KBI_FITS = !streamed<KD>() && BM * RB * 2 <= STAGE_BYTES && (!RSLOAD || BM <= 64);
-  constexpr int KBI = (KBI_FITS && (PHASE == 1 || (BM <= 32 && LB <= 16))) ? 2 : 1;
+  constexpr int KBI = (KBI_FITS && (PHASE == 1 || (BM <= 32 && LB <= 16) || INT)) ? 2 : 1;
   static_assert(KBI == 1 || KBI_FITS, "two-block stage layout");
   Raw<KD> raw[KBI][NL][NF];   // low-bit kinds: next group(s), prefetched a step ahead
   u32x4 st[J][NL][NF];   // streamed kinds: step j of the k block, reloaded one block ahead
@@ -1071,12 +1069,49 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           rsh_out[(int64_t)ro * nkb + kbg] = t;
         }
       }
+    } else if constexpr (PHASE == 1) {
+      // The tile's fp32 slot rows (value x router gate weight) go through LDS
+      // (the idle stage buffers), RP rows at a time, and leave as 16-byte
+      // pieces of whole rows: a store instruction writes 64 x 16 contiguous
+      // bytes instead of 16-lane 64-byte segments of four rows.
+      constexpr int FP = BN + 4;                  // row pitch in floats (16-byte pad against bank conflicts)
+      constexpr int RP = (BM >= 32 && 32 * FP * 4 <= 2 * STAGE_BYTES) ? 32 : 16;  // rows per pass
+      static_assert(RP * FP * 4 <= 2 * STAGE_BYTES, "slot rows fit the stage buffers");
+      float* fl = reinterpret_cast<float*>(&sm.act[0][0]);
+      constexpr int CH = BN / 4;                  // 16-byte pieces of a tile row
+      int nch = (N - nt * BN) / 4;
+      nch = nch > CH ? CH : nch;
+#pragma unroll
+      for (int pass = 0; pass < BM / RP; ++pass) {
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          if ((mf * 16) / RP != pass) continue;
+          const int r = mf * 16 + 4 * q;
+          const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
+          const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            if (nf >= nvalid) continue;
+            const int c = (wave * NF + nf) * 16 + li;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) fl[(r + i - pass * RP) * FP + c] = outv(0, nf, mf, i, rs) * gwv[i];
+          }
+        }
+        lds_barrier();
+        for (int idx = tid; idx < RP * CH; idx += kThreads) {
+          const int r = idx / CH, c = idx % CH;
+          const int ro = sm.rowout[pass * RP + r];
+          if (ro >= 0 && c < nch)
+            *reinterpret_cast<u32x4*>(a.slots + (int64_t)ro * N + nt * BN + 4 * c) =
+                *reinterpret_cast<const u32x4*>(fl + r * FP + 4 * c);
+        }
+        lds_barrier();
+      }
     } else {
 #pragma unroll
     for (int mf = 0; mf < MF; ++mf) {
       const int r = mf * 16 + 4 * q;
       const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
-      const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
       const i32x4 ro = *reinterpret_cast<const i32x4*>(&sm.rowout[r]);
 #pragma unroll
       for (int nf = 0; nf < NF; ++nf) {
@@ -1086,9 +1121,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int i = 0; i < 4; ++i) {
           const int64_t orow = (int64_t)ro[i] * N + n;
           if (GUARD && ro[i] < 0) continue;
-          if constexpr (PHASE == 1) {
-            a.slots[orow] = outv(0, nf, mf, i, rs) * gwv[i];
-          } else if constexpr (INT && !GSC && !F8) {
+          if constexpr (INT && !GSC && !F8) {
             int iv = acc[0][nf][mf][i];
             if constexpr (KD == K_W4A4) iv >>= 4;
             reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
