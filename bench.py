@@ -38,7 +38,7 @@ import numpy as np
 
 HBM_PEAK = 8.0e12            # B/s
 # dense MFMA peaks of MI355X by operand type (int8 in OP/s)
-MFMA_PEAK = {"i8": 5.0e15, "fp8": 5.0e15, "fp4": 10.1e15, "bf16": 2.5e15, "fp16": 2.5e15}
+MFMA_PEAK = {"i8": 5.0e15, "fp8": 5.0e15, "fp6": 10.1e15, "fp4": 10.1e15, "bf16": 2.5e15, "fp16": 2.5e15}
 ROTATE_BYTES = 512 << 20     # Infinity Cache (256 MiB) defeat: rotate copies covering twice its size
 
 
@@ -61,6 +61,8 @@ def mfma_dtype(s, act):
         return "fp4"
     if fmt == 2:
         return "fp8"
+    if fmt == 3:
+        return "fp6"
     return "i8" if s.a_bits < 16 else act
 
 

@@ -77,6 +77,11 @@ typedef enum { MXMOE_F16 = 0, MXMOE_BF16 = 1 } mxmoe_dtype;
  *                    scale per 32 consecutive k; activations are encoded at
  *                    run time (e = floor(log2 amax) - 2, elements rounded to
  *                    nearest, ties to even, clamped to 6)
+ *   {4,4,-1,-1,1} with fmt = 3: w4a4 (per channel / per token, the same
+ *                    quantization and results as fmt = 0) whose int4 codes are
+ *                    held as FP6 e2m3 values, so that the MI355X FP6 matrix
+ *                    cores (twice the int8 rate) compute the exact integer
+ *                    sums; weights take 6 bits per code (24 bytes per 32)
  *   {8,8,-1,-1,1} with fmt = 2: fp8, OCP FP8 e4m3 elements (sign bit 7,
  *                    exponent bias 7, no infinities, 448 the largest finite
  *                    value) on both operands; fp32 scale per output channel
@@ -92,7 +97,8 @@ typedef struct {
   int32_t a_group;    /* 128 or 32 (mxfp4), or -1 = per token                   */
   int32_t symmetric;  /* 1 for w8a8 / w4a4 (per channel or g128) and mxfp4      */
   int32_t fmt;        /* 0: integer codes; 1: OCP MX floating point (mxfp4);
-                         2: FP8 e4m3 with per-channel / per-token scales       */
+                         2: FP8 e4m3 with per-channel / per-token scales;
+                         3: w4a4 codes held as FP6 e2m3 operands             */
 } mxmoe_scheme;
 
 /* One linear block y = x W^T with W of shape [n, k] = [out, in].
@@ -108,6 +114,7 @@ typedef struct {
 /* Bytes of the packed form of linear *L (host) for activations `act`:
  *   wNg128: n*k*N/8 + (n*k/128)*4   (N + 0.25 bits per weight, Sec. 5.2)
  *   w8a8/w4a4/fp8: n*k*b/8 + 4*n
+ *   w4a4 on FP6 operands: n*k*6/8 + 4*n
  *   w4a4-g128: n*k/2 + (n*k/128)*4   (fp16 group scale, 4-byte slot per group)
  *   mxfp4: n*k/2 + n*k/32            (4.25 bits per weight)
  *   w16: 2*n*k
@@ -118,7 +125,7 @@ MXMOE_API size_t mxmoe_packed_bytes(const mxmoe_linear* L, mxmoe_dtype act);
  * Group-GEMM streams (weight fragments in MFMA lane order, group metadata next
  * to its codes).  Runs once per weight load.
  *   codes  : wNg128 uint8 [n,k] in [0, 2^N-1]; w8a8/w4a4/w4a4-g128 int8
- *            [n,k] in [-qmax, qmax]; mxfp4 uint8 [n,k] e2m1 codes 0..15
+ *            [n,k] in [-qmax, qmax] (w4a4 on FP6 operands too); mxfp4 uint8 [n,k] e2m1 codes 0..15
  *            (sign in bit 3); fp8 uint8 [n,k] e4m3 bytes (no NaN code);
  *            w16: 16-bit weights [n,k] of `w16_src`.
  *   scales : wNg128 and w4a4-g128 fp16 [n, k/128]; w8a8/w4a4/fp8 fp32 [n];
@@ -200,8 +207,8 @@ MXMOE_API size_t mxmoe_linear_workspace_bytes(const mxmoe_linear* L, int32_t m);
 /* out = a W^T for one packed linear, through the same micro-kernels the block
  * uses (testing and single-GEMM measurement).
  *   a  : [m, k] `act` activations (dense)
- *   out: w8a8 / w4a4 -> int32 [m, n] exact integer accumulators
- *        sum_c qa[m,c]*qw[n,c] (qa from the per-token quantizer);
+ *   out: w8a8 / w4a4 (int8 or FP6 operands) -> int32 [m, n] exact integer
+ *        accumulators sum_c qa[m,c]*qw[n,c] (qa from the per-token quantizer);
  *        w4a4-g128 -> fp32 [m, n]: per 128-wide block the exact integer sum
  *        times s_a[m,b]*s_w[n,b], added over the blocks in fp32;
  *        mxfp4 -> fp32 [m, n]: a encoded as mxfp4 at run time, products of
@@ -366,6 +373,11 @@ typedef struct {
   size_t xqf8, xsf8;    /* uint8 [T, H] e4m3 codes, fp32 [T] scales: x for fp8
                            gate|up (else -1); h rows of an fp8 down projection
                            use hq / hs and hq_shared / hs_shared             */
+  size_t xqf6, xsf6;    /* uint8 [T, H] FP6-encoded int4 codes (per 32 elements
+                           24 bytes of e2m3 codes, 8 zero bytes), fp32 [T]
+                           scales: x for w4a4 gate|up on FP6 operands (else
+                           -1); h rows of such a down projection use hq / hs
+                           and hq_shared / hs_shared in the same encoding    */
 } mxmoe_ws_layout;
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);

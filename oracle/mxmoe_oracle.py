@@ -497,7 +497,8 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   mt row tiles share a weight tile, its nt channel tiles an activation tile),
 #   wbytes = linears * BN * K * wbits / 8, abytes = BM * K * (1 or 2), plus
 #   8 * BM * BN * linears for a sliced tile (its partial sums written and read
-#   back); flops = 2 * linears * BM * BN * K, rate 19531 (int8) or 9766 (16-bit)
+#   back); flops = 2 * linears * BM * BN * K, rate 39062 (FP4, and w4a4 on FP6
+#   operands, whose weights count 6 bits), 19531 (int8) or 9766 (16-bit)
 #   FLOP/ns - one CU's share of 8 TB/s and of 5.0 / 2.5 PFLOP/s - and 2e6 ps
 #   (2 us) of fixed per-tile work;
 #   queue order: decreasing cost, ties by lower expert index.
@@ -524,12 +525,13 @@ _TILE_FIXED_PS = 2.0e6
 def _tile_cost(bm: int, bn: int, nl: int, scheme, kk: int, split: int, mt: int, nt: int) -> int:
     is_int = scheme.a_bits < 16
     mx = getattr(scheme, "fmt", 0) == 1
-    wbytes = float(nl * bn * kk * scheme.w_bits) / 8.0
+    f6 = getattr(scheme, "fmt", 0) == 3        # int4 codes stored as 6-bit e2m3, FP6 MFMA rate
+    wbytes = float(nl * bn * kk * (6 if f6 else scheme.w_bits)) / 8.0
     abytes = float(bm) * kk * (0.5 if mx else (1.0 if is_int else 2.0))
     pbytes = 8.0 * bm * bn * nl if split > 1 else 0.0
     flops = 2.0 * nl * bm * bn * kk
     t_mem = (wbytes / max(mt, 1) + abytes / max(nt, 1) + pbytes) * 32.0
-    t_mma = flops * 1000.0 / (39062.0 if mx else (19531.0 if is_int else 9766.0))
+    t_mma = flops * 1000.0 / (39062.0 if (mx or f6) else (19531.0 if is_int else 9766.0))
     c = max(t_mem, t_mma) + _TILE_FIXED_PS
     return int(min(c, 2.0e9))
 

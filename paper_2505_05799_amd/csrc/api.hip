@@ -26,6 +26,8 @@ int scheme_kind(const mxmoe_scheme& s) {
     return (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 32 && s.a_group == 32 && s.symmetric == 1) ? K_MXFP4 : -1;
   if (s.fmt == 2)  // FP8 e4m3: per-channel weight scales, per-token activation scales
     return (s.w_bits == 8 && s.a_bits == 8 && s.w_group == -1 && s.a_group == -1 && s.symmetric == 1) ? K_F8A8 : -1;
+  if (s.fmt == 3)  // w4a4 (per channel / per token) with its int4 codes held as FP6 e2m3 operands
+    return (s.w_bits == 4 && s.a_bits == 4 && s.w_group == -1 && s.a_group == -1 && s.symmetric == 1) ? K_W4A4F6 : -1;
   if (s.fmt != 0) return -1;
   if (s.w_bits == 4 && s.a_bits == 4 && s.w_group == 128 && s.a_group == 128 && s.symmetric == 1) return K_W4A4G;
   if (s.a_group != -1) return -1;
@@ -76,6 +78,7 @@ struct BlockInfo {
   bool any_x4g = false, any_hg = false, any_hg_sh = false;  // w4a4-g128 gate|up, routed / shared down
   bool any_xmx = false, any_hmx = false, any_hmx_sh = false;  // mxfp4 gate|up, routed / shared down
   bool any_xf8 = false;  // FP8 gate|up
+  bool any_xf6 = false;  // w4a4 on FP6 operands, gate|up
   int kinds[kMaxG][3];
 };
 
@@ -100,6 +103,7 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
   bi->any_x4g = bi->any_hg = bi->any_hg_sh = false;
   bi->any_xmx = bi->any_hmx = bi->any_hmx_sh = false;
   bi->any_xf8 = false;
+  bi->any_xf6 = false;
   if (bi->G > kMaxG) return MXMOE_ERR_UNSUPPORTED;
   for (int g = 0; g < bi->G; ++g) {
     const mxmoe_scheme* s = B->scheme + 3 * g;
@@ -117,6 +121,7 @@ mxmoe_status check_block(const mxmoe_block* B, BlockInfo* bi) {
     if (bi->kinds[g][2] == K_W4A4G) (sh ? bi->any_hg_sh : bi->any_hg) = true;
     if (kg == K_MXFP4) bi->any_xmx = true;
     if (kg == K_F8A8) bi->any_xf8 = true;
+    if (kg == K_W4A4F6) bi->any_xf6 = true;
     if (bi->kinds[g][2] == K_MXFP4) (sh ? bi->any_hmx_sh : bi->any_hmx) = true;
     if (kind_is_int(bi->kinds[g][2])) (sh ? bi->any_hq_sh : bi->any_hq) = true;
     if (bi->act == MXMOE_BF16 && kind_is_magic(kg)) bi->rs_x = true;
@@ -187,6 +192,8 @@ WsLayout layout_of(const BlockInfo& bi, int T) {
   L.hsmx_shared = bi.any_hmx_sh ? take((size_t)bi.nsh * T * bi.Fsh / 32) : kNone;
   L.xqf8 = bi.any_xf8 ? take((size_t)T * bi.H) : kNone;
   L.xsf8 = bi.any_xf8 ? take(4 * (size_t)T) : kNone;
+  L.xqf6 = bi.any_xf6 ? take((size_t)T * bi.H) : kNone;
+  L.xsf6 = bi.any_xf6 ? take(4 * (size_t)T) : kNone;
   L.rids = take(4 * P);
   L.rw = take(4 * P);
   L.shw = bi.nsh ? take(4 * (size_t)T * bi.nsh) : kNone;
@@ -376,10 +383,12 @@ mxmoe_status mxmoe_linear_forward(const mxmoe_linear* L, mxmoe_dtype act, const 
     int8_t* aq = at<int8_t>(workspace, w.aq);
     float* as = at<float>(workspace, w.as);
     hipError_t e = kd == K_W4A4G ? launch_act_quant_g128(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream)
-                                 : launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream);
+                   : (kd == K_W4A4F6 ? launch_act_quant_f6(a, act, m, L->k, L->k, reinterpret_cast<uint8_t*>(aq), as, stream)
+                                     : launch_act_quant(a, act, m, L->k, L->k, kind_qmax(kd), aq, as, stream));
     if (e != hipSuccess) return MXMOE_ERR_HIP;
     if (kd == K_W8A8) { ga.xq8 = aq; ga.xs8 = as; }
     else if (kd == K_F8A8) { ga.xqf8 = reinterpret_cast<const uint8_t*>(aq); ga.xsf8 = as; }
+    else if (kd == K_W4A4F6) { ga.xqf6 = reinterpret_cast<const uint8_t*>(aq); ga.xsf6 = as; }
     else if (kd == K_W4A4G) { ga.xq4g = aq; ga.xs4g = as; }
     else { ga.xq4 = aq; ga.xs4 = as; }
   }
@@ -487,6 +496,8 @@ mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_la
   out->hsmx_shared = L.hsmx_shared;
   out->xqf8 = L.xqf8;
   out->xsf8 = L.xsf8;
+  out->xqf6 = L.xqf6;
+  out->xsf6 = L.xsf6;
   out->router_ids = L.rids;
   out->router_w = L.rw;
   out->shared_w = L.shw;
@@ -599,6 +610,10 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     xp.qf8 = at<uint8_t>(workspace, L.xqf8);
     xp.sf8 = at<float>(workspace, L.xsf8);
   }
+  if (bi.any_xf6) {
+    xp.qf6 = at<uint8_t>(workspace, L.xqf6);
+    xp.sf6 = at<float>(workspace, L.xsf6);
+  }
   MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
                        down_qmax, grid, xp, stream));
   MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
@@ -655,6 +670,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.hsmx_shared = at<uint8_t>(workspace, L.hsmx_shared);
   ga.xqf8 = at<uint8_t>(workspace, L.xqf8);
   ga.xsf8 = at<float>(workspace, L.xsf8);
+  ga.xqf6 = at<uint8_t>(workspace, L.xqf6);
+  ga.xsf6 = at<float>(workspace, L.xsf6);
   MX_EVENT(1);
   MX_EVENT(2);
   MX_CHECK(launch_group_gemm(ga, 0, grid, stream));
@@ -675,6 +692,11 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     const int qm = kind_qmax(bi.kinds[bi.E + j][2]);
     if (!qm) continue;
     int8_t* hq = at<int8_t>(workspace, L.hq_shared) + rows * bi.Fsh;
+    if (bi.kinds[bi.E + j][2] == K_W4A4F6) {
+      MX_CHECK(launch_act_quant_f6(hsrc, bi.act, T, bi.Fsh, bi.Fsh, reinterpret_cast<uint8_t*>(hq),
+                                   at<float>(workspace, L.hs_shared) + rows, stream));
+      continue;
+    }
     if (bi.kinds[bi.E + j][2] == K_W4A4G)
       MX_CHECK(launch_act_quant_g128(hsrc, bi.act, T, bi.Fsh, bi.Fsh, qm, hq,
                                      at<float>(workspace, L.hsg_shared) + rows * (bi.Fsh / 128), stream));

@@ -100,15 +100,15 @@ template <int W> __device__ inline int64_t my_row() {
   return W == 1 ? (int64_t)blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6) : (int64_t)blockIdx.x;
 }
 
-template <int NC, int W>
+template <int NC, int W, bool F6 = false>
 __global__ void __launch_bounds__(kThreads) act_quant_vec_kernel(const void* a, int act, int rows, int cols,
                                                                  int64_t ld, int qmax, int8_t* codes,
                                                                  float* scales) {
   __shared__ uint32_t red[kThreads / 64];
   const int64_t r = my_row<W>();
   if (r >= rows) return;
-  quant_row_vec<NC, W>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a) + r * ld), cols, act,
-                       qmax, reinterpret_cast<uint2*>(codes + r * cols), scales + r, red);
+  quant_row_vec<NC, W, F6>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(a) + r * ld), cols, act,
+                           qmax, reinterpret_cast<uint2*>(codes + r * cols), scales + r, red);
 }
 
 // Rows of the sorted (token, slot) pairs whose expert's down projection takes
@@ -142,6 +142,11 @@ __global__ void __launch_bounds__(kThreads) hquant_routed_kernel(const void* h, 
     if (W == 1 || threadIdx.x < 64)
       quant_row_groups(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F, act,
                        qm & 0xFF, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hsg + (int64_t)r * (F >> 7));
+    return;
+  }
+  if (qm & kDownQF6) {  // int4 codes as FP6 e2m3 groups
+    quant_row_vec<NC, W, true>(reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(h) + (int64_t)r * F), F,
+                               act, 7, reinterpret_cast<uint2*>(hq + (int64_t)r * F), hs + r, red);
     return;
   }
   const int qmax = (qm & kDownQF8) ? kQmaxF8 : qm;
@@ -261,6 +266,7 @@ hipError_t launch_rows(int rows, int cols, hipStream_t s, Args... args) {
   return hipGetLastError();
 }
 template <int NC, int W> struct ActQuantK { static constexpr auto fn = act_quant_vec_kernel<NC, W>; };
+template <int NC, int W> struct ActQuantF6K { static constexpr auto fn = act_quant_vec_kernel<NC, W, true>; };
 template <int NC, int W> struct HQuantK { static constexpr auto fn = hquant_routed_kernel<NC, W>; };
 }  // namespace
 
@@ -282,6 +288,14 @@ hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t 
     return hipGetLastError();
   }
   return launch_rows<ActQuantK>(rows, cols, s, a, act, rows, cols, ld, qmax, codes, scales);
+}
+
+hipError_t launch_act_quant_f6(const void* a, int act, int rows, int cols, int64_t ld, uint8_t* codes, float* scales,
+                               hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15) || (reinterpret_cast<uintptr_t>(codes) & 31) || cols % 128 || ld % 8)
+    return hipErrorInvalidValue;
+  return launch_rows<ActQuantF6K>(rows, cols, s, a, act, rows, cols, ld, 7, reinterpret_cast<int8_t*>(codes), scales);
 }
 
 hipError_t launch_act_quant_g128(const void* a, int act, int rows, int cols, int64_t ld, int qmax, int8_t* codes,

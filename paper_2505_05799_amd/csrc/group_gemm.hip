@@ -137,7 +137,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     if (raw_m < 0) {
       const int dk = experts[g].lin[2].kind;
       down_qmax[g] = dk == K_MXFP4 ? kDownQMX
-                    : (dk == K_F8A8 ? kDownQF8 : (kind_qmax(dk) | (dk == K_W4A4G ? kDownQGroup : 0)));
+                    : (dk == K_F8A8 ? kDownQF8
+                                    : (kind_qmax(dk) | (dk == K_W4A4G ? kDownQGroup : 0) | (dk == K_W4A4F6 ? kDownQF6 : 0)));
     }
   }
   if (tid < 2) s_ng[tid] = 0;

@@ -32,6 +32,10 @@
 //           operands), fp32 accumulation.
 //   w8a8  : int8 MFMA, exact int32 sums, then fp32 (acc * s_a) * s_w.
 //   w4a4  : nibbles widened to int8 as 16*q, int8 MFMA, exact sum / 16.
+//   w4a4 on FP6 operands: the int4 codes of both operands stored as e2m3
+//           values, scaled FP6 MFMA (twice the int8 rate); every product is an
+//           integer and every fp32 sum stays below 2^24, so the sums are the
+//           exact integer ones; then fp32 (acc * s_a) * s_w as w8a8.
 //   wNg128: the 16-bit operand is formed exactly.  bf16 activations: a packed
 //           integer add turns the codes of two slots into bf16 values
 //           c + (q - z), c = 128 + 2^N - 1, and the row sums R of the staged
@@ -165,6 +169,7 @@ template <> struct Raw<K_W2G> { u32x2 d; };
 template <> struct Raw<K_W3G> { uint32_t d[3]; };
 template <> struct Raw<K_W8A8> { u32x4 d[2]; };
 template <> struct Raw<K_F8A8> { u32x4 d[2]; };
+template <> struct Raw<K_W4A4F6> { u32x4 d0; u32x2 d1; };  // 24 bytes: 32 e2m3 codes
 
 // loads through the global address space (the pointers come from the block
 // table, so the compiler cannot infer it and would emit flat loads)
@@ -183,6 +188,9 @@ template <int KD> __device__ inline void load_raw(Raw<KD>& r, const uint8_t* p) 
   } else if constexpr (KD == K_W8A8 || KD == K_F8A8) {
     r.d[0] = gload<u32x4>(p);
     r.d[1] = gload<u32x4>(p + 16);
+  } else if constexpr (KD == K_W4A4F6) {  // 24-byte lanes: 8-byte aligned
+    r.d0 = gload<u32x4>(p);
+    r.d1 = gload<u32x2>(p + 16);
   } else if constexpr (!streamed<KD>()) {
     r.d[0] = gload<u32x4>(p);
   }
@@ -489,6 +497,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   constexpr bool GSC = KD == K_W4A4G;                   // per-128-group activation and weight scales
   constexpr bool MX = kind_is_mx(KD);                   // FP4 e2m1 operands with E8M0 scales per 32
   constexpr bool F8 = kind_is_f8(KD);                   // FP8 e4m3 operands, fp32 accumulation
+  constexpr bool F6 = kind_is_f6(KD);                   // int4 codes as FP6 e2m3 operands, exact fp32 sums
   constexpr bool GMETA = kind_has_gmeta(KD);            // group metadata after each fragment block
   constexpr bool RSLOAD = RSUM || GSC || MX;            // a per-row value per k block rides with the stage
   constexpr int RB = stage_rb<KD>();                    // activation bytes per row and k block
@@ -532,8 +541,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     const int8_t* qb;
     if constexpr (PHASE == 1) { qb = shared ? a.hq_shared : a.hq; ascale = shared ? a.hs_shared : a.hs; }
     else {
-      qb = F8 ? reinterpret_cast<const int8_t*>(a.xqf8) : (KD == K_W8A8 ? a.xq8 : (GSC ? a.xq4g : a.xq4));
-      ascale = F8 ? a.xsf8 : (KD == K_W8A8 ? a.xs8 : a.xs4);
+      qb = F8 ? reinterpret_cast<const int8_t*>(a.xqf8)
+              : (F6 ? reinterpret_cast<const int8_t*>(a.xqf6) : (KD == K_W8A8 ? a.xq8 : (GSC ? a.xq4g : a.xq4)));
+      ascale = F8 ? a.xsf8 : (F6 ? a.xsf6 : (KD == K_W8A8 ? a.xs8 : a.xs4));
     }
     abase = reinterpret_cast<const uint8_t*>(qb);
   } else {
@@ -551,7 +561,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     if constexpr (PHASE == 0) {
       src = shared ? m : a.rtok[off_e + m];
       out = shared ? (g - a.E_routed) * a.T + m : off_e + m;
-      if constexpr (F8) sc = ascale[src];
+      if constexpr (F8 || F6) sc = ascale[src];
       else if constexpr (INT && !GSC) sc = shared ? ascale[m] : (KD == K_W8A8 ? a.rxs8 : a.rxs4)[off_e + m];
     } else if constexpr (PHASE == 1) {
       src = shared ? (g - a.E_routed) * a.T + m : off_e + m;
@@ -593,7 +603,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   }
 
   // ---- accumulators and weight streams
-  typedef typename std::conditional<INT && !GSC && !F8, i32x4, f32x4>::type AccT;
+  typedef typename std::conditional<INT && !GSC && !F8 && !F6, i32x4, f32x4>::type AccT;
   typedef typename std::conditional<INT, i32x4, u32x4>::type OpT;
   constexpr int J = MX ? 1 : (INT ? 2 : 4);      // MFMA steps per 128-wide k block
   constexpr bool HOLD_W = NL * NF <= MF;         // hold the smaller operand set in registers
@@ -666,7 +676,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // (weight-only).  Waiting for
   // this many leaves the weight prefetch in flight across the barrier.
   constexpr int kLoadsAfterStage =
-      NL * NF * (streamed<KD>() ? J : ((KD == K_W8A8 || KD == K_F8A8) ? 2 : 1)) + (GMETA ? NL * NF : 0);
+      NL * NF * (streamed<KD>() ? J : ((KD == K_W8A8 || KD == K_F8A8 || KD == K_W4A4F6) ? 2 : 1)) + (GMETA ? NL * NF : 0);
 
   stage_load<RB, BM>(sm, 0, abase, soffs, kb0, wave);
   if constexpr (RSLOAD) rowsum_load<BM, MX>(sm, 0, rsbase, rsoff, kb0, wave);
@@ -809,6 +819,36 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           }
       // the activation fragments two row fragments ahead of the MFMAs (two
       // LDS reads each), so that few of them are live at once
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
+        if (mf + 2 < MF) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+    } else if constexpr (F6) {
+      // w4a4 on FP6 operands: one 16x16x128 FP6 MFMA per (row fragment,
+      // channel fragment) covers the k block.  Lane (li, q) holds k = 32q ..
+      // 32q + 31: for its row the first 24 bytes of the staged row's 32-byte
+      // group q (chunk 2q and the low half of chunk 2q + 1), for its channel
+      // the packed lane's 24 bytes.  Unit scales (E8M0 127) on both operands.
+      i32x8 A[MF];
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const u32x4 a0 = act_frag<RB>(sm, cur, ra + mf * 16 + li, 2 * q);
+        const u32x4 a1 = act_frag<RB>(sm, cur, ra + mf * 16 + li, 2 * q + 1);
+        A[mf] = i32x8{(int)a0[0], (int)a0[1], (int)a0[2], (int)a0[3], (int)a1[0], (int)a1[1], 0, 0};
+      }
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+        for (int l = 0; l < NL; ++l)
+#pragma unroll
+          for (int nf = 0; nf < NF; ++nf) {
+            const u32x4 w0 = wr[l][nf].d0;
+            const u32x2 w1 = wr[l][nf].d1;
+            const i32x8 B = {(int)w0[0], (int)w0[1], (int)w0[2], (int)w0[3], (int)w1[0], (int)w1[1], 0, 0};
+            acc[l][nf][mf] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(A[mf], B, acc[l][nf][mf], 2, 2, 0, 127, 0, 127);
+          }
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
       for (int mf = 0; mf < MF; ++mf) {
@@ -1006,7 +1046,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       }
     // value of accumulator (l, nf, mf, i) after the scheme's scales
     auto outv = [&](int l, int nf, int mf, int i, const f32x4& rs) -> float {
-      if constexpr (F8) {
+      if constexpr (F8 || F6) {
         return (acc[l][nf][mf][i] * rs[i]) * cs[l][nf];
       } else if constexpr (INT && !GSC) {
         int iv = acc[l][nf][mf][i];
@@ -1121,7 +1161,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int i = 0; i < 4; ++i) {
           const int64_t orow = (int64_t)ro[i] * N + n;
           if (GUARD && ro[i] < 0) continue;
-          if constexpr (INT && !GSC && !F8) {
+          if constexpr (F6) {  // the exact integer sum, held in fp32
+            reinterpret_cast<int32_t*>(a.raw_out)[orow] = (int32_t)acc[0][nf][mf][i];
+          } else if constexpr (INT && !GSC && !F8) {
             int iv = acc[0][nf][mf][i];
             if constexpr (KD == K_W4A4) iv >>= 4;
             reinterpret_cast<int32_t*>(a.raw_out)[orow] = iv;
@@ -1150,6 +1192,7 @@ __device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExper
       if constexpr (CFG != CFG_L || PHASE == 1) run_tile<K_F8A8, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split);
       break;
     case K_W4A4: run_tile<K_W4A4, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
+    case K_W4A4F6: run_tile<K_W4A4F6, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W2G: run_tile<K_W2G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W3G: run_tile<K_W3G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;
     case K_W4G: run_tile<K_W4G, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;

@@ -25,16 +25,23 @@ enum Kind : int32_t {
   K_W4A4G = 7, // int4 weights and activations with per-128-group scales (w4a4-g128)
   K_MXFP4 = 8, // FP4 e2m1 weights and activations with E8M0 scales per 32 (scaled FP4 MFMA)
   K_F8A8 = 9,  // FP8 e4m3 weights (per-channel fp32 scale) and activations (per-token), FP8 MFMA
-  K_COUNT = 10
+  K_W4A4F6 = 10,  // w4a4 (per channel / per token) with the int4 codes as FP6 e2m3 operands, FP6 MFMA
+  K_COUNT = 11
 };
 
 // kinds whose activations arrive as one byte per element with a per-token
 // (or per-group) fp32 scale and whose weights carry fp32 channel scales: the
 // integer kinds and FP8, which shares their layouts
 __host__ __device__ constexpr inline bool kind_is_int(int kd) {
-  return kd == K_W8A8 || kd == K_W4A4 || kd == K_W4A4G || kd == K_F8A8;
+  return kd == K_W8A8 || kd == K_W4A4 || kd == K_W4A4G || kd == K_F8A8 || kd == K_W4A4F6;
 }
 __host__ __device__ constexpr inline bool kind_is_f8(int kd) { return kd == K_F8A8; }
+// w4a4 on FP6 operands: every int4 code in [-7, 7] is an e2m3 value, products
+// are integers up to 49 and a 128-wide k block sums to at most 6272 in
+// magnitude, so the FP6 MFMA's fp32 results are the exact integer sums.
+// Activations: per 32 consecutive elements 24 bytes of 6-bit codes (element i
+// at bits 6i..6i+5) and 8 zero bytes, one byte per element like int8 codes.
+__host__ __device__ constexpr inline bool kind_is_f6(int kd) { return kd == K_W4A4F6; }
 __host__ __device__ constexpr inline bool kind_is_wonly(int kd) { return kd >= K_W2G && kd <= K_W8G; }
 // kinds whose scales come per 128-wide group along K (a 64-byte metadata tail
 // per fragment block): the weight-only kinds and w4a4-g128
@@ -49,6 +56,7 @@ __host__ __device__ constexpr inline int kind_wbits(int kd) {
     case K_W16: return 16;
     case K_W8A8: return 8;
     case K_F8A8: return 8;
+    case K_W4A4F6: return 6;  // stored bits (4-bit codes held as e2m3)
     case K_W4A4: return 4;
     case K_W4A4G: return 4;
     case K_MXFP4: return 4;
@@ -66,7 +74,7 @@ __host__ __device__ constexpr inline bool kind_is_magic(int kd) { return kd == K
 // largest finite e4m3 value, which takes the place of qmax in the recipe
 constexpr int kQmaxF8 = 448;
 __host__ __device__ constexpr inline int kind_qmax(int kd) {
-  return kd == K_W8A8 ? 127 : ((kd == K_W4A4 || kd == K_W4A4G) ? 7 : (kd == K_F8A8 ? kQmaxF8 : 0));
+  return kd == K_W8A8 ? 127 : ((kd == K_W4A4 || kd == K_W4A4G || kd == K_W4A4F6) ? 7 : (kd == K_F8A8 ? kQmaxF8 : 0));
 }
 
 // Packed layout: the weight matrix [n, k] is cut into fragment blocks of
@@ -81,6 +89,7 @@ __host__ __device__ constexpr inline int lane_bytes(int kd) {
     case K_W16: return 64;
     case K_W8A8: return 32;
     case K_F8A8: return 32;
+    case K_W4A4F6: return 24;  // 32 e2m3 codes
     case K_W4A4: return 16;
     case K_W4A4G: return 16;
     case K_MXFP4: return 16;
@@ -198,8 +207,8 @@ __host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int spli
   return g | (cfg << 16) | (kind << 20) | ((split - 1) << 24);
 }
 // Static cost of one tile in ps: the larger of its memory time and its MFMA
-// time at one CU's share of the MI355X peaks (8 TB/s; 10 PFLOP/s FP4, 5.0
-// POPS int8, 2.5 PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
+// time at one CU's share of the MI355X peaks (8 TB/s; 10 PFLOP/s FP4 / FP6,
+// 5.0 POPS int8, 2.5 PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
 // (prologue, epilogue).  The group's mt row tiles share each weight tile and
 // its nt channel tiles share each activation tile through L2, so a tile is
 // charged those shares of its HBM bytes; a sliced tile also writes its partial
@@ -212,7 +221,8 @@ __host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int
   const double pbytes = split > 1 ? 8.0 * bm * bn * nl : 0.0;
   const double flops = 2.0 * nl * bm * bn * kk;
   const double t_mem = (wbytes / (mt > 0 ? mt : 1) + abytes / (nt > 0 ? nt : 1) + pbytes) * 32.0;
-  const double t_mma = flops * 1000.0 / (kind_is_mx(kd) ? 39062.0 : (kind_is_int(kd) ? 19531.0 : 9766.0));
+  const double t_mma =
+      flops * 1000.0 / ((kind_is_mx(kd) || kind_is_f6(kd)) ? 39062.0 : (kind_is_int(kd) ? 19531.0 : 9766.0));
   double c = t_mem > t_mma ? t_mem : t_mma;
   c += kTileFixedPs;
   if (c > 2.0e9) c = 2.0e9;
@@ -259,6 +269,7 @@ struct WsLayout {
   size_t rids, rw, shw;  // router front-end outputs: ids, gate weights, shared-expert gates
   size_t xqmx, xsmx, hqmx, hsmx, hqmx_shared, hsmx_shared;  // mxfp4 activation codes and E8M0 bytes
   size_t xqf8, xsf8;  // FP8 e4m3 codes and per-token scales of x
+  size_t xqf6, xsf6;  // FP6-encoded int4 codes and per-token scales of x
   int qcap;  // XCD queue capacity of the tile plan (super-tiles)
   int fcap;  // XCD queue capacity of the tile plan (tiles)
   int64_t pfloats;  // size of the partial buffer
@@ -306,14 +317,20 @@ hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, i
 // down_qmax[e] = qmax | kDownQGroup for per-128-group scales (into hsg
 // [P][F/128]), else per-row scales (into hs); 0 = not quantized.
 constexpr int kDownQGroup = 0x100;
-constexpr int kDownQMX = 0x200;
-constexpr int kDownQF8 = 0x400;  // FP8 e4m3 codes into hq, per-row scales into hs  // MXFP4 codes into hqmx [P][F/2], E8M0 bytes into hsmx [P][F/32]
+constexpr int kDownQMX = 0x200;  // MXFP4 codes into hqmx [P][F/2], E8M0 bytes into hsmx [P][F/32]
+constexpr int kDownQF8 = 0x400;  // FP8 e4m3 codes into hq, per-row scales into hs
+constexpr int kDownQF6 = 0x800;  // int4 codes as FP6 e2m3 (32 per 24 + 8 zero bytes) into hq, scales into hs
 hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int32_t* offsets,
                                 int E, const int32_t* down_qmax, int8_t* hq, float* hs, float* hsg,
                                 uint8_t* hqmx, uint8_t* hsmx, hipStream_t s);
 // MXFP4 encoding of rows (cols a multiple of 128): codes [rows][cols/2] (two
 // e2m1 nibbles a byte, element order), E8M0 bytes [rows][cols/32].
 hipError_t launch_act_quant_mx(const void* a, int act, int rows, int cols, int64_t ld, uint8_t* codes, uint8_t* exps,
+                               hipStream_t s);
+// Per-row int4 quantization (qmax 7, the per-token recipe) written as FP6 e2m3
+// groups: per 32 elements 24 bytes of 6-bit codes and 8 zero bytes, codes
+// [rows, cols] bytes, scales [rows]; cols a multiple of 128.
+hipError_t launch_act_quant_f6(const void* a, int act, int rows, int cols, int64_t ld, uint8_t* codes, float* scales,
                                hipStream_t s);
 
 struct GemmArgs {
@@ -336,6 +353,10 @@ struct GemmArgs {
   // FP8: e4m3 codes [T,H] and per-token scales [T] of x (h rows of an FP8 down
   // projection use hq / hs and hq_shared / hs_shared)
   const uint8_t* xqf8; const float* xsf8;
+  // w4a4 on FP6 operands: x codes [T,H] (e2m3 groups of 32, one byte per
+  // element) and per-token scales [T]; h rows of such a down projection use
+  // hq / hs and hq_shared / hs_shared
+  const uint8_t* xqf6; const float* xsf6;
   void* h; void* h_shared;
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;
@@ -379,6 +400,8 @@ struct XPrep {
   uint8_t* smx;
   uint8_t* qf8;   // FP8 e4m3 codes [rows, cols], scales sf8 [rows]
   float* sf8;
+  uint8_t* qf6;   // int4 codes as FP6 e2m3 groups [rows, cols] (one byte per element), scales sf6 [rows]
+  float* sf6;
 };
 
 // raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of

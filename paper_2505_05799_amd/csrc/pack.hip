@@ -29,13 +29,18 @@
 //          v (dword v/8, bits 4(v%8)): the operand layout of one 16x16x128 FP4
 //          MFMA.  The block ends with 16 dwords, one per channel, whose byte b
 //          is the E8M0 scale of the channel's 32-wide block b of this k block.
+//   w4a4 on FP6 operands: lane l holds k = 128*kb + 32*qd + v, slot v as the
+//          6-bit e2m3 code of the int4 value at bits 6v..6v+5 of the lane's 24
+//          bytes (the operand layout of one 16x16x128 FP6 MFMA); per-channel
+//          fp32 scales after the last block, as w4a4.
 #include "mxmoe_internal.h"
+#include "rowquant.h"
 
 namespace mxmoe {
 namespace {
 
 __device__ inline int slot_k(int kd, int v, int qd) {
-  if (kd == K_MXFP4) return 32 * qd + v;
+  if (kd == K_MXFP4 || kd == K_W4A4F6) return 32 * qd + v;
   if (kind_is_int(kd)) return 64 * (v >> 4) + 16 * qd + (v & 15);
   return 32 * (v >> 3) + 8 * qd + (v & 7);
 }
@@ -132,6 +137,13 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
       const int sc = (int)(int8_t)codes[idx];
       bad |= sc < -7 || sc > 7;
     }
+    if (kd == K_W4A4F6) {  // 6-bit e2m3 field at bit 6v, possibly across two dwords
+      const uint32_t e = e2m3_of_int((int)(int8_t)c) & 63u;
+      const int b = 6 * v;
+      w[b >> 5] |= e << (b & 31);
+      if ((b & 31) > 26) w[(b >> 5) + 1] |= e >> (32 - (b & 31));
+      continue;
+    }
     int dw, bit;
     uint32_t mask;
     slot_field(kd, v, &dw, &bit, &mask);
@@ -156,7 +168,8 @@ __global__ void pack_kernel(int kd, int n, int k, int act, int w16_src,
   }
 }
 
-// Per-channel w4a4: a channel with a code outside [-7, 7] gets a NaN scale
+// Per-channel w4a4 (int8 or FP6 operands): a channel with a code outside
+// [-7, 7] gets a NaN scale
 // (after pack_kernel wrote the scales, same stream), one workgroup per channel.
 __global__ void __launch_bounds__(256) poison_channels_kernel(int n, int k, const int8_t* __restrict__ codes,
                                                               float* __restrict__ wscale) {
@@ -189,6 +202,16 @@ __global__ void unpack_kernel(int kd, int n, int k, int act, const uint8_t* __re
   const uint32_t* w = reinterpret_cast<const uint32_t*>(packed + blk * block_bytes(kd) + lane * lane_bytes(kd));
   for (int v = 0; v < 32; ++v) {
     const int64_t idx = rbase + slot_k(kd, v, qd);
+    if (kd == K_W4A4F6) {  // e2m3 field -> the integer it holds
+      const int b = 6 * v;
+      uint32_t e = w[b >> 5] >> (b & 31);
+      if ((b & 31) > 26) e |= w[(b >> 5) + 1] << (32 - (b & 31));
+      e &= 63u;
+      const int ex = (int)((e >> 3) & 3u), mn = (int)(e & 7u);
+      const int mag = ex == 0 ? 0 : ((8 + mn) << (ex - 1)) >> 3;  // (1 + m/8) 2^(ex-1) for the integer codes
+      codes[idx] = (uint8_t)(int8_t)((e & 32u) ? -mag : mag);
+      continue;
+    }
     int dw, bit;
     uint32_t mask;
     slot_field(kd, v, &dw, &bit, &mask);
@@ -223,7 +246,7 @@ hipError_t launch_pack(int kind, int n, int k, int act, int w16_src, const void*
   int64_t blocks = (threads + 255) / 256;
   hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, kind, n, k, act, w16_src,
                      (const uint8_t*)codes, (const uint8_t*)scales, (const uint8_t*)zeros, packed);
-  if (kind == K_W4A4) {
+  if (kind == K_W4A4 || kind == K_W4A4F6) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(poison_channels_kernel, dim3((unsigned)n), dim3(256), 0, s, n, k, (const int8_t*)codes,

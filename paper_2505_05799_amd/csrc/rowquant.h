@@ -89,11 +89,45 @@ __device__ inline uint2 codes8(uint4 u, int act, float inv, float q) {
   return make_uint2(w[0], w[1]);
 }
 
+// FP6 e2m3 code of an integer v in [-7, 7] (sign bit 5, two exponent bits of
+// bias 1, three mantissa bits): magnitudes 0..7 have codes 0, 8, 16, 20, 24,
+// 26, 28, 30.
+__device__ inline uint32_t e2m3_of_int(int v) {
+  const uint32_t m = (uint32_t)(v < 0 ? -v : v);
+  const uint32_t mag = m == 0 ? 0u : (m == 1 ? 8u : (m < 4 ? 16u + 4u * (m - 2u) : 24u + 2u * (m - 4u)));
+  return (v < 0 ? 0x20u : 0u) | mag;
+}
+// int4 codes of 8 elements (the per-token recipe with q = 7) as one 48-bit
+// run of 6-bit e2m3 codes, element i at bits 6i..6i+5.
+__device__ inline uint64_t codes8_f6(uint4 u, int act, float inv) {
+  float f[8];
+  unpack8(u, act, f);
+  uint64_t w = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float r = __builtin_rintf(__fmul_rn(f[i], inv));
+    r = fminf(fmaxf(r, -7.f), 7.f);
+    w |= (uint64_t)e2m3_of_int((int)r) << (6 * i);
+  }
+  return w;
+}
+// Store of 8 elements' e2m3 codes (chunk c of the row, 8 elements per chunk):
+// a group of 32 elements is 24 bytes of codes then 8 zero bytes, so chunk c
+// lands at byte 32 (c / 4) + 6 (c % 4); the last chunk of a group also writes
+// the group's 8 zero bytes.
+__device__ inline void store_f6_chunk(uint8_t* row, int c, uint64_t w) {
+  uint16_t* p = reinterpret_cast<uint16_t*>(row + 32 * (c >> 2) + 6 * (c & 3));
+  p[0] = (uint16_t)w;
+  p[1] = (uint16_t)(w >> 16);
+  p[2] = (uint16_t)(w >> 32);
+  if ((c & 3) == 3) *reinterpret_cast<uint2*>(row + 32 * (c >> 2) + 24) = make_uint2(0u, 0u);
+}
+
 // Quantizes one row of cols (a multiple of 8) elements with W wavefronts (1:
 // each wavefront of the workgroup takes its own row, 4: the workgroup takes
 // one row).  NC > 0: the row's 16-byte chunks stay in registers
 // (cols <= 512 * W * NC); NC == 0: any length, the row is read twice.
-template <int NC, int W>
+template <int NC, int W, bool F6 = false>
 __device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, int act, int qmax,
                                      uint2* __restrict__ codes, float* __restrict__ scale, uint32_t* red) {
   const int idx = W == 1 ? (threadIdx.x & 63) : threadIdx.x, nch = cols >> 3;
@@ -126,14 +160,21 @@ __device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, in
     inv = __fdiv_rn(q, amax);
     s = __fdiv_rn(amax, q);
   }
+  uint8_t* cb = reinterpret_cast<uint8_t*>(codes);
   if constexpr (NC > 0) {
 #pragma unroll
     for (int i = 0; i < NC; ++i) {
       const int c = idx + kStride * i;
-      if (c < nch) codes[c] = codes8(v[i], act, inv, q);
+      if (c < nch) {
+        if constexpr (F6) store_f6_chunk(cb, c, codes8_f6(v[i], act, inv));
+        else codes[c] = codes8(v[i], act, inv, q);
+      }
     }
   } else {
-    for (int c = idx; c < nch; c += kStride) codes[c] = codes8(row[c], act, inv, q);
+    for (int c = idx; c < nch; c += kStride) {
+      if constexpr (F6) store_f6_chunk(cb, c, codes8_f6(row[c], act, inv));
+      else codes[c] = codes8(row[c], act, inv, q);
+    }
   }
   if (idx == 0) *scale = s;
 }
@@ -248,6 +289,10 @@ __device__ inline void x_prep_row(const XPrep& p, int64_t r) {
   if (p.qf8) {
     if (cols <= 4096) quant_row_vec<8, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
     else quant_row_vec<0, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
+  }
+  if (p.qf6) {
+    if (cols <= 4096) quant_row_vec<8, 1, true>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.qf6 + r * cols), p.sf6 + r, nullptr);
+    else quant_row_vec<0, 1, true>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.qf6 + r * cols), p.sf6 + r, nullptr);
   }
 }
 

@@ -51,7 +51,7 @@ WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8",
              "h", "h_shared", "hq", "hs", "hq_shared", "hs_shared", "slots", "total", "plan_queue_cap",
              "plan_flat_cap", "partial", "partial_floats", "rsx", "rsh", "rsh_shared", "xq4g", "xs4g", "hsg",
              "hsg_shared", "xqmx", "xsmx", "hqmx", "hsmx", "hqmx_shared", "hsmx_shared", "router_ids", "router_w",
-             "shared_w", "xqf8", "xsf8"]
+             "shared_w", "xqf8", "xsf8", "xqf6", "xsf6"]
 
 
 class WsLayout_t(C.Structure):
@@ -262,7 +262,7 @@ class PackedLinear:
         c = codes.cpu().numpy()
         if s.w_bits == 16:
             c = c.view(np.uint16)
-        elif s.a_bits < 16 and s.fmt == 0:
+        elif s.a_bits < 16 and s.fmt in (0, 3):
             c = c.view(np.int8)
         sc = None if scales is None else scales.cpu().numpy()
         if sc is not None and s.fmt == 0 and (s.a_bits == 16 or s.w_group > 0):
@@ -272,14 +272,14 @@ class PackedLinear:
 
 
 def linear_forward(pl: PackedLinear, a, stream=None, return_ws: bool = False):
-    """out = a W^T through the micro-kernels: int32 for w8a8/w4a4 (per channel),
-    else fp32 (fp8: scaled by s_a[m] s_w[n]).  return_ws: also return the
+    """out = a W^T through the micro-kernels: int32 for w8a8/w4a4 (per channel,
+    int8 or FP6 operands), else fp32 (fp8: scaled by s_a[m] s_w[n]).  return_ws: also return the
     workspace (its tile plan starts at offset 0)."""
     torch = _torch()
     lib = load_library()
     m = a.shape[0]
     s = pl.q.scheme
-    raw_int = s.a_bits < 16 and s.a_group < 0 and getattr(s, "fmt", 0) == 0
+    raw_int = s.a_bits < 16 and s.a_group < 0 and getattr(s, "fmt", 0) in (0, 3)
     out = torch.empty((m, pl.q.n), dtype=torch.int32 if raw_int else torch.float32, device=a.device)
     wsb = lib.mxmoe_linear_workspace_bytes(C.byref(pl.L), m)
     ws = empty_aligned(wsb, a.device)

@@ -64,7 +64,8 @@ class Scheme:
     a_group: int     # 128 for groups along K, -1 = per token
     symmetric: int   # 1 for w8a8 / w4a4 (per channel or g128), 0 for wNg128 asym and 16-bit
     fmt: int = 0     # 0 integer codes; 1 OCP MX floating point (e2m1 elements, E8M0 scale per 32);
-                     # 2 FP8 e4m3 elements with per-channel / per-token fp32 scales
+                     # 2 FP8 e4m3 elements with per-channel / per-token fp32 scales;
+                     # 3 w4a4 codes held as FP6 e2m3 operands (same quantization as fmt 0)
 
     @property
     def name(self) -> str:
@@ -72,6 +73,8 @@ class Scheme:
             return "mxfp4"
         if self.fmt == 2:
             return "fp8"
+        if self.fmt == 3:
+            return "w4a4f6"
         if self.w_bits == 16:
             return "w16"
         if self.a_bits < 16:
@@ -89,6 +92,8 @@ class Scheme:
             return 16.0
         if self.fmt == 1:
             return self.w_bits + 8.0 / self.w_group    # one E8M0 byte per 32
+        if self.fmt == 3:
+            return 6.0 + 32.0 / k                      # 4-bit codes stored as 6-bit e2m3, fp32 row scale
         if self.weight_only:
             return self.w_bits + 32.0 / self.w_group   # fp16 scale + fp16 zero
         if self.w_group > 0:
@@ -106,7 +111,8 @@ W8G128 = Scheme(8, 16, 128, -1, 0)
 W4A4G128 = Scheme(4, 4, 128, 128, 1)   # 4-bit weights and activations, per-128 group scales
 MXFP4 = Scheme(4, 4, 32, 32, 1, 1)     # FP4 e2m1 weights and activations, E8M0 scale per 32
 FP8 = Scheme(8, 8, -1, -1, 1, 2)       # FP8 e4m3 weights (per channel) and activations (per token)
-ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128, MXFP4, FP8)
+W4A4F6 = Scheme(4, 4, -1, -1, 1, 3)    # w4a4 whose int4 codes run as FP6 e2m3 operands (6 stored bits)
+ALL_SCHEMES = (W16, W8A8, W4A4, W2G128, W3G128, W4G128, W8G128, W4A4G128, MXFP4, FP8, W4A4F6)
 SCHEME_BY_NAME = {s.name: s for s in ALL_SCHEMES}
 
 LINEAR_NAMES = ("gate", "up", "down")
@@ -206,6 +212,10 @@ def _qwen2_alloc(e: int, rank: int):
     return (W8A8, W8A8, W8A8) if rank <= 10 else (W4A4, W4A4, W4A4)
 
 
+def _qwen2_f6_alloc(e: int, rank: int):
+    return (W8A8, W8A8, W8A8) if rank <= 10 else (W4A4F6, W4A4F6, W4A4F6)
+
+
 CONFIGS: Dict[str, BlockConfig] = {
     "tiny": BlockConfig(
         "tiny", T=64, H=256, F=512, E=4, k=2, n_shared=0, F_shared=0, act="fp16",
@@ -245,6 +255,11 @@ CONFIGS: Dict[str, BlockConfig] = {
         zipf_s=1.0, alloc=_qwen2_alloc, shared_alloc=(W8A8, W8A8, W8A8),
         description="Qwen2-57B-A14B-shaped prefill: 16384 tokens, hidden 3584, 64 experts FFN "
                     "2560, top-8, shared FFN 20480, w8a8/w4a4"),
+    "qwen2_f6": BlockConfig(
+        "qwen2_f6", T=16384, H=3584, F=2560, E=64, k=8, n_shared=1, F_shared=20480, act="bf16",
+        zipf_s=1.0, alloc=_qwen2_f6_alloc, shared_alloc=(W8A8, W8A8, W8A8),
+        description="Qwen2-57B-A14B-shaped prefill (16384 tokens, w8a8/w4a4) with the w4a4 experts' int4 codes "
+                    "run as FP6 e2m3 operands"),
 }
 
 # ----------------------------------------------------------------------------
@@ -400,6 +415,8 @@ class QLinear:
             return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
         if s.fmt == 1:      # e2m1 nibbles + one E8M0 byte per 32
             return self.n * self.k // 2 + self.n * self.k // 32
+        if s.fmt == 3:      # 6-bit e2m3 codes + one fp32 scale per row
+            return self.n * self.k * 6 // 8 + 4 * self.n
         if s.w_group > 0:   # packed with the same 4-byte metadata slot per group
             return self.n * self.k * s.w_bits // 8 + (self.n * self.k // 128) * 4
         return self.n * self.k * s.w_bits // 8 + 4 * self.n

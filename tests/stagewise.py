@@ -55,11 +55,41 @@ def _down_kind(s):
         return "mx"
     if fmt == 2:
         return "fp8"
+    if fmt == 3:
+        return "f6"
     if s.a_bits < 16 and s.a_group > 0:
         return "g"
     if s.a_bits < 16:
         return "int"
     return "float"
+
+
+# e2m3 codes of the integers -7..7 from the bit-field definition (sign bit 5,
+# two exponent bits of bias 1, three mantissa bits): |v| = (1 + m/8) 2^(e-1)
+_E2M3_OF = {}
+for _e in range(1, 4):
+    for _m in range(8):
+        _v = (1 + _m / 8) * 2.0 ** (_e - 1)
+        if _v == int(_v) and _v <= 7:
+            _E2M3_OF[int(_v)] = (_e << 3) | _m
+_E2M3_OF[0] = 0
+
+
+def f6_bytes(q):
+    """int4 codes [rows, cols] -> the FP6 byte layout of the workspace: per 32
+    elements 24 bytes of 6-bit e2m3 codes (element i at bits 6i..6i+5, little
+    endian) followed by 8 zero bytes."""
+    q = np.asarray(q, dtype=np.int64)
+    rows, cols = q.shape
+    code = np.vectorize(lambda v: (0x20 if v < 0 else 0) | _E2M3_OF[abs(int(v))], otypes=[np.int64])(q)
+    g = code.reshape(rows, cols // 32, 32)
+    out = np.zeros((rows, cols // 32, 32), np.uint8)
+    bits = np.zeros((rows, cols // 32), dtype=object)
+    for i in range(32):
+        bits = bits + (g[:, :, i].astype(object) << (6 * i))
+    for b in range(24):
+        out[:, :, b] = np.vectorize(lambda x: (x >> (8 * b)) & 0xFF, otypes=[np.uint8])(bits)
+    return out.reshape(rows, cols)
 
 
 def _codes(h32, s):
@@ -68,6 +98,9 @@ def _codes(h32, s):
     kind = _down_kind(s)
     if kind == "int":
         return O.act_quant(h32, (1 << (s.a_bits - 1)) - 1)
+    if kind == "f6":
+        q, sc = O.act_quant(h32, 7)
+        return f6_bytes(q), sc
     if kind == "g":
         return O.act_quant_groups(h32, (1 << (s.a_bits - 1)) - 1, s.a_group)
     if kind == "fp8":
@@ -83,7 +116,7 @@ def _down_ref(hv, lin, act, gw):
     None, per-element bound or None)."""
     kind = _down_kind(lin.scheme)
     gw64 = gw.astype(np.float64)[:, None]
-    if kind == "int":
+    if kind in ("int", "f6"):
         h32 = hv.astype(np.float32)
         qa, sa = O.act_quant(h32, (1 << (lin.scheme.a_bits - 1)) - 1)
         acc = O.linear(hv, lin, act, return_int=True)
@@ -150,9 +183,9 @@ def check_forward(mb, blk, y, shared_w=None, chunk=4096, log=None) -> Report:
         nrows = P if not shared else nsh * T
         base = 0 if not shared else j * T
         lo, hi = base + rows_lo, base + rows_hi
-        if kind in ("int", "fp8", "g"):
+        if kind in ("int", "fp8", "g", "f6"):
             q = buf("hq" + pre, torch.int8, nrows, F)[lo:hi]
-            if kind == "fp8":
+            if kind in ("fp8", "f6"):
                 q = q.view(np.uint8)
             if kind == "g":
                 return q, buf("hsg" + pre, torch.float32, nrows, F // 128)[lo:hi]

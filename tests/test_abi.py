@@ -53,6 +53,8 @@ def test_packed_bytes_closed_form(lib, s):
     got = lib.mxmoe_packed_bytes(C.byref(_L(s, n, k)), M.BF16)
     if s.w_bits == 16:
         want = 2 * n * k
+    elif s.fmt == 3:
+        want = n * k * 6 // 8 + 4 * n                          # 4-bit codes held as 6-bit e2m3
     elif s.a_bits == 16:
         want = n * k * s.w_bits // 8 + (n * k // 128) * 4      # N + 0.25 bits per weight
     elif s.w_group > 0:

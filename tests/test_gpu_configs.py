@@ -17,12 +17,13 @@ from tests.stagewise import check_forward
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["tiny", "mixtral", "dsv2lite", "qwen15_uniform", "qwen15_mixed", "qwen15_w5a5", "qwen15_float", "qwen2"]
+NAMES = ["tiny", "mixtral", "dsv2lite", "qwen15_uniform", "qwen15_mixed", "qwen15_w5a5", "qwen15_float", "qwen2",
+         "qwen2_f6"]
 
 
 # micro-kernel ids of the schemes in the plan's tile entries
 KIND = {"w16": 0, "w8a8": 1, "w4a4": 2, "w2g128": 3, "w3g128": 4, "w4g128": 5, "w8g128": 6, "w4a4g128": 7,
-        "mxfp4": 8, "fp8": 9}
+        "mxfp4": 8, "fp8": 9, "w4a4f6": 10}
 
 
 PF_N = 12  # int32 fields per group record of the tile plan

@@ -70,6 +70,9 @@ MIXES = [
     # fp8 (e4m3 with per-channel / per-token scales, on the FP8 MFMA) beside the others
     [(W.FP8,) * 3, (W.FP8, W.FP8, W.W2G128), (W.W8A8, W.W8A8, W.FP8), (W.W16, W.W16, W.FP8),
      (W.FP8, W.FP8, W.W4A4G128), (W.MXFP4, W.MXFP4, W.FP8), (W.FP8, W.FP8, W.W8A8)],
+    # w4a4 on FP6 e2m3 operands beside the others (and beside int8-MFMA w4a4)
+    [(W.W4A4F6,) * 3, (W.W4A4F6, W.W4A4F6, W.W2G128), (W.W8A8, W.W8A8, W.W4A4F6), (W.W16, W.W16, W.W4A4F6),
+     (W.W4A4F6, W.W4A4F6, W.W4A4G128), (W.W4A4, W.W4A4, W.W4A4F6), (W.W4A4F6, W.W4A4F6, W.W4A4)],
 ]
 
 

@@ -138,7 +138,7 @@ def _check_linear(q, a, got, act):
     within the fp32 accumulation model on the operands as the kernel
     multiplies them (tests/tolerance.py)."""
     s = q.scheme
-    if s.a_bits < 16 and s.a_group < 0 and s.fmt == 0:
+    if s.a_bits < 16 and s.a_group < 0 and s.fmt in (0, 3):
         want = O.linear(a, q, act, return_int=True)
         assert np.array_equal(got.astype(np.int64), want)
         return 0.0
@@ -233,7 +233,7 @@ def test_linear_deterministic():
     assert np.array_equal(o1.view(np.uint32), o2.view(np.uint32))
 
 
-@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W4A4G128, W.W4A4])
+@pytest.mark.parametrize("scheme", [W.W2G128, W.W3G128, W.W4G128, W.W8G128, W.W4A4G128, W.W4A4, W.W4A4F6])
 def test_pack_domain_of_codes_and_zeros(scheme):
     """Boundary zero points (0 and 2^N - 1, with the extreme codes) pack
     exactly and the linear matches the oracle in those channels; a zero

@@ -214,3 +214,28 @@ def test_ulp_act_spacing():
     for act, nxt in (("fp16", lambda t: np.nextafter(t.astype(np.float16), np.float16(np.inf)).astype(np.float64)),):
         r = O.round_to_act(v, act)
         assert np.all(nxt(np.abs(r)) - np.abs(r) == TL.ulp_act(r, act))
+
+
+def test_f6_encoder_of_the_stagewise_check():
+    """The FP6 byte layout the stage-wise check compares against: every int4
+    value -7..7 decodes back from its 6-bit field by the e2m3 bit-field
+    definition ((-1)^s (1 + m/8) 2^(e-1), e > 0; 0 for e = m = 0), fields sit at
+    bits 6i..6i+5 of each 32-element group's 24 bytes, and the 8 bytes after
+    them are zero."""
+    from tests.stagewise import f6_bytes
+    rng = np.random.default_rng(4)
+    q = rng.integers(-7, 8, size=(3, 128))
+    q[0, :15] = np.arange(-7, 8)
+    b = f6_bytes(q)
+    assert b.shape == q.shape and b.dtype == np.uint8
+    for r in range(3):
+        for g in range(4):
+            grp = b[r, 32 * g:32 * g + 32]
+            assert not grp[24:].any()
+            bits = int.from_bytes(bytes(grp[:24]), "little")
+            for i in range(32):
+                f = (bits >> (6 * i)) & 63
+                s, e, m = f >> 5, (f >> 3) & 3, f & 7
+                v = 0.0 if e == 0 else (1 + m / 8) * 2.0 ** (e - 1)
+                assert e != 0 or m == 0
+                assert (-v if s else v) == q[r, 32 * g + i]
