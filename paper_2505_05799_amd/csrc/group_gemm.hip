@@ -109,7 +109,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   __shared__ int32_t s_cost[2][kMaxG];    // budget need, then tile cost
   __shared__ int32_t s_tiles[2][kMaxG];   // sliced output tiles, then queued tiles
   __shared__ int32_t s_order[2][kMaxG];   // group per rank
-  __shared__ int32_t s_ns[kMaxG];         // first super-tile per rank (one phase at a time)
+  __shared__ int32_t s_c1[2][kMaxG];      // unsliced tile cost
+  __shared__ int32_t s_cs[2][kMaxG];      // tile cost with the proposed slices
   __shared__ int32_t s_red[1025];
   __shared__ int64_t s_work[2][1024 / 64];
   __shared__ int64_t s_theta[2];          // slicing threshold per phase
@@ -162,16 +163,19 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     return q;
   };
 
-  // 1. the phase's work (tiles times unsliced tile cost, summed exactly) sets
-  //    the slicing threshold; then per group the proposed slices and, for the
-  //    budget pass, the partial-sum floats (capped at pfloats + 1, which no
-  //    budget admits) and the output tiles of every group that would be sliced
+  // 1. per group the unsliced tile cost (kept for the steps below); the
+  //    phase's work (tiles times that cost, summed exactly) sets the slicing
+  //    threshold; then per group the proposed slices and, for the budget
+  //    pass, the partial-sum floats (capped at pfloats + 1, which no budget
+  //    admits) and the output tiles of every group that would be sliced
   for (int ph = 0; ph < nphase; ++ph) {
     int64_t w = 0;
     for (int g = tid; g < G; g += blockDim.x) {
       const Geom q = geom(ph, g);
       const int tiles = q.mt * q.nt;
-      if (tiles > 0) w += (int64_t)tiles * tile_cost(q.bm, q.bn, q.nl, q.kd, q.kb * 128, 1, q.mt, q.nt);
+      const int32_t c = tiles > 0 ? tile_cost(q.bm, q.bn, q.nl, q.kd, q.kb * 128, 1, q.mt, q.nt) : 0;
+      s_c1[ph][g] = c;
+      w += (int64_t)tiles * c;
     }
     for (int d = 32; d > 0; d >>= 1) w += __shfl_xor(w, d, 64);
     if (lane == 0) s_work[ph][wave] = w;
@@ -183,22 +187,55 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     s_theta[tid] = work / nwg / kSplitShare;
   }
   lds_barrier();
-  for (int item = tid; item < nphase * G; item += blockDim.x) {
-    const int ph = item >= G, g = item - ph * G;
-    const int64_t theta = s_theta[ph];
+  // The slice rule of choose_split, evaluated by eight lanes per group: lane
+  // j prices j + 1 slices; the group takes the fewest slices whose tile cost
+  // is within theta, else the cheapest (the fewest slices among equals).
+  for (int base = 0; base < nphase * G; base += (int)blockDim.x / 8) {
+    const int item = base + tid / 8, s = (tid & 7) + 1;
+    const bool live = item < nphase * G;
+    const int ph = live && item >= G ? 1 : 0, g = live ? item - ph * G : 0;
     const Geom q = geom(ph, g);
-    const int sp = choose_split(q.bm, q.bn, q.nl, q.kd, q.kb, q.mt, q.nt, theta);
-    int32_t* r = rec_of(ph, g);
-    r[PF_EXPERT] = g;
-    r[PF_M] = q.m;
-    r[PF_CFG] = q.cfg;
-    r[PF_MTILES] = q.mt;
-    r[PF_NTILES] = q.nt;
-    r[PF_START] = 0;
-    const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
-    s_sp[ph][g] = (int8_t)sp;
-    s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
-    s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
+    const bool tiled = live && q.mt * q.nt > 0;
+    int smax = q.kb / kSplitMinKb;
+    smax = smax < 1 ? 1 : (smax > kSplitMax ? kSplitMax : smax);
+    const bool ok = tiled && s <= smax;
+    int32_t c = 0;
+    if (ok) c = s == 1 ? s_c1[ph][g] : tile_cost(q.bm, q.bn, q.nl, q.kd, (q.kb + s - 1) / s * 128, s, q.mt, q.nt);
+    int first = (ok && c <= s_theta[ph]) ? s : 64;
+    int64_t key = ok ? (((int64_t)c << 8) | s) : INT64_MAX;
+    for (int d = 1; d < 8; d <<= 1) {
+      first = min(first, __shfl_xor(first, d, 64));
+      const int64_t kk = __shfl_xor(key, d, 64);
+      key = kk < key ? kk : key;
+    }
+    // the cost of `first` slices, from the lane that priced it (every lane
+    // takes part in the shuffle)
+    const int32_t c_first = __shfl(c, (lane & ~7) + (first <= kSplitMax ? first - 1 : 0), 64);
+    if (live && s == 1) {
+      int sp = 1;
+      int32_t csp = s_c1[ph][g];
+      if (tiled) {
+        if (first <= kSplitMax) {
+          sp = first;
+          csp = c_first;
+        } else {
+          sp = (int)(key & 0xFF);
+          csp = (int32_t)(key >> 8);
+        }
+      }
+      int32_t* r = rec_of(ph, g);
+      r[PF_EXPERT] = g;
+      r[PF_M] = q.m;
+      r[PF_CFG] = q.cfg;
+      r[PF_MTILES] = q.mt;
+      r[PF_NTILES] = q.nt;
+      r[PF_START] = 0;
+      const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
+      s_sp[ph][g] = (int8_t)sp;
+      s_cs[ph][g] = csp;
+      s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
+      s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
+    }
   }
   lds_barrier();
   // 2. slices within the budgets, greedily in group order: a group is sliced
@@ -270,13 +307,14 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     }
   }
   lds_barrier();
-  // 3. per-tile cost estimate with the final slices, arrival counters cleared
+  // 3. per-tile cost with the final slices (priced in step 1), arrival
+  //    counters cleared
   for (int ph = 0; ph < nphase; ++ph) {
     for (int g = tid; g < G; g += blockDim.x) {
       const Geom q = geom(ph, g);
       const int sp = s_sp[ph][g];
       const int tiles = q.mt * q.nt * sp;
-      const int c = tiles ? tile_cost(q.bm, q.bn, q.nl, q.kd, (q.kb + sp - 1) / sp * 128, sp, q.mt, q.nt) : 0;
+      const int c = tiles ? (sp > 1 ? s_cs[ph][g] : s_c1[ph][g]) : 0;
       rec_of(ph, g)[PF_COST] = c;
       s_cost[ph][g] = c;
       s_tiles[ph][g] = tiles;
@@ -286,8 +324,27 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     for (int i = tid; i < s_used[ph]; i += blockDim.x) cnt[i] = 0;
   }
   lds_barrier();
-  // 4. rank the groups by decreasing tile cost (ties: lower group first); one
-  //    wavefront counts the groups ahead of one group
+  // 4. rank the groups by decreasing tile cost (ties: lower group first):
+  //    up to 256 groups one thread counts the groups ahead of one group,
+  //    beyond that one wavefront does
+  if (G <= 256) {
+    for (int item = tid; item < nphase * G; item += blockDim.x) {
+      const int ph = item >= G, g = item - ph * G;
+      int rank = -1;
+      if (s_tiles[ph][g] > 0) {
+        const int cg = s_cost[ph][g];
+        int ahead = 0;
+        for (int h = 0; h < G; ++h) {
+          const int ch = s_cost[ph][h];
+          ahead += s_tiles[ph][h] > 0 && ((ch > cg) || (ch == cg && h < g));
+        }
+        rank = ahead;
+        s_order[ph][rank] = g;
+        order[(int64_t)ph * G + rank] = g;
+      }
+      rec_of(ph, g)[PF_RANK] = rank;
+    }
+  } else
   for (int item = wave; item < nphase * G; item += nwave) {
     const int ph = item >= G, g = item - ph * G;
     int rank = -1;
@@ -308,23 +365,36 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     if (lane == 0) rec_of(ph, g)[PF_RANK] = rank;
   }
   lds_barrier();
-  // 5. super-tiles dealt to the XCD queues, 6. expanded to tile entries
+  // 5. super-tiles dealt to the XCD queues, 6. expanded to tile entries;
+  //    both phases at once (waves 8p .. 8p + 7 build the queues of phase p).
+  //    s_cost is free from here on: s_cost[p][r] holds the super-tile count
+  //    of rank r, then its exclusive prefix sum (first global super-tile).
+  auto dims = [&](int ph, int g, int* mt, int* ntv) {  // row tiles, channel tiles x slices
+    const Geom q = geom(ph, g);
+    *mt = q.mt;
+    *ntv = q.nt * s_sp[ph][g];
+  };
   for (int ph = 0; ph < nphase; ++ph) {
     const int ng = s_ng[ph];
     for (int r = ng + tid; r < G; r += blockDim.x) order[(int64_t)ph * G + r] = -1;
-    auto dims = [&](int g, int* mt, int* ntv) {  // row tiles, channel tiles x slices
-      const Geom q = geom(ph, g);
-      *mt = q.mt;
-      *ntv = q.nt * s_sp[ph][g];
-    };
     for (int r = tid; r < ng; r += blockDim.x) {
       int mt, ntv;
-      dims(s_order[ph][r], &mt, &ntv);
+      dims(ph, s_order[ph][r], &mt, &ntv);
       const SuperDims dd = plan_super_dims(mt, ntv);
-      s_ns[r] = (mt > 0 && ntv > 0) ? dd.nsm * dd.nsn : 0;
+      s_cost[ph][r] = (mt > 0 && ntv > 0) ? dd.nsm * dd.nsn : 0;
     }
-    lds_barrier();
-    const int S = block_scan(s_ns, ng, s_red);  // s_ns[r]: first global super-tile of rank r
+  }
+  lds_barrier();
+  int S_ph[2] = {0, 0};
+  for (int ph = 0; ph < nphase; ++ph) S_ph[ph] = block_scan(s_cost[ph], s_ng[ph], s_red);
+  if (tid < nphase) {
+    if ((S_ph[tid] + kXcd - 1) / kXcd > qcap) misc[4] = 1;  // cannot happen with the host's capacity bound
+    misc[2 + tid] = s_ng[tid];
+  }
+  if (wave < nphase * kXcd) {
+    const int ph = wave / kXcd, x = wave % kXcd;
+    const int ng = s_ng[ph], S = S_ph[ph];
+    const int32_t* s_ns = s_cost[ph];
     // super-tile u -> (rank, index within the group)
     auto locate = [&](int u, int* g, int* st) {
       int lo = 0, hi = ng;
@@ -337,83 +407,77 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     };
     int32_t* ent = plan + PL.ent + (int64_t)ph * kXcd * qcap * 3;
     int32_t* ctr = plan + PL.ctr + (int64_t)ph * kXcd * 4;
-    if (tid == 0 && (S + kXcd - 1) / kXcd > qcap) misc[4] = 1;  // cannot happen with the host's capacity bound
-    // deal super-tile u to queue u % kXcd, position u / kXcd; one wavefront per
-    // queue forms the exclusive prefix sums of the entry sizes (each entry's
-    // first tile) and expands each entry into its tiles
+    // deal super-tile u to queue u % kXcd, position u / kXcd; the queue's
+    // wavefront forms the exclusive prefix sums of the entry sizes (each
+    // entry's first tile) and expands each entry into its tiles
     int32_t* flat = plan + PL.flat + (int64_t)ph * kXcd * fcap * 4;
-    if (wave < kXcd) {
-      const int x = wave;
-      int n = S / kXcd + (x < S % kXcd ? 1 : 0);
-      n = n < qcap ? n : qcap;
-      int32_t* q = ent + (int64_t)x * qcap * 3;
-      int run = 0;
-      for (int c0 = 0; c0 < n; c0 += 64) {
-        const int i = c0 + lane;
-        int g = 0, st = 0, v = 0, mt = 0, ntv = 0;
-        if (i < n) {
-          locate(i * kXcd + x, &g, &st);
-          dims(g, &mt, &ntv);
+    int n = S / kXcd + (x < S % kXcd ? 1 : 0);
+    n = n < qcap ? n : qcap;
+    int32_t* q = ent + (int64_t)x * qcap * 3;
+    int run = 0;
+    for (int c0 = 0; c0 < n; c0 += 64) {
+      const int i = c0 + lane;
+      int g = 0, st = 0, v = 0, mt = 0, ntv = 0;
+      if (i < n) {
+        locate(i * kXcd + x, &g, &st);
+        dims(ph, g, &mt, &ntv);
+        const SuperDims dd = plan_super_dims(mt, ntv);
+        const int sni = div_small(st, dd.nsm), smi = st - sni * dd.nsm;
+        v = min(dd.sm, mt - smi * dd.sm) * min(dd.sn, ntv - sni * dd.sn);
+      }
+      int incl = v;
+      for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += t;
+      }
+      const int first = run + incl - v;
+      run += __shfl(incl, 63, 64);
+      // this lane's entry: its record, and what expanding it takes
+      int w0 = 0, off_e = 0, m_g = 0, mi0 = 0, ni0 = 0, em = 1, inv = 65536, size = 0;
+      if (i < n) {
+        q[(int64_t)i * 3 + 0] = g;
+        q[(int64_t)i * 3 + 1] = st;
+        q[(int64_t)i * 3 + 2] = first;
+        if (first + v <= fcap) {
           const SuperDims dd = plan_super_dims(mt, ntv);
           const int sni = div_small(st, dd.nsm), smi = st - sni * dd.nsm;
-          v = min(dd.sm, mt - smi * dd.sm) * min(dd.sn, ntv - sni * dd.sn);
-        }
-        int incl = v;
-        for (int d = 1; d < 64; d <<= 1) {
-          const int t = __shfl_up(incl, d, 64);
-          if (lane >= d) incl += t;
-        }
-        const int first = run + incl - v;
-        run += __shfl(incl, 63, 64);
-        // this lane's entry: its record, and what expanding it takes
-        int w0 = 0, off_e = 0, m_g = 0, mi0 = 0, ni0 = 0, em = 1, inv = 65536, size = 0;
-        if (i < n) {
-          q[(int64_t)i * 3 + 0] = g;
-          q[(int64_t)i * 3 + 1] = st;
-          q[(int64_t)i * 3 + 2] = first;
-          if (first + v <= fcap) {
-            const SuperDims dd = plan_super_dims(mt, ntv);
-            const int sni = div_small(st, dd.nsm), smi = st - sni * dd.nsm;
-            em = min(dd.sm, mt - smi * dd.sm);
-            inv = div_small(65536 + em - 1, em);  // t / em = (t * inv) >> 16 for t < 64, em <= 8
-            mi0 = smi * dd.sm;
-            ni0 = sni * dd.sn;
-            w0 = tile_word0(g, pick_cfg(s_m[g], s_kd[ph][g], raw_m >= 0 ? 0 : ph), s_kd[ph][g], s_sp[ph][g]);
-            off_e = s_off[g];
-            m_g = s_m[g];
-            size = v;
-          } else {
-            misc[4] = 1;  // cannot happen with the host's capacity bound
-          }
-        }
-        // The chunk's entries are expanded one at a time by the whole
-        // wavefront (lane t writes the entry's tile t, row tile fastest, the
-        // order of super_tile_pos), so that every store is contiguous; the
-        // entry's fields come from its lane's registers.
-        const int cnt = n - c0 < 64 ? n - c0 : 64;
-        for (int j = 0; j < cnt; ++j) {
-          const int sz = __builtin_amdgcn_readlane(size, j);
-          if (sz == 0) continue;
-          const int fj = __builtin_amdgcn_readlane(first, j);
-          const int emj = __builtin_amdgcn_readlane(em, j), invj = __builtin_amdgcn_readlane(inv, j);
-          const int w0j = __builtin_amdgcn_readlane(w0, j), offj = __builtin_amdgcn_readlane(off_e, j);
-          const int mgj = __builtin_amdgcn_readlane(m_g, j);
-          const int mi0j = __builtin_amdgcn_readlane(mi0, j), ni0j = __builtin_amdgcn_readlane(ni0, j);
-          if (lane < sz) {
-            const int b2 = (int)(((uint32_t)lane * (uint32_t)invj) >> 16), a2 = lane - b2 * emj;
-            reinterpret_cast<int4*>(flat + ((int64_t)x * fcap + fj) * 4)[lane] =
-                make_int4(w0j, (mi0j + a2) | ((ni0j + b2) << 16), offj, mgj);
-          }
+          em = min(dd.sm, mt - smi * dd.sm);
+          inv = div_small(65536 + em - 1, em);  // t / em = (t * inv) >> 16 for t < 64, em <= 8
+          mi0 = smi * dd.sm;
+          ni0 = sni * dd.sn;
+          w0 = tile_word0(g, pick_cfg(s_m[g], s_kd[ph][g], raw_m >= 0 ? 0 : ph), s_kd[ph][g], s_sp[ph][g]);
+          off_e = s_off[g];
+          m_g = s_m[g];
+          size = v;
+        } else {
+          misc[4] = 1;  // cannot happen with the host's capacity bound
         }
       }
-      if (lane == 0) {
-        ctr[x * 4 + 0] = 0;
-        ctr[x * 4 + 1] = run;
-        ctr[x * 4 + 2] = n;
+      // The chunk's entries are expanded one at a time by the whole
+      // wavefront (lane t writes the entry's tile t, row tile fastest, the
+      // order of super_tile_pos), so that every store is contiguous; the
+      // entry's fields come from its lane's registers.
+      const int cnt = n - c0 < 64 ? n - c0 : 64;
+      for (int j = 0; j < cnt; ++j) {
+        const int sz = __builtin_amdgcn_readlane(size, j);
+        if (sz == 0) continue;
+        const int fj = __builtin_amdgcn_readlane(first, j);
+        const int emj = __builtin_amdgcn_readlane(em, j), invj = __builtin_amdgcn_readlane(inv, j);
+        const int w0j = __builtin_amdgcn_readlane(w0, j), offj = __builtin_amdgcn_readlane(off_e, j);
+        const int mgj = __builtin_amdgcn_readlane(m_g, j);
+        const int mi0j = __builtin_amdgcn_readlane(mi0, j), ni0j = __builtin_amdgcn_readlane(ni0, j);
+        if (lane < sz) {
+          const int b2 = (int)(((uint32_t)lane * (uint32_t)invj) >> 16), a2 = lane - b2 * emj;
+          reinterpret_cast<int4*>(flat + ((int64_t)x * fcap + fj) * 4)[lane] =
+              make_int4(w0j, (mi0j + a2) | ((ni0j + b2) << 16), offj, mgj);
+        }
       }
     }
-    if (tid == 0) misc[2 + ph] = ng;
-    lds_barrier();
+    if (lane == 0) {
+      ctr[x * 4 + 0] = 0;
+      ctr[x * 4 + 1] = run;
+      ctr[x * 4 + 2] = n;
+    }
   }
   if (nphase == 1) {  // single-linear mode: the second phase is empty
     int32_t* ctr = plan + PL.ctr + (int64_t)kXcd * 4;
