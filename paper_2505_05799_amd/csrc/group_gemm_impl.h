@@ -208,6 +208,19 @@ template <int KD> __device__ inline u32x4 load_step(const uint8_t* p, int j) {
 
 // Wait until at most N vector-memory loads of this wavefront are outstanding
 // (loads complete in issue order), leaving LDS and export counters alone.
+// An empty statement that reads a value: the compiler waits for the loads of
+// its registers before it.
+__device__ inline void touch(uint32_t v) { asm volatile("" ::"v"(v)); }
+__device__ inline void touch(const u32x2& v) { asm volatile("" ::"v"(v)); }
+__device__ inline void touch(const u32x4& v) { asm volatile("" ::"v"(v)); }
+template <int KD> __device__ inline void touch_raw(const Raw<KD>& r) {
+  if constexpr (KD == K_W2G) touch(r.d);
+  else if constexpr (KD == K_W3G) { touch(r.d[0]); touch(r.d[1]); touch(r.d[2]); }
+  else if constexpr (KD == K_W4A4F6) { touch(r.d0); touch(r.d1); }
+  else if constexpr (KD == K_W8A8 || KD == K_F8A8) { touch(r.d[0]); touch(r.d[1]); }
+  else touch(r.d[0]);
+}
+
 template <int N> __device__ inline void wait_vmem() {
   static_assert(N >= 0 && N < 64, "vmcnt is six bits");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
@@ -635,8 +648,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // stage buffer (1.5% on the gate|up launch of the Qwen2-shaped block);
   // 16-bit-activation gate/up tiles of more rows lose a little (their two
   // weight sets already fill the registers).
-  // Slot s of the weight registers serves k block kb + s and is refilled
-  // right after its MFMAs (no register copy).  The per-row values of the
+  // Slot s of the weight registers serves k block kb + s: slot 0 is refilled
+  // right after its MFMAs (for the next step), slot 1 at the top of the step,
+  // after the stage loads (no register copy).  The per-row values of the
   // second block sit at rsum[buf][64..], so tiles with them stop at 64 rows.
   constexpr bool KBI_FITS = !streamed<KD>() && BM * RB * 2 <= STAGE_BYTES && (!RSLOAD || BM <= 64);
   constexpr int KBI = (KBI_FITS && (PHASE == 1 || (BM <= 32 && LB <= 16) || INT)) ? 2 : 1;
@@ -687,7 +701,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     }
   }
   load_group(std::integral_constant<int, 0>{}, kb0, false);
-  if constexpr (KBI == 2) load_group(std::integral_constant<int, 1>{}, kb0 + 1, kb0 + 1 >= kb1);
   if constexpr (streamed<KD>()) {
 #pragma unroll
     for (int j = 0; j < J; ++j) load_steps(kb0, false, j);
@@ -698,6 +711,19 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   for (int kb = kb0, it = 0; kb < kb1; kb += KBI, ++it) {
     const int cur = it & 1;
     const bool more = kb + KBI < kb1;
+    // The weights of the step's first k block (loaded a step ago) are waited
+    // for here, before the stage loads below go out: the compiler does not
+    // count those direct loads, so a wait it placed after them for an older
+    // load would wait for them too (vector-memory loads complete in order).
+    if constexpr (!streamed<KD>()) {
+#pragma unroll
+      for (int l = 0; l < NL; ++l)
+#pragma unroll
+        for (int nf = 0; nf < NF; ++nf) {
+          touch_raw<KD>(raw[0][l][nf]);
+          if constexpr (GMETA) touch(meta[0][l][nf]);
+        }
+    }
 #pragma unroll
     for (int sb = 0; sb < KBI; ++sb) {
       if (kb + KBI + sb < kb1) {
@@ -708,12 +734,21 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    // one k block (kbs = kb + SL) of the step
-    auto kstep = [&](auto S) {
+    // two k blocks per step: the second block's weights, used after the first
+    // block's MFMAs
+    if constexpr (KBI == 2) {
+      load_group(std::integral_constant<int, 1>{}, kb + 1, kb + 1 >= kb1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // one k block (kbs = kb + SL) of the step; an inactive block (the second
+    // one past the last k block) issues only what every path through the step
+    // issues, so the compiler's wait counts need no drain where paths join
+    auto kstep = [&](auto S, bool active) {
     constexpr int SL = decltype(S)::value;
     const int kbs = kb + SL;
     const int ra = SL * BM;   // first staged row of this k block
     const int rs0 = SL * 64;  // its per-row values
+    if (active) {
     Raw<KD> rw[NL][NF];
     uint32_t bz[NL][NF];
     float zf[NL][NF];
@@ -939,19 +974,15 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       }
     }
     }
-    if constexpr (KBI == 2) {
-      // this slot's registers are free: prefetch the k block one step ahead
+    }  // active
+    if constexpr (KBI == 2 && SL == 0) {
+      // the first slot's registers are free: prefetch the next step's first block
       load_group(S, kbs + KBI, kbs + KBI >= kb1);
       __builtin_amdgcn_sched_barrier(0);
     }
     };  // kstep
-    kstep(std::integral_constant<int, 0>{});
-    if constexpr (KBI == 2) {
-      if (kb + 1 < kb1) kstep(std::integral_constant<int, 1>{});
-    }
-    // Last k block: claim the next tile and bring its entry into LDS (the
-    // entry is read at the top of the tile loop, after the final barrier).
-    if (!more && tid == 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
+    kstep(std::integral_constant<int, 0>{}, true);
+    if constexpr (KBI == 2) kstep(std::integral_constant<int, 1>{}, kb + 1 < kb1);
     // The next stages have landed once no more than the weight prefetch is
     // outstanding (vector-memory loads complete in issue order; when more
     // steps follow, every k block of this one issued its prefetch).
@@ -959,6 +990,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     else wait_vmem<0>();
     lds_barrier();
   }
+
+  // Claim the next tile and bring its entry into LDS (read at the top of the
+  // tile loop, after the final barrier).  Its loads are waited for before the
+  // next barrier of the split-K hand-off or the epilogue.  Claiming here and
+  // not inside the k loop keeps the claim's pending loads out of the loop: the
+  // compiler would otherwise drain every outstanding load, the prefetch of the
+  // next k blocks included, at the top of each step.
+  if (tid == 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
 
   // ---- split-K: partial sums of this slice; the last slice to arrive adds
   // all slices' partials in slice order and runs the epilogue
@@ -1076,6 +1115,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             hl[(r + i) * HP + c] = f32_to_act<ACT>(silu_f32(outv(0, nf, mf, i, rs)) * outv(1, nf, mf, i, rs));
         }
       }
+      wait_vmem<0>();  // the next tile's entry has landed
       lds_barrier();
       constexpr int CH = BN / 8;  // 16-byte pieces of a tile row
       int nch = (N - nt * BN) / 8;
@@ -1137,6 +1177,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
             for (int i = 0; i < 4; ++i) fl[(r + i - pass * RP) * FP + c] = outv(0, nf, mf, i, rs) * gwv[i];
           }
         }
+        if (pass == 0) wait_vmem<0>();  // the next tile's entry has landed
         lds_barrier();
         for (int idx = tid; idx < RP * CH; idx += kThreads) {
           const int r = idx / CH, c = idx % CH;
@@ -1179,6 +1220,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     if (full) epilogue(std::false_type{});
     else epilogue(std::true_type{});
   }
+  if constexpr (PHASE == kPhaseRaw) wait_vmem<0>();  // the next tile's entry (no barrier in this epilogue)
   __syncthreads();  // the next tile rewrites rowsrc and the stages
 }
 
