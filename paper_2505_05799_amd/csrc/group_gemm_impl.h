@@ -336,6 +336,9 @@ struct __align__(16) Smem {
   int32_t qtotal[kXcd];          // tiles per XCD queue
   int32_t qi;                    // queues tried so far by this workgroup
   int32_t last;                  // split-K: this workgroup finishes the output tile
+  int32_t spec;                  // index claimed ahead on queue qi, or -1
+  int32_t cur_idx;               // queue index of the tile in progress
+  float wsc[512];                // per-channel weight scales of the tile's channels (a8/a4, FP8, FP6)
 };
 
 // Tile queues of one phase, rebuilt from the kernel arguments where needed so
@@ -434,13 +437,13 @@ template <bool UP = false> __device__ inline void lds_dma16(const uint8_t* base,
 // Claim the next tile and load its entry straight into sm.entry (thread 0;
 // the caller waits for the load with its vector-memory count), or mark the
 // end with group -1.  The first claim of a workgroup uses a plain load.
-template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& sm) {
+template <bool DMA> __device__ inline void claim_from(const TileQueue& Q, Smem& sm, int idx) {
   int qi = sm.qi;
-  int idx = pop_start(Q, sm, qi);
   while (qi < kXcd) {
     const int x = (Q.x0 + qi) % kXcd;
     if (idx < sm.qtotal[x]) {
       sm.qi = qi;
+      sm.cur_idx = idx;
       if constexpr (DMA) {
         const uint32_t lds = (uint32_t)reinterpret_cast<uintptr_t>((lds_ptr_t)&sm.entry);
         lds_dma16(reinterpret_cast<const uint8_t*>(Q.flat), (uint32_t)(((int64_t)x * Q.fcap + idx) * 16),
@@ -456,6 +459,14 @@ template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& 
   sm.qi = qi;
   sm.entry.x = -1;  // only the group field is read when no tile is left
 }
+template <bool DMA> __device__ inline void claim_next(const TileQueue& Q, Smem& sm) {
+  claim_from<DMA>(Q, sm, pop_start(Q, sm, sm.qi));
+}
+// A tile started while its queue still holds more than this many unclaimed
+// tiles claims the next one at its start (the claim's round trips then hide
+// behind the tile); near a queue's end the claim waits for the tile's end, so
+// that no tile sits reserved by a busy workgroup while others run out.
+constexpr int kClaimAheadMargin = 256;
 
 // sub: sub-stage of the buffer (tiles that stage two k blocks per step put
 // the second one's BM rows after the first one's)
@@ -565,6 +576,12 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 
   // ---- per-row data: activation source row (rows past the group repeat its
   // last row), output row, activation scale, router gate weight
+  int spec = -1;
+  if (tid == 0 && sm.qi < kXcd) {
+    const TileQueue Q = tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE);
+    const int x = (Q.x0 + sm.qi) % kXcd;
+    if (sm.qtotal[x] - sm.cur_idx > kClaimAheadMargin) spec = atomicAdd(&Q.ctr[x * 4], 1);
+  }
   if (tid < BM) {
     const int m0 = row0 + tid;
     const int m = m0 < m_g ? m0 : m_g - 1;
@@ -596,7 +613,15 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     sm.rowgw[tid] = gw;
     sm.rowscale[tid] = sc;
   }
+  if constexpr (INT && !GSC) {  // the channels' weight scales, for the epilogue
+    for (int i = tid; i < NL * BN; i += kThreads) {
+      const int l = i / BN, c = i - l * BN;
+      const int n = nt * BN + c;
+      sm.wsc[i] = n < N ? lins[l]->wscale[n] : 0.f;
+    }
+  }
   const int64_t row_bytes = MX ? (int64_t)K / 2 : (int64_t)K * (INT ? 1 : 2);
+  if (tid == 0) sm.spec = spec;
   __syncthreads();
   StageOffs<RB, BM> soffs;
   stage_offsets<RB, BM>(soffs, sm, row_bytes, wave, lane);
@@ -648,9 +673,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   // stage buffer (1.5% on the gate|up launch of the Qwen2-shaped block);
   // 16-bit-activation gate/up tiles of more rows lose a little (their two
   // weight sets already fill the registers).
-  // Slot s of the weight registers serves k block kb + s: slot 0 is refilled
-  // right after its MFMAs (for the next step), slot 1 at the top of the step,
-  // after the stage loads (no register copy).  The per-row values of the
+  // Slot s of the weight registers serves k block kb + s and is refilled
+  // right after its MFMAs, for the next step (no register copy).  The per-row values of the
   // second block sit at rsum[buf][64..], so tiles with them stop at 64 rows.
   constexpr bool KBI_FITS = !streamed<KD>() && BM * RB * 2 <= STAGE_BYTES && (!RSLOAD || BM <= 64);
   constexpr int KBI = (KBI_FITS && (PHASE == 1 || (BM <= 32 && LB <= 16) || INT)) ? 2 : 1;
@@ -701,6 +725,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     }
   }
   load_group(std::integral_constant<int, 0>{}, kb0, false);
+  if constexpr (KBI == 2) load_group(std::integral_constant<int, 1>{}, kb0 + 1, kb0 + 1 >= kb1);
   if constexpr (streamed<KD>()) {
 #pragma unroll
     for (int j = 0; j < J; ++j) load_steps(kb0, false, j);
@@ -711,7 +736,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   for (int kb = kb0, it = 0; kb < kb1; kb += KBI, ++it) {
     const int cur = it & 1;
     const bool more = kb + KBI < kb1;
-    // The weights of the step's first k block (loaded a step ago) are waited
+    // The weights of the step (prefetched during the previous one) are waited
     // for here, before the stage loads below go out: the compiler does not
     // count those direct loads, so a wait it placed after them for an older
     // load would wait for them too (vector-memory loads complete in order).
@@ -722,6 +747,10 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         for (int nf = 0; nf < NF; ++nf) {
           touch_raw<KD>(raw[0][l][nf]);
           if constexpr (GMETA) touch(meta[0][l][nf]);
+          if constexpr (KBI == 2) {
+            touch_raw<KD>(raw[KBI - 1][l][nf]);
+            if constexpr (GMETA) touch(meta[KBI - 1][l][nf]);
+          }
         }
     }
 #pragma unroll
@@ -734,12 +763,6 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     // every weight load below is issued after the stage (see wait_vmem)
     asm volatile("" ::: "memory");
     __builtin_amdgcn_sched_barrier(0);
-    // two k blocks per step: the second block's weights, used after the first
-    // block's MFMAs
-    if constexpr (KBI == 2) {
-      load_group(std::integral_constant<int, 1>{}, kb + 1, kb + 1 >= kb1);
-      __builtin_amdgcn_sched_barrier(0);
-    }
     // one k block (kbs = kb + SL) of the step; an inactive block (the second
     // one past the last k block) issues only what every path through the step
     // issues, so the compiler's wait counts need no drain where paths join
@@ -975,8 +998,8 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     }
     }
     }  // active
-    if constexpr (KBI == 2 && SL == 0) {
-      // the first slot's registers are free: prefetch the next step's first block
+    if constexpr (KBI == 2) {
+      // this slot's registers are free: prefetch its block of the next step
       load_group(S, kbs + KBI, kbs + KBI >= kb1);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -991,13 +1014,18 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     lds_barrier();
   }
 
-  // Claim the next tile and bring its entry into LDS (read at the top of the
-  // tile loop, after the final barrier).  Its loads are waited for before the
-  // next barrier of the split-K hand-off or the epilogue.  Claiming here and
-  // not inside the k loop keeps the claim's pending loads out of the loop: the
-  // compiler would otherwise drain every outstanding load, the prefetch of the
-  // next k blocks included, at the top of each step.
-  if (tid == 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
+  // Claim the next tile (or take the one claimed ahead at the start of this
+  // one) and bring its entry into LDS (read at the top of the tile loop, after
+  // the final barrier).  Its loads are waited for before the next barrier of
+  // the split-K hand-off or the epilogue.  Claiming here and not inside the k
+  // loop keeps the claim's pending loads out of the loop: the compiler would
+  // otherwise drain every outstanding load, the prefetch of the next k blocks
+  // included, at the top of each step.
+  if (tid == 0) {
+    const TileQueue Q = tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE);
+    if (sm.spec >= 0) claim_from<true>(Q, sm, sm.spec);
+    else claim_next<true>(Q, sm);
+  }
 
   // ---- split-K: partial sums of this slice; the last slice to arrive adds
   // all slices' partials in slice order and runs the epilogue
@@ -1080,7 +1108,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
         cs[l][nf] = 1.f;
-        if constexpr (INT && !GSC) cs[l][nf] = nf < nvalid ? lins[l]->wscale[16 * (nb0 + nf) + li] : 0.f;
+        if constexpr (INT && !GSC) cs[l][nf] = sm.wsc[l * BN + (wave * NF + nf) * 16 + li];
         if constexpr (WONLY) cs[l][nf] = s_prev[l][nf];
       }
     // value of accumulator (l, nf, mf, i) after the scheme's scales
@@ -1255,7 +1283,7 @@ __global__ void __launch_bounds__(kThreads, 2) group_gemm_kernel(GemmArgs a) {
   {
     const TileQueue Q = tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE);
     if (threadIdx.x < kXcd) sm.qtotal[threadIdx.x] = min(Q.ctr[threadIdx.x * 4 + 1], a.fcap);
-    if (threadIdx.x == 0) sm.qi = 0;
+    if (threadIdx.x == 0) { sm.qi = 0; sm.cur_idx = 0; }
     __syncthreads();
     if (threadIdx.x == 0) claim_next<false>(Q, sm);
     __syncthreads();
