@@ -148,15 +148,15 @@ template <int ACT> __device__ inline uint16_t f32_to_act(float f) {
     return __builtin_bit_cast(uint16_t, (_Float16)f);
 }
 
-// SiLU(g) = g / (1 + e^-g) with e^-g = 2^t, t = -g log2(e) rounded to fp32 and
-// capped at 126 (a large negative g then yields a tiny finite value instead of
-// inf * 0).  The rounding of t moves e^-g by at most |t| 2^-24 relatively,
-// which with the exp2 and reciprocal instructions (about one ulp each) keeps
-// the result within 2^-16 of the exact value for |g| < 64: far below the one
-// rounding of h to the 16-bit activation dtype that follows.
-__device__ inline float silu_f32(float g) {
-  const float e = __builtin_amdgcn_exp2f(fminf(g * -1.44269502162933349609375f, 126.0f));
-  return g * __builtin_amdgcn_rcpf(1.0f + e);
+// SiLU(g) = g / (1 + e^-g), formed as g * rcp(1 + e^-g) with e^-g = 2^t,
+// t = -g log2(e) rounded to fp32 and capped at 126 (a large negative g then
+// yields a tiny finite value instead of inf * 0).  The rounding of t moves
+// e^-g by at most |t| 2^-24 relatively, which with the exp2 and reciprocal
+// instructions (about one ulp each) keeps the result within 2^-16 of the exact
+// value for |g| < 64: far below the one rounding of h to the 16-bit
+// activation dtype that follows.  silu_exp(g) = e^-g.
+__device__ inline float silu_exp(float g) {
+  return __builtin_amdgcn_exp2f(fminf(g * -1.44269502162933349609375f, 126.0f));
 }
 
 // ------------------------------------------------------- weight operands
@@ -1130,17 +1130,28 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
       constexpr int HP = BN + 8;  // row pitch in elements (16-byte pad: reads of 16 rows hit distinct banks)
       static_assert(BM * HP * 2 <= 2 * STAGE_BYTES, "h tile fits the stage buffers");
       uint16_t* hl = reinterpret_cast<uint16_t*>(&sm.act[0][0]);
+      // (channels past N are computed too, without a branch per fragment,
+      // and never stored; each fragment's four values go through the SiLU in
+      // step, so that four independent chains hide each other's latencies)
 #pragma unroll
       for (int mf = 0; mf < MF; ++mf) {
         const int r = mf * 16 + 4 * q;
         const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
 #pragma unroll
         for (int nf = 0; nf < NF; ++nf) {
-          if (nf >= nvalid) continue;
           const int c = (wave * NF + nf) * 16 + li;
+          float gv[4], uv[4], ev[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            hl[(r + i) * HP + c] = f32_to_act<ACT>(silu_f32(outv(0, nf, mf, i, rs)) * outv(1, nf, mf, i, rs));
+          for (int i = 0; i < 4; ++i) {
+            gv[i] = outv(0, nf, mf, i, rs);
+            uv[i] = outv(1, nf, mf, i, rs);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ev[i] = silu_exp(gv[i]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ev[i] = __builtin_amdgcn_rcpf(1.0f + ev[i]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) hl[(r + i) * HP + c] = f32_to_act<ACT>((gv[i] * ev[i]) * uv[i]);
         }
       }
       wait_vmem<0>();  // the next tile's entry has landed
@@ -1198,8 +1209,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
           const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
 #pragma unroll
-          for (int nf = 0; nf < NF; ++nf) {
-            if (nf >= nvalid) continue;
+          for (int nf = 0; nf < NF; ++nf) {  // (channels past N: written, never stored)
             const int c = (wave * NF + nf) * 16 + li;
 #pragma unroll
             for (int i = 0; i < 4; ++i) fl[(r + i - pass * RP) * FP + c] = outv(0, nf, mf, i, rs) * gwv[i];
