@@ -970,12 +970,15 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         // Software pipeline of the activation fragments: two LDS reads ahead,
         // then the MFMAs of one fragment and the read of the fragment two
         // places further, so an MFMA group never waits for a read issued just
-        // before it.
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        // before it (streamed kinds: per MFMA step; the others over all steps
+        // of the k block, below).
+        if constexpr (streamed<KD>()) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-        for (int mf = 0; mf < MF; ++mf) {
-          __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
-          if (mf + 2 < MF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int mf = 0; mf < MF; ++mf) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
+            if (mf + 2 < MF) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
         }
       } else {
         OpT af[MF];
@@ -994,6 +997,17 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         // step j's registers are free: refill them with step j of the next block
         load_steps(kb + 1, !more, j);
         __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if constexpr (HOLD_W && !streamed<KD>()) {
+      // the activation fragments of all MFMA steps of the k block in one
+      // pipeline, three reads ahead, with no drain between steps
+      constexpr int T = J * MF, LA = 3;
+      __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, NL * NF, 0);
+        if (t + LA < T) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
     }
     }
