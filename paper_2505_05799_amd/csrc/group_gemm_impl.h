@@ -623,6 +623,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
   const int64_t row_bytes = MX ? (int64_t)K / 2 : (int64_t)K * (INT ? 1 : 2);
   if (tid == 0) sm.spec = spec;
   __syncthreads();
+  // the tile after this one, claimed ahead: its entry comes into LDS now (every
+  // thread has read this tile's entry before the barrier above)
+  if (tid == 0 && spec >= 0) claim_from<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm, spec);
   StageOffs<RB, BM> soffs;
   stage_offsets<RB, BM>(soffs, sm, row_bytes, wave, lane);
   // row sums of the tile's activation rows per k block (bias-dequantized
@@ -970,9 +973,9 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         // Software pipeline of the activation fragments: two LDS reads ahead,
         // then the MFMAs of one fragment and the read of the fragment two
         // places further, so an MFMA group never waits for a read issued just
-        // before it (streamed kinds: per MFMA step; the others over all steps
-        // of the k block, below).
-        if constexpr (streamed<KD>()) {
+        // before it (16-bit MFMA kinds: per MFMA step; the integer kinds over
+        // all steps of the k block, below).
+        if constexpr (!INT) {
           __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
           for (int mf = 0; mf < MF; ++mf) {
@@ -999,9 +1002,10 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    if constexpr (HOLD_W && !streamed<KD>()) {
+    if constexpr (HOLD_W && INT) {
       // the activation fragments of all MFMA steps of the k block in one
-      // pipeline, three reads ahead, with no drain between steps
+      // pipeline, three reads ahead, with no drain between steps (with the
+      // weight decode of 16-bit MFMA kinds in flight too, the fp16 kernel spilled)
       constexpr int T = J * MF, LA = 3;
       __builtin_amdgcn_sched_group_barrier(0x100, LA, 0);
 #pragma unroll
@@ -1028,18 +1032,14 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
     lds_barrier();
   }
 
-  // Claim the next tile (or take the one claimed ahead at the start of this
-  // one) and bring its entry into LDS (read at the top of the tile loop, after
-  // the final barrier).  Its loads are waited for before the next barrier of
-  // the split-K hand-off or the epilogue.  Claiming here and not inside the k
-  // loop keeps the claim's pending loads out of the loop: the compiler would
+  // Claim the next tile, unless it was claimed ahead at the start of this one,
+  // and bring its entry into LDS (read at the top of the tile loop, after the
+  // final barrier).  Its loads are waited for before the next barrier of the
+  // split-K hand-off or the epilogue.  Claiming here and not inside the k loop
+  // keeps the claim's pending loads out of the loop: the compiler would
   // otherwise drain every outstanding load, the prefetch of the next k blocks
   // included, at the top of each step.
-  if (tid == 0) {
-    const TileQueue Q = tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE);
-    if (sm.spec >= 0) claim_from<true>(Q, sm, sm.spec);
-    else claim_next<true>(Q, sm);
-  }
+  if (tid == 0 && sm.spec < 0) claim_next<true>(tile_queue(a, PHASE == kPhaseRaw ? 0 : PHASE), sm);
 
   // ---- split-K: partial sums of this slice; the last slice to arrive adds
   // all slices' partials in slice order and runs the epilogue
