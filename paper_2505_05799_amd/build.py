@@ -59,10 +59,21 @@ def build(jobs: int | None = None, verbose: bool = False) -> str:
 
     def compile_one(so):
         s, o = so
-        return _run([hipcc, *HIPCC_FLAGS, "-c", s, "-o", o])
+        # the Group-GEMM translation units report their register use
+        extra = ["-Rpass-analysis=kernel-resource-usage"] if os.path.basename(s).startswith("gg_") else []
+        return _run([hipcc, *HIPCC_FLAGS, *extra, "-c", s, "-o", o])
 
     with ThreadPoolExecutor(jobs) as ex:
         logs = list(ex.map(compile_one, zip(srcs, objs)))
+    # A persistent Group-GEMM kernel that spills VGPRs runs far slower than its
+    # register budget allows: say so loudly (the build still succeeds).
+    for s, l in zip(srcs, logs):
+        for line in l.splitlines():
+            if "VGPRs Spill:" in line:
+                n = int(line.split("VGPRs Spill:")[1].split()[0])
+                if n > 0:
+                    print(f"warning: {os.path.basename(s)} spills {n} VGPRs", file=sys.stderr)
+    logs = ["\n".join(x for x in l.splitlines() if "remark:" not in x and "-Rpass-analysis" not in x) for l in logs]
     tmp = LIB + ".tmp"
     _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs])
     os.replace(tmp, LIB)
