@@ -1,4 +1,4 @@
-"""Hardware-aware bit-width allocation (Sec. 3, Eq. 3-7).
+"""Hardware-aware bit-width allocation (Sec. 4.2, Eq. 3-7).
 
 For one MoE block, pick a scheme for every linear block (expert i, linear j)
 from a candidate set S to minimize L^r * T^(1-r) subject to the packed weight

@@ -1,4 +1,4 @@
-"""Tile costs and the runtime model of the allocator (Sec. 3.2, runtime cost
+"""Tile costs and the runtime model of the allocator (Sec. 4.2.2, runtime cost
 modelling).
 
 The paper decomposes each linear block into tiles, profiles the cost c_t of a
@@ -22,6 +22,7 @@ c_t(K) = a + b * K / 128.  The table is stored as JSON beside this module.
 from __future__ import annotations
 
 import argparse
+import heapq
 import json
 import math
 import os
@@ -38,6 +39,8 @@ N_CFG = 4
 BM = (16, 32, 64, 128)
 BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][configuration]
 P_SLOTS = 512                                        # persistent grid: 2 workgroups x 256 CUs
+LAUNCH_NS = 6600.0        # an empty persistent Group-GEMM launch (measured on MI355X)
+SLICE_NS = 4000.0         # a sliced tile's partial-sum hand-off (3-6 us measured)
 
 
 def pick_cfg(m: int, scheme, phase: int = 0) -> int:
@@ -90,6 +93,52 @@ class CostTable:
             out[0] += self.linear_ns(m, F, cfg.H, 0, sch[0])
             out[1] += self.linear_ns(m, cfg.H, F, 1, sch[2])
         return [v / self.P for v in out]
+
+    def block_makespan_ns(self, cfg, counts: Sequence[int], schemes) -> List[float]:
+        """Modelled Group-GEMM time per phase as the paper defines it before its
+        approximation, T = max over workers of the worker's summed tile costs,
+        with the tiles dealt the way the kernel deals them: each group's tiles
+        sliced along K by the kernel's rule (the fewest slices, at most 8 of at
+        least 6 k blocks, whose cost is within half the mean work per worker),
+        longest first, each to the least loaded of the P workers; a sliced tile
+        pays SLICE_NS for its partial-sum hand-off, and the launch LAUNCH_NS.
+        Where tiles far outnumber workers this equals sum c_t / P."""
+        out = []
+        for ph in (0, 1):
+            groups = []
+            for e, sch in enumerate(schemes):
+                m = int(counts[e]) if e < cfg.E else cfg.T
+                if m <= 0:
+                    continue
+                F = cfg.F if e < cfg.E else cfg.F_shared
+                n, k = (F, cfg.H) if ph == 0 else (cfg.H, F)
+                scheme = sch[0] if ph == 0 else sch[2]
+                c = pick_cfg(m, scheme, ph)
+                a, b = self.data["cost"][str(ph)][scheme.name][c]
+                groups.append((n_tiles(m, n, ph, c), a, b, k // 128))
+            work = sum(nt * max(a + b * kb, b) for nt, a, b, kb in groups)
+            theta = work / self.P / 2.0
+            tiles = []
+            for nt, a, b, kb in groups:
+                smax = max(1, min(8, kb // 6))
+                best, cbest = 1, None
+                for sl in range(1, smax + 1):
+                    cs = max(a + b * (-(-kb // sl)), b) + (SLICE_NS if sl > 1 else 0.0)
+                    if cs <= theta:
+                        best = sl
+                        break
+                    if cbest is None or cs < cbest:
+                        best, cbest = sl, cs
+                cs = max(a + b * (-(-kb // best)), b) + (SLICE_NS if best > 1 else 0.0)
+                tiles += [cs] * (nt * best)
+            tiles.sort(reverse=True)
+            load = [0.0] * self.P
+            heap = [(0.0, i) for i in range(self.P)]
+            for c in tiles:
+                t, i = heapq.heappop(heap)
+                heapq.heappush(heap, (t + c, i))
+            out.append(max(t for t, _ in heap) + LAUNCH_NS)
+        return out
 
 
 # ----------------------------------------------------------------------------
@@ -243,8 +292,11 @@ def validate(table: CostTable, names: Sequence[str], log=print) -> List[dict]:
         cfg = W.CONFIGS[n]
         meas = measure_block(cfg)
         model = table.block_ns(cfg, meas["counts"], meas["schemes"])
+        mk = table.block_makespan_ns(cfg, meas["counts"], meas["schemes"])
         rec = {"workload": n, "gate_up_ms": round(meas["gate_up_ms"], 4), "gate_up_model_ms": round(model[0] / 1e6, 4),
-               "down_ms": round(meas["down_ms"], 4), "down_model_ms": round(model[1] / 1e6, 4)}
+               "gate_up_makespan_ms": round(mk[0] / 1e6, 4),
+               "down_ms": round(meas["down_ms"], 4), "down_model_ms": round(model[1] / 1e6, 4),
+               "down_makespan_ms": round(mk[1] / 1e6, 4)}
         log(f"[tile_cost] validate {json.dumps(rec)}")
         out.append(rec)
     return out
