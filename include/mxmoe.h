@@ -382,6 +382,44 @@ typedef struct {
 
 MXMOE_API mxmoe_status mxmoe_workspace_layout(const mxmoe_block* B, int32_t T, mxmoe_ws_layout* out);
 
+/* ------------------------------------------------------- tile cost model */
+
+/* The run-time tile plan (one per forward, built on the GPU) prices every
+ * output tile with the per-tile cost c_t that the paper profiles ahead of
+ * time for each tile configuration (Sec. 4.2.2, runtime cost modelling), and
+ * uses the costs to order tiles longest first and to choose how many slices
+ * along K a group's tiles take.  The costs do not change any result, only
+ * the schedule.
+ *
+ * Table (host, int32, MXMOE_TILE_COST_ENTRIES values), indexed
+ *   [phase][scheme][configuration][value]
+ *   phase          0: gate|up (both linears of a tile), 1: down, and the
+ *                  single linear of mxmoe_linear_forward
+ *   scheme         0 w16, 1 w8a8, 2 w4a4, 3 w2g128, 4 w3g128, 5 w4g128,
+ *                  6 w8g128, 7 w4a4-g128, 8 mxfp4, 9 fp8, 10 w4a4 on FP6
+ *   configuration  0..3: tiles of 16, 32, 64, 128 rows (the kernel picks
+ *                  the smallest that holds the group's rows, up to 64 rows
+ *                  for w4a4-g128 and mxfp4, and for fp8 outside the down
+ *                  phase)
+ *   value          a, bs, bu, h in picoseconds (bs, bu, h >= 0):
+ *                  a  fixed cost of a tile (the intercept of a fit over K,
+ *                     so it may be negative),
+ *                  bs cost per 128-wide k block not shared with other tiles,
+ *                  bu cost per k block of the weight stream, which the
+ *                     group's mt row tiles share (charged bu / mt),
+ *                  h  hand-off cost of a tile sliced along K.
+ * A tile of kb k blocks costs a + kb*bs + floor(kb*bu/mt) + (sliced ? h : 0)
+ * in exact integer arithmetic, clamped to [1, 2e9].
+ *
+ * mxmoe_set_tile_costs copies the table into a process-wide setting used by
+ * every later forward on any device (table NULL restores the built-in
+ * roofline default).  A forward reads the setting when it is enqueued; the
+ * calls are thread-safe.  mxmoe_get_tile_costs copies the current table out.
+ * Errors: INVALID_ARG (n_entries wrong, a negative bs, bu or h, out NULL).  */
+#define MXMOE_TILE_COST_ENTRIES (2 * 11 * 4 * 4)
+MXMOE_API mxmoe_status mxmoe_set_tile_costs(const int32_t* table, int32_t n_entries);
+MXMOE_API mxmoe_status mxmoe_get_tile_costs(int32_t* out, int32_t n_entries);
+
 MXMOE_API const char* mxmoe_status_string(mxmoe_status s);
 
 /* Library version, (major << 16) | minor.                                    */

@@ -50,7 +50,7 @@ import numpy as np
 __all__ = [
     "bf16_bits_to_f64", "round_to_act", "act_values", "route", "router_topk", "shared_gate", "dequant",
     "act_quant", "fp8_quant", "e4m3_values", "e4m3_code", "linear", "moe_forward", "lpt_makespan", "optimal_makespan",
-    "silu", "tile_plan", "xcd_queues", "xcd_tiles",
+    "silu", "tile_plan", "scheme_index", "xcd_queues", "xcd_tiles",
 ]
 
 # ----------------------------------------------------------------------------
@@ -506,12 +506,24 @@ def optimal_makespan(costs: Sequence[float], P: int) -> float:
 #   theta = (sum over the phase's tiles of the unsliced tile cost) // nwg // 2,
 #   nwg the workgroups of the launch; a group takes the fewest slices S in
 #   1 .. Smax = clamp(K/128 // 6, 1, 8) whose tile cost (reduction length
-#   ceil(K/128 / S) * 128) is at most theta, else the S of the cheapest tile
+#   ceil(K/128 / S) k blocks) is at most theta, else the S of the cheapest tile
 #   (the fewest slices among equals); groups without tiles are not sliced;
 #   budgets, granted in group order: the slices' partial sums (tiles * S * BM *
 #   BN * linears floats) fit the partial buffer and the tiles added by slicing
-#   (tiles * (S - 1)) stay within 16384 per phase, else S = 1;
+#   (tiles * (S - 1)) stay within 16384 per phase, and a group whose S is the
+#   cheapest tile's (none within theta) is sliced only if the phase's unsliced
+#   tiles plus every added tile granted so far plus its own stay within nwg
+#   and no earlier such group failed that test; else S = 1;
 #   a sliced group queues tiles * S tiles.
+#
+# Tile cost (Sec. 4.2.2: the cost c_t of a tile of each configuration is
+# profiled ahead of time and given to the scheduler): `costs` is that table,
+# an input like the weights, [phase][scheme][configuration] -> (a, bs, bu, h)
+# in ps, schemes numbered w16, w8a8, w4a4, w2g128, w3g128, w4g128, w8g128,
+# w4a4-g128, mxfp4, fp8, w4a4 on FP6.  A tile of kb k blocks whose group has
+# mt row tiles (which share its weights) costs
+#   a + kb * bs + floor(kb * bu / mt) + (h if the group is sliced),
+# clamped to [1, 2 * 10^9].
 
 _TILE_BM = (16, 32, 64, 128)
 _TILE_BN = ((256, 256, 128, 128), (512, 512, 256, 256))   # [phase][config]
@@ -519,49 +531,58 @@ _SPLIT_EXTRA = 16384
 _SPLIT_MAX = 8
 _SPLIT_SHARE = 2
 _SPLIT_MIN_KB = 6
-_TILE_FIXED_PS = 2.0e6
 
 
-def _tile_cost(bm: int, bn: int, nl: int, scheme, kk: int, split: int, mt: int, nt: int) -> int:
-    is_int = scheme.a_bits < 16
-    mx = getattr(scheme, "fmt", 0) == 1
-    f6 = getattr(scheme, "fmt", 0) == 3        # int4 codes stored as 6-bit e2m3, FP6 MFMA rate
-    wbytes = float(nl * bn * kk * (6 if f6 else scheme.w_bits)) / 8.0
-    abytes = float(bm) * kk * (0.5 if mx else (1.0 if is_int else 2.0))
-    pbytes = 8.0 * bm * bn * nl if split > 1 else 0.0
-    flops = 2.0 * nl * bm * bn * kk
-    t_mem = (wbytes / max(mt, 1) + abytes / max(nt, 1) + pbytes) * 32.0
-    t_mma = flops * 1000.0 / (39062.0 if (mx or f6) else (19531.0 if is_int else 9766.0))
-    c = max(t_mem, t_mma) + _TILE_FIXED_PS
-    return int(min(c, 2.0e9))
+def scheme_index(s) -> int:
+    """Position of a scheme in the cost table's scheme axis."""
+    fmt = getattr(s, "fmt", 0)
+    if s.a_bits == 16:
+        return 0 if s.w_bits == 16 else {2: 3, 3: 4, 4: 5, 8: 6}[s.w_bits]
+    if fmt == 1:
+        return 8
+    if fmt == 2:
+        return 9
+    if fmt == 3:
+        return 10
+    if s.a_group > 0:
+        return 7
+    return 1 if s.w_bits == 8 else 2
 
 
-def _choose_split(bm: int, bn: int, nl: int, scheme, kblocks: int, mt: int, nt: int, theta: int) -> int:
+def _tile_cost(entry, kb: int, split: int, mt: int) -> int:
+    a, bs, bu, h = (int(v) for v in entry)
+    c = a + kb * bs + (kb * bu) // max(mt, 1) + (h if split > 1 else 0)
+    return min(max(c, 1), 2 * 10**9)
+
+
+def _choose_split(entry, kblocks: int, mt: int, nt: int, theta: int):
+    """(slices, True if no slice count is within theta)."""
     if mt * nt <= 0:
-        return 1
+        return 1, False
     smax = max(1, min(_SPLIT_MAX, kblocks // _SPLIT_MIN_KB))
     best, cbest = 1, None
     for sp in range(1, smax + 1):
-        c = _tile_cost(bm, bn, nl, scheme, -(-kblocks // sp) * 128, sp, mt, nt)
+        c = _tile_cost(entry, -(-kblocks // sp), sp, mt)
         if c <= theta:
-            return sp
+            return sp, False
         if cbest is None or c < cbest:
             best, cbest = sp, c
-    return best
+    return best, True
 
 
-def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int = 0, nwg: int = 512):
+def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, costs, partial_floats: int = 0, nwg: int = 512):
     """Tile configuration, tile counts, slices, cost and queue rank per group.
 
     ms[g]: rows of group g; lins[g]: its linear (gate for phase 0, down for 1);
-    partial_floats: size of the split-K partial buffer; nwg: workgroups of the
-    launch.  Returns a list of dicts (cfg, mtiles, ntiles, split, tiles, cost,
-    rank) and the queue order (group indices with tiles, longest tile first).
+    costs: the tile cost table (see above); partial_floats: size of the
+    split-K partial buffer; nwg: workgroups of the launch.  Returns a list of
+    dicts (cfg, mtiles, ntiles, split, tiles, cost, rank) and the queue order
+    (group indices with tiles, longest tile first).
     """
     out = []
-    nl = 2 if phase == 0 else 1
     geo = []
     work = 0
+    unsliced = 0
     for m, lin in zip(ms, lins):
         m = int(m)  # Python integers: the sums below exceed 32 bits
         cfg = 0 if m <= 16 else (1 if m <= 32 else (2 if m <= 64 else 3))
@@ -571,28 +592,31 @@ def tile_plan(ms: Sequence[int], lins: Sequence, phase: int, partial_floats: int
         bm, bn = _TILE_BM[cfg], _TILE_BN[phase][cfg]
         mt = -(-m // bm) if m > 0 else 0
         nt = -(-int(lin.n) // bn)
-        geo.append((cfg, bm, bn, mt, nt))
+        entry = costs[phase][scheme_index(lin.scheme)][cfg]
+        geo.append((cfg, mt, nt, entry))
         if mt * nt > 0:
-            work += mt * nt * _tile_cost(bm, bn, nl, lin.scheme, (lin.k // 128) * 128, 1, mt, nt)
+            work += mt * nt * _tile_cost(entry, lin.k // 128, 1, mt)
+            unsliced += mt * nt
     theta = work // nwg // _SPLIT_SHARE
     pused = eused = 0
-    for (cfg, bm, bn, mt, nt), lin in zip(geo, lins):
-        sp = _choose_split(bm, bn, nl, lin.scheme, lin.k // 128, mt, nt, theta)
+    stopped = False
+    for (cfg, mt, nt, entry), lin in zip(geo, lins):
+        sp, fallback = _choose_split(entry, lin.k // 128, mt, nt, theta)
         if sp > 1:
-            need = mt * nt * sp * bm * bn * nl
+            need = mt * nt * sp * _TILE_BM[cfg] * _TILE_BN[phase][cfg] * (2 if phase == 0 else 1)
             extra = mt * nt * (sp - 1)
-            if pused + need > partial_floats or eused + extra > _SPLIT_EXTRA:
+            if fallback and unsliced + eused + extra > nwg:
+                stopped = True
+            if pused + need > partial_floats or eused + extra > _SPLIT_EXTRA or (fallback and stopped):
                 sp = 1
             else:
                 pused += need
                 eused += extra
         out.append({"cfg": cfg, "mtiles": mt, "ntiles": nt, "split": sp})
-    for r, lin in zip(out, lins):
-        bm, bn = _TILE_BM[r["cfg"]], _TILE_BN[phase][r["cfg"]]
-        kk = -(-(lin.k // 128) // r["split"]) * 128
+    for r, lin, (_, _, _, entry) in zip(out, lins, geo):
         tiles = r["mtiles"] * r["ntiles"] * r["split"]
         r["tiles"] = tiles
-        r["cost"] = _tile_cost(bm, bn, nl, lin.scheme, kk, r["split"], r["mtiles"], r["ntiles"]) if tiles else 0
+        r["cost"] = _tile_cost(entry, -(-(lin.k // 128) // r["split"]), r["split"], r["mtiles"]) if tiles else 0
     live = [g for g, r in enumerate(out) if r["tiles"] > 0]
     order = sorted(live, key=lambda g: (-out[g]["cost"], g))
     for r in out:

@@ -219,6 +219,30 @@ extern "C" {
 
 int32_t mxmoe_version(void) { return (0 << 16) | 1; }
 
+mxmoe_status mxmoe_set_tile_costs(const int32_t* table, int32_t n_entries) {
+  static_assert(MXMOE_TILE_COST_ENTRIES == mxmoe::kCostEntries, "cost table size");
+  if (!table) {
+    mxmoe::tile_costs_set(nullptr);
+    return MXMOE_OK;
+  }
+  if (n_entries != MXMOE_TILE_COST_ENTRIES) return MXMOE_ERR_INVALID_ARG;
+  mxmoe::TileCosts t;
+  for (int i = 0; i < MXMOE_TILE_COST_ENTRIES; ++i) {
+    if (table[i] < 0 && i % 4 != 0) return MXMOE_ERR_INVALID_ARG;  // a may be negative
+    t.v[i] = table[i];
+  }
+  mxmoe::tile_costs_set(&t);
+  return MXMOE_OK;
+}
+
+mxmoe_status mxmoe_get_tile_costs(int32_t* out, int32_t n_entries) {
+  if (!out || n_entries != MXMOE_TILE_COST_ENTRIES) return MXMOE_ERR_INVALID_ARG;
+  mxmoe::TileCosts t;
+  mxmoe::tile_costs_get(&t);
+  for (int i = 0; i < MXMOE_TILE_COST_ENTRIES; ++i) out[i] = t.v[i];
+  return MXMOE_OK;
+}
+
 const char* mxmoe_status_string(mxmoe_status s) {
   switch (s) {
     case MXMOE_OK: return "ok";

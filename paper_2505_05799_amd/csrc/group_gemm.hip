@@ -16,6 +16,8 @@
 // Groups may be sliced along the reduction (split-K, see split_rule): their
 // slices are queued as extra channel tiles, within fixed budgets of added
 // tiles and of partial-sum storage.
+#include <mutex>
+
 #include "group_gemm_impl.h"
 #include "rowquant.h"
 
@@ -88,7 +90,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
                                                     const int32_t* __restrict__ offsets, int raw_m,
                                                     DevLinear raw_lin, MaskBits mask, int32_t* __restrict__ plan,
                                                     int qcap, int fcap, int64_t pfloats,
-                                                    int32_t* __restrict__ down_qmax, int nwg, XPrep xp) {
+                                                    int32_t* __restrict__ down_qmax, int nwg, XPrep xp,
+                                                    TileCosts tc) {
   // workgroups 1.. encode x, one row per wavefront (grid-stride); the plan
   // below runs on workgroup 0 alone
   if (blockIdx.x > 0) {
@@ -105,7 +108,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   __shared__ int32_t s_n[2][kMaxG];       // output channels of the phase's linear
   __shared__ int32_t s_kb[2][kMaxG];      // its 128-wide k blocks
   __shared__ int8_t s_kd[2][kMaxG];       // its micro-kernel kind
-  __shared__ int8_t s_sp[2][kMaxG];       // slices: proposed, then final
+  __shared__ int8_t s_sp[2][kMaxG];       // slices: proposed (| 16 if by the fallback), then final
   __shared__ int32_t s_cost[2][kMaxG];    // budget need, then tile cost
   __shared__ int32_t s_tiles[2][kMaxG];   // sliced output tiles, then queued tiles
   __shared__ int32_t s_order[2][kMaxG];   // group per rank
@@ -114,7 +117,9 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   __shared__ int32_t s_red[1025];
   __shared__ int64_t s_work[2][1024 / 64];
   __shared__ int64_t s_theta[2];          // slicing threshold per phase
+  __shared__ int32_t s_ut[2][1024 / 64];  // unsliced tiles per wavefront, then per phase in [p][0]
   __shared__ int32_t s_used[2];           // output-tile counters used per phase
+  __shared__ int32_t s_tc[kCostEntries];  // tile cost table
   __shared__ int32_t s_ng[2];             // groups with tiles per phase
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
   const int nphase = raw_m >= 0 ? 1 : 2;
@@ -123,7 +128,8 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   int32_t* order = plan + PL.order;
   auto rec_of = [&](int ph, int g) { return plan + PL.rec + ((int64_t)ph * G + g) * PF_N; };
 
-  // 0. inputs
+  // 0. inputs (and the cost table)
+  for (int i = tid; i < kCostEntries; i += blockDim.x) s_tc[i] = tc.v[i];
   for (int g = tid; g < G; g += blockDim.x) {
     int m = raw_m >= 0 ? raw_m : (g < E ? counts[g] : T);
     if (!((mask.w[g >> 5] >> (g & 31)) & 1u)) m = 0;
@@ -148,7 +154,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     misc[8] = nwg;
   }
   lds_barrier();
-  struct Geom { int m, cfg, bm, bn, mt, nt, kb, kd, nl; };
+  struct Geom { int m, cfg, bm, bn, mt, nt, kb, kd, nl, ce; };
   auto geom = [&](int ph, int g) {
     Geom q;
     q.m = s_m[g];
@@ -160,34 +166,49 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     q.kb = s_kb[ph][g];
     q.kd = s_kd[ph][g];
     q.nl = (raw_m < 0 && ph == 0) ? 2 : 1;
+    q.ce = cost_index(raw_m >= 0 ? 1 : ph, q.kd, q.cfg);  // raw mode: one linear
     return q;
   };
 
   // 1. per group the unsliced tile cost (kept for the steps below); the
   //    phase's work (tiles times that cost, summed exactly) sets the slicing
-  //    threshold; then per group the proposed slices and, for the budget
-  //    pass, the partial-sum floats (capped at pfloats + 1, which no budget
-  //    admits) and the output tiles of every group that would be sliced
+  //    threshold and its unsliced tiles the fallback budget; then per group
+  //    the proposed slices and, for the budget pass, the partial-sum floats
+  //    (capped at pfloats + 1, which no budget admits) and the output tiles
+  //    of every group that would be sliced
   for (int ph = 0; ph < nphase; ++ph) {
     int64_t w = 0;
+    int u = 0;
     for (int g = tid; g < G; g += blockDim.x) {
       const Geom q = geom(ph, g);
       const int tiles = q.mt * q.nt;
-      const int32_t c = tiles > 0 ? tile_cost(q.bm, q.bn, q.nl, q.kd, q.kb * 128, 1, q.mt, q.nt) : 0;
+      const int32_t c = tiles > 0 ? tile_cost(s_tc + q.ce, q.kb, 1, q.mt) : 0;
       s_c1[ph][g] = c;
       w += (int64_t)tiles * c;
+      u += tiles;
     }
-    for (int d = 32; d > 0; d >>= 1) w += __shfl_xor(w, d, 64);
-    if (lane == 0) s_work[ph][wave] = w;
+    for (int d = 32; d > 0; d >>= 1) {
+      w += __shfl_xor(w, d, 64);
+      u += __shfl_xor(u, d, 64);
+    }
+    if (lane == 0) {
+      s_work[ph][wave] = w;
+      s_ut[ph][wave] = u;
+    }
   }
   lds_barrier();
   if (tid < nphase) {
     int64_t work = 0;
-    for (int i = 0; i < nwave; ++i) work += s_work[tid][i];
+    int ut = 0;
+    for (int i = 0; i < nwave; ++i) {
+      work += s_work[tid][i];
+      ut += s_ut[tid][i];
+    }
     s_theta[tid] = work / nwg / kSplitShare;
+    s_ut[tid][0] = ut;
   }
   lds_barrier();
-  // The slice rule of choose_split, evaluated by eight lanes per group: lane
+  // The slice rule (kSplitShare, kSplitMinKb), evaluated by eight lanes per group: lane
   // j prices j + 1 slices; the group takes the fewest slices whose tile cost
   // is within theta, else the cheapest (the fewest slices among equals).
   for (int base = 0; base < nphase * G; base += (int)blockDim.x / 8) {
@@ -200,7 +221,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     smax = smax < 1 ? 1 : (smax > kSplitMax ? kSplitMax : smax);
     const bool ok = tiled && s <= smax;
     int32_t c = 0;
-    if (ok) c = s == 1 ? s_c1[ph][g] : tile_cost(q.bm, q.bn, q.nl, q.kd, (q.kb + s - 1) / s * 128, s, q.mt, q.nt);
+    if (ok) c = s == 1 ? s_c1[ph][g] : tile_cost(s_tc + q.ce, (q.kb + s - 1) / s, s, q.mt);
     int first = (ok && c <= s_theta[ph]) ? s : 64;
     int64_t key = ok ? (((int64_t)c << 8) | s) : INT64_MAX;
     for (int d = 1; d < 8; d <<= 1) {
@@ -231,7 +252,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       r[PF_NTILES] = q.nt;
       r[PF_START] = 0;
       const int64_t need = (int64_t)q.mt * q.nt * sp * q.bm * q.bn * q.nl;
-      s_sp[ph][g] = (int8_t)sp;
+      s_sp[ph][g] = (int8_t)(sp | (tiled && first > kSplitMax && sp > 1 ? 16 : 0));
       s_cs[ph][g] = csp;
       s_tiles[ph][g] = sp > 1 ? q.mt * q.nt : 0;
       s_cost[ph][g] = sp > 1 ? (int32_t)(need <= pfloats ? need : pfloats + 1) : 0;
@@ -239,48 +260,77 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   }
   lds_barrier();
   // 2. slices within the budgets, greedily in group order: a group is sliced
-  //    if its partial sums and added tiles still fit, else it runs unsliced.
-  //    One wavefront per phase takes 64 groups at a time; a chunk that fits
-  //    whole is accepted at once (what the greedy pass does with it), any
-  //    other chunk is decided group by group.
+  //    if its partial sums and added tiles still fit; a group whose slices
+  //    come from the fallback (no slice count within theta) also needs the
+  //    phase's tiles, with every slice granted so far and its own, to stay
+  //    within one tile per workgroup, and once one such group is refused
+  //    for that no later one is sliced.  (Slicing the long tiles of a launch
+  //    with fewer tiles than workgroups shortens its one wave of tiles; past
+  //    one tile per workgroup it adds a second wave.)  Groups not sliced run
+  //    unsliced.  One wavefront per phase takes 64 groups at a time; in a
+  //    chunk whose partial sums and added tiles fit whole the fallback rule
+  //    is one prefix sum, any other chunk is decided group by group.
   if (wave < nphase) {
     const int ph = wave;
+    const int64_t ut = s_ut[ph][0];
     int64_t pused = 0;
     int eused = 0, cused = 0;
+    bool stopped = false;  // a fallback group was refused (wave-uniform)
+    auto scan3 = [&](int64_t& p, int& e, int& c) {
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t tp = __shfl_up(p, d, 64);
+        const int te = __shfl_up(e, d, 64), tc = __shfl_up(c, d, 64);
+        if (lane >= d) {
+          p += tp;
+          e += te;
+          c += tc;
+        }
+      }
+    };
     for (int c0 = 0; c0 < G; c0 += 64) {
       const int g = c0 + lane;
-      const int sp = g < G ? s_sp[ph][g] : 1;
+      const int spv = g < G ? s_sp[ph][g] : 1;
+      const int sp = spv & 15;
+      const bool fb = (spv & 16) != 0;
       const int tl = g < G ? s_tiles[ph][g] : 0;  // 0 unless sliced
       const int64_t need = g < G ? s_cost[ph][g] : 0;
       const int extra = tl * (sp - 1) <= kSplitExtra ? tl * (sp - 1) : kSplitExtra + 1;
       int64_t pin = need;
       int ein = extra, cin = tl;
-      for (int d = 1; d < 64; d <<= 1) {
-        const int64_t tp = __shfl_up(pin, d, 64);
-        const int te = __shfl_up(ein, d, 64), tc = __shfl_up(cin, d, 64);
-        if (lane >= d) {
-          pin += tp;
-          ein += te;
-          cin += tc;
-        }
-      }
+      scan3(pin, ein, cin);
       const int64_t ptot = __shfl(pin, 63, 64);
-      const int etot = __shfl(ein, 63, 64), ctot = __shfl(cin, 63, 64);
+      const int etot = __shfl(ein, 63, 64);
       bool take = tl > 0;
       int64_t pbase = 0;
       int cbase = 0;
       if (pused + ptot <= pfloats && (int64_t)eused + etot <= kSplitExtra) {
-        pbase = pused + pin - need;
-        cbase = cused + cin - tl;
-        pused += ptot;
-        eused += etot;
-        cused += ctot;
+        // every group before the first refused fallback group is granted, so
+        // the tiles a group sees are the prefix sum over all candidates
+        const uint64_t fm = __ballot(fb && tl > 0 && (stopped || ut + eused + ein > nwg));
+        const int f = fm ? __ffsll((unsigned long long)fm) - 1 : 64;
+        take = tl > 0 && (!fb || lane < f);
+        stopped = stopped || fm != 0;
+        int64_t p2 = take ? need : 0;
+        int e2 = take ? extra : 0, c2 = take ? tl : 0;
+        scan3(p2, e2, c2);
+        pbase = pused + p2 - (take ? need : 0);
+        cbase = cused + c2 - (take ? tl : 0);
+        pused += __shfl(p2, 63, 64);
+        eused += __shfl(e2, 63, 64);
+        cused += __shfl(c2, 63, 64);
       } else {
-        for (int j = 0; j < 64; ++j) {
-          const int64_t nj = __shfl(need, j, 64);
-          const int ej = __shfl(extra, j, 64), tj = __shfl(tl, j, 64);
-          if (tj <= 0) continue;
-          const bool ok = pused + nj <= pfloats && eused + ej <= kSplitExtra;
+        // the chunk's candidates in group order (a wave-uniform lane index,
+        // so each input is one lane read)
+        uint64_t cand = __ballot(tl > 0);
+        while (cand) {
+          const int j = __ffsll((unsigned long long)cand) - 1;
+          cand &= cand - 1;
+          const int64_t nj = __builtin_amdgcn_readlane((int)need, j);
+          const int ej = __builtin_amdgcn_readlane(extra, j);
+          const int tj = __builtin_amdgcn_readlane(tl, j);
+          const bool fj = __builtin_amdgcn_readlane((int)fb, j) != 0;
+          if (fj && ut + eused + ej > nwg) stopped = true;
+          const bool ok = pused + nj <= pfloats && eused + ej <= kSplitExtra && (!fj || !stopped);
           if (lane == j) {
             take = ok;
             pbase = pused;
@@ -492,6 +542,51 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
 
 }  // namespace
 
+// Roofline default of the tile cost table, in the table's additive form: a
+// fixed 2 us per tile; bs the MFMA time of a k block at one CU's share of the
+// MI355X dense peak of the kind's operands (10 PFLOP/s FP4 / FP6, 5 POPS int8
+// and FP8, 2.5 PFLOP/s 16-bit); bu the time of the tile's weight bytes of a k
+// block at one CU's share of 8 TB/s (32 ps per byte); h the time of writing
+// and reading back the tile's fp32 partial sums (8 bytes per output) at that
+// share.
+void tile_costs_default(TileCosts* out) {
+  for (int ph = 0; ph < 2; ++ph)
+    for (int kd = 0; kd < K_COUNT; ++kd)
+      for (int c = 0; c < kCostCfgs; ++c) {
+        const int bm = cfg_bm(c), bn = cfg_bn(c, ph), nl = ph == 0 ? 2 : 1;
+        const double rate = (kind_is_mx(kd) || kind_is_f6(kd)) ? 39062.0 : (kind_is_int(kd) ? 19531.0 : 9766.0);
+        int32_t* e = out->v + cost_index(ph, kd, c);
+        e[0] = 2000000;
+        e[1] = (int32_t)(2.0 * nl * bm * bn * 128 * 1000.0 / rate);
+        e[2] = (int32_t)((double)nl * bn * 128 * kind_wbits(kd) / 8.0 * 32.0);
+        e[3] = (int32_t)(8.0 * bm * bn * nl * 32.0);
+      }
+}
+
+namespace {
+std::mutex g_cost_mu;
+TileCosts g_costs;
+bool g_costs_init = false;
+}  // namespace
+
+void tile_costs_set(const TileCosts* t) {
+  std::lock_guard<std::mutex> lk(g_cost_mu);
+  if (t)
+    g_costs = *t;
+  else
+    tile_costs_default(&g_costs);
+  g_costs_init = true;
+}
+
+void tile_costs_get(TileCosts* out) {
+  std::lock_guard<std::mutex> lk(g_cost_mu);
+  if (!g_costs_init) {
+    tile_costs_default(&g_costs);
+    g_costs_init = true;
+  }
+  *out = g_costs;
+}
+
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
                        int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
@@ -502,8 +597,10 @@ hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int3
   // 16 rows per encoding workgroup, at most 1024 of them (grid-stride beyond)
   int nxb = xp.rows > 0 ? (xp.rows + 15) / 16 : 0;
   nxb = nxb < 1024 ? nxb : 1024;
+  TileCosts tc;
+  tile_costs_get(&tc);
   hipLaunchKernelGGL(plan_kernel, dim3(1 + nxb), dim3(1024), 0, s, experts, E, G, T, counts, offsets, raw_m, raw_lin,
-                     mb, plan, qcap, fcap, pfloats, down_qmax, nwg < 1 ? 1 : nwg, xp);
+                     mb, plan, qcap, fcap, pfloats, down_qmax, nwg < 1 ? 1 : nwg, xp, tc);
   return hipGetLastError();
 }
 

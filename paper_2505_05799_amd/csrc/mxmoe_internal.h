@@ -206,26 +206,34 @@ __host__ __device__ inline int plan_flat_cap(int qcap) {
 __host__ __device__ inline int32_t tile_word0(int g, int cfg, int kind, int split) {
   return g | (cfg << 16) | (kind << 20) | ((split - 1) << 24);
 }
-// Static cost of one tile in ps: the larger of its memory time and its MFMA
-// time at one CU's share of the MI355X peaks (8 TB/s; 10 PFLOP/s FP4 / FP6,
-// 5.0 POPS int8, 2.5 PFLOP/s 16-bit) for a reduction of length kk, plus a fixed per-tile cost
-// (prologue, epilogue).  The group's mt row tiles share each weight tile and
-// its nt channel tiles share each activation tile through L2, so a tile is
-// charged those shares of its HBM bytes; a sliced tile also writes its partial
-// sums and reads them back.  Every step is a single rounding of exact
-// operands, so the value does not depend on operation fusion.
-constexpr double kTileFixedPs = 2.0e6;
-__host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int kk, int split, int mt, int nt) {
-  const double wbytes = (double)nl * bn * kk * kind_wbits(kd) / 8.0;
-  const double abytes = (double)bm * kk * (kind_is_mx(kd) ? 0.5 : (kind_is_int(kd) ? 1.0 : 2.0));
-  const double pbytes = split > 1 ? 8.0 * bm * bn * nl : 0.0;
-  const double flops = 2.0 * nl * bm * bn * kk;
-  const double t_mem = (wbytes / (mt > 0 ? mt : 1) + abytes / (nt > 0 ? nt : 1) + pbytes) * 32.0;
-  const double t_mma =
-      flops * 1000.0 / ((kind_is_mx(kd) || kind_is_f6(kd)) ? 39062.0 : (kind_is_int(kd) ? 19531.0 : 9766.0));
-  double c = t_mem > t_mma ? t_mem : t_mma;
-  c += kTileFixedPs;
-  if (c > 2.0e9) c = 2.0e9;
+// Tile cost of the run-time plan: the paper's per-tile cost c_t, profiled
+// ahead of time per tile configuration (Sec. 4.2.2), held as a table of four
+// integers in ps per (phase, kind, configuration):
+//   a   fixed cost of a tile (prologue, epilogue, queue pop; a fit's
+//       intercept, so it may be negative)
+//   bs  cost per 128-wide k block that no other tile shares (MFMA issue,
+//       activation streaming)
+//   bu  cost per k block of streaming the tile's weights; the group's mt row
+//       tiles share each weight tile through L2, so a tile is charged bu / mt
+//   h   hand-off cost of a sliced tile (partial sums written, then read back)
+// A tile of kb k blocks (its slice's share when sliced) costs
+//   c = a + kb * bs + floor(kb * bu / mt) + (slices > 1 ? h : 0)
+// in exact integer arithmetic, clamped to [1, 2e9].  Phase 1 also serves the
+// single-linear plan.  The table comes from the caller (mxmoe_set_tile_costs)
+// or is the roofline default below.
+constexpr int kCostCfgs = 4;
+constexpr int kCostVals = 4;
+constexpr int kCostEntries = 2 * K_COUNT * kCostCfgs * kCostVals;
+struct TileCosts {
+  int32_t v[kCostEntries];
+};
+__host__ __device__ constexpr inline int cost_index(int ph, int kd, int cfg) {
+  return ((ph * K_COUNT + kd) * kCostCfgs + cfg) * kCostVals;
+}
+constexpr int64_t kCostMaxPs = 2000000000LL;
+__host__ __device__ inline int32_t tile_cost(const int32_t* e, int kb, int split, int mt) {
+  int64_t c = (int64_t)e[0] + (int64_t)kb * e[1] + (int64_t)kb * e[2] / (mt > 0 ? mt : 1) + (split > 1 ? e[3] : 0);
+  c = c < 1 ? 1 : (c > kCostMaxPs ? kCostMaxPs : c);
   return (int32_t)c;
 }
 // Slices of a group (split-K, the paper's slice-K tile parameter): the fewest
@@ -234,29 +242,11 @@ __host__ __device__ inline int32_t tile_cost(int bm, int bn, int nl, int kd, int
 // cheapest tile (the fewest slices among equals).  theta is half of the
 // phase's mean work per workgroup (unsliced tile costs summed over all tiles,
 // over the grid), so that no tile is long next to the schedule it is part of.
-// A slice costs a partial-sum hand-off that the static cost underrates (the
-// last slice reads every slice's sums back before its epilogue); at a quarter
-// of the mean work, or with 4 k blocks per slice, the launches measured slower
-// (DeepSeek-V2-Lite-shaped forward 8% and Qwen1.5-MoE-shaped 12% slower).
+// At a quarter of the mean work, or with 4 k blocks per slice, the launches
+// measured slower (DeepSeek-V2-Lite-shaped forward 8% and Qwen1.5-MoE-shaped
+// 12% slower).
 constexpr int kSplitShare = 2;
 constexpr int kSplitMinKb = 6;
-__host__ __device__ inline int choose_split(int bm, int bn, int nl, int kd, int kblocks, int mt, int nt,
-                                            int64_t theta) {
-  if (mt * nt <= 0) return 1;
-  int smax = kblocks / kSplitMinKb;
-  smax = smax < 1 ? 1 : (smax > kSplitMax ? kSplitMax : smax);
-  int best = 1;
-  int32_t cbest = 0;
-  for (int s = 1; s <= smax; ++s) {
-    const int32_t c = tile_cost(bm, bn, nl, kd, (kblocks + s - 1) / s * 128, s, mt, nt);
-    if (c <= theta) return s;
-    if (s == 1 || c < cbest) {
-      best = s;
-      cbest = c;
-    }
-  }
-  return best;
-}
 
 // Workspace layout (byte offsets), shared by host code of the forward.
 struct WsLayout {
@@ -408,10 +398,16 @@ struct XPrep {
 // both phases from counts.  mask_words: 64 words, bit g = expert g gets tiles.
 // The same launch encodes xp on its other workgroups (they do not wait for
 // the plan, nor it for them).
+// The plan prices tiles with the process-wide cost table (tile_costs_get).
 hipError_t launch_plan(const DevExpert* experts, int E, int G, int T, const int32_t* counts,
                        const int32_t* offsets, int raw_m, const DevLinear& raw_lin, const uint32_t* mask_words,
                        int32_t* plan, int qcap, int fcap, int64_t pfloats, int32_t* down_qmax, int nwg,
                        const XPrep& xp, hipStream_t s);
+// Process-wide tile cost table: the roofline default until a caller sets one;
+// set (nullptr restores the default) and get copy under a lock.
+void tile_costs_default(TileCosts* out);
+void tile_costs_set(const TileCosts* t);
+void tile_costs_get(TileCosts* out);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 

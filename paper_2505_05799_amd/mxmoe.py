@@ -63,8 +63,9 @@ EXPORTS = [
     "mxmoe_route_permute", "mxmoe_router_topk", "mxmoe_act_quant", "mxmoe_linear_workspace_bytes", "mxmoe_linear_forward",
     "mxmoe_block_table_bytes", "mxmoe_block_table_fill", "mxmoe_workspace_bytes", "mxmoe_moe_forward",
     "mxmoe_moe_forward_ex", "mxmoe_workspace_layout", "mxmoe_status_string", "mxmoe_version",
-    "mxmoe_moe_forward_noalloc",
+    "mxmoe_moe_forward_noalloc", "mxmoe_set_tile_costs", "mxmoe_get_tile_costs",
 ]
+TILE_COST_SHAPE = (2, 11, 4, 4)     # [phase][scheme][configuration][a, bs, bu, h], MXMOE_TILE_COST_ENTRIES
 NOALLOC_SCRATCH_BYTES = 128 << 20   # MXMOE_NOALLOC_SCRATCH_BYTES
 
 _lib = None
@@ -100,13 +101,39 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "mxmoe_moe_forward_noalloc": (C.c_int, [PB, vp, i32, vp, vp, vp, vp, vp]),
         "mxmoe_status_string": (C.c_char_p, [C.c_int]),
         "mxmoe_version": (i32, []),
+        "mxmoe_set_tile_costs": (C.c_int, [vp, i32]),
+        "mxmoe_get_tile_costs": (C.c_int, [vp, i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
         f.restype = res
         f.argtypes = args
     _lib = lib
+    # the run-time plan prices tiles with the profiled cost table when there is one
+    from . import tile_cost
+    if os.path.exists(tile_cost.DEFAULT_TABLE):
+        set_tile_costs(tile_cost.CostTable.load().device_table())
     return lib
+
+
+def set_tile_costs(table=None):
+    """Install the run-time plan's tile cost table (int32 TILE_COST_SHAPE, ps),
+    or the library's roofline default with None (mxmoe_set_tile_costs)."""
+    lib = load_library()
+    if table is None:
+        _check(lib.mxmoe_set_tile_costs(None, 0), "mxmoe_set_tile_costs")
+        return
+    t = np.ascontiguousarray(table, dtype=np.int32)
+    if t.shape != TILE_COST_SHAPE:
+        raise ValueError(f"tile cost table of shape {t.shape}, expected {TILE_COST_SHAPE}")
+    _check(lib.mxmoe_set_tile_costs(t.ctypes.data_as(C.c_void_p), t.size), "mxmoe_set_tile_costs")
+
+
+def get_tile_costs() -> np.ndarray:
+    """The tile cost table forwards use now (mxmoe_get_tile_costs)."""
+    t = np.zeros(TILE_COST_SHAPE, dtype=np.int32)
+    _check(load_library().mxmoe_get_tile_costs(t.ctypes.data_as(C.c_void_p), t.size), "mxmoe_get_tile_costs")
+    return t
 
 
 class MxmoeError(RuntimeError):

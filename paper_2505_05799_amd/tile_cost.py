@@ -11,10 +11,20 @@ parallel workers P (valid when tiles far outnumber workers):
 Here a worker is one slot of the persistent Group-GEMM grid (two workgroups
 per CU, P = 2 * 256), and a tile is one unsliced output tile of the kernel:
 BM rows x BN channels over the whole K (phase 0 covers gate and up together).
-`profile()` measures c_t on the GPU for every (phase, scheme, configuration)
-as D * P / n_tiles, where D is the duration of a Group-GEMM launch over
-n_tiles >= 4 P equal tiles, at two reduction depths, and fits
-c_t(K) = a + b * K / 128.  The table is stored as JSON beside this module.
+A tile's cost depends on how many row tiles of its group share its weights
+through L2 (mt, the group's row tiles), so the table holds, per (phase,
+scheme, configuration), three coefficients of
+
+    c_t(K, mt) = a + (K / 128) * (bs + bu / mt)     (ns)
+
+`profile()` measures c_t on the GPU as D * P / n_tiles, where D is the
+duration of a Group-GEMM launch over n_tiles >= 4 P equal tiles, at two
+reduction depths, with one row tile per group (mt = 1) for every
+configuration and also with 8 row tiles per group for the largest
+configuration of the scheme (the only one a group of more rows takes), and
+fits a, bs, bu.  The same table, in picoseconds, prices the tiles of the
+run-time plan on the GPU (`device_table`, mxmoe_set_tile_costs).  It is stored
+as JSON beside this module.
 
     python -m paper_2505_05799_amd.tile_cost --out paper_2505_05799_amd/tile_costs_mi355x.json
 """
@@ -61,27 +71,33 @@ def n_tiles(m: int, n: int, phase: int, cfg: int) -> int:
 
 
 class CostTable:
-    """c_t(K) = a + b * K / 128 in ns per tile, per (phase, scheme name, configuration)."""
+    """c_t(K, mt) = a + K / 128 * (bs + bu / mt) in ns per tile, per (phase,
+    scheme name, configuration); entries of two values [a, b] mean bu = 0."""
 
     def __init__(self, data: dict):
         self.data = data
         self.P = int(data.get("P", P_SLOTS))
+        self.slice_ns = float(data.get("slice_ns", SLICE_NS))
 
     @classmethod
     def load(cls, path: str = DEFAULT_TABLE) -> "CostTable":
         with open(path) as fh:
             return cls(json.load(fh))
 
-    def tile_ns(self, phase: int, scheme, cfg: int, k: int) -> float:
-        a, b = self.data["cost"][str(phase)][scheme.name][cfg]
-        return a + b * (k / 128.0)
+    def coef(self, phase: int, scheme, cfg: int):
+        e = self.data["cost"][str(phase)][scheme.name][cfg]
+        return (float(e[0]), float(e[1]), float(e[2]) if len(e) > 2 else 0.0)
+
+    def tile_ns(self, phase: int, scheme, cfg: int, k: int, mt: int = 1) -> float:
+        a, bs, bu = self.coef(phase, scheme, cfg)
+        return a + (k / 128.0) * (bs + bu / max(mt, 1))
 
     def linear_ns(self, m: int, n: int, k: int, phase: int, scheme) -> float:
         """Serial tile time of one linear block (phase 0: gate and up together)."""
         if m <= 0:
             return 0.0
         c = pick_cfg(m, scheme, phase)
-        return n_tiles(m, n, phase, c) * self.tile_ns(phase, scheme, c, k)
+        return n_tiles(m, n, phase, c) * self.tile_ns(phase, scheme, c, k, -(-m // BM[c]))
 
     def block_ns(self, cfg, counts: Sequence[int], schemes) -> List[float]:
         """Modelled Group-GEMM time per phase, T = sum c_t / P, for a block
@@ -99,10 +115,11 @@ class CostTable:
         approximation, T = max over workers of the worker's summed tile costs,
         with the tiles dealt the way the kernel deals them: each group's tiles
         sliced along K by the kernel's rule (the fewest slices, at most 8 of at
-        least 6 k blocks, whose cost is within half the mean work per worker),
-        longest first, each to the least loaded of the P workers; a sliced tile
-        pays SLICE_NS for its partial-sum hand-off, and the launch LAUNCH_NS.
-        Where tiles far outnumber workers this equals sum c_t / P."""
+        least 6 k blocks, whose cost is within half the mean work per worker,
+        else the cheapest tile's slices as long as the phase keeps at most one
+        tile per worker, up to the first group refused for that), longest first, each to the least loaded of the P
+        workers; a sliced tile pays the table's slice hand-off, and the launch
+        LAUNCH_NS.  Where tiles far outnumber workers this equals sum c_t / P."""
         out = []
         for ph in (0, 1):
             groups = []
@@ -114,31 +131,62 @@ class CostTable:
                 n, k = (F, cfg.H) if ph == 0 else (cfg.H, F)
                 scheme = sch[0] if ph == 0 else sch[2]
                 c = pick_cfg(m, scheme, ph)
-                a, b = self.data["cost"][str(ph)][scheme.name][c]
-                groups.append((n_tiles(m, n, ph, c), a, b, k // 128))
-            work = sum(nt * max(a + b * kb, b) for nt, a, b, kb in groups)
+                a, bs, bu = self.coef(ph, scheme, c)
+                mt = -(-m // BM[c])
+                groups.append((n_tiles(m, n, ph, c), a, bs + bu / mt, k // 128))
+            work = sum(nt * max(a + b * kb, 1e-3) for nt, a, b, kb in groups)
             theta = work / self.P / 2.0
+            unsliced = sum(g[0] for g in groups)
+            added = 0
+            stopped = False
             tiles = []
             for nt, a, b, kb in groups:
                 smax = max(1, min(8, kb // 6))
-                best, cbest = 1, None
+                cost = lambda sl: max(a + b * (-(-kb // sl)), 1e-3) + (self.slice_ns if sl > 1 else 0.0)
+                best, cbest, fallback = 1, None, True
                 for sl in range(1, smax + 1):
-                    cs = max(a + b * (-(-kb // sl)), b) + (SLICE_NS if sl > 1 else 0.0)
+                    cs = cost(sl)
                     if cs <= theta:
-                        best = sl
+                        best, fallback = sl, False
                         break
                     if cbest is None or cs < cbest:
                         best, cbest = sl, cs
-                cs = max(a + b * (-(-kb // best)), b) + (SLICE_NS if best > 1 else 0.0)
-                tiles += [cs] * (nt * best)
+                if fallback and best > 1 and unsliced + added + nt * (best - 1) > self.P:
+                    stopped = True
+                if fallback and stopped:
+                    best = 1
+                added += nt * (best - 1)
+                tiles += [cost(best)] * (nt * best)
             tiles.sort(reverse=True)
-            load = [0.0] * self.P
             heap = [(0.0, i) for i in range(self.P)]
             for c in tiles:
                 t, i = heapq.heappop(heap)
                 heapq.heappush(heap, (t + c, i))
             out.append(max(t for t, _ in heap) + LAUNCH_NS)
         return out
+
+    def device_table(self) -> np.ndarray:
+        """The table as the run-time plan takes it (mxmoe_set_tile_costs): int32
+        [phase][scheme][configuration][a, bs, bu, h] in ps, schemes in the
+        order of ALL_SCHEMES (the library's kind ids), each value rounded to the
+        nearest ps and clamped to the int32 range (bs, bu, h to >= 0; a, a fit's
+        intercept, may be negative); h is the slice hand-off.
+        Schemes absent from the table get the largest cost, so that a missing
+        profile shows as a slow tile rather than a free one."""
+        from . import workloads as W
+        out = np.zeros((2, len(W.ALL_SCHEMES), N_CFG, 4), dtype=np.int64)
+        h = int(round(self.slice_ns * 1000.0))
+        for ph in (0, 1):
+            for i, s in enumerate(W.ALL_SCHEMES):
+                for c in range(N_CFG):
+                    if s.name in self.data["cost"][str(ph)]:
+                        a, bs, bu = self.coef(ph, s, c)
+                        out[ph, i, c] = [round(a * 1000.0), round(bs * 1000.0), round(bu * 1000.0), h]
+                    else:
+                        out[ph, i, c] = [2_000_000_000, 0, 0, h]
+        out[..., 1:] = np.clip(out[..., 1:], 0, 2**31 - 1)
+        out[..., 0] = np.clip(out[..., 0], -2**31, 2**31 - 1)
+        return out.astype(np.int32)
 
 
 # ----------------------------------------------------------------------------
@@ -179,19 +227,26 @@ def _device_linear(scheme, n: int, k: int, gen, dev: str = "cuda"):
     return W.QLinear(s, n, k, codes, scales)
 
 
-def _probe(scheme, phase: int, k: int, cfgs: Sequence[int], reps: int, n_sets: int = 8, log=print):
-    """Launch durations (ms) of the profiled phase for each configuration."""
+REUSE_ROWS = 8   # row tiles per group in the weight-sharing probe
+
+
+def _probe(scheme, phase: int, k: int, cfgs: Sequence[int], reps: int, n_sets: int = 8, reuse: int = 1,
+           log=print):
+    """Launch durations (ms) of the profiled phase for each configuration, with
+    `reuse` row tiles per group."""
     import torch
     from . import mxmoe as M
     from . import workloads as W
-    # the profiled phase has N = 8192 output channels and reduction depth k
+    # the profiled phase has N = 8192 output channels and reduction depth k;
+    # with one row tile per group 64 (gate|up) or 128 (down) experts, with
+    # several 16 experts, so that every launch holds >= 4 P tiles
     H, F = (k, 8192) if phase == 0 else (8192, k)
-    E = 64 if phase == 0 else 128
-    T_max = E * 128
-    cfg = W.BlockConfig(f"probe_{scheme.name}_p{phase}_k{k}", T=T_max, H=H, F=F, E=E, k=1, n_shared=0,
+    E = 16 if reuse > 1 else (64 if phase == 0 else 128)
+    T_max = E * 128 * reuse
+    cfg = W.BlockConfig(f"probe_{scheme.name}_p{phase}_k{k}_r{reuse}", T=T_max, H=H, F=F, E=E, k=1, n_shared=0,
                         F_shared=0, act="bf16", zipf_s=None, alloc=lambda e, r: (scheme,) * 3)
     gen = torch.Generator(device="cuda")
-    gen.manual_seed(1234 + phase * 7 + k)
+    gen.manual_seed(1234 + phase * 7 + k + reuse)
     # n_sets distinct weight sets, dealt to the experts in turn: the working set
     # (several hundred MB at least) stays well above what the caches hold
     sets = []
@@ -208,7 +263,7 @@ def _probe(scheme, phase: int, k: int, cfgs: Sequence[int], reps: int, n_sets: i
     out = {}
     ev = M.PhaseEvents()
     for c in cfgs:
-        m = BM[c]
+        m = BM[c] * reuse
         T = E * m
         ids = (torch.arange(T, device="cuda", dtype=torch.int32) // m).reshape(T, 1).contiguous()
         w = torch.ones((T, 1), dtype=torch.float32, device="cuda")
@@ -223,32 +278,55 @@ def _probe(scheme, phase: int, k: int, cfgs: Sequence[int], reps: int, n_sets: i
             d.append(ev.elapsed_ms()[1 if phase == 0 else 3])
         nt = E * n_tiles(m, F if phase == 0 else H, phase, c)
         out[c] = (float(np.median(d)), nt)
-        log(f"[tile_cost] {scheme.name} phase {phase} K {k} cfg {c}: {out[c][0]:.4f} ms over {nt} tiles")
+        log(f"[tile_cost] {scheme.name} phase {phase} K {k} cfg {c} row tiles {reuse}: "
+            f"{out[c][0]:.4f} ms over {nt} tiles")
     del mb, sets
     torch.cuda.empty_cache()
     return out
 
 
 def profile(schemes=None, k_lo: int = 1024, k_hi: int = 4096, reps: int = 5, log=print) -> dict:
+    """Per (phase, scheme, configuration) [a, bs, bu]: every configuration is
+    timed with one row tile per group at K = k_lo and k_hi, giving a and the
+    slope b1 = bs + bu; the scheme's largest configuration also with
+    REUSE_ROWS row tiles per group, giving the slope bR = bs + bu / REUSE_ROWS,
+    so bu = (b1 - bR) R / (R - 1) (>= 0) and bs = b1 - bu; a is the mean of the
+    two fits' intercepts.  Smaller configurations hold one row tile per group
+    whatever the rows, so they keep bs = b1, bu = 0."""
     from . import workloads as W
     schemes = list(schemes or W.ALL_SCHEMES)
-    table = {"P": P_SLOTS, "k_points": [k_lo, k_hi], "unit": "ns per tile; c_t(K) = a + b * K / 128",
+    R = REUSE_ROWS
+    kb_lo, kb_hi = k_lo / 128.0, k_hi / 128.0
+    table = {"P": P_SLOTS, "k_points": [k_lo, k_hi], "reuse_rows": R, "slice_ns": SLICE_NS,
+             "unit": "ns per tile; c_t(K, mt) = a + K / 128 * (bs + bu / mt)",
              "cost": {"0": {}, "1": {}}, "raw": {"0": {}, "1": {}}}
     for s in schemes:
         for phase in (0, 1):
-            cfgs = [0, 1, 2] if pick_cfg(1 << 20, s, phase) == 2 else [0, 1, 2, 3]   # kinds capped at 64-row tiles
+            top = pick_cfg(1 << 20, s, phase)            # kinds capped at 64-row tiles stop at 2
+            cfgs = list(range(top + 1))
             lo = _probe(s, phase, k_lo, cfgs, reps, log=log)
             hi = _probe(s, phase, k_hi, cfgs, reps, log=log)
-            ab = []
-            raw = []
+            rlo = _probe(s, phase, k_lo, [top], reps, reuse=R, log=log)
+            rhi = _probe(s, phase, k_hi, [top], reps, reuse=R, log=log)
+            per_tile = lambda r, c: r[c][0] * 1e6 * P_SLOTS / r[c][1]
+            ab, raw = [], []
             for c in range(N_CFG):
-                cc = c if c in cfgs else 2
-                c1 = lo[cc][0] * 1e6 * P_SLOTS / lo[cc][1]
-                c2 = hi[cc][0] * 1e6 * P_SLOTS / hi[cc][1]
-                b = (c2 - c1) / ((k_hi - k_lo) / 128.0)
-                a = c1 - b * (k_lo / 128.0)
-                ab.append([round(a, 1), round(b, 2)])
-                raw.append([round(c1, 1), round(c2, 1)])
+                cc = min(c, top)
+                c1, c2 = per_tile(lo, cc), per_tile(hi, cc)
+                b1 = (c2 - c1) / (kb_hi - kb_lo)
+                a1 = c1 - b1 * kb_lo
+                if cc == top:
+                    r1, r2 = per_tile(rlo, top), per_tile(rhi, top)
+                    bR = (r2 - r1) / (kb_hi - kb_lo)
+                    aR = r1 - bR * kb_lo
+                    bu = max(0.0, (b1 - bR) * R / (R - 1))
+                    bs = b1 - bu
+                    a = 0.5 * (a1 + aR)
+                    raw.append([round(c1, 1), round(c2, 1), round(r1, 1), round(r2, 1)])
+                else:
+                    bs, bu, a = b1, 0.0, a1
+                    raw.append([round(c1, 1), round(c2, 1)])
+                ab.append([round(a, 1), round(bs, 2), round(bu, 2)])
             table["cost"][str(phase)][s.name] = ab
             table["raw"][str(phase)][s.name] = raw
     return table

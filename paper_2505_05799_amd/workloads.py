@@ -548,6 +548,20 @@ def make_linears(cfg: BlockConfig, seed: int = 0, threads: Optional[int] = None)
     return out
 
 
+def random_tile_costs(seed: int) -> np.ndarray:
+    """A seeded tile cost table of the run-time plan's shape, int32
+    [phase][scheme][configuration][a, bs, bu, h] in ps: a in [0.1, 10] us,
+    bs and bu in [0, 10] us per k block (a quarter of the entries with bu = 0),
+    h in [0, 10] us."""
+    rng = np.random.default_rng(seed)
+    t = np.zeros((2, len(ALL_SCHEMES), 4, 4), dtype=np.int64)
+    t[..., 0] = rng.integers(100_000, 10_000_000, t.shape[:-1])
+    t[..., 1] = rng.integers(0, 10_000_000, t.shape[:-1])
+    t[..., 2] = rng.integers(0, 10_000_000, t.shape[:-1]) * (rng.random(t.shape[:-1]) > 0.25)
+    t[..., 3] = rng.integers(0, 10_000_000, t.shape[:-1])
+    return t.astype(np.int32)
+
+
 def make_block(cfg: BlockConfig | str, seed: int = 0, T: Optional[int] = None,
                with_weights: bool = True) -> Block:
     if isinstance(cfg, str):

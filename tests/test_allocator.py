@@ -64,7 +64,7 @@ def test_tile_counts_and_configuration_match_the_plan():
     for s in W.ALL_SCHEMES:
         lins = [W.QLinear(s, 1408, 2048, None) for _ in counts]
         for phase in (0, 1):
-            plan, _ = O.tile_plan(counts, lins, phase, partial_floats=0)
+            plan, _ = O.tile_plan(counts, lins, phase, TC.CostTable.load().device_table(), partial_floats=0)
             for m, r in zip(counts, plan):
                 if m == 0:
                     continue

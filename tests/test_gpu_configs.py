@@ -44,31 +44,13 @@ def plan_misc(mb, T, G, cap):
     return p[o_ctr + 64: o_ctr + 80]
 
 
-@pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", NAMES)
-def test_full_workload(name):
+def check_plan(mb, blk, r, costs):
+    """The tile plan of the last forward, bit-exact against the oracle's plan
+    under the cost table `costs`: configuration, tile counts, cost, rank, queue
+    order, the per-XCD queues of super-tiles and their expansion to tiles."""
     torch = torch_mod()
-    t0 = time.perf_counter()
-    blk = W.make_block(name)
     cfg = blk.cfg
-    say(f"[{name}] inputs {time.perf_counter() - t0:.1f}s")
-    mb = M.MoEBlock(blk)
-    x, ids, w = upload_inputs(blk)
-    y = mb.forward(x, ids, w)
-    torch.cuda.synchronize()
-    say(f"[{name}] forward done {time.perf_counter() - t0:.1f}s")
-    T, k, E, G = cfg.T, cfg.k, cfg.E, cfg.E + cfg.n_shared
-
-    # routing, bit-exact
-    r = O.route(blk.topk_ids, E)
-    assert np.array_equal(mb.ws_view("counts", torch.int32, E, T).cpu().numpy(), r["counts"])
-    assert np.array_equal(mb.ws_view("offsets", torch.int32, E + 1, T).cpu().numpy(), r["offsets"])
-    assert np.array_equal(mb.ws_view("sorted_pair", torch.int32, T * k, T).cpu().numpy(), r["sorted_pair"])
-    assert np.array_equal(mb.ws_view("inv", torch.int32, T * k, T).cpu().numpy(), r["inv"])
-    assert int(mb.ws_view("status", torch.int32, 1, T).cpu().numpy()[0]) == 0
-
-    # tile plan, bit-exact: configuration, tile counts, cost, rank, queue order,
-    # and the per-XCD queues of super-tiles
+    T, E, G = cfg.T, cfg.E, cfg.E + cfg.n_shared
     lay = mb.workspace_layout(T)
     cap = lay["plan_queue_cap"]
     o_ord = 2 * G * PF_N
@@ -81,7 +63,7 @@ def test_full_workload(name):
     assert nwg == 2 * torch.cuda.get_device_properties(0).multi_processor_count
     for phase in (0, 1):
         lins = [blk.linears[g][0 if phase == 0 else 2] for g in range(G)]
-        want, order = O.tile_plan(ms, lins, phase, partial_floats=lay["partial_floats"], nwg=nwg)
+        want, order = O.tile_plan(ms, lins, phase, costs, partial_floats=lay["partial_floats"], nwg=nwg)
         for g in range(G):
             got = rec[phase, g]
             assert got[1] == ms[g] and got[2] == want[g]["cfg"], (phase, g)
@@ -108,8 +90,67 @@ def test_full_workload(name):
             assert np.array_equal(fl[x, : len(tiles[x])].astype(np.int64), exp.reshape(-1, 4)), (phase, x)
     assert plan_misc(mb, T, G, cap)[4] == 0      # no queue overflow
 
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", NAMES)
+def test_full_workload(name):
+    torch = torch_mod()
+    t0 = time.perf_counter()
+    blk = W.make_block(name)
+    cfg = blk.cfg
+    say(f"[{name}] inputs {time.perf_counter() - t0:.1f}s")
+    mb = M.MoEBlock(blk)
+    x, ids, w = upload_inputs(blk)
+    y = mb.forward(x, ids, w)
+    torch.cuda.synchronize()
+    say(f"[{name}] forward done {time.perf_counter() - t0:.1f}s")
+    T, k, E, G = cfg.T, cfg.k, cfg.E, cfg.E + cfg.n_shared
+
+    # routing, bit-exact
+    r = O.route(blk.topk_ids, E)
+    assert np.array_equal(mb.ws_view("counts", torch.int32, E, T).cpu().numpy(), r["counts"])
+    assert np.array_equal(mb.ws_view("offsets", torch.int32, E + 1, T).cpu().numpy(), r["offsets"])
+    assert np.array_equal(mb.ws_view("sorted_pair", torch.int32, T * k, T).cpu().numpy(), r["sorted_pair"])
+    assert np.array_equal(mb.ws_view("inv", torch.int32, T * k, T).cpu().numpy(), r["inv"])
+    assert int(mb.ws_view("status", torch.int32, 1, T).cpu().numpy()[0]) == 0
+
+    check_plan(mb, blk, r, M.get_tile_costs())
+
     # every token, stage by stage
     rep = check_forward(mb, blk, y, log=say if G <= 16 else None)
     say(f"[{name}] all {T} tokens: {rep.line()}; {time.perf_counter() - t0:.1f}s")
     del mb
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("table", ["default", "random11", "random12"])
+@pytest.mark.parametrize("name", ["dsv2lite", "qwen15_mixed"])
+def test_plan_follows_the_cost_table(name, table):
+    """The run-time plan prices tiles with whatever cost table is installed
+    (mxmoe_set_tile_costs): the library's roofline default or a seeded random
+    table give the oracle's plan under that table, and the forward's output
+    stays correct; the profiled table is reinstalled afterwards."""
+    from paper_2505_05799_amd import tile_cost as TC
+    torch = torch_mod()
+    blk = W.make_block(name)
+    say(f"[{name}] cost table {table}")
+    try:
+        if table == "default":
+            M.set_tile_costs(None)
+        else:
+            M.set_tile_costs(W.random_tile_costs(int(table[6:])))
+        costs = M.get_tile_costs()
+        if table != "default":
+            assert np.array_equal(costs, W.random_tile_costs(int(table[6:])))
+        mb = M.MoEBlock(blk)
+        x, ids, w = upload_inputs(blk)
+        y = mb.forward(x, ids, w)
+        torch.cuda.synchronize()
+        check_plan(mb, blk, O.route(blk.topk_ids, blk.cfg.E), costs)
+        rep = check_forward(mb, blk, y)
+        say(f"[{name}] {table}: {rep.line()}")
+        del mb
+    finally:
+        M.set_tile_costs(TC.CostTable.load().device_table())
+    assert np.array_equal(M.get_tile_costs(), TC.CostTable.load().device_table())

@@ -586,11 +586,48 @@ def test_runtime_model_many_tiles():
     assert errs[-1] < 0.01 and errs[0] > errs[-1]
 
 
+def _cost_table(which: str):
+    from paper_2505_05799_amd import tile_cost as TC
+    return TC.CostTable.load().device_table() if which == "profiled" else W.random_tile_costs(int(which[6:]))
+
+
+def test_tile_cost_of_the_table():
+    """The plan's tile cost against the profiled model it encodes: the table
+    in ps prices every tile within the rounding of its coefficients (1 ps per
+    term) of the continuous model c_t(K, mt) = a + K/128 (bs + bu / mt) in ns;
+    a larger mt never costs more; a sliced tile pays the hand-off h once; the
+    clamp holds at both ends."""
+    from paper_2505_05799_amd import tile_cost as TC
+    t = TC.CostTable.load()
+    dev = t.device_table()
+    for ph in (0, 1):
+        for s in W.ALL_SCHEMES:
+            i = O.scheme_index(s)
+            assert W.ALL_SCHEMES[i] is s
+            for c in range(4):
+                e = dev[ph][i][c]
+                for kb in (1, 8, 28, 160):
+                    prev = None
+                    for mt in (1, 2, 3, 8, 128):
+                        got = O._tile_cost(e, kb, 1, mt)
+                        want = t.tile_ns(ph, s, c, kb * 128, mt) * 1000.0
+                        assert abs(got - min(max(want, 1.0), 2e9)) <= 2 + kb * 2, (ph, s.name, c, kb, mt)
+                        assert prev is None or got <= prev
+                        prev = got
+                    assert O._tile_cost(e, kb, 2, 1) - O._tile_cost(e, kb, 1, 1) == min(
+                        int(e[3]), 2 * 10**9 - O._tile_cost(e, kb, 1, 1))
+    assert O._tile_cost((0, 0, 0, 0), 5, 1, 1) == 1
+    assert O._tile_cost((2 * 10**9, 10**7, 0, 0), 500, 1, 1) == 2 * 10**9
+    assert O._tile_cost((0, 0, 7, 0), 3, 1, 4) == 5        # floor(21 / 4)
+
+
+@pytest.mark.parametrize("table", ["profiled", "random1", "random2"])
 @pytest.mark.parametrize("nwg", [2, 64, 512])
-def test_tile_plan_slices_minimal(nwg):
+def test_tile_plan_slices_minimal(nwg, table):
     """Slicing invariants: with an ample partial buffer a group takes the fewest
     slices whose tile cost is within the threshold, or if there are none the
     cheapest tile's slice count; a budget of zero floats slices nothing."""
+    costs = _cost_table(table)
     blk = W.make_block("dsv2lite", with_weights=False)
     cfg = blk.cfg
     counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E).tolist() + [cfg.T] * cfg.n_shared
@@ -599,44 +636,59 @@ def test_tile_plan_slices_minimal(nwg):
                           (cfg.F_shared if phase == 0 else cfg.H),
                           k if e < cfg.E else (cfg.H if phase == 0 else cfg.F_shared), None)
                 for e, s in enumerate(W.schemes_of(cfg))]
-        plan, _ = O.tile_plan(counts, lins, phase, partial_floats=1 << 40, nwg=nwg)
-        nl = 2 if phase == 0 else 1
-        bms, bns = (16, 32, 64, 128), ((256, 256, 128, 128), (512, 512, 256, 256))[phase]
-        work = sum(r["mtiles"] * r["ntiles"] * O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme,
-                                                           lin.k // 128 * 128, 1, r["mtiles"], r["ntiles"])
+        plan, _ = O.tile_plan(counts, lins, phase, costs, partial_floats=1 << 40, nwg=nwg)
+        entry = lambda r, lin: costs[phase][O.scheme_index(lin.scheme)][r["cfg"]]
+        work = sum(r["mtiles"] * r["ntiles"] * O._tile_cost(entry(r, lin), lin.k // 128, 1, r["mtiles"])
                    for r, lin in zip(plan, lins) if r["mtiles"] * r["ntiles"])
         theta = work // nwg // 2
+        fb_groups = []
         for r, lin in zip(plan, lins):
             if r["mtiles"] * r["ntiles"] == 0:
                 assert r["split"] == 1
                 continue
             kb = lin.k // 128
             smax = max(1, min(8, kb // 6))
-            cost = lambda sp: O._tile_cost(bms[r["cfg"]], bns[r["cfg"]], nl, lin.scheme, -(-kb // sp) * 128, sp,
-                                           r["mtiles"], r["ntiles"])
+            cost = lambda sp: O._tile_cost(entry(r, lin), -(-kb // sp), sp, r["mtiles"])
             sp = r["split"]
             assert 1 <= sp <= smax
+            assert r["cost"] == cost(sp)
             if cost(sp) <= theta:   # the fewest slices within the threshold
                 assert sp == 1 or cost(sp - 1) > theta
-            else:                   # none within it: the cheapest tile
+            elif sp > 1:            # none within it: the cheapest tile
                 assert all(cost(s) > theta for s in range(1, smax + 1))
                 assert cost(sp) == min(cost(s) for s in range(1, smax + 1))
                 assert all(cost(s) > cost(sp) for s in range(1, sp))
-        none, _ = O.tile_plan(counts, lins, phase, partial_floats=0, nwg=nwg)
+            else:                   # unsliced: S = 1 is the cheapest, or slicing would pass nwg tiles
+                cheapest = min(range(1, smax + 1), key=lambda s: (cost(s), s))
+                fb_groups.append((r, cheapest))
+        # a fallback group left unsliced although slicing was cheaper: its added
+        # tiles would have taken the phase past one tile per workgroup
+        unsliced = sum(r["mtiles"] * r["ntiles"] for r in plan)
+        added = 0
+        for r in plan:
+            if r["split"] > 1:
+                added += r["mtiles"] * r["ntiles"] * (r["split"] - 1)
+        refused = [r for r, cheapest in fb_groups if cheapest > 1]
+        if refused:   # the first refused one would have passed nwg tiles
+            r0 = refused[0]
+            cheapest0 = dict((id(r), c) for r, c in fb_groups)[id(r0)]
+            assert unsliced + added + r0["mtiles"] * r0["ntiles"] * (cheapest0 - 1) > nwg
+        none, _ = O.tile_plan(counts, lins, phase, costs, partial_floats=0, nwg=nwg)
         assert all(r["split"] == 1 for r in none)
     # numpy int32 row counts (as routing returns them) plan like Python ints:
     # the phase's work sum exceeds 32 bits at full size
     big = [c * 64 for c in counts]
-    assert O.tile_plan([np.int32(c) for c in big], lins, 1, partial_floats=1 << 40)[0] == \
-        O.tile_plan(big, lins, 1, partial_floats=1 << 40)[0]
+    assert O.tile_plan([np.int32(c) for c in big], lins, 1, costs, partial_floats=1 << 40)[0] == \
+        O.tile_plan(big, lins, 1, costs, partial_floats=1 << 40)[0]
     # fewer workgroups -> a larger threshold -> never more slices
-    a, _ = O.tile_plan(counts, lins, 1, partial_floats=1 << 40, nwg=2)
-    b, _ = O.tile_plan(counts, lins, 1, partial_floats=1 << 40, nwg=512)
+    a, _ = O.tile_plan(counts, lins, 1, costs, partial_floats=1 << 40, nwg=2)
+    b, _ = O.tile_plan(counts, lins, 1, costs, partial_floats=1 << 40, nwg=512)
     assert all(x["split"] <= y["split"] for x, y in zip(a, b))
 
 
+@pytest.mark.parametrize("table", ["profiled", "random3"])
 @pytest.mark.parametrize("name", ["tiny", "dsv2lite", "qwen15_mixed", "qwen15_w5a5"])
-def test_tile_plan_covers_every_output(name):
+def test_tile_plan_covers_every_output(name, table):
     blk = W.make_block(name, with_weights=False)
     cfg = blk.cfg
     counts = np.bincount(blk.topk_ids.ravel(), minlength=cfg.E).tolist() + [cfg.T] * cfg.n_shared
@@ -645,7 +697,7 @@ def test_tile_plan_covers_every_output(name):
                           (cfg.F_shared if phase == 0 else cfg.H),
                           k if e < cfg.E else (cfg.H if phase == 0 else cfg.F_shared), None)
                 for e, s in enumerate(W.schemes_of(cfg))]
-        plan, order = O.tile_plan(counts, lins, phase, partial_floats=1 << 26)
+        plan, order = O.tile_plan(counts, lins, phase, _cost_table(table), partial_floats=1 << 26)
         for m, lin, r in zip(counts, lins, plan):
             bm = (16, 32, 64, 128)[r["cfg"]]
             bn = ((256, 256, 128, 128), (512, 512, 256, 256))[phase][r["cfg"]]
