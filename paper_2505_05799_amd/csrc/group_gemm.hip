@@ -26,44 +26,6 @@ namespace {
 
 struct MaskBits { uint32_t w[64]; };
 
-// In-place exclusive scan of n ints v[0], v[stride], ... by one workgroup
-// (chunk sums per thread, wavefront prefix sums, then wavefront totals);
-// returns the sum.  v and red: LDS (barriers wait for LDS traffic only), red
-// holding blockDim/64 + 1 ints.
-__device__ int block_scan(int32_t* v, int n, int32_t* red, int stride = 1) {
-  const int tid = threadIdx.x, nt = blockDim.x, lane = tid & 63, w = tid >> 6, nw = nt >> 6;
-  const int per = (n + nt - 1) / nt;
-  const int lo = tid * per, hi = min(n, lo + per);
-  int s = 0;
-  for (int i = lo; i < hi; ++i) s += v[(int64_t)i * stride];
-  int incl = s;
-  for (int d = 1; d < 64; d <<= 1) {
-    const int t = __shfl_up(incl, d, 64);
-    if (lane >= d) incl += t;
-  }
-  if (lane == 63) red[w] = incl;
-  lds_barrier();
-  if (tid == 0) {
-    int run = 0;
-    for (int i = 0; i < nw; ++i) {
-      const int t = red[i];
-      red[i] = run;
-      run += t;
-    }
-    red[nw] = run;
-  }
-  lds_barrier();
-  int run = red[w] + incl - s;
-  for (int i = lo; i < hi; ++i) {
-    const int t = v[(int64_t)i * stride];
-    v[(int64_t)i * stride] = run;
-    run += t;
-  }
-  const int total = red[nw];
-  lds_barrier();
-  return total;
-}
-
 // x / d for 0 <= x < 2^22 and 1 <= d < 2^22, exactly: a float reciprocal
 // estimate (within one of the quotient there) and one correction step; a
 // fraction of the cost of a general integer division, which the plan's
@@ -114,13 +76,13 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   __shared__ int32_t s_order[2][kMaxG];   // group per rank
   __shared__ int32_t s_c1[2][kMaxG];      // unsliced tile cost
   __shared__ int32_t s_cs[2][kMaxG];      // tile cost with the proposed slices
-  __shared__ int32_t s_red[1025];
   __shared__ int64_t s_work[2][1024 / 64];
   __shared__ int64_t s_theta[2];          // slicing threshold per phase
   __shared__ int32_t s_ut[2][1024 / 64];  // unsliced tiles per wavefront, then per phase in [p][0]
   __shared__ int32_t s_used[2];           // output-tile counters used per phase
   __shared__ int32_t s_tc[kCostEntries];  // tile cost table
   __shared__ int32_t s_ng[2];             // groups with tiles per phase
+  __shared__ int32_t s_nst[2];            // super-tiles per phase
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nwave = blockDim.x >> 6;
   const int nphase = raw_m >= 0 ? 1 : 2;
   const PlanLayout PL = plan_layout(G, qcap, fcap);
@@ -197,15 +159,17 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     }
   }
   lds_barrier();
-  if (tid < nphase) {
-    int64_t work = 0;
-    int ut = 0;
-    for (int i = 0; i < nwave; ++i) {
-      work += s_work[tid][i];
-      ut += s_ut[tid][i];
+  if (wave < nphase) {  // wavefront p sums phase p's per-wavefront totals
+    int64_t work = lane < nwave ? s_work[wave][lane] : 0;
+    int ut = lane < nwave ? s_ut[wave][lane] : 0;
+    for (int d = 32; d > 0; d >>= 1) {
+      work += __shfl_xor(work, d, 64);
+      ut += __shfl_xor(ut, d, 64);
     }
-    s_theta[tid] = work / nwg / kSplitShare;
-    s_ut[tid][0] = ut;
+    if (lane == 0) {
+      s_theta[wave] = work / nwg / kSplitShare;
+      s_ut[wave][0] = ut;
+    }
   }
   lds_barrier();
   // The slice rule (kSplitShare, kSplitMinKb), evaluated by eight lanes per group: lane
@@ -375,44 +339,31 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
   }
   lds_barrier();
   // 4. rank the groups by decreasing tile cost (ties: lower group first):
-  //    up to 256 groups one thread counts the groups ahead of one group,
-  //    beyond that one wavefront does
-  if (G <= 256) {
-    for (int item = tid; item < nphase * G; item += blockDim.x) {
-      const int ph = item >= G, g = item - ph * G;
+  //    one wavefront per group, each lane tests the groups of one chunk of 64
+  //    and a ballot counts those ahead; the first chunk's costs stay in
+  //    registers across the wavefront's groups of a phase
+  for (int ph = 0; ph < nphase; ++ph) {
+    const int own_c = lane < G ? s_cost[ph][lane] : 0;
+    const bool own_l = lane < G && s_tiles[ph][lane] > 0;
+    for (int g = wave; g < G; g += nwave) {
       int rank = -1;
       if (s_tiles[ph][g] > 0) {
         const int cg = s_cost[ph][g];
         int ahead = 0;
-        for (int h = 0; h < G; ++h) {
-          const int ch = s_cost[ph][h];
-          ahead += s_tiles[ph][h] > 0 && ((ch > cg) || (ch == cg && h < g));
+        for (int c0 = 0; c0 < G; c0 += 64) {
+          const int h = c0 + lane;
+          const int ch = c0 == 0 ? own_c : (h < G ? s_cost[ph][h] : 0);
+          const bool live = c0 == 0 ? own_l : (h < G && s_tiles[ph][h] > 0);
+          ahead += __popcll(__ballot(live && (ch > cg || (ch == cg && h < g))));
         }
         rank = ahead;
-        s_order[ph][rank] = g;
-        order[(int64_t)ph * G + rank] = g;
+        if (lane == 0) {
+          s_order[ph][rank] = g;
+          order[(int64_t)ph * G + rank] = g;
+        }
       }
-      rec_of(ph, g)[PF_RANK] = rank;
+      if (lane == 0) rec_of(ph, g)[PF_RANK] = rank;
     }
-  } else
-  for (int item = wave; item < nphase * G; item += nwave) {
-    const int ph = item >= G, g = item - ph * G;
-    int rank = -1;
-    if (s_tiles[ph][g] > 0) {
-      const int cg = s_cost[ph][g];
-      int ahead = 0;
-      for (int h = lane; h < G; h += 64) {
-        const int ch = s_cost[ph][h];
-        ahead += s_tiles[ph][h] > 0 && ((ch > cg) || (ch == cg && h < g));
-      }
-      for (int d = 32; d > 0; d >>= 1) ahead += __shfl_xor(ahead, d, 64);
-      rank = ahead;
-      if (lane == 0) {
-        s_order[ph][rank] = g;
-        order[(int64_t)ph * G + rank] = g;
-      }
-    }
-    if (lane == 0) rec_of(ph, g)[PF_RANK] = rank;
   }
   lds_barrier();
   // 5. super-tiles dealt to the XCD queues, 6. expanded to tile entries;
@@ -435,8 +386,27 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
     }
   }
   lds_barrier();
+  // exclusive prefix sums of the super-tile counts in rank order, one
+  //    wavefront per phase, 64 ranks at a time
+  if (wave < nphase) {
+    const int ph = wave, n = s_ng[ph];
+    int run = 0;
+    for (int c0 = 0; c0 < n; c0 += 64) {
+      const int i = c0 + lane;
+      const int v = i < n ? s_cost[ph][i] : 0;
+      int incl = v;
+      for (int d = 1; d < 64; d <<= 1) {
+        const int t = __shfl_up(incl, d, 64);
+        if (lane >= d) incl += t;
+      }
+      if (i < n) s_cost[ph][i] = run + incl - v;
+      run += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) s_nst[ph] = run;
+  }
+  lds_barrier();
   int S_ph[2] = {0, 0};
-  for (int ph = 0; ph < nphase; ++ph) S_ph[ph] = block_scan(s_cost[ph], s_ng[ph], s_red);
+  for (int ph = 0; ph < nphase; ++ph) S_ph[ph] = s_nst[ph];
   if (tid < nphase) {
     if ((S_ph[tid] + kXcd - 1) / kXcd > qcap) misc[4] = 1;  // cannot happen with the host's capacity bound
     misc[2 + tid] = s_ng[tid];

@@ -232,7 +232,10 @@ __host__ __device__ constexpr inline int cost_index(int ph, int kd, int cfg) {
 }
 constexpr int64_t kCostMaxPs = 2000000000LL;
 __host__ __device__ inline int32_t tile_cost(const int32_t* e, int kb, int split, int mt) {
-  int64_t c = (int64_t)e[0] + (int64_t)kb * e[1] + (int64_t)kb * e[2] / (mt > 0 ? mt : 1) + (split > 1 ? e[3] : 0);
+  const int64_t wu = (int64_t)kb * e[2];  // >= 0; a 32-bit quotient where it fits
+  const uint32_t d = mt > 0 ? (uint32_t)mt : 1u;
+  const int64_t shared = wu < (1LL << 32) ? (int64_t)((uint32_t)wu / d) : wu / d;
+  int64_t c = (int64_t)e[0] + (int64_t)kb * e[1] + shared + (split > 1 ? e[3] : 0);
   c = c < 1 ? 1 : (c > kCostMaxPs ? kCostMaxPs : c);
   return (int32_t)c;
 }

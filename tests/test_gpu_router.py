@@ -70,16 +70,18 @@ def test_router_rejects():
 
 
 @pytest.mark.parametrize("renorm", [False, True])
-def test_forward_from_logits(renorm):
+@pytest.mark.parametrize("T", [300, 2500])
+def test_forward_from_logits(renorm, T):
     """Router mode of the forward: same ids and weights as the standalone
     router, the same output bit for bit as the forward given those ids, and
-    the oracle's output with the sigmoid shared gates."""
+    the oracle's output with the sigmoid shared gates; 300 x 2 pairs route in
+    the one-workgroup routing kernel, 2500 x 2 in the chunked launches."""
     torch = torch_mod()
     sch = [(W.W4G128,) * 3, (W.W8A8, W.W8A8, W.W2G128), (W.W4A4,) * 3, (W.W16,) * 3, (W.W4A4G128,) * 3,
            (W.W3G128, W.W3G128, W.W8A8), (W.W8A8,) * 3]
-    blk = W.random_small_block(77, T=300, H=256, F=384, E=6, k=2, n_shared=1, F_shared=256, act="bf16",
+    blk = W.random_small_block(77, T=T, H=256, F=384, E=6, k=2, n_shared=1, F_shared=256, act="bf16",
                                schemes=sch)
-    T, E, k = 300, 6, 2
+    E, k = 6, 2
     l, sh = W.router_logits(T, E, seed=9, zipf_s=1.0, n_shared=1)
     lt, sht = torch.from_numpy(l).cuda(), torch.from_numpy(sh).cuda()
     mb = M.MoEBlock(blk)
