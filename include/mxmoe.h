@@ -305,9 +305,10 @@ typedef struct {
    * 3 down Group-GEMM, 4 combine).                                          */
   hipEvent_t* events;
   /* fp32 [T, E] router logits, or NULL.  When set, the forward starts with
-   * the router front-end of mxmoe_router_topk: topk_ids / topk_w may then be
-   * NULL and are not read; the chosen ids and weights land in the workspace
-   * (router_ids / router_w of mxmoe_ws_layout).                              */
+   * the router front-end of mxmoe_router_topk (same results; inside the
+   * routing launch when T*k <= 4096, E <= 64 and k <= 8): topk_ids / topk_w
+   * may then be NULL and are not read; the chosen ids and weights land in the
+   * workspace (router_ids / router_w of mxmoe_ws_layout).                    */
   const float* router_logits;
   int32_t renormalize;           /* with router_logits: as in mxmoe_router_topk */
   /* With router_logits: fp32 [T, n_shared] shared-expert gate logits or NULL;

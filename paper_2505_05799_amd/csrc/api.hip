@@ -589,19 +589,23 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   const int32_t* ids = topk_ids;
   const float* tw = topk_w;
   const float* shw = opts ? opts->shared_w : nullptr;
-  if (router) {
+  if (router) {  // in the routing launch where the batch allows
     int32_t* rids = at<int32_t>(workspace, L.rids);
     float* rw = at<float>(workspace, L.rw);
     float* rshw = (bi.nsh && opts->shared_logits) ? at<float>(workspace, L.shw) : nullptr;
-    MX_CHECK(launch_router_topk(opts->router_logits, T, bi.E, bi.k, opts->renormalize, rshw ? opts->shared_logits : nullptr,
-                                bi.nsh, rids, rw, rshw, stream));
+    MX_CHECK(launch_router_route(opts->router_logits, T, bi.E, bi.k, opts->renormalize,
+                                 rshw ? opts->shared_logits : nullptr, bi.nsh, rids, rw, rshw, counts, offsets,
+                                 sorted_pair, at<int32_t>(workspace, L.inv), at<int32_t>(workspace, L.status),
+                                 at<int32_t>(workspace, L.chunk_counts), at<int32_t>(workspace, L.chunk_bad),
+                                 stream));
     ids = rids;
     tw = rw;
     shw = rshw;
+  } else {
+    MX_CHECK(launch_route(ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
+                          at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
+                          at<int32_t>(workspace, L.chunk_bad), stream));
   }
-  MX_CHECK(launch_route(ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
-                        at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
-                        at<int32_t>(workspace, L.chunk_bad), stream));
   DevLinear none;
   memset(&none, 0, sizeof(none));
   const int grid = group_gemm_grid(current_device());

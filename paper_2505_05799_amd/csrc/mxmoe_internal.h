@@ -286,6 +286,13 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
 constexpr int kRouterMaxK = 64;
 hipError_t launch_router_topk(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
                               int n_sh, int32_t* ids, float* w, float* shared_w, hipStream_t s);
+// The router front-end followed by routing of the ids it writes: one launch
+// where the batch fits the one-workgroup routing kernel (E <= 64, k <= 8),
+// else the two calls above.  Results equal those of the two calls.
+hipError_t launch_router_route(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
+                               int n_sh, int32_t* ids, float* w, float* shared_w, int32_t* counts,
+                               int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
+                               int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
 
 // Row sums of each 128-wide block of bf16 rows: out[r][b] = sum of a[r][128b ..
 // 128b + 127] in fp32; cols a multiple of 128, rows 16-byte aligned.

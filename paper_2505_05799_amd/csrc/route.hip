@@ -15,6 +15,8 @@
 //                      wavefront finds lanes with equal expert ids with one
 //                      ballot per id bit, ranks them by lane, and wavefront
 //                      totals are combined through LDS in wavefront order.
+#include <cstring>
+
 #include "mxmoe_internal.h"
 
 namespace mxmoe {
@@ -163,6 +165,230 @@ __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restr
   }
 }
 
+// ---------------------------------------------------------- router front-end
+// Eq. (2) weights its experts by the router's softmax.  One wavefront per
+// token; lane l holds the logits of experts l, l + 64, ... in registers.  The
+// k largest are found in k rounds of a wavefront arg-max under the strict
+// order (larger logit, then lower id), which all lanes agree on, so the
+// result is unique and every lane of the butterfly ends with the same value.
+constexpr int kRouterJ = kMaxE / 64;
+
+__device__ inline bool router_better(float va, int ea, float vb, int eb) {
+  return va > vb || (va == vb && ea < eb);
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int d = 32; d; d >>= 1) v += __shfl_xor(v, d, 64);
+  return v;
+}
+
+struct RouterArgs {
+  const float* logits;  // [T, E]
+  int k, renorm;
+  const float* shared_logits;  // [T, n_sh] or null
+  int n_sh;
+  int32_t* ids;  // [T, k]
+  float* w;      // [T, k]
+  float* shared_w;
+};
+
+// Token t by the calling wavefront.
+__device__ void router_token_wave(const RouterArgs& ra, int t, int E, int lane) {
+  const float* __restrict__ logits = ra.logits;
+  const int k = ra.k, renorm = ra.renorm, n_sh = ra.n_sh;
+  const float* __restrict__ shared_logits = ra.shared_logits;
+  int32_t* __restrict__ ids = ra.ids;
+  float* __restrict__ w = ra.w;
+  float* __restrict__ shared_w = ra.shared_w;
+  const float* row = logits + (int64_t)t * E;
+  const int J = (E + 63) >> 6;
+  float v[kRouterJ];
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < kRouterJ; ++j) {
+    const int e = lane + 64 * j;
+    v[j] = (j < J && e < E) ? row[e] : -INFINITY;
+    m = fmaxf(m, v[j]);
+  }
+#pragma unroll
+  for (int d = 32; d; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+  float se = 0.f;
+#pragma unroll
+  for (int j = 0; j < kRouterJ; ++j)
+    if (j < J && lane + 64 * j < E) se += expf(v[j] - m);
+  se = wave_sum(se);
+
+  uint32_t taken = 0;  // bit j: this lane's v[j] is chosen
+  int my_e = -1;
+  float my_v = -INFINITY;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int be = 0x7fffffff;
+#pragma unroll
+    for (int j = 0; j < kRouterJ; ++j) {
+      const int e = lane + 64 * j;
+      if (j < J && e < E && !((taken >> j) & 1u) && router_better(v[j], e, bv, be)) {
+        bv = v[j];
+        be = e;
+      }
+    }
+#pragma unroll
+    for (int d = 32; d; d >>= 1) {
+      const float ov = __shfl_xor(bv, d, 64);
+      const int oe = __shfl_xor(be, d, 64);
+      if (router_better(ov, oe, bv, be)) {
+        bv = ov;
+        be = oe;
+      }
+    }
+    if (be != 0x7fffffff && (be & 63) == lane) taken |= 1u << (be >> 6);
+    if (lane == r) {
+      my_e = be == 0x7fffffff ? -1 : be;
+      my_v = bv;
+    }
+  }
+  const float q = (lane < k && my_e >= 0) ? expf(my_v - m) : 0.f;
+  const float den = renorm ? wave_sum(q) : se;
+  if (lane < k) {
+    ids[(int64_t)t * k + lane] = my_e;
+    w[(int64_t)t * k + lane] = q / den;
+  }
+  if (shared_logits && lane < n_sh)
+    shared_w[(int64_t)t * n_sh + lane] = 1.f / (1.f + expf(-shared_logits[(int64_t)t * n_sh + lane]));
+}
+
+// Token t by a group of 8 lanes (E <= 64, k <= 8): lane j of the group holds
+// experts j, j + 8, ..., j + 56.  Each lane keeps its best k entries sorted;
+// three butterfly steps (partner lane^1, ^2, ^4) merge two sorted lists into
+// the best k of their union (a bitonic merge), so that every lane ends with
+// the token's k best, sorted.  The maximum and the sum of exp(v - max) take
+// the same butterfly, after the lane's own 8 values in expert order.  The
+// best k under the strict order are unique, so the ids equal those of the
+// wavefront form; the weights differ from it only in the order of the sum.
+constexpr int kGroupMaxE = 64;
+constexpr int kGroupMaxK = 8;
+__host__ __device__ constexpr bool router_by_group(int E, int k) { return E <= kGroupMaxE && k <= kGroupMaxK; }
+
+// the strict order without short-circuit evaluation, so that the compare-
+// exchanges below compile to selects rather than branches
+__device__ inline bool router_better_sel(float va, int ea, float vb, int eb) {
+  return (va > vb) | ((va == vb) & (ea < eb));
+}
+__device__ inline void router_cmpx(float& va, int& ea, float& vb, int& eb) {  // (a, b) -> (better, worse)
+  const bool sw = router_better_sel(vb, eb, va, ea);
+  const float xa = sw ? vb : va, xb = sw ? va : vb;
+  const int ya = sw ? eb : ea, yb = sw ? ea : eb;
+  va = xa;
+  vb = xb;
+  ea = ya;
+  eb = yb;
+}
+
+__device__ void router_token_group(const RouterArgs& ra, int t, bool live, int E, int j) {
+  constexpr int K = kGroupMaxK;
+  const float* row = ra.logits + (int64_t)(live ? t : 0) * E;
+  float v[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = (live && j + 8 * i < E) ? row[j + 8 * i] : -INFINITY;
+  const float shl = (live && ra.shared_logits && j < ra.n_sh) ? ra.shared_logits[(int64_t)t * ra.n_sh + j] : 0.f;
+  float m = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m = fmaxf(m, v[i]);
+#pragma unroll
+  for (int d = 1; d < 8; d <<= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
+  float se = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    if (j + 8 * i < E) se += expf(v[i] - m);
+#pragma unroll
+  for (int d = 1; d < 8; d <<= 1) se += __shfl_xor(se, d, 64);
+  // the lane's own list: its 8 entries sorted by a bitonic network, past-E
+  // entries and NaNs replaced by the sentinel (-inf, max int), which every
+  // real entry beats (a NaN is never chosen)
+  float tv[K];
+  int te[K];
+#pragma unroll
+  for (int i = 0; i < K; ++i) {
+    const bool ok = (j + 8 * i < E) & (v[i] == v[i]);
+    tv[i] = ok ? v[i] : -INFINITY;
+    te[i] = ok ? j + 8 * i : 0x7fffffff;
+  }
+#pragma unroll
+  for (int kk = 2; kk <= K; kk <<= 1)
+#pragma unroll
+    for (int jj = kk >> 1; jj > 0; jj >>= 1)
+#pragma unroll
+      for (int i = 0; i < K; ++i) {
+        const int l = i ^ jj;
+        if (l > i) {
+          if ((i & kk) == 0)
+            router_cmpx(tv[i], te[i], tv[l], te[l]);  // better first
+          else
+            router_cmpx(tv[l], te[l], tv[i], te[i]);
+        }
+      }
+  // butterfly merges
+#pragma unroll
+  for (int d = 1; d < 8; d <<= 1) {
+    float ov[K];
+    int oe[K];
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      ov[r] = __shfl_xor(tv[r], d, 64);
+      oe[r] = __shfl_xor(te[r], d, 64);
+    }
+    // the better of tv[r] and ov[K-1-r]: the best K of the union, bitonic
+#pragma unroll
+    for (int r = 0; r < K; ++r) {
+      const bool b = router_better_sel(ov[K - 1 - r], oe[K - 1 - r], tv[r], te[r]);
+      tv[r] = b ? ov[K - 1 - r] : tv[r];
+      te[r] = b ? oe[K - 1 - r] : te[r];
+    }
+    // sort the bitonic sequence: half-cleaners of span 4, 2, 1
+#pragma unroll
+    for (int h = K / 2; h > 0; h >>= 1)
+#pragma unroll
+      for (int r = 0; r < K; ++r)
+        if ((r & h) == 0) router_cmpx(tv[r], te[r], tv[r + h], te[r + h]);
+  }
+  if (!live) return;
+  const int k = ra.k;
+  float q = 0.f, den = 0.f;
+  int my_e = -1;
+#pragma unroll
+  for (int r = 0; r < K; ++r) {
+    const float qr = (r < k && te[r] != 0x7fffffff) ? expf(tv[r] - m) : 0.f;
+    if (r < k) den += qr;
+    if (r == j) {
+      q = qr;
+      my_e = te[r] == 0x7fffffff ? -1 : te[r];
+    }
+  }
+  if (!ra.renorm) den = se;
+  if (j < k) {
+    ra.ids[(int64_t)t * k + j] = my_e;
+    ra.w[(int64_t)t * k + j] = q / den;
+  }
+  if (ra.shared_logits)
+    for (int s2 = j; s2 < ra.n_sh; s2 += 8)
+      ra.shared_w[(int64_t)t * ra.n_sh + s2] =
+          1.f / (1.f + expf(-(s2 == j ? shl : ra.shared_logits[(int64_t)t * ra.n_sh + s2])));
+}
+
+// One wavefront per token, or 8 tokens per wavefront where router_by_group
+// (the launcher sizes the grid to match).
+__global__ void __launch_bounds__(kThreads) router_topk_kernel(RouterArgs ra, int T, int E) {
+  if (router_by_group(E, ra.k)) {
+    const int t = blockIdx.x * (kThreads / 8) + (threadIdx.x >> 3);
+    router_token_group(ra, t, t < T, E, threadIdx.x & 7);  // every lane takes part in the shuffles
+    return;
+  }
+  const int t = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (t >= T) return;  // a whole wavefront leaves together
+  router_token_wave(ra, t, E, threadIdx.x & 63);
+}
+
 // Batches of at most kRouteSmall pairs: the three steps in one workgroup of
 // 1024 threads, with barriers where the launches were.  The pairs are ranked
 // 1024 at a time by the same ballots; positions follow from the expert's base,
@@ -170,17 +396,30 @@ __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restr
 // so the order (expert, then pair id) is the one the chunked launches give.
 constexpr int kRouteSmall = 4096;  // one step costs ~1 us: past 4096 pairs the chunked launches win
 constexpr int kSmallThreads = 1024;
-__global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* __restrict__ ids, int P, int E, int ebits,
+// With ra.logits set (and router_by_group(E, k)) the workgroup first runs the
+// router front-end for the T = P / k tokens, 8 lanes per token, and routes the
+// ids it wrote (ids == ra.ids; the barrier makes them visible to the
+// workgroup).
+__global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* ids, int P, int E, int ebits,
                                                              int32_t* __restrict__ counts,
                                                              int32_t* __restrict__ offsets,
                                                              int32_t* __restrict__ sorted_pair,
-                                                             int32_t* __restrict__ inv, int32_t* __restrict__ status) {
+                                                             int32_t* __restrict__ inv, int32_t* __restrict__ status,
+                                                             RouterArgs ra) {
   constexpr int NW = kSmallThreads / 64;
   __shared__ int32_t base[kMaxE];
   __shared__ int32_t wcnt[NW][kMaxE];
   __shared__ int32_t wsum[NW];
   __shared__ int32_t bad;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  if (ra.logits) {
+    const int T = P / ra.k;
+    for (int t0 = 0; t0 < T; t0 += kSmallThreads / 8) {  // uniform trip count: every lane shuffles
+      const int t = t0 + (tid >> 3);
+      router_token_group(ra, t, t < T, E, tid & 7);
+    }
+    __syncthreads();
+  }
   for (int e = tid; e < E; e += kSmallThreads) base[e] = 0;
   if (tid == 0) bad = 0x7fffffff;
   __syncthreads();
@@ -253,98 +492,33 @@ __global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* __re
   }
 }
 
-// ---------------------------------------------------------- router front-end
-// Eq. (2) weights its experts by the router's softmax.  One wavefront per
-// token; lane l holds the logits of experts l, l + 64, ... in registers.  The
-// k largest are found in k rounds of a wavefront arg-max under the strict
-// order (larger logit, then lower id), which all lanes agree on, so the
-// result is unique and every lane of the butterfly ends with the same value.
-constexpr int kRouterJ = kMaxE / 64;
-
-__device__ inline bool router_better(float va, int ea, float vb, int eb) {
-  return va > vb || (va == vb && ea < eb);
-}
-
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-  for (int d = 32; d; d >>= 1) v += __shfl_xor(v, d, 64);
-  return v;
-}
-
-__global__ void __launch_bounds__(kThreads) router_topk_kernel(const float* __restrict__ logits, int T, int E,
-                                                                int k, int renorm,
-                                                                const float* __restrict__ shared_logits, int n_sh,
-                                                                int32_t* __restrict__ ids, float* __restrict__ w,
-                                                                float* __restrict__ shared_w) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  if (t >= T) return;  // a whole wavefront leaves together
-  const float* row = logits + (int64_t)t * E;
-  const int J = (E + 63) >> 6;
-  float v[kRouterJ];
-  float m = -INFINITY;
-#pragma unroll
-  for (int j = 0; j < kRouterJ; ++j) {
-    const int e = lane + 64 * j;
-    v[j] = (j < J && e < E) ? row[e] : -INFINITY;
-    m = fmaxf(m, v[j]);
-  }
-#pragma unroll
-  for (int d = 32; d; d >>= 1) m = fmaxf(m, __shfl_xor(m, d, 64));
-  float se = 0.f;
-#pragma unroll
-  for (int j = 0; j < kRouterJ; ++j)
-    if (j < J && lane + 64 * j < E) se += expf(v[j] - m);
-  se = wave_sum(se);
-
-  uint32_t taken = 0;  // bit j: this lane's v[j] is chosen
-  int my_e = -1;
-  float my_v = -INFINITY;
-  for (int r = 0; r < k; ++r) {
-    float bv = -INFINITY;
-    int be = 0x7fffffff;
-#pragma unroll
-    for (int j = 0; j < kRouterJ; ++j) {
-      const int e = lane + 64 * j;
-      if (j < J && e < E && !((taken >> j) & 1u) && router_better(v[j], e, bv, be)) {
-        bv = v[j];
-        be = e;
-      }
-    }
-#pragma unroll
-    for (int d = 32; d; d >>= 1) {
-      const float ov = __shfl_xor(bv, d, 64);
-      const int oe = __shfl_xor(be, d, 64);
-      if (router_better(ov, oe, bv, be)) {
-        bv = ov;
-        be = oe;
-      }
-    }
-    if (be != 0x7fffffff && (be & 63) == lane) taken |= 1u << (be >> 6);
-    if (lane == r) {
-      my_e = be == 0x7fffffff ? -1 : be;
-      my_v = bv;
-    }
-  }
-  const float q = (lane < k && my_e >= 0) ? expf(my_v - m) : 0.f;
-  const float den = renorm ? wave_sum(q) : se;
-  if (lane < k) {
-    ids[(int64_t)t * k + lane] = my_e;
-    w[(int64_t)t * k + lane] = q / den;
-  }
-  if (shared_logits && lane < n_sh)
-    shared_w[(int64_t)t * n_sh + lane] = 1.f / (1.f + expf(-shared_logits[(int64_t)t * n_sh + lane]));
-}
-
 }  // namespace
 
 hipError_t launch_router_topk(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
                               int n_sh, int32_t* ids, float* w, float* shared_w, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  const int per = kThreads / 64;
-  hipLaunchKernelGGL(router_topk_kernel, dim3((T + per - 1) / per), dim3(kThreads), 0, s, logits, T, E, k, renorm,
-                     shared_logits, n_sh, ids, w, shared_w);
+  const int per = router_by_group(E, k) ? kThreads / 8 : kThreads / 64;
+  const RouterArgs ra{logits, k, renorm, shared_logits, n_sh, ids, w, shared_w};
+  hipLaunchKernelGGL(router_topk_kernel, dim3((T + per - 1) / per), dim3(kThreads), 0, s, ra, T, E);
   return hipGetLastError();
+}
+
+hipError_t launch_router_route(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
+                               int n_sh, int32_t* ids, float* w, float* shared_w, int32_t* counts,
+                               int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
+                               int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s) {
+  const int P = T * k;
+  if (P > 0 && P <= kRouteSmall && router_by_group(E, k)) {
+    int ebits = 0;
+    while ((1 << ebits) < E) ++ebits;
+    const RouterArgs ra{logits, k, renorm, shared_logits, n_sh, ids, w, shared_w};
+    hipLaunchKernelGGL(route_small, dim3(1), dim3(kSmallThreads), 0, s, ids, P, E, ebits, counts, offsets,
+                       sorted_pair, inv, status, ra);
+    return hipGetLastError();
+  }
+  hipError_t e = launch_router_topk(logits, T, E, k, renorm, shared_logits, n_sh, ids, w, shared_w, s);
+  if (e != hipSuccess) return e;
+  return launch_route(ids, T, k, E, counts, offsets, sorted_pair, inv, status, chunk_counts, chunk_bad, s);
 }
 
 hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts, int32_t* offsets,
@@ -355,8 +529,10 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
   int ebits = 0;
   while ((1 << ebits) < E) ++ebits;
   if (P <= kRouteSmall) {
+    RouterArgs none;
+    memset(&none, 0, sizeof(none));
     hipLaunchKernelGGL(route_small, dim3(1), dim3(kSmallThreads), 0, s, ids, P, E, ebits, counts, offsets,
-                       sorted_pair, inv, status);
+                       sorted_pair, inv, status, none);
     return hipGetLastError();
   }
   if (nchunks > 0) {
