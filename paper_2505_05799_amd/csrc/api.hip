@@ -305,7 +305,7 @@ mxmoe_status mxmoe_route_permute(const int32_t* topk_ids, int32_t T, int32_t k, 
   const size_t nchunks = (P + kRouteChunk - 1) / kRouteChunk;
   int32_t* cc = reinterpret_cast<int32_t*>(workspace);
   int32_t* cb = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(workspace) + align256(4 * nchunks * E));
-  return hip_status(launch_route(topk_ids, T, k, E, counts, offsets, sorted_pair, inv, status, cc, cb, stream));
+  return hip_status(launch_route(topk_ids, T, k, E, counts, offsets, sorted_pair, inv, status, cc, cb, nullptr, stream));
 }
 
 mxmoe_status mxmoe_router_topk(const float* logits, int32_t T, int32_t E, int32_t k, int32_t renormalize,
@@ -589,6 +589,15 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   const int32_t* ids = topk_ids;
   const float* tw = topk_w;
   const float* shw = opts ? opts->shared_w : nullptr;
+  // the routing launch also writes each sorted row's token, slot row and
+  // gate weight
+  RowMeta rm;
+  rm.k = bi.k;
+  rm.n_sh = bi.nsh;
+  rm.topk_w = tw;
+  rm.rtok = at<int32_t>(workspace, L.rtok);
+  rm.rslot = at<int32_t>(workspace, L.rslot);
+  rm.rgw = at<float>(workspace, L.rgw);
   if (router) {  // in the routing launch where the batch allows
     int32_t* rids = at<int32_t>(workspace, L.rids);
     float* rw = at<float>(workspace, L.rw);
@@ -596,7 +605,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     MX_CHECK(launch_router_route(opts->router_logits, T, bi.E, bi.k, opts->renormalize,
                                  rshw ? opts->shared_logits : nullptr, bi.nsh, rids, rw, rshw, counts, offsets,
                                  sorted_pair, at<int32_t>(workspace, L.inv), at<int32_t>(workspace, L.status),
-                                 at<int32_t>(workspace, L.chunk_counts), at<int32_t>(workspace, L.chunk_bad),
+                                 at<int32_t>(workspace, L.chunk_counts), at<int32_t>(workspace, L.chunk_bad), &rm,
                                  stream));
     ids = rids;
     tw = rw;
@@ -604,7 +613,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   } else {
     MX_CHECK(launch_route(ids, T, bi.k, bi.E, counts, offsets, sorted_pair, at<int32_t>(workspace, L.inv),
                           at<int32_t>(workspace, L.status), at<int32_t>(workspace, L.chunk_counts),
-                          at<int32_t>(workspace, L.chunk_bad), stream));
+                          at<int32_t>(workspace, L.chunk_bad), &rm, stream));
   }
   DevLinear none;
   memset(&none, 0, sizeof(none));
@@ -642,12 +651,13 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
     xp.qf6 = at<uint8_t>(workspace, L.xqf6);
     xp.sf6 = at<float>(workspace, L.xsf6);
   }
+  // the x encodings also copy the per-token scales to the token's sorted rows
+  xp.inv = at<int32_t>(workspace, L.inv);
+  xp.k = bi.k;
+  if (xp.q8) xp.r8 = at<float>(workspace, L.rxs8);
+  if (xp.q4) xp.r4 = at<float>(workspace, L.rxs4);
   MX_CHECK(launch_plan(experts, bi.E, bi.G, T, counts, offsets, -1, none, mask, plan, L.qcap, L.fcap, L.pfloats,
                        down_qmax, grid, xp, stream));
-  MX_CHECK(launch_row_meta(sorted_pair, offsets, bi.E, T * bi.k, bi.k, bi.nsh, tw, at<float>(workspace, L.xs8),
-                           at<float>(workspace, L.xs4), at<int32_t>(workspace, L.rtok), at<int32_t>(workspace, L.rslot),
-                           at<float>(workspace, L.rgw), at<float>(workspace, L.rxs8), at<float>(workspace, L.rxs4),
-                           stream));
   GemmArgs ga;
   memset(&ga, 0, sizeof(ga));
   ga.experts = experts;

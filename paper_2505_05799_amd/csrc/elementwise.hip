@@ -209,35 +209,6 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(const float* __restri
   *reinterpret_cast<uint4*>(y + (int64_t)t * H + h) = o;
 }
 
-// Per-row data of the sorted (token, slot) pairs, read by every Group-GEMM
-// tile with contiguous loads instead of gathers through the permutation.
-__global__ void row_meta_kernel(const int32_t* __restrict__ sorted_pair, const int32_t* __restrict__ offsets, int E,
-                                int k, int n_sh, const float* __restrict__ topk_w, const float* __restrict__ xs8,
-                                const float* __restrict__ xs4, int32_t* __restrict__ rtok, int32_t* __restrict__ rslot,
-                                float* __restrict__ rgw, float* __restrict__ rxs8, float* __restrict__ rxs4) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= offsets[E]) return;  // pairs dropped for an invalid expert id have no row
-  const int p = sorted_pair[j];
-  const int t = p / k, sl = p - t * k;
-  rtok[j] = t;
-  rslot[j] = t * (k + n_sh) + sl;
-  rgw[j] = topk_w[p];
-  if (xs8) rxs8[j] = xs8[t];
-  if (xs4) rxs4[j] = xs4[t];
-}
-
-}  // namespace
-
-hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, int E, int P, int k, int n_sh,
-                           const float* topk_w, const float* xs8, const float* xs4, int32_t* rtok, int32_t* rslot,
-                           float* rgw, float* rxs8, float* rxs4, hipStream_t s) {
-  if (P <= 0) return hipSuccess;
-  hipLaunchKernelGGL(row_meta_kernel, dim3((P + kThreads - 1) / kThreads), dim3(kThreads), 0, s, sorted_pair, offsets,
-                     E, k, n_sh, topk_w, xs8, xs4, rtok, rslot, rgw, rxs8, rxs4);
-  return hipGetLastError();
-}
-
-namespace {
 // Register-resident shapes by row length: (chunks per lane, wavefronts per row).
 enum RowShape { RS_1x2, RS_1x4, RS_1x8, RS_4x4, RS_4x8, RS_4x16, RS_STREAM };
 RowShape row_shape(int cols) {

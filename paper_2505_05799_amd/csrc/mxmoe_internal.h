@@ -278,9 +278,22 @@ hipError_t launch_pack(int kind, int n, int k, int act, int w16_src, const void*
 hipError_t launch_unpack(int kind, int n, int k, int act, const uint8_t* packed, void* codes,
                          void* scales, void* zeros, hipStream_t s);
 
+// Per sorted row j of the routed groups, written by the routing launch that
+// places the pair p = sorted_pair[j] (token t = p / k, slot p % k): rtok[j] =
+// t, rslot[j] = t * (k + n_sh) + p % k (its row of the down-projection slots),
+// rgw[j] = topk_w[p].  The per-token activation scales of the row follow from
+// the x encodings (XPrep::inv).
+struct RowMeta {
+  int k, n_sh;
+  const float* topk_w;
+  int32_t* rtok;
+  int32_t* rslot;
+  float* rgw;
+};
+// rm may be null (routing arrays only).
 hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
-                        int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
+                        int32_t* chunk_counts, int32_t* chunk_bad, const RowMeta* rm, hipStream_t s);
 // Router front-end, one wavefront per token: softmax top-k of fp32 logits
 // [T,E] (E <= 1024, k <= 64) and, if shared_logits, sigmoid gates [T,n_sh].
 constexpr int kRouterMaxK = 64;
@@ -289,10 +302,11 @@ hipError_t launch_router_topk(const float* logits, int T, int E, int k, int reno
 // The router front-end followed by routing of the ids it writes: one launch
 // where the batch fits the one-workgroup routing kernel (E <= 64, k <= 8),
 // else the two calls above.  Results equal those of the two calls.
+// (rm->topk_w is ignored: the rows take the router's weights w.)
 hipError_t launch_router_route(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
                                int n_sh, int32_t* ids, float* w, float* shared_w, int32_t* counts,
                                int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
-                               int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s);
+                               int32_t* chunk_counts, int32_t* chunk_bad, const RowMeta* rm, hipStream_t s);
 
 // Row sums of each 128-wide block of bf16 rows: out[r][b] = sum of a[r][128b ..
 // 128b + 127] in fp32; cols a multiple of 128, rows 16-byte aligned.
@@ -307,9 +321,7 @@ hipError_t launch_act_quant(const void* a, int act, int rows, int cols, int64_t 
 // Per sorted row j < offsets[E] (pair p = sorted_pair[j], token t = p / k,
 // slot s = p % k): rtok[j] = t, rslot[j] = t (k + n_sh) + s, rgw[j] = topk_w[p],
 // and rxs8[j] / rxs4[j] = the token's activation scale where those exist.
-hipError_t launch_row_meta(const int32_t* sorted_pair, const int32_t* offsets, int E, int P, int k, int n_sh,
-                           const float* topk_w, const float* xs8, const float* xs4, int32_t* rtok, int32_t* rslot,
-                           float* rgw, float* rxs8, float* rxs4, hipStream_t s);
+
 
 // Quantize routed h rows whose expert's down projection is a8/a4 (qmax from
 // down_qmax[expert]); rows of other experts are skipped.
@@ -371,7 +383,7 @@ struct GemmArgs {
   int32_t qcap;        // capacity of each XCD queue in the plan region (super-tiles)
   int32_t fcap;        // capacity of each XCD queue in the plan region (tiles)
   float* partial;      // split-K partial sums
-  // per sorted row (see launch_row_meta)
+  // per sorted row (RowMeta; rxs8 / rxs4 from the x encodings, XPrep::inv)
   const int32_t* rtok; const int32_t* rslot; const float* rgw; const float* rxs8; const float* rxs4;
   // Row sums of each 128-wide k block of the 16-bit activation rows that the
   // bias-dequantized weight kinds need (bf16): x [T][H/128] (the input in
@@ -402,6 +414,12 @@ struct XPrep {
   float* sf8;
   uint8_t* qf6;   // int4 codes as FP6 e2m3 groups [rows, cols] (one byte per element), scales sf6 [rows]
   float* sf6;
+  // the routed rows' copies of the per-token scales s8 / s4: row inv[r * k +
+  // s] (skipped where -1) of r8 / r4, for s < k (null: none)
+  const int32_t* inv;
+  int k;
+  float* r8;
+  float* r4;
 };
 
 // raw_m >= 0: single-linear plan (raw_lin, m = raw_m); else the block plan of

@@ -117,7 +117,8 @@ __global__ void __launch_bounds__(1024) route_scan(int nchunks, int E, int32_t* 
 __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restrict__ ids, int P, int E, int ebits,
                                                           const int32_t* __restrict__ chunk_base,
                                                           int32_t* __restrict__ sorted_pair,
-                                                          int32_t* __restrict__ inv) {
+                                                          int32_t* __restrict__ inv,
+                                                          RowMeta rm) {
   __shared__ int32_t base[kMaxE];
   __shared__ int32_t wcnt[kThreads / 64][kMaxE];
   const int c = blockIdx.x;
@@ -152,6 +153,12 @@ __global__ void __launch_bounds__(kThreads) route_scatter(const int32_t* __restr
       for (int i = 0; i < w; ++i) pos += wcnt[i][e];
       sorted_pair[pos] = p;
       inv[p] = pos;
+      if (rm.rtok) {
+        const int t = p / rm.k, sl = p - t * rm.k;
+        rm.rtok[pos] = t;
+        rm.rslot[pos] = t * (rm.k + rm.n_sh) + sl;
+        rm.rgw[pos] = rm.topk_w[p];
+      }
     } else if (p < p1) {
       inv[p] = -1;
     }
@@ -405,7 +412,7 @@ __global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* ids,
                                                              int32_t* __restrict__ offsets,
                                                              int32_t* __restrict__ sorted_pair,
                                                              int32_t* __restrict__ inv, int32_t* __restrict__ status,
-                                                             RouterArgs ra) {
+                                                             RouterArgs ra, RowMeta rm) {
   constexpr int NW = kSmallThreads / 64;
   __shared__ int32_t base[kMaxE];
   __shared__ int32_t wcnt[NW][kMaxE];
@@ -476,6 +483,12 @@ __global__ void __launch_bounds__(kSmallThreads) route_small(const int32_t* ids,
       for (int i = 0; i < w; ++i) pos += wcnt[i][e];
       sorted_pair[pos] = p;
       inv[p] = pos;
+      if (rm.rtok) {
+        const int t = p / rm.k, sl = p - t * rm.k;
+        rm.rtok[pos] = t;
+        rm.rslot[pos] = t * (rm.k + rm.n_sh) + sl;
+        rm.rgw[pos] = rm.topk_w[p];
+      }
     } else if (p < P) {
       inv[p] = -1;
     }
@@ -506,25 +519,34 @@ hipError_t launch_router_topk(const float* logits, int T, int E, int k, int reno
 hipError_t launch_router_route(const float* logits, int T, int E, int k, int renorm, const float* shared_logits,
                                int n_sh, int32_t* ids, float* w, float* shared_w, int32_t* counts,
                                int32_t* offsets, int32_t* sorted_pair, int32_t* inv, int32_t* status,
-                               int32_t* chunk_counts, int32_t* chunk_bad, hipStream_t s) {
+                               int32_t* chunk_counts, int32_t* chunk_bad, const RowMeta* rm, hipStream_t s) {
   const int P = T * k;
+  RowMeta rmv;
+  memset(&rmv, 0, sizeof(rmv));
+  if (rm) rmv = *rm;
+  rmv.k = k;
+  rmv.topk_w = w;
   if (P > 0 && P <= kRouteSmall && router_by_group(E, k)) {
     int ebits = 0;
     while ((1 << ebits) < E) ++ebits;
     const RouterArgs ra{logits, k, renorm, shared_logits, n_sh, ids, w, shared_w};
     hipLaunchKernelGGL(route_small, dim3(1), dim3(kSmallThreads), 0, s, ids, P, E, ebits, counts, offsets,
-                       sorted_pair, inv, status, ra);
+                       sorted_pair, inv, status, ra, rmv);
     return hipGetLastError();
   }
   hipError_t e = launch_router_topk(logits, T, E, k, renorm, shared_logits, n_sh, ids, w, shared_w, s);
   if (e != hipSuccess) return e;
-  return launch_route(ids, T, k, E, counts, offsets, sorted_pair, inv, status, chunk_counts, chunk_bad, s);
+  return launch_route(ids, T, k, E, counts, offsets, sorted_pair, inv, status, chunk_counts, chunk_bad, &rmv, s);
 }
 
 hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts, int32_t* offsets,
                         int32_t* sorted_pair, int32_t* inv, int32_t* status, int32_t* chunk_counts,
-                        int32_t* chunk_bad, hipStream_t s) {
+                        int32_t* chunk_bad, const RowMeta* rm, hipStream_t s) {
   const int P = T * k;
+  RowMeta rmv;
+  memset(&rmv, 0, sizeof(rmv));
+  if (rm) rmv = *rm;
+  rmv.k = k;
   const int nchunks = (P + kRouteChunk - 1) / kRouteChunk;
   int ebits = 0;
   while ((1 << ebits) < E) ++ebits;
@@ -532,7 +554,7 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
     RouterArgs none;
     memset(&none, 0, sizeof(none));
     hipLaunchKernelGGL(route_small, dim3(1), dim3(kSmallThreads), 0, s, ids, P, E, ebits, counts, offsets,
-                       sorted_pair, inv, status, none);
+                       sorted_pair, inv, status, none, rmv);
     return hipGetLastError();
   }
   if (nchunks > 0) {
@@ -545,7 +567,7 @@ hipError_t launch_route(const int32_t* ids, int T, int k, int E, int32_t* counts
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || nchunks == 0) return err;
   hipLaunchKernelGGL(route_scatter, dim3(nchunks), dim3(kThreads), 0, s, ids, P, E, ebits, chunk_counts,
-                     sorted_pair, inv);
+                     sorted_pair, inv, rmv);
   return hipGetLastError();
 }
 

@@ -128,8 +128,8 @@ __device__ inline void store_f6_chunk(uint8_t* row, int c, uint64_t w) {
 // one row).  NC > 0: the row's 16-byte chunks stay in registers
 // (cols <= 512 * W * NC); NC == 0: any length, the row is read twice.
 template <int NC, int W, bool F6 = false>
-__device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, int act, int qmax,
-                                     uint2* __restrict__ codes, float* __restrict__ scale, uint32_t* red) {
+__device__ inline float quant_row_vec(const uint4* __restrict__ row, int cols, int act, int qmax,
+                                      uint2* __restrict__ codes, float* __restrict__ scale, uint32_t* red) {
   const int idx = W == 1 ? (threadIdx.x & 63) : threadIdx.x, nch = cols >> 3;
   constexpr int kStride = 64 * W;
   const uint32_t nan_lo = act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;  // smallest NaN magnitude
@@ -177,6 +177,7 @@ __device__ inline void quant_row_vec(const uint4* __restrict__ row, int cols, in
     }
   }
   if (idx == 0) *scale = s;
+  return s;  // on every lane
 }
 
 // Quantizes one row per block of 128 elements (w4a4-g128 activations), one
@@ -273,13 +274,28 @@ __device__ inline void rowsum_row(const uint4* __restrict__ row, int cols, float
 __device__ inline void x_prep_row(const XPrep& p, int64_t r) {
   const int cols = p.cols;
   const uint4* row = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(p.x) + r * cols);
+  const int lane = threadIdx.x & 63;
+  // the token's routed rows get their copy of a per-token scale
+  auto to_rows = [&](float* dst, float v) {
+    if (!p.inv || !dst) return;
+    for (int sl = lane; sl < p.k; sl += 64) {
+      const int32_t j = p.inv[r * p.k + sl];
+      if (j >= 0) dst[j] = v;
+    }
+  };
   if (p.q8) {
-    if (cols <= 4096) quant_row_vec<8, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr);
-    else quant_row_vec<0, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr);
+    const float s8 =
+        cols <= 4096
+            ? quant_row_vec<8, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr)
+            : quant_row_vec<0, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr);
+    to_rows(p.r8, s8);
   }
   if (p.q4) {
-    if (cols <= 4096) quant_row_vec<8, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr);
-    else quant_row_vec<0, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr);
+    const float s4 =
+        cols <= 4096
+            ? quant_row_vec<8, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr)
+            : quant_row_vec<0, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr);
+    to_rows(p.r4, s4);
   }
   if (p.rs) rowsum_row(row, cols, p.rs + r * (cols >> 7));
   if (p.q4g)
