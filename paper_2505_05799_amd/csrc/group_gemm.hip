@@ -4,7 +4,8 @@
 //
 // plan_kernel (one workgroup, no host round trip):
 //   1. per (phase, expert) group: rows m (routing counts, T for shared experts),
-//      tile configuration from m, tile counts, a static per-tile cost;
+//      tile configuration from m, tile counts, the per-tile cost from the
+//      cost table (tile_cost);
 //   2. rank the groups by decreasing tile cost (ties: lower expert first) - the
 //      greedy longest-tile-first order of the paper's tile schedule;
 //   3. cut every group into super-tiles (up to 64 tiles that share row and
@@ -13,7 +14,7 @@
 //   4. expand every queue into one 16-byte entry per tile (group, configuration,
 //      kind, slices, tile coordinates, first sorted row and rows of the group),
 //      so that a workgroup resolves a popped tile with a single load.
-// Groups may be sliced along the reduction (split-K, see split_rule): their
+// Groups may be sliced along the reduction (split-K, kSplitShare / kSplitMinKb): their
 // slices are queued as extra channel tiles, within fixed budgets of added
 // tiles and of partial-sum storage.
 #include <mutex>
