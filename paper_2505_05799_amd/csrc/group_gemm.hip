@@ -37,7 +37,7 @@ __device__ inline int div_small(int x, int d) {
   q += (q + 1) * d <= x;
   return q;
 }
-// super_dims with div_small (same values)
+// Super-tile geometry (SuperDims), with div_small for the divisions
 __device__ inline SuperDims plan_super_dims(int mt, int nt) {
   SuperDims d;
   d.sm = mt < 8 ? mt : 8;
@@ -476,7 +476,7 @@ __global__ void __launch_bounds__(1024) plan_kernel(const DevExpert* __restrict_
       }
       // The chunk's entries are expanded one at a time by the whole
       // wavefront (lane t writes the entry's tile t, row tile fastest, the
-      // order of super_tile_pos), so that every store is contiguous; the
+      // order of the SuperDims geometry), so that every store is contiguous; the
       // entry's fields come from its lane's registers.
       const int cnt = n - c0 < 64 ? n - c0 : 64;
       for (int j = 0; j < cnt; ++j) {

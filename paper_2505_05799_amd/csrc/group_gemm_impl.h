@@ -96,35 +96,9 @@ __host__ __device__ inline int pick_cfg(int m, int kind, int phase) {
 
 // Super-tile geometry of a group of mt x nt tiles: sm x sn tiles per super-tile
 // (sm = min(mt, 8), sn = min(nt, 64 / sm)), nsm x nsn super-tiles, super-tile
-// s at (s % nsm, s / nsm); inside, tile t at (t % em, t / em).
+// s at (s % nsm, s / nsm); inside, tile t at (t % em, t / em) with em the
+// super-tile's row tiles (the plan expands the queues in this order).
 struct SuperDims { int sm, sn, nsm, nsn; };
-__host__ __device__ inline SuperDims super_dims(int mt, int nt) {
-  SuperDims d;
-  d.sm = mt < 8 ? mt : 8;
-  const int cap = kSuperTiles / (d.sm > 0 ? d.sm : 1);
-  d.sn = nt < cap ? nt : cap;
-  d.nsm = d.sm ? (mt + d.sm - 1) / d.sm : 0;
-  d.nsn = d.sn ? (nt + d.sn - 1) / d.sn : 0;
-  return d;
-}
-__host__ __device__ inline int super_tiles(int mt, int nt) {
-  if (mt <= 0 || nt <= 0) return 0;
-  const SuperDims d = super_dims(mt, nt);
-  return d.nsm * d.nsn;
-}
-__host__ __device__ inline int super_tile_size(int mt, int nt, int s) {
-  const SuperDims d = super_dims(mt, nt);
-  const int smi = s % d.nsm, sni = s / d.nsm;
-  const int em = min(d.sm, mt - smi * d.sm), en = min(d.sn, nt - sni * d.sn);
-  return em * en;
-}
-__host__ __device__ inline void super_tile_pos(int mt, int nt, int s, int t, int* mi, int* ni) {
-  const SuperDims d = super_dims(mt, nt);
-  const int smi = s % d.nsm, sni = s / d.nsm;
-  const int em = min(d.sm, mt - smi * d.sm);
-  *mi = smi * d.sm + t % em;
-  *ni = sni * d.sn + t / em;
-}
 
 // ---------------------------------------------------------- MFMA helpers
 template <int ACT> __device__ inline f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
