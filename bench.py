@@ -81,7 +81,7 @@ def group_stats(blk, counts):
                 fl += 2.0 * m * q.n * q.k
                 by += q.nbytes_packed + m * q.k * act_bytes(q.scheme)
             n_out = lins[idx[0]].n
-            by += m * n_out * (2.0 if phase == 0 else 4.0)
+            by += m * n_out * 2.0          # h rows, or slot rows in the activation dtype
             s = lins[idx[0]].scheme
             out.append({"expert": e, "phase": phase, "m": m, "flops": fl, "bytes": by,
                         "dtype": mfma_dtype(s, cfg.act), "scheme": s.name})

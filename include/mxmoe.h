@@ -317,7 +317,12 @@ typedef struct {
   /* Without router_logits: fp32 [T, n_shared] weights of the shared experts'
    * outputs, or NULL for weight 1.                                           */
   const float* shared_w;
-  int32_t reserved[2];
+  /* 1: keep the down projection's weighted rows (the slot rows the combine
+   * sums) in fp32, for callers that difference them (the allocator's error
+   * probe); 0 (default): each slot row element is rounded once to the
+   * activation dtype before the combine, which halves their traffic.        */
+  int32_t fp32_slots;
+  int32_t reserved1;             /* must be 0 */
 } mxmoe_forward_opts;
 
 #define MXMOE_N_PHASES 5
@@ -347,7 +352,9 @@ typedef struct {
   size_t h_shared;      /* act [n_shared, T, F_shared]                       */
   size_t hq, hs;        /* int8 [T*k, F], fp32 [T*k]: routed h codes         */
   size_t hq_shared, hs_shared; /* int8 [n_shared,T,F_shared], fp32 [n_shared,T] */
-  size_t slots;         /* fp32 [T, k + n_shared, H]: weighted down rows     */
+  size_t slots;         /* [T, k + n_shared, H]: weighted down rows, in the
+                           activation dtype (fp32 with opts.fp32_slots; the
+                           buffer is sized for fp32)                          */
   size_t total;         /* = mxmoe_workspace_bytes                           */
   size_t plan_queue_cap;/* entries per XCD queue in the tile plan            */
   size_t plan_flat_cap; /* tiles per XCD queue in the tile plan              */

@@ -164,7 +164,7 @@ def sensitivity(cfg, candidates, calib_tokens: int = 1024, seed: int = 0, log=pr
 
     def slots(block):
         mb = M.MoEBlock(block, T_max=T)
-        mb.forward(x, ids, w, skip_combine=True)
+        mb.forward(x, ids, w, skip_combine=True, fp32_slots=True)   # differences need the fp32 rows
         torch.cuda.synchronize()
         s = mb.ws_view("slots", torch.float32, T * S * cfg.H, T).reshape(T, S, cfg.H).double().cpu().numpy()
         del mb

@@ -538,7 +538,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   if ((int64_t)T * bi.k >= (1LL << 31)) return MXMOE_ERR_UNSUPPORTED;
   if (!activations_fit(bi, T)) return MXMOE_ERR_UNSUPPORTED;
   const bool router = opts && opts->router_logits;
-  if (opts && (opts->reserved0 != 0 || opts->reserved[0] != 0 || opts->reserved[1] != 0)) return MXMOE_ERR_INVALID_ARG;
+  if (opts && (opts->reserved0 != 0 || (opts->fp32_slots != 0 && opts->fp32_slots != 1) || opts->reserved1 != 0))
+    return MXMOE_ERR_INVALID_ARG;
   if (router) {
     if (opts->renormalize != 0 && opts->renormalize != 1) return MXMOE_ERR_INVALID_ARG;
     if (opts->shared_w || !aligned(opts->router_logits, 4) || !aligned(opts->shared_logits, 4))
@@ -677,7 +678,8 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   ga.hs = at<float>(workspace, L.hs);
   ga.hq_shared = at<int8_t>(workspace, L.hq_shared);
   ga.hs_shared = at<float>(workspace, L.hs_shared);
-  ga.slots = at<float>(workspace, L.slots);
+  ga.slots = at<void>(workspace, L.slots);
+  ga.slot16 = (opts && opts->fp32_slots) ? 0 : 1;
   ga.down_qmax = down_qmax;
   ga.T = T;
   ga.k = bi.k;
@@ -748,7 +750,7 @@ mxmoe_status mxmoe_moe_forward_ex(const mxmoe_block* B, const void* block_table,
   MX_EVENT(7);
   MX_EVENT(8);
   if (!(opts && opts->skip_combine))
-    MX_CHECK(launch_combine(ga.slots, ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
+    MX_CHECK(launch_combine(ga.slots, ga.slot16, ids, T, bi.k, bi.E, bi.nsh, bi.H, bi.act, y, stream));
   MX_EVENT(9);
 #undef MX_EVENT
 #undef MX_CHECK

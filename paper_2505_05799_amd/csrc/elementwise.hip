@@ -167,8 +167,10 @@ __global__ void __launch_bounds__(kThreads) rowsum_kernel(const uint16_t* __rest
 // 8 outputs per thread.  SC > 0 slots (compile time): every slot row is
 // loaded before the expert ids are consulted (rows of dropped pairs are in
 // bounds, their values unused); SC == 0: any slot count, one slot at a time.
-template <int SC>
-__global__ void __launch_bounds__(kThreads) combine_kernel(const float* __restrict__ slots,
+// F32: fp32 slot rows (two 16-byte loads per slot), else rows in the
+// activation dtype (one 16-byte load per slot, widened exactly to fp32).
+template <int SC, bool F32>
+__global__ void __launch_bounds__(kThreads) combine_kernel(const void* __restrict__ slots,
                                                            const int32_t* __restrict__ ids, int T, int k, int E,
                                                            int S, int H, int act, uint16_t* __restrict__ y) {
   const int64_t i8 = (int64_t)blockIdx.x * kThreads + threadIdx.x;  // index of 8 outputs
@@ -176,11 +178,19 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(const float* __restri
   if (i8 >= (int64_t)T * q8) return;
   const int t = (int)(i8 / q8), h = (int)(i8 % q8) * 8;
   if constexpr (SC > 0) S = SC;
-  const float4* base = reinterpret_cast<const float4*>(slots + (int64_t)t * S * H + h);
+  const int64_t off = (int64_t)t * S * H + h;  // element offset of slot 0
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  auto add = [&](float4 a, float4 b) {
-    acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
-    acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+  typedef float f8v[8];
+  auto load = [&](int s, f8v& v) {
+    if constexpr (F32) {
+      const float4* p = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(slots) + off + (int64_t)s * H);
+      const float4 a = p[0], b = p[1];
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+      v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+      const uint4 u = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(slots) + off + (int64_t)s * H);
+      unpack8(u, act, v);
+    }
   };
   auto valid = [&](int s) {
     if (s >= k) return true;  // shared-expert slots
@@ -188,18 +198,23 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(const float* __restri
     return e >= 0 && e < E;
   };
   if constexpr (SC > 0) {
-    float4 v[SC][2];
+    float v[SC][8];
 #pragma unroll
-    for (int s = 0; s < SC; ++s) {
-      v[s][0] = base[(int64_t)s * (H / 4)];
-      v[s][1] = base[(int64_t)s * (H / 4) + 1];
-    }
+    for (int s = 0; s < SC; ++s) load(s, v[s]);
 #pragma unroll
     for (int s = 0; s < SC; ++s)
-      if (valid(s)) add(v[s][0], v[s][1]);
+      if (valid(s)) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += v[s][i];
+      }
   } else {
     for (int s = 0; s < S; ++s)
-      if (valid(s)) add(base[(int64_t)s * (H / 4)], base[(int64_t)s * (H / 4) + 1]);
+      if (valid(s)) {
+        float v[8];
+        load(s, v);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] += v[i];
+      }
   }
   uint4 o;
   o.x = (uint32_t)f32_to_act(acc[0], act) | ((uint32_t)f32_to_act(acc[1], act) << 16);
@@ -299,25 +314,31 @@ hipError_t launch_hquant_routed(const void* h, int act, int P, int F, const int3
   return launch_rows<HQuantK>(P, F, s, h, act, P, F, offsets, E, down_qmax, hq, hs, hsg, hqmx, hsmx);
 }
 
-hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int nsh, int H, int act,
-                          void* y, hipStream_t s) {
+hipError_t launch_combine(const void* slots, int slot16, const int32_t* ids, int T, int k, int E, int nsh, int H,
+                          int act, void* y, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   if (H % 8 || (reinterpret_cast<uintptr_t>(y) & 15) || (reinterpret_cast<uintptr_t>(slots) & 15))
     return hipErrorInvalidValue;
   const int64_t n8 = (int64_t)T * (H / 8);
   const dim3 grid((unsigned)((n8 + kThreads - 1) / kThreads));
   const int S = k + nsh;
-  switch (S) {
+  auto run = [&](auto f32) {
+    constexpr bool F = decltype(f32)::value;
+    switch (S) {
 #define MX_COMBINE(S_) \
   case S_:             \
-    hipLaunchKernelGGL(combine_kernel<S_>, grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act, (uint16_t*)y); \
+    hipLaunchKernelGGL((combine_kernel<S_, F>), grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act, (uint16_t*)y); \
     break;
-    MX_COMBINE(1) MX_COMBINE(2) MX_COMBINE(3) MX_COMBINE(4) MX_COMBINE(5) MX_COMBINE(6) MX_COMBINE(7) MX_COMBINE(8)
-    MX_COMBINE(9) MX_COMBINE(10)
+      MX_COMBINE(1) MX_COMBINE(2) MX_COMBINE(3) MX_COMBINE(4) MX_COMBINE(5) MX_COMBINE(6) MX_COMBINE(7) MX_COMBINE(8)
+      MX_COMBINE(9) MX_COMBINE(10)
 #undef MX_COMBINE
-    default:
-      hipLaunchKernelGGL(combine_kernel<0>, grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act, (uint16_t*)y);
-  }
+      default:
+        hipLaunchKernelGGL((combine_kernel<0, F>), grid, dim3(kThreads), 0, s, slots, ids, T, k, E, S, H, act,
+                           (uint16_t*)y);
+    }
+  };
+  if (slot16) run(std::false_type{});
+  else run(std::true_type{});
   return hipGetLastError();
 }
 

@@ -492,7 +492,7 @@ __device__ inline void rowsum_load(Smem& sm, int buf, const float* rsbase, uint3
 
 // ---------------------------------------------------------- tile body
 template <int KD, int ACT, int CFG, int PHASE>
-__device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int ntv,
+__device__ __attribute__((always_inline)) inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int ntv,
                                 int off_e, int split) {
   constexpr int MF = cfg_mf(CFG);
   constexpr int NF = cfg_nf(CFG, PHASE == 0 ? 0 : 1);
@@ -1232,10 +1232,54 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
         }
       }
     } else if constexpr (PHASE == 1) {
-      // The tile's fp32 slot rows (value x router gate weight) go through LDS
-      // (the idle stage buffers), RP rows at a time, and leave as 16-byte
-      // pieces of whole rows: a store instruction writes 64 x 16 contiguous
-      // bytes instead of 16-lane 64-byte segments of four rows.
+      // The tile's slot rows (value x router gate weight) go through LDS (the
+      // idle stage buffers), RP rows at a time, and leave as 16-byte pieces of
+      // whole rows: a store instruction writes 64 x 16 contiguous bytes
+      // instead of 16-lane segments of four rows.  Slot rows are rounded once
+      // to the activation dtype (a.slot16, the default), or kept in fp32.
+      if (a.slot16) {
+        constexpr int HP = BN + 8;                  // row pitch in elements (16-byte pad against bank conflicts)
+        constexpr int RP = (BM >= 64 && 64 * HP * 2 <= 2 * STAGE_BYTES) ? 64 : BM;  // rows per pass
+        static_assert(RP * HP * 2 <= 2 * STAGE_BYTES, "slot rows fit the stage buffers");
+        uint16_t* hl = reinterpret_cast<uint16_t*>(&sm.act[0][0]);
+        constexpr int CH = BN / 8;                  // 16-byte pieces of a tile row
+        int nch = (N - nt * BN) / 8;
+        nch = nch > CH ? CH : nch;
+        uint16_t* sout = reinterpret_cast<uint16_t*>(a.slots);
+#pragma unroll
+        for (int pass = 0; pass < BM / RP; ++pass) {
+#pragma unroll
+          for (int mf = 0; mf < MF; ++mf) {
+            if ((mf * 16) / RP != pass) continue;
+            const int r = mf * 16 + 4 * q;
+            const f32x4 rs = *reinterpret_cast<const f32x4*>(&sm.rowscale[r]);
+            const f32x4 gwv = *reinterpret_cast<const f32x4*>(&sm.rowgw[r]);
+#pragma unroll
+            for (int nf = 0; nf < NF; ++nf) {  // (channels past N: written, never stored)
+              const int c = (wave * NF + nf) * 16 + li;
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                // the fp32 product is rounded first, then converted: the
+                // barrier keeps the compiler from fusing the multiply into a
+                // mixed-precision instruction that rounds once to fp16
+                float v = outv(0, nf, mf, i, rs) * gwv[i];
+                asm volatile("" : "+v"(v));
+                hl[(r + i - pass * RP) * HP + c] = f32_to_act<ACT>(v);
+              }
+            }
+          }
+          if (pass == 0) wait_vmem<0>();  // the next tile's entry has landed
+          lds_barrier();
+          for (int idx = tid; idx < RP * CH; idx += kThreads) {
+            const int r = idx / CH, c = idx % CH;
+            const int ro = sm.rowout[pass * RP + r];
+            if (ro >= 0 && c < nch)
+              *reinterpret_cast<u32x4*>(sout + (int64_t)ro * N + nt * BN + 8 * c) =
+                  *reinterpret_cast<const u32x4*>(hl + r * HP + 8 * c);
+          }
+          lds_barrier();
+        }
+      } else {
       constexpr int FP = BN + 4;                  // row pitch in floats (16-byte pad against bank conflicts)
       constexpr int RP = (BM >= 32 && 32 * FP * 4 <= 2 * STAGE_BYTES) ? 32 : 16;  // rows per pass
       static_assert(RP * FP * 4 <= 2 * STAGE_BYTES, "slot rows fit the stage buffers");
@@ -1264,10 +1308,11 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
           const int r = idx / CH, c = idx % CH;
           const int ro = sm.rowout[pass * RP + r];
           if (ro >= 0 && c < nch)
-            *reinterpret_cast<u32x4*>(a.slots + (int64_t)ro * N + nt * BN + 4 * c) =
+            *reinterpret_cast<u32x4*>(reinterpret_cast<float*>(a.slots) + (int64_t)ro * N + nt * BN + 4 * c) =
                 *reinterpret_cast<const u32x4*>(fl + r * FP + 4 * c);
         }
         lds_barrier();
+      }
       }
     } else {
 #pragma unroll
@@ -1306,7 +1351,7 @@ __device__ inline void run_tile(Smem& sm, const GemmArgs& a, const DevExpert* ex
 }
 
 template <int ACT, int PHASE, int CFG>
-__device__ inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
+__device__ __attribute__((always_inline)) inline void dispatch_kind(Smem& sm, const GemmArgs& a, const DevExpert* ex, int g, int m_g, int mt, int nt,
                                      int off_e, int kd, int split) {
   switch (kd) {
     case K_W16: run_tile<K_W16, ACT, CFG, PHASE>(sm, a, ex, g, m_g, mt, nt, off_e, split); break;

@@ -372,7 +372,8 @@ struct GemmArgs {
   void* h; void* h_shared;
   const int8_t* hq; const float* hs;
   const int8_t* hq_shared; const float* hs_shared;
-  float* slots;
+  void* slots;         // weighted down rows [T][k + n_shared][H]: activation dtype (slot16), else fp32
+  int32_t slot16;
   const float* shared_w;     // [T][n_shared] weights of the shared experts' rows, or null (weight 1)
   const int32_t* down_qmax;
   int32_t T, k;
@@ -439,7 +440,8 @@ void tile_costs_get(TileCosts* out);
 hipError_t launch_group_gemm(const GemmArgs& a, int phase, int grid, hipStream_t s);
 int group_gemm_grid(int device);
 
-hipError_t launch_combine(const float* slots, const int32_t* ids, int T, int k, int E, int n_sh,
+// slots in the activation dtype (slot16) or fp32
+hipError_t launch_combine(const void* slots, int slot16, const int32_t* ids, int T, int k, int E, int n_sh,
                           int H, int act, void* y, hipStream_t s);
 
 }  // namespace mxmoe

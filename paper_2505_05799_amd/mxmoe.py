@@ -44,7 +44,7 @@ class ForwardOpts_t(C.Structure):
     _fields_ = [("expert_mask", C.POINTER(C.c_uint8)), ("reserved0", C.c_int32),
                 ("skip_combine", C.c_int32), ("events", C.POINTER(C.c_void_p)),
                 ("router_logits", C.c_void_p), ("renormalize", C.c_int32), ("shared_logits", C.c_void_p),
-                ("shared_w", C.c_void_p), ("reserved", C.c_int32 * 2)]
+                ("shared_w", C.c_void_p), ("fp32_slots", C.c_int32), ("reserved1", C.c_int32)]
 
 
 WS_FIELDS = ["status", "counts", "offsets", "sorted_pair", "inv", "plan", "xq8", "xs8", "xq4", "xs4",
@@ -408,9 +408,11 @@ class MoEBlock:
 
     def forward(self, x, topk_ids, topk_w, y=None, expert_mask: Optional[Sequence[int]] = None,
                 skip_combine: bool = False, events=None, stream=None, router_logits=None,
-                renormalize: bool = False, shared_logits=None, shared_w=None):
+                renormalize: bool = False, shared_logits=None, shared_w=None, fp32_slots: bool = False):
         """topk_ids / topk_w may be None when router_logits (fp32 [T,E]) is
-        given; the router's choice is then left in the workspace."""
+        given; the router's choice is then left in the workspace.
+        fp32_slots: keep the weighted down rows in fp32 (default: rounded to
+        the activation dtype); slot_dtype() says which the last call used."""
         torch = _torch()
         lib = load_library()
         T = x.shape[0]
@@ -419,9 +421,11 @@ class MoEBlock:
         if y is None:
             y = torch.empty_like(x)
         opts = None
+        self._fp32_slots = bool(fp32_slots)
         if (expert_mask is not None or skip_combine or events is not None or router_logits is not None
-                or shared_w is not None):
+                or shared_w is not None or fp32_slots):
             o = ForwardOpts_t()
+            o.fp32_slots = 1 if fp32_slots else 0
             o.router_logits = _ptr(router_logits)
             o.renormalize = 1 if renormalize else 0
             o.shared_logits = _ptr(shared_logits)
@@ -449,6 +453,21 @@ class MoEBlock:
                                            _ptr(topk_w), _ptr(y), _stream_ptr(stream))
         _check(st, "mxmoe_moe_forward_noalloc")
         return y
+
+    def slot_dtype(self):
+        """torch dtype of the slot rows the last forward wrote."""
+        torch = _torch()
+        if getattr(self, "_fp32_slots", False):
+            return torch.float32
+        return torch.bfloat16 if self.act == "bf16" else torch.float16
+
+    def slot_rows(self, T: int):
+        """The last forward's weighted down rows [T, k + n_shared, H] as a
+        float32 numpy array (exact: a 16-bit slot widens without rounding)."""
+        cfg = self.cfg
+        n = T * (cfg.k + cfg.n_shared) * cfg.H
+        v = self.ws_view("slots", self.slot_dtype(), n, T)
+        return v.float().cpu().numpy().reshape(T, cfg.k + cfg.n_shared, cfg.H)
 
     def ws_view(self, field: str, dtype, count: int, T: int):
         """Typed view of an intermediate buffer inside the workspace (after a forward)."""

@@ -10,13 +10,15 @@ it actually received (read back from the workspace):
   B  down-projection activation encodings (a8 / a4 / per-128-group / FP8 /
      MXFP4): the oracle's encoder applied to the GPU's h, byte for byte;
   C  down projection: the oracle's down linear on the GPU's h (so on exactly
-     the codes of B), times the router gate weight, against the GPU's fp32
-     slot rows - bit for bit for w8a8 / w4a4 (their fp32 epilogue products
-     are evaluated here in IEEE float32 in the kernel's order), within the
-     accumulation models of tolerance.py for the other kinds;
-  D  combine: the GPU's slot rows summed in fp32 in slot order (dropped pairs
-     skipped) and rounded once to the activation dtype, evaluated here in
-     IEEE float32: bit for bit;
+     the codes of B), times the router gate weight, against the GPU's slot
+     rows (rounded to the activation dtype, or fp32 when the forward kept
+     them so) - bit for bit for w8a8 / w4a4 (their fp32 epilogue products
+     are evaluated here in IEEE float32 in the kernel's order, then rounded
+     the same way), within the accumulation models of tolerance.py plus the
+     slot rounding for the other kinds;
+  D  combine: the GPU's slot rows widened to fp32, summed in fp32 in slot
+     order (dropped pairs skipped) and rounded once to the activation dtype,
+     evaluated here in IEEE float32: bit for bit;
   E  end to end, against the oracle alone (its own rounded h): every row
      within REL_TOL of its largest |y|, no slack.  Where h sits near a
      rounding midpoint, the GPU's fp32 h and the oracle's fp64 h can round
@@ -163,7 +165,8 @@ def check_forward(mb, blk, y, shared_w=None, chunk=4096, log=None) -> Report:
     xv = O.act_values(blk.x, act)
     ynp = y.detach().contiguous().view(torch.int16).cpu().numpy()
     y_gpu = _act16(ynp, act)
-    slots = _ws(mb, T, "slots", torch.float32, T * S * H).reshape(T, S, H)
+    slots = mb.slot_rows(T)                      # float32 (16-bit slots widen exactly)
+    slot16 = mb.slot_dtype() != torch.float32
     h_r = _ws(mb, T, "h", torch.int16, P * cfg.F).reshape(P, cfg.F) if P else None
     h_s = _ws(mb, T, "h_shared", torch.int16, nsh * T * cfg.F_shared).reshape(nsh, T, cfg.F_shared) if nsh else None
 
@@ -252,12 +255,16 @@ def check_forward(mb, blk, y, shared_w=None, chunk=4096, log=None) -> Report:
             ref, exact32, bound = _down_ref(hg, down, act, gwc)
             got = slots[tok[c0:c1], slot_idx[c0:c1]]
             if exact32 is not None:
+                if slot16:
+                    exact32 = O.round_to_act(exact32.astype(np.float64), act).astype(np.float32)
                 if not TL.f32_bits_equal(got, exact32):
                     i, n = np.argwhere(got.view(np.uint32) != exact32.view(np.uint32))[0]
                     raise AssertionError(f"stage C, group {g}: int slot [{c0 + i}, {n}] gpu={got[i, n]!r} "
                                          f"emulated={exact32[i, n]!r}")
                 rep["int_slots_exact"] += int(got.size)
             else:
+                if slot16:
+                    bound = TL.slot_bound(ref, bound, act)
                 e = np.abs(got.astype(np.float64) - ref)
                 if e.size:
                     rep["slot_ratio"] = max(rep["slot_ratio"], float((e / bound).max()))
@@ -293,7 +300,8 @@ def check_forward(mb, blk, y, shared_w=None, chunk=4096, log=None) -> Report:
     acc = np.zeros((T, H), np.float32)
     valid = np.concatenate([(blk.topk_ids >= 0) & (blk.topk_ids < E), np.ones((T, nsh), bool)], axis=1)
     for s in range(S):
-        acc = np.where(valid[:, s:s + 1], (acc + slots[:, s]).astype(np.float32), acc)
+        # (rows of dropped pairs hold whatever the workspace held: never added)
+        acc = np.where(valid[:, s:s + 1], (acc + np.where(valid[:, s:s + 1], slots[:, s], 0)).astype(np.float32), acc)
     want = O.round_to_act(acc.astype(np.float64), act)
     if not np.array_equal(want, y_gpu):
         t, h = np.argwhere(want != y_gpu)[0]

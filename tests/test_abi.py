@@ -246,12 +246,9 @@ def test_activation_buffers_beyond_4gib_are_rejected(lib):
 def test_forward_reserved_options_must_be_zero(lib):
     B, keep = _block("tiny")
     p = C.c_void_p(1 << 20)
-    for field in ("reserved0", "reserved"):
+    for field in ("reserved0", "reserved1", "fp32_slots"):
         o = M.ForwardOpts_t()
-        if field == "reserved0":
-            o.reserved0 = 1
-        else:
-            o.reserved[1] = 1
+        setattr(o, field, 2 if field == "fp32_slots" else 1)   # fp32_slots takes 0 or 1
         assert lib.mxmoe_moe_forward_ex(C.byref(B), p, 64, p, p, p, p, p, 10 ** 9, C.byref(o), None) == \
             M.ERR_INVALID_ARG
 

@@ -232,3 +232,25 @@ def test_expert_mask_and_skip_combine():
     yv = O.act_values(M.act_numpy(y, "bf16"), "bf16")[sel]
     r = ref["y"][sel]
     assert np.all(np.abs(yv - r) <= 1e-2 * np.abs(r).max(axis=1, keepdims=True))
+
+
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+def test_fp32_slots_option(act):
+    """fp32_slots keeps the weighted down rows in fp32: the stage-wise check
+    then compares them bit for bit (integer kinds) or within the fp32 models,
+    and the combine sums the fp32 rows; the default path rounds every slot
+    row element once to the activation dtype (checked by every other test)."""
+    torch = torch_mod()
+    blk = W.random_small_block(911, T=200, H=256, F=384, E=6, k=2, n_shared=1, F_shared=256, act=act,
+                               schemes=MIXES[0], skew=1.0)
+    mb = M.MoEBlock(blk)
+    x, ids, w = upload_inputs(blk)
+    y32 = mb.forward(x, ids, w, fp32_slots=True)
+    torch.cuda.synchronize()
+    assert mb.slot_dtype() == torch.float32
+    rep = check_forward(mb, blk, y32)
+    y16 = mb.forward(x, ids, w)
+    torch.cuda.synchronize()
+    assert mb.slot_dtype() != torch.float32
+    rep16 = check_forward(mb, blk, y16)
+    say(f"fp32 slots {act}: {rep.line()}; 16-bit slots: {rep16.line()}")

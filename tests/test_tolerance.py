@@ -239,3 +239,25 @@ def test_f6_encoder_of_the_stagewise_check():
                 v = 0.0 if e == 0 else (1 + m / 8) * 2.0 ** (e - 1)
                 assert e != 0 or m == 0
                 assert (-v if s else v) == q[r, 32 * g + i]
+
+
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+def test_slot_bound_covers_rounding_to_the_activation_dtype(act):
+    """slot_bound: a value v within `bound` of ref, rounded to nearest in the
+    activation dtype (here by the workloads' bf16 bit rounding of float32 and
+    numpy's float16 cast, not the oracle's rounding), stays within
+    slot_bound(ref, bound) of ref - on values straddling powers of two, near
+    zero and at the largest v; the rounding part is used at least halfway."""
+    rng = np.random.default_rng(11)
+    ref = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-4, 3, 4000),
+                          2.0 ** rng.integers(-10, 8, 2000) * (1 - 2.0 ** -20), [0.0, 1e-6, -1.0]])
+    bound = np.abs(ref) * 2.0 ** -14 + 1e-9
+    worst = 0.0
+    for frac in (-1.0, -0.37, 0.0, 0.61, 1.0):
+        v = (ref + frac * bound).astype(np.float32)
+        r = _bf16(v).astype(np.float64) if act == "bf16" else v.astype(np.float16).astype(np.float64)
+        b = TL.slot_bound(ref, bound, act)
+        err = np.abs(r - ref)
+        assert np.all(err <= b), float((err / b).max())
+        worst = max(worst, float(((err - bound) / (b - bound)).max()))
+    assert worst >= 0.5

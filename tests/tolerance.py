@@ -19,6 +19,10 @@ that every emulated error stays at least a factor 4 inside the bound.
   than 127 * 2^(e_max - 18) <= 2^-11 max|p|, and the bound charges
   FP8_BLOCK_EPS * max|a| * max|w| per block plus ACC16_EPS * sum |a||w| for the
   fp32 sums across blocks and slices.
+* Slot rows (stage C): the down epilogue forms value x gate weight in fp32 and,
+  by default, rounds it once to the activation dtype (nearest, ties to even);
+  a stored slot then lies within the fp32 bound plus half the dtype's spacing
+  at |ref| + bound of the exact value (slot_bound).
 * Gated intermediate h (stage A of the stage-wise check): the GPU forms h in
   fp32 from fp32 g and u, and rounds it once to the activation dtype.  Under
   the models above the fp32 value sits within 2^-14 of the row's largest
@@ -65,6 +69,13 @@ def ulp_act(x: np.ndarray, act: str) -> np.ndarray:
     if act == "fp16":                   # 11 significant bits, subnormal spacing 2^-24
         return np.where(ax == 0, 2.0 ** -24, np.ldexp(1.0, np.maximum(e - 11, -24)))
     raise ValueError(act)
+
+
+def slot_bound(ref: np.ndarray, bound: np.ndarray, act: str) -> np.ndarray:
+    """Bound on |stored slot - ref| for a slot computed within `bound` of
+    `ref` and then rounded to nearest in the activation dtype: the rounding
+    moves a value v by at most half the spacing at |v| <= |ref| + bound."""
+    return bound + 0.5 * ulp_act(np.abs(ref) + bound, act)
 
 
 def h_tolerance(h64: np.ndarray, act: str) -> np.ndarray:
