@@ -283,33 +283,61 @@ __device__ inline void x_prep_row(const XPrep& p, int64_t r) {
       if (j >= 0) dst[j] = v;
     }
   };
-  if (p.q8) {
-    const float s8 =
-        cols <= 4096
-            ? quant_row_vec<8, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr)
-            : quant_row_vec<0, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r, nullptr);
-    to_rows(p.r8, s8);
-  }
-  if (p.q4) {
-    const float s4 =
-        cols <= 4096
-            ? quant_row_vec<8, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr)
-            : quant_row_vec<0, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r, nullptr);
-    to_rows(p.r4, s4);
+  if (cols <= 4096 && (p.q8 || p.q4 || p.qf8 || p.qf6)) {
+    // the per-token encodings share the row maximum: the row is loaded and
+    // reduced once, then each encoding is formed from the registers (the
+    // recipes of quant_row_vec, so the codes and scales are the same)
+    const int nch = cols >> 3;
+    const uint32_t nan_lo = p.act == MXMOE_BF16 ? 0x7f81u : 0x7c01u;
+    uint4 v[8];
+    uint32_t mb = 0u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int c = lane + 64 * i;
+      v[i] = c < nch ? row[c] : make_uint4(0u, 0u, 0u, 0u);
+      mb = max(mb, amax8_bits(v[i], nan_lo));
+    }
+    for (int d = 32; d > 0; d >>= 1) mb = max(mb, (uint32_t)__shfl_xor((int)mb, d, 64));
+    const float amax = bits_to_f32(mb, p.act);
+    auto enc = [&](uint8_t* codes, float* scale, int qmax, bool f6) {
+      const float q = (float)qmax;
+      float inv = 0.f, sc = 0.f;
+      if (amax > 0.f) {
+        inv = __fdiv_rn(q, amax);
+        sc = __fdiv_rn(amax, q);
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int c = lane + 64 * i;
+        if (c < nch) {
+          if (f6) store_f6_chunk(codes, c, codes8_f6(v[i], p.act, inv));
+          else reinterpret_cast<uint2*>(codes)[c] = codes8(v[i], p.act, inv, q);
+        }
+      }
+      if (lane == 0) *scale = sc;
+      return sc;
+    };
+    if (p.q8) to_rows(p.r8, enc(reinterpret_cast<uint8_t*>(p.q8 + r * cols), p.s8 + r, 127, false));
+    if (p.q4) to_rows(p.r4, enc(reinterpret_cast<uint8_t*>(p.q4 + r * cols), p.s4 + r, 7, false));
+    if (p.qf8) enc(p.qf8 + r * cols, p.sf8 + r, kQmaxF8, false);
+    if (p.qf6) enc(p.qf6 + r * cols, p.sf6 + r, 7, true);
+  } else {  // longer rows: each encoding streams the row
+    if (p.q8)
+      to_rows(p.r8, quant_row_vec<0, 1>(row, cols, p.act, 127, reinterpret_cast<uint2*>(p.q8 + r * cols), p.s8 + r,
+                                        nullptr));
+    if (p.q4)
+      to_rows(p.r4, quant_row_vec<0, 1>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4 + r * cols), p.s4 + r,
+                                        nullptr));
+    if (p.qf8)
+      quant_row_vec<0, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
+    if (p.qf6)
+      quant_row_vec<0, 1, true>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.qf6 + r * cols), p.sf6 + r, nullptr);
   }
   if (p.rs) rowsum_row(row, cols, p.rs + r * (cols >> 7));
   if (p.q4g)
     quant_row_groups(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.q4g + r * cols), p.s4g + r * (cols >> 7));
   if (p.qmx)
     quant_row_mx(row, cols, p.act, reinterpret_cast<uint4*>(p.qmx + r * (cols >> 1)), p.smx + r * (cols >> 5));
-  if (p.qf8) {
-    if (cols <= 4096) quant_row_vec<8, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
-    else quant_row_vec<0, 1>(row, cols, p.act, kQmaxF8, reinterpret_cast<uint2*>(p.qf8 + r * cols), p.sf8 + r, nullptr);
-  }
-  if (p.qf6) {
-    if (cols <= 4096) quant_row_vec<8, 1, true>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.qf6 + r * cols), p.sf6 + r, nullptr);
-    else quant_row_vec<0, 1, true>(row, cols, p.act, 7, reinterpret_cast<uint2*>(p.qf6 + r * cols), p.sf6 + r, nullptr);
-  }
 }
 
 }  // namespace
