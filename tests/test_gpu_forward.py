@@ -254,3 +254,21 @@ def test_fp32_slots_option(act):
     assert mb.slot_dtype() != torch.float32
     rep16 = check_forward(mb, blk, y16)
     say(f"fp32 slots {act}: {rep.line()}; 16-bit slots: {rep16.line()}")
+
+
+@pytest.mark.parametrize("fp32_slots", [False, True])
+def test_combine_of_more_than_ten_slots(fp32_slots):
+    """k + n_shared = 11 slots per token: the combine takes its generic path
+    (any slot count, one slot at a time) for 16-bit and fp32 slot rows; the
+    stage-wise check emulates it bit for bit."""
+    torch = torch_mod()
+    sch = [(W.W8A8,) * 3, (W.W4G128,) * 3, (W.W16,) * 3, (W.W4A4,) * 3] * 3 + [(W.W8A8,) * 3, (W.W16,) * 3,
+                                                                              (W.W4A4,) * 3]
+    blk = W.random_small_block(1234, T=50, H=256, F=256, E=12, k=8, n_shared=3, F_shared=256, act="bf16",
+                               schemes=sch, skew=0.5)
+    mb = M.MoEBlock(blk)
+    x, ids, w = upload_inputs(blk)
+    y = mb.forward(x, ids, w, fp32_slots=fp32_slots)
+    torch.cuda.synchronize()
+    rep = check_forward(mb, blk, y)
+    say(f"11 slots, fp32_slots={fp32_slots}: {rep.line()}")
