@@ -320,7 +320,8 @@ typedef struct {
   /* 1: keep the down projection's weighted rows (the slot rows the combine
    * sums) in fp32, for callers that difference them (the allocator's error
    * probe); 0 (default): each slot row element is rounded once to the
-   * activation dtype before the combine, which halves their traffic.        */
+   * activation dtype before the combine, which halves their traffic (with
+   * fp16 activations an element beyond the fp16 range then becomes inf).    */
   int32_t fp32_slots;
   int32_t reserved1;             /* must be 0 */
 } mxmoe_forward_opts;
